@@ -1,0 +1,684 @@
+/*
+ * hxo.c -- CPU oracle for batched placement scoring (HexGen-2, arXiv 2502.07903).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is the plain, slow, obviously-correct reference
+ * the HIP path is checked against.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg load it; the product path never does.  It shares
+ * no code, header, table or helper with the HIP path.
+ *
+ * Per candidate placement it computes, in the paper's order:
+ *   1. the Table 1 cost model of every admissible TP x PP strategy of every group
+ *      (computation, TP and PP communication, memory limit), and the node
+ *      capacity of Appendix A ("Node capacity estimation"): prefill T/latency at
+ *      batch 1, decode b_max*T/latency; prefill keeps its latency-optimal
+ *      strategy, decode its throughput-optimal one (Sec. 3.3, "Compute nodes");
+ *   2. the KV-cache edge capacities (Table 1 last row; Sec. 3.3 "Network
+ *      connections", connection type 3; Appendix A "Edge capacity estimation");
+ *   3. the directed flow network of Sec. 3.3 with split in/out compute nodes;
+ *   4. its maximum s-t flow.  The paper runs preflow-push; any exact algorithm
+ *      reaches the same value (max-flow = min-cut), and this oracle uses
+ *      Edmonds-Karp (shortest augmenting paths found by BFS);
+ *   5. the best candidate (highest flow, lowest index on ties; Sec. 3.1, 3.4).
+ *
+ * Readings where the paper is silent or ambiguous (all listed in the design notes):
+ *   - m_d is two inputs: memory bandwidth (decode weight scan) and memory limit.
+ *   - KV-cache terms use the KV hidden size H*n_kv_heads/n_heads (grouped-query
+ *     attention); every other term uses H.
+ *   - Stage j of a (tp, pp) strategy holds the group's members ranked j*tp ..
+ *     j*tp+tp-1 in ascending GPU id, and floor(L/pp) + [j < L mod pp] layers.
+ *   - Prefill is evaluated at batch 1, decode at b_max, the largest batch the
+ *     memory limit admits on every device: floor((M - A)/K) with A the weight term
+ *     and K the per-request term of the memory row, clamped to 2^30.
+ *   - Latency = sum over stages of (computation + TP) + sum of the PP terms.
+ *   - Capacities are int32 milli-requests per second: x = 1000*b/latency,
+ *     cap = min(2^24 - 1, floor(x)).
+ *   - KV edge: for every pair of (prefill stage, decode stage) sharing n layers and
+ *     every pair of ranks whose KV-head slices overlap by a fraction f, a link
+ *     carries 2*s_in*H_kv*B*n*f bytes in alpha + bytes/beta; links run in
+ *     parallel, so the KV time is the slowest link.  Per-GPU flow nodes use the
+ *     per-GPU rule of kv_gpu_time().
+ *   - Source and sink edges are unbounded (2^24 - 1) unless a coordinator
+ *     bandwidth and request size are given.
+ *
+ * Floating point: IEEE-754 binary64, round to nearest, no contraction into FMA
+ * (built with -ffp-contract=off, no fast-math), correctly rounded division, and
+ * every expression evaluated left to right as written here.
+ *
+ * Parity pins: the cost model against hand-derived worked values and closed
+ * forms, the memory limit against exact rational arithmetic, the max-flow against
+ * brute-force min-cut enumeration and library solvers, and flow validity
+ * (conservation, capacity, cut capacity) on every result.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define HXO_CAP_MAX 16777215          /* 2^24 - 1 milli-requests/s */
+#define HXO_BMAX_CLAMP 1073741824.0   /* 2^30 */
+#define HXO_UNUSED 0xFF
+#define HXO_PREFILL 0
+#define HXO_DECODE 1
+#define HXO_MAX_TP 8
+#define HXO_MAX_PP 32
+
+typedef struct {
+    int32_t n_gpus, n_types;
+    const int32_t *gpu_type;
+    const double *type_flops, *type_hbm_bw, *type_mem;
+    const double *beta, *alpha;
+    double coord_bw, req_bytes;
+} hxo_cluster;
+
+typedef struct { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hxo_model;
+typedef struct { double s_in, s_out; } hxo_workload;
+typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; } hxo_space;
+
+/* ------------------------------------------------------------------ helpers */
+
+static double flops_of(const hxo_cluster *c, int d) { return c->type_flops[c->gpu_type[d]]; }
+static double hbm_of(const hxo_cluster *c, int d) { return c->type_hbm_bw[c->gpu_type[d]]; }
+static double memlim_of(const hxo_cluster *c, int d) { return c->type_mem[c->gpu_type[d]]; }
+static double beta_of(const hxo_cluster *c, int d, int e) { return c->beta[(int64_t)d * c->n_gpus + e]; }
+static double alpha_of(const hxo_cluster *c, int d, int e) { return c->alpha[(int64_t)d * c->n_gpus + e]; }
+
+static double kv_hidden(const hxo_model *m)
+{
+    return (double)((int64_t)m->hidden * m->n_kv_heads / m->n_heads);
+}
+
+/* layers held by stage j of pp stages: uniform split, remainder to earlier stages */
+static int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
+static int stage_first_layer(int L, int pp, int j)
+{
+    int s = 0;
+    for (int i = 0; i < j; i++) s += stage_layers(L, pp, i);
+    return s;
+}
+
+int32_t hxo_quantize(double x)
+{
+    if (!(x >= 0.0)) return 0;
+    if (x >= (double)HXO_CAP_MAX) return HXO_CAP_MAX;
+    return (int32_t)floor(x);
+}
+
+int32_t hxo_coord_cap(const hxo_cluster *c)
+{
+    if (c->coord_bw > 0.0 && c->req_bytes > 0.0) return hxo_quantize((1000.0 * c->coord_bw) / c->req_bytes);
+    return HXO_CAP_MAX;
+}
+
+/* ------------------------------------------------------------------ Table 1 */
+
+/* Memory limit row of Table 1 for the stage devices S (tp of them, l layers):
+ * the largest batch b with (12H^2B/t + 2b(s_in+s_out)H_kv B/t) l + 4b(s_in+s_out)HB <= M_d
+ * on every device d of the stage, written as floor((M_d - A)/K). */
+static double stage_batch_limit(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                                const int32_t *S, int tp, int l)
+{
+    const double H = m->hidden, Hkv = kv_hidden(m), B = m->bytes_per_elem;
+    const double t = tp, ld = l;
+    const double A = ((12.0 * H * H * B) / t) * ld;
+    const double K = ((2.0 * (w->s_in + w->s_out) * Hkv * B) / t) * ld + 4.0 * (w->s_in + w->s_out) * H * B;
+    double best = HXO_BMAX_CLAMP;
+    for (int r = 0; r < tp; r++) {
+        double q = (memlim_of(c, S[r]) - A) / K;
+        double b = q >= HXO_BMAX_CLAMP ? HXO_BMAX_CLAMP : (q <= -HXO_BMAX_CLAMP ? -HXO_BMAX_CLAMP : floor(q));
+        if (b < best) best = b;
+    }
+    return best;
+}
+
+/* Computation cost of one stage (Table 1 row 1). */
+static double stage_compute(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                            const int32_t *S, int tp, int l, int role, double b)
+{
+    const double H = m->hidden, B = m->bytes_per_elem, t = tp, ld = l;
+    if (role == HXO_PREFILL) {
+        double mx = 0.0;
+        for (int r = 0; r < tp; r++) {
+            double v = (24.0 * b * w->s_in * H * H) / (t * flops_of(c, S[r]));
+            if (r == 0 || v > mx) mx = v;
+        }
+        return mx * ld;
+    }
+    double scan = 0.0, fl = 0.0;
+    for (int r = 0; r < tp; r++) {
+        double v = (12.0 * H * H * B * w->s_out) / (t * hbm_of(c, S[r]));
+        if (r == 0 || v > scan) scan = v;
+    }
+    for (int r = 0; r < tp; r++) {
+        double v = (24.0 * b * w->s_out * H * H) / (t * flops_of(c, S[r]));
+        if (r == 0 || v > fl) fl = v;
+    }
+    return scan * ld + fl * ld;
+}
+
+/* TP communication cost of one stage (Table 1 row 2): the slowest device's sum over its peers. */
+static double stage_tp_comm(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                            const int32_t *S, int tp, int l, int role, double b)
+{
+    const double H = m->hidden, B = m->bytes_per_elem, t = tp, ld = l;
+    const double X = role == HXO_PREFILL ? b * w->s_in * H * B : b * H * B;
+    double mx = 0.0;
+    for (int r = 0; r < tp; r++) {
+        double sum = 0.0;
+        for (int q = 0; q < tp; q++) {
+            if (q == r) continue;
+            sum = sum + (alpha_of(c, S[r], S[q]) + X / (t * beta_of(c, S[r], S[q])));
+        }
+        if (r == 0 || sum > mx) mx = sum;
+    }
+    if (role == HXO_PREFILL) return (mx * 4.0) * ld;
+    return ((mx * 4.0) * w->s_out) * ld;
+}
+
+/* PP communication cost between consecutive stages S -> S2 (Table 1 row 3): the fastest pair. */
+static double stage_pp_comm(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                            const int32_t *S, const int32_t *S2, int tp, int role, double b)
+{
+    const double H = m->hidden, B = m->bytes_per_elem;
+    const double X = role == HXO_PREFILL ? b * w->s_in * H * B : b * H * B;
+    double mn = 0.0;
+    int first = 1;
+    for (int r = 0; r < tp; r++)
+        for (int q = 0; q < tp; q++) {
+            double v = alpha_of(c, S[r], S2[q]) + X / beta_of(c, S[r], S2[q]);
+            if (first || v < mn) mn = v;
+            first = 0;
+        }
+    if (role == HXO_PREFILL) return mn;
+    return mn * w->s_out;
+}
+
+/* One strategy (tp, pp) of one group (members ascending, n = tp*pp of them).
+ * Returns 1 if the memory limit admits a batch of at least 1, else 0.
+ * Outputs b_max, the latency of one batch, and x = 1000*b/latency milli-requests/s. */
+int hxo_strategy_cost(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                      const int32_t *members, int32_t n, int32_t tp, int32_t pp, int32_t role,
+                      int32_t *bmax_out, double *lat_out, double *x_out)
+{
+    const int L = m->n_layers;
+    *bmax_out = 0; *lat_out = 0.0; *x_out = 0.0;
+    if (tp < 1 || pp < 1 || tp * pp != n || pp > L) return 0;
+    double bmax = HXO_BMAX_CLAMP;
+    for (int j = 0; j < pp; j++) {
+        double bj = stage_batch_limit(c, m, w, members + j * tp, tp, stage_layers(L, pp, j));
+        if (bj < bmax) bmax = bj;
+    }
+    *bmax_out = (int32_t)bmax;
+    if (bmax < 1.0) return 0;
+    const double b = role == HXO_PREFILL ? 1.0 : bmax;
+    double s1 = 0.0, s2 = 0.0;
+    for (int j = 0; j < pp; j++) {
+        const int32_t *S = members + j * tp;
+        const int l = stage_layers(L, pp, j);
+        s1 = s1 + (stage_compute(c, m, w, S, tp, l, role, b) + stage_tp_comm(c, m, w, S, tp, l, role, b));
+    }
+    for (int j = 0; j + 1 < pp; j++)
+        s2 = s2 + stage_pp_comm(c, m, w, members + j * tp, members + (j + 1) * tp, tp, role, b);
+    const double lat = s1 + s2;
+    *lat_out = lat;
+    *x_out = (1000.0 * b) / lat;
+    return 1;
+}
+
+/* Try every admissible TP x PP of a group and keep prefill's latency-optimal and decode's
+ * throughput-optimal strategy (ties keep the smaller tp).  No feasible strategy: all zero. */
+int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, const hxo_space *sp,
+                     const int32_t *members, int32_t n, int32_t role,
+                     int32_t *tp_out, int32_t *pp_out, int32_t *bmax_out, int32_t *cap_out, double *lat_out)
+{
+    int have = 0;
+    double best_lat = 0.0, best_x = 0.0;
+    *tp_out = 0; *pp_out = 0; *bmax_out = 0; *cap_out = 0; *lat_out = 0.0;
+    for (int tp = 1; tp <= HXO_MAX_TP; tp++) {
+        if (!((sp->tp_mask >> (tp - 1)) & 1u)) continue;
+        if (n % tp != 0) continue;
+        int pp = n / tp;
+        if (pp > HXO_MAX_PP || !((sp->pp_mask >> (pp - 1)) & 1u) || pp > m->n_layers) continue;
+        int32_t bmax;
+        double lat, x;
+        if (!hxo_strategy_cost(c, m, w, members, n, tp, pp, role, &bmax, &lat, &x)) continue;
+        int better = !have || (role == HXO_PREFILL ? lat < best_lat : x > best_x);
+        if (better) {
+            have = 1; best_lat = lat; best_x = x;
+            *tp_out = tp; *pp_out = pp; *bmax_out = bmax; *cap_out = hxo_quantize(x); *lat_out = lat;
+        }
+    }
+    return have;
+}
+
+/* KV-cache transfer time of one request from a prefill replica (members pm, ptp x ppp) to a
+ * decode replica (dm, dtp x dpp): every GPU holding layer j's KV heads sends them to the
+ * GPUs holding the same layer and heads on the decode side; the slowest link decides. */
+double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                   const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *dm, int32_t dtp, int32_t dpp)
+{
+    const int L = m->n_layers;
+    const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
+    double worst = 0.0;
+    for (int a = 0; a < ppp; a++) {
+        int a0 = stage_first_layer(L, ppp, a), a1 = a0 + stage_layers(L, ppp, a);
+        for (int bb = 0; bb < dpp; bb++) {
+            int b0 = stage_first_layer(L, dpp, bb), b1 = b0 + stage_layers(L, dpp, bb);
+            int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+            if (nab <= 0) continue;
+            for (int r = 0; r < ptp; r++)
+                for (int q = 0; q < dtp; q++) {
+                    int hi = (r + 1) * dtp < (q + 1) * ptp ? (r + 1) * dtp : (q + 1) * ptp;
+                    int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
+                    int ov = hi - lo;
+                    if (ov <= 0) continue;
+                    int g = pm[a * ptp + r], h = dm[bb * dtp + q];
+                    double bytes = ((V1 * (double)nab) * (double)ov) / (double)(ptp * dtp);
+                    double time = alpha_of(c, g, h) + bytes / beta_of(c, g, h);
+                    if (time > worst) worst = time;
+                }
+        }
+    }
+    return worst;
+}
+
+/* Per-GPU flow nodes: the link from prefill GPU g (one of n_p GPUs of its replica) to decode
+ * GPU h carries g's 1/n_p share of a request's KV cache for all L layers. */
+double hxo_kv_gpu_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                       int32_t g, int32_t h, int32_t n_p)
+{
+    const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
+    const double share = (V1 * (double)m->n_layers) / (double)n_p;
+    return alpha_of(c, g, h) + share / beta_of(c, g, h);
+}
+
+/* ------------------------------------------------------------------ batch cost model */
+
+typedef struct {
+    const hxo_cluster *c; const hxo_model *m; const hxo_workload *w; const hxo_space *sp;
+    int32_t n_cand, max_groups;
+    const uint8_t *assign, *role;
+} hxo_batch;
+
+/* members of group k of candidate n, ascending GPU id; returns the count */
+static int group_members(const hxo_batch *bt, int n, int k, int32_t *out)
+{
+    int cnt = 0;
+    for (int g = 0; g < bt->c->n_gpus; g++)
+        if (bt->assign[(int64_t)g * bt->n_cand + n] == k) out[cnt++] = g;
+    return cnt;
+}
+
+static int group_role(const hxo_batch *bt, int n, int k)
+{
+    return bt->role[(int64_t)k * bt->n_cand + n];
+}
+
+static void cost_range(const hxo_batch *bt, int n0, int n1, uint8_t *tp, uint8_t *pp, int32_t *bmax,
+                       int32_t *cap, double *lat)
+{
+    int32_t *mem = (int32_t *)malloc(sizeof(int32_t) * (bt->c->n_gpus + 1));
+    for (int n = n0; n < n1; n++)
+        for (int k = 0; k < bt->max_groups; k++) {
+            int64_t o = (int64_t)k * bt->n_cand + n;
+            int r = group_role(bt, n, k);
+            int cnt = group_members(bt, n, k, mem);
+            int32_t t = 0, p = 0, b = 0, cp = 0;
+            double l = 0.0;
+            if (cnt > 0 && (r == HXO_PREFILL || r == HXO_DECODE))
+                hxo_group_select(bt->c, bt->m, bt->w, bt->sp, mem, cnt, r, &t, &p, &b, &cp, &l);
+            tp[o] = (uint8_t)t; pp[o] = (uint8_t)p; bmax[o] = b; cap[o] = cp; lat[o] = l;
+        }
+    free(mem);
+}
+
+int hxo_cost_eval(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, const hxo_space *sp,
+                  int32_t n_cand, int32_t max_groups, const uint8_t *assign, const uint8_t *role,
+                  uint8_t *tp, uint8_t *pp, int32_t *bmax, int32_t *cap, double *lat)
+{
+    hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
+    cost_range(&bt, 0, n_cand, tp, pp, bmax, cap, lat);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ flow network */
+
+typedef struct {
+    int32_t max_p, max_d, max_pd;
+    int32_t *n_p, *n_d, *p_slot, *d_slot, *src_cap, *p_cap, *kv_cap, *d_cap, *sink_cap;
+} hxo_flownet;
+
+static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp, const uint8_t *pp,
+                          const int32_t *cap, const hxo_flownet *f)
+{
+    const hxo_cluster *c = bt->c;
+    const int N = bt->n_cand, G = c->n_gpus, Kmax = bt->max_groups;
+    int32_t *pm = (int32_t *)malloc(sizeof(int32_t) * (G + 1));
+    int32_t *dm = (int32_t *)malloc(sizeof(int32_t) * (G + 1));
+    int32_t *pnode = (int32_t *)malloc(sizeof(int32_t) * (G + Kmax + 1));
+    int32_t *dnode = (int32_t *)malloc(sizeof(int32_t) * (G + Kmax + 1));
+    const int32_t cc = hxo_coord_cap(c);
+    for (int n = n0; n < n1; n++) {
+        int np = 0, nd = 0;
+        if (bt->sp->granularity == 0) {
+            for (int k = 0; k < Kmax; k++) {
+                int r = group_role(bt, n, k);
+                if (group_members(bt, n, k, pm) == 0) continue;
+                if (r == HXO_PREFILL) pnode[np++] = k;
+                else if (r == HXO_DECODE) dnode[nd++] = k;
+            }
+        } else {
+            for (int g = 0; g < G; g++) {
+                int k = bt->assign[(int64_t)g * N + n];
+                if (k >= Kmax) continue;
+                int r = group_role(bt, n, k);
+                if (r == HXO_PREFILL) pnode[np++] = g;
+                else if (r == HXO_DECODE) dnode[nd++] = g;
+            }
+        }
+        f->n_p[n] = np; f->n_d[n] = nd;
+        for (int i = 0; i < f->max_p; i++) {
+            int64_t o = (int64_t)i * N + n;
+            f->p_slot[o] = -1; f->src_cap[o] = 0; f->p_cap[o] = 0;
+        }
+        for (int j = 0; j < f->max_d; j++) {
+            int64_t o = (int64_t)j * N + n;
+            f->d_slot[o] = -1; f->d_cap[o] = 0; f->sink_cap[o] = 0;
+        }
+        for (int e = 0; e < f->max_pd; e++) f->kv_cap[(int64_t)e * N + n] = 0;
+
+        if (bt->sp->granularity == 0) {
+            for (int i = 0; i < np; i++) {
+                int64_t o = (int64_t)i * N + n, go = (int64_t)pnode[i] * N + n;
+                f->p_slot[o] = pnode[i]; f->src_cap[o] = cc; f->p_cap[o] = cap[go];
+            }
+            for (int j = 0; j < nd; j++) {
+                int64_t o = (int64_t)j * N + n, go = (int64_t)dnode[j] * N + n;
+                f->d_slot[o] = dnode[j]; f->d_cap[o] = cap[go]; f->sink_cap[o] = cc;
+            }
+            for (int i = 0; i < np; i++) {
+                int64_t gp = (int64_t)pnode[i] * N + n;
+                int pn = group_members(bt, n, pnode[i], pm);
+                for (int j = 0; j < nd; j++) {
+                    int64_t gd = (int64_t)dnode[j] * N + n;
+                    int dn = group_members(bt, n, dnode[j], dm);
+                    int32_t kv = 0;
+                    (void)pn; (void)dn;
+                    if (tp[gp] > 0 && tp[gd] > 0) {
+                        double t = hxo_kv_time(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                        kv = hxo_quantize(1000.0 / t);
+                    }
+                    f->kv_cap[(int64_t)(i * nd + j) * N + n] = kv;
+                }
+            }
+        } else {
+            /* per-GPU nodes: a GPU's node capacity is its equal share of its replica's capacity */
+            for (int side = 0; side < 2; side++) {
+                int cnt = side == 0 ? np : nd;
+                int32_t *node = side == 0 ? pnode : dnode;
+                for (int i = 0; i < cnt; i++) {
+                    int g = node[i];
+                    int k = bt->assign[(int64_t)g * N + n];
+                    int64_t go = (int64_t)k * N + n;
+                    int sz = group_members(bt, n, k, pm);
+                    int rank = 0;
+                    while (pm[rank] != g) rank++;
+                    int32_t C = cap[go];
+                    int32_t share = C / sz + (rank < C % sz ? 1 : 0);
+                    int64_t o = (int64_t)i * N + n;
+                    if (side == 0) { f->p_slot[o] = g; f->src_cap[o] = cc; f->p_cap[o] = share; }
+                    else { f->d_slot[o] = g; f->d_cap[o] = share; f->sink_cap[o] = cc; }
+                }
+            }
+            for (int i = 0; i < np; i++) {
+                int g = pnode[i];
+                int kp = bt->assign[(int64_t)g * N + n];
+                int szp = group_members(bt, n, kp, pm);
+                for (int j = 0; j < nd; j++) {
+                    int h = dnode[j];
+                    int kd = bt->assign[(int64_t)h * N + n];
+                    int32_t kv = 0;
+                    if (tp[(int64_t)kp * N + n] > 0 && tp[(int64_t)kd * N + n] > 0)
+                        kv = hxo_quantize(1000.0 / hxo_kv_gpu_time(c, bt->m, bt->w, g, h, szp));
+                    f->kv_cap[(int64_t)(i * nd + j) * N + n] = kv;
+                }
+            }
+        }
+    }
+    free(pm); free(dm); free(pnode); free(dnode);
+}
+
+int hxo_build_flownet(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, const hxo_space *sp,
+                      int32_t n_cand, int32_t max_groups, const uint8_t *assign, const uint8_t *role,
+                      const uint8_t *tp, const uint8_t *pp, const int32_t *cap,
+                      int32_t max_p, int32_t max_d, int32_t max_pd,
+                      int32_t *n_p, int32_t *n_d, int32_t *p_slot, int32_t *d_slot,
+                      int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap)
+{
+    hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
+    hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
+    flownet_range(&bt, 0, n_cand, tp, pp, cap, &f);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ max-flow (Edmonds-Karp) */
+
+typedef struct {
+    int nv, na;
+    int *head, *next, *to;
+    int64_t *res;
+    int *parent_arc, *queue;
+} ek_graph;
+
+static void ek_init(ek_graph *g, int nv, int max_edges)
+{
+    g->nv = nv; g->na = 0;
+    g->head = (int *)malloc(sizeof(int) * nv);
+    g->next = (int *)malloc(sizeof(int) * 2 * max_edges);
+    g->to = (int *)malloc(sizeof(int) * 2 * max_edges);
+    g->res = (int64_t *)malloc(sizeof(int64_t) * 2 * max_edges);
+    g->parent_arc = (int *)malloc(sizeof(int) * nv);
+    g->queue = (int *)malloc(sizeof(int) * nv);
+    for (int v = 0; v < nv; v++) g->head[v] = -1;
+}
+
+static void ek_free(ek_graph *g)
+{
+    free(g->head); free(g->next); free(g->to); free(g->res); free(g->parent_arc); free(g->queue);
+}
+
+/* adds edge u->v with capacity cap as arc pair (2e forward, 2e+1 reverse); returns e */
+static int ek_add(ek_graph *g, int u, int v, int64_t cap)
+{
+    int a = g->na;
+    g->to[a] = v; g->res[a] = cap; g->next[a] = g->head[u]; g->head[u] = a;
+    g->to[a + 1] = u; g->res[a + 1] = 0; g->next[a + 1] = g->head[v]; g->head[v] = a + 1;
+    g->na += 2;
+    return a / 2;
+}
+
+/* BFS over arcs with residual > 0 from s; fills parent_arc (-1 unreached, -2 for s) */
+static void ek_bfs(ek_graph *g, int s)
+{
+    for (int v = 0; v < g->nv; v++) g->parent_arc[v] = -1;
+    g->parent_arc[s] = -2;
+    int qh = 0, qt = 0;
+    g->queue[qt++] = s;
+    while (qh < qt) {
+        int u = g->queue[qh++];
+        for (int a = g->head[u]; a >= 0; a = g->next[a])
+            if (g->res[a] > 0 && g->parent_arc[g->to[a]] == -1) {
+                g->parent_arc[g->to[a]] = a;
+                g->queue[qt++] = g->to[a];
+            }
+    }
+}
+
+static int64_t ek_run(ek_graph *g, int s, int t)
+{
+    int64_t total = 0;
+    for (;;) {
+        ek_bfs(g, s);
+        if (g->parent_arc[t] == -1) break;
+        int64_t aug = INT64_MAX;
+        for (int v = t; v != s; v = g->to[g->parent_arc[v] ^ 1])
+            if (g->res[g->parent_arc[v]] < aug) aug = g->res[g->parent_arc[v]];
+        for (int v = t; v != s; v = g->to[g->parent_arc[v] ^ 1]) {
+            g->res[g->parent_arc[v]] -= aug;
+            g->res[g->parent_arc[v] ^ 1] += aug;
+        }
+        total += aug;
+    }
+    return total;
+}
+
+/* Max s-t flow of an explicit edge list; flow[e] receives edge e's flow, reach[v] (nullable)
+ * is 1 for the vertices reachable from s in the final residual graph. */
+int64_t hxo_maxflow_edges(int32_t nv, int32_t ne, const int32_t *from, const int32_t *to, const int64_t *cap,
+                          int32_t s, int32_t t, int64_t *flow, uint8_t *reach)
+{
+    ek_graph g;
+    ek_init(&g, nv, ne > 0 ? ne : 1);
+    for (int e = 0; e < ne; e++) ek_add(&g, from[e], to[e], cap[e]);
+    int64_t v = ek_run(&g, s, t);
+    for (int e = 0; e < ne; e++) flow[e] = g.res[2 * e + 1];
+    if (reach) {
+        ek_bfs(&g, s);
+        for (int u = 0; u < nv; u++) reach[u] = g.parent_arc[u] != -1;
+    }
+    ek_free(&g);
+    return v;
+}
+
+typedef struct {
+    int32_t n_cand, max_p, max_d, max_pd;
+    const int32_t *n_p, *n_d, *src_cap, *p_cap, *kv_cap, *d_cap, *sink_cap;
+    int32_t *flow_value, *kv_flow;
+    uint8_t *cut;
+} hxo_mf;
+
+/* The Sec. 3.3 network of candidate n: s=0, t=1, prefill replica i as in 2+2i -> out 3+2i,
+ * decode replica j as in 2+2P+2j -> out 3+2P+2j; edges s->phi_in, phi_in->phi_out,
+ * phi_out->delta_in (every pair), delta_in->delta_out, delta_out->t. */
+static void maxflow_range(const hxo_mf *q, int n0, int n1)
+{
+    const int N = q->n_cand;
+    const int maxv = 2 + 2 * (q->max_p + q->max_d);
+    const int maxe = q->max_p * 2 + q->max_d * 2 + q->max_pd;
+    int32_t *from = (int32_t *)malloc(sizeof(int32_t) * (maxe + 1));
+    int32_t *to = (int32_t *)malloc(sizeof(int32_t) * (maxe + 1));
+    int64_t *cp = (int64_t *)malloc(sizeof(int64_t) * (maxe + 1));
+    int64_t *fl = (int64_t *)malloc(sizeof(int64_t) * (maxe + 1));
+    uint8_t *reach = (uint8_t *)malloc(maxv);
+    for (int n = n0; n < n1; n++) {
+        const int P = q->n_p[n], D = q->n_d[n];
+        int ne = 0;
+        for (int i = 0; i < P; i++) {
+            int64_t o = (int64_t)i * N + n;
+            from[ne] = 0; to[ne] = 2 + 2 * i; cp[ne++] = q->src_cap[o];
+            from[ne] = 2 + 2 * i; to[ne] = 3 + 2 * i; cp[ne++] = q->p_cap[o];
+        }
+        const int kv0 = ne;
+        for (int i = 0; i < P; i++)
+            for (int j = 0; j < D; j++) {
+                from[ne] = 3 + 2 * i; to[ne] = 2 + 2 * P + 2 * j;
+                cp[ne++] = q->kv_cap[(int64_t)(i * D + j) * N + n];
+            }
+        for (int j = 0; j < D; j++) {
+            int64_t o = (int64_t)j * N + n;
+            from[ne] = 2 + 2 * P + 2 * j; to[ne] = 3 + 2 * P + 2 * j; cp[ne++] = q->d_cap[o];
+            from[ne] = 3 + 2 * P + 2 * j; to[ne] = 1; cp[ne++] = q->sink_cap[o];
+        }
+        int64_t v = hxo_maxflow_edges(2 + 2 * (P + D), ne, from, to, cp, 0, 1, fl, reach);
+        q->flow_value[n] = (int32_t)v;
+        if (q->kv_flow) {
+            for (int e = 0; e < q->max_pd; e++) q->kv_flow[(int64_t)e * N + n] = 0;
+            for (int e = 0; e < P * D; e++) q->kv_flow[(int64_t)e * N + n] = (int32_t)fl[kv0 + e];
+        }
+        if (q->cut) {
+            for (int i = 0; i < q->max_p + q->max_d; i++) q->cut[(int64_t)i * N + n] = 0;
+            for (int i = 0; i < P; i++)
+                q->cut[(int64_t)i * N + n] = (uint8_t)(reach[2 + 2 * i] | (reach[3 + 2 * i] << 1));
+            for (int j = 0; j < D; j++)
+                q->cut[(int64_t)(q->max_p + j) * N + n] =
+                    (uint8_t)(reach[2 + 2 * P + 2 * j] | (reach[3 + 2 * P + 2 * j] << 1));
+        }
+    }
+    free(from); free(to); free(cp); free(fl); free(reach);
+}
+
+int hxo_maxflow_batch(int32_t n_cand, int32_t max_p, int32_t max_d, int32_t max_pd,
+                      const int32_t *n_p, const int32_t *n_d, const int32_t *src_cap, const int32_t *p_cap,
+                      const int32_t *kv_cap, const int32_t *d_cap, const int32_t *sink_cap,
+                      int32_t *flow_value, int32_t *kv_flow, uint8_t *cut)
+{
+    hxo_mf q = {n_cand, max_p, max_d, max_pd, n_p, n_d, src_cap, p_cap, kv_cap, d_cap, sink_cap,
+                flow_value, kv_flow, cut};
+    maxflow_range(&q, 0, n_cand);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ argmax */
+
+int hxo_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best)
+{
+    if (n_cand <= 0) return -1;
+    int32_t bi = 0, bv = flow_value[0];
+    for (int32_t n = 1; n < n_cand; n++)
+        if (flow_value[n] > bv) { bv = flow_value[n]; bi = n; }
+    best[0] = bi; best[1] = bv;
+    return 0;
+}
+
+/* ------------------------------------------------------------------ whole batch, threaded */
+
+typedef struct {
+    const hxo_batch *bt;
+    hxo_flownet f;
+    uint8_t *tp, *pp;
+    int32_t *bmax, *cap;
+    double *lat;
+    int32_t *flow_value;
+    int n0, n1;
+} hxo_job;
+
+static void *score_worker(void *arg)
+{
+    hxo_job *j = (hxo_job *)arg;
+    cost_range(j->bt, j->n0, j->n1, j->tp, j->pp, j->bmax, j->cap, j->lat);
+    flownet_range(j->bt, j->n0, j->n1, j->tp, j->pp, j->cap, &j->f);
+    hxo_mf q = {j->bt->n_cand, j->f.max_p, j->f.max_d, j->f.max_pd, j->f.n_p, j->f.n_d, j->f.src_cap,
+                j->f.p_cap, j->f.kv_cap, j->f.d_cap, j->f.sink_cap, j->flow_value, NULL, NULL};
+    maxflow_range(&q, j->n0, j->n1);
+    return NULL;
+}
+
+/* Scores candidates [0, n_cand) end to end on n_threads host threads (all buffers caller
+ * owned, same layouts as the individual calls) and writes the best (index, value). */
+int hxo_score_batch(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, const hxo_space *sp,
+                    int32_t n_cand, int32_t max_groups, const uint8_t *assign, const uint8_t *role,
+                    uint8_t *tp, uint8_t *pp, int32_t *bmax, int32_t *cap, double *lat,
+                    int32_t max_p, int32_t max_d, int32_t max_pd,
+                    int32_t *n_p, int32_t *n_d, int32_t *p_slot, int32_t *d_slot,
+                    int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap,
+                    int32_t *flow_value, int32_t *best, int32_t n_threads)
+{
+    hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
+    hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > n_cand) n_threads = n_cand > 0 ? n_cand : 1;
+    hxo_job *jobs = (hxo_job *)calloc(n_threads, sizeof(hxo_job));
+    pthread_t *th = (pthread_t *)calloc(n_threads, sizeof(pthread_t));
+    for (int i = 0; i < n_threads; i++) {
+        jobs[i].bt = &bt; jobs[i].f = f;
+        jobs[i].tp = tp; jobs[i].pp = pp; jobs[i].bmax = bmax; jobs[i].cap = cap; jobs[i].lat = lat;
+        jobs[i].flow_value = flow_value;
+        jobs[i].n0 = (int)((int64_t)n_cand * i / n_threads);
+        jobs[i].n1 = (int)((int64_t)n_cand * (i + 1) / n_threads);
+    }
+    for (int i = 1; i < n_threads; i++) pthread_create(&th[i], NULL, score_worker, &jobs[i]);
+    score_worker(&jobs[0]);
+    for (int i = 1; i < n_threads; i++) pthread_join(th[i], NULL);
+    free(jobs); free(th);
+    return hxo_best_candidate(flow_value, n_cand, best);
+}

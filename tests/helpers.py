@@ -1,0 +1,197 @@
+"""Shared test helpers: golden-file parsing, small clusters, and checkers that certify a
+max-flow independently of both the oracle and the HIP path."""
+from __future__ import annotations
+
+import dataclasses
+import itertools
+import os
+from typing import Dict, List, Optional
+
+import numpy as np
+
+from paper_2502_07903_amd import inputs as I
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+CAP_MAX = 16777215
+ROLE = {"prefill": 0, "decode": 1}
+
+
+def parse_golden(name: str) -> List[Dict[str, str]]:
+    cases, cur = [], None
+    with open(os.path.join(GOLDEN, name)) as f:
+        for raw in f:
+            line = raw.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("["):
+                cur = {"name": line.strip("[]")}
+                cases.append(cur)
+            else:
+                k, v = (s.strip() for s in line.split("=", 1))
+                cur[k] = v
+    return cases
+
+
+def ints(s: str) -> List[int]:
+    return [int(x) for x in s.split(",")]
+
+
+# ------------------------------------------------------------------ small clusters
+
+TYPE_AB = np.array([I.GPU_TYPES["A"], I.GPU_TYPES["B"]], np.float64)
+
+
+def cluster_c1() -> I.Cluster:
+    return I.cluster_from_nodes(np.array([0] * 4 + [1] * 4, np.int32), TYPE_AB,
+                                np.array([[0.0, 12.5e9], [12.5e9, 0.0]]))
+
+
+def cluster_asym() -> I.Cluster:
+    cl = cluster_c1()
+    beta = cl.beta.reshape(8, 8).copy()
+    alpha = cl.alpha.reshape(8, 8).copy()
+    beta[4:, :4] = 6.25e9
+    alpha[4:, :4] = 8e-5
+    return dataclasses.replace(cl, beta=np.ascontiguousarray(beta.reshape(-1)),
+                               alpha=np.ascontiguousarray(alpha.reshape(-1)))
+
+
+CLUSTERS = {"c1": cluster_c1, "asym": cluster_asym}
+MODELS = {"opt30b": dict(I.OPT_30B), "opt30b_l3": dict(I.OPT_30B, n_layers=3)}
+
+
+def problem(cluster: I.Cluster, model: Dict[str, int], assign: np.ndarray, role: np.ndarray,
+            s_in: float = 512.0, s_out: float = 128.0, tp=(1, 2, 4), pp=(1, 2), granularity: int = 0,
+            max_groups: Optional[int] = None) -> I.Problem:
+    mg = role.shape[0] if max_groups is None else max_groups
+    tpm = sum(1 << (t - 1) for t in tp)
+    ppm = sum(1 << (p - 1) for p in pp)
+    return I.Problem(cluster, dict(model), float(s_in), float(s_out), tpm, ppm, granularity, mg,
+                     np.ascontiguousarray(assign, np.uint8), np.ascontiguousarray(role, np.uint8))
+
+
+def single_group_problem(cluster_name: str, model_name: str, members: List[int]) -> I.Problem:
+    cl = CLUSTERS[cluster_name]()
+    a, r = I.placement_from_groups([members], [0], cl.n_gpus, 1)
+    return problem(cl, MODELS[model_name], a, r)
+
+
+# ------------------------------------------------------------------ flow networks
+
+def network_edges(fn: Dict[str, np.ndarray], n: int):
+    """Explicit Sec. 3.3 network of candidate n of a flownet (candidate-fastest arrays):
+    s=0, t=1, prefill i: in 2+2i, out 3+2i; decode j: in 2+2P+2j, out 3+2P+2j."""
+    P, D = int(fn["n_p"][n]), int(fn["n_d"][n])
+    E = []
+    for i in range(P):
+        E.append((0, 2 + 2 * i, int(fn["src_cap"][i, n])))
+        E.append((2 + 2 * i, 3 + 2 * i, int(fn["p_cap"][i, n])))
+    for i in range(P):
+        for j in range(D):
+            E.append((3 + 2 * i, 2 + 2 * P + 2 * j, int(fn["kv_cap"][i * D + j, n])))
+    for j in range(D):
+        E.append((2 + 2 * P + 2 * j, 3 + 2 * P + 2 * j, int(fn["d_cap"][j, n])))
+        E.append((3 + 2 * P + 2 * j, 1, int(fn["sink_cap"][j, n])))
+    return 2 + 2 * (P + D), E
+
+
+def brute_force_min_cut(nv: int, edges, s: int = 0, t: int = 1) -> int:
+    """Minimum s-t cut capacity by enumerating every vertex subset containing s but not t."""
+    others = [v for v in range(nv) if v not in (s, t)]
+    k = len(others)
+    assert k <= 20
+    fr = np.array([e[0] for e in edges], np.int64)
+    to = np.array([e[1] for e in edges], np.int64)
+    cap = np.array([e[2] for e in edges], np.int64)
+    masks = np.arange(1 << k, dtype=np.int64)
+    side = np.zeros((1 << k, nv), bool)             # True = on the source side
+    side[:, s] = True
+    for b, v in enumerate(others):
+        side[:, v] = (masks >> b) & 1 == 1
+    crossing = side[:, fr] & ~side[:, to]
+    return int((crossing * cap[None, :]).sum(axis=1).min())
+
+
+def check_flow(fn: Dict[str, np.ndarray], flow_value: np.ndarray, kv_flow: Optional[np.ndarray],
+               cut: Optional[np.ndarray], idx=None) -> None:
+    """Certify max-flow results on the Sec. 3.3 network without any max-flow solver.
+
+    kv_flow (the flow on every prefill->decode edge) fixes the whole flow: a replica's in->out
+    and source/sink edges carry the sum over its KV edges.  Checks 0 <= f <= cap on every edge
+    and conservation, that the value equals the total, and -- with the cut -- that the cut is
+    exactly the set reachable from s in the residual graph and that its capacity equals the
+    value, which proves the flow maximum."""
+    N = flow_value.shape[0]
+    idx = range(N) if idx is None else idx
+    for n in idx:
+        P, D = int(fn["n_p"][n]), int(fn["n_d"][n])
+        v = int(flow_value[n])
+        if kv_flow is None:
+            assert v >= 0
+            continue
+        f = kv_flow[:P * D, n].astype(np.int64).reshape(P, D)
+        c = fn["kv_cap"][:P * D, n].astype(np.int64).reshape(P, D)
+        assert (f >= 0).all() and (f <= c).all(), f"candidate {n}: KV flow outside [0, cap]"
+        out_p = f.sum(axis=1)
+        in_d = f.sum(axis=0)
+        a = np.minimum(fn["src_cap"][:P, n], fn["p_cap"][:P, n]).astype(np.int64)
+        b = np.minimum(fn["d_cap"][:D, n], fn["sink_cap"][:D, n]).astype(np.int64)
+        assert (out_p <= a).all(), f"candidate {n}: prefill replica over capacity"
+        assert (in_d <= b).all(), f"candidate {n}: decode replica over capacity"
+        assert int(f.sum()) == v, f"candidate {n}: value {v} != total flow {int(f.sum())}"
+        if cut is None:
+            continue
+        nv, E = network_edges(fn, n)
+        flows = []
+        for i in range(P):
+            flows += [out_p[i], out_p[i]]
+        flows += list(f.reshape(-1))
+        for j in range(D):
+            flows += [in_d[j], in_d[j]]
+        reach = residual_reach(nv, E, flows)
+        assert not reach[1], f"candidate {n}: sink reachable, flow not maximum"
+        want = np.zeros(P + D, np.uint8)
+        for i in range(P):
+            want[i] = reach[2 + 2 * i] | (reach[3 + 2 * i] << 1)
+        for j in range(D):
+            want[P + j] = reach[2 + 2 * P + 2 * j] | (reach[3 + 2 * P + 2 * j] << 1)
+        mp = fn["dims"][0] if "dims" in fn else fn["p_slot"].shape[0]
+        got = np.concatenate([cut[:P, n], cut[mp:mp + D, n]])
+        assert np.array_equal(got, want), f"candidate {n}: cut {got} != residual-reachable set {want}"
+        cap_cut = sum(cp for (u, w, cp) in E if reach[u] and not reach[w])
+        assert cap_cut == v, f"candidate {n}: cut capacity {cap_cut} != value {v}"
+
+
+def residual_reach(nv: int, edges, flows) -> np.ndarray:
+    """Vertices reachable from s = 0 along forward arcs with f < cap or reverse arcs with f > 0."""
+    adj = [[] for _ in range(nv)]
+    for (u, w, cp), fl in zip(edges, flows):
+        if fl < cp:
+            adj[u].append(w)
+        if fl > 0:
+            adj[w].append(u)
+    seen = np.zeros(nv, bool)
+    seen[0] = True
+    stack = [0]
+    while stack:
+        u = stack.pop()
+        for w in adj[u]:
+            if not seen[w]:
+                seen[w] = True
+                stack.append(w)
+    return seen
+
+
+def bipartite_closed_form(a: np.ndarray, b: np.ndarray, c: np.ndarray) -> int:
+    """Max-flow of s -> p (a_p) -> d (c_pd) -> t (b_d) as its minimum cut: over every set X of
+    prefill nodes kept on the source side, sum_{p not in X} a_p + sum_d min(b_d, sum_{p in X} c_pd)
+    (each decode node is cut on whichever side is cheaper)."""
+    P = len(a)
+    best = None
+    for bits in range(1 << P):
+        X = [p for p in range(P) if (bits >> p) & 1]
+        v = sum(int(a[p]) for p in range(P) if p not in X)
+        for d in range(len(b)):
+            v += min(int(b[d]), sum(int(c[p, d]) for p in X))
+        best = v if best is None else min(best, v)
+    return best
