@@ -1,0 +1,185 @@
+/*
+ * hx.h -- C-ABI of libhx: batched scoring of HexGen-2 model placements on one MI355X.
+ *
+ * HexGen-2 (arXiv 2502.07903) schedules LLM serving on a heterogeneous GPU cluster by
+ * searching over "model placement strategies" (Sec. 3.1): a partition of the GPUs into
+ * groups, a role per group (prefill or decode replica), a TP x PP strategy per group and
+ * a KV-cache routing between replicas.  The inner loop of that search (Sec. 3.3, run again
+ * after every refinement step of Sec. 3.4) scores a placement: the Table 1 cost model gives
+ * each replica's capacity, the placement becomes a flow network, and its maximum flow is
+ * the placement's serving throughput.  libhx runs that loop for many thousands of candidate
+ * placements at once:
+ *
+ *   hx_cost_eval       Table 1 + Appendix A node capacities     (one lane per candidate group)
+ *   hx_build_flownet   the Sec. 3.3 network and its KV edges     (one lane per candidate / node)
+ *   hx_maxflow_batch   maximum flow, flow assignment, min cut    (one workgroup per candidate)
+ *   hx_best_candidate  the best candidate                        (one workgroup)
+ *
+ * Conventions
+ *   - Every array pointer is a DEVICE pointer unless marked [host].  The caller owns every
+ *     buffer; libhx allocates no device memory and keeps no state between calls.
+ *   - Per-candidate arrays are candidate-fastest ("structure of arrays"): element (row, n)
+ *     of an array with R rows lives at [row * n_cand + n].
+ *   - Every call validates its arguments on the host (no device access, no sync), enqueues
+ *     its kernels on `stream` and returns.  The return code reports validation and launch
+ *     errors; results are ready when the stream reaches the enqueued work.
+ *   - Capacities and flows are int32 milli-requests per second (1000 x requests/s),
+ *     clamped to HX_CAP_MAX so that any cut of <= 128 edges fits in int32.
+ *   - Floating point is IEEE binary64 with no contraction into fused multiply-add and
+ *     correctly rounded division, each expression evaluated in the order documented at
+ *     the function, so results do not depend on the launch shape.
+ */
+#ifndef HX_H
+#define HX_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HX_ABI_VERSION 1
+#define HX_CAP_MAX 16777215      /* 2^24 - 1 */
+#define HX_MAX_GPUS 255
+#define HX_MAX_GROUPS 255
+#define HX_MAX_TP 8              /* tp_mask bits 0..7 */
+#define HX_MAX_PP 32             /* pp_mask bits 0..31 */
+#define HX_UNUSED 0xFF
+#define HX_PREFILL 0
+#define HX_DECODE 1
+
+/* Return codes.  HX_ENOCONV is never returned: it marks a candidate's flow_value on the device. */
+enum {
+    HX_OK = 0,
+    HX_EINVAL = -1,   /* invalid argument (null pointer, size or mask out of range) */
+    HX_ETOOBIG = -2,  /* a flow network exceeds the max-flow kernel's LDS plan */
+    HX_EHIP = -3,     /* a HIP launch failed; hx_last_error() keeps the runtime's message */
+    HX_ENOCONV = -4   /* max-flow did not finish within its operation budget (per candidate) */
+};
+
+/* The device graph G = (D, E) of Sec. 3.2 with the per-GPU parameters of Table 1's legend. */
+typedef struct hx_cluster {
+    int32_t n_gpus;             /* G, 1..255 */
+    int32_t n_types;            /* T >= 1 */
+    const int32_t *gpu_type;    /* [G], each in [0, T) */
+    const double *type_flops;   /* [T] c_d, tensor FLOP/s */
+    const double *type_hbm_bw;  /* [T] m_d as memory bandwidth, bytes/s (decode weight scan) */
+    const double *type_mem;     /* [T] m_d as memory limit, bytes (memory-limit row) */
+    const double *beta;         /* [G*G] beta_{d,d'} bytes/s, row d = sender; diagonal unused, > 0 elsewhere */
+    const double *alpha;        /* [G*G] alpha_{d,d'} seconds, row d = sender; diagonal unused */
+    double coord_bw;            /* [host] coordinator link bytes/s; 0 = source/sink edges unbounded */
+    double req_bytes;           /* [host] bytes per request on coordinator links */
+} hx_cluster;
+
+/* Model shape (Table 1 legend): L layers, hidden size H, B bytes per element.  KV-cache
+ * terms use H_kv = H * n_kv_heads / n_heads (grouped-query attention); H*n_kv_heads must be
+ * divisible by n_heads. */
+typedef struct hx_model { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hx_model;
+
+/* Inference task t of Table 1: prompt length s_in and output length s_out (> 0, may be means). */
+typedef struct hx_workload { double s_in, s_out; } hx_workload;
+
+/* Strategy space: bit k of tp_mask admits TP degree k+1 (<= 8), bit k of pp_mask PP degree
+ * k+1 (<= 32).  granularity 0: one flow node per replica; 1: one flow node per GPU. */
+typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; } hx_space;
+
+/* Candidate placements (Sec. 3.1).  assign[g][n] = group of GPU g in candidate n (HX_UNUSED
+ * or >= max_groups: GPU unused); role[k][n] = HX_PREFILL, HX_DECODE, or anything else (no
+ * group).  A group exists when it has a member and a valid role. */
+typedef struct hx_candidates {
+    int32_t n_cand;             /* N >= 1 */
+    int32_t max_groups;         /* Kmax, 1..255 */
+    const uint8_t *assign;      /* [G][N] */
+    const uint8_t *role;        /* [Kmax][N] */
+} hx_candidates;
+
+/* Per (group slot k, candidate n): the kept strategy and its node capacity.  Absent groups
+ * and groups with no feasible strategy: every field 0. */
+typedef struct hx_cost_out {
+    uint8_t *tp, *pp;           /* [Kmax][N] */
+    int32_t *bmax;              /* [Kmax][N] largest batch the memory limit admits */
+    int32_t *cap;               /* [Kmax][N] node capacity, milli-requests/s */
+    double *lat;                /* [Kmax][N] latency of one batch, seconds */
+} hx_cost_out;
+
+/* The Sec. 3.3 network of every candidate.  Prefill nodes i < n_p and decode nodes j < n_d
+ * (replicas in ascending group id, or GPUs in ascending GPU id at granularity 1); the edges
+ * are source->phi_in (src_cap), phi_in->phi_out (p_cap), phi_out(i)->delta_in(j) (kv_cap row
+ * i*n_d + j), delta_in->delta_out (d_cap), delta_out->sink (sink_cap).  Rows past n_p, n_d
+ * and n_p*n_d are not written.  max_p, max_d >= max_groups (granularity 0) or n_gpus
+ * (granularity 1), and max_pd >= floor(B/2)*ceil(B/2) for that bound B. */
+typedef struct hx_flownet {
+    int32_t n_cand, max_p, max_d, max_pd;
+    int32_t *n_p, *n_d;         /* [N] */
+    int32_t *p_slot, *d_slot;   /* [max_p][N], [max_d][N]: group id (or GPU id) of each node */
+    int32_t *src_cap, *p_cap;   /* [max_p][N] */
+    int32_t *kv_cap;            /* [max_pd][N] */
+    int32_t *d_cap, *sink_cap;  /* [max_d][N] */
+} hx_flownet;
+
+/* Host-only check of everything the calls below validate (no HIP call, no device access).
+ * cost / net may be NULL to skip their checks.  Returns HX_OK, HX_EINVAL or HX_ETOOBIG. */
+int hx_validate(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
+                const hx_candidates *cand, const hx_cost_out *cost, const hx_flownet *net);
+
+/* Table 1 cost model and Appendix A node capacities.  For every group of every candidate,
+ * every admissible strategy (tp*pp = group size, tp and pp in the masks, pp <= L; stage j =
+ * the members ranked j*tp .. j*tp+tp-1 in ascending GPU id, holding floor(L/pp) + [j < L mod
+ * pp] layers) is costed:
+ *   b_max   = min over stages and their devices of floor((M_d - A)/K) (clamped to 2^30),
+ *             A = ((12*H*H*B)/tp)*l, K = ((2*(s_in+s_out)*H_kv*B)/tp)*l + 4*(s_in+s_out)*H*B;
+ *             b_max < 1 makes the strategy infeasible.  Prefill runs at b = 1, decode at b_max.
+ *   latency = sum_j (comp_j + tp_j) + sum_{j<pp-1} pp_j with, for stage j (t = tp, l = l_j):
+ *     prefill comp = max_d((24*b*s_in*H*H)/(t*c_d))*l
+ *     decode  comp = max_d((12*H*H*B*s_out)/(t*m_d))*l + max_d((24*b*s_out*H*H)/(t*c_d))*l
+ *     TP: max_d sum_{d' != d, ascending} (alpha_{dd'} + X/(t*beta_{dd'})), times 4 then
+ *         (decode) s_out then l; X = b*s_in*H*B (prefill) or b*H*B (decode)
+ *     PP: min over d in stage j, d' in stage j+1 of (alpha_{dd'} + X/beta_{dd'}), decode
+ *         times s_out
+ *   x = (1000*b)/latency milli-requests/s; cap = min(HX_CAP_MAX, floor(x)).
+ * A prefill group keeps its lowest-latency strategy, a decode group its highest-x one (Sec.
+ * 3.3 "Compute nodes"); ties keep the smaller tp. */
+int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
+                 const hx_candidates *cand, const hx_cost_out *out, hipStream_t stream);
+
+/* Sec. 3.3 network and Appendix A edge capacities.  Node capacities come from cost->cap
+ * (granularity 1: GPU k of a group of n GPUs with capacity C gets floor(C/n) + [k < C mod n],
+ * k its rank by GPU id).  Source and sink edges carry floor(1000*coord_bw/req_bytes), or
+ * HX_CAP_MAX when either is 0.  KV edge (connection type 3) of a prefill replica (tp_p x
+ * pp_p) and a decode replica (tp_d x pp_d): over every pair of a prefill stage and a decode
+ * stage sharing n > 0 layers and every rank pair (r, q) whose KV-head slices overlap by
+ * ov = min((r+1)tp_d, (q+1)tp_p) - max(r tp_d, q tp_p) > 0, the link g -> h carries
+ * bytes = ((V1*n)*ov)/(tp_p*tp_d) with V1 = (2*s_in)*H_kv*B, in alpha_{gh} + bytes/beta_{gh};
+ * the KV time is the largest of these, and the edge capacity floor(1000/time) clamped to
+ * HX_CAP_MAX, or 0 when either replica is infeasible.  Granularity 1: the edge from prefill
+ * GPU g (replica of n_g GPUs) to decode GPU h has time alpha_{gh} + ((V1*L)/n_g)/beta_{gh}. */
+int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
+                     const hx_candidates *cand, const hx_cost_out *cost, const hx_flownet *net,
+                     hipStream_t stream);
+
+/* Maximum source-sink flow of every candidate's network (Sec. 3.3, solved there by
+ * preflow-push), by a synchronous push-relabel on the network with each replica's
+ * in -> out chain contracted, one workgroup per candidate with the residual graph in LDS.
+ *   flow_value [N]       the maximum flow (or HX_ENOCONV)
+ *   kv_flow    [max_pd][N] nullable: one maximum flow's value on every KV edge (not unique)
+ *   cut        [max_p + max_d][N] nullable: the canonical minimum cut, the nodes reachable from
+ *              the source in the residual graph; row i < max_p is prefill node i, row max_p + j
+ *              decode node j; bit 0 = its in-node, bit 1 = its out-node.  Unique for every max flow.
+ * Returns HX_ETOOBIG when max_p, max_d or max_pd exceed the kernel's LDS plan. */
+int hx_maxflow_batch(const hx_flownet *net, int32_t *flow_value, int32_t *kv_flow, uint8_t *cut,
+                     hipStream_t stream);
+
+/* The candidate with the highest flow_value (Sec. 3.1 objective), lowest index on ties.
+ * best = device int32[2]: {index, value}.  n_cand >= 1. */
+int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, hipStream_t stream);
+
+/* Human-readable text of a return code, and the last HIP error message kept by HX_EHIP. */
+const char *hx_strerror(int code);
+const char *hx_last_error(void);
+int hx_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HX_H */

@@ -1,0 +1,182 @@
+// hx_api.cpp -- the C-ABI of libhx: host-side validation, launch geometry and error codes.
+// Every entry point checks its arguments without touching device memory, enqueues its
+// kernels on the caller's stream and returns; see include/hx.h for the contract.
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "hx_internal.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int hip_error(hipError_t e) {
+    snprintf(g_last_error, sizeof g_last_error, "%s: %s", hipGetErrorName(e), hipGetErrorString(e));
+    return HX_EHIP;
+}
+
+bool finite_pos(double x) { return isfinite(x) && x > 0.0; }
+
+int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, const hx_space& s,
+                  const hx_candidates* k) {
+    if (!c || !k) return HX_EINVAL;
+    if (c->n_gpus < 1 || c->n_gpus > HX_MAX_GPUS || c->n_types < 1) return HX_EINVAL;
+    if (!c->gpu_type || !c->type_flops || !c->type_hbm_bw || !c->type_mem || !c->beta || !c->alpha)
+        return HX_EINVAL;
+    if (!(c->coord_bw >= 0.0) || !(c->req_bytes >= 0.0) || !isfinite(c->coord_bw) || !isfinite(c->req_bytes))
+        return HX_EINVAL;
+    if (m.n_layers < 1 || m.hidden < 1 || m.n_heads < 1 || m.n_kv_heads < 1 || m.n_kv_heads > m.n_heads ||
+        m.bytes_per_elem < 1)
+        return HX_EINVAL;
+    if (((int64_t)m.hidden * m.n_kv_heads) % m.n_heads != 0) return HX_EINVAL;
+    if (!finite_pos(w.s_in) || !finite_pos(w.s_out)) return HX_EINVAL;
+    if (s.tp_mask == 0 || s.tp_mask >= (1u << HX_MAX_TP) || s.pp_mask == 0) return HX_EINVAL;
+    if (s.granularity != 0 && s.granularity != 1) return HX_EINVAL;
+    if (k->n_cand < 1 || k->max_groups < 1 || k->max_groups > HX_MAX_GROUPS || !k->assign || !k->role)
+        return HX_EINVAL;
+    return HX_OK;
+}
+
+int check_cost(const hx_cost_out* o) {
+    if (!o || !o->tp || !o->pp || !o->bmax || !o->cap || !o->lat) return HX_EINVAL;
+    return HX_OK;
+}
+
+// Room every network of the batch needs: nodes per side and KV edges.
+int check_net_shape(const hx_flownet* f) {
+    if (!f || f->n_cand < 1 || f->max_p < 1 || f->max_d < 1 || f->max_pd < 1) return HX_EINVAL;
+    if (!f->n_p || !f->n_d || !f->src_cap || !f->p_cap || !f->kv_cap || !f->d_cap || !f->sink_cap)
+        return HX_EINVAL;
+    return HX_OK;
+}
+
+int check_net_for(const hx_cluster* c, const hx_space& s, const hx_candidates* k, const hx_flownet* f) {
+    int rc = check_net_shape(f);
+    if (rc) return rc;
+    if (!f->p_slot || !f->d_slot || f->n_cand != k->n_cand) return HX_EINVAL;
+    const int64_t bound = s.granularity == 0 ? k->max_groups : c->n_gpus;
+    if (f->max_p < bound || f->max_d < bound || f->max_pd < (bound / 2) * ((bound + 1) / 2)) return HX_EINVAL;
+    return HX_OK;
+}
+
+int32_t coord_cap(const hx_cluster* c) {
+    if (c->coord_bw > 0.0 && c->req_bytes > 0.0) {
+        const double x = (1000.0 * c->coord_bw) / c->req_bytes;
+        if (!(x >= 0.0)) return 0;
+        return x >= (double)HX_CAP_MAX ? HX_CAP_MAX : (int32_t)floor(x);
+    }
+    return HX_CAP_MAX;
+}
+
+hx::Problem make_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, const hx_space& s,
+                         const hx_candidates* k) {
+    hx::Problem p;
+    p.G = c->n_gpus;
+    p.T = c->n_types;
+    p.N = k->n_cand;
+    p.Kmax = k->max_groups;
+    p.L = m.n_layers;
+    p.tp_mask = s.tp_mask;
+    p.pp_mask = s.pp_mask;
+    p.granularity = s.granularity;
+    p.H = (double)m.hidden;
+    p.Hkv = (double)((int64_t)m.hidden * m.n_kv_heads / m.n_heads);
+    p.B = (double)m.bytes_per_elem;
+    p.s_in = w.s_in;
+    p.s_out = w.s_out;
+    p.coord_cap = coord_cap(c);
+    p.gpu_type = c->gpu_type;
+    p.flops = c->type_flops;
+    p.hbm = c->type_hbm_bw;
+    p.mem = c->type_mem;
+    p.beta = c->beta;
+    p.alpha = c->alpha;
+    p.assign = k->assign;
+    p.role = k->role;
+    return p;
+}
+
+hx::CostOut make_cost(const hx_cost_out* o) { return hx::CostOut{o->tp, o->pp, o->bmax, o->cap, o->lat}; }
+
+hx::FlowNet make_net(const hx_flownet* f) {
+    return hx::FlowNet{f->n_cand, f->max_p,   f->max_d,  f->max_pd, f->n_p,   f->n_d,    f->p_slot,
+                       f->d_slot, f->src_cap, f->p_cap, f->kv_cap, f->d_cap, f->sink_cap};
+}
+
+// Rounds of push-relabel allowed per candidate; HX_MAXFLOW_ROUND_BUDGET overrides it so that
+// tests can force the non-convergence path from the host.
+int32_t round_budget() {
+    const char* e = getenv("HX_MAXFLOW_ROUND_BUDGET");
+    if (e && *e) {
+        long v = strtol(e, nullptr, 10);
+        if (v >= 1 && v <= (1L << 30)) return (int32_t)v;
+    }
+    return 1 << 22;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hx_abi_version(void) { return HX_ABI_VERSION; }
+
+const char* hx_strerror(int code) {
+    switch (code) {
+        case HX_OK: return "ok";
+        case HX_EINVAL: return "invalid argument";
+        case HX_ETOOBIG: return "flow network exceeds the max-flow kernel's LDS plan";
+        case HX_EHIP: return "HIP launch error (see hx_last_error)";
+        case HX_ENOCONV: return "max-flow did not converge within its round budget";
+        default: return "unknown error";
+    }
+}
+
+const char* hx_last_error(void) { return g_last_error; }
+
+int hx_validate(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space, const hx_candidates* cand,
+                const hx_cost_out* cost, const hx_flownet* net) {
+    int rc = check_problem(cluster, model, wl, space, cand);
+    if (rc) return rc;
+    if (cost && (rc = check_cost(cost))) return rc;
+    if (net) {
+        if ((rc = check_net_for(cluster, space, cand, net))) return rc;
+        if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
+    }
+    return HX_OK;
+}
+
+int hx_cost_eval(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space, const hx_candidates* cand,
+                 const hx_cost_out* out, hipStream_t stream) {
+    int rc = check_problem(cluster, model, wl, space, cand);
+    if (rc || (rc = check_cost(out))) return rc;
+    hipError_t e = hx::launch_cost(make_problem(cluster, model, wl, space, cand), make_cost(out), stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_build_flownet(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
+                     const hx_candidates* cand, const hx_cost_out* cost, const hx_flownet* net, hipStream_t stream) {
+    int rc = check_problem(cluster, model, wl, space, cand);
+    if (rc || (rc = check_cost(cost)) || (rc = check_net_for(cluster, space, cand, net))) return rc;
+    hipError_t e = hx::launch_flownet(make_problem(cluster, model, wl, space, cand), make_cost(cost), make_net(net),
+                                      stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_maxflow_batch(const hx_flownet* net, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, hipStream_t stream) {
+    int rc = check_net_shape(net);
+    if (rc) return rc;
+    if (!flow_value) return HX_EINVAL;
+    if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
+    hipError_t e = hx::launch_maxflow(make_net(net), flow_value, kv_flow, cut, round_budget(), stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, hipStream_t stream) {
+    if (!flow_value || !best || n_cand < 1) return HX_EINVAL;
+    hipError_t e = hx::launch_best(flow_value, n_cand, best, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,203 @@
+// hx_flownet.hip -- the Sec. 3.3 flow network of every candidate, on gfx950.
+//
+// Two kernels, both candidate-fastest so that loads and stores of the [row][n] arrays are
+// coalesced across the wavefront:
+//   nodes_kernel  one lane per candidate: lists the prefill and decode nodes (replicas in
+//                 ascending group id, or GPUs in ascending id at per-GPU granularity) with
+//                 their source, node and sink capacities (Appendix A);
+//   kv_kernel     one lane per (prefill node i, candidate): the KV edges from node i to every
+//                 decode node (connection type 3; Table 1 last row; Appendix A).
+// Per-lane scratch (group sizes, member lists) lives in LDS columns, one per lane.
+#include "hx_internal.h"
+
+namespace hx {
+namespace {
+
+constexpr int kNodeBlock = 64;
+constexpr int kKvBlock = 64;
+
+__global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o, FlowNet f) {
+    extern __shared__ uint8_t sm[];
+    const int tid = threadIdx.x;
+    const int stride = blockDim.x;
+    const int n = blockIdx.x * blockDim.x + tid;
+    if (n >= p.N) return;
+    uint8_t* size = sm + tid;                       // [Kmax][blockDim] members per group
+    uint8_t* rank = sm + p.Kmax * stride + tid;     // [Kmax][blockDim] members seen so far
+    for (int k = 0; k < p.Kmax; ++k) {
+        size[k * stride] = 0;
+        rank[k * stride] = 0;
+    }
+    for (int g = 0; g < p.G; ++g) {
+        const int k = p.assign[(int64_t)g * p.N + n];
+        if (k < p.Kmax) size[k * stride] += 1;
+    }
+    const int N = p.N;
+    int np = 0, nd = 0;
+    if (p.granularity == 0) {
+        for (int k = 0; k < p.Kmax; ++k) {
+            if (size[k * stride] == 0) continue;
+            const int r = p.role[(int64_t)k * N + n];
+            const int32_t c = o.cap[(int64_t)k * N + n];
+            if (r == HX_PREFILL) {
+                const int64_t e = (int64_t)np * N + n;
+                f.p_slot[e] = k;
+                f.src_cap[e] = p.coord_cap;
+                f.p_cap[e] = c;
+                ++np;
+            } else if (r == HX_DECODE) {
+                const int64_t e = (int64_t)nd * N + n;
+                f.d_slot[e] = k;
+                f.d_cap[e] = c;
+                f.sink_cap[e] = p.coord_cap;
+                ++nd;
+            }
+        }
+    } else {
+        // Per-GPU nodes: the k-th member (by GPU id) of a replica of sz GPUs and capacity C
+        // carries floor(C/sz) + [k < C mod sz].
+        for (int g = 0; g < p.G; ++g) {
+            const int k = p.assign[(int64_t)g * N + n];
+            if (k >= p.Kmax) continue;
+            const int r = p.role[(int64_t)k * N + n];
+            if (r != HX_PREFILL && r != HX_DECODE) continue;
+            const int rk = rank[k * stride];
+            rank[k * stride] = (uint8_t)(rk + 1);
+            const int sz = size[k * stride];
+            const int32_t C = o.cap[(int64_t)k * N + n];
+            const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
+            if (r == HX_PREFILL) {
+                const int64_t e = (int64_t)np * N + n;
+                f.p_slot[e] = g;
+                f.src_cap[e] = p.coord_cap;
+                f.p_cap[e] = share;
+                ++np;
+            } else {
+                const int64_t e = (int64_t)nd * N + n;
+                f.d_slot[e] = g;
+                f.d_cap[e] = share;
+                f.sink_cap[e] = p.coord_cap;
+                ++nd;
+            }
+        }
+    }
+    f.n_p[n] = np;
+    f.n_d[n] = nd;
+}
+
+// Members of group k of candidate n in ascending GPU id, into out[r * stride]; returns the count.
+__device__ int group_members(const Problem& p, int n, int k, uint8_t* out, int stride) {
+    int cnt = 0;
+    for (int g = 0; g < p.G; ++g)
+        if (p.assign[(int64_t)g * p.N + n] == k) out[(cnt++) * stride] = (uint8_t)g;
+    return cnt;
+}
+
+// KV time of one request from a prefill replica (pm, ptp x ppp) to a decode replica
+// (dm, dtp x dpp): the slowest of the links that carry a layer range and head slice.
+__device__ double kv_time(const Problem& p, const uint8_t* pm, int ptp, int ppp, const uint8_t* dm, int dtp,
+                          int dpp, int stride) {
+    const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
+    const double den = (double)(ptp * dtp);
+    double worst = 0.0;
+    int a0 = 0;
+    for (int a = 0; a < ppp; ++a) {
+        const int a1 = a0 + stage_layers(p.L, ppp, a);
+        int b0 = 0;
+        for (int bb = 0; bb < dpp; ++bb) {
+            const int b1 = b0 + stage_layers(p.L, dpp, bb);
+            const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+            if (nab > 0) {
+                const double Vn = V1 * (double)nab;
+                for (int r = 0; r < ptp; ++r) {
+                    const int g = pm[(a * ptp + r) * stride];
+                    const double* arow = p.alpha + g * p.G;
+                    const double* brow = p.beta + g * p.G;
+                    for (int q = 0; q < dtp; ++q) {
+                        const int hi = (r + 1) * dtp < (q + 1) * ptp ? (r + 1) * dtp : (q + 1) * ptp;
+                        const int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
+                        const int ov = hi - lo;
+                        if (ov <= 0) continue;
+                        const int h = dm[(bb * dtp + q) * stride];
+                        const double bytes = (Vn * (double)ov) / den;
+                        const double time = arow[h] + bytes / brow[h];
+                        if (time > worst) worst = time;
+                    }
+                }
+            }
+            b0 = b1;
+        }
+        a0 = a1;
+    }
+    return worst;
+}
+
+__global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
+    extern __shared__ uint8_t sm[];
+    const int tid = threadIdx.x;
+    const int stride = blockDim.x;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
+    const int N = p.N;
+    if (gid >= (int64_t)f.max_p * N) return;
+    const int i = (int)(gid / N);
+    const int n = (int)(gid - (int64_t)i * N);
+    const int np = f.n_p[n];
+    if (i >= np) return;
+    const int nd = f.n_d[n];
+    int32_t* kv = f.kv_cap + (int64_t)(i * nd) * N + n;
+
+    if (p.granularity == 0) {
+        uint8_t* pm = sm + tid;                   // [G][blockDim]
+        uint8_t* dm = sm + p.G * stride + tid;    // [G][blockDim]
+        // A strategy whose tp*pp is not the group's size (cost outputs of another batch) is
+        // treated as infeasible rather than read past the member list.
+        const int kp = f.p_slot[(int64_t)i * N + n];
+        const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
+        const bool p_ok = ptp > 0 && group_members(p, n, kp, pm, stride) == ptp * ppp;
+        for (int j = 0; j < nd; ++j) {
+            const int kd = f.d_slot[(int64_t)j * N + n];
+            const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
+            int32_t c = 0;
+            if (p_ok && dtp > 0 && group_members(p, n, kd, dm, stride) == dtp * dpp)
+                c = quantize(1000.0 / kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride));
+            kv[(int64_t)j * N] = c;
+        }
+    } else {
+        // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
+        const int g = f.p_slot[(int64_t)i * N + n];
+        const int kp = p.assign[(int64_t)g * N + n];
+        int szp = 0;
+        for (int x = 0; x < p.G; ++x) szp += p.assign[(int64_t)x * N + n] == kp ? 1 : 0;
+        const bool feas_p = o.tp[(int64_t)kp * N + n] > 0;
+        const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
+        const double share = (V1 * (double)p.L) / (double)szp;
+        const double* arow = p.alpha + g * p.G;
+        const double* brow = p.beta + g * p.G;
+        for (int j = 0; j < nd; ++j) {
+            const int h = f.d_slot[(int64_t)j * N + n];
+            const int kd = p.assign[(int64_t)h * N + n];
+            int32_t c = 0;
+            if (feas_p && o.tp[(int64_t)kd * N + n] > 0) c = quantize(1000.0 / (arow[h] + share / brow[h]));
+            kv[(int64_t)j * N] = c;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
+    {
+        const int blocks = (p.N + kNodeBlock - 1) / kNodeBlock;
+        const size_t lds = 2 * (size_t)p.Kmax * kNodeBlock;
+        hipLaunchKernelGGL(nodes_kernel, dim3(blocks), dim3(kNodeBlock), lds, s, p, o, f);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int64_t lanes = (int64_t)f.max_p * p.N;
+    const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
+    const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
+    hipLaunchKernelGGL(kv_kernel, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    return hipGetLastError();
+}
+
+}  // namespace hx

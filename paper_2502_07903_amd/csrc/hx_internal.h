@@ -1,0 +1,57 @@
+// hx_internal.h -- launch interfaces and device helpers shared by libhx's HIP sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hx.h"
+
+namespace hx {
+
+constexpr double kBmaxClamp = 1073741824.0;  // 2^30
+
+// Scalars of one scoring problem, copied into every kernel's argument block.
+struct Problem {
+    int32_t G, T, N, Kmax, L;
+    uint32_t tp_mask, pp_mask;
+    int32_t granularity;
+    double H, Hkv, B, s_in, s_out;
+    int32_t coord_cap;
+    const int32_t* gpu_type;
+    const double *flops, *hbm, *mem, *beta, *alpha;
+    const uint8_t *assign, *role;
+};
+
+struct CostOut {
+    uint8_t *tp, *pp;
+    int32_t *bmax, *cap;
+    double* lat;
+};
+
+struct FlowNet {
+    int32_t N, max_p, max_d, max_pd;
+    int32_t *n_p, *n_d, *p_slot, *d_slot, *src_cap, *p_cap, *kv_cap, *d_cap, *sink_cap;
+};
+
+// Capacity in milli-requests/s: floor(x), clamped to [0, HX_CAP_MAX].
+__device__ __forceinline__ int32_t quantize(double x) {
+    if (!(x >= 0.0)) return 0;
+    if (x >= (double)HX_CAP_MAX) return HX_CAP_MAX;
+    return (int32_t)floor(x);
+}
+
+__device__ __forceinline__ double dmin(double a, double b) { return b < a ? b : a; }
+__device__ __forceinline__ double dmax(double a, double b) { return b > a ? b : a; }
+
+// Layers held by stage j of pp: floor(L/pp) + [j < L mod pp].
+__device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
+
+hipError_t launch_cost(const Problem& p, const CostOut& o, hipStream_t s);
+hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s);
+// LDS bytes the max-flow kernel needs for a network plan; 0 if it does not fit.
+size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
+hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
+                          int32_t op_budget, hipStream_t s);
+hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
+
+}  // namespace hx

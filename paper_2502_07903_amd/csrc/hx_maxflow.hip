@@ -1,0 +1,321 @@
+// hx_maxflow.hip -- maximum flow of every candidate's network (Sec. 3.3) on gfx950.
+//
+// The paper solves each network with preflow-push.  Here one workgroup owns one candidate
+// and runs a synchronous push-relabel with its whole residual graph in LDS.
+//
+// Network.  In the Sec. 3.3 network every replica is an in -> out chain with one edge in
+// and the KV edges out (prefill) or the KV edges in and one edge out (decode), so the
+// chains contract without changing any s-t cut: prefill node p gets a_p = min(src, p_cap)
+// from the source, decode node d sends b_d = min(d_cap, sink) to the sink, and c_pd are the
+// KV edges.  The contracted graph is bipartite: s -> P -> D -> t.
+//
+// Algorithm (Goldberg-Tarjan push-relabel, in synchronous rounds).  The source sits at
+// height V = P + D + 2, the sink at 0.  A round has two phases separated by barriers:
+//   P-phase: each active prefill node pushes along its admissible arcs (to decode nodes one
+//            level lower, then back to the source), then relabels if excess remains;
+//   D-phase: each active decode node pushes to the sink and back along its reverse KV arcs,
+//            then relabels if excess remains.
+// Within a phase the active nodes lie on one side of the bipartition, so their pushes touch
+// disjoint arcs and their relabels read only the other side's heights, which that phase never
+// changes: the phase equals some sequential order of the same push/relabel operations, and
+// the usual termination and optimality arguments apply.  Excess arriving at the other side
+// is added with LDS atomics.  Exact heights (BFS distances to the sink, else V + distance to
+// the source) are recomputed every few rounds by label-correcting sweeps (global relabel).
+// The run ends when no node has excess: the preflow is then a maximum flow.
+//
+// Outputs: the flow value, the flow on every KV edge, and the canonical minimum cut (nodes of
+// the uncontracted network reachable from the source in the residual graph).
+#include <stdlib.h>
+
+#include "hx_internal.h"
+
+namespace hx {
+namespace {
+
+constexpr int kGlobalRelabelEvery = 8;  // rounds between exact relabels
+
+struct MfLayout {
+    int32_t* cap;   // [P][Ds] KV capacities, row stride Ds = D | 1 (odd: no bank conflicts)
+    int32_t* fl;    // [P][Ds] KV flows
+    int32_t* a;     // [P] source -> p capacity
+    int32_t* fs;    // [P] source -> p flow
+    int32_t* ep;    // [P] excess
+    int32_t* hp;    // [P] height
+    int32_t* b;     // [D] d -> sink capacity
+    int32_t* ft;    // [D] d -> sink flow
+    int32_t* ed;    // [D] excess
+    int32_t* hd;    // [D] height
+    int32_t* misc;  // [4] scalars
+};
+
+__device__ inline MfLayout carve(int32_t* sm, int max_p, int max_d, int max_pd) {
+    MfLayout L;
+    const int arc = max_pd + max_p;  // P*(D|1) <= P*D + P
+    L.cap = sm;
+    L.fl = L.cap + arc;
+    L.a = L.fl + arc;
+    L.fs = L.a + max_p;
+    L.ep = L.fs + max_p;
+    L.hp = L.ep + max_p;
+    L.b = L.hp + max_p;
+    L.ft = L.b + max_d;
+    L.ed = L.ft + max_d;
+    L.hd = L.ed + max_d;
+    L.misc = L.hd + max_d;
+    return L;
+}
+
+// Exact heights by label-correcting sweeps: hd = 1 where d -> t has residual, hp = V + 1 where
+// p -> s has residual (reverse of a used source edge), then relax along residual arcs.
+__device__ void global_relabel(const MfLayout& L, int P, int D, int Ds, int V, int INF) {
+    const int tid = threadIdx.x, T = blockDim.x;
+    for (int i = tid; i < P; i += T) L.hp[i] = L.fs[i] > 0 ? V + 1 : INF;
+    for (int j = tid; j < D; j += T) L.hd[j] = L.b[j] - L.ft[j] > 0 ? 1 : INF;
+    __syncthreads();
+    for (;;) {
+        bool changed = false;
+        for (int i = tid; i < P; i += T) {
+            int h = L.hp[i];
+            const int32_t* c = L.cap + i * Ds;
+            const int32_t* f = L.fl + i * Ds;
+            for (int d = 0; d < D; ++d)
+                if (c[d] - f[d] > 0 && L.hd[d] + 1 < h) h = L.hd[d] + 1;
+            if (h < L.hp[i]) {
+                L.hp[i] = h;
+                changed = true;
+            }
+        }
+        __syncthreads();
+        for (int j = tid; j < D; j += T) {
+            int h = L.hd[j];
+            for (int q = 0; q < P; ++q)
+                if (L.fl[q * Ds + j] > 0 && L.hp[q] + 1 < h) h = L.hp[q] + 1;
+            if (h < L.hd[j]) {
+                L.hd[j] = h;
+                changed = true;
+            }
+        }
+        if (!__syncthreads_or(changed)) break;
+    }
+}
+
+__global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
+                                                      int32_t round_budget) {
+    // XCD-aware order: the hardware deals consecutive workgroups to the 8 XCDs in turn, so
+    // workgroup w takes candidate (w mod 8) * chunk + w / 8 and each XCD walks a contiguous
+    // candidate range, sharing the L2 lines of the candidate-fastest input arrays.
+    const int chunk = (f.N + 7) / 8;
+    const int n = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
+    if (n >= f.N) return;
+    extern __shared__ int32_t smem[];
+    const MfLayout L = carve(smem, f.max_p, f.max_d, f.max_pd);
+    const int tid = threadIdx.x, T = blockDim.x;
+    const int N = f.N;
+    const int P = f.n_p[n], D = f.n_d[n];
+    // A network larger than the plan it was built for is rejected before any LDS or array
+    // index is formed from it.
+    if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || P * D > f.max_pd) {
+        if (threadIdx.x == 0) flow_value[n] = HX_EINVAL;
+        return;
+    }
+    const int Ds = D | 1;
+
+    for (int e = tid; e < P * D; e += T) {
+        const int i = e / D, d = e - i * D;
+        L.cap[i * Ds + d] = f.kv_cap[(int64_t)e * N + n];
+        L.fl[i * Ds + d] = 0;
+    }
+    for (int i = tid; i < P; i += T) {
+        const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+        const int32_t a = s < c ? s : c;
+        L.a[i] = a;
+        L.fs[i] = a;  // saturate every source edge
+        L.ep[i] = a;
+    }
+    for (int j = tid; j < D; j += T) {
+        const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+        L.b[j] = c < t ? c : t;
+        L.ft[j] = 0;
+        L.ed[j] = 0;
+    }
+    if (tid == 0) L.misc[0] = 0;
+    __syncthreads();
+
+    const int V = P + D + 2;
+    const int INF = 2 * V + 2;
+    bool converged = false;
+    if (P > 0 && D > 0) {
+        for (int round = 0; round < round_budget; ++round) {
+            if (round % kGlobalRelabelEvery == 0) {
+                global_relabel(L, P, D, Ds, V, INF);
+                __syncthreads();
+            }
+            // P-phase
+            for (int i = tid; i < P; i += T) {
+                int e = L.ep[i];
+                if (e <= 0) continue;
+                const int h = L.hp[i];
+                const int32_t* c = L.cap + i * Ds;
+                int32_t* fr = L.fl + i * Ds;
+                for (int d = 0; d < D && e > 0; ++d) {
+                    const int r = c[d] - fr[d];
+                    if (r > 0 && h == L.hd[d] + 1) {
+                        const int amt = r < e ? r : e;
+                        fr[d] += amt;
+                        e -= amt;
+                        atomicAdd(&L.ed[d], amt);
+                    }
+                }
+                if (e > 0 && h == V + 1) {
+                    const int amt = L.fs[i] < e ? L.fs[i] : e;
+                    L.fs[i] -= amt;
+                    e -= amt;
+                }
+                if (e > 0) {
+                    int mh = INF;
+                    for (int d = 0; d < D; ++d)
+                        if (c[d] - fr[d] > 0 && L.hd[d] < mh) mh = L.hd[d];
+                    if (L.fs[i] > 0 && V < mh) mh = V;
+                    L.hp[i] = mh + 1 < INF ? mh + 1 : INF;
+                }
+                L.ep[i] = e;
+            }
+            __syncthreads();
+            // D-phase
+            for (int j = tid; j < D; j += T) {
+                int e = L.ed[j];
+                if (e <= 0) continue;
+                const int h = L.hd[j];
+                if (h == 1) {
+                    const int r = L.b[j] - L.ft[j];
+                    const int amt = r < e ? r : e;
+                    if (amt > 0) {
+                        L.ft[j] += amt;
+                        e -= amt;
+                    }
+                }
+                for (int q = 0; q < P && e > 0; ++q) {
+                    const int fq = L.fl[q * Ds + j];
+                    if (fq > 0 && h == L.hp[q] + 1) {
+                        const int amt = fq < e ? fq : e;
+                        L.fl[q * Ds + j] = fq - amt;
+                        e -= amt;
+                        atomicAdd(&L.ep[q], amt);
+                    }
+                }
+                if (e > 0) {
+                    int mh = L.b[j] - L.ft[j] > 0 ? 0 : INF;
+                    for (int q = 0; q < P; ++q)
+                        if (L.fl[q * Ds + j] > 0 && L.hp[q] < mh) mh = L.hp[q];
+                    L.hd[j] = mh + 1 < INF ? mh + 1 : INF;
+                }
+                L.ed[j] = e;
+            }
+            __syncthreads();
+            bool active = false;
+            for (int i = tid; i < P; i += T) active |= L.ep[i] > 0;
+            for (int j = tid; j < D; j += T) active |= L.ed[j] > 0;
+            if (!__syncthreads_or(active)) {
+                converged = true;
+                break;
+            }
+        }
+    } else {
+        converged = true;  // no prefill or no decode node: the maximum flow is 0
+        for (int i = tid; i < P; i += T) L.fs[i] = 0;
+        __syncthreads();
+    }
+
+    // Flow value = total flow into the sink.
+    for (int j = tid; j < D; j += T)
+        if (L.ft[j] > 0) atomicAdd(&L.misc[0], L.ft[j]);
+    __syncthreads();
+    if (tid == 0) flow_value[n] = converged ? L.misc[0] : HX_ENOCONV;
+    if (kv_flow)
+        for (int e = tid; e < P * D; e += T) {
+            const int i = e / D, d = e - i * D;
+            kv_flow[(int64_t)e * N + n] = L.fl[i * Ds + d];
+        }
+    if (!cut) return;
+
+    // Canonical minimum cut: reachability from s in the residual graph of the uncontracted
+    // network, by sweeps until nothing changes.  Reuses a/ep (prefill in/out flags) and
+    // b/ed (decode in/out flags); source/node/sink capacities are reloaded.
+    int32_t* rin = L.ep;
+    int32_t* rout = L.a;
+    int32_t* din = L.ed;
+    int32_t* dout = L.b;
+    __syncthreads();
+    for (int i = tid; i < P; i += T) {
+        rin[i] = f.src_cap[(int64_t)i * N + n] - L.fs[i] > 0;
+        rout[i] = 0;
+    }
+    for (int j = tid; j < D; j += T) {
+        din[j] = 0;
+        dout[j] = 0;
+    }
+    __syncthreads();
+    for (;;) {
+        bool changed = false;
+        // prefill replica: phi_out is reached from a reached delta_in over a used KV edge (its
+        // reverse arc), and in <-> out inside the chain along whichever arcs have residual.
+        for (int i = tid; i < P; i += T) {
+            const int32_t fsi = L.fs[i];
+            const int32_t pres = f.p_cap[(int64_t)i * N + n] - fsi;
+            int in = rin[i], out = rout[i];
+            for (int d = 0; d < D && !out; ++d) out = din[d] && L.fl[i * Ds + d] > 0;
+            for (int k = 0; k < 2; ++k) {
+                in |= out && fsi > 0;
+                out |= in && pres > 0;
+            }
+            if (in != rin[i] || out != rout[i]) {
+                rin[i] = in;
+                rout[i] = out;
+                changed = true;
+            }
+        }
+        __syncthreads();
+        // decode replica: delta_in is reached from a reached phi_out over a KV edge with
+        // residual capacity, then in <-> out inside the chain.
+        for (int j = tid; j < D; j += T) {
+            const int32_t ftj = L.ft[j];
+            const int32_t dres = f.d_cap[(int64_t)j * N + n] - ftj;
+            int in = din[j], out = dout[j];
+            for (int q = 0; q < P && !in; ++q) in = rout[q] && L.cap[q * Ds + j] - L.fl[q * Ds + j] > 0;
+            for (int k = 0; k < 2; ++k) {
+                out |= in && dres > 0;
+                in |= out && ftj > 0;
+            }
+            if (in != din[j] || out != dout[j]) {
+                din[j] = in;
+                dout[j] = out;
+                changed = true;
+            }
+        }
+        if (!__syncthreads_or(changed)) break;
+    }
+    for (int i = tid; i < P; i += T) cut[(int64_t)i * N + n] = (uint8_t)(rin[i] | (rout[i] << 1));
+    for (int j = tid; j < D; j += T) cut[(int64_t)(f.max_p + j) * N + n] = (uint8_t)(din[j] | (dout[j] << 1));
+}
+
+}  // namespace
+
+size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd) {
+    const size_t words = 2 * ((size_t)max_pd + max_p) + 4 * (size_t)max_p + 4 * (size_t)max_d + 4;
+    const size_t bytes = words * sizeof(int32_t);
+    return bytes <= 64 * 1024 ? bytes : 0;
+}
+
+hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
+                          hipStream_t s) {
+    const size_t lds = maxflow_lds_bytes(f.max_p, f.max_d, f.max_pd);
+    const int widest = f.max_p > f.max_d ? f.max_p : f.max_d;
+    int threads = ((widest + 63) / 64) * 64;
+    if (threads > 256) threads = 256;
+    const int chunk = (f.N + 7) / 8;
+    const int blocks = 8 * chunk;
+    hipLaunchKernelGGL(maxflow_kernel, dim3(blocks), dim3(threads), lds, s, f, flow_value, kv_flow, cut, round_budget);
+    return hipGetLastError();
+}
+
+}  // namespace hx

@@ -195,3 +195,60 @@ def bipartite_closed_form(a: np.ndarray, b: np.ndarray, c: np.ndarray) -> int:
             v += min(int(b[d]), sum(int(c[p, d]) for p in X))
         best = v if best is None else min(best, v)
     return best
+
+
+def used_rows(fn: Dict[str, np.ndarray]):
+    """Masks of the rows the network of each candidate uses: prefill, decode and KV rows."""
+    mp, md, mpd = fn["dims"]
+    P, D = fn["n_p"].astype(np.int64), fn["n_d"].astype(np.int64)
+    return (np.arange(mp)[:, None] < P[None, :], np.arange(md)[:, None] < D[None, :],
+            np.arange(mpd)[:, None] < (P * D)[None, :])
+
+
+def compare_flownet(got: Dict[str, np.ndarray], want: Dict[str, np.ndarray]) -> None:
+    assert np.array_equal(got["n_p"], want["n_p"]), "n_p differs"
+    assert np.array_equal(got["n_d"], want["n_d"]), "n_d differs"
+    up, ud, ukv = used_rows(want)
+    for k, m in (("p_slot", up), ("src_cap", up), ("p_cap", up), ("d_slot", ud), ("d_cap", ud),
+                 ("sink_cap", ud), ("kv_cap", ukv)):
+        bad = m & (got[k] != want[k])
+        assert not bad.any(), f"{k} differs at (row, candidate) {np.argwhere(bad)[:5].tolist()}"
+
+
+def check_flow_batch(fn: Dict[str, np.ndarray], flow_value: np.ndarray, kv_flow: np.ndarray,
+                     chunk: int = 16384) -> None:
+    """Vectorised validity of KV flows: 0 <= f <= cap, node throughput within the contracted
+    capacities min(src, p_cap) and min(d_cap, sink), and total = flow_value."""
+    mp, md, mpd = fn["dims"]
+    N = flow_value.shape[0]
+    for c0 in range(0, N, chunk):
+        c1 = min(N, c0 + chunk)
+        P = fn["n_p"][c0:c1].astype(np.int64)
+        D = fn["n_d"][c0:c1].astype(np.int64)
+        kv = kv_flow[:, c0:c1].astype(np.int64)
+        cap = fn["kv_cap"][:, c0:c1].astype(np.int64)
+        rows = np.arange(mpd)[:, None]
+        used = rows < (P * D)[None, :]
+        assert ((kv >= 0) & (kv <= cap) | ~used).all(), "KV flow outside [0, cap]"
+        r, n = np.nonzero(used)
+        Dn = D[n]
+        i, j = r // Dn, r % Dn
+        out_p = np.zeros((mp, c1 - c0), np.int64)
+        in_d = np.zeros((md, c1 - c0), np.int64)
+        np.add.at(out_p, (i, n), kv[r, n])
+        np.add.at(in_d, (j, n), kv[r, n])
+        a = np.minimum(fn["src_cap"][:, c0:c1], fn["p_cap"][:, c0:c1]).astype(np.int64)
+        b = np.minimum(fn["d_cap"][:, c0:c1], fn["sink_cap"][:, c0:c1]).astype(np.int64)
+        up = np.arange(mp)[:, None] < P[None, :]
+        ud = np.arange(md)[:, None] < D[None, :]
+        assert ((out_p <= a) | ~up).all(), "prefill node over capacity"
+        assert ((in_d <= b) | ~ud).all(), "decode node over capacity"
+        assert np.array_equal(out_p.sum(0), flow_value[c0:c1].astype(np.int64)), "flow value != total KV flow"
+
+
+def compare_cut(got: np.ndarray, want: np.ndarray, fn: Dict[str, np.ndarray]) -> None:
+    mp, md, _ = fn["dims"]
+    up, ud, _ = used_rows(fn)
+    mask = np.concatenate([up, ud], axis=0)
+    bad = mask & (got != want)
+    assert not bad.any(), f"cut differs at (row, candidate) {np.argwhere(bad)[:5].tolist()}"

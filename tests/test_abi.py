@@ -1,0 +1,115 @@
+"""Host-side checks of the C-ABI library (no GPU): it loads, exports every function that
+include/hx.h declares, and hx_validate accepts and rejects arguments as documented without
+any device access (the pointers below are never dereferenced)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2502_07903_amd import hx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "hx.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hx_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    names = _declared_functions()
+    assert "hx_maxflow_batch" in names and "hx_cost_eval" in names
+    lib = hx.lib()
+    for name in names:
+        assert hasattr(lib, name), f"libhx.so does not export {name}"
+    assert set(hx.EXPORTS) <= set(names)
+
+
+def test_abi_version_and_strings():
+    assert hx.lib().hx_abi_version() == 1
+    for code in (0, -1, -2, -3, -4):
+        assert hx.strerror(code)
+    assert hx.lib().hx_last_error() is not None
+
+
+FAKE = 0x1000  # a non-null address that validation must never dereference
+
+
+def _args(G=32, T=4, N=100, Kmax=16, tp=0b1011, pp=0xFF, gran=0):
+    cl = hx.hx_cluster(G, T, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, 0.0)
+    md = hx.hx_model(80, 8192, 64, 8, 2)
+    wl = hx.hx_workload(1024.0, 256.0)
+    sp = hx.hx_space(tp, pp, gran)
+    cand = hx.hx_candidates(N, Kmax, FAKE, FAKE)
+    cost = hx.hx_cost_out(FAKE, FAKE, FAKE, FAKE, FAKE)
+    b = Kmax if gran == 0 else G
+    net = hx.hx_flownet(N, b, b, (b // 2) * ((b + 1) // 2), *([FAKE] * 9))
+    return cl, md, wl, sp, cand, cost, net
+
+
+def _validate(cl, md, wl, sp, cand, cost, net):
+    return hx.lib().hx_validate(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost) if cost else None,
+                                C.byref(net) if net else None)
+
+
+def test_validate_accepts_workloads():
+    for kw in (dict(G=8, T=2, N=256, Kmax=4), dict(G=32, N=65536, Kmax=16), dict(G=64, T=5, N=262144, Kmax=32),
+               dict(G=128, T=6, N=131072, Kmax=32, gran=1)):
+        assert _validate(*_args(**kw)) == hx.HX_OK
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda a: setattr(a[0], "n_gpus", 0),
+    lambda a: setattr(a[0], "n_gpus", 256),
+    lambda a: setattr(a[0], "beta", None),
+    lambda a: setattr(a[0], "coord_bw", -1.0),
+    lambda a: setattr(a[1], "n_layers", 0),
+    lambda a: setattr(a[1], "n_kv_heads", 65),
+    lambda a: setattr(a[1], "n_heads", 48),          # H_kv = 8192 * 8 / 48 is not whole
+    lambda a: setattr(a[2], "s_in", 0.0),
+    lambda a: setattr(a[2], "s_out", float("nan")),
+    lambda a: setattr(a[3], "tp_mask", 0),
+    lambda a: setattr(a[3], "tp_mask", 1 << 8),      # TP degree 9 > 8
+    lambda a: setattr(a[3], "pp_mask", 0),
+    lambda a: setattr(a[3], "granularity", 2),
+    lambda a: setattr(a[4], "n_cand", 0),
+    lambda a: setattr(a[4], "max_groups", 256),
+    lambda a: setattr(a[4], "role", None),
+    lambda a: setattr(a[5], "lat", None),
+    lambda a: setattr(a[6], "max_pd", 63),           # 16 groups may split 8/8: 64 KV edges
+    lambda a: setattr(a[6], "max_p", 15),
+    lambda a: setattr(a[6], "n_cand", 99),
+    lambda a: setattr(a[6], "kv_cap", None),
+], ids=lambda f: "")
+def test_validate_rejects(mutate):
+    a = list(_args())
+    mutate(a)
+    assert _validate(*a) == hx.HX_EINVAL
+
+
+def test_validate_too_big_for_lds():
+    # 255 GPUs at per-GPU granularity: 127*128 KV edges exceed the LDS plan.
+    a = _args(G=255, T=6, N=10, Kmax=32, gran=1)
+    assert _validate(*a) == hx.HX_ETOOBIG
+
+
+def test_calls_reject_before_any_device_work():
+    cl, md, wl, sp, cand, cost, net = _args()
+    cand.n_cand = 0
+    L = hx.lib()
+    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None) == hx.HX_EINVAL
+    assert L.hx_build_flownet(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), C.byref(net), None) == hx.HX_EINVAL
+    assert L.hx_maxflow_batch(C.byref(net), None, None, None, None) == hx.HX_EINVAL
+    assert L.hx_best_candidate(None, 10, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_best_candidate(FAKE, 0, FAKE, None) == hx.HX_EINVAL
+    big = _args(G=255, T=6, N=10, Kmax=32, gran=1)[6]
+    assert L.hx_maxflow_batch(C.byref(big), FAKE, None, None, None) == hx.HX_ETOOBIG
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(hx, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(hx, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        hx.lib()
