@@ -10,9 +10,9 @@
  * the placement's serving throughput.  libhx runs that loop for many thousands of candidate
  * placements at once:
  *
- *   hx_cost_eval       Table 1 + Appendix A node capacities     (one lane per candidate group)
- *   hx_build_flownet   the Sec. 3.3 network and its KV edges     (one lane per candidate / node)
- *   hx_maxflow_batch   maximum flow, flow assignment, min cut    (one workgroup per candidate)
+ *   hx_cost_eval       Table 1 + Appendix A node capacities     (one lane per group, sorted by shape)
+ *   hx_build_flownet   the Sec. 3.3 network and its KV edges     (one lane per candidate / KV edge)
+ *   hx_maxflow_batch   maximum flow, flow assignment, min cut    (one lane per node, LDS-resident)
  *   hx_best_candidate  the best candidate                        (one workgroup)
  *
  * Conventions
@@ -32,6 +32,7 @@
 #ifndef HX_H
 #define HX_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -95,12 +96,15 @@ typedef struct hx_candidates {
 } hx_candidates;
 
 /* Per (group slot k, candidate n): the kept strategy and its node capacity.  Absent groups
- * and groups with no feasible strategy: every field 0. */
+ * and groups with no feasible strategy: every field 0.  members[k][w][n] is the group's
+ * member set as a GPU bitmask (bit g of word w = GPU 64w + g), hx_member_words(n_gpus) words
+ * per group; hx_build_flownet reads it. */
 typedef struct hx_cost_out {
     uint8_t *tp, *pp;           /* [Kmax][N] */
     int32_t *bmax;              /* [Kmax][N] largest batch the memory limit admits */
     int32_t *cap;               /* [Kmax][N] node capacity, milli-requests/s */
     double *lat;                /* [Kmax][N] latency of one batch, seconds */
+    uint64_t *members;          /* [Kmax][W][N] group member bitmasks, W = hx_member_words(n_gpus) */
 } hx_cost_out;
 
 /* The Sec. 3.3 network of every candidate.  Prefill nodes i < n_p and decode nodes j < n_d
@@ -141,7 +145,16 @@ int hx_validate(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_sp
  * A prefill group keeps its lowest-latency strategy, a decode group its highest-x one (Sec.
  * 3.3 "Compute nodes"); ties keep the smaller tp. */
 int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
-                 const hx_candidates *cand, const hx_cost_out *out, hipStream_t stream);
+                 const hx_candidates *cand, const hx_cost_out *out, void *workspace,
+                 size_t workspace_bytes, hipStream_t stream);
+
+/* Device scratch hx_cost_eval needs (it sorts the batch's groups by role and size so that
+ * a wavefront costs groups of one shape): caller-owned, >= this many bytes, 256-byte
+ * aligned, contents ignored on entry.  Calls that share a workspace must not overlap. */
+size_t hx_cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
+
+/* 64-bit words per GPU bitmask: 1 for n_gpus <= 64, 2 for <= 128, 4 for <= 255. */
+int hx_member_words(int32_t n_gpus);
 
 /* Sec. 3.3 network and Appendix A edge capacities.  Node capacities come from cost->cap
  * (granularity 1: GPU k of a group of n GPUs with capacity C gets floor(C/n) + [k < C mod n],

@@ -40,7 +40,7 @@ int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, 
 }
 
 int check_cost(const hx_cost_out* o) {
-    if (!o || !o->tp || !o->pp || !o->bmax || !o->cap || !o->lat) return HX_EINVAL;
+    if (!o || !o->tp || !o->pp || !o->bmax || !o->cap || !o->lat || !o->members) return HX_EINVAL;
     return HX_OK;
 }
 
@@ -98,7 +98,7 @@ hx::Problem make_problem(const hx_cluster* c, const hx_model& m, const hx_worklo
     return p;
 }
 
-hx::CostOut make_cost(const hx_cost_out* o) { return hx::CostOut{o->tp, o->pp, o->bmax, o->cap, o->lat}; }
+hx::CostOut make_cost(const hx_cost_out* o) { return hx::CostOut{o->tp, o->pp, o->bmax, o->cap, o->lat, o->members}; }
 
 hx::FlowNet make_net(const hx_flownet* f) {
     return hx::FlowNet{f->n_cand, f->max_p,   f->max_d,  f->max_pd, f->n_p,   f->n_d,    f->p_slot,
@@ -147,11 +147,21 @@ int hx_validate(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_sp
     return HX_OK;
 }
 
+size_t hx_cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    if (n_gpus < 1 || n_gpus > HX_MAX_GPUS || max_groups < 1 || max_groups > HX_MAX_GROUPS || n_cand < 1) return 0;
+    return hx::cost_workspace_bytes(n_gpus, max_groups, n_cand);
+}
+
+int hx_member_words(int32_t n_gpus) { return n_gpus < 1 || n_gpus > HX_MAX_GPUS ? 0 : hx::mask_words(n_gpus); }
+
 int hx_cost_eval(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space, const hx_candidates* cand,
-                 const hx_cost_out* out, hipStream_t stream) {
+                 const hx_cost_out* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     int rc = check_problem(cluster, model, wl, space, cand);
     if (rc || (rc = check_cost(out))) return rc;
-    hipError_t e = hx::launch_cost(make_problem(cluster, model, wl, space, cand), make_cost(out), stream);
+    if (!workspace || ((uintptr_t)workspace & 255) ||
+        workspace_bytes < hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand))
+        return HX_EINVAL;
+    hipError_t e = hx::launch_cost(make_problem(cluster, model, wl, space, cand), make_cost(out), workspace, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

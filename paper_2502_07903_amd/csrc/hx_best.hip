@@ -24,7 +24,17 @@ __global__ void __launch_bounds__(kBestBlock) best_kernel(const int32_t* __restr
     __shared__ int32_t wv[kBestBlock / 64], wi[kBestBlock / 64];
     const int tid = threadIdx.x;
     int32_t bv = INT_MIN, bi = INT_MAX;
-    for (int32_t i = tid; i < n; i += kBestBlock) take(bv, bi, v[i], i);
+    // Eight independent coalesced loads in flight per lane, then the compares in index order.
+    constexpr int kUnroll = 8;
+    int64_t i = tid;
+    for (; i + (kUnroll - 1) * kBestBlock < n; i += kUnroll * kBestBlock) {
+        int32_t x[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) x[k] = v[i + k * kBestBlock];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) take(bv, bi, x[k], (int32_t)(i + k * kBestBlock));
+    }
+    for (; i < n; i += kBestBlock) take(bv, bi, v[i], (int32_t)i);
     for (int off = 32; off > 0; off >>= 1) {
         const int32_t ov = __shfl_down(bv, off, 64);
         const int32_t oi = __shfl_down(bi, off, 64);

@@ -1,22 +1,74 @@
 // hx_cost.hip -- Table 1 cost model and Appendix A node capacities on gfx950.
 //
-// One lane per (group slot k, candidate n), candidate-fastest, so every load of the
-// candidate arrays (assign[g][n], role[k][n]) and every store of the outputs ([k][n]) is
-// coalesced across the wavefront.  A lane decodes its group's members (ascending GPU id)
-// into an LDS column of its own, then costs every admissible TP x PP strategy and keeps
-// prefill's latency-optimal / decode's throughput-optimal one (Sec. 3.3, "Compute nodes").
-// The work is FP64 scalar arithmetic: no dense contraction, so no MFMA.
+// The cost of a group depends on its role and size (which strategies exist, how many
+// stages, how many TP peers); mixing sizes in one wavefront serialises every size's loop
+// nest.  So the batch is first sorted, globally, into work units bucketed by (role, size),
+// and the costing kernel then runs one unit per lane with a wavefront-uniform control path:
 //
-// Per-GPU parameters (c_d, memory bandwidth, memory limit) are gathered once per block into
-// LDS.  Every expression follows the evaluation order documented in hx.h; a stage's max over
-// devices of X/(t*c_d) is taken as X/(t*min c_d), which is the same binary64 value because
-// rounding is monotone.
+//   decode_kernel   one lane per candidate: each group's member set as a GPU bitmask
+//                   (an output: the flow-network build reuses it), absent slots zeroed, and a
+//                   per-workgroup histogram of units per (role, size) added to the global one;
+//   scan_kernel     one workgroup: exclusive scan of the histogram into bucket offsets;
+//   scatter_kernel  one lane per candidate: units written bucket by bucket, each workgroup
+//                   reserving its ranges with one atomic per bucket;
+//   eval_kernel     one lane per unit: every admissible TP x PP strategy, prefill keeping its
+//                   latency-optimal and decode its throughput-optimal one (Sec. 3.3,
+//                   "Compute nodes").  The unit's bitmask is expanded into the lane's own LDS
+//                   column of member ids (ascending), from which stage j of (tp, pp) is the
+//                   slice [j*tp, (j+1)*tp).
+// Per-GPU parameters, and the alpha/beta tables when they fit, are staged in LDS.  The
+// arithmetic is FP64 scalar work, not a dense contraction, so there is no MFMA here.
+//
+// Every expression follows the evaluation order documented in hx.h; a stage's max over
+// devices of X/(t*c_d) is taken as X/(t*min c_d), the same binary64 value because rounding
+// is monotone (likewise the memory limit on the stage's smallest memory).
 #include "hx_internal.h"
 
 namespace hx {
 namespace {
 
-constexpr int kCostBlock = 128;
+constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40^2 doubles (25.6 KB)
+constexpr int kEvalBlock = 128;
+
+// ------------------------------------------------------------------ member bitmasks
+
+// Ascending-id iterator over the set bits of a W-word GPU bitmask held in registers.
+template <int W>
+struct Members {
+    uint64_t w[W];
+    __device__ __forceinline__ int next() {
+#pragma unroll
+        for (int i = 0; i < W; ++i)
+            if (w[i]) {
+                const int b = __builtin_ctzll(w[i]);
+                w[i] &= w[i] - 1;
+                return i * 64 + b;
+            }
+        return 0;
+    }
+};
+
+template <int W>
+__device__ __forceinline__ Members<W> load_members(const uint64_t* gmask, int k, int64_t N, int n) {
+    Members<W> m;
+#pragma unroll
+    for (int i = 0; i < W; ++i) m.w[i] = gmask[((int64_t)k * W + i) * N + n];
+    return m;
+}
+
+template <int W>
+__device__ __forceinline__ int popcount(const Members<W>& m) {
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) s += __popcll(m.w[i]);
+    return s;
+}
+
+// ------------------------------------------------------------------ one strategy
+
+struct Tables {
+    const double *gfl, *ghb, *gme, *alpha, *beta;
+};
 
 struct StrategyCost {
     double bmax, lat, x;
@@ -24,23 +76,25 @@ struct StrategyCost {
 
 // Costs strategy (tp, pp) of a group whose r-th member (ascending id) is mem[r * stride].
 // Returns false when the memory limit admits no batch of 1.
-__device__ bool cost_strategy(const Problem& p, const double* gfl, const double* ghb, const double* gme,
-                              const uint8_t* mem, int stride, int tp, int pp, int role, StrategyCost& out) {
+__device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
+                                              int tp, int pp, int role, StrategyCost& out) {
     const double t = (double)tp;
     const double H = p.H, B = p.B;
     const double W12 = 12.0 * H * H * B;
     const double Kkv = 2.0 * (p.s_in + p.s_out) * p.Hkv * B;
     const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
+    const int G = p.G;
+    const int lq = p.L / pp, lr = p.L % pp;
 
     // Memory-limit row: b_j = floor((M_j - A_j)/K_j) on the stage's smallest memory.
     double bmin = kBmaxClamp;
     for (int j = 0; j < pp; ++j) {
-        const double l = (double)stage_layers(p.L, pp, j);
+        const double l = (double)(lq + (j < lr ? 1 : 0));
         const double A = (W12 / t) * l;
         const double K = (Kkv / t) * l + Kact;
         const uint8_t* S = mem + (j * tp) * stride;
-        double Mmin = gme[S[0]];
-        for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, gme[S[r * stride]]);
+        double Mmin = tb.gme[S[0]];
+        for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, tb.gme[S[r * stride]]);
         const double q = (Mmin - A) / K;
         const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
         bmin = dmin(bmin, b);
@@ -55,14 +109,14 @@ __device__ bool cost_strategy(const Problem& p, const double* gfl, const double*
     const double Xcomp_d = 24.0 * b * p.s_out * H * H;
     const double X = prefill ? b * p.s_in * H * B : b * H * B;
 
-    double s1 = 0.0;
+    double s1 = 0.0, s2 = 0.0;
     for (int j = 0; j < pp; ++j) {
-        const double l = (double)stage_layers(p.L, pp, j);
+        const double l = (double)(lq + (j < lr ? 1 : 0));
         const uint8_t* S = mem + (j * tp) * stride;
-        double cmin = gfl[S[0]], hmin = ghb[S[0]];
+        double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
         for (int r = 1; r < tp; ++r) {
-            cmin = dmin(cmin, gfl[S[r * stride]]);
-            hmin = dmin(hmin, ghb[S[r * stride]]);
+            cmin = dmin(cmin, tb.gfl[S[r * stride]]);
+            hmin = dmin(hmin, tb.ghb[S[r * stride]]);
         }
         const double comp = prefill ? (Xcomp_p / (t * cmin)) * l
                                     : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
@@ -70,8 +124,8 @@ __device__ bool cost_strategy(const Problem& p, const double* gfl, const double*
         double mx = 0.0;
         for (int r = 0; r < tp; ++r) {
             const int d = S[r * stride];
-            const double* arow = p.alpha + d * p.G;
-            const double* brow = p.beta + d * p.G;
+            const double* arow = tb.alpha + d * G;
+            const double* brow = tb.beta + d * G;
             double sum = 0.0;
             for (int q = 0; q < tp; ++q) {
                 if (q == r) continue;
@@ -82,94 +136,266 @@ __device__ bool cost_strategy(const Problem& p, const double* gfl, const double*
         }
         const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
         s1 = s1 + (comp + tpc);
-    }
-    // PP row: the fastest link between consecutive stages.
-    double s2 = 0.0;
-    for (int j = 0; j + 1 < pp; ++j) {
-        const uint8_t* S = mem + (j * tp) * stride;
-        const uint8_t* S2 = mem + ((j + 1) * tp) * stride;
-        double mn = 0.0;
-        for (int r = 0; r < tp; ++r) {
-            const int d = S[r * stride];
-            for (int q = 0; q < tp; ++q) {
-                const int e = S2[q * stride];
-                const double v = p.alpha[d * p.G + e] + X / p.beta[d * p.G + e];
-                if ((r == 0 && q == 0) || v < mn) mn = v;
+        // PP row between stage j-1 and stage j: the fastest link.
+        if (j > 0) {
+            const uint8_t* Sp = S - tp * stride;
+            double mn = 0.0;
+            for (int r = 0; r < tp; ++r) {
+                const int d = Sp[r * stride];
+                const double* arow = tb.alpha + d * G;
+                const double* brow = tb.beta + d * G;
+                for (int q = 0; q < tp; ++q) {
+                    const int e = S[q * stride];
+                    const double v = arow[e] + X / brow[e];
+                    if ((r == 0 && q == 0) || v < mn) mn = v;
+                }
             }
+            s2 = s2 + (prefill ? mn : mn * p.s_out);
         }
-        s2 = s2 + (prefill ? mn : mn * p.s_out);
     }
     out.lat = s1 + s2;
     out.x = (1000.0 * b) / out.lat;
     return true;
 }
 
-__global__ void __launch_bounds__(kCostBlock) cost_kernel(Problem p, CostOut o) {
-    extern __shared__ double smem[];
-    double* gfl = smem;
-    double* ghb = gfl + p.G;
-    double* gme = ghb + p.G;
-    uint8_t* lists = reinterpret_cast<uint8_t*>(gme + p.G);  // [G][blockDim]
-    const int tid = threadIdx.x;
-    for (int g = tid; g < p.G; g += blockDim.x) {
+// ------------------------------------------------------------------ kernels
+
+struct CostWork {
+    int32_t* hist;    // [nb + 1]: per (role, size) unit counts, then offsets; [nb] = total
+    int32_t* cursor;  // [nb]
+    uint64_t* units;  // [n_cand * max units per candidate]: (n << 8) | k
+    uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
+};
+
+__global__ void fill_kernel(int32_t* a, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) a[i] = 0;
+}
+
+// One lane per candidate.  LDS: the lane's masks [Kmax*W][blockDim] and a local histogram.
+template <int W>
+__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int nb = 2 * (p.G + 1);
+    int32_t* lhist = reinterpret_cast<int32_t*>(smem);
+    uint64_t* ms = reinterpret_cast<uint64_t*>(smem + ((sizeof(int32_t) * nb + 15) & ~(size_t)15));
+    const int tid = threadIdx.x, bs = blockDim.x;
+    for (int b = tid; b < nb; b += bs) lhist[b] = 0;
+    const int n = blockIdx.x * bs + tid;
+    const int N = p.N, Kmax = p.Kmax;
+    if (n < N) {
+        for (int e = 0; e < Kmax * W; ++e) ms[e * bs + tid] = 0;
+        for (int g = 0; g < p.G; ++g) {
+            const int k = p.assign[(int64_t)g * N + n];
+            if (k < Kmax) ms[(k * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
+        }
+    }
+    __syncthreads();
+    if (n < N) {
+        for (int k = 0; k < Kmax; ++k) {
+            int size = 0;
+            for (int i = 0; i < W; ++i) {
+                const uint64_t m = ms[(k * W + i) * bs + tid];
+                wk.gmask[((int64_t)k * W + i) * N + n] = m;
+                size += __popcll(m);
+            }
+            const int role = p.role[(int64_t)k * N + n];
+            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
+                atomicAdd(&lhist[role * (p.G + 1) + size], 1);
+            } else {
+                const int64_t o_ = (int64_t)k * N + n;
+                o.tp[o_] = 0;
+                o.pp[o_] = 0;
+                o.bmax[o_] = 0;
+                o.cap[o_] = 0;
+                o.lat[o_] = 0.0;
+            }
+        }
+    }
+    __syncthreads();
+    for (int b = tid; b < nb; b += bs)
+        if (lhist[b]) atomicAdd(&wk.hist[b], lhist[b]);
+}
+
+// Exclusive scan of hist[0..nb) into hist (offsets) and cursor; hist[nb] = total.
+__global__ void __launch_bounds__(64) scan_kernel(CostWork wk, int nb) {
+    const int lane = threadIdx.x;
+    const int per = (nb + 63) / 64;
+    const int lo = lane * per, hi = lo + per < nb ? lo + per : nb;
+    int32_t s = 0;
+    for (int i = lo; i < hi; ++i) s += wk.hist[i];
+    int32_t incl = s;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+    }
+    int32_t run = incl - s;
+    for (int i = lo; i < hi; ++i) {
+        const int32_t v = wk.hist[i];
+        wk.hist[i] = run;
+        wk.cursor[i] = run;
+        run += v;
+    }
+    if (lane == 63) wk.hist[nb] = incl;
+}
+
+template <int W>
+__global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int nb = 2 * (p.G + 1);
+    int32_t* lcount = reinterpret_cast<int32_t*>(smem);
+    int32_t* lbase = lcount + nb;
+    const int tid = threadIdx.x, bs = blockDim.x;
+    for (int b = tid; b < nb; b += bs) lcount[b] = 0;
+    __syncthreads();
+    const int n = blockIdx.x * bs + tid;
+    const int N = p.N, Kmax = p.Kmax;
+    if (n < N)
+        for (int k = 0; k < Kmax; ++k) {
+            const int size = popcount(load_members<W>(wk.gmask, k, N, n));
+            const int role = p.role[(int64_t)k * N + n];
+            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) atomicAdd(&lcount[role * (p.G + 1) + size], 1);
+        }
+    __syncthreads();
+    for (int b = tid; b < nb; b += bs) {
+        lbase[b] = lcount[b] ? atomicAdd(&wk.cursor[b], lcount[b]) : 0;
+        lcount[b] = 0;
+    }
+    __syncthreads();
+    if (n < N)
+        for (int k = 0; k < Kmax; ++k) {
+            const int size = popcount(load_members<W>(wk.gmask, k, N, n));
+            const int role = p.role[(int64_t)k * N + n];
+            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
+                const int b = role * (p.G + 1) + size;
+                const int pos = lbase[b] + atomicAdd(&lcount[b], 1);
+                wk.units[pos] = ((uint64_t)n << 8) | (uint64_t)k;
+            }
+        }
+}
+
+template <int W, bool kTables>
+__global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
+    extern __shared__ __attribute__((aligned(16))) double dsm[];
+    const int G = p.G;
+    double* gfl = dsm;
+    double* ghb = gfl + G;
+    double* gme = ghb + G;
+    for (int g = threadIdx.x; g < G; g += kEvalBlock) {
         const int t = p.gpu_type[g];
         const bool ok = t >= 0 && t < p.T;  // an unknown type can hold nothing: infeasible
         gfl[g] = ok ? p.flops[t] : 0.0;
         ghb[g] = ok ? p.hbm[t] : 0.0;
         gme[g] = ok ? p.mem[t] : 0.0;
     }
+    Tables tb{gfl, ghb, gme, p.alpha, p.beta};
+    double* tb_end = gme + G;
+    if (kTables) {
+        double* a = gme + G;
+        double* b = a + G * G;
+        for (int e = threadIdx.x; e < G * G; e += kEvalBlock) {
+            a[e] = p.alpha[e];
+            b[e] = p.beta[e];
+        }
+        tb.alpha = a;
+        tb.beta = b;
+        tb_end = b + G * G;
+    }
     __syncthreads();
-
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
-    if (gid >= (int64_t)p.Kmax * p.N) return;
-    const int k = (int)(gid / p.N);
-    const int n = (int)(gid - (int64_t)k * p.N);
-    const int stride = blockDim.x;
-    uint8_t* mem = lists + tid;
-
-    int cnt = 0;
-    for (int g = 0; g < p.G; ++g)
-        if (p.assign[(int64_t)g * p.N + n] == k) mem[(cnt++) * stride] = (uint8_t)g;
-    const int role = p.role[gid];
-
-    int best_tp = 0, best_pp = 0;
-    int32_t best_b = 0, best_cap = 0;
-    double best_lat = 0.0, best_x = 0.0;
-    if (cnt > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
+    const int64_t total = wk.hist[nb];
+    const int64_t N = p.N;
+    uint8_t* mem = reinterpret_cast<uint8_t*>(tb_end) + threadIdx.x;  // [G][kEvalBlock] member list
+    for (int64_t u = (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total; u += (int64_t)gridDim.x * kEvalBlock) {
+        const uint64_t w = wk.units[u];
+        const int n = (int)(w >> 8), k = (int)(w & 0xFF);
+        int cnt = 0;
+#pragma unroll
+        for (int i = 0; i < W; ++i) {
+            uint64_t m = wk.gmask[((int64_t)k * W + i) * N + n];
+            while (m) {
+                mem[(cnt++) * kEvalBlock] = (uint8_t)(i * 64 + __builtin_ctzll(m));
+                m &= m - 1;
+            }
+        }
+        const int role = p.role[(int64_t)k * N + n];
         bool have = false;
+        int best_tp = 0, best_pp = 0;
+        double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
         for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
             if (!((p.tp_mask >> (tp - 1)) & 1u) || cnt % tp != 0) continue;
             const int pp = cnt / tp;
             if (pp > HX_MAX_PP || !((p.pp_mask >> (pp - 1)) & 1u) || pp > p.L) continue;
-            StrategyCost c;
-            if (!cost_strategy(p, gfl, ghb, gme, mem, stride, tp, pp, role, c)) continue;
-            const bool better = !have || (role == HX_PREFILL ? c.lat < best_lat : c.x > best_x);
+            StrategyCost sc;
+            if (!cost_strategy(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
             if (better) {
                 have = true;
                 best_tp = tp;
                 best_pp = pp;
-                best_b = (int32_t)c.bmax;
-                best_cap = quantize(c.x);
-                best_lat = c.lat;
-                best_x = c.x;
+                best_b = sc.bmax;
+                best_lat = sc.lat;
+                best_x = sc.x;
             }
         }
+        const int64_t o_ = (int64_t)k * N + n;
+        o.tp[o_] = (uint8_t)best_tp;
+        o.pp[o_] = (uint8_t)best_pp;
+        o.bmax[o_] = (int32_t)best_b;
+        o.cap[o_] = have ? quantize(best_x) : 0;
+        o.lat[o_] = best_lat;
     }
-    o.tp[gid] = (uint8_t)best_tp;
-    o.pp[gid] = (uint8_t)best_pp;
-    o.bmax[gid] = best_b;
-    o.cap[gid] = best_cap;
-    o.lat[gid] = best_lat;
+}
+
+// Units a candidate can contribute: one per group, at most min(Kmax, G).
+int64_t max_units(int G, int Kmax, int64_t N) { return (int64_t)(Kmax < G ? Kmax : G) * N; }
+
+template <int W>
+hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipStream_t s) {
+    const int nb = 2 * (p.G + 1);
+    hipLaunchKernelGGL(fill_kernel, dim3((2 * nb + 1 + 255) / 256), dim3(256), 0, s, wk.hist, 2 * nb + 1);
+    // decode: the widest block whose per-lane masks fit in 32 KB of LDS
+    int bs = 256;
+    while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
+    const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)p.Kmax * W * bs * 8;
+    hipLaunchKernelGGL(decode_kernel<W>, dim3((p.N + bs - 1) / bs), dim3(bs), lds_dec, s, p, o, wk);
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(64), 0, s, wk, nb);
+    hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 2 * sizeof(int32_t) * nb, s, p, wk);
+    const bool tables = p.G <= kTableMaxG;
+    const size_t lds_eval =
+        sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) + (size_t)p.G * kEvalBlock;
+    // A grid-stride loop over the units: enough workgroups to fill the chip several times.
+    const int64_t units = max_units(p.G, p.Kmax, p.N);
+    const int64_t want = (units + kEvalBlock - 1) / kEvalBlock;
+    const int blocks = (int)(want < 2048 ? want : 2048);
+    if (tables)
+        hipLaunchKernelGGL((eval_kernel<W, true>), dim3(blocks), dim3(kEvalBlock), lds_eval, s, p, o, wk, nb);
+    else
+        hipLaunchKernelGGL((eval_kernel<W, false>), dim3(blocks), dim3(kEvalBlock), lds_eval, s, p, o, wk, nb);
+    return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_cost(const Problem& p, const CostOut& o, hipStream_t s) {
-    const int64_t lanes = (int64_t)p.Kmax * p.N;
-    const int blocks = (int)((lanes + kCostBlock - 1) / kCostBlock);
-    const size_t lds = 3 * sizeof(double) * p.G + (size_t)p.G * kCostBlock;
-    hipLaunchKernelGGL(cost_kernel, dim3(blocks), dim3(kCostBlock), lds, s, p, o);
-    return hipGetLastError();
+size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    const size_t nb = 2 * ((size_t)n_gpus + 1);
+    const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
+    return head + sizeof(uint64_t) * (size_t)max_units(n_gpus, max_groups, n_cand);
+}
+
+int mask_words(int32_t n_gpus) { return n_gpus <= 64 ? 1 : (n_gpus <= 128 ? 2 : 4); }
+
+hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
+    const size_t nb = 2 * ((size_t)p.G + 1);
+    const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
+    CostWork wk;
+    wk.hist = reinterpret_cast<int32_t*>(workspace);
+    wk.cursor = wk.hist + nb + 1;
+    wk.units = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(workspace) + head);
+    wk.gmask = o.members;
+    switch (mask_words(p.G)) {
+        case 1: return launch_w<1>(p, o, wk, s);
+        case 2: return launch_w<2>(p, o, wk, s);
+        default: return launch_w<4>(p, o, wk, s);
+    }
 }
 
 }  // namespace hx

@@ -1,42 +1,51 @@
 // hx_flownet.hip -- the Sec. 3.3 flow network of every candidate, on gfx950.
 //
-// Two kernels, both candidate-fastest so that loads and stores of the [row][n] arrays are
-// coalesced across the wavefront:
+// Both kernels read the group member bitmasks hx_cost_eval wrote, so no kernel here scans
+// the assign array for a group's members.  Both run candidate-fastest, so loads and stores
+// of the [row][n] arrays coalesce across the wavefront:
 //   nodes_kernel  one lane per candidate: lists the prefill and decode nodes (replicas in
 //                 ascending group id, or GPUs in ascending id at per-GPU granularity) with
 //                 their source, node and sink capacities (Appendix A);
-//   kv_kernel     one lane per (prefill node i, candidate): the KV edges from node i to every
-//                 decode node (connection type 3; Table 1 last row; Appendix A).
-// Per-lane scratch (group sizes, member lists) lives in LDS columns, one per lane.
+//   kv_kernel     one lane per (KV edge, candidate): the edge capacity between prefill node
+//                 i and decode node j (connection type 3; Table 1 last row; Appendix A).
 #include "hx_internal.h"
 
 namespace hx {
 namespace {
 
-constexpr int kNodeBlock = 64;
+constexpr int kNodeBlock = 128;
 constexpr int kKvBlock = 64;
 
+template <int W>
+__device__ __forceinline__ int mask_size(const uint64_t* gm, int k, int64_t N, int n) {
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) s += __popcll(gm[((int64_t)k * W + i) * N + n]);
+    return s;
+}
+
+// Members of group k below GPU g (its rank inside the group).
+template <int W>
+__device__ __forceinline__ int mask_rank(const uint64_t* gm, int k, int64_t N, int n, int g) {
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        const uint64_t m = gm[((int64_t)k * W + i) * N + n];
+        if (i < (g >> 6)) s += __popcll(m);
+        else if (i == (g >> 6)) s += __popcll(m & ((1ull << (g & 63)) - 1));
+    }
+    return s;
+}
+
+template <int W>
 __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o, FlowNet f) {
-    extern __shared__ uint8_t sm[];
-    const int tid = threadIdx.x;
-    const int stride = blockDim.x;
-    const int n = blockIdx.x * blockDim.x + tid;
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= p.N) return;
-    uint8_t* size = sm + tid;                       // [Kmax][blockDim] members per group
-    uint8_t* rank = sm + p.Kmax * stride + tid;     // [Kmax][blockDim] members seen so far
-    for (int k = 0; k < p.Kmax; ++k) {
-        size[k * stride] = 0;
-        rank[k * stride] = 0;
-    }
-    for (int g = 0; g < p.G; ++g) {
-        const int k = p.assign[(int64_t)g * p.N + n];
-        if (k < p.Kmax) size[k * stride] += 1;
-    }
-    const int N = p.N;
+    const int64_t N = p.N;
     int np = 0, nd = 0;
     if (p.granularity == 0) {
         for (int k = 0; k < p.Kmax; ++k) {
-            if (size[k * stride] == 0) continue;
+            if (mask_size<W>(o.members, k, N, n) == 0) continue;
             const int r = p.role[(int64_t)k * N + n];
             const int32_t c = o.cap[(int64_t)k * N + n];
             if (r == HX_PREFILL) {
@@ -61,9 +70,8 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
             if (k >= p.Kmax) continue;
             const int r = p.role[(int64_t)k * N + n];
             if (r != HX_PREFILL && r != HX_DECODE) continue;
-            const int rk = rank[k * stride];
-            rank[k * stride] = (uint8_t)(rk + 1);
-            const int sz = size[k * stride];
+            const int rk = mask_rank<W>(o.members, k, N, n, g);
+            const int sz = mask_size<W>(o.members, k, N, n);
             const int32_t C = o.cap[(int64_t)k * N + n];
             const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
             if (r == HX_PREFILL) {
@@ -85,11 +93,18 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
     f.n_d[n] = nd;
 }
 
-// Members of group k of candidate n in ascending GPU id, into out[r * stride]; returns the count.
-__device__ int group_members(const Problem& p, int n, int k, uint8_t* out, int stride) {
+// Members of group k in ascending GPU id into out[r * stride]; returns the count.
+template <int W>
+__device__ __forceinline__ int expand(const uint64_t* gm, int k, int64_t N, int n, uint8_t* out, int stride) {
     int cnt = 0;
-    for (int g = 0; g < p.G; ++g)
-        if (p.assign[(int64_t)g * p.N + n] == k) out[(cnt++) * stride] = (uint8_t)g;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        uint64_t m = gm[((int64_t)k * W + i) * N + n];
+        while (m) {
+            out[(cnt++) * stride] = (uint8_t)(i * 64 + __builtin_ctzll(m));
+            m &= m - 1;
+        }
+    }
     return cnt;
 }
 
@@ -132,72 +147,65 @@ __device__ double kv_time(const Problem& p, const uint8_t* pm, int ptp, int ppp,
     return worst;
 }
 
+template <int W>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ uint8_t sm[];
     const int tid = threadIdx.x;
     const int stride = blockDim.x;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
-    const int N = p.N;
-    if (gid >= (int64_t)f.max_p * N) return;
-    const int i = (int)(gid / N);
-    const int n = (int)(gid - (int64_t)i * N);
-    const int np = f.n_p[n];
-    if (i >= np) return;
-    const int nd = f.n_d[n];
-    int32_t* kv = f.kv_cap + (int64_t)(i * nd) * N + n;
-
+    const int64_t N = p.N;
+    if (gid >= (int64_t)f.max_pd * N) return;
+    const int e = (int)(gid / N);
+    const int n = (int)(gid - (int64_t)e * N);
+    const int np = f.n_p[n], nd = f.n_d[n];
+    if (e >= np * nd) return;
+    const int i = e / nd, j = e - i * nd;
+    int32_t c = 0;
     if (p.granularity == 0) {
-        uint8_t* pm = sm + tid;                   // [G][blockDim]
-        uint8_t* dm = sm + p.G * stride + tid;    // [G][blockDim]
-        // A strategy whose tp*pp is not the group's size (cost outputs of another batch) is
-        // treated as infeasible rather than read past the member list.
-        const int kp = f.p_slot[(int64_t)i * N + n];
+        const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
         const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
-        const bool p_ok = ptp > 0 && group_members(p, n, kp, pm, stride) == ptp * ppp;
-        for (int j = 0; j < nd; ++j) {
-            const int kd = f.d_slot[(int64_t)j * N + n];
-            const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
-            int32_t c = 0;
-            if (p_ok && dtp > 0 && group_members(p, n, kd, dm, stride) == dtp * dpp)
+        const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
+        if (ptp > 0 && dtp > 0) {
+            uint8_t* pm = sm + tid;                   // [G][blockDim]
+            uint8_t* dm = sm + p.G * stride + tid;    // [G][blockDim]
+            // A strategy whose tp*pp is not the group's size (cost outputs of another batch)
+            // is treated as infeasible rather than read past the member list.
+            if (expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
+                expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp)
                 c = quantize(1000.0 / kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride));
-            kv[(int64_t)j * N] = c;
         }
     } else {
         // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
-        const int g = f.p_slot[(int64_t)i * N + n];
-        const int kp = p.assign[(int64_t)g * N + n];
-        int szp = 0;
-        for (int x = 0; x < p.G; ++x) szp += p.assign[(int64_t)x * N + n] == kp ? 1 : 0;
-        const bool feas_p = o.tp[(int64_t)kp * N + n] > 0;
-        const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
-        const double share = (V1 * (double)p.L) / (double)szp;
-        const double* arow = p.alpha + g * p.G;
-        const double* brow = p.beta + g * p.G;
-        for (int j = 0; j < nd; ++j) {
-            const int h = f.d_slot[(int64_t)j * N + n];
-            const int kd = p.assign[(int64_t)h * N + n];
-            int32_t c = 0;
-            if (feas_p && o.tp[(int64_t)kd * N + n] > 0) c = quantize(1000.0 / (arow[h] + share / brow[h]));
-            kv[(int64_t)j * N] = c;
+        const int g = f.p_slot[(int64_t)i * N + n], h = f.d_slot[(int64_t)j * N + n];
+        const int kp = p.assign[(int64_t)g * N + n], kd = p.assign[(int64_t)h * N + n];
+        if (o.tp[(int64_t)kp * N + n] > 0 && o.tp[(int64_t)kd * N + n] > 0) {
+            const int szp = mask_size<W>(o.members, kp, N, n);
+            const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
+            const double share = (V1 * (double)p.L) / (double)szp;
+            c = quantize(1000.0 / (p.alpha[g * p.G + h] + share / p.beta[g * p.G + h]));
         }
     }
+    f.kv_cap[(int64_t)e * N + n] = c;
+}
+
+template <int W>
+hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
+    hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
+    const int64_t lanes = (int64_t)f.max_pd * p.N;
+    const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
+    const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
+    hipLaunchKernelGGL(kv_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
-    {
-        const int blocks = (p.N + kNodeBlock - 1) / kNodeBlock;
-        const size_t lds = 2 * (size_t)p.Kmax * kNodeBlock;
-        hipLaunchKernelGGL(nodes_kernel, dim3(blocks), dim3(kNodeBlock), lds, s, p, o, f);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+    switch (mask_words(p.G)) {
+        case 1: return launch_w<1>(p, o, f, s);
+        case 2: return launch_w<2>(p, o, f, s);
+        default: return launch_w<4>(p, o, f, s);
     }
-    const int64_t lanes = (int64_t)f.max_p * p.N;
-    const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
-    const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
-    hipLaunchKernelGGL(kv_kernel, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
-    return hipGetLastError();
 }
 
 }  // namespace hx

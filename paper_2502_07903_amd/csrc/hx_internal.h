@@ -26,6 +26,7 @@ struct CostOut {
     uint8_t *tp, *pp;
     int32_t *bmax, *cap;
     double* lat;
+    uint64_t* members;  // [Kmax][W][N] group member bitmasks
 };
 
 struct FlowNet {
@@ -46,7 +47,10 @@ __device__ __forceinline__ double dmax(double a, double b) { return b > a ? b : 
 // Layers held by stage j of pp: floor(L/pp) + [j < L mod pp].
 __device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
 
-hipError_t launch_cost(const Problem& p, const CostOut& o, hipStream_t s);
+// 64-bit words of a GPU bitmask: 1 up to 64 GPUs, 2 up to 128, 4 up to 255.
+int mask_words(int32_t n_gpus);
+size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
+hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s);
 hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s);
 // LDS bytes the max-flow kernel needs for a network plan; 0 if it does not fit.
 size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);

@@ -1,7 +1,10 @@
 // hx_maxflow.hip -- maximum flow of every candidate's network (Sec. 3.3) on gfx950.
 //
-// The paper solves each network with preflow-push.  Here one workgroup owns one candidate
-// and runs a synchronous push-relabel with its whole residual graph in LDS.
+// The paper solves each network with preflow-push.  Here a segment of SEG lanes owns one
+// candidate and runs a synchronous push-relabel with the candidate's whole residual graph
+// in LDS, one lane per node.  Small networks (SEG <= 64, e.g. <= 16 replicas per side) pack
+// 64/SEG candidates into one wavefront, so a wave's rounds serve several candidates at
+// once; larger networks (per-GPU nodes) take a workgroup of SEG = 128 or 256 lanes each.
 //
 // Network.  In the Sec. 3.3 network every replica is an in -> out chain with one edge in
 // and the KV edges out (prefill) or the KV edges in and one edge out (decode), so the
@@ -21,12 +24,10 @@
 // the usual termination and optimality arguments apply.  Excess arriving at the other side
 // is added with LDS atomics.  Exact heights (BFS distances to the sink, else V + distance to
 // the source) are recomputed every few rounds by label-correcting sweeps (global relabel).
-// The run ends when no node has excess: the preflow is then a maximum flow.
+// A candidate is done when none of its nodes has excess: the preflow is then a maximum flow.
 //
 // Outputs: the flow value, the flow on every KV edge, and the canonical minimum cut (nodes of
 // the uncontracted network reachable from the source in the residual graph).
-#include <stdlib.h>
-
 #include "hx_internal.h"
 
 namespace hx {
@@ -48,6 +49,10 @@ struct MfLayout {
     int32_t* misc;  // [4] scalars
 };
 
+__host__ __device__ inline size_t mf_words(int max_p, int max_d, int max_pd) {
+    return 2 * ((size_t)max_pd + max_p) + 4 * (size_t)max_p + 4 * (size_t)max_d + 4;
+}
+
 __device__ inline MfLayout carve(int32_t* sm, int max_p, int max_d, int max_pd) {
     MfLayout L;
     const int arc = max_pd + max_p;  // P*(D|1) <= P*D + P
@@ -66,15 +71,16 @@ __device__ inline MfLayout carve(int32_t* sm, int max_p, int max_d, int max_pd) 
 }
 
 // Exact heights by label-correcting sweeps: hd = 1 where d -> t has residual, hp = V + 1 where
-// p -> s has residual (reverse of a used source edge), then relax along residual arcs.
-__device__ void global_relabel(const MfLayout& L, int P, int D, int Ds, int V, int INF) {
-    const int tid = threadIdx.x, T = blockDim.x;
-    for (int i = tid; i < P; i += T) L.hp[i] = L.fs[i] > 0 ? V + 1 : INF;
-    for (int j = tid; j < D; j += T) L.hd[j] = L.b[j] - L.ft[j] > 0 ? 1 : INF;
+// p -> s has residual (reverse of a used source edge), then relax along residual arcs.  Every
+// lane of the workgroup calls it (barriers inside); lane l of a segment owns node l, l+SEG, ...
+template <int SEG>
+__device__ void global_relabel(const MfLayout& L, int l, int P, int D, int Ds, int V, int INF) {
+    for (int i = l; i < P; i += SEG) L.hp[i] = L.fs[i] > 0 ? V + 1 : INF;
+    for (int j = l; j < D; j += SEG) L.hd[j] = L.b[j] - L.ft[j] > 0 ? 1 : INF;
     __syncthreads();
     for (;;) {
         bool changed = false;
-        for (int i = tid; i < P; i += T) {
+        for (int i = l; i < P; i += SEG) {
             int h = L.hp[i];
             const int32_t* c = L.cap + i * Ds;
             const int32_t* f = L.fl + i * Ds;
@@ -86,7 +92,7 @@ __device__ void global_relabel(const MfLayout& L, int P, int D, int Ds, int V, i
             }
         }
         __syncthreads();
-        for (int j = tid; j < D; j += T) {
+        for (int j = l; j < D; j += SEG) {
             int h = L.hd[j];
             for (int q = 0; q < P; ++q)
                 if (L.fl[q * Ds + j] > 0 && L.hp[q] + 1 < h) h = L.hp[q] + 1;
@@ -99,144 +105,152 @@ __device__ void global_relabel(const MfLayout& L, int P, int D, int Ds, int V, i
     }
 }
 
-__global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
-                                                      int32_t round_budget) {
-    // XCD-aware order: the hardware deals consecutive workgroups to the 8 XCDs in turn, so
-    // workgroup w takes candidate (w mod 8) * chunk + w / 8 and each XCD walks a contiguous
-    // candidate range, sharing the L2 lines of the candidate-fastest input arrays.
-    const int chunk = (f.N + 7) / 8;
-    const int n = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
-    if (n >= f.N) return;
-    extern __shared__ int32_t smem[];
-    const MfLayout L = carve(smem, f.max_p, f.max_d, f.max_pd);
-    const int tid = threadIdx.x, T = blockDim.x;
+// SEG lanes per candidate; the workgroup holds max(64, SEG) lanes, i.e. 64/SEG candidates
+// when SEG <= 64.  Workgroups are ordered XCD-aware: the hardware deals consecutive
+// workgroups to the 8 XCDs in turn, so workgroup w takes tile (w mod 8) * chunk + w / 8 and
+// each XCD walks a contiguous candidate range, sharing the L2 lines of the candidate-fastest
+// input arrays.
+template <int SEG>
+__global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
+    maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget) {
+    constexpr int kLanes = SEG < 64 ? 64 : SEG;
+    constexpr int kPer = kLanes / SEG;
     const int N = f.N;
-    const int P = f.n_p[n], D = f.n_d[n];
-    // A network larger than the plan it was built for is rejected before any LDS or array
-    // index is formed from it.
-    if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || P * D > f.max_pd) {
-        if (threadIdx.x == 0) flow_value[n] = HX_EINVAL;
-        return;
+    const int tiles = (N + kPer - 1) / kPer;
+    const int chunk = (tiles + 7) / 8;
+    const int tile = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
+    const int seg = threadIdx.x / SEG, l = threadIdx.x % SEG;
+    const int n = tile * kPer + seg;
+
+    extern __shared__ int32_t smem[];
+    const MfLayout L = carve(smem + seg * mf_words(f.max_p, f.max_d, f.max_pd), f.max_p, f.max_d, f.max_pd);
+    int P = 0, D = 0;
+    bool valid = tile < tiles && n < N;
+    if (valid) {
+        P = f.n_p[n];
+        D = f.n_d[n];
+        // A network larger than the plan it was built for is rejected before any LDS or array
+        // index is formed from it.
+        if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || P * D > f.max_pd) {
+            if (l == 0) flow_value[n] = HX_EINVAL;
+            valid = false;
+        }
     }
+    if (!valid) P = D = 0;
     const int Ds = D | 1;
 
-    for (int e = tid; e < P * D; e += T) {
+    for (int e = l; e < P * D; e += SEG) {
         const int i = e / D, d = e - i * D;
         L.cap[i * Ds + d] = f.kv_cap[(int64_t)e * N + n];
         L.fl[i * Ds + d] = 0;
     }
-    for (int i = tid; i < P; i += T) {
+    const bool has_flow = P > 0 && D > 0;
+    for (int i = l; i < P; i += SEG) {
         const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
-        const int32_t a = s < c ? s : c;
+        const int32_t a = has_flow ? (s < c ? s : c) : 0;  // no decode node: nothing can flow
         L.a[i] = a;
         L.fs[i] = a;  // saturate every source edge
         L.ep[i] = a;
     }
-    for (int j = tid; j < D; j += T) {
+    for (int j = l; j < D; j += SEG) {
         const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
         L.b[j] = c < t ? c : t;
         L.ft[j] = 0;
         L.ed[j] = 0;
     }
-    if (tid == 0) L.misc[0] = 0;
+    if (l == 0) {
+        L.misc[0] = 0;
+        L.misc[1] = 0;
+    }
     __syncthreads();
 
     const int V = P + D + 2;
     const int INF = 2 * V + 2;
-    bool converged = false;
-    if (P > 0 && D > 0) {
-        for (int round = 0; round < round_budget; ++round) {
-            if (round % kGlobalRelabelEvery == 0) {
-                global_relabel(L, P, D, Ds, V, INF);
-                __syncthreads();
-            }
-            // P-phase
-            for (int i = tid; i < P; i += T) {
-                int e = L.ep[i];
-                if (e <= 0) continue;
-                const int h = L.hp[i];
-                const int32_t* c = L.cap + i * Ds;
-                int32_t* fr = L.fl + i * Ds;
-                for (int d = 0; d < D && e > 0; ++d) {
-                    const int r = c[d] - fr[d];
-                    if (r > 0 && h == L.hd[d] + 1) {
-                        const int amt = r < e ? r : e;
-                        fr[d] += amt;
-                        e -= amt;
-                        atomicAdd(&L.ed[d], amt);
-                    }
+    bool active = false;
+    for (int i = l; i < P; i += SEG) active |= L.ep[i] > 0;
+    for (int round = 0; __syncthreads_or(active) && round < round_budget; ++round) {
+        if (round % kGlobalRelabelEvery == 0) {
+            global_relabel<SEG>(L, l, P, D, Ds, V, INF);
+            __syncthreads();
+        }
+        // P-phase
+        for (int i = l; i < P; i += SEG) {
+            int e = L.ep[i];
+            if (e <= 0) continue;
+            const int h = L.hp[i];
+            const int32_t* c = L.cap + i * Ds;
+            int32_t* fr = L.fl + i * Ds;
+            for (int d = 0; d < D && e > 0; ++d) {
+                const int r = c[d] - fr[d];
+                if (r > 0 && h == L.hd[d] + 1) {
+                    const int amt = r < e ? r : e;
+                    fr[d] += amt;
+                    e -= amt;
+                    atomicAdd(&L.ed[d], amt);
                 }
-                if (e > 0 && h == V + 1) {
-                    const int amt = L.fs[i] < e ? L.fs[i] : e;
-                    L.fs[i] -= amt;
+            }
+            if (e > 0 && h == V + 1) {
+                const int amt = L.fs[i] < e ? L.fs[i] : e;
+                L.fs[i] -= amt;
+                e -= amt;
+            }
+            if (e > 0) {
+                int mh = INF;
+                for (int d = 0; d < D; ++d)
+                    if (c[d] - fr[d] > 0 && L.hd[d] < mh) mh = L.hd[d];
+                if (L.fs[i] > 0 && V < mh) mh = V;
+                L.hp[i] = mh + 1 < INF ? mh + 1 : INF;
+            }
+            L.ep[i] = e;
+        }
+        __syncthreads();
+        // D-phase
+        for (int j = l; j < D; j += SEG) {
+            int e = L.ed[j];
+            if (e <= 0) continue;
+            const int h = L.hd[j];
+            if (h == 1) {
+                const int r = L.b[j] - L.ft[j];
+                const int amt = r < e ? r : e;
+                if (amt > 0) {
+                    L.ft[j] += amt;
                     e -= amt;
                 }
-                if (e > 0) {
-                    int mh = INF;
-                    for (int d = 0; d < D; ++d)
-                        if (c[d] - fr[d] > 0 && L.hd[d] < mh) mh = L.hd[d];
-                    if (L.fs[i] > 0 && V < mh) mh = V;
-                    L.hp[i] = mh + 1 < INF ? mh + 1 : INF;
-                }
-                L.ep[i] = e;
             }
-            __syncthreads();
-            // D-phase
-            for (int j = tid; j < D; j += T) {
-                int e = L.ed[j];
-                if (e <= 0) continue;
-                const int h = L.hd[j];
-                if (h == 1) {
-                    const int r = L.b[j] - L.ft[j];
-                    const int amt = r < e ? r : e;
-                    if (amt > 0) {
-                        L.ft[j] += amt;
-                        e -= amt;
-                    }
+            for (int q = 0; q < P && e > 0; ++q) {
+                const int fq = L.fl[q * Ds + j];
+                if (fq > 0 && h == L.hp[q] + 1) {
+                    const int amt = fq < e ? fq : e;
+                    L.fl[q * Ds + j] = fq - amt;
+                    e -= amt;
+                    atomicAdd(&L.ep[q], amt);
                 }
-                for (int q = 0; q < P && e > 0; ++q) {
-                    const int fq = L.fl[q * Ds + j];
-                    if (fq > 0 && h == L.hp[q] + 1) {
-                        const int amt = fq < e ? fq : e;
-                        L.fl[q * Ds + j] = fq - amt;
-                        e -= amt;
-                        atomicAdd(&L.ep[q], amt);
-                    }
-                }
-                if (e > 0) {
-                    int mh = L.b[j] - L.ft[j] > 0 ? 0 : INF;
-                    for (int q = 0; q < P; ++q)
-                        if (L.fl[q * Ds + j] > 0 && L.hp[q] < mh) mh = L.hp[q];
-                    L.hd[j] = mh + 1 < INF ? mh + 1 : INF;
-                }
-                L.ed[j] = e;
             }
-            __syncthreads();
-            bool active = false;
-            for (int i = tid; i < P; i += T) active |= L.ep[i] > 0;
-            for (int j = tid; j < D; j += T) active |= L.ed[j] > 0;
-            if (!__syncthreads_or(active)) {
-                converged = true;
-                break;
+            if (e > 0) {
+                int mh = L.b[j] - L.ft[j] > 0 ? 0 : INF;
+                for (int q = 0; q < P; ++q)
+                    if (L.fl[q * Ds + j] > 0 && L.hp[q] < mh) mh = L.hp[q];
+                L.hd[j] = mh + 1 < INF ? mh + 1 : INF;
             }
+            L.ed[j] = e;
         }
-    } else {
-        converged = true;  // no prefill or no decode node: the maximum flow is 0
-        for (int i = tid; i < P; i += T) L.fs[i] = 0;
         __syncthreads();
+        active = false;
+        for (int i = l; i < P; i += SEG) active |= L.ep[i] > 0;
+        for (int j = l; j < D; j += SEG) active |= L.ed[j] > 0;
     }
-
-    // Flow value = total flow into the sink.
-    for (int j = tid; j < D; j += T)
+    // Flow value = total flow into the sink; a candidate still holding excess ran out of rounds.
+    for (int j = l; j < D; j += SEG)
         if (L.ft[j] > 0) atomicAdd(&L.misc[0], L.ft[j]);
+    if (active) L.misc[1] = 1;
     __syncthreads();
-    if (tid == 0) flow_value[n] = converged ? L.misc[0] : HX_ENOCONV;
-    if (kv_flow)
-        for (int e = tid; e < P * D; e += T) {
+    if (valid && l == 0) flow_value[n] = L.misc[1] ? HX_ENOCONV : L.misc[0];
+    if (valid && kv_flow)
+        for (int e = l; e < P * D; e += SEG) {
             const int i = e / D, d = e - i * D;
             kv_flow[(int64_t)e * N + n] = L.fl[i * Ds + d];
         }
-    if (!cut) return;
+    if (!cut) return;  // uniform across the workgroup
 
     // Canonical minimum cut: reachability from s in the residual graph of the uncontracted
     // network, by sweeps until nothing changes.  Reuses a/ep (prefill in/out flags) and
@@ -246,11 +260,11 @@ __global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_v
     int32_t* din = L.ed;
     int32_t* dout = L.b;
     __syncthreads();
-    for (int i = tid; i < P; i += T) {
+    for (int i = l; i < P; i += SEG) {
         rin[i] = f.src_cap[(int64_t)i * N + n] - L.fs[i] > 0;
         rout[i] = 0;
     }
-    for (int j = tid; j < D; j += T) {
+    for (int j = l; j < D; j += SEG) {
         din[j] = 0;
         dout[j] = 0;
     }
@@ -259,7 +273,7 @@ __global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_v
         bool changed = false;
         // prefill replica: phi_out is reached from a reached delta_in over a used KV edge (its
         // reverse arc), and in <-> out inside the chain along whichever arcs have residual.
-        for (int i = tid; i < P; i += T) {
+        for (int i = l; i < P; i += SEG) {
             const int32_t fsi = L.fs[i];
             const int32_t pres = f.p_cap[(int64_t)i * N + n] - fsi;
             int in = rin[i], out = rout[i];
@@ -277,7 +291,7 @@ __global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_v
         __syncthreads();
         // decode replica: delta_in is reached from a reached phi_out over a KV edge with
         // residual capacity, then in <-> out inside the chain.
-        for (int j = tid; j < D; j += T) {
+        for (int j = l; j < D; j += SEG) {
             const int32_t ftj = L.ft[j];
             const int32_t dres = f.d_cap[(int64_t)j * N + n] - ftj;
             int in = din[j], out = dout[j];
@@ -294,28 +308,52 @@ __global__ void __launch_bounds__(256) maxflow_kernel(FlowNet f, int32_t* flow_v
         }
         if (!__syncthreads_or(changed)) break;
     }
-    for (int i = tid; i < P; i += T) cut[(int64_t)i * N + n] = (uint8_t)(rin[i] | (rout[i] << 1));
-    for (int j = tid; j < D; j += T) cut[(int64_t)(f.max_p + j) * N + n] = (uint8_t)(din[j] | (dout[j] << 1));
+    if (!valid) return;
+    for (int i = l; i < P; i += SEG) cut[(int64_t)i * N + n] = (uint8_t)(rin[i] | (rout[i] << 1));
+    for (int j = l; j < D; j += SEG) cut[(int64_t)(f.max_p + j) * N + n] = (uint8_t)(din[j] | (dout[j] << 1));
+}
+
+constexpr size_t kMaxLds = 64 * 1024;
+
+// Lanes per candidate: the smallest power of two >= the widest side (at least 8), so that
+// one lane owns one node; beyond 256 nodes per side a lane owns several.
+int segment_lanes(int max_p, int max_d) {
+    const int widest = max_p > max_d ? max_p : max_d;
+    int s = 8;
+    while (s < widest && s < 256) s *= 2;
+    return s;
+}
+
+template <int SEG>
+hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, int32_t budget, hipStream_t s) {
+    constexpr int kLanes = SEG < 64 ? 64 : SEG;
+    constexpr int kPer = kLanes / SEG;
+    const size_t lds = kPer * mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
+    const int tiles = (f.N + kPer - 1) / kPer;
+    const int blocks = 8 * ((tiles + 7) / 8);
+    hipLaunchKernelGGL(maxflow_kernel<SEG>, dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget);
+    return hipGetLastError();
 }
 
 }  // namespace
 
 size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd) {
-    const size_t words = 2 * ((size_t)max_pd + max_p) + 4 * (size_t)max_p + 4 * (size_t)max_d + 4;
-    const size_t bytes = words * sizeof(int32_t);
-    return bytes <= 64 * 1024 ? bytes : 0;
+    const int seg = segment_lanes(max_p, max_d);
+    const int per = seg < 64 ? 64 / seg : 1;
+    const size_t bytes = per * mf_words(max_p, max_d, max_pd) * sizeof(int32_t);
+    return bytes <= kMaxLds ? bytes : 0;
 }
 
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           hipStream_t s) {
-    const size_t lds = maxflow_lds_bytes(f.max_p, f.max_d, f.max_pd);
-    const int widest = f.max_p > f.max_d ? f.max_p : f.max_d;
-    int threads = ((widest + 63) / 64) * 64;
-    if (threads > 256) threads = 256;
-    const int chunk = (f.N + 7) / 8;
-    const int blocks = 8 * chunk;
-    hipLaunchKernelGGL(maxflow_kernel, dim3(blocks), dim3(threads), lds, s, f, flow_value, kv_flow, cut, round_budget);
-    return hipGetLastError();
+    switch (segment_lanes(f.max_p, f.max_d)) {
+        case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, s);
+        case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, s);
+        case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, s);
+        case 64: return launch_seg<64>(f, flow_value, kv_flow, cut, round_budget, s);
+        case 128: return launch_seg<128>(f, flow_value, kv_flow, cut, round_budget, s);
+        default: return launch_seg<256>(f, flow_value, kv_flow, cut, round_budget, s);
+    }
 }
 
 }  // namespace hx

@@ -57,7 +57,7 @@ class hx_candidates(C.Structure):
 
 class hx_cost_out(C.Structure):
     _fields_ = [("tp", C.c_void_p), ("pp", C.c_void_p), ("bmax", C.c_void_p), ("cap", C.c_void_p),
-                ("lat", C.c_void_p)]
+                ("lat", C.c_void_p), ("members", C.c_void_p)]
 
 
 class hx_flownet(C.Structure):
@@ -67,8 +67,8 @@ class hx_flownet(C.Structure):
                 ("sink_cap", C.c_void_p)]
 
 
-EXPORTS = ("hx_validate", "hx_cost_eval", "hx_build_flownet", "hx_maxflow_batch", "hx_best_candidate",
-           "hx_strerror", "hx_last_error", "hx_abi_version")
+EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
+           "hx_maxflow_batch", "hx_best_candidate", "hx_strerror", "hx_last_error", "hx_abi_version")
 
 _lib = None
 
@@ -84,7 +84,11 @@ def lib() -> C.CDLL:
         L.hx_validate.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
                                   P(hx_cost_out), P(hx_flownet)]
         L.hx_cost_eval.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
-                                   P(hx_cost_out), C.c_void_p]
+                                   P(hx_cost_out), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.hx_cost_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32]
+        L.hx_cost_workspace_bytes.restype = C.c_size_t
+        L.hx_member_words.argtypes = [C.c_int32]
+        L.hx_member_words.restype = C.c_int
         L.hx_build_flownet.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
                                        P(hx_cost_out), P(hx_flownet), C.c_void_p]
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
@@ -192,15 +196,24 @@ class CostBuffers:
     bmax: object
     cap: object
     lat: object
+    members: object     # int64 [Kmax * W, N]: the group member bitmasks (uint64 bit patterns)
+    workspace: object   # uint8 scratch of hx_cost_workspace_bytes
 
     @classmethod
-    def empty(cls, max_groups: int, n_cand: int, device: str = "cuda") -> "CostBuffers":
+    def empty(cls, max_groups: int, n_cand: int, n_gpus: int, device: str = "cuda") -> "CostBuffers":
         torch = _torch()
         z = lambda dt: torch.empty((max_groups, n_cand), dtype=dt, device=device)
-        return cls(z(torch.uint8), z(torch.uint8), z(torch.int32), z(torch.int32), z(torch.float64))
+        words = lib().hx_member_words(n_gpus)
+        wsb = int(lib().hx_cost_workspace_bytes(n_gpus, max_groups, n_cand))
+        if words <= 0 or wsb <= 0:
+            raise ValueError("invalid sizes for the cost-model buffers")
+        return cls(z(torch.uint8), z(torch.uint8), z(torch.int32), z(torch.int32), z(torch.float64),
+                   torch.empty((max_groups * words, n_cand), dtype=torch.int64, device=device),
+                   torch.empty(wsb, dtype=torch.uint8, device=device))
 
     def struct(self) -> hx_cost_out:
-        return hx_cost_out(_ptr(self.tp), _ptr(self.pp), _ptr(self.bmax), _ptr(self.cap), _ptr(self.lat))
+        return hx_cost_out(_ptr(self.tp), _ptr(self.pp), _ptr(self.bmax), _ptr(self.cap), _ptr(self.lat),
+                           _ptr(self.members))
 
 
 @dataclasses.dataclass
@@ -261,7 +274,8 @@ def validate(dp: DeviceProblem, cost: Optional[CostBuffers] = None, net: Optiona
 def cost_eval(dp: DeviceProblem, out: CostBuffers, stream=None) -> CostBuffers:
     o = out.struct()
     _check(lib().hx_cost_eval(C.byref(dp.cluster), dp.model, dp.workload, dp.space, C.byref(dp.cand), C.byref(o),
-                              _stream(stream)), "hx_cost_eval")
+                              _ptr(out.workspace), C.c_size_t(int(out.workspace.numel())), _stream(stream)),
+           "hx_cost_eval")
     return out
 
 
@@ -306,7 +320,7 @@ class Workspace:
         dims = flownet_dims(dp.max_groups, dp.n_gpus, dp.space.granularity)
         kv = torch.zeros((dims[2], N), dtype=torch.int32, device=device) if flows else None
         cut = torch.zeros((dims[0] + dims[1], N), dtype=torch.uint8, device=device) if flows else None
-        return cls(CostBuffers.empty(dp.max_groups, N, device), FlowNetBuffers.empty(dims, N, device),
+        return cls(CostBuffers.empty(dp.max_groups, N, dp.n_gpus, device), FlowNetBuffers.empty(dims, N, device),
                    torch.empty(N, dtype=torch.int32, device=device), kv, cut,
                    torch.empty(2, dtype=torch.int32, device=device))
 

@@ -43,7 +43,7 @@ def _args(G=32, T=4, N=100, Kmax=16, tp=0b1011, pp=0xFF, gran=0):
     wl = hx.hx_workload(1024.0, 256.0)
     sp = hx.hx_space(tp, pp, gran)
     cand = hx.hx_candidates(N, Kmax, FAKE, FAKE)
-    cost = hx.hx_cost_out(FAKE, FAKE, FAKE, FAKE, FAKE)
+    cost = hx.hx_cost_out(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
     b = Kmax if gran == 0 else G
     net = hx.hx_flownet(N, b, b, (b // 2) * ((b + 1) // 2), *([FAKE] * 9))
     return cl, md, wl, sp, cand, cost, net
@@ -78,6 +78,7 @@ def test_validate_accepts_workloads():
     lambda a: setattr(a[4], "max_groups", 256),
     lambda a: setattr(a[4], "role", None),
     lambda a: setattr(a[5], "lat", None),
+    lambda a: setattr(a[5], "members", None),
     lambda a: setattr(a[6], "max_pd", 63),           # 16 groups may split 8/8: 64 KV edges
     lambda a: setattr(a[6], "max_p", 15),
     lambda a: setattr(a[6], "n_cand", 99),
@@ -99,13 +100,31 @@ def test_calls_reject_before_any_device_work():
     cl, md, wl, sp, cand, cost, net = _args()
     cand.n_cand = 0
     L = hx.lib()
-    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None) == hx.HX_EINVAL
+    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), FAKE, 1 << 30, None) == hx.HX_EINVAL
+    cand.n_cand = 100
+    need = L.hx_cost_workspace_bytes(32, 16, 100)
+    assert need > 0
+    ws = 0x100000  # 256-byte aligned, never dereferenced: every call below fails validation
+    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), ws, need - 1, None) == hx.HX_EINVAL
+    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), ws + 8, need, None) == hx.HX_EINVAL
+    assert L.hx_cost_eval(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None, need, None) == hx.HX_EINVAL
+    cand.n_cand = 0
     assert L.hx_build_flownet(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), C.byref(net), None) == hx.HX_EINVAL
     assert L.hx_maxflow_batch(C.byref(net), None, None, None, None) == hx.HX_EINVAL
     assert L.hx_best_candidate(None, 10, FAKE, None) == hx.HX_EINVAL
     assert L.hx_best_candidate(FAKE, 0, FAKE, None) == hx.HX_EINVAL
     big = _args(G=255, T=6, N=10, Kmax=32, gran=1)[6]
     assert L.hx_maxflow_batch(C.byref(big), FAKE, None, None, None) == hx.HX_ETOOBIG
+
+
+def test_workspace_and_mask_sizes():
+    L = hx.lib()
+    assert [L.hx_member_words(g) for g in (1, 64, 65, 128, 129, 255)] == [1, 1, 2, 2, 4, 4]
+    assert L.hx_member_words(0) == 0 and L.hx_member_words(256) == 0
+    assert L.hx_cost_workspace_bytes(0, 16, 10) == 0
+    # one unit slot per candidate and group (at most min(Kmax, G) groups) plus the histogram
+    assert L.hx_cost_workspace_bytes(32, 16, 1000) >= 8 * 16 * 1000
+    assert L.hx_cost_workspace_bytes(8, 16, 1000) >= 8 * 8 * 1000
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

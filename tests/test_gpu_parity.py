@@ -37,7 +37,7 @@ def run_gpu(torch, prob, flows: bool = True):
     ws = hx.Workspace.for_problem(dp, flows=flows)
     hx.score(dp, ws)
     torch.cuda.synchronize()
-    out = dict(cost={k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")},
+    out = dict(cost={k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat", "members")},
                flownet=ws.net.host(), flow_value=ws.flow_value.cpu().numpy(),
                best=tuple(int(x) for x in ws.best.cpu().numpy()))
     if flows:
@@ -64,11 +64,25 @@ def compare_cost(got, want):
     assert np.array_equal(g, w), f"latencies not bit-identical ({int((g != w).sum())} differ)"
 
 
+def expected_members(prob) -> np.ndarray:
+    """Group member bitmasks straight from assign: [Kmax * W][N] uint64, bit g of word w = GPU 64w + g."""
+    G, N, K = prob.n_gpus, prob.n_cand, prob.max_groups
+    W = 1 if G <= 64 else (2 if G <= 128 else 4)
+    m = np.zeros((K * W, N), np.uint64)
+    cols = np.arange(N)
+    for g in range(G):
+        k = prob.assign[g].astype(np.int64)
+        ok = k < K
+        np.bitwise_or.at(m, (k[ok] * W + g // 64, cols[ok]), np.uint64(1) << np.uint64(g % 64))
+    return m
+
+
 def full_parity(torch, prob, label):
     say(f"{label}: N={prob.n_cand} G={prob.n_gpus} Kmax={prob.max_groups} gran={prob.granularity}")
     got = run_gpu(torch, prob)
     want = oracle_all(prob)
     compare_cost(got["cost"], want["cost"])
+    assert np.array_equal(got["cost"]["members"].view(np.uint64), expected_members(prob)), "member bitmasks differ"
     Hh.compare_flownet(got["flownet"], want["flownet"])
     assert np.array_equal(got["flow_value"], want["flow_value"]), \
         f"flow values differ at {np.flatnonzero(got['flow_value'] != want['flow_value'])[:8].tolist()}"
@@ -120,6 +134,7 @@ def test_refinement_round0_sample(torch):
     want = oracle_all(sub)
     for k in ("tp", "pp", "bmax", "cap", "lat"):
         assert np.array_equal(got["cost"][k][:, idx], want["cost"][k]), f"cost {k} differs"
+    assert np.array_equal(got["cost"]["members"].view(np.uint64)[:, idx], expected_members(sub))
     gfn = {k: (v[..., idx] if isinstance(v, np.ndarray) else v) for k, v in got["flownet"].items()}
     Hh.compare_flownet(gfn, want["flownet"])
     assert np.array_equal(got["flow_value"][idx], want["flow_value"])
