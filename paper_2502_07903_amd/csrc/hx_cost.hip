@@ -28,7 +28,7 @@ namespace hx {
 namespace {
 
 constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40^2 doubles (25.6 KB)
-constexpr int kEvalBlock = 128;
+
 
 // ------------------------------------------------------------------ member bitmasks
 
@@ -75,9 +75,14 @@ struct StrategyCost {
 };
 
 // Costs strategy (tp, pp) of a group whose r-th member (ascending id) is mem[r * stride].
-// Returns false when the memory limit admits no batch of 1.
+// Returns false when the memory limit admits no batch of 1.  TPC > 0 fixes tp at compile
+// time: a stage's member ids are then held in registers and each device's peer loop is
+// unrolled, so its loads and divisions overlap; TPC == 0 is the same arithmetic for any tp.
+template <int TPC>
 __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
-                                              int tp, int pp, int role, StrategyCost& out) {
+                                              int tp_rt, int pp, int role, StrategyCost& out) {
+    constexpr int kMax = TPC > 0 ? TPC : HX_MAX_TP;
+    const int tp = TPC > 0 ? TPC : tp_rt;
     const double t = (double)tp;
     const double H = p.H, B = p.B;
     const double W12 = 12.0 * H * H * B;
@@ -94,7 +99,9 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
         const double K = (Kkv / t) * l + Kact;
         const uint8_t* S = mem + (j * tp) * stride;
         double Mmin = tb.gme[S[0]];
-        for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, tb.gme[S[r * stride]]);
+#pragma unroll
+        for (int r = 1; r < kMax; ++r)
+            if (TPC > 0 || r < tp) Mmin = dmin(Mmin, tb.gme[S[r * stride]]);
         const double q = (Mmin - A) / K;
         const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
         bmin = dmin(bmin, b);
@@ -109,28 +116,37 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
     const double Xcomp_d = 24.0 * b * p.s_out * H * H;
     const double X = prefill ? b * p.s_in * H * B : b * H * B;
 
+    int S[kMax], Sp[kMax];
     double s1 = 0.0, s2 = 0.0;
     for (int j = 0; j < pp; ++j) {
         const double l = (double)(lq + (j < lr ? 1 : 0));
-        const uint8_t* S = mem + (j * tp) * stride;
+        const uint8_t* Sl = mem + (j * tp) * stride;
+#pragma unroll
+        for (int r = 0; r < kMax; ++r) S[r] = (TPC > 0 || r < tp) ? Sl[r * stride] : 0;
         double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
-        for (int r = 1; r < tp; ++r) {
-            cmin = dmin(cmin, tb.gfl[S[r * stride]]);
-            hmin = dmin(hmin, tb.ghb[S[r * stride]]);
-        }
+#pragma unroll
+        for (int r = 1; r < kMax; ++r)
+            if (TPC > 0 || r < tp) {
+                cmin = dmin(cmin, tb.gfl[S[r]]);
+                hmin = dmin(hmin, tb.ghb[S[r]]);
+            }
         const double comp = prefill ? (Xcomp_p / (t * cmin)) * l
                                     : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
         // TP row: the device with the largest sum over its peers (ascending peer order).
         double mx = 0.0;
+#pragma unroll 1
         for (int r = 0; r < tp; ++r) {
-            const int d = S[r * stride];
+            int d = S[0];
+#pragma unroll
+            for (int x = 1; x < kMax; ++x)
+                if (x == r) d = S[x];
             const double* arow = tb.alpha + d * G;
             const double* brow = tb.beta + d * G;
             double sum = 0.0;
-            for (int q = 0; q < tp; ++q) {
-                if (q == r) continue;
-                const int e = S[q * stride];
-                sum = sum + (arow[e] + X / (t * brow[e]));
+#pragma unroll
+            for (int q = 0; q < kMax; ++q) {
+                if ((TPC == 0 && q >= tp) || q == r) continue;
+                sum = sum + (arow[S[q]] + X / (t * brow[S[q]]));
             }
             if (r == 0 || sum > mx) mx = sum;
         }
@@ -138,24 +154,41 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
         s1 = s1 + (comp + tpc);
         // PP row between stage j-1 and stage j: the fastest link.
         if (j > 0) {
-            const uint8_t* Sp = S - tp * stride;
             double mn = 0.0;
+#pragma unroll 1
             for (int r = 0; r < tp; ++r) {
-                const int d = Sp[r * stride];
+                int d = Sp[0];
+#pragma unroll
+                for (int x = 1; x < kMax; ++x)
+                    if (x == r) d = Sp[x];
                 const double* arow = tb.alpha + d * G;
                 const double* brow = tb.beta + d * G;
-                for (int q = 0; q < tp; ++q) {
-                    const int e = S[q * stride];
-                    const double v = arow[e] + X / brow[e];
+#pragma unroll
+                for (int q = 0; q < kMax; ++q) {
+                    if (TPC == 0 && q >= tp) continue;
+                    const double v = arow[S[q]] + X / brow[S[q]];
                     if ((r == 0 && q == 0) || v < mn) mn = v;
                 }
             }
             s2 = s2 + (prefill ? mn : mn * p.s_out);
         }
+#pragma unroll
+        for (int r = 0; r < kMax; ++r) Sp[r] = S[r];
     }
     out.lat = s1 + s2;
     out.x = (1000.0 * b) / out.lat;
     return true;
+}
+
+__device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, const uint8_t* mem, int stride, int tp,
+                                         int pp, int role, StrategyCost& out) {
+    switch (tp) {
+        case 1: return cost_strategy<1>(p, tb, mem, stride, tp, pp, role, out);
+        case 2: return cost_strategy<2>(p, tb, mem, stride, tp, pp, role, out);
+        case 4: return cost_strategy<4>(p, tb, mem, stride, tp, pp, role, out);
+        case 8: return cost_strategy<8>(p, tb, mem, stride, tp, pp, role, out);
+        default: return cost_strategy<0>(p, tb, mem, stride, tp, pp, role, out);
+    }
 }
 
 // ------------------------------------------------------------------ kernels
@@ -200,7 +233,7 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
             }
             const int role = p.role[(int64_t)k * N + n];
             if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
-                atomicAdd(&lhist[role * (p.G + 1) + size], 1);
+                atomicAdd(&lhist[(p.G - size) * 2 + role], 1);
             } else {
                 const int64_t o_ = (int64_t)k * N + n;
                 o.tp[o_] = 0;
@@ -253,7 +286,7 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
         for (int k = 0; k < Kmax; ++k) {
             const int size = popcount(load_members<W>(wk.gmask, k, N, n));
             const int role = p.role[(int64_t)k * N + n];
-            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) atomicAdd(&lcount[role * (p.G + 1) + size], 1);
+            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) atomicAdd(&lcount[(p.G - size) * 2 + role], 1);
         }
     __syncthreads();
     for (int b = tid; b < nb; b += bs) {
@@ -266,14 +299,14 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
             const int size = popcount(load_members<W>(wk.gmask, k, N, n));
             const int role = p.role[(int64_t)k * N + n];
             if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
-                const int b = role * (p.G + 1) + size;
+                const int b = (p.G - size) * 2 + role;
                 const int pos = lbase[b] + atomicAdd(&lcount[b], 1);
                 wk.units[pos] = ((uint64_t)n << 8) | (uint64_t)k;
             }
         }
 }
 
-template <int W, bool kTables>
+template <int W, bool kTables, int kEvalBlock>
 __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
     const int G = p.G;
@@ -325,7 +358,7 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
             const int pp = cnt / tp;
             if (pp > HX_MAX_PP || !((p.pp_mask >> (pp - 1)) & 1u) || pp > p.L) continue;
             StrategyCost sc;
-            if (!cost_strategy(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            if (!cost_any(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
             const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
             if (better) {
                 have = true;
@@ -360,16 +393,23 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(64), 0, s, wk, nb);
     hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 2 * sizeof(int32_t) * nb, s, p, wk);
     const bool tables = p.G <= kTableMaxG;
-    const size_t lds_eval =
-        sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) + (size_t)p.G * kEvalBlock;
     // A grid-stride loop over the units: enough workgroups to fill the chip several times.
+    // 256 lanes per workgroup amortise the staged tables; the per-lane member columns take
+    // G bytes per lane, so beyond 128 GPUs the workgroup halves to stay within 64 KB of LDS.
     const int64_t units = max_units(p.G, p.Kmax, p.N);
-    const int64_t want = (units + kEvalBlock - 1) / kEvalBlock;
+    const int eb = p.G <= 128 ? 256 : 128;
+    const size_t lds_eval =
+        sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) + (size_t)p.G * eb;
+    const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
-    if (tables)
-        hipLaunchKernelGGL((eval_kernel<W, true>), dim3(blocks), dim3(kEvalBlock), lds_eval, s, p, o, wk, nb);
-    else
-        hipLaunchKernelGGL((eval_kernel<W, false>), dim3(blocks), dim3(kEvalBlock), lds_eval, s, p, o, wk, nb);
+    if (eb == 256) {
+        if (tables)
+            hipLaunchKernelGGL((eval_kernel<W, true, 256>), dim3(blocks), dim3(256), lds_eval, s, p, o, wk, nb);
+        else
+            hipLaunchKernelGGL((eval_kernel<W, false, 256>), dim3(blocks), dim3(256), lds_eval, s, p, o, wk, nb);
+    } else {
+        hipLaunchKernelGGL((eval_kernel<W, false, 128>), dim3(blocks), dim3(128), lds_eval, s, p, o, wk, nb);
+    }
     return hipGetLastError();
 }
 

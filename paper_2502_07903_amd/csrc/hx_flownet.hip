@@ -109,40 +109,45 @@ __device__ __forceinline__ int expand(const uint64_t* gm, int k, int64_t N, int 
 }
 
 // KV time of one request from a prefill replica (pm, ptp x ppp) to a decode replica
-// (dm, dtp x dpp): the slowest of the links that carry a layer range and head slice.
+// (dm, dtp x dpp): the slowest of the links that carry a layer range and head slice.  The
+// stage layer ranges of the two sides are two partitions of [0, L), and the rank head
+// slices (in units of 1/(ptp*dtp)) two partitions of [0, ptp*dtp), so merge walks visit
+// exactly the overlapping (stage, stage) and (rank, rank) pairs.
 __device__ double kv_time(const Problem& p, const uint8_t* pm, int ptp, int ppp, const uint8_t* dm, int dtp,
                           int dpp, int stride) {
     const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
     const double den = (double)(ptp * dtp);
+    const int lqp = p.L / ppp, lrp = p.L % ppp, lqd = p.L / dpp, lrd = p.L % dpp;
     double worst = 0.0;
-    int a0 = 0;
-    for (int a = 0; a < ppp; ++a) {
-        const int a1 = a0 + stage_layers(p.L, ppp, a);
-        int b0 = 0;
-        for (int bb = 0; bb < dpp; ++bb) {
-            const int b1 = b0 + stage_layers(p.L, dpp, bb);
-            const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
-            if (nab > 0) {
-                const double Vn = V1 * (double)nab;
-                for (int r = 0; r < ptp; ++r) {
-                    const int g = pm[(a * ptp + r) * stride];
-                    const double* arow = p.alpha + g * p.G;
-                    const double* brow = p.beta + g * p.G;
-                    for (int q = 0; q < dtp; ++q) {
-                        const int hi = (r + 1) * dtp < (q + 1) * ptp ? (r + 1) * dtp : (q + 1) * ptp;
-                        const int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
-                        const int ov = hi - lo;
-                        if (ov <= 0) continue;
-                        const int h = dm[(bb * dtp + q) * stride];
-                        const double bytes = (Vn * (double)ov) / den;
-                        const double time = arow[h] + bytes / brow[h];
-                        if (time > worst) worst = time;
-                    }
-                }
-            }
-            b0 = b1;
+    int a = 0, bb = 0, a0 = 0, b0 = 0;
+    int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
+    while (a < ppp && bb < dpp) {
+        const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+        const double Vn = V1 * (double)nab;
+        const uint8_t* Sa = pm + (a * ptp) * stride;
+        const uint8_t* Sb = dm + (bb * dtp) * stride;
+        int r = 0, q = 0;
+        while (r < ptp && q < dtp) {
+            const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+            const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+            const int g = Sa[r * stride], h = Sb[q * stride];
+            const double bytes = (Vn * (double)ov) / den;
+            const double time = p.alpha[g * p.G + h] + bytes / p.beta[g * p.G + h];
+            if (time > worst) worst = time;
+            if (re <= qe) ++r;
+            if (qe <= re) ++q;
         }
-        a0 = a1;
+        const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
+        if (adv_a) {
+            ++a;
+            a0 = a1;
+            a1 = a0 + lqp + (a < lrp ? 1 : 0);
+        }
+        if (adv_b) {
+            ++bb;
+            b0 = b1;
+            b1 = b0 + lqd + (bb < lrd ? 1 : 0);
+        }
     }
     return worst;
 }

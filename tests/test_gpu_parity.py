@@ -286,6 +286,12 @@ def test_best_candidate(torch, n):
     hx.best_candidate(t, best)
     torch.cuda.synchronize()
     assert tuple(best.cpu().tolist()) == hxo.best_candidate(v)
+    for off in (1, 2, 3):                      # inputs that do not start on a 16-byte boundary
+        if n - off < 1:
+            continue
+        hx.best_candidate(t[off:], best)
+        torch.cuda.synchronize()
+        assert tuple(best.cpu().tolist()) == hxo.best_candidate(v[off:])
 
 
 # ------------------------------------------------------------------ exhaustive search
