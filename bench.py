@@ -34,6 +34,13 @@ HBM_PEAK_GBS = 8000.0
 LDS_PEAK_GBS = 128 * 256 * 2.4          # 128 B/clk/CU -> 78,643 GB/s
 FP64_VALU_PEAK_TFLOPS = 78.6
 
+# HBM bytes per launch of the max-flow kernel at workload 3, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE passes (profiles/all_kernels_workload3.md), each scaled by what the counter reads
+# for a 256 MiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for the kernel
+# source they were taken on (first 16 hex digits of its SHA-256); otherwise traffic is null.
+MAXFLOW_TRAFFIC = {"source_sha256_16": "68896aad8bb1c1e6", "fetch_kib": 13355.0, "write_kib": 256.4,
+                   "fetch_scale": 2.0, "write_scale": 1.0}
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -70,6 +77,17 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
     maxflow = N * 8 + used_nodes * 4 * 2 + used_pd * 4 + N * 4
     best = N * 4 + 8
     return dict(cost=cost, flownet=flownet, maxflow=maxflow, best=best)
+
+
+def maxflow_traffic(workload: int):
+    """Counter-measured HBM bytes per max-flow launch, or None when they do not apply."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", "hx_maxflow.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    t = MAXFLOW_TRAFFIC
+    if workload != 3 or sha != t["source_sha256_16"]:
+        return None
+    return 1024.0 * (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"])
 
 
 def main():
@@ -139,8 +157,8 @@ def main():
         alg = float(lds_floor_bytes(n_p, n_d).sum())
         achieved = alg / (per_kernel["maxflow"] / 1000.0) / 1e9
         roof = {"kernel": "hx_maxflow_batch (maxflow_kernel)", "bound": "lds", "achieved": achieved,
-                "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS, "traffic": None,
-                "algorithmic_bytes_per_launch": alg}
+                "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
+                "traffic": maxflow_traffic(args.workload), "algorithmic_bytes_per_launch": alg}
     else:
         alg = float(hbm[dominant])
         achieved = alg / (per_kernel[dominant] / 1000.0) / 1e9
