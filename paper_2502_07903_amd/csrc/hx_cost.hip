@@ -2,20 +2,23 @@
 //
 // The cost of a group depends on its role and size (which strategies exist, how many
 // stages, how many TP peers); mixing sizes in one wavefront serialises every size's loop
-// nest.  So the batch is first sorted, globally, into work units bucketed by (role, size),
-// and the costing kernel then runs one unit per lane with a wavefront-uniform control path:
+// nest.  So the batch is first sorted, globally, into work units bucketed by (size, role),
+// largest groups first so that the longest lanes start at once, and the costing kernel then
+// runs one unit per lane with a wavefront-uniform control path:
 //
-//   decode_kernel   one lane per candidate: each group's member set as a GPU bitmask
-//                   (an output: the flow-network build reuses it), absent slots zeroed, and a
-//                   per-workgroup histogram of units per (role, size) added to the global one;
-//   scan_kernel     one workgroup: exclusive scan of the histogram into bucket offsets;
-//   scatter_kernel  one lane per candidate: units written bucket by bucket, each workgroup
-//                   reserving its ranges with one atomic per bucket;
+//   decode_kernel   one lane per candidate: each group's member set as a GPU bitmask (an
+//                   output: the flow-network build reuses it), absent slots zeroed, and a
+//                   per-workgroup histogram of units per bucket added to the global one;
+//   scan_kernel     one wavefront: exclusive scan of the histogram into bucket offsets;
+//   scatter_kernel  one lane per candidate: each present group's unit record
+//                   (candidate, slot, role, member mask) written into its bucket, a workgroup
+//                   reserving its range of each bucket with one atomic;
 //   eval_kernel     one lane per unit: every admissible TP x PP strategy, prefill keeping its
 //                   latency-optimal and decode its throughput-optimal one (Sec. 3.3,
-//                   "Compute nodes").  The unit's bitmask is expanded into the lane's own LDS
+//                   "Compute nodes").  The unit's mask is expanded into the lane's own LDS
 //                   column of member ids (ascending), from which stage j of (tp, pp) is the
-//                   slice [j*tp, (j+1)*tp).
+//                   slice [j*tp, (j+1)*tp); for tp in {1, 2, 4, 8} the stage's ids sit in
+//                   registers and each device's peer loop is unrolled.
 // Per-GPU parameters, and the alpha/beta tables when they fit, are staged in LDS.  The
 // arithmetic is FP64 scalar work, not a dense contraction, so there is no MFMA here.
 //
@@ -29,40 +32,6 @@ namespace {
 
 constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40^2 doubles (25.6 KB)
 
-
-// ------------------------------------------------------------------ member bitmasks
-
-// Ascending-id iterator over the set bits of a W-word GPU bitmask held in registers.
-template <int W>
-struct Members {
-    uint64_t w[W];
-    __device__ __forceinline__ int next() {
-#pragma unroll
-        for (int i = 0; i < W; ++i)
-            if (w[i]) {
-                const int b = __builtin_ctzll(w[i]);
-                w[i] &= w[i] - 1;
-                return i * 64 + b;
-            }
-        return 0;
-    }
-};
-
-template <int W>
-__device__ __forceinline__ Members<W> load_members(const uint64_t* gmask, int k, int64_t N, int n) {
-    Members<W> m;
-#pragma unroll
-    for (int i = 0; i < W; ++i) m.w[i] = gmask[((int64_t)k * W + i) * N + n];
-    return m;
-}
-
-template <int W>
-__device__ __forceinline__ int popcount(const Members<W>& m) {
-    int s = 0;
-#pragma unroll
-    for (int i = 0; i < W; ++i) s += __popcll(m.w[i]);
-    return s;
-}
 
 // ------------------------------------------------------------------ one strategy
 
@@ -194,9 +163,9 @@ __device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, con
 // ------------------------------------------------------------------ kernels
 
 struct CostWork {
-    int32_t* hist;    // [nb + 1]: per (role, size) unit counts, then offsets; [nb] = total
+    int32_t* hist;    // [nb + 1]: per (size, role) unit counts, then offsets; [nb] = total
     int32_t* cursor;  // [nb]
-    uint64_t* units;  // [n_cand * max units per candidate]: (n << 8) | k
+    uint64_t* units;  // [max units][1 + W]: (n << 16 | k << 8 | role), then the member mask words
     uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
 };
 
@@ -204,7 +173,15 @@ __global__ void fill_kernel(int32_t* a, int n) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) a[i] = 0;
 }
 
-// One lane per candidate.  LDS: the lane's masks [Kmax*W][blockDim] and a local histogram.
+// Bucket of a present group: largest sizes first, roles interleaved.
+__device__ __forceinline__ int bucket_of(int G, int size, int role) { return (G - size) * 2 + role; }
+
+// One lane per candidate (candidate-fastest, so every [row][n] access coalesces): the member
+// bitmask of each group slot, built in the lane's LDS column from its assign column; absent
+// slots' zero outputs; a per-workgroup histogram of units per bucket, added to the global one
+// with one atomic per bucket.  Slots go in chunks of kSlotChunk whose loads issue together.
+constexpr int kSlotChunk = 8;
+
 template <int W>
 __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -214,9 +191,11 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     const int tid = threadIdx.x, bs = blockDim.x;
     for (int b = tid; b < nb; b += bs) lhist[b] = 0;
     const int n = blockIdx.x * bs + tid;
-    const int N = p.N, Kmax = p.Kmax;
+    const int64_t N = p.N;
+    const int Kmax = p.Kmax;
     if (n < N) {
         for (int e = 0; e < Kmax * W; ++e) ms[e * bs + tid] = 0;
+#pragma unroll 8
         for (int g = 0; g < p.G; ++g) {
             const int k = p.assign[(int64_t)g * N + n];
             if (k < Kmax) ms[(k * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
@@ -224,23 +203,32 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     }
     __syncthreads();
     if (n < N) {
-        for (int k = 0; k < Kmax; ++k) {
-            int size = 0;
-            for (int i = 0; i < W; ++i) {
-                const uint64_t m = ms[(k * W + i) * bs + tid];
-                wk.gmask[((int64_t)k * W + i) * N + n] = m;
-                size += __popcll(m);
-            }
-            const int role = p.role[(int64_t)k * N + n];
-            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
-                atomicAdd(&lhist[(p.G - size) * 2 + role], 1);
-            } else {
-                const int64_t o_ = (int64_t)k * N + n;
-                o.tp[o_] = 0;
-                o.pp[o_] = 0;
-                o.bmax[o_] = 0;
-                o.cap[o_] = 0;
-                o.lat[o_] = 0.0;
+        for (int k0 = 0; k0 < Kmax; k0 += kSlotChunk) {
+            int rl[kSlotChunk];
+#pragma unroll
+            for (int x = 0; x < kSlotChunk; ++x)
+                rl[x] = k0 + x < Kmax ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
+#pragma unroll
+            for (int x = 0; x < kSlotChunk; ++x) {
+                const int k = k0 + x;
+                if (k >= Kmax) break;
+                int size = 0;
+#pragma unroll
+                for (int i = 0; i < W; ++i) {
+                    const uint64_t m = ms[(k * W + i) * bs + tid];
+                    wk.gmask[((int64_t)k * W + i) * N + n] = m;
+                    size += __popcll(m);
+                }
+                if (size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE)) {
+                    atomicAdd(&lhist[bucket_of(p.G, size, rl[x])], 1);
+                } else {
+                    const int64_t o_ = (int64_t)k * N + n;
+                    o.tp[o_] = 0;
+                    o.pp[o_] = 0;
+                    o.bmax[o_] = 0;
+                    o.cap[o_] = 0;
+                    o.lat[o_] = 0.0;
+                }
             }
         }
     }
@@ -271,39 +259,56 @@ __global__ void __launch_bounds__(64) scan_kernel(CostWork wk, int nb) {
     if (lane == 63) wk.hist[nb] = incl;
 }
 
+// One lane per candidate: every present group becomes a unit record (candidate, slot, role,
+// member mask) in its bucket.  Two passes over the slots: count per bucket, reserve the
+// workgroup's range of each bucket with one atomic, then write.
 template <int W>
 __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    __shared__ int32_t lcount[2 * (HX_MAX_GPUS + 1)];
+    __shared__ int32_t lbase[2 * (HX_MAX_GPUS + 1)];
     const int nb = 2 * (p.G + 1);
-    int32_t* lcount = reinterpret_cast<int32_t*>(smem);
-    int32_t* lbase = lcount + nb;
-    const int tid = threadIdx.x, bs = blockDim.x;
-    for (int b = tid; b < nb; b += bs) lcount[b] = 0;
+    for (int b = threadIdx.x; b < nb; b += blockDim.x) lcount[b] = 0;
     __syncthreads();
-    const int n = blockIdx.x * bs + tid;
-    const int N = p.N, Kmax = p.Kmax;
-    if (n < N)
-        for (int k = 0; k < Kmax; ++k) {
-            const int size = popcount(load_members<W>(wk.gmask, k, N, n));
-            const int role = p.role[(int64_t)k * N + n];
-            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) atomicAdd(&lcount[(p.G - size) * 2 + role], 1);
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t N = p.N;
+    const int Kmax = p.Kmax;
+    for (int pass = 0; pass < 2; ++pass) {
+        if (pass == 1) {
+            __syncthreads();
+            for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+                lbase[b] = lcount[b] ? atomicAdd(&wk.cursor[b], lcount[b]) : 0;
+                lcount[b] = 0;
+            }
+            __syncthreads();
         }
-    __syncthreads();
-    for (int b = tid; b < nb; b += bs) {
-        lbase[b] = lcount[b] ? atomicAdd(&wk.cursor[b], lcount[b]) : 0;
-        lcount[b] = 0;
-    }
-    __syncthreads();
-    if (n < N)
-        for (int k = 0; k < Kmax; ++k) {
-            const int size = popcount(load_members<W>(wk.gmask, k, N, n));
-            const int role = p.role[(int64_t)k * N + n];
-            if (size > 0 && (role == HX_PREFILL || role == HX_DECODE)) {
-                const int b = (p.G - size) * 2 + role;
-                const int pos = lbase[b] + atomicAdd(&lcount[b], 1);
-                wk.units[pos] = ((uint64_t)n << 8) | (uint64_t)k;
+        if (n >= N) continue;
+        for (int k0 = 0; k0 < Kmax; k0 += kSlotChunk) {
+            int rl[kSlotChunk];
+            uint64_t m[kSlotChunk][W];
+#pragma unroll
+            for (int x = 0; x < kSlotChunk; ++x) {
+                const bool in = k0 + x < Kmax;
+                rl[x] = in ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
+#pragma unroll
+                for (int i = 0; i < W; ++i) m[x][i] = in ? wk.gmask[((int64_t)(k0 + x) * W + i) * N + n] : 0;
+            }
+#pragma unroll
+            for (int x = 0; x < kSlotChunk; ++x) {
+                int size = 0;
+#pragma unroll
+                for (int i = 0; i < W; ++i) size += __popcll(m[x][i]);
+                if (size == 0 || (rl[x] != HX_PREFILL && rl[x] != HX_DECODE)) continue;
+                const int b = bucket_of(p.G, size, rl[x]);
+                const int rank = atomicAdd(&lcount[b], 1);
+                if (pass == 1) {
+                    uint64_t* rec = wk.units + (int64_t)(lbase[b] + rank) * (1 + W);
+                    rec[0] = ((uint64_t)n << 16) | ((uint64_t)(k0 + x) << 8) | (uint64_t)rl[x];
+#pragma unroll
+                    for (int i = 0; i < W; ++i) rec[1 + i] = m[x][i];
+                }
             }
         }
+    }
 }
 
 template <int W, bool kTables, int kEvalBlock>
@@ -338,18 +343,18 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
     const int64_t N = p.N;
     uint8_t* mem = reinterpret_cast<uint8_t*>(tb_end) + threadIdx.x;  // [G][kEvalBlock] member list
     for (int64_t u = (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total; u += (int64_t)gridDim.x * kEvalBlock) {
-        const uint64_t w = wk.units[u];
-        const int n = (int)(w >> 8), k = (int)(w & 0xFF);
+        const uint64_t* rec = wk.units + u * (1 + W);
+        const uint64_t w = rec[0];
+        const int n = (int)(w >> 16), k = (int)((w >> 8) & 0xFF), role = (int)(w & 0xFF);
         int cnt = 0;
 #pragma unroll
         for (int i = 0; i < W; ++i) {
-            uint64_t m = wk.gmask[((int64_t)k * W + i) * N + n];
+            uint64_t m = rec[1 + i];
             while (m) {
                 mem[(cnt++) * kEvalBlock] = (uint8_t)(i * 64 + __builtin_ctzll(m));
                 m &= m - 1;
             }
         }
-        const int role = p.role[(int64_t)k * N + n];
         bool have = false;
         int best_tp = 0, best_pp = 0;
         double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
@@ -385,13 +390,13 @@ template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipStream_t s) {
     const int nb = 2 * (p.G + 1);
     hipLaunchKernelGGL(fill_kernel, dim3((2 * nb + 1 + 255) / 256), dim3(256), 0, s, wk.hist, 2 * nb + 1);
-    // decode: the widest block whose per-lane masks fit in 32 KB of LDS
+    // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS
     int bs = 256;
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)p.Kmax * W * bs * 8;
     hipLaunchKernelGGL(decode_kernel<W>, dim3((p.N + bs - 1) / bs), dim3(bs), lds_dec, s, p, o, wk);
     hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(64), 0, s, wk, nb);
-    hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 2 * sizeof(int32_t) * nb, s, p, wk);
+    hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 0, s, p, wk);
     const bool tables = p.G <= kTableMaxG;
     // A grid-stride loop over the units: enough workgroups to fill the chip several times.
     // 256 lanes per workgroup amortise the staged tables; the per-lane member columns take
@@ -415,13 +420,13 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
 
 }  // namespace
 
+int mask_words(int32_t n_gpus) { return n_gpus <= 64 ? 1 : (n_gpus <= 128 ? 2 : 4); }
+
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
-    return head + sizeof(uint64_t) * (size_t)max_units(n_gpus, max_groups, n_cand);
+    return head + sizeof(uint64_t) * (1 + mask_words(n_gpus)) * (size_t)max_units(n_gpus, max_groups, n_cand);
 }
-
-int mask_words(int32_t n_gpus) { return n_gpus <= 64 ? 1 : (n_gpus <= 128 ? 2 : 4); }
 
 hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
     const size_t nb = 2 * ((size_t)p.G + 1);

@@ -44,22 +44,37 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
     const int64_t N = p.N;
     int np = 0, nd = 0;
     if (p.granularity == 0) {
-        for (int k = 0; k < p.Kmax; ++k) {
-            if (mask_size<W>(o.members, k, N, n) == 0) continue;
-            const int r = p.role[(int64_t)k * N + n];
-            const int32_t c = o.cap[(int64_t)k * N + n];
-            if (r == HX_PREFILL) {
-                const int64_t e = (int64_t)np * N + n;
-                f.p_slot[e] = k;
-                f.src_cap[e] = p.coord_cap;
-                f.p_cap[e] = c;
-                ++np;
-            } else if (r == HX_DECODE) {
-                const int64_t e = (int64_t)nd * N + n;
-                f.d_slot[e] = k;
-                f.d_cap[e] = c;
-                f.sink_cap[e] = p.coord_cap;
-                ++nd;
+        // Group slots in chunks of 8: the chunk's loads are issued together, then its slots
+        // are appended to the node lists in ascending order.
+        constexpr int kC = 8;
+        for (int k0 = 0; k0 < p.Kmax; k0 += kC) {
+            int sz[kC], rl[kC];
+            int32_t cp[kC];
+#pragma unroll
+            for (int x = 0; x < kC; ++x) {
+                const int k = k0 + x;
+                const bool in = k < p.Kmax;
+                sz[x] = in ? mask_size<W>(o.members, k, N, n) : 0;
+                rl[x] = in ? p.role[(int64_t)k * N + n] : HX_UNUSED;
+                cp[x] = in ? o.cap[(int64_t)k * N + n] : 0;
+            }
+#pragma unroll
+            for (int x = 0; x < kC; ++x) {
+                if (sz[x] == 0) continue;
+                const int k = k0 + x;
+                if (rl[x] == HX_PREFILL) {
+                    const int64_t e = (int64_t)np * N + n;
+                    f.p_slot[e] = k;
+                    f.src_cap[e] = p.coord_cap;
+                    f.p_cap[e] = cp[x];
+                    ++np;
+                } else if (rl[x] == HX_DECODE) {
+                    const int64_t e = (int64_t)nd * N + n;
+                    f.d_slot[e] = k;
+                    f.d_cap[e] = cp[x];
+                    f.sink_cap[e] = p.coord_cap;
+                    ++nd;
+                }
             }
         }
     } else {

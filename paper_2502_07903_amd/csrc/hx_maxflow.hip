@@ -33,7 +33,8 @@
 namespace hx {
 namespace {
 
-constexpr int kGlobalRelabelEvery = 8;  // rounds between exact relabels
+constexpr int kGlobalRelabelEvery = 2;  // rounds between exact relabels
+constexpr int kPackedLanes = 64;  // workgroup size for packed segments: one wavefront
 
 struct MfLayout {
     int32_t* cap;   // [P][Ds] KV capacities, row stride Ds = D | 1 (odd: no bank conflicts)
@@ -111,9 +112,9 @@ __device__ void global_relabel(const MfLayout& L, int l, int P, int D, int Ds, i
 // each XCD walks a contiguous candidate range, sharing the L2 lines of the candidate-fastest
 // input arrays.
 template <int SEG>
-__global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
+__global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
     maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget) {
-    constexpr int kLanes = SEG < 64 ? 64 : SEG;
+    constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const int N = f.N;
     const int tiles = (N + kPer - 1) / kPer;
@@ -124,14 +125,38 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
 
     extern __shared__ int32_t smem[];
     const MfLayout L = carve(smem + seg * mf_words(f.max_p, f.max_d, f.max_pd), f.max_p, f.max_d, f.max_pd);
-    int P = 0, D = 0;
     bool valid = tile < tiles && n < N;
+
+    // Packed segments (SEG <= 64) own at most one node row per side and SEG/4 KV rows per
+    // lane, so every global load is issued at once, before the counts that say which rows
+    // are used have arrived: one memory round trip instead of three.  Unused rows are read
+    // from the caller's [max][N] arrays and ignored.
+    constexpr int kKvRows = SEG <= 64 ? (SEG / 4 > 0 ? SEG / 4 : 1) : 1;
+    int32_t src0 = 0, pc0 = 0, dc0 = 0, sk0 = 0;
+    int32_t kvr[kKvRows];
+    int P = 0, D = 0;
     if (valid) {
         P = f.n_p[n];
         D = f.n_d[n];
+        if (SEG <= 64) {
+            if (l < f.max_p) {
+                src0 = f.src_cap[(int64_t)l * N + n];
+                pc0 = f.p_cap[(int64_t)l * N + n];
+            }
+            if (l < f.max_d) {
+                dc0 = f.d_cap[(int64_t)l * N + n];
+                sk0 = f.sink_cap[(int64_t)l * N + n];
+            }
+#pragma unroll
+            for (int r = 0; r < kKvRows; ++r) {
+                const int e = l + r * SEG;
+                kvr[r] = e < f.max_pd ? f.kv_cap[(int64_t)e * N + n] : 0;
+            }
+        }
         // A network larger than the plan it was built for is rejected before any LDS or array
         // index is formed from it.
-        if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || P * D > f.max_pd) {
+        if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || P * D > f.max_pd ||
+            (SEG <= 64 && (P > SEG || D > SEG || P * D > kKvRows * SEG))) {
             if (l == 0) flow_value[n] = HX_EINVAL;
             valid = false;
         }
@@ -139,28 +164,55 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
     if (!valid) P = D = 0;
     const int Ds = D | 1;
 
-    for (int e = l; e < P * D; e += SEG) {
-        const int i = e / D, d = e - i * D;
-        L.cap[i * Ds + d] = f.kv_cap[(int64_t)e * N + n];
-        L.fl[i * Ds + d] = 0;
-    }
-    const bool has_flow = P > 0 && D > 0;
-    for (int i = l; i < P; i += SEG) {
-        const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
-        const int32_t a = has_flow ? (s < c ? s : c) : 0;  // no decode node: nothing can flow
-        L.a[i] = a;
-        L.fs[i] = a;  // saturate every source edge
-        L.ep[i] = a;
-    }
-    for (int j = l; j < D; j += SEG) {
-        const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
-        L.b[j] = c < t ? c : t;
-        L.ft[j] = 0;
-        L.ed[j] = 0;
-    }
+    // Node capacities first: a candidate whose source side or sink side carries nothing has
+    // flow 0 and never needs its KV capacities (the cut sweep still sees zero flows).
     if (l == 0) {
         L.misc[0] = 0;
         L.misc[1] = 0;
+        L.misc[2] = 0;
+        L.misc[3] = 0;
+    }
+    __syncthreads();
+    for (int i = l; i < P; i += SEG) {
+        const int32_t s = SEG <= 64 ? src0 : f.src_cap[(int64_t)i * N + n];
+        const int32_t c = SEG <= 64 ? pc0 : f.p_cap[(int64_t)i * N + n];
+        const int32_t a = s < c ? s : c;
+        L.a[i] = a;
+        if (a > 0) L.misc[2] = 1;
+    }
+    for (int j = l; j < D; j += SEG) {
+        const int32_t c = SEG <= 64 ? dc0 : f.d_cap[(int64_t)j * N + n];
+        const int32_t t = SEG <= 64 ? sk0 : f.sink_cap[(int64_t)j * N + n];
+        const int32_t b = c < t ? c : t;
+        L.b[j] = b;
+        L.ft[j] = 0;
+        L.ed[j] = 0;
+        if (b > 0) L.misc[3] = 1;
+    }
+    __syncthreads();
+    const bool has_flow = P > 0 && D > 0 && L.misc[2] && L.misc[3];
+    for (int i = l; i < P; i += SEG) {
+        const int32_t a = has_flow ? L.a[i] : 0;
+        L.fs[i] = a;  // saturate every source edge
+        L.ep[i] = a;
+    }
+    if (SEG <= 64) {
+#pragma unroll
+        for (int r = 0; r < kKvRows; ++r) {
+            const int e = l + r * SEG;
+            if (e < P * D) {
+                const int i = e / D, d = e - i * D;
+                L.cap[i * Ds + d] = kvr[r];
+                L.fl[i * Ds + d] = 0;
+            }
+        }
+    } else {
+        const bool need_kv = has_flow || kv_flow != nullptr || cut != nullptr;
+        for (int e = l; need_kv && e < P * D; e += SEG) {
+            const int i = e / D, d = e - i * D;
+            L.cap[i * Ds + d] = f.kv_cap[(int64_t)e * N + n];
+            L.fl[i * Ds + d] = 0;
+        }
     }
     __syncthreads();
 
@@ -173,21 +225,27 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
             global_relabel<SEG>(L, l, P, D, Ds, V, INF);
             __syncthreads();
         }
-        // P-phase
+        // P-phase: push along admissible arcs and, in the same pass, track the lowest height
+        // across arcs still holding residual capacity, for the relabel if excess remains.
         for (int i = l; i < P; i += SEG) {
             int e = L.ep[i];
             if (e <= 0) continue;
             const int h = L.hp[i];
             const int32_t* c = L.cap + i * Ds;
             int32_t* fr = L.fl + i * Ds;
+            int mh = INF;
             for (int d = 0; d < D && e > 0; ++d) {
-                const int r = c[d] - fr[d];
-                if (r > 0 && h == L.hd[d] + 1) {
+                int r = c[d] - fr[d];
+                if (r <= 0) continue;
+                const int hd = L.hd[d];
+                if (h == hd + 1) {
                     const int amt = r < e ? r : e;
                     fr[d] += amt;
                     e -= amt;
+                    r -= amt;
                     atomicAdd(&L.ed[d], amt);
                 }
+                if (r > 0 && hd < mh) mh = hd;
             }
             if (e > 0 && h == V + 1) {
                 const int amt = L.fs[i] < e ? L.fs[i] : e;
@@ -195,16 +253,14 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
                 e -= amt;
             }
             if (e > 0) {
-                int mh = INF;
-                for (int d = 0; d < D; ++d)
-                    if (c[d] - fr[d] > 0 && L.hd[d] < mh) mh = L.hd[d];
                 if (L.fs[i] > 0 && V < mh) mh = V;
                 L.hp[i] = mh + 1 < INF ? mh + 1 : INF;
             }
             L.ep[i] = e;
         }
         __syncthreads();
-        // D-phase
+        // D-phase: push to the sink, then back along used KV arcs, tracking the lowest height
+        // across arcs left with residual capacity for the relabel.
         for (int j = l; j < D; j += SEG) {
             int e = L.ed[j];
             if (e <= 0) continue;
@@ -217,19 +273,22 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
                     e -= amt;
                 }
             }
+            int mh = INF;
             for (int q = 0; q < P && e > 0; ++q) {
-                const int fq = L.fl[q * Ds + j];
-                if (fq > 0 && h == L.hp[q] + 1) {
+                int fq = L.fl[q * Ds + j];
+                if (fq <= 0) continue;
+                const int hq = L.hp[q];
+                if (h == hq + 1) {
                     const int amt = fq < e ? fq : e;
-                    L.fl[q * Ds + j] = fq - amt;
+                    fq -= amt;
+                    L.fl[q * Ds + j] = fq;
                     e -= amt;
                     atomicAdd(&L.ep[q], amt);
                 }
+                if (fq > 0 && hq < mh) mh = hq;
             }
             if (e > 0) {
-                int mh = L.b[j] - L.ft[j] > 0 ? 0 : INF;
-                for (int q = 0; q < P; ++q)
-                    if (L.fl[q * Ds + j] > 0 && L.hp[q] < mh) mh = L.hp[q];
+                if (L.b[j] - L.ft[j] > 0) mh = 0;
                 L.hd[j] = mh + 1 < INF ? mh + 1 : INF;
             }
             L.ed[j] = e;
@@ -315,18 +374,19 @@ __global__ void __launch_bounds__(SEG < 64 ? 64 : SEG)
 
 constexpr size_t kMaxLds = 64 * 1024;
 
-// Lanes per candidate: the smallest power of two >= the widest side (at least 8), so that
-// one lane owns one node; beyond 256 nodes per side a lane owns several.
-int segment_lanes(int max_p, int max_d) {
+// Lanes per candidate: the smallest power of two (at least 8) with one lane per node of the
+// widest side and SEG/4 KV rows per lane covering max_pd (SEG^2/4 >= max_pd); beyond 256
+// lanes a lane owns several nodes.
+int segment_lanes(int max_p, int max_d, int max_pd) {
     const int widest = max_p > max_d ? max_p : max_d;
     int s = 8;
-    while (s < widest && s < 256) s *= 2;
+    while (s < 256 && (s < widest || (int64_t)s * s / 4 < max_pd)) s *= 2;
     return s;
 }
 
 template <int SEG>
 hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, int32_t budget, hipStream_t s) {
-    constexpr int kLanes = SEG < 64 ? 64 : SEG;
+    constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const size_t lds = kPer * mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
     const int tiles = (f.N + kPer - 1) / kPer;
@@ -338,15 +398,15 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
 }  // namespace
 
 size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd) {
-    const int seg = segment_lanes(max_p, max_d);
-    const int per = seg < 64 ? 64 / seg : 1;
+    const int seg = segment_lanes(max_p, max_d, max_pd);
+    const int per = seg < 64 ? kPackedLanes / seg : 1;
     const size_t bytes = per * mf_words(max_p, max_d, max_pd) * sizeof(int32_t);
     return bytes <= kMaxLds ? bytes : 0;
 }
 
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           hipStream_t s) {
-    switch (segment_lanes(f.max_p, f.max_d)) {
+    switch (segment_lanes(f.max_p, f.max_d, f.max_pd)) {
         case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, s);
         case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, s);
         case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, s);

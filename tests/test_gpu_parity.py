@@ -229,18 +229,21 @@ def test_maxflow_adversarial(torch):
     Hh.compare_cut(cut, want["cut"], fn)
 
 
-def test_maxflow_random_networks(torch):
-    """Random capacities (not from the cost model) over every shape up to 16 x 16."""
-    rng = np.random.default_rng(78)
-    N, mp, md = 3000, 16, 16
-    fn = dict(n_p=rng.integers(0, mp + 1, N).astype(np.int32), n_d=rng.integers(0, md + 1, N).astype(np.int32),
-              dims=(mp, md, mp * md))
-    for k, rows in (("src_cap", mp), ("p_cap", mp), ("d_cap", md), ("sink_cap", md), ("kv_cap", mp * md),
+@pytest.mark.parametrize("mp,md,total,N", [(16, 16, 32, 3000), (40, 40, 40, 800), (6, 6, 12, 2000)])
+def test_maxflow_random_networks(torch, mp, md, total, N):
+    """Random capacities (not from the cost model) over every shape with P + D <= total; the
+    plans select 32-, 64- and 8-lane segments."""
+    rng = np.random.default_rng(78 + mp)
+    n_p = rng.integers(0, mp + 1, N)
+    n_d = np.minimum(rng.integers(0, md + 1, N), total - n_p)
+    mpd = (total // 2) * ((total + 1) // 2)
+    fn = dict(n_p=n_p.astype(np.int32), n_d=n_d.astype(np.int32), dims=(mp, md, mpd))
+    for k, rows in (("src_cap", mp), ("p_cap", mp), ("d_cap", md), ("sink_cap", md), ("kv_cap", mpd),
                     ("p_slot", mp), ("d_slot", md)):
         hi = rng.choice([2, 100, 10 ** 5, Hh.CAP_MAX], size=N)
         fn[k] = (rng.random((rows, N)) * (hi[None, :] + 1)).astype(np.int32)
     want = hxo.maxflow_batch(fn)
-    say(f"random networks: {N}")
+    say(f"random networks: {N} with P + D <= {total}")
     fv, kv, cut = _maxflow_on(torch, fn)
     assert np.array_equal(fv, want["flow_value"])
     Hh.check_flow_batch(fn, fv, kv)
