@@ -37,6 +37,8 @@ constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40^2 d
 
 struct Tables {
     const double *gfl, *ghb, *gme, *alpha, *beta;
+    const double* tp_pre;  // [tp - 1][G][G] alpha + X/(tp beta) at batch 1 (prefill), per call
+    const double* pp_pre;  // [G][G] alpha + X/beta at batch 1
 };
 
 struct StrategyCost {
@@ -111,11 +113,12 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                 if (x == r) d = S[x];
             const double* arow = tb.alpha + d * G;
             const double* brow = tb.beta + d * G;
+            const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
             double sum = 0.0;
 #pragma unroll
             for (int q = 0; q < kMax; ++q) {
                 if ((TPC == 0 && q >= tp) || q == r) continue;
-                sum = sum + (arow[S[q]] + X / (t * brow[S[q]]));
+                sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
             }
             if (r == 0 || sum > mx) mx = sum;
         }
@@ -132,10 +135,11 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                     if (x == r) d = Sp[x];
                 const double* arow = tb.alpha + d * G;
                 const double* brow = tb.beta + d * G;
+                const double* prow = tb.pp_pre + (size_t)d * G;
 #pragma unroll
                 for (int q = 0; q < kMax; ++q) {
                     if (TPC == 0 && q >= tp) continue;
-                    const double v = arow[S[q]] + X / brow[S[q]];
+                    const double v = prefill ? prow[S[q]] : arow[S[q]] + X / brow[S[q]];
                     if ((r == 0 && q == 0) || v < mn) mn = v;
                 }
             }
@@ -163,15 +167,38 @@ __device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, con
 // ------------------------------------------------------------------ kernels
 
 struct CostWork {
-    int32_t* hist;    // [nb + 1]: per (size, role) unit counts, then offsets; [nb] = total
-    int32_t* cursor;  // [nb]
+    int32_t* hist;    // [nb + 1]: per (size, role) unit counts ([nb] unused)
+    int32_t* cursor;  // [nb]: units placed so far per bucket
     uint64_t* units;  // [max units][1 + W]: (n << 16 | k << 8 | role), then the member mask words
     uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
+    double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables)
+    double* pp_pre;   // [G][G] prefill PP terms
 };
 
-__global__ void fill_kernel(int32_t* a, int n) {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) a[i] = 0;
+// First kernel of a call: clears the histogram and cursors (n_clear words) and tabulates the
+// prefill link terms.  Prefill runs at batch 1, so its per-link TP and PP terms depend only on
+// the cluster and the task: alpha + X/(tp beta) for every TP degree of the mask and
+// alpha + X/beta, X = 1*s_in*H*B, evaluated exactly as the costing expressions do (the same
+// binary64 values).
+__global__ void setup_kernel(Problem p, CostWork wk, int n_clear) {
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t nth = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = tid; i < n_clear; i += nth) wk.hist[i] = 0;
+    const int G = p.G;
+    const int64_t gg = (int64_t)G * G;
+    const double X = 1.0 * p.s_in * p.H * p.B;
+    for (int64_t i = tid; i < (HX_MAX_TP + 1) * gg; i += nth) {
+        const int slot = (int)(i / gg);
+        const int64_t de = i - slot * gg;
+        if (slot == HX_MAX_TP) {
+            wk.pp_pre[de] = p.alpha[de] + X / p.beta[de];
+        } else {
+            const int tp = slot + 1;
+            if (tp >= 2 && ((p.tp_mask >> (tp - 1)) & 1u)) wk.tp_pre[i] = p.alpha[de] + X / ((double)tp * p.beta[de]);
+        }
+    }
 }
+
 
 // Bucket of a present group: largest sizes first, roles interleaved.
 __device__ __forceinline__ int bucket_of(int G, int size, int role) { return (G - size) * 2 + role; }
@@ -237,46 +264,62 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
         if (lhist[b]) atomicAdd(&wk.hist[b], lhist[b]);
 }
 
-// Exclusive scan of hist[0..nb) into hist (offsets) and cursor; hist[nb] = total.
-__global__ void __launch_bounds__(64) scan_kernel(CostWork wk, int nb) {
-    const int lane = threadIdx.x;
-    const int per = (nb + 63) / 64;
-    const int lo = lane * per, hi = lo + per < nb ? lo + per : nb;
+// Workgroup barrier that first drains the calling wave's outstanding LDS operations
+// (lgkmcnt(0); the vector-memory and export counters are left at their maxima).  The counting
+// pass ends in LDS atomics whose results are unused; the barrier the compiler emits after them
+// does not wait for them on every path, and without the wait some increments were measured to
+// land after the workgroup had read the counts.
+__device__ __forceinline__ void lds_drain_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __syncthreads();
+}
+
+// Sum of h[0..hi) across one wavefront; every lane receives it.
+__device__ __forceinline__ int32_t wave_sum(const int32_t* h, int hi, int lane) {
     int32_t s = 0;
-    for (int i = lo; i < hi; ++i) s += wk.hist[i];
-    int32_t incl = s;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int32_t v = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += v;
-    }
-    int32_t run = incl - s;
-    for (int i = lo; i < hi; ++i) {
-        const int32_t v = wk.hist[i];
-        wk.hist[i] = run;
-        wk.cursor[i] = run;
-        run += v;
-    }
-    if (lane == 63) wk.hist[nb] = incl;
+    for (int i = lane; i < hi; i += 64) s += h[i];
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    return s;
 }
 
 // One lane per candidate: every present group becomes a unit record (candidate, slot, role,
-// member mask) in its bucket.  Two passes over the slots: count per bucket, reserve the
-// workgroup's range of each bucket with one atomic, then write.
+// member mask) in its bucket.  Each workgroup scans the bucket counts into bucket offsets
+// itself (a few hundred words from L2).  Two passes over the slots: count per bucket, reserve
+// the workgroup's range of each bucket with one atomic on the bucket's cursor, then write.
 template <int W>
 __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     __shared__ int32_t lcount[2 * (HX_MAX_GPUS + 1)];
     __shared__ int32_t lbase[2 * (HX_MAX_GPUS + 1)];
+    __shared__ int32_t loff[2 * (HX_MAX_GPUS + 1)];
     const int nb = 2 * (p.G + 1);
     for (int b = threadIdx.x; b < nb; b += blockDim.x) lcount[b] = 0;
+    if (threadIdx.x < 64) {
+        // exclusive scan of the bucket counts, each lane over a run of consecutive buckets
+        const int lane = threadIdx.x;
+        const int per = (nb + 63) / 64;
+        const int lo = lane * per, hi = lo + per < nb ? lo + per : nb;
+        int32_t sum = 0;
+        for (int i = lo; i < hi; ++i) sum += wk.hist[i];
+        int32_t incl = sum;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t v = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += v;
+        }
+        int32_t run = incl - sum;
+        for (int i = lo; i < hi; ++i) {
+            loff[i] = run;
+            run += wk.hist[i];
+        }
+    }
     __syncthreads();
     const int n = blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
     for (int pass = 0; pass < 2; ++pass) {
         if (pass == 1) {
-            __syncthreads();
+            lds_drain_barrier();
             for (int b = threadIdx.x; b < nb; b += blockDim.x) {
-                lbase[b] = lcount[b] ? atomicAdd(&wk.cursor[b], lcount[b]) : 0;
+                lbase[b] = lcount[b] ? loff[b] + atomicAdd(&wk.cursor[b], lcount[b]) : 0;
                 lcount[b] = 0;
             }
             __syncthreads();
@@ -311,6 +354,167 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     }
 }
 
+// ------------------------------------------------------------------ large groups
+
+// Groups of at least kCoopMin GPUs carry a long serial chain of divisions when one lane costs
+// them (hundreds for a 24-GPU decode group), so kCoopLanes lanes of a wavefront cost each:
+// lane-parallel over stages for the memory row and the computation term, over (stage,
+// device) rows for the TP sums and PP minima; one lane then combines the rows in the
+// documented order, so every value is the same binary64 the one-lane path produces.
+constexpr int kCoopMin = 12;
+constexpr int kCoopLanes = 16;
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Per-group LDS: member ids [G], row values tsum/pmin [G] (one per (stage, device)), stage
+// computation terms comp [HX_MAX_PP].
+struct CoopLds {
+    uint8_t* mem;
+    double *tsum, *pmin, *comp;
+};
+
+__host__ __device__ inline size_t coop_group_bytes(int G) {
+    return ((size_t)G + 7) / 8 * 8 + sizeof(double) * (2 * (size_t)G + HX_MAX_PP);
+}
+
+__device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
+    CoopLds c;
+    c.mem = base;
+    c.tsum = reinterpret_cast<double*>(base + ((size_t)G + 7) / 8 * 8);
+    c.pmin = c.tsum + G;
+    c.comp = c.pmin + G;
+    return c;
+}
+
+// One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
+// is false for groups past the last large unit (they still join every wave-level sync).
+__device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, int gl, bool live,
+                          int n, int k, int role, uint64_t mask) {
+    const int G = p.G;
+    const int cnt = live ? __popcll(mask) : 0;
+    for (int g = gl; g < G && live; g += kCoopLanes)
+        if ((mask >> g) & 1ull) c.mem[__popcll(mask & ((1ull << g) - 1))] = (uint8_t)g;
+    wave_sync();
+    const double H = p.H, B = p.B;
+    const double W12 = 12.0 * H * H * B;
+    const double Kkv = 2.0 * (p.s_in + p.s_out) * p.Hkv * B;
+    const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
+    const bool prefill = role == HX_PREFILL;
+    bool have = false;
+    int best_tp = 0, best_pp = 0;
+    double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
+    for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
+        const bool adm = live && ((p.tp_mask >> (tp - 1)) & 1u) && cnt % tp == 0 && cnt / tp <= HX_MAX_PP &&
+                         ((p.pp_mask >> (cnt / tp - 1)) & 1u) && cnt / tp <= p.L;
+        const int pp = adm ? cnt / tp : 0;
+        const double t = (double)tp;
+        const int lq = adm ? p.L / pp : 0, lr = adm ? p.L % pp : 0;
+        // Memory-limit row, one lane per stage, then the group's minimum (exact).
+        double bl = kBmaxClamp;
+        for (int j = gl; j < pp; j += kCoopLanes) {
+            const double l = (double)(lq + (j < lr ? 1 : 0));
+            const double A = (W12 / t) * l;
+            const double K = (Kkv / t) * l + Kact;
+            const uint8_t* S = c.mem + j * tp;
+            double Mmin = tb.gme[S[0]];
+            for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, tb.gme[S[r]]);
+            const double q = (Mmin - A) / K;
+            const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
+            bl = dmin(bl, b);
+        }
+        for (int off = kCoopLanes / 2; off > 0; off >>= 1) bl = dmin(bl, __shfl_xor(bl, off, kCoopLanes));
+        const bool feas = adm && bl >= 1.0;
+        const double b = prefill ? 1.0 : bl;
+        const double Xcomp_p = 24.0 * b * p.s_in * H * H;
+        const double Xscan_d = 12.0 * H * H * B * p.s_out;
+        const double Xcomp_d = 24.0 * b * p.s_out * H * H;
+        const double X = prefill ? b * p.s_in * H * B : b * H * B;
+        // Rows (stage j, device r): the device's TP sum over its peers (ascending) and its
+        // fastest link into stage j+1.
+        for (int it = gl; feas && it < cnt; it += kCoopLanes) {
+            const int j = it / tp, r = it - j * tp;
+            const uint8_t* S = c.mem + j * tp;
+            const int d = S[r];
+            const double* arow = tb.alpha + d * G;
+            const double* brow = tb.beta + d * G;
+            const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
+            const double* qrow = tb.pp_pre + (size_t)d * G;
+            double sum = 0.0;
+            for (int q = 0; q < tp; ++q) {
+                if (q == r) continue;
+                sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
+            }
+            c.tsum[it] = sum;
+            if (j + 1 < pp) {
+                const uint8_t* S2 = S + tp;
+                double mn = 0.0;
+                for (int q = 0; q < tp; ++q) {
+                    const double v = prefill ? qrow[S2[q]] : arow[S2[q]] + X / brow[S2[q]];
+                    if (q == 0 || v < mn) mn = v;
+                }
+                c.pmin[it] = mn;
+            }
+        }
+        for (int j = gl; feas && j < pp; j += kCoopLanes) {
+            const double l = (double)(lq + (j < lr ? 1 : 0));
+            const uint8_t* S = c.mem + j * tp;
+            double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
+            for (int r = 1; r < tp; ++r) {
+                cmin = dmin(cmin, tb.gfl[S[r]]);
+                hmin = dmin(hmin, tb.ghb[S[r]]);
+            }
+            c.comp[j] = prefill ? (Xcomp_p / (t * cmin)) * l
+                                : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
+        }
+        wave_sync();
+        if (feas && gl == 0) {
+            double s1 = 0.0, s2 = 0.0;
+            for (int j = 0; j < pp; ++j) {
+                const double l = (double)(lq + (j < lr ? 1 : 0));
+                double mx = 0.0;
+                for (int r = 0; r < tp; ++r) {
+                    const double v = c.tsum[j * tp + r];
+                    if (r == 0 || v > mx) mx = v;
+                }
+                const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
+                s1 = s1 + (c.comp[j] + tpc);
+            }
+            for (int j = 0; j + 1 < pp; ++j) {
+                double mn = 0.0;
+                for (int r = 0; r < tp; ++r) {
+                    const double v = c.pmin[j * tp + r];
+                    if (r == 0 || v < mn) mn = v;
+                }
+                s2 = s2 + (prefill ? mn : mn * p.s_out);
+            }
+            const double lat = s1 + s2;
+            const double x = (1000.0 * b) / lat;
+            const bool better = !have || (prefill ? lat < best_lat : x > best_x);
+            if (better) {
+                have = true;
+                best_tp = tp;
+                best_pp = pp;
+                best_b = bl;
+                best_lat = lat;
+                best_x = x;
+            }
+        }
+        wave_sync();
+    }
+    if (live && gl == 0) {
+        const int64_t o_ = (int64_t)k * p.N + n;
+        o.tp[o_] = (uint8_t)best_tp;
+        o.pp[o_] = (uint8_t)best_pp;
+        o.bmax[o_] = (int32_t)best_b;
+        o.cap[o_] = have ? quantize(best_x) : 0;
+        o.lat[o_] = best_lat;
+    }
+}
+
 template <int W, bool kTables, int kEvalBlock>
 __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
@@ -325,7 +529,7 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
         ghb[g] = ok ? p.hbm[t] : 0.0;
         gme[g] = ok ? p.mem[t] : 0.0;
     }
-    Tables tb{gfl, ghb, gme, p.alpha, p.beta};
+    Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre};
     double* tb_end = gme + G;
     if (kTables) {
         double* a = gme + G;
@@ -338,11 +542,48 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
         tb.beta = b;
         tb_end = b + G * G;
     }
+    // Units in all: the sum of the bucket counts.  Units before the (size kCoopMin - 1)
+    // buckets are the large groups (sizes descend).
+    __shared__ int32_t counts[2];
+    if (threadIdx.x < 64) {
+        const int32_t t = wave_sum(wk.hist, nb, threadIdx.x);
+        const int32_t f = W == 1 && G >= kCoopMin ? wave_sum(wk.hist, bucket_of(G, kCoopMin - 1, 0), threadIdx.x) : 0;
+        if (threadIdx.x == 0) {
+            counts[0] = t;
+            counts[1] = f;
+        }
+    }
     __syncthreads();
-    const int64_t total = wk.hist[nb];
+    const int64_t total = counts[0];
     const int64_t N = p.N;
     uint8_t* mem = reinterpret_cast<uint8_t*>(tb_end) + threadIdx.x;  // [G][kEvalBlock] member list
-    for (int64_t u = (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total; u += (int64_t)gridDim.x * kEvalBlock) {
+    const int64_t first_small = counts[1];
+    if (W == 1 && G >= kCoopMin) {
+        unsigned char* cbase = reinterpret_cast<unsigned char*>(tb_end) + (size_t)G * kEvalBlock;
+        const int lane = threadIdx.x & 63, grp = lane / kCoopLanes, gl = lane % kCoopLanes;
+        const int wave = threadIdx.x >> 6;
+        constexpr int kGroupsPerWave = 64 / kCoopLanes;
+        const CoopLds c = carve_coop(cbase + (wave * kGroupsPerWave + grp) * coop_group_bytes(G), G);
+        const int64_t waves = (int64_t)gridDim.x * (kEvalBlock / 64);
+        for (int64_t base = ((int64_t)blockIdx.x * (kEvalBlock / 64) + wave) * kGroupsPerWave; base < first_small;
+             base += waves * kGroupsPerWave) {
+            const int64_t u = base + grp;
+            const bool live = u < first_small;
+            int n = 0, k = 0, role = 0;
+            uint64_t mask = 0;
+            if (live) {
+                const uint64_t* rec = wk.units + u * (1 + W);
+                const uint64_t w = rec[0];
+                n = (int)(w >> 16);
+                k = (int)((w >> 8) & 0xFF);
+                role = (int)(w & 0xFF);
+                mask = rec[1];
+            }
+            coop_unit(p, tb, o, c, gl, live, n, k, role, mask);
+        }
+    }
+    for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
+         u += (int64_t)gridDim.x * kEvalBlock) {
         const uint64_t* rec = wk.units + u * (1 + W);
         const uint64_t w = rec[0];
         const int n = (int)(w >> 16), k = (int)((w >> 8) & 0xFF), role = (int)(w & 0xFF);
@@ -389,13 +630,18 @@ int64_t max_units(int G, int Kmax, int64_t N) { return (int64_t)(Kmax < G ? Kmax
 template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipStream_t s) {
     const int nb = 2 * (p.G + 1);
-    hipLaunchKernelGGL(fill_kernel, dim3((2 * nb + 1 + 255) / 256), dim3(256), 0, s, wk.hist, 2 * nb + 1);
+    {
+        // hist and cursor are contiguous: 2 nb + 1 words to clear
+        const int64_t cells = (int64_t)(HX_MAX_TP + 1) * p.G * p.G;
+        const int64_t want = (cells > 2 * nb + 1 ? cells : 2 * nb + 1) + 255;
+        const int blocks = (int)(want / 256 < 1024 ? want / 256 : 1024);
+        hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1);
+    }
     // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS
     int bs = 256;
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)p.Kmax * W * bs * 8;
     hipLaunchKernelGGL(decode_kernel<W>, dim3((p.N + bs - 1) / bs), dim3(bs), lds_dec, s, p, o, wk);
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(64), 0, s, wk, nb);
     hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 0, s, p, wk);
     const bool tables = p.G <= kTableMaxG;
     // A grid-stride loop over the units: enough workgroups to fill the chip several times.
@@ -403,8 +649,8 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     // G bytes per lane, so beyond 128 GPUs the workgroup halves to stay within 64 KB of LDS.
     const int64_t units = max_units(p.G, p.Kmax, p.N);
     const int eb = p.G <= 128 ? 256 : 128;
-    const size_t lds_eval =
-        sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) + (size_t)p.G * eb;
+    const size_t lds_eval = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) +
+                            (size_t)p.G * eb + (W == 1 ? (size_t)(eb / kCoopLanes) * coop_group_bytes(p.G) : 0);
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     if (eb == 256) {
@@ -422,10 +668,16 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
 
 int mask_words(int32_t n_gpus) { return n_gpus <= 64 ? 1 : (n_gpus <= 128 ? 2 : 4); }
 
+static size_t units_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    const size_t b = sizeof(uint64_t) * (1 + mask_words(n_gpus)) * (size_t)max_units(n_gpus, max_groups, n_cand);
+    return (b + 255) & ~(size_t)255;
+}
+
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
-    return head + sizeof(uint64_t) * (1 + mask_words(n_gpus)) * (size_t)max_units(n_gpus, max_groups, n_cand);
+    const size_t tables = sizeof(double) * (HX_MAX_TP + 1) * (size_t)n_gpus * n_gpus;
+    return head + units_bytes(n_gpus, max_groups, n_cand) + tables;
 }
 
 hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
@@ -435,6 +687,9 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
     wk.hist = reinterpret_cast<int32_t*>(workspace);
     wk.cursor = wk.hist + nb + 1;
     wk.units = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(workspace) + head);
+    wk.tp_pre = reinterpret_cast<double*>(reinterpret_cast<unsigned char*>(workspace) + head +
+                                          units_bytes(p.G, p.Kmax, p.N));
+    wk.pp_pre = wk.tp_pre + (size_t)HX_MAX_TP * p.G * p.G;
     wk.gmask = o.members;
     switch (mask_words(p.G)) {
         case 1: return launch_w<1>(p, o, wk, s);

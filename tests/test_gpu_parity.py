@@ -277,6 +277,52 @@ def test_deterministic(torch):
         assert np.array_equal(g1["cost"][k], g2["cost"][k])
 
 
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_every_output_written_repeatedly(torch, cfg):
+    """Repeated full-size passes with every output and scratch buffer pre-filled with a garbage
+    pattern: every present group's cost outputs and every candidate's flow value must be
+    written on every call, identically.  This catches a unit the sort loses, or a value left
+    over from an earlier call, which a single call on fresh, zeroed memory can hide.  Sizes 32
+    GPUs (one mask word) and 128 GPUs (two)."""
+    prob = I.make_problem(cfg)
+    say(f"workload {cfg}: 12 repeated passes over dirty buffers, N={prob.n_cand}")
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    net_rows = ("n_p", "n_d", "p_slot", "d_slot", "src_cap", "p_cap", "kv_cap", "d_cap", "sink_cap")
+    ref = None
+    for it in range(12):
+        ws.cost.tp.fill_(0xAB)
+        ws.cost.pp.fill_(0xAB)
+        ws.cost.bmax.fill_(-12345)
+        ws.cost.cap.fill_(-12345)
+        ws.cost.lat.fill_(float("nan"))
+        ws.cost.members.fill_(-1)
+        ws.cost.workspace.fill_(0x5A)
+        for k in net_rows:
+            getattr(ws.net, k).fill_(0x7F7F7F7F if k not in ("n_p", "n_d") else 0)
+        ws.flow_value.fill_(-12345)
+        ws.best.fill_(-12345)
+        hx.score(dp, ws)
+        torch.cuda.synchronize()
+        got = {k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")}
+        got["flow_value"] = ws.flow_value.cpu().numpy()
+        got["best"] = ws.best.cpu().numpy()
+        assert not np.isnan(got["lat"]).any(), f"call {it}: unwritten latencies"
+        assert not (got["cap"] == -12345).any(), f"call {it}: unwritten capacities"
+        if ref is None:
+            ref = got
+            rng = np.random.default_rng(cfg)
+            idx = np.sort(rng.choice(prob.n_cand, 512, replace=False))
+            res = hxo.score_batch(prob.subset(idx), n_threads=N_THREADS)
+            for k in ("tp", "pp", "bmax", "cap", "lat"):
+                assert np.array_equal(got[k][:, idx], res["cost"][k]), f"cost {k} differs from the oracle"
+            assert np.array_equal(got["flow_value"][idx], res["flow_value"])
+        else:
+            for k in got:
+                bad = np.argwhere(got[k] != ref[k])
+                assert len(bad) == 0, f"call {it}: {k} differs from call 0 at (group, candidate) {bad[:5].tolist()}"
+
+
 # ------------------------------------------------------------------ argmax
 
 @pytest.mark.parametrize("n", [1, 2, 63, 64, 1025, 100003])
