@@ -203,13 +203,33 @@ __global__ void setup_kernel(Problem p, CostWork wk, int n_clear) {
 // Bucket of a present group: largest sizes first, roles interleaved.
 __device__ __forceinline__ int bucket_of(int G, int size, int role) { return (G - size) * 2 + role; }
 
+// Workgroup barrier that first drains the calling wave's outstanding LDS operations
+// (lgkmcnt(0); the vector-memory and export counters are left at their maxima).  The counting
+// pass ends in LDS atomics whose results are unused; the barrier the compiler emits after them
+// does not wait for them on every path, and without the wait some increments were measured to
+// land after the workgroup had read the counts.
+__device__ __forceinline__ void lds_drain_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __syncthreads();
+}
+
+// Group slots per chunk whose loads a lane issues together (C slots of 1 + W words each):
+// 8, 16 or 32, the smallest covering every slot, with at most 32 mask words in flight.
+__host__ inline int slot_chunk(int W, int Kmax) {
+    int c = Kmax <= 8 ? 8 : (Kmax <= 16 ? 16 : 32);
+    while (c > 8 && c * W > 32) c /= 2;
+    return c;
+}
+
+// GPUs per chunk of assign rows a lane loads together.
+constexpr int kGpuChunk = 32;
+
 // One lane per candidate (candidate-fastest, so every [row][n] access coalesces): the member
 // bitmask of each group slot, built in the lane's LDS column from its assign column; absent
 // slots' zero outputs; a per-workgroup histogram of units per bucket, added to the global one
-// with one atomic per bucket.  Slots go in chunks of kSlotChunk whose loads issue together.
-constexpr int kSlotChunk = 8;
-
-template <int W>
+// with one atomic per bucket.  Loads go in chunks (kGpuChunk assign rows, C role rows) that
+// issue together, so a lane waits on memory once per chunk.
+template <int W, int C>
 __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int nb = 2 * (p.G + 1);
@@ -222,21 +242,26 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     const int Kmax = p.Kmax;
     if (n < N) {
         for (int e = 0; e < Kmax * W; ++e) ms[e * bs + tid] = 0;
-#pragma unroll 8
-        for (int g = 0; g < p.G; ++g) {
-            const int k = p.assign[(int64_t)g * N + n];
-            if (k < Kmax) ms[(k * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
+        for (int g0 = 0; g0 < p.G; g0 += kGpuChunk) {
+            int a[kGpuChunk];
+#pragma unroll
+            for (int x = 0; x < kGpuChunk; ++x) a[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
+#pragma unroll
+            for (int x = 0; x < kGpuChunk; ++x) {
+                const int g = g0 + x, k = a[x];
+                if (k < Kmax) ms[(k * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
+            }
         }
     }
     __syncthreads();
     if (n < N) {
-        for (int k0 = 0; k0 < Kmax; k0 += kSlotChunk) {
-            int rl[kSlotChunk];
+        for (int k0 = 0; k0 < Kmax; k0 += C) {
+            int rl[C];
 #pragma unroll
-            for (int x = 0; x < kSlotChunk; ++x)
+            for (int x = 0; x < C; ++x)
                 rl[x] = k0 + x < Kmax ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
 #pragma unroll
-            for (int x = 0; x < kSlotChunk; ++x) {
+            for (int x = 0; x < C; ++x) {
                 const int k = k0 + x;
                 if (k >= Kmax) break;
                 int size = 0;
@@ -259,19 +284,9 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
             }
         }
     }
-    __syncthreads();
+    lds_drain_barrier();
     for (int b = tid; b < nb; b += bs)
         if (lhist[b]) atomicAdd(&wk.hist[b], lhist[b]);
-}
-
-// Workgroup barrier that first drains the calling wave's outstanding LDS operations
-// (lgkmcnt(0); the vector-memory and export counters are left at their maxima).  The counting
-// pass ends in LDS atomics whose results are unused; the barrier the compiler emits after them
-// does not wait for them on every path, and without the wait some increments were measured to
-// land after the workgroup had read the counts.
-__device__ __forceinline__ void lds_drain_barrier() {
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    __syncthreads();
 }
 
 // Sum of h[0..hi) across one wavefront; every lane receives it.
@@ -286,7 +301,7 @@ __device__ __forceinline__ int32_t wave_sum(const int32_t* h, int hi, int lane) 
 // member mask) in its bucket.  Each workgroup scans the bucket counts into bucket offsets
 // itself (a few hundred words from L2).  Two passes over the slots: count per bucket, reserve
 // the workgroup's range of each bucket with one atomic on the bucket's cursor, then write.
-template <int W>
+template <int W, int C>
 __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     __shared__ int32_t lcount[2 * (HX_MAX_GPUS + 1)];
     __shared__ int32_t lbase[2 * (HX_MAX_GPUS + 1)];
@@ -315,6 +330,17 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     const int n = blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
+    // The first chunk of slots is loaded once and serves both passes (every slot, when
+    // Kmax <= C); later chunks are loaded in each pass.
+    int rl0[C];
+    uint64_t m0[C][W];
+#pragma unroll
+    for (int x = 0; x < C; ++x) {
+        const bool in = n < N && x < Kmax;
+        rl0[x] = in ? p.role[(int64_t)x * N + n] : HX_UNUSED;
+#pragma unroll
+        for (int i = 0; i < W; ++i) m0[x][i] = in ? wk.gmask[((int64_t)x * W + i) * N + n] : 0;
+    }
     for (int pass = 0; pass < 2; ++pass) {
         if (pass == 1) {
             lds_drain_barrier();
@@ -325,18 +351,19 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
             __syncthreads();
         }
         if (n >= N) continue;
-        for (int k0 = 0; k0 < Kmax; k0 += kSlotChunk) {
-            int rl[kSlotChunk];
-            uint64_t m[kSlotChunk][W];
+        for (int k0 = 0; k0 < Kmax; k0 += C) {
+            int rl[C];
+            uint64_t m[C][W];
 #pragma unroll
-            for (int x = 0; x < kSlotChunk; ++x) {
+            for (int x = 0; x < C; ++x) {
                 const bool in = k0 + x < Kmax;
-                rl[x] = in ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
+                rl[x] = k0 == 0 ? rl0[x] : (in ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED);
 #pragma unroll
-                for (int i = 0; i < W; ++i) m[x][i] = in ? wk.gmask[((int64_t)(k0 + x) * W + i) * N + n] : 0;
+                for (int i = 0; i < W; ++i)
+                    m[x][i] = k0 == 0 ? m0[x][i] : (in ? wk.gmask[((int64_t)(k0 + x) * W + i) * N + n] : 0);
             }
 #pragma unroll
-            for (int x = 0; x < kSlotChunk; ++x) {
+            for (int x = 0; x < C; ++x) {
                 int size = 0;
 #pragma unroll
                 for (int i = 0; i < W; ++i) size += __popcll(m[x][i]);
@@ -641,8 +668,21 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     int bs = 256;
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)p.Kmax * W * bs * 8;
-    hipLaunchKernelGGL(decode_kernel<W>, dim3((p.N + bs - 1) / bs), dim3(bs), lds_dec, s, p, o, wk);
-    hipLaunchKernelGGL(scatter_kernel<W>, dim3((p.N + 255) / 256), dim3(256), 0, s, p, wk);
+    const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
+    switch (slot_chunk(W, p.Kmax)) {
+        case 8:
+            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk);
+            break;
+        case 16:
+            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk);
+            break;
+        default:
+            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk);
+            break;
+    }
     const bool tables = p.G <= kTableMaxG;
     // A grid-stride loop over the units: enough workgroups to fill the chip several times.
     // 256 lanes per workgroup amortise the staged tables; the per-lane member columns take

@@ -26,6 +26,13 @@
 // the source) are recomputed every few rounds by label-correcting sweeps (global relabel).
 // A candidate is done when none of its nodes has excess: the preflow is then a maximum flow.
 //
+// Shortcuts (single-wavefront plans).  Nodes that can carry nothing (a = 0 or b = 0) leave
+// most networks trivial.  If one side has a single node that can, the network is a star and
+// its maximum flow has a closed form (with a flow that fills the star's arcs in node order).
+// If only the value is wanted and the smaller side has m <= kEnumMax such nodes, the minimum
+// cut is taken over the 2^m ways to split that side.  Push-relabel runs for the rest; every
+// path gives the unique maximum-flow value.
+//
 // Outputs: the flow value, the flow on every KV edge, and the canonical minimum cut (nodes of
 // the uncontracted network reachable from the source in the residual graph).
 #include "hx_internal.h"
@@ -34,6 +41,9 @@ namespace hx {
 namespace {
 
 constexpr int kGlobalRelabelEvery = 2;  // rounds between exact relabels
+// Largest smaller side whose 2^m minimum-cut subsets are enumerated when only the flow value
+// is wanted (64 subsets over a candidate's lanes).
+constexpr int kEnumMax = 6;
 constexpr int kPackedLanes = 64;  // workgroup size for packed segments: one wavefront
 
 struct MfLayout {
@@ -216,6 +226,104 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
     }
     __syncthreads();
 
+    // One side with a single node that can carry flow (a > 0 on the prefill side, b > 0 on
+    // the decode side) makes the network a star: with prefill node i alone the maximum flow
+    // is min(a_i, sum_j min(c_ij, b_j)), with decode node j alone min(b_j, sum_i min(a_i,
+    // c_ij)).  Such a candidate takes that value and a flow that fills the star's arcs in
+    // node order (a prefix sum over the candidate's lanes), and skips push-relabel; the cut
+    // sweep below works from any maximum flow.  Only the single-wavefront plans do this.
+    // The shuffles below stay inside a candidate's lanes, whose branches agree.
+    int32_t cut_value = -1;  // the flow value when a minimum cut was taken directly
+    if (SEG <= 64) {
+        const uint64_t segmask = SEG == 64 ? ~0ull : ((1ull << SEG) - 1);
+        const int sh = (seg * SEG) & 63;
+        const uint64_t ba = (__ballot(l < P && L.a[l] > 0) >> sh) & segmask;
+        const uint64_t bb = (__ballot(l < D && L.b[l] > 0) >> sh) & segmask;
+        const bool one_p = __popcll(ba) == 1, one_d = __popcll(bb) == 1;
+        if (has_flow && (one_p || one_d)) {
+            const int is = __ffsll((unsigned long long)ba) - 1, js = __ffsll((unsigned long long)bb) - 1;
+            int32_t v = 0;
+            if (one_p) {
+                if (l < D && L.b[l] > 0) {
+                    const int32_t c = L.cap[is * Ds + l];
+                    v = c < L.b[l] ? c : L.b[l];
+                }
+            } else if (l < P && L.a[l] > 0) {
+                const int32_t c = L.cap[l * Ds + js];
+                v = c < L.a[l] ? c : L.a[l];
+            }
+            int32_t incl = v;
+#pragma unroll
+            for (int off = 1; off < SEG; off <<= 1) {
+                const int32_t u = __shfl_up(incl, off, SEG);
+                if (l >= off) incl += u;
+            }
+            const int32_t total = __shfl(incl, SEG - 1, SEG);
+            const int32_t side = one_p ? L.a[is] : L.b[js];
+            const int32_t F = total < side ? total : side;
+            const int32_t room = F - (incl - v);
+            const int32_t fv = room <= 0 ? 0 : (room < v ? room : v);
+            if (one_p) {
+                if (l < D) {
+                    L.fl[is * Ds + l] = fv;
+                    L.ft[l] = fv;
+                }
+                if (l == is) L.fs[is] = F;
+            } else {
+                if (l < P) {
+                    L.fl[l * Ds + js] = fv;
+                    L.fs[l] = fv;
+                }
+                if (l == js) L.ft[js] = F;
+            }
+            if (l < P) L.ep[l] = 0;
+        } else if (has_flow && kv_flow == nullptr && cut == nullptr) {
+            // Only the value is wanted: with m = min(P', D') <= kEnumMax nodes that can carry
+            // flow on the smaller side, take the minimum cut directly.  Fixing which of those
+            // nodes stay on the source side (a subset A of the prefill side, say) leaves every
+            // other node one cheapest choice: cut = sum_{i not in A} a_i + sum_j min(b_j,
+            // sum_{i in A} c_ij); the maximum flow is the minimum over the 2^m subsets, which
+            // the candidate's lanes share.
+            const int pe = __popcll(ba), de = __popcll(bb);
+            const int m = pe <= de ? pe : de;
+            if (m <= kEnumMax) {
+                const bool byp = pe <= de;
+                const uint64_t side = byp ? ba : bb, other = byp ? bb : ba;
+                int32_t best = 0x7fffffff;
+                for (int sub = l; sub < (1 << m); sub += SEG) {
+                    int32_t cost = 0;
+                    uint64_t rest = side;
+                    for (int k = 0; rest; ++k, rest &= rest - 1)
+                        if (!((sub >> k) & 1)) {
+                            const int u = __ffsll((unsigned long long)rest) - 1;
+                            cost += byp ? L.a[u] : L.b[u];
+                        }
+                    for (uint64_t ow = other; ow; ow &= ow - 1) {
+                        const int w = __ffsll((unsigned long long)ow) - 1;
+                        int32_t arcs = 0;
+                        uint64_t in = side;
+                        for (int k = 0; in; ++k, in &= in - 1)
+                            if ((sub >> k) & 1) {
+                                const int u = __ffsll((unsigned long long)in) - 1;
+                                arcs += byp ? L.cap[u * Ds + w] : L.cap[w * Ds + u];
+                            }
+                        const int32_t cw = byp ? L.b[w] : L.a[w];
+                        cost += cw < arcs ? cw : arcs;
+                    }
+                    best = cost < best ? cost : best;
+                }
+#pragma unroll
+                for (int off = SEG / 2; off > 0; off >>= 1) {
+                    const int32_t o2 = __shfl_xor(best, off, SEG);
+                    best = o2 < best ? o2 : best;
+                }
+                cut_value = best;
+                if (l < P) L.ep[l] = 0;
+            }
+        }
+        __syncthreads();
+    }
+
     const int V = P + D + 2;
     const int INF = 2 * V + 2;
     bool active = false;
@@ -303,7 +411,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
         if (L.ft[j] > 0) atomicAdd(&L.misc[0], L.ft[j]);
     if (active) L.misc[1] = 1;
     __syncthreads();
-    if (valid && l == 0) flow_value[n] = L.misc[1] ? HX_ENOCONV : L.misc[0];
+    if (valid && l == 0) flow_value[n] = cut_value >= 0 ? cut_value : (L.misc[1] ? HX_ENOCONV : L.misc[0]);
     if (valid && kv_flow)
         for (int e = l; e < P * D; e += SEG) {
             const int i = e / D, d = e - i * D;

@@ -168,6 +168,8 @@ def test_refinement_round1(torch):
 # ------------------------------------------------------------------ max-flow alone
 
 def _maxflow_on(torch, fn):
+    """Max-flow of host networks twice: with the flow assignment and cut, and value only (the
+    value-only call may take minimum cuts directly); both values must agree."""
     nb = hx.FlowNetBuffers.from_host(fn)
     N = fn["n_p"].shape[0]
     mp, md, mpd = fn["dims"]
@@ -175,8 +177,12 @@ def _maxflow_on(torch, fn):
     kv = torch.zeros((mpd, N), dtype=torch.int32, device="cuda")
     cut = torch.zeros((mp + md, N), dtype=torch.uint8, device="cuda")
     hx.maxflow_batch(nb, fv, kv, cut)
+    fv_only = torch.full((N,), -12345, dtype=torch.int32, device="cuda")
+    hx.maxflow_batch(nb, fv_only)
     torch.cuda.synchronize()
-    return fv.cpu().numpy(), kv.cpu().numpy(), cut.cpu().numpy()
+    fv_h = fv.cpu().numpy()
+    assert np.array_equal(fv_only.cpu().numpy(), fv_h), "value-only max-flow differs"
+    return fv_h, kv.cpu().numpy(), cut.cpu().numpy()
 
 
 def _adversarial_networks(rng):
@@ -251,13 +257,15 @@ def test_maxflow_random_networks(torch, mp, md, total, N):
 
 
 def test_maxflow_round_budget_reports_noconv(torch, monkeypatch):
-    """A round budget of 1 (set from the host) stops every candidate that needs more rounds
-    with HX_ENOCONV; every workgroup still exits normally."""
-    prob = I.make_problem(3, n_cand=512)
+    """A round budget of 1 (set from the host) stops every candidate that needs more
+    push-relabel rounds with HX_ENOCONV; every workgroup still exits normally.  Flows are
+    requested, so only star networks skip push-relabel; the 64-GPU workload has plenty of
+    others."""
+    prob = I.make_problem(4, n_cand=512)
     want = oracle_all(prob)
     monkeypatch.setenv("HX_MAXFLOW_ROUND_BUDGET", "1")
     say("round budget 1")
-    got = run_gpu(torch, prob, flows=False)
+    got = run_gpu(torch, prob, flows=True)
     fv = got["flow_value"]
     assert set(np.unique(fv)) <= set(np.unique(want["flow_value"])) | {hx.HX_ENOCONV}
     assert (fv == hx.HX_ENOCONV).any()
