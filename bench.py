@@ -8,10 +8,11 @@ model with lognormal request lengths, 65,536 seeded random candidates of 2-16 gr
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 3] [--no-cpu-baseline]
 
-Prints ONE JSON line.  Per-kernel durations come from HIP events recorded around every call
-inside the timed region, on the stream the kernels run on; the roofline object reports the
-kernel with the largest share.  The CPU baseline times the oracle (test infrastructure, not
-the product) on the same batch on the host's cores.
+Prints ONE JSON line.  Per-call durations come from HIP events recorded around every call
+inside the timed region, on the stream the kernels run on; per-kernel durations from a second
+pass of the same steps with libhx's diagnostic per-kernel events (hx_profile).  The roofline
+object reports the kernel with the largest share.  The CPU baseline times the oracle (test
+infrastructure, not the product) on the same batch on the host's cores.
 """
 from __future__ import annotations
 
@@ -32,14 +33,19 @@ METRIC = "candidate placements scored/sec (cost model + max-flow) at 1 GPU; % HB
 # MI355X (gfx950) peaks: 256 CUs at 2.4 GHz.
 HBM_PEAK_GBS = 8000.0
 LDS_PEAK_GBS = 128 * 256 * 2.4          # 128 B/clk/CU -> 78,643 GB/s
-FP64_VALU_PEAK_TFLOPS = 78.6
+# FP64 vector operations that are not fused multiply-adds: 256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz = 39,322 G op/s (the 78.6 TFLOP/s headline counts an FMA as two).
+FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 
-# HBM bytes per launch of the max-flow kernel at workload 3, from rocprofv3 FETCH_SIZE and
-# WRITE_SIZE passes (profiles/all_kernels_workload3.md), each scaled by what the counter reads
-# for a 256 MiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for the kernel
-# source they were taken on (first 16 hex digits of its SHA-256); otherwise traffic is null.
-MAXFLOW_TRAFFIC = {"source_sha256_16": "68896aad8bb1c1e6", "fetch_kib": 13355.0, "write_kib": 256.4,
-                   "fetch_scale": 2.0, "write_scale": 1.0}
+# HBM bytes per launch at workload 3 from rocprofv3 FETCH_SIZE and WRITE_SIZE passes
+# (profiles/all_kernels_workload3.md), each scaled by what the counter reads for a 256 MiB
+# device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for the kernel source they were
+# taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
+COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
+KERNEL_TRAFFIC = {}
+KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
+                 "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
+                 "best": "hx_best.hip"}
 
 
 def parse():
@@ -79,15 +85,79 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
     return dict(cost=cost, flownet=flownet, maxflow=maxflow, best=best)
 
 
-def maxflow_traffic(workload: int):
-    """Counter-measured HBM bytes per max-flow launch, or None when they do not apply."""
+def kernel_traffic(kernel: str, workload: int):
+    """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply."""
     import hashlib
-    src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", "hx_maxflow.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    t = MAXFLOW_TRAFFIC
-    if workload != 3 or sha != t["source_sha256_16"]:
+    t = KERNEL_TRAFFIC.get(kernel)
+    if t is None or workload != 3:
         return None
-    return 1024.0 * (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"])
+    src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", KERNEL_SOURCE[kernel])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != t["source_sha256_16"]:
+        return None
+    return 1024.0 * (t["fetch_kib"] * COUNTER_SCALE["fetch"] + t["write_kib"] * COUNTER_SCALE["write"])
+
+
+def group_members(prob):
+    """(members [U][size] ascending GPU ids, role [U]) of every present group, listed by size."""
+    G, K, N = prob.n_gpus, prob.max_groups, prob.n_cand
+    g, n = np.nonzero(prob.assign < K)
+    k = prob.assign[g, n].astype(np.int64)
+    order = np.lexsort((g, k, n))
+    g, n, k = g[order], n[order], k[order]
+    key = n * K + k
+    starts = np.flatnonzero(np.concatenate([[True], key[1:] != key[:-1]]))
+    sizes = np.diff(np.concatenate([starts, [len(key)]]))
+    role = prob.role[k[starts], n[starts]]
+    keep = (role == 0) | (role == 1)
+    out = {}
+    for sz in np.unique(sizes[keep]):
+        sel = starts[keep & (sizes == sz)]
+        mem = g[sel[:, None] + np.arange(sz)[None, :]]
+        out[int(sz)] = (mem, role[keep & (sizes == sz)])
+    return out
+
+
+def eval_fp64_ops(prob) -> float:
+    """Algorithmic FP64 operations of the strategy-evaluation kernel (Table 1 rows as written,
+    each add, multiply, divide, min or max one operation; prefill link terms, which do not
+    depend on the candidate, count one add each).  Every admissible strategy costs its memory
+    row; a strategy whose memory row admits a batch of 1 costs the full latency sum."""
+    m = prob.model
+    L = m["n_layers"]
+    H = float(m["hidden"])
+    Hkv = float(m["hidden"] * m["n_kv_heads"] // m["n_heads"])
+    B = float(m["bytes_per_elem"])
+    W12 = 12.0 * H * H * B
+    Kkv = 2.0 * (prob.s_in + prob.s_out) * Hkv * B
+    Kact = 4.0 * (prob.s_in + prob.s_out) * H * B
+    cl = prob.cluster
+    gmem = np.asarray(cl.type_mem, np.float64)[np.asarray(cl.gpu_type)]
+    tps = [t for t in range(1, 9) if (prob.tp_mask >> (t - 1)) & 1]
+    total = 0.0
+    for sz, (mem, role) in group_members(prob).items():
+        dec = role == 1
+        for tp in tps:
+            if sz % tp:
+                continue
+            pp = sz // tp
+            if pp > 8 or not (prob.pp_mask >> (pp - 1)) & 1 or pp > L:
+                continue
+            bmin = np.full(len(mem), 2.0 ** 30)
+            for j in range(pp):
+                l = L // pp + (1 if j < L % pp else 0)
+                A = (W12 / tp) * l
+                Kj = (Kkv / tp) * l + Kact
+                mm = gmem[mem[:, j * tp:(j + 1) * tp]].min(axis=1)
+                bmin = np.minimum(bmin, np.floor((mm - A) / Kj))
+            feas = bmin >= 1.0
+            total += len(mem) * pp * (tp + 8)
+            nf_d = int((feas & dec).sum())
+            nf_p = int((feas & ~dec).sum())
+            common = 4 + 4 + pp * (2 + (tp - 1) + 2) + 3
+            pre = common + pp * (3 + tp * (tp - 1) + 2) + (pp - 1) * (tp * tp + 1)
+            dcd = common + pp * ((tp - 1) + 7 + 4 * tp * (tp - 1) + 3) + (pp - 1) * (3 * tp * tp + 2)
+            total += nf_p * pre + nf_d * dcd
+    return float(total)
 
 
 def main():
@@ -146,24 +216,45 @@ def main():
                   for i, k in enumerate(names)}
     value = prob.n_cand / (ms_per_step / 1000.0)
 
+    # Per-kernel durations: the same steps again with libhx recording HIP events around each of
+    # its kernels on this stream (kept out of the timed region above).
+    hx.profile(True)
+    for _ in range(args.steps):
+        hx.score(dp, ws)
+    torch.cuda.synchronize()
+    prof = hx.profile_read()
+    hx.profile(False)
+    kernel_us = {k: 1000.0 * ms / n for k, (ms, n) in prof.items() if n > 0}
+
     # Roofline of the kernel with the largest share of the step.
     n_p = ws.net.n_p.cpu().numpy()
     n_d = ws.net.n_d.cpu().numpy()
     dims = ws.net.dims
     best = [int(x) for x in ws.best.cpu().numpy()]
-    dominant = max(per_kernel, key=per_kernel.get)
+    dominant = max(kernel_us, key=kernel_us.get)
+    t_dom = kernel_us[dominant] * 1e-6
     hbm = hbm_bytes_per_step(prob, dims, n_p, n_d)
-    if dominant == "maxflow":
+    if dominant == "eval":
+        ops = eval_fp64_ops(prob)
+        achieved = ops / t_dom / 1e9
+        roof = {"kernel": "eval (hx_cost_eval)", "bound": "alu", "achieved": achieved, "peak": FP64_VALU_PEAK_GOPS,
+                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", args.workload),
+                "algorithmic_flops_per_launch": ops}
+    elif dominant == "maxflow":
         alg = float(lds_floor_bytes(n_p, n_d).sum())
-        achieved = alg / (per_kernel["maxflow"] / 1000.0) / 1e9
-        roof = {"kernel": "hx_maxflow_batch (maxflow_kernel)", "bound": "lds", "achieved": achieved,
+        achieved = alg / t_dom / 1e9
+        roof = {"kernel": "maxflow (hx_maxflow_batch)", "bound": "lds", "achieved": achieved,
                 "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
-                "traffic": maxflow_traffic(args.workload), "algorithmic_bytes_per_launch": alg}
+                "traffic": kernel_traffic("maxflow", args.workload), "algorithmic_bytes_per_launch": alg}
     else:
-        alg = float(hbm[dominant])
-        achieved = alg / (per_kernel[dominant] / 1000.0) / 1e9
+        call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(dominant,
+                                                                                                          dominant)
+        alg = float(hbm[call])
+        achieved = alg / t_dom / 1e9
         roof = {"kernel": dominant, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_launch": alg}
+                "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, args.workload),
+                "algorithmic_bytes_per_launch": alg}
+    roof["avg_launch_us"] = kernel_us[dominant]
 
     out = {
         "metric": METRIC,
@@ -181,6 +272,7 @@ def main():
         "config": {"workload": f"workload{wl.cfg}: {wl.name}", "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity},
         "kernel_ms": per_kernel,
+        "kernel_us": kernel_us,
         "hbm_bytes_per_step": hbm,
         "best": best,
         "roofline": roof,

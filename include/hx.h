@@ -174,6 +174,9 @@ int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, 
 /* Maximum source-sink flow of every candidate's network (Sec. 3.3, solved there by
  * preflow-push), by a synchronous push-relabel on the network with each replica's
  * in -> out chain contracted, one workgroup per candidate with the residual graph in LDS.
+ * Networks where one side has a single node that can carry flow take a closed form; when
+ * kv_flow and cut are both null, networks whose smaller side has at most 6 such nodes take
+ * the minimum cut directly.  Every path gives the same (unique) flow value.
  *   flow_value [N]       the maximum flow (or HX_ENOCONV)
  *   kv_flow    [max_pd][N] nullable: one maximum flow's value on every KV edge (not unique)
  *   cut        [max_p + max_d][N] nullable: the canonical minimum cut, the nodes reachable from
@@ -186,6 +189,19 @@ int hx_maxflow_batch(const hx_flownet *net, int32_t *flow_value, int32_t *kv_flo
 /* The candidate with the highest flow_value (Sec. 3.1 objective), lowest index on ties.
  * best = device int32[2]: {index, value}.  n_cand >= 1. */
 int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, hipStream_t stream);
+
+/* Diagnostic per-kernel timing (not part of the scoring path; process-global, for one host
+ * thread).  hx_profile(1) clears earlier records and makes every later launch by libhx record a
+ * HIP event on the call's stream before and after each of its kernels; hx_profile(0) stops
+ * recording.  hx_profile_read waits for the recorded events and fills ms[k] (total
+ * milliseconds) and launches[k] for kernel k = 0 .. n-1 since the last hx_profile call, then
+ * clears the records; n >= HX_KERNELS.  Returns HX_KERNELS or a negative error.  hx_kernel_name
+ * gives kernel k's name: setup, decode, scatter, eval (hx_cost_eval), nodes, kv
+ * (hx_build_flownet), maxflow, best. */
+#define HX_KERNELS 8
+int hx_profile(int32_t enable);
+int hx_profile_read(double *ms, int32_t *launches, int32_t n);
+const char *hx_kernel_name(int32_t k);
 
 /* Human-readable text of a return code, and the last HIP error message kept by HX_EHIP. */
 const char *hx_strerror(int code);

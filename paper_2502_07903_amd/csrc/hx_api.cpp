@@ -116,9 +116,132 @@ int32_t round_budget() {
     return 1 << 22;
 }
 
+static_assert(hx::kKCount == HX_KERNELS, "kernel ids and HX_KERNELS disagree");
+
+// Diagnostic per-kernel timing (hx_profile): HIP event pairs recorded around every launch
+// while enabled, from a pool that grows as needed.  Process-global, for one host thread.
+struct Profile {
+    bool on = false;
+    hipEvent_t open[hx::kKCount] = {};
+    struct Pair {
+        int k;
+        hipEvent_t b, e;
+    };
+    Pair* pairs = nullptr;
+    size_t n = 0, cap = 0;
+    hipEvent_t* pool = nullptr;
+    size_t npool = 0, cappool = 0;
+};
+Profile g_prof;
+
+// Timing-only events: no system-scope fence when they are recorded, so that recording one
+// does not write back and invalidate caches between the kernels it brackets.
+hipEvent_t prof_event() {
+    if (g_prof.npool) return g_prof.pool[--g_prof.npool];
+    hipEvent_t e = nullptr;
+    return hipEventCreateWithFlags(&e, hipEventDisableSystemFence) == hipSuccess ? e : nullptr;
+}
+
+void prof_release(hipEvent_t e) {
+    if (!e) return;
+    if (g_prof.npool == g_prof.cappool) {
+        const size_t c = g_prof.cappool ? 2 * g_prof.cappool : 64;
+        hipEvent_t* q = static_cast<hipEvent_t*>(realloc(g_prof.pool, c * sizeof(hipEvent_t)));
+        if (!q) {
+            hipEventDestroy(e);
+            return;
+        }
+        g_prof.pool = q;
+        g_prof.cappool = c;
+    }
+    g_prof.pool[g_prof.npool++] = e;
+}
+
+void prof_clear() {
+    for (size_t i = 0; i < g_prof.n; ++i) {
+        prof_release(g_prof.pairs[i].b);
+        prof_release(g_prof.pairs[i].e);
+    }
+    g_prof.n = 0;
+    for (int k = 0; k < hx::kKCount; ++k) {
+        prof_release(g_prof.open[k]);
+        g_prof.open[k] = nullptr;
+    }
+}
+
 }  // namespace
 
+namespace hx {
+
+void prof_mark(int k, bool end, hipStream_t s) {
+    if (!g_prof.on || k < 0 || k >= kKCount) return;
+    hipEvent_t e = prof_event();
+    if (!e || hipEventRecord(e, s) != hipSuccess) {
+        prof_release(e);
+        return;
+    }
+    if (!end) {
+        prof_release(g_prof.open[k]);
+        g_prof.open[k] = e;
+        return;
+    }
+    if (!g_prof.open[k]) {
+        prof_release(e);
+        return;
+    }
+    if (g_prof.n == g_prof.cap) {
+        const size_t c = g_prof.cap ? 2 * g_prof.cap : 256;
+        auto* q = static_cast<Profile::Pair*>(realloc(g_prof.pairs, c * sizeof(Profile::Pair)));
+        if (!q) {
+            prof_release(e);
+            return;
+        }
+        g_prof.pairs = q;
+        g_prof.cap = c;
+    }
+    g_prof.pairs[g_prof.n++] = Profile::Pair{k, g_prof.open[k], e};
+    g_prof.open[k] = nullptr;
+}
+
+}  // namespace hx
+
 extern "C" {
+
+int hx_profile(int32_t enable) {
+    prof_clear();
+    g_prof.on = enable != 0;
+    return HX_OK;
+}
+
+int hx_profile_read(double* ms, int32_t* launches, int32_t n) {
+    if (!ms || !launches || n < hx::kKCount) return HX_EINVAL;
+    for (int k = 0; k < hx::kKCount; ++k) {
+        ms[k] = 0.0;
+        launches[k] = 0;
+    }
+    // The events carry no fence, so wait for the device before reading their timestamps.
+    if (g_prof.n) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return hip_error(e);
+    }
+    for (size_t i = 0; i < g_prof.n; ++i) {
+        const auto& q = g_prof.pairs[i];
+        float t = 0.0f;
+        hipError_t e = hipEventSynchronize(q.e);
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, q.b, q.e);
+        if (e != hipSuccess) return hip_error(e);
+        ms[q.k] += t;
+        launches[q.k] += 1;
+    }
+    prof_clear();
+    return hx::kKCount;
+}
+
+const char* hx_kernel_name(int32_t k) {
+    static const char* names[hx::kKCount] = {"setup", "decode", "scatter", "eval", "nodes", "kv", "maxflow", "best"};
+    return k >= 0 && k < hx::kKCount ? names[k] : "";
+}
+
 
 int hx_abi_version(void) { return HX_ABI_VERSION; }
 

@@ -78,7 +78,9 @@ __global__ void __launch_bounds__(kBestBlock) best_kernel(const int32_t* __restr
 }  // namespace
 
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s) {
+    prof_mark(kKBest, false, s);
     hipLaunchKernelGGL(best_kernel, dim3(1), dim3(kBestBlock), 0, s, flow_value, n, best);
+    prof_mark(kKBest, true, s);
     return hipGetLastError();
 }
 

@@ -381,6 +381,24 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     }
 }
 
+// Admissible strategies of a group of c GPUs, bit tp-1 for each tp of the mask dividing c with
+// pp = c/tp in the PP mask and at most L (the strategy list of Sec. 3.2 for that size).
+__device__ __forceinline__ uint8_t admissible(const Problem& p, int c) {
+    uint8_t a = 0;
+    for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
+        if (!((p.tp_mask >> (tp - 1)) & 1u) || c % tp != 0) continue;
+        const int pp = c / tp;
+        if (pp >= 1 && pp <= HX_MAX_PP && ((p.pp_mask >> (pp - 1)) & 1u) && pp <= p.L) a |= (uint8_t)(1u << (tp - 1));
+    }
+    return a;
+}
+
+// c / tp for an admissible strategy (tp divides c <= 255): multiply by ceil(2^16 / tp).
+__device__ __forceinline__ int stage_count(int c, int tp) {
+    constexpr uint32_t kRecip[HX_MAX_TP + 1] = {0, 65536, 32768, 21846, 16384, 13108, 10923, 9363, 8192};
+    return (int)(((uint32_t)c * kRecip[tp]) >> 16);
+}
+
 // ------------------------------------------------------------------ large groups
 
 // Groups of at least kCoopMin GPUs carry a long serial chain of divisions when one lane costs
@@ -419,8 +437,8 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
 
 // One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
 // is false for groups past the last large unit (they still join every wave-level sync).
-__device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, int gl, bool live,
-                          int n, int k, int role, uint64_t mask) {
+__device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, const uint8_t* adm_tab,
+                          int gl, bool live, int n, int k, int role, uint64_t mask) {
     const int G = p.G;
     const int cnt = live ? __popcll(mask) : 0;
     for (int g = gl; g < G && live; g += kCoopLanes)
@@ -434,10 +452,10 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
     bool have = false;
     int best_tp = 0, best_pp = 0;
     double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
+    const uint32_t am = live ? adm_tab[cnt] : 0u;
     for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
-        const bool adm = live && ((p.tp_mask >> (tp - 1)) & 1u) && cnt % tp == 0 && cnt / tp <= HX_MAX_PP &&
-                         ((p.pp_mask >> (cnt / tp - 1)) & 1u) && cnt / tp <= p.L;
-        const int pp = adm ? cnt / tp : 0;
+        const bool adm = (am >> (tp - 1)) & 1u;
+        const int pp = adm ? stage_count(cnt, tp) : 0;
         const double t = (double)tp;
         const int lq = adm ? p.L / pp : 0, lr = adm ? p.L % pp : 0;
         // Memory-limit row, one lane per stage, then the group's minimum (exact).
@@ -543,7 +561,7 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
 }
 
 template <int W, bool kTables, int kEvalBlock>
-__global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
+__global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
     const int G = p.G;
     double* gfl = dsm;
@@ -569,6 +587,9 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
         tb.beta = b;
         tb_end = b + G * G;
     }
+    // Admissible strategies by group size, for every size up to G.
+    __shared__ uint8_t adm_tab[HX_MAX_GPUS + 1];
+    for (int c = threadIdx.x; c <= G; c += kEvalBlock) adm_tab[c] = admissible(p, c);
     // Units in all: the sum of the bucket counts.  Units before the (size kCoopMin - 1)
     // buckets are the large groups (sizes descend).
     __shared__ int32_t counts[2];
@@ -606,7 +627,7 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
                 role = (int)(w & 0xFF);
                 mask = rec[1];
             }
-            coop_unit(p, tb, o, c, gl, live, n, k, role, mask);
+            coop_unit(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
@@ -626,10 +647,9 @@ __global__ void __launch_bounds__(kEvalBlock) eval_kernel(Problem p, CostOut o, 
         bool have = false;
         int best_tp = 0, best_pp = 0;
         double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
-        for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
-            if (!((p.tp_mask >> (tp - 1)) & 1u) || cnt % tp != 0) continue;
-            const int pp = cnt / tp;
-            if (pp > HX_MAX_PP || !((p.pp_mask >> (pp - 1)) & 1u) || pp > p.L) continue;
+        for (uint32_t am = adm_tab[cnt]; am; am &= am - 1) {
+            const int tp = __ffs(am);
+            const int pp = stage_count(cnt, tp);
             StrategyCost sc;
             if (!cost_any(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
             const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
@@ -662,7 +682,9 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
         const int64_t cells = (int64_t)(HX_MAX_TP + 1) * p.G * p.G;
         const int64_t want = (cells > 2 * nb + 1 ? cells : 2 * nb + 1) + 255;
         const int blocks = (int)(want / 256 < 1024 ? want / 256 : 1024);
+        prof_mark(kKSetup, false, s);
         hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1);
+        prof_mark(kKSetup, true, s);
     }
     // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS
     int bs = 256;
@@ -671,16 +693,28 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
     switch (slot_chunk(W, p.Kmax)) {
         case 8:
+            prof_mark(kKDecode, false, s);
             hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            prof_mark(kKDecode, true, s);
+            prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk);
+            prof_mark(kKScatter, true, s);
             break;
         case 16:
+            prof_mark(kKDecode, false, s);
             hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            prof_mark(kKDecode, true, s);
+            prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk);
+            prof_mark(kKScatter, true, s);
             break;
         default:
+            prof_mark(kKDecode, false, s);
             hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            prof_mark(kKDecode, true, s);
+            prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk);
+            prof_mark(kKScatter, true, s);
             break;
     }
     const bool tables = p.G <= kTableMaxG;
@@ -693,6 +727,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
                             (size_t)p.G * eb + (W == 1 ? (size_t)(eb / kCoopLanes) * coop_group_bytes(p.G) : 0);
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
+    prof_mark(kKEval, false, s);
     if (eb == 256) {
         if (tables)
             hipLaunchKernelGGL((eval_kernel<W, true, 256>), dim3(blocks), dim3(256), lds_eval, s, p, o, wk, nb);
@@ -701,6 +736,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     } else {
         hipLaunchKernelGGL((eval_kernel<W, false, 128>), dim3(blocks), dim3(128), lds_eval, s, p, o, wk, nb);
     }
+    prof_mark(kKEval, true, s);
     return hipGetLastError();
 }
 

@@ -215,11 +215,15 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
 
 template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
+    prof_mark(kKNodes, false, s);
     hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
+    prof_mark(kKNodes, true, s);
     const int64_t lanes = (int64_t)f.max_pd * p.N;
     const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
     const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
+    prof_mark(kKKv, false, s);
     hipLaunchKernelGGL(kv_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    prof_mark(kKKv, true, s);
     return hipGetLastError();
 }
 

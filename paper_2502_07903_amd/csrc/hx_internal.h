@@ -47,6 +47,12 @@ __device__ __forceinline__ double dmax(double a, double b) { return b > a ? b : 
 // Layers held by stage j of pp: floor(L/pp) + [j < L mod pp].
 __device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
 
+// Kernels of libhx, for the diagnostic per-kernel timing behind hx_profile.
+enum KernelId { kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKCount };
+// While profiling is enabled, records a HIP event on s before (end = false) or after
+// (end = true) a launch of kernel k; does nothing otherwise.
+void prof_mark(int k, bool end, hipStream_t s);
+
 // 64-bit words of a GPU bitmask: 1 up to 64 GPUs, 2 up to 128, 4 up to 255.
 int mask_words(int32_t n_gpus);
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);

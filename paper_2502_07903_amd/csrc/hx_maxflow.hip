@@ -499,7 +499,9 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
     const size_t lds = kPer * mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
     const int tiles = (f.N + kPer - 1) / kPer;
     const int blocks = 8 * ((tiles + 7) / 8);
+    prof_mark(kKMaxflow, false, s);
     hipLaunchKernelGGL(maxflow_kernel<SEG>, dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget);
+    prof_mark(kKMaxflow, true, s);
     return hipGetLastError();
 }
 

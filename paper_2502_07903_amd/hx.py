@@ -68,7 +68,9 @@ class hx_flownet(C.Structure):
 
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
-           "hx_maxflow_batch", "hx_best_candidate", "hx_strerror", "hx_last_error", "hx_abi_version")
+           "hx_maxflow_batch", "hx_best_candidate", "hx_profile", "hx_profile_read", "hx_kernel_name",
+           "hx_strerror", "hx_last_error", "hx_abi_version")
+HX_KERNELS = 8
 
 _lib = None
 
@@ -93,12 +95,33 @@ def lib() -> C.CDLL:
                                        P(hx_cost_out), P(hx_flownet), C.c_void_p]
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_best_candidate.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+        L.hx_profile.argtypes = [C.c_int32]
+        L.hx_profile.restype = C.c_int
+        L.hx_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
+        L.hx_profile_read.restype = C.c_int
+        L.hx_kernel_name.argtypes = [C.c_int32]
+        L.hx_kernel_name.restype = C.c_char_p
         L.hx_strerror.restype = C.c_char_p
         L.hx_strerror.argtypes = [C.c_int]
         L.hx_last_error.restype = C.c_char_p
         L.hx_abi_version.restype = C.c_int
         _lib = L
     return _lib
+
+
+def profile(enable: bool) -> None:
+    """Diagnostic per-kernel timing: HIP events around every later libhx kernel launch."""
+    _check(lib().hx_profile(1 if enable else 0), "hx_profile")
+
+
+def profile_read() -> Dict[str, Tuple[float, int]]:
+    """{kernel name: (total ms, launches)} since the last profile() call; clears the records."""
+    ms = (C.c_double * HX_KERNELS)()
+    n = (C.c_int32 * HX_KERNELS)()
+    rc = lib().hx_profile_read(C.cast(ms, C.c_void_p), C.cast(n, C.c_void_p), HX_KERNELS)
+    if rc < 0:
+        _check(rc, "hx_profile_read")
+    return {lib().hx_kernel_name(k).decode(): (float(ms[k]), int(n[k])) for k in range(HX_KERNELS)}
 
 
 def strerror(code: int) -> str:

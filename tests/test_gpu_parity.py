@@ -385,3 +385,21 @@ def test_exhaustive_search_best():
     want = hxo.score_batch(prob, n_threads=N_THREADS)
     assert np.array_equal(got["flow_value"], want["flow_value"])
     assert got["best"] == want["best"]
+
+
+def test_profile_counts_each_kernel(torch):
+    """The diagnostic per-kernel timing sees every kernel of one pass exactly once, with a
+    positive duration, and records nothing once disabled."""
+    prob = I.make_problem(2, n_cand=1000)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp)
+    hx.profile(True)
+    hx.score(dp, ws)
+    prof = hx.profile_read()
+    hx.profile(False)
+    assert set(prof) == {"setup", "decode", "scatter", "eval", "nodes", "kv", "maxflow", "best"}
+    for name, (ms, n) in prof.items():
+        assert n == 1 and ms > 0.0, (name, ms, n)
+    hx.score(dp, ws)
+    torch.cuda.synchronize()
+    assert all(n == 0 for _, n in hx.profile_read().values())
