@@ -42,7 +42,16 @@ FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 # device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for the kernel source they were
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
-KERNEL_TRAFFIC = {}
+KERNEL_TRAFFIC = {
+    "setup": {"source_sha256_16": "2fe02144148e6483", "fetch_kib": 37.7, "write_kib": 32.5},
+    "decode": {"source_sha256_16": "2fe02144148e6483", "fetch_kib": 1635.8, "write_kib": 22443.6},
+    "scatter": {"source_sha256_16": "2fe02144148e6483", "fetch_kib": 4679.0, "write_kib": 9337.1},
+    "eval": {"source_sha256_16": "2fe02144148e6483", "fetch_kib": 5310.8, "write_kib": 65706.0},
+    "nodes": {"source_sha256_16": "5fbd4e7404ecfaea", "fetch_kib": 6697.6, "write_kib": 20441.6},
+    "kv": {"source_sha256_16": "5fbd4e7404ecfaea", "fetch_kib": 5895.5, "write_kib": 13399.1},
+    "maxflow": {"source_sha256_16": "092d98a1f13d354c", "fetch_kib": 16706.6, "write_kib": 256.0},
+    "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.3, "write_kib": 0.0},
+}
 KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
                  "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
                  "best": "hx_best.hip"}
