@@ -682,3 +682,258 @@ int hxo_score_batch(const hxo_cluster *c, const hxo_model *m, const hxo_workload
     free(jobs); free(th);
     return hxo_best_candidate(flow_value, n_cand, best);
 }
+
+/* ------------------------------------------------------------------ refinement (Sec. 3.4) */
+
+/*
+ * Max-flow guided refinement (Sec. 3.4).  The paper compares every edge's flow with its
+ * capacity: a bottleneck edge carries flow at its capacity and holds the total back, an
+ * underutilized edge carries less than it could; GPUs are then swapped between groups to
+ * relieve the one with the other, the new partition is scored again, and the loop stops when
+ * nothing improves.  A maximum flow assignment is not unique, so the two properties are taken
+ * here in the form every maximum flow agrees on (the same for any solver):
+ *   bottleneck     raising the edge's capacity by one raises the maximum flow;
+ *   underutilized  the capacity is >= 1 and lowering it by one keeps the maximum flow.
+ * For an edge u -> v with flow f of capacity c in one maximum flow, in that flow's residual
+ * graph (arc u -> v when f < c, arc v -> u when f > 0):
+ *   bottleneck     iff s reaches u and v reaches t (the extra unit is the only way through);
+ *   underutilized  iff c >= 1 and (f < c, or u reaches v: the residual cycle through v -> u
+ *                  moves one unit off the edge without changing the value).
+ */
+
+/* reach[u * nv + v] = 1 when v is reachable from u in the residual graph of the flow fl on
+ * the edge list (from, to, cp); every vertex reaches itself. */
+static void residual_reach(int nv, int ne, const int32_t *from, const int32_t *to, const int64_t *cp,
+                           const int64_t *fl, uint8_t *reach)
+{
+    int *queue = (int *)malloc(sizeof(int) * nv);
+    memset(reach, 0, (size_t)nv * nv);
+    for (int src = 0; src < nv; src++) {
+        uint8_t *seen = reach + (size_t)src * nv;
+        int qh = 0, qt = 0;
+        seen[src] = 1;
+        queue[qt++] = src;
+        while (qh < qt) {
+            int u = queue[qh++];
+            for (int e = 0; e < ne; e++) {
+                int w = -1;
+                if (from[e] == u && fl[e] < cp[e]) w = to[e];
+                else if (to[e] == u && fl[e] > 0) w = from[e];
+                if (w >= 0 && !seen[w]) { seen[w] = 1; queue[qt++] = w; }
+            }
+        }
+    }
+    free(queue);
+}
+
+static uint8_t edge_class(int nv, const uint8_t *reach, int s, int t, int u, int v, int64_t f, int64_t c)
+{
+    uint8_t k = 0;
+    if (reach[(size_t)s * nv + u] && reach[(size_t)v * nv + t]) k |= 1;
+    if (c >= 1 && (f < c || reach[(size_t)u * nv + v])) k |= 2;
+    return k;
+}
+
+/* Edge classes of every candidate's Sec. 3.3 network (same layout as hxo_maxflow_batch's
+ * inputs).  node_cls[i][n] for prefill node i, node_cls[max_p + j][n] for decode node j:
+ * bit 0 / bit 1 = the node edge (in -> out) is a bottleneck / underutilized, bit 2 / bit 3 =
+ * the same for its coordinator edge (source -> in, resp. out -> sink), bit 4 = a KV edge at the
+ * node is a bottleneck.  kv_cls[i*n_d + j][n]: bit 0 / bit 1 for the KV edge of prefill i and
+ * decode j.  Rows past the counts are left. */
+int hxo_edge_classes(int32_t n_cand, int32_t max_p, int32_t max_d, int32_t max_pd,
+                     const int32_t *n_p, const int32_t *n_d, const int32_t *src_cap, const int32_t *p_cap,
+                     const int32_t *kv_cap, const int32_t *d_cap, const int32_t *sink_cap,
+                     uint8_t *node_cls, uint8_t *kv_cls)
+{
+    const int N = n_cand;
+    const int maxv = 2 + 2 * (max_p + max_d);
+    const int maxe = max_p * 2 + max_d * 2 + max_pd;
+    int32_t *from = (int32_t *)malloc(sizeof(int32_t) * (maxe + 1));
+    int32_t *to = (int32_t *)malloc(sizeof(int32_t) * (maxe + 1));
+    int64_t *cp = (int64_t *)malloc(sizeof(int64_t) * (maxe + 1));
+    int64_t *fl = (int64_t *)malloc(sizeof(int64_t) * (maxe + 1));
+    uint8_t *reach = (uint8_t *)malloc((size_t)maxv * maxv);
+    for (int n = 0; n < N; n++) {
+        const int P = n_p[n], D = n_d[n];
+        const int nv = 2 + 2 * (P + D);
+        int ne = 0;
+        /* the same vertex and edge numbering as the max-flow above */
+        for (int i = 0; i < P; i++) {
+            int64_t o = (int64_t)i * N + n;
+            from[ne] = 0; to[ne] = 2 + 2 * i; cp[ne++] = src_cap[o];
+            from[ne] = 2 + 2 * i; to[ne] = 3 + 2 * i; cp[ne++] = p_cap[o];
+        }
+        const int kv0 = ne;
+        for (int i = 0; i < P; i++)
+            for (int j = 0; j < D; j++) {
+                from[ne] = 3 + 2 * i; to[ne] = 2 + 2 * P + 2 * j;
+                cp[ne++] = kv_cap[(int64_t)(i * D + j) * N + n];
+            }
+        const int d0 = ne;
+        for (int j = 0; j < D; j++) {
+            int64_t o = (int64_t)j * N + n;
+            from[ne] = 2 + 2 * P + 2 * j; to[ne] = 3 + 2 * P + 2 * j; cp[ne++] = d_cap[o];
+            from[ne] = 3 + 2 * P + 2 * j; to[ne] = 1; cp[ne++] = sink_cap[o];
+        }
+        hxo_maxflow_edges(nv, ne, from, to, cp, 0, 1, fl, NULL);
+        residual_reach(nv, ne, from, to, cp, fl, reach);
+        for (int i = 0; i < P; i++) {
+            const int es = 2 * i, en = 2 * i + 1;
+            uint8_t k = edge_class(nv, reach, 0, 1, from[en], to[en], fl[en], cp[en]);
+            k |= (uint8_t)(edge_class(nv, reach, 0, 1, from[es], to[es], fl[es], cp[es]) << 2);
+            node_cls[(int64_t)i * N + n] = k;
+        }
+        for (int j = 0; j < D; j++) {
+            const int en = d0 + 2 * j, et = d0 + 2 * j + 1;
+            uint8_t k = edge_class(nv, reach, 0, 1, from[en], to[en], fl[en], cp[en]);
+            k |= (uint8_t)(edge_class(nv, reach, 0, 1, from[et], to[et], fl[et], cp[et]) << 2);
+            node_cls[(int64_t)(max_p + j) * N + n] = k;
+        }
+        for (int e = 0; e < P * D; e++) {
+            const uint8_t k = edge_class(nv, reach, 0, 1, from[kv0 + e], to[kv0 + e], fl[kv0 + e], cp[kv0 + e]);
+            kv_cls[(int64_t)e * N + n] = k;
+            if (k & 1) {
+                node_cls[(int64_t)(e / D) * N + n] |= 16;
+                node_cls[(int64_t)(max_p + e % D) * N + n] |= 16;
+            }
+        }
+    }
+    free(from); free(to); free(cp); free(fl); free(reach);
+    return 0;
+}
+
+/* Index into a list of m entries from a b-bit uniform draw u: floor(u * m / 2^b). */
+static int pick_index(uint64_t u, int m, int bits) { return (int)((u * (uint64_t)m) >> bits); }
+
+/*
+ * Guided moves (Sec. 3.4): the children of a batch of parent placements.  Child c descends
+ * from parent c mod n_par; children 0 .. n_par-1 are the parents themselves, so the best
+ * child of a batch is never worse than its parent and a batch whose best is a parent has
+ * found no improvement.  Every other child applies one move, read from the parent's edge
+ * classes (hxo_edge_classes of the parent's own network):
+ *   a GPU is a donor when it is unused or the node edge of its flow node is underutilized;
+ *   a group is a receiver when the node edge of one of its members' flow nodes, or a KV
+ *   edge at one of them, is a bottleneck;
+ *   a group may flip its role when it is no receiver, all its members are donors, and some
+ *   receiver has the other role.
+ * (A member's flow node is its group's replica node, or at per-GPU granularity its own.)
+ *   MOVE  a donor GPU outside the receiver joins a receiver group;
+ *   SWAP  a GPU of a receiver group and a donor GPU of another group (or unused) trade places;
+ *   FLIP  a flip-eligible group takes the other role.
+ * Random draws come from rnd[c]: bits 0-15 choose the first move type tried (MOVE, SWAP,
+ * FLIP in turn after it, the first that has a choice is applied), bits 16-39 the receiver
+ * (MOVE: a receiver group; SWAP: a GPU of any receiver group; FLIP: a flip-eligible group),
+ * bits 40-63 the donor GPU among those allowed; each choice is the floor(u*m/2^b)-th of the
+ * m candidates in ascending id.  move[c] = type | a << 8 | b << 16: 0 none, 1 MOVE (a GPU,
+ * b group), 2 SWAP (a, b GPUs), 3 FLIP (a group).
+ */
+int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
+                     int32_t n_par, const uint8_t *p_assign, const uint8_t *p_role,
+                     int32_t max_p, const int32_t *n_p, const int32_t *n_d,
+                     const int32_t *p_slot, const int32_t *d_slot, const uint8_t *node_cls, const uint8_t *kv_cls,
+                     int32_t n_child, const uint64_t *rnd, uint8_t *c_assign, uint8_t *c_role, int32_t *move)
+{
+    const int G = n_gpus, K = max_groups, M = n_par;
+    int grp[256], node_row[256], donor[256], recv_grp[256], flip_ok[256], members[256];
+    int recv_list[256], donor_list[256], recv_gpu_list[256], flip_list[256];
+    for (int c = 0; c < n_child; c++) {
+        const int m = c % M;
+        for (int g = 0; g < G; g++) c_assign[(int64_t)g * n_child + c] = p_assign[(int64_t)g * M + m];
+        for (int k = 0; k < K; k++) c_role[(int64_t)k * n_child + c] = p_role[(int64_t)k * M + m];
+        move[c] = 0;
+        if (c < M) continue;
+
+        /* the parent's groups: a GPU belongs to group a = assign when a < K has a valid role */
+        for (int k = 0; k < K; k++) members[k] = 0;
+        for (int g = 0; g < G; g++) {
+            const int a = p_assign[(int64_t)g * M + m];
+            const int r = a < K ? p_role[(int64_t)a * M + m] : HXO_UNUSED;
+            grp[g] = (a < K && (r == HXO_PREFILL || r == HXO_DECODE)) ? a : -1;
+            if (grp[g] >= 0) members[grp[g]]++;
+        }
+        /* flow node of each GPU: the row of its node in the parent's network (prefill i ->
+         * row i, decode j -> row max_p + j), or -1 */
+        const int P = n_p[m], D = n_d[m];
+        for (int g = 0; g < G; g++) {
+            node_row[g] = -1;
+            if (grp[g] < 0) continue;
+            const int key = granularity == 0 ? grp[g] : g;
+            const int r = p_role[(int64_t)grp[g] * M + m];
+            if (r == HXO_PREFILL) {
+                for (int i = 0; i < P; i++)
+                    if (p_slot[(int64_t)i * M + m] == key) node_row[g] = i;
+            } else {
+                for (int j = 0; j < D; j++)
+                    if (d_slot[(int64_t)j * M + m] == key) node_row[g] = max_p + j;
+            }
+        }
+        /* donors and receivers */
+        for (int k = 0; k < K; k++) recv_grp[k] = 0;
+        for (int g = 0; g < G; g++) {
+            donor[g] = grp[g] < 0;
+            if (node_row[g] < 0) continue;
+            const int row = node_row[g];
+            const uint8_t nc = node_cls[(int64_t)row * M + m];
+            if (nc & 2) donor[g] = 1;
+            int bott = nc & 1;
+            if (row < max_p) {
+                for (int j = 0; j < D; j++)
+                    if (kv_cls[(int64_t)(row * D + j) * M + m] & 1) bott = 1;
+            } else {
+                for (int i = 0; i < P; i++)
+                    if (kv_cls[(int64_t)(i * D + (row - max_p)) * M + m] & 1) bott = 1;
+            }
+            if (bott) recv_grp[grp[g]] = 1;
+        }
+        int recv_role_seen[2] = {0, 0};
+        for (int k = 0; k < K; k++)
+            if (recv_grp[k]) recv_role_seen[p_role[(int64_t)k * M + m]] = 1;
+        for (int k = 0; k < K; k++) flip_ok[k] = members[k] > 0 && !recv_grp[k];
+        for (int g = 0; g < G; g++)
+            if (grp[g] >= 0 && !donor[g]) flip_ok[grp[g]] = 0;
+        for (int k = 0; k < K; k++)
+            if (flip_ok[k] && !recv_role_seen[1 - p_role[(int64_t)k * M + m]]) flip_ok[k] = 0;
+        int n_recv = 0, n_donor = 0, n_rg = 0, n_flip = 0;
+        for (int k = 0; k < K; k++) {
+            if (recv_grp[k]) recv_list[n_recv++] = k;
+            if (flip_ok[k]) flip_list[n_flip++] = k;
+        }
+        for (int g = 0; g < G; g++) {
+            if (donor[g]) donor_list[n_donor++] = g;
+            if (grp[g] >= 0 && recv_grp[grp[g]]) recv_gpu_list[n_rg++] = g;
+        }
+
+        const uint64_t r = rnd[c];
+        const uint64_t u0 = r & 0xFFFF, u1 = (r >> 16) & 0xFFFFFF, u2 = r >> 40;
+        const int t0 = pick_index(u0, 3, 16);
+        for (int attempt = 0; attempt < 3 && move[c] == 0; attempt++) {
+            const int t = (t0 + attempt) % 3;
+            if (t == 0 && n_recv > 0) {
+                const int k = recv_list[pick_index(u1, n_recv, 24)];
+                int allowed[256], na = 0;
+                for (int x = 0; x < n_donor; x++)
+                    if (grp[donor_list[x]] != k) allowed[na++] = donor_list[x];
+                if (na == 0) continue;
+                const int g = allowed[pick_index(u2, na, 24)];
+                c_assign[(int64_t)g * n_child + c] = (uint8_t)k;
+                move[c] = 1 | (g << 8) | (k << 16);
+            } else if (t == 1 && n_rg > 0) {
+                const int g = recv_gpu_list[pick_index(u1, n_rg, 24)];
+                int allowed[256], na = 0;
+                for (int x = 0; x < n_donor; x++)
+                    if (grp[donor_list[x]] != grp[g]) allowed[na++] = donor_list[x];
+                if (na == 0) continue;
+                const int h = allowed[pick_index(u2, na, 24)];
+                const uint8_t ag = p_assign[(int64_t)g * M + m], ah = p_assign[(int64_t)h * M + m];
+                c_assign[(int64_t)g * n_child + c] = ah;
+                c_assign[(int64_t)h * n_child + c] = ag;
+                move[c] = 2 | (g << 8) | (h << 16);
+            } else if (t == 2 && n_flip > 0) {
+                const int k = flip_list[pick_index(u1, n_flip, 24)];
+                c_role[(int64_t)k * n_child + c] = (uint8_t)(1 - p_role[(int64_t)k * M + m]);
+                move[c] = 3 | (k << 8);
+            }
+        }
+    }
+    return 0;
+}

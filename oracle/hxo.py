@@ -231,3 +231,40 @@ def maxflow_edges(nv: int, edges: List[Tuple[int, int, int]], s: int, t: int):
     v = lib().hxo_maxflow_edges(C.c_int32(nv), C.c_int32(ne), _p(fr), _p(to), _p(cp), C.c_int32(s),
                                 C.c_int32(t), _p(fl), _p(reach))
     return int(v), fl[:ne].copy(), reach.astype(bool)
+
+
+# ------------------------------------------------------------------ refinement (Sec. 3.4)
+
+def edge_classes(f) -> Dict[str, np.ndarray]:
+    """Bottleneck (bit 0) / underutilized (bit 1) classes of every edge of every network.
+
+    node_cls [max_p + max_d][N]: node edges in bits 0-1, coordinator edges in bits 2-3;
+    kv_cls [max_pd][N]: KV edges.  Rows past a network's counts stay 0.
+    """
+    mp, md, mpd = f["dims"]
+    N = f["n_p"].shape[0]
+    node = np.zeros((mp + md, N), np.uint8)
+    kv = np.zeros((mpd, N), np.uint8)
+    lib().hxo_edge_classes(C.c_int32(N), C.c_int32(mp), C.c_int32(md), C.c_int32(mpd),
+                           *(_p(f[k]) for k in ("n_p", "n_d", "src_cap", "p_cap", "kv_cap", "d_cap",
+                                                "sink_cap")),
+                           _p(node), _p(kv))
+    return dict(node_cls=node, kv_cls=kv)
+
+
+def guided_moves(n_gpus: int, max_groups: int, granularity: int, p_assign: np.ndarray, p_role: np.ndarray,
+                 f, cls: Dict[str, np.ndarray], rnd: np.ndarray) -> Dict[str, np.ndarray]:
+    """Children of the parent placements (columns of p_assign / p_role, scored into network f
+    with edge classes cls): child c descends from parent c mod M; one guided move each."""
+    M = p_assign.shape[1]
+    mp = f["dims"][0]
+    rnd = np.ascontiguousarray(rnd, np.uint64)
+    Nc = rnd.shape[0]
+    out = dict(assign=np.zeros((n_gpus, Nc), np.uint8), role=np.zeros((max_groups, Nc), np.uint8),
+               move=np.zeros(Nc, np.int32))
+    lib().hxo_guided_moves(C.c_int32(n_gpus), C.c_int32(max_groups), C.c_int32(granularity), C.c_int32(M),
+                           _p(np.ascontiguousarray(p_assign, np.uint8)), _p(np.ascontiguousarray(p_role, np.uint8)),
+                           C.c_int32(mp), _p(f["n_p"]), _p(f["n_d"]), _p(f["p_slot"]), _p(f["d_slot"]),
+                           _p(cls["node_cls"]), _p(cls["kv_cls"]), C.c_int32(Nc), _p(rnd),
+                           _p(out["assign"]), _p(out["role"]), _p(out["move"]))
+    return out

@@ -391,6 +391,15 @@ def make_problem(cfg: int, n_cand: Optional[int] = None, rnd: int = 0,
                    wl.max_groups, assign, role)
 
 
+GUIDED_STREAM = 1 << 20   # seed stream of guided refinement round r: GUIDED_STREAM + r
+
+
+def move_draws(cfg: int, rnd: int, n: int) -> np.ndarray:
+    """The uniform 64-bit draws of guided refinement round rnd of workload cfg, one per child
+    (the move generator takes its random choices from them)."""
+    return _rng(cfg, GUIDED_STREAM + rnd).integers(0, 2**64, size=n, dtype=np.uint64, endpoint=False)
+
+
 def placement_from_groups(groups: List[List[int]], roles: List[int], n_gpus: int,
                           max_groups: int) -> Tuple[np.ndarray, np.ndarray]:
     """One candidate from explicit groups (lists of GPU ids) and roles, as [G][1] / [Kmax][1]."""
