@@ -15,6 +15,12 @@
  *   hx_maxflow_batch   maximum flow, flow assignment, min cut    (one lane per node, LDS-resident)
  *   hx_best_candidate  the best candidate                        (one workgroup)
  *
+ * and the max-flow guided refinement step of Sec. 3.4 that feeds the next batch:
+ *
+ *   hx_edge_classes       bottleneck / underutilized edges        (one workgroup per candidate)
+ *   hx_guided_moves       children of the best placements          (one lane per child)
+ *   hx_gather_candidates  the chosen candidates into a new batch   (one lane per byte)
+ *
  * Conventions
  *   - Every array pointer is a DEVICE pointer unless marked [host].  The caller owns every
  *     buffer; libhx allocates no device memory and keeps no state between calls.
@@ -190,6 +196,58 @@ int hx_maxflow_batch(const hx_flownet *net, int32_t *flow_value, int32_t *kv_flo
  * best = device int32[2]: {index, value}.  n_cand >= 1. */
 int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, hipStream_t stream);
 
+/* ---------------------------------------------------------------- refinement (Sec. 3.4)
+ * The refinement step compares each edge's flow with its capacity and swaps GPUs between groups
+ * so that underutilized capacity relieves bottlenecks, then scores the new partitions again;
+ * it stops when no new partition scores higher.  A flow assignment is not unique, so the edge
+ * classes are taken in the form every maximum flow agrees on:
+ *   bottleneck     raising the edge's capacity by one raises the maximum flow;
+ *   underutilized  its capacity is >= 1 and lowering it by one keeps the maximum flow. */
+
+/* Edge classes of every candidate's network, from one maximum flow of it (flow_value and
+ * kv_flow as written by hx_maxflow_batch with kv_flow requested; node flows follow by
+ * conservation).  One workgroup per candidate.
+ *   node_cls [max_p + max_d][N]: row i < max_p prefill node i, row max_p + j decode node j;
+ *            bit 0 / 1 = its node edge (in -> out) is a bottleneck / underutilized, bit 2 / 3 =
+ *            the same for its coordinator edge (source -> in, out -> sink), bit 4 = a KV edge at
+ *            the node is a bottleneck.
+ *   kv_cls   [max_pd][N]: row i*n_d + j, bit 0 / 1 for the KV edge of prefill i and decode j.
+ * Rows past a network's counts are not written.  A candidate with flow_value < 0, counts
+ * outside the plan, or more than 255 nodes (n_p + n_d > 255: the closure's LDS rows) gets
+ * node_cls 0 in every row and no kv_cls. */
+int hx_edge_classes(const hx_flownet *net, const int32_t *flow_value, const int32_t *kv_flow, uint8_t *node_cls,
+                    uint8_t *kv_cls, hipStream_t stream);
+
+/* Guided moves: n_child children of the M = parents->n_cand (<= 65535) parent placements, whose network
+ * (parent_net, built for this batch of M) and node classes (hx_edge_classes) are given.  Child c
+ * descends from parent c mod M; children 0 .. M-1 are the parents unchanged (move 0), so a
+ * scored batch's best is never worse than its parent.  Every other child applies one move:
+ *   a GPU is a donor when it is unused, or the node edge of its flow node is underutilized
+ *   (its flow node: its group's replica node, or its own node at granularity 1);
+ *   a group is a receiver when a member's flow node has a bottleneck node edge or KV edge;
+ *   a group may flip when it is no receiver, every member is a donor, and a receiver has the
+ *   other role.
+ *   MOVE (1)  a donor GPU outside the receiver joins a receiver group;
+ *   SWAP (2)  a GPU of a receiver group and a donor GPU of another group (or unused) exchange
+ *             their assign entries;
+ *   FLIP (3)  a flip-eligible group takes the other role.
+ * rnd[c] (uniform 64-bit draws, [n_child]) chooses: bits 0-15 the first type tried (u*3/2^16;
+ * the next types in turn when it has no choice), bits 16-39 the receiver (MOVE: a receiver group,
+ * SWAP: a GPU of a receiver group, FLIP: a flip-eligible group), bits 40-63 the donor GPU among
+ * those allowed; each choice is entry floor(u*m/2^b) of the m candidates in ascending id.
+ * A child with no possible move copies its parent (move 0).
+ *   child_assign [n_gpus][n_child], child_role [max_groups][n_child]: written;
+ *   move [n_child]: type | a << 8 | b << 16 (MOVE: GPU a, group b; SWAP: GPUs a, b; FLIP: group a). */
+int hx_guided_moves(int32_t n_gpus, int32_t granularity, const hx_candidates *parents, const hx_flownet *parent_net,
+                    const uint8_t *node_cls, int32_t n_child, const uint64_t *rnd, uint8_t *child_assign,
+                    uint8_t *child_role, int32_t *move, hipStream_t stream);
+
+/* dst column m = src column index[m] for m < count (index: device int32[count], e.g. the best
+ * index of hx_best_candidate); an index outside [0, src->n_cand) gives a column of HX_UNUSED.
+ *   dst_assign [n_gpus][count], dst_role [src->max_groups][count]. */
+int hx_gather_candidates(int32_t n_gpus, const hx_candidates *src, const int32_t *index, int32_t count,
+                         uint8_t *dst_assign, uint8_t *dst_role, hipStream_t stream);
+
 /* Diagnostic per-kernel timing (not part of the scoring path; process-global, for one host
  * thread).  hx_profile(1) clears earlier records and makes every later launch by libhx record a
  * HIP event on the call's stream before and after each of its kernels; hx_profile(0) stops
@@ -197,8 +255,9 @@ int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, 
  * milliseconds) and launches[k] for kernel k = 0 .. n-1 since the last hx_profile call, then
  * clears the records; n >= HX_KERNELS.  Returns HX_KERNELS or a negative error.  hx_kernel_name
  * gives kernel k's name: setup, decode, scatter, eval (hx_cost_eval), nodes, kv
- * (hx_build_flownet), maxflow, best. */
-#define HX_KERNELS 8
+ * (hx_build_flownet), maxflow, best, classes (hx_edge_classes), moves (hx_guided_moves),
+ * gather (hx_gather_candidates). */
+#define HX_KERNELS 11
 int hx_profile(int32_t enable);
 int hx_profile_read(double *ms, int32_t *launches, int32_t n);
 const char *hx_kernel_name(int32_t k);

@@ -148,7 +148,7 @@ void prof_release(hipEvent_t e) {
         const size_t c = g_prof.cappool ? 2 * g_prof.cappool : 64;
         hipEvent_t* q = static_cast<hipEvent_t*>(realloc(g_prof.pool, c * sizeof(hipEvent_t)));
         if (!q) {
-            hipEventDestroy(e);
+            (void)hipEventDestroy(e);
             return;
         }
         g_prof.pool = q;
@@ -238,7 +238,8 @@ int hx_profile_read(double* ms, int32_t* launches, int32_t n) {
 }
 
 const char* hx_kernel_name(int32_t k) {
-    static const char* names[hx::kKCount] = {"setup", "decode", "scatter", "eval", "nodes", "kv", "maxflow", "best"};
+    static const char* names[hx::kKCount] = {"setup",   "decode", "scatter", "eval",  "nodes", "kv",
+                                             "maxflow", "best",   "classes", "moves", "gather"};
     return k >= 0 && k < hx::kKCount ? names[k] : "";
 }
 
@@ -309,6 +310,44 @@ int hx_maxflow_batch(const hx_flownet* net, int32_t* flow_value, int32_t* kv_flo
 int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, hipStream_t stream) {
     if (!flow_value || !best || n_cand < 1) return HX_EINVAL;
     hipError_t e = hx::launch_best(flow_value, n_cand, best, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_edge_classes(const hx_flownet* net, const int32_t* flow_value, const int32_t* kv_flow, uint8_t* node_cls,
+                    uint8_t* kv_cls, hipStream_t stream) {
+    int rc = check_net_shape(net);
+    if (rc) return rc;
+    if (!flow_value || !kv_flow || !node_cls || !kv_cls) return HX_EINVAL;
+    hipError_t e = hx::launch_classes(make_net(net), flow_value, kv_flow, node_cls, kv_cls, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_guided_moves(int32_t n_gpus, int32_t granularity, const hx_candidates* parents, const hx_flownet* parent_net,
+                    const uint8_t* node_cls, int32_t n_child, const uint64_t* rnd, uint8_t* child_assign,
+                    uint8_t* child_role, int32_t* move, hipStream_t stream) {
+    if (n_gpus < 1 || n_gpus > HX_MAX_GPUS || (granularity != 0 && granularity != 1)) return HX_EINVAL;
+    if (!parents || parents->n_cand < 1 || parents->max_groups < 1 || parents->max_groups > HX_MAX_GROUPS ||
+        !parents->assign || !parents->role)
+        return HX_EINVAL;
+    int rc = check_net_shape(parent_net);
+    if (rc) return rc;
+    if (!parent_net->p_slot || !parent_net->d_slot || parent_net->n_cand != parents->n_cand) return HX_EINVAL;
+    if (parents->n_cand > 65535) return HX_EINVAL;  // one grid row per parent
+    if (!node_cls || !rnd || !child_assign || !child_role || !move || n_child < 1) return HX_EINVAL;
+    hipError_t e = hx::launch_moves(n_gpus, parents->max_groups, granularity, parents->n_cand, parents->assign,
+                                    parents->role, make_net(parent_net), node_cls, n_child, rnd, child_assign,
+                                    child_role, move, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_gather_candidates(int32_t n_gpus, const hx_candidates* src, const int32_t* index, int32_t count,
+                         uint8_t* dst_assign, uint8_t* dst_role, hipStream_t stream) {
+    if (n_gpus < 1 || n_gpus > HX_MAX_GPUS || !src || src->n_cand < 1 || src->max_groups < 1 ||
+        src->max_groups > HX_MAX_GROUPS || !src->assign || !src->role)
+        return HX_EINVAL;
+    if (!index || count < 1 || !dst_assign || !dst_role) return HX_EINVAL;
+    hipError_t e = hx::launch_gather(n_gpus, src->max_groups, src->n_cand, src->assign, src->role, index, count,
+                                     dst_assign, dst_role, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

@@ -48,7 +48,9 @@ __device__ __forceinline__ double dmax(double a, double b) { return b > a ? b : 
 __device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
 
 // Kernels of libhx, for the diagnostic per-kernel timing behind hx_profile.
-enum KernelId { kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKCount };
+enum KernelId {
+    kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKClasses, kKMoves, kKGather, kKCount
+};
 // While profiling is enabled, records a HIP event on s before (end = false) or after
 // (end = true) a launch of kernel k; does nothing otherwise.
 void prof_mark(int k, bool end, hipStream_t s);
@@ -63,5 +65,16 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
                           int32_t op_budget, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
+
+// Refinement (Sec. 3.4): edge classes of networks of at most kClsMaxV vertices, guided moves,
+// and the column gather.
+constexpr int kClsMaxV = 512;
+hipError_t launch_classes(const FlowNet& f, const int32_t* flow_value, const int32_t* kv_flow, uint8_t* node_cls,
+                          uint8_t* kv_cls, hipStream_t s);
+hipError_t launch_moves(int32_t G, int32_t K, int32_t gran, int32_t M, const uint8_t* p_assign,
+                        const uint8_t* p_role, const FlowNet& pn, const uint8_t* node_cls, int32_t n_child,
+                        const uint64_t* rnd, uint8_t* c_assign, uint8_t* c_role, int32_t* move, hipStream_t s);
+hipError_t launch_gather(int32_t G, int32_t K, int32_t Ns, const uint8_t* sa, const uint8_t* sr, const int32_t* index,
+                         int32_t count, uint8_t* da, uint8_t* dr, hipStream_t s);
 
 }  // namespace hx

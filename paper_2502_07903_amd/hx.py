@@ -5,6 +5,10 @@ HIP kernels of libhx.so.  The functions keep the C names:
 
     cost_eval, build_flownet, maxflow_batch, best_candidate, validate
 
+the refinement calls of Sec. 3.4
+
+    edge_classes, guided_moves, gather_candidates
+
 and `DeviceProblem` uploads a seeded `inputs.Problem` once so that repeated calls read
 device-resident inputs.  There is no fallback: without the built library or a GPU every
 call raises.
@@ -68,9 +72,9 @@ class hx_flownet(C.Structure):
 
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
-           "hx_maxflow_batch", "hx_best_candidate", "hx_profile", "hx_profile_read", "hx_kernel_name",
-           "hx_strerror", "hx_last_error", "hx_abi_version")
-HX_KERNELS = 8
+           "hx_maxflow_batch", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves", "hx_gather_candidates",
+           "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error", "hx_abi_version")
+HX_KERNELS = 11
 
 _lib = None
 
@@ -95,6 +99,11 @@ def lib() -> C.CDLL:
                                        P(hx_cost_out), P(hx_flownet), C.c_void_p]
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_best_candidate.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+        L.hx_edge_classes.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.hx_guided_moves.argtypes = [C.c_int32, C.c_int32, P(hx_candidates), P(hx_flownet), C.c_void_p,
+                                      C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.hx_gather_candidates.argtypes = [C.c_int32, P(hx_candidates), C.c_void_p, C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_void_p]
         L.hx_profile.argtypes = [C.c_int32]
         L.hx_profile.restype = C.c_int
         L.hx_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
@@ -354,3 +363,76 @@ def score(dp: DeviceProblem, ws: Workspace, stream=None) -> None:
     build_flownet(dp, ws.cost, ws.net, stream)
     maxflow_batch(ws.net, ws.flow_value, ws.kv_flow, ws.cut, stream)
     best_candidate(ws.flow_value, ws.best, dp.n_cand, stream)
+
+
+# ------------------------------------------------------------------ refinement (Sec. 3.4)
+
+def edge_classes(net: FlowNetBuffers, flow_value, kv_flow, node_cls, kv_cls, stream=None):
+    """Bottleneck / underutilized classes of every network edge (hx_edge_classes)."""
+    f = net.struct()
+    _check(lib().hx_edge_classes(C.byref(f), _ptr(flow_value), _ptr(kv_flow), _ptr(node_cls), _ptr(kv_cls),
+                                 _stream(stream)), "hx_edge_classes")
+    return node_cls, kv_cls
+
+
+def guided_moves(parents: DeviceProblem, parent_net: FlowNetBuffers, node_cls, rnd, child_assign, child_role, move,
+                 stream=None):
+    """Children of the parent batch, one guided move each (hx_guided_moves)."""
+    f = parent_net.struct()
+    _check(lib().hx_guided_moves(C.c_int32(parents.n_gpus), C.c_int32(int(parents.space.granularity)),
+                                 C.byref(parents.cand), C.byref(f), _ptr(node_cls), C.c_int32(int(rnd.shape[0])),
+                                 _ptr(rnd), _ptr(child_assign), _ptr(child_role), _ptr(move), _stream(stream)),
+           "hx_guided_moves")
+    return child_assign, child_role, move
+
+
+def gather_candidates(src: DeviceProblem, index, dst_assign, dst_role, stream=None):
+    """dst column m = src column index[m] (hx_gather_candidates)."""
+    _check(lib().hx_gather_candidates(C.c_int32(src.n_gpus), C.byref(src.cand), _ptr(index),
+                                      C.c_int32(int(index.shape[0])), _ptr(dst_assign), _ptr(dst_role),
+                                      _stream(stream)), "hx_gather_candidates")
+    return dst_assign, dst_role
+
+
+@dataclasses.dataclass
+class Refiner:
+    """Max-flow guided refinement on the device (Sec. 3.4): one parent placement and a batch of
+    n_child children per round.  A round enqueues, with no host synchronisation:
+      1. the parent scored with a flow assignment (cost, network, max-flow with kv_flow) and
+         its edge classes;
+      2. the children (child 0 = the parent) by guided moves;
+      3. the children scored (value only) and the best chosen (lowest index on ties);
+      4. the best child gathered into the parent for the next round.
+    best_value after a round is the parent's new score; a round whose best index is 0 found
+    no improvement."""
+    parent: DeviceProblem
+    parent_ws: Workspace
+    node_cls: object
+    kv_cls: object
+    children: DeviceProblem
+    child_ws: Workspace
+    move: object
+
+    @classmethod
+    def create(cls, dp: DeviceProblem, parent_col: int, n_child: int, device: str = "cuda") -> "Refiner":
+        torch = _torch()
+        pa = dp.tensors["assign"][:, parent_col:parent_col + 1].contiguous()
+        pr = dp.tensors["role"][:, parent_col:parent_col + 1].contiguous()
+        parent = dp.with_candidates(pa, pr)
+        pws = Workspace.for_problem(parent, flows=True, device=device)
+        mp, md, mpd = pws.net.dims
+        ca = torch.empty((dp.n_gpus, n_child), dtype=torch.uint8, device=device)
+        cr = torch.empty((dp.max_groups, n_child), dtype=torch.uint8, device=device)
+        children = dp.with_candidates(ca, cr)
+        return cls(parent, pws, torch.zeros((mp + md, 1), dtype=torch.uint8, device=device),
+                   torch.zeros((mpd, 1), dtype=torch.uint8, device=device), children,
+                   Workspace.for_problem(children, device=device),
+                   torch.empty(n_child, dtype=torch.int32, device=device))
+
+    def round(self, rnd, stream=None) -> None:
+        p, pw, ch, cw = self.parent, self.parent_ws, self.children, self.child_ws
+        score(p, pw, stream)
+        edge_classes(pw.net, pw.flow_value, pw.kv_flow, self.node_cls, self.kv_cls, stream)
+        guided_moves(p, pw.net, self.node_cls, rnd, ch.tensors["assign"], ch.tensors["role"], self.move, stream)
+        score(ch, cw, stream)
+        gather_candidates(ch, cw.best[:1], p.tensors["assign"], p.tensors["role"], stream)

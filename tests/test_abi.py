@@ -117,6 +117,37 @@ def test_calls_reject_before_any_device_work():
     assert L.hx_maxflow_batch(C.byref(big), FAKE, None, None, None) == hx.HX_ETOOBIG
 
 
+def test_refinement_calls_reject_before_any_device_work():
+    cl, md, wl, sp, cand, cost, net = _args()
+    L = hx.lib()
+    u8 = lambda: C.c_void_p(FAKE)
+    assert L.hx_edge_classes(C.byref(net), None, FAKE, FAKE, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_edge_classes(C.byref(net), FAKE, None, FAKE, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_edge_classes(C.byref(net), FAKE, FAKE, None, FAKE, None) == hx.HX_EINVAL
+    bad_net = hx.hx_flownet(0, 1, 1, 1, *([FAKE] * 9))
+    assert L.hx_edge_classes(C.byref(bad_net), FAKE, FAKE, FAKE, FAKE, None) == hx.HX_EINVAL
+    # guided moves: the parents' network must be built for the parent batch
+    par = hx.hx_candidates(3, 16, FAKE, FAKE)
+    pnet = hx.hx_flownet(3, 16, 16, 64, *([FAKE] * 9))
+    ok = (32, 0, C.byref(par), C.byref(pnet), u8(), 100, u8(), u8(), u8(), u8(), None)
+    for i, bad in ((0, 0), (0, 256), (1, 2), (5, 0), (4, None), (6, None), (7, None), (8, None), (9, None)):
+        a = list(ok)
+        a[i] = bad
+        assert L.hx_guided_moves(*a) == hx.HX_EINVAL, (i, bad)
+    pnet.n_cand = 4
+    assert L.hx_guided_moves(*ok) == hx.HX_EINVAL
+    many = hx.hx_candidates(70000, 16, FAKE, FAKE)
+    mnet = hx.hx_flownet(70000, 16, 16, 64, *([FAKE] * 9))
+    assert L.hx_guided_moves(32, 0, C.byref(many), C.byref(mnet), u8(), 100, u8(), u8(), u8(), u8(), None) == \
+        hx.HX_EINVAL
+    # gather
+    src = hx.hx_candidates(10, 16, FAKE, FAKE)
+    assert L.hx_gather_candidates(32, C.byref(src), None, 1, FAKE, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_gather_candidates(32, C.byref(src), FAKE, 0, FAKE, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_gather_candidates(0, C.byref(src), FAKE, 1, FAKE, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_gather_candidates(32, C.byref(src), FAKE, 1, None, FAKE, None) == hx.HX_EINVAL
+
+
 def test_workspace_and_mask_sizes():
     L = hx.lib()
     assert [L.hx_member_words(g) for g in (1, 64, 65, 128, 129, 255)] == [1, 1, 2, 2, 4, 4]
