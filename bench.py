@@ -7,6 +7,12 @@ The default workload is the 32-GPU / 8-node / 4-type cluster serving a Llama-2-7
 model with lognormal request lengths, 65,536 seeded random candidates of 2-16 groups.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 3] [--no-cpu-baseline]
+    python bench.py --refine [--steps 10] [--warmup 2] [--children 131072]
+
+--refine times rounds of the max-flow guided refinement of Sec. 3.4 instead (the 128-GPU
+workload with per-GPU flow nodes): each round scores the parent placement with a flow
+assignment, classifies its edges, emits the children by guided moves, scores them and keeps
+the best; value = children per second.
 
 Prints ONE JSON line.  Per-call durations come from HIP events recorded around every call
 inside the timed region, on the stream the kernels run on; per-kernel durations from a second
@@ -17,6 +23,7 @@ infrastructure, not the product) on the same batch on the host's cores.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -65,6 +72,11 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
+    ap.add_argument("--refine", action="store_true",
+                    help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
+    ap.add_argument("--children", type=int, default=131072, help="children per refinement round (--refine)")
+    ap.add_argument("--quality-rounds", type=int, default=8,
+                    help="--refine: also run this many guided and random-perturbation rounds and report the best")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -169,6 +181,178 @@ def eval_fp64_ops(prob) -> float:
     return float(total)
 
 
+def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
+    """Roofline object of one kernel: FP64 ALU for the strategy evaluation, LDS for the
+    max-flow, HBM for the streaming kernels."""
+    t_dom = kernel_us[dominant] * 1e-6
+    if dominant == "eval":
+        ops = eval_fp64_ops(prob)
+        achieved = ops / t_dom / 1e9
+        roof = {"kernel": "eval (hx_cost_eval)", "bound": "alu", "achieved": achieved, "peak": FP64_VALU_PEAK_GOPS,
+                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", workload),
+                "algorithmic_flops_per_launch": ops}
+    elif dominant == "maxflow":
+        alg = float(lds_floor_bytes(n_p, n_d).sum())
+        achieved = alg / t_dom / 1e9
+        roof = {"kernel": "maxflow (hx_maxflow_batch)", "bound": "lds", "achieved": achieved,
+                "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
+                "traffic": kernel_traffic("maxflow", workload), "algorithmic_bytes_per_launch": alg}
+    else:
+        call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(dominant,
+                                                                                                          dominant)
+        alg = float(hbm[call])
+        achieved = alg / t_dom / 1e9
+        roof = {"kernel": dominant, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, workload),
+                "algorithmic_bytes_per_launch": alg}
+    roof["avg_launch_us"] = kernel_us[dominant]
+    return roof
+
+
+def moves_hbm_bytes(G: int, K: int, n_child: int) -> int:
+    """Algorithmic HBM bytes of one guided-moves launch: every child's assign and role column
+    and move word written, its 8-byte draw read (the parent's few hundred bytes are cached)."""
+    return n_child * (G + K + 4 + 8)
+
+
+def refine_main(args, torch, hx, I):
+    """Max-flow guided refinement rounds (Sec. 3.4) on the 128-GPU workload with per-GPU flow
+    nodes: each round scores the parent with a flow assignment, classifies its edges, emits
+    --children guided children (child 0 = the parent), scores them and keeps the best."""
+    cfg = 5
+    wl = I.WORKLOADS[cfg]
+    base = I.base_placement(wl)
+    prob0 = dataclasses.replace(I.make_problem(cfg, n_cand=1), assign=np.ascontiguousarray(base[0].reshape(-1, 1)),
+                                role=np.ascontiguousarray(base[1].reshape(-1, 1)))
+    n_child = args.children
+    rounds_total = args.warmup + args.steps
+    draws = [torch.as_tensor(I.move_draws(cfg, r, n_child).view(np.int64)).to("cuda") for r in range(rounds_total)]
+    dp = hx.DeviceProblem.upload(prob0)
+    ref = hx.Refiner.create(dp, 0, n_child)
+    trace = []
+    for r in range(args.warmup):
+        ref.round(draws[r])
+        trace.append(int(ref.child_ws.best[1].item()))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for r in range(args.warmup, rounds_total):
+        ref.round(draws[r])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_round = (t1 - t0) * 1000.0 / args.steps
+    value = n_child / (ms_per_round / 1000.0)
+    final = [int(x) for x in ref.child_ws.best.cpu().numpy()]
+
+    # per-kernel durations over a replay of the same rounds from the same start
+    ref2 = hx.Refiner.create(dp, 0, n_child)
+    hx.profile(True)
+    for r in range(rounds_total):
+        ref2.round(draws[r])
+    torch.cuda.synchronize()
+    prof = hx.profile_read()
+    hx.profile(False)
+    kernel_us = {k: 1000.0 * ms / n for k, (ms, n) in prof.items() if n > 0}
+    kernel_ms_per_round = {k: ms / rounds_total for k, (ms, n) in prof.items() if n > 0}
+    child = ref.children
+    cp = dataclasses.replace(prob0, assign=child.tensors["assign"].cpu().numpy(),
+                             role=child.tensors["role"].cpu().numpy())
+    n_p = ref.child_ws.net.n_p.cpu().numpy()
+    n_d = ref.child_ws.net.n_d.cpu().numpy()
+    hbm = hbm_bytes_per_step(cp, ref.child_ws.net.dims, n_p, n_d)
+    hbm["moves"] = moves_hbm_bytes(cp.n_gpus, cp.max_groups, n_child)
+    # the children's scoring kernels run once per round on the full batch; the parent's on one
+    # candidate: the dominant kernel by time per round
+    dominant = max(kernel_ms_per_round, key=kernel_ms_per_round.get)
+    scoring = {"setup", "decode", "scatter", "eval", "nodes", "kv", "maxflow", "best"}
+    if dominant in scoring:
+        # a round launches each scoring kernel twice, on the parent (one candidate) and on the
+        # children; the roofline charges the children's work with both launches' time
+        roof = roofline_for(dominant, {dominant: 1000.0 * kernel_ms_per_round[dominant]}, cp, hbm, n_p, n_d, cfg)
+    else:
+        alg = float(hbm.get(dominant, 0))
+        t = kernel_ms_per_round[dominant] * 1e-3
+        roof = {"kernel": dominant, "bound": "hbm", "achieved": alg / t / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": alg / t / 1e9 / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_launch": alg,
+                "avg_launch_us": 1000.0 * kernel_ms_per_round[dominant]}
+    t_mv = kernel_us["moves"] * 1e-6
+    moves_roof = {"kernel": "moves (hx_guided_moves)", "bound": "hbm", "achieved": hbm["moves"] / t_mv / 1e9,
+                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["moves"] / t_mv / 1e9 / HBM_PEAK_GBS,
+                  "traffic": None, "algorithmic_bytes_per_launch": hbm["moves"], "avg_launch_us": kernel_us["moves"]}
+
+    # quality beside it: random single-step perturbations (the same move kinds, drawn without
+    # the max-flow classes) for the same number of rounds, scored on the GPU
+    rand_best = None
+    if args.quality_rounds > 0:
+        cur = (base[0].copy(), base[1].copy())
+        ws_r = None
+        rand_best = []
+        for r in range(args.quality_rounds):
+            pr = I.make_problem(cfg, n_cand=n_child, rnd=r, base=cur)
+            dpr = hx.DeviceProblem.upload(pr)
+            if ws_r is None:
+                ws_r = hx.Workspace.for_problem(dpr)
+            hx.score(dpr, ws_r)
+            bi, bv = (int(x) for x in ws_r.best.cpu().numpy())
+            rand_best.append(bv)
+            cur = (pr.assign[:, bi].copy(), pr.role[:, bi].copy())
+        ref3 = hx.Refiner.create(dp, 0, n_child)
+        guided_best = []
+        for r in range(args.quality_rounds):
+            ref3.round(draws[r] if r < rounds_total else
+                       torch.as_tensor(I.move_draws(cfg, r, n_child).view(np.int64)).to("cuda"))
+            guided_best.append(int(ref3.child_ws.best[1].item()))
+
+    out = {
+        "metric": "guided refinement children generated and scored/sec (Sec. 3.4 round) at 1 GPU",
+        "value": value,
+        "unit": "children/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_round,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64+i32",
+        "data": "synthetic",
+        "config": {"workload": f"workload{cfg}: {wl.name}, max-flow guided rounds from the one-group-per-node base",
+                   "children_per_round": n_child, "cluster_gpus": cp.n_gpus, "max_groups": cp.max_groups,
+                   "granularity": cp.granularity},
+        "kernel_ms_per_round": kernel_ms_per_round,
+        "best_after_warmup_rounds": trace,
+        "best": final,
+        "roofline": roof,
+        "moves_roofline": moves_roof,
+    }
+    if rand_best is not None:
+        out["quality"] = {"rounds": args.quality_rounds, "guided_best_per_round": guided_best,
+                          "random_best_per_round": rand_best,
+                          "random_best_so_far": [int(x) for x in np.maximum.accumulate(rand_best)]}
+
+    if not args.no_cpu_baseline:
+        from oracle import hxo  # test infrastructure: only this baseline leg uses it
+        cores = max(1, min(len(os.sched_getaffinity(0)), 64))
+        par = prob0
+
+        def oracle_round(n):
+            fn = hxo.build_flownet(par, hxo.cost_eval(par))
+            cls = hxo.edge_classes(fn)
+            rnd_h = I.move_draws(cfg, 0, n)
+            ch = hxo.guided_moves(par.n_gpus, par.max_groups, par.granularity, par.assign, par.role, fn, cls, rnd_h)
+            hxo.score_batch(dataclasses.replace(par, assign=ch["assign"], role=ch["role"]), n_threads=cores)
+        n = 1024
+        t = time.perf_counter()
+        oracle_round(n)
+        first = time.perf_counter() - t
+        n = int(min(n_child, max(1024, n * args.cpu_seconds / max(first, 1e-3))))
+        t = time.perf_counter()
+        oracle_round(n)
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": n / dt, "unit": "children/s", "cores": cores, "kind": "oracle",
+                               "sample": f"round 0 from the base placement with {n} children (of {n_child})"}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -193,6 +377,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.refine:
+        refine_main(args, torch, hx, I)
+        return
     wl = I.WORKLOADS[args.workload]
     prob = I.make_problem(args.workload)
     dp = hx.DeviceProblem.upload(prob)
@@ -241,29 +428,8 @@ def main():
     dims = ws.net.dims
     best = [int(x) for x in ws.best.cpu().numpy()]
     dominant = max(kernel_us, key=kernel_us.get)
-    t_dom = kernel_us[dominant] * 1e-6
     hbm = hbm_bytes_per_step(prob, dims, n_p, n_d)
-    if dominant == "eval":
-        ops = eval_fp64_ops(prob)
-        achieved = ops / t_dom / 1e9
-        roof = {"kernel": "eval (hx_cost_eval)", "bound": "alu", "achieved": achieved, "peak": FP64_VALU_PEAK_GOPS,
-                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", args.workload),
-                "algorithmic_flops_per_launch": ops}
-    elif dominant == "maxflow":
-        alg = float(lds_floor_bytes(n_p, n_d).sum())
-        achieved = alg / t_dom / 1e9
-        roof = {"kernel": "maxflow (hx_maxflow_batch)", "bound": "lds", "achieved": achieved,
-                "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
-                "traffic": kernel_traffic("maxflow", args.workload), "algorithmic_bytes_per_launch": alg}
-    else:
-        call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(dominant,
-                                                                                                          dominant)
-        alg = float(hbm[call])
-        achieved = alg / t_dom / 1e9
-        roof = {"kernel": dominant, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, args.workload),
-                "algorithmic_bytes_per_launch": alg}
-    roof["avg_launch_us"] = kernel_us[dominant]
+    roof = roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, args.workload)
 
     out = {
         "metric": METRIC,

@@ -180,9 +180,12 @@ int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, 
 /* Maximum source-sink flow of every candidate's network (Sec. 3.3, solved there by
  * preflow-push), by a synchronous push-relabel on the network with each replica's
  * in -> out chain contracted, one workgroup per candidate with the residual graph in LDS.
- * Networks where one side has a single node that can carry flow take a closed form; when
- * kv_flow and cut are both null, networks whose smaller side has at most 6 such nodes take
- * the minimum cut directly.  Every path gives the same (unique) flow value.
+ * Closed forms skip push-relabel: networks where one side has a single node that can carry
+ * flow (a star), and networks whose every KV edge can carry min(a_i, b_j) (a_i = min(source,
+ * prefill node) and b_j = min(decode node, sink) capacities), whose maximum flow is
+ * min(sum a, sum b) with the north-west-corner flow; when kv_flow and cut are both null,
+ * networks whose smaller side has at most 6 nodes that can carry flow take the minimum cut
+ * directly.  Every path gives the same (unique) flow value.
  *   flow_value [N]       the maximum flow (or HX_ENOCONV)
  *   kv_flow    [max_pd][N] nullable: one maximum flow's value on every KV edge (not unique)
  *   cut        [max_p + max_d][N] nullable: the canonical minimum cut, the nodes reachable from

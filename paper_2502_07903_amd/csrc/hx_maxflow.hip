@@ -26,12 +26,14 @@
 // the source) are recomputed every few rounds by label-correcting sweeps (global relabel).
 // A candidate is done when none of its nodes has excess: the preflow is then a maximum flow.
 //
-// Shortcuts (single-wavefront plans).  Nodes that can carry nothing (a = 0 or b = 0) leave
-// most networks trivial.  If one side has a single node that can, the network is a star and
+// Shortcuts.  Nodes that can carry nothing (a = 0 or b = 0) leave most networks trivial.
+// Single-wavefront plans: if one side has a single node that can, the network is a star and
 // its maximum flow has a closed form (with a flow that fills the star's arcs in node order).
-// If only the value is wanted and the smaller side has m <= kEnumMax such nodes, the minimum
-// cut is taken over the 2^m ways to split that side.  Push-relabel runs for the rest; every
-// path gives the unique maximum-flow value.
+// Every plan: if every KV arc can carry min(a_i, b_j), the maximum flow is min(sum a, sum b)
+// with the north-west-corner flow (below).  Single-wavefront plans, value only: if the
+// smaller side has m <= kEnumMax nodes that can carry flow, the minimum cut is taken over the
+// 2^m ways to split that side.  Push-relabel runs for the rest; every path gives the unique
+// maximum-flow value.
 //
 // Outputs: the flow value, the flow on every KV edge, and the canonical minimum cut (nodes of
 // the uncontracted network reachable from the source in the residual graph).
@@ -116,13 +118,88 @@ __device__ void global_relabel(const MfLayout& L, int l, int P, int D, int Ds, i
     }
 }
 
+// Dominant KV arcs.  When c_ij >= min(a_i, b_j) on every KV arc, no cut is below
+// U = min(sum a, sum b): a cut keeping prefill set A on the source side costs
+// sum_{i not in A} a_i + sum_j min(b_j, sum_{i in A} c_ij) >= sum_{i not in A} a_i +
+// sum_j min(b_j, S) with S = sum_{i in A} a_i (each term: some a_i >= b_j gives b_j, else
+// c_ij >= a_i for all of A), which is >= sum b when S >= every b_j and >= sum a otherwise.
+// The maximum flow is then U, and the north-west-corner fill is one: with prefix sums A_i of a
+// and B_j of b clamped to U, arc (i, j) carries the overlap of [A_{i-1}, A_i) and
+// [B_{j-1}, B_j), at most min(a_i, b_j) <= c_ij; node i sends A_i - A_{i-1}, node j receives
+// B_j - B_{j-1}.
+__device__ __forceinline__ int32_t nw_overlap(int32_t ae, int32_t ai, int32_t be, int32_t bi) {
+    const int32_t hi = ai < bi ? ai : bi, lo = ae > be ? ae : be;
+    return hi > lo ? hi - lo : 0;
+}
+
+// Value-only pre-pass of the workgroup plans.  Those plans give a workgroup one candidate,
+// whose KV rows then sit in as many cache lines as it has arcs; here one lane per candidate
+// (candidate-fastest, so every row load coalesces across the wavefront) tests the dominant-KV
+// condition on every arc and writes min(sum a, sum b) as the flow value when it holds, 0 when
+// no source-side or no sink-side node can carry flow, and -1 otherwise; maxflow_kernel then
+// solves only the candidates left at -1.  Networks with negative capacities or counts
+// outside the plan are left to maxflow_kernel.
+constexpr int kBoundBlock = 256;
+
+__global__ void __launch_bounds__(kBoundBlock) bound_kernel(FlowNet f, int32_t* flow_value) {
+    const int n = blockIdx.x * kBoundBlock + threadIdx.x;
+    if (n >= f.N) return;
+    const int64_t N = f.N;
+    const int P = f.n_p[n], D = f.n_d[n];
+    int32_t out = -1;
+    if (P >= 0 && D >= 0 && P <= f.max_p && D <= f.max_d && P * D <= f.max_pd) {
+        auto a_of = [&](int i) {
+            const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+            return s < c ? s : c;
+        };
+        auto b_of = [&](int j) {
+            const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+            return c < t ? c : t;
+        };
+        long long sa = 0, sb = 0;
+        bool neg = false, any_a = false, any_b = false;
+        for (int i = 0; i < P; ++i) {
+            const int32_t a = a_of(i);
+            sa += a;
+            neg |= a < 0;
+            any_a |= a > 0;
+        }
+        for (int j = 0; j < D; ++j) {
+            const int32_t b = b_of(j);
+            sb += b;
+            neg |= b < 0;
+            any_b |= b > 0;
+        }
+        if (!neg) {
+            if (!any_a || !any_b) {
+                out = 0;
+            } else {
+                bool dom = true;
+                int i = 0, j = 0;
+                int32_t ai = a_of(0);
+                for (int e = 0; e < P * D && dom; ++e) {
+                    const int32_t c = f.kv_cap[(int64_t)e * N + n];
+                    const int32_t bj = b_of(j);
+                    dom = c >= (ai < bj ? ai : bj);
+                    if (++j == D) {
+                        j = 0;
+                        if (++i < P) ai = a_of(i);
+                    }
+                }
+                if (dom) out = (int32_t)(sa < sb ? sa : sb);
+            }
+        }
+    }
+    flow_value[n] = out;
+}
+
 // SEG lanes per candidate; the workgroup holds max(64, SEG) lanes, i.e. 64/SEG candidates
 // when SEG <= 64.  Workgroups are ordered XCD-aware: the hardware deals consecutive
 // workgroups to the 8 XCDs in turn, so workgroup w takes tile (w mod 8) * chunk + w / 8 and
 // each XCD walks a contiguous candidate range, sharing the L2 lines of the candidate-fastest
 // input arrays.
 template <int SEG>
-__global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
+__global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 : 1)
     maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
@@ -136,6 +213,9 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
     extern __shared__ int32_t smem[];
     const MfLayout L = carve(smem + seg * mf_words(f.max_p, f.max_d, f.max_pd), f.max_p, f.max_d, f.max_pd);
     bool valid = tile < tiles && n < N;
+    // value-only workgroup plans: bound_kernel has already written the candidates it could
+    // (one candidate per workgroup, so the exit is uniform)
+    if (SEG > 64 && kv_flow == nullptr && cut == nullptr && valid && flow_value[n] >= 0) return;
 
     // Packed segments (SEG <= 64) own at most one node row per side and SEG/4 KV rows per
     // lane, so every global load is issued at once, before the counts that say which rows
@@ -240,6 +320,17 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
         const uint64_t ba = (__ballot(l < P && L.a[l] > 0) >> sh) & segmask;
         const uint64_t bb = (__ballot(l < D && L.b[l] > 0) >> sh) & segmask;
         const bool one_p = __popcll(ba) == 1, one_d = __popcll(bb) == 1;
+        bool thin = false;  // some KV arc below min(a_i, b_j)
+#pragma unroll
+        for (int r = 0; r < kKvRows; ++r) {
+            const int e = l + r * SEG;
+            if (e < P * D) {
+                const int i = e / D, d = e - i * D;
+                const int32_t m = L.a[i] < L.b[d] ? L.a[i] : L.b[d];
+                thin |= L.cap[i * Ds + d] < m;
+            }
+        }
+        const bool dominant = ((__ballot(thin) >> sh) & segmask) == 0;
         if (has_flow && (one_p || one_d)) {
             const int is = __ffsll((unsigned long long)ba) - 1, js = __ffsll((unsigned long long)bb) - 1;
             int32_t v = 0;
@@ -277,6 +368,37 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
                 if (l == js) L.ft[js] = F;
             }
             if (l < P) L.ep[l] = 0;
+        } else if (has_flow && dominant) {
+            // lane l holds prefill node l and decode node l (packed plans: P, D <= SEG); the
+            // sums stay below 64 * 2^24 < 2^31
+            const int32_t av = l < P ? L.a[l] : 0, bv = l < D ? L.b[l] : 0;
+            int32_t ia = av, ib = bv;
+#pragma unroll
+            for (int off = 1; off < SEG; off <<= 1) {
+                const int32_t ua = __shfl_up(ia, off, SEG), ub = __shfl_up(ib, off, SEG);
+                if (l >= off) {
+                    ia += ua;
+                    ib += ub;
+                }
+            }
+            const int32_t ta = __shfl(ia, SEG - 1, SEG), tb = __shfl(ib, SEG - 1, SEG);
+            const int32_t U = ta < tb ? ta : tb;
+            const int32_t ai = ia < U ? ia : U, ae = ia - av < U ? ia - av : U;
+            const int32_t bi = ib < U ? ib : U, be = ib - bv < U ? ib - bv : U;
+            if (l < P) {
+                L.fs[l] = ai - ae;
+                L.ep[l] = 0;
+            }
+            if (l < D) L.ft[l] = bi - be;
+#pragma unroll
+            for (int r = 0; r < kKvRows; ++r) {
+                const int e = l + r * SEG;
+                const bool in = e < P * D;
+                const int i = in ? e / D : 0, d = in ? e - i * D : 0;
+                const int32_t Ai = __shfl(ai, i, SEG), Ae = __shfl(ae, i, SEG);
+                const int32_t Bj = __shfl(bi, d, SEG), Be = __shfl(be, d, SEG);
+                if (in) L.fl[i * Ds + d] = nw_overlap(Ae, Ai, Be, Bj);
+            }
         } else if (has_flow && kv_flow == nullptr && cut == nullptr) {
             // Only the value is wanted: with m = min(P', D') <= kEnumMax nodes that can carry
             // flow on the smaller side, take the minimum cut directly.  Fixing which of those
@@ -320,6 +442,66 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG)
                 cut_value = best;
                 if (l < P) L.ep[l] = 0;
             }
+        }
+        __syncthreads();
+    } else {
+        // Workgroup plans (one candidate per workgroup, so every branch here is uniform).
+        __shared__ long long wave_sum[SEG > 64 ? SEG / 64 : 1];
+        bool thin = false;
+        for (int e = l; has_flow && e < P * D; e += SEG) {
+            const int i = e / D, d = e - i * D;
+            const int32_t m = L.a[i] < L.b[d] ? L.a[i] : L.b[d];
+            thin |= L.cap[i * Ds + d] < m;
+        }
+        if (!__syncthreads_or(thin) && has_flow) {
+            // block scan: lane l owns a contiguous run of nodes on each side; clamped inclusive
+            // prefix sums go to ep (prefill) and ed (decode), then become the flows
+            const int cp = (P + SEG - 1) / SEG, cd = (D + SEG - 1) / SEG;
+            const int p0 = l * cp < P ? l * cp : P, p1 = p0 + cp < P ? p0 + cp : P;
+            const int d0 = l * cd < D ? l * cd : D, d1 = d0 + cd < D ? d0 + cd : D;
+            long long sa = 0, sb = 0;
+            for (int i = p0; i < p1; ++i) sa += L.a[i];
+            for (int j = d0; j < d1; ++j) sb += L.b[j];
+            long long tot[2], excl[2];
+            const long long v2[2] = {sa, sb};
+            for (int k = 0; k < 2; ++k) {
+                long long incl = v2[k];
+                for (int off = 1; off < 64; off <<= 1) {
+                    const long long u = __shfl_up(incl, off, 64);
+                    if ((l & 63) >= off) incl += u;
+                }
+                if ((l & 63) == 63) wave_sum[l >> 6] = incl;
+                __syncthreads();
+                long long before = 0, all = 0;
+                for (int w = 0; w < SEG / 64; ++w) {
+                    if (w < (l >> 6)) before += wave_sum[w];
+                    all += wave_sum[w];
+                }
+                __syncthreads();
+                excl[k] = before + incl - v2[k];
+                tot[k] = all;
+            }
+            const long long U = tot[0] < tot[1] ? tot[0] : tot[1];  // < 2^31: min(P, D) <= 127
+            long long run = excl[0];
+            for (int i = p0; i < p1; ++i) {
+                run += L.a[i];
+                L.ep[i] = (int32_t)(run < U ? run : U);
+            }
+            run = excl[1];
+            for (int j = d0; j < d1; ++j) {
+                run += L.b[j];
+                L.ed[j] = (int32_t)(run < U ? run : U);
+            }
+            __syncthreads();
+            for (int e = l; e < P * D; e += SEG) {
+                const int i = e / D, d = e - i * D;
+                L.fl[i * Ds + d] = nw_overlap(i > 0 ? L.ep[i - 1] : 0, L.ep[i], d > 0 ? L.ed[d - 1] : 0, L.ed[d]);
+            }
+            for (int i = l; i < P; i += SEG) L.fs[i] = L.ep[i] - (i > 0 ? L.ep[i - 1] : 0);
+            for (int j = l; j < D; j += SEG) L.ft[j] = L.ed[j] - (j > 0 ? L.ed[j - 1] : 0);
+            __syncthreads();
+            for (int i = l; i < P; i += SEG) L.ep[i] = 0;
+            for (int j = l; j < D; j += SEG) L.ed[j] = 0;
         }
         __syncthreads();
     }
@@ -500,6 +682,8 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
     const int tiles = (f.N + kPer - 1) / kPer;
     const int blocks = 8 * ((tiles + 7) / 8);
     prof_mark(kKMaxflow, false, s);
+    if (SEG > 64 && kv == nullptr && cut == nullptr)
+        hipLaunchKernelGGL(bound_kernel, dim3((f.N + kBoundBlock - 1) / kBoundBlock), dim3(kBoundBlock), 0, s, f, fv);
     hipLaunchKernelGGL(maxflow_kernel<SEG>, dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget);
     prof_mark(kKMaxflow, true, s);
     return hipGetLastError();

@@ -416,8 +416,8 @@ class Refiner:
     @classmethod
     def create(cls, dp: DeviceProblem, parent_col: int, n_child: int, device: str = "cuda") -> "Refiner":
         torch = _torch()
-        pa = dp.tensors["assign"][:, parent_col:parent_col + 1].contiguous()
-        pr = dp.tensors["role"][:, parent_col:parent_col + 1].contiguous()
+        pa = dp.tensors["assign"][:, parent_col:parent_col + 1].clone()
+        pr = dp.tensors["role"][:, parent_col:parent_col + 1].clone()
         parent = dp.with_candidates(pa, pr)
         pws = Workspace.for_problem(parent, flows=True, device=device)
         mp, md, mpd = pws.net.dims
