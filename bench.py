@@ -56,9 +56,13 @@ KERNEL_TRAFFIC = {
     "eval": {"source_sha256_16": "2fe02144148e6483", "fetch_kib": 5310.8, "write_kib": 65706.0},
     "nodes": {"source_sha256_16": "5fbd4e7404ecfaea", "fetch_kib": 6697.6, "write_kib": 20441.6},
     "kv": {"source_sha256_16": "5fbd4e7404ecfaea", "fetch_kib": 5895.5, "write_kib": 13399.1},
-    "maxflow": {"source_sha256_16": "092d98a1f13d354c", "fetch_kib": 16706.6, "write_kib": 256.0},
+    "maxflow": {"source_sha256_16": "021cf0e400191f75", "fetch_kib": 16730.0, "write_kib": 256.0},
     "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.3, "write_kib": 0.0},
 }
+# The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
+# 131,072 children, same scaling.
+MOVES_TRAFFIC = {"source_sha256_16": "2902f3b847ca3ebd", "children": 131072, "fetch_kib": 561.0,
+                 "write_kib": 20990.0}
 KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
                  "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
                  "best": "hx_best.hip"}
@@ -275,9 +279,15 @@ def refine_main(args, torch, hx, I):
                 "frac": alg / t / 1e9 / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_launch": alg,
                 "avg_launch_us": 1000.0 * kernel_ms_per_round[dominant]}
     t_mv = kernel_us["moves"] * 1e-6
+    import hashlib
+    mt = None
+    src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", "hx_refine.hip")
+    if (hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] == MOVES_TRAFFIC["source_sha256_16"]
+            and n_child == MOVES_TRAFFIC["children"]):
+        mt = 1024.0 * (MOVES_TRAFFIC["fetch_kib"] * COUNTER_SCALE["fetch"] + MOVES_TRAFFIC["write_kib"] * COUNTER_SCALE["write"])
     moves_roof = {"kernel": "moves (hx_guided_moves)", "bound": "hbm", "achieved": hbm["moves"] / t_mv / 1e9,
                   "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["moves"] / t_mv / 1e9 / HBM_PEAK_GBS,
-                  "traffic": None, "algorithmic_bytes_per_launch": hbm["moves"], "avg_launch_us": kernel_us["moves"]}
+                  "traffic": mt, "algorithmic_bytes_per_launch": hbm["moves"], "avg_launch_us": kernel_us["moves"]}
 
     # quality beside it: random single-step perturbations (the same move kinds, drawn without
     # the max-flow classes) for the same number of rounds, scored on the GPU
