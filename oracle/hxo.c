@@ -73,7 +73,9 @@ typedef struct {
 
 typedef struct { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hxo_model;
 typedef struct { double s_in, s_out; } hxo_workload;
-typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; } hxo_space;
+/* variant bit 0: pipelined decode capacity (below) */
+typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; uint32_t variant; } hxo_space;
+#define HXO_VARIANT_PIPELINED 1u
 
 /* ------------------------------------------------------------------ helpers */
 
@@ -195,10 +197,16 @@ static double stage_pp_comm(const hxo_cluster *c, const hxo_model *m, const hxo_
 
 /* One strategy (tp, pp) of one group (members ascending, n = tp*pp of them).
  * Returns 1 if the memory limit admits a batch of at least 1, else 0.
- * Outputs b_max, the latency of one batch, and x = 1000*b/latency milli-requests/s. */
-int hxo_strategy_cost(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
-                      const int32_t *members, int32_t n, int32_t tp, int32_t pp, int32_t role,
-                      int32_t *bmax_out, double *lat_out, double *x_out)
+ * Outputs b_max, the latency of one batch, and x = 1000*b/latency milli-requests/s.
+ *
+ * Variant HXO_VARIANT_PIPELINED (an alternative reading of Appendix A): the latency stays the
+ * sum over stages, but a decode replica runs its stages as a pipeline, so batches leave it at
+ * the pace of its slowest stage: x = 1000*b / max_j T_j with T_j = (comp_j + tp_j) + pp_j, the
+ * PP term of the link into stage j+1 counted with stage j (none after the last stage).
+ * Prefill capacity is unchanged (one request's latency). */
+int hxo_strategy_cost_v(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                        const int32_t *members, int32_t n, int32_t tp, int32_t pp, int32_t role, uint32_t variant,
+                        int32_t *bmax_out, double *lat_out, double *x_out)
 {
     const int L = m->n_layers;
     *bmax_out = 0; *lat_out = 0.0; *x_out = 0.0;
@@ -222,7 +230,25 @@ int hxo_strategy_cost(const hxo_cluster *c, const hxo_model *m, const hxo_worklo
     const double lat = s1 + s2;
     *lat_out = lat;
     *x_out = (1000.0 * b) / lat;
+    if ((variant & HXO_VARIANT_PIPELINED) && role == HXO_DECODE) {
+        double slowest = 0.0;
+        for (int j = 0; j < pp; j++) {
+            const int32_t *S = members + j * tp;
+            const int l = stage_layers(L, pp, j);
+            double T = stage_compute(c, m, w, S, tp, l, role, b) + stage_tp_comm(c, m, w, S, tp, l, role, b);
+            if (j + 1 < pp) T = T + stage_pp_comm(c, m, w, S, members + (j + 1) * tp, tp, role, b);
+            if (T > slowest) slowest = T;
+        }
+        *x_out = (1000.0 * b) / slowest;
+    }
     return 1;
+}
+
+int hxo_strategy_cost(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                      const int32_t *members, int32_t n, int32_t tp, int32_t pp, int32_t role,
+                      int32_t *bmax_out, double *lat_out, double *x_out)
+{
+    return hxo_strategy_cost_v(c, m, w, members, n, tp, pp, role, 0u, bmax_out, lat_out, x_out);
 }
 
 /* Try every admissible TP x PP of a group and keep prefill's latency-optimal and decode's
@@ -241,7 +267,7 @@ int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workloa
         if (pp > HXO_MAX_PP || !((sp->pp_mask >> (pp - 1)) & 1u) || pp > m->n_layers) continue;
         int32_t bmax;
         double lat, x;
-        if (!hxo_strategy_cost(c, m, w, members, n, tp, pp, role, &bmax, &lat, &x)) continue;
+        if (!hxo_strategy_cost_v(c, m, w, members, n, tp, pp, role, sp->variant, &bmax, &lat, &x)) continue;
         int better = !have || (role == HXO_PREFILL ? lat < best_lat : x > best_x);
         if (better) {
             have = 1; best_lat = lat; best_x = x;

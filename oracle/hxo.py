@@ -46,7 +46,8 @@ class _Workload(C.Structure):
 
 
 class _Space(C.Structure):
-    _fields_ = [("tp_mask", C.c_uint32), ("pp_mask", C.c_uint32), ("granularity", C.c_int32)]
+    _fields_ = [("tp_mask", C.c_uint32), ("pp_mask", C.c_uint32), ("granularity", C.c_int32),
+                ("variant", C.c_uint32)]
 
 
 _lib = None
@@ -85,7 +86,8 @@ class _Args:
         m = prob.model
         self.model = _Model(m["n_layers"], m["hidden"], m["n_heads"], m["n_kv_heads"], m["bytes_per_elem"])
         self.wl = _Workload(float(prob.s_in), float(prob.s_out))
-        self.space = _Space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity))
+        self.space = _Space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity),
+                            int(getattr(prob, "variant", 0)))
 
     def refs(self):
         return C.byref(self.cluster), C.byref(self.model), C.byref(self.wl), C.byref(self.space)
@@ -178,16 +180,18 @@ def score_batch(prob, n_threads: int = 1, dims=None) -> Dict[str, object]:
 
 # ------------------------------------------------------------------ single-group entry points
 
-def strategy_cost(prob, members: Sequence[int], tp: int, pp: int, role: int):
-    """(feasible, b_max, latency, x) of one strategy of one group of prob's cluster."""
+def strategy_cost(prob, members: Sequence[int], tp: int, pp: int, role: int, variant: Optional[int] = None):
+    """(feasible, b_max, latency, x) of one strategy of one group of prob's cluster (variant:
+    prob's by default)."""
     a = _Args(prob)
+    v = int(getattr(prob, "variant", 0)) if variant is None else int(variant)
     mem = np.ascontiguousarray(np.asarray(members, np.int32))
     bmax = C.c_int32()
     lat = C.c_double()
     x = C.c_double()
-    ok = lib().hxo_strategy_cost(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(mem),
-                                 C.c_int32(len(mem)), C.c_int32(tp), C.c_int32(pp), C.c_int32(role),
-                                 C.byref(bmax), C.byref(lat), C.byref(x))
+    ok = lib().hxo_strategy_cost_v(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(mem),
+                                   C.c_int32(len(mem)), C.c_int32(tp), C.c_int32(pp), C.c_int32(role),
+                                   C.c_uint32(v), C.byref(bmax), C.byref(lat), C.byref(x))
     return bool(ok), bmax.value, lat.value, x.value
 
 

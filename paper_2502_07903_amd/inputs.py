@@ -142,6 +142,7 @@ class Problem:
     max_groups: int
     assign: np.ndarray        # uint8 [G][N]
     role: np.ndarray          # uint8 [max_groups][N]
+    variant: int = 0          # cost-model variant bits (bit 0: pipelined decode capacity)
 
     @property
     def n_cand(self) -> int:
