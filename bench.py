@@ -75,6 +75,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--variant", choices=["as-written", "pipelined"], default="as-written",
+                    help="cost-model variant: the model as written, or pipelined decode capacity")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
     ap.add_argument("--refine", action="store_true",
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
@@ -392,6 +394,8 @@ def main():
         return
     wl = I.WORKLOADS[args.workload]
     prob = I.make_problem(args.workload)
+    if args.variant == "pipelined":
+        prob = dataclasses.replace(prob, variant=1)
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp, flows=False)
     stream = torch.cuda.current_stream()
@@ -455,7 +459,8 @@ def main():
         "dtype": "f64+i32",
         "data": "synthetic",
         "config": {"workload": f"workload{wl.cfg}: {wl.name}", "candidates": prob.n_cand,
-                   "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity},
+                   "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
+                   "cost_model": args.variant},
         "kernel_ms": per_kernel,
         "kernel_us": kernel_us,
         "hbm_bytes_per_step": hbm,

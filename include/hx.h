@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define HX_ABI_VERSION 1
+#define HX_ABI_VERSION 2
 #define HX_CAP_MAX 16777215      /* 2^24 - 1 */
 #define HX_MAX_GPUS 255
 #define HX_MAX_GROUPS 255
@@ -88,8 +88,13 @@ typedef struct hx_model { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_p
 typedef struct hx_workload { double s_in, s_out; } hx_workload;
 
 /* Strategy space: bit k of tp_mask admits TP degree k+1 (<= 8), bit k of pp_mask PP degree
- * k+1 (<= 32).  granularity 0: one flow node per replica; 1: one flow node per GPU. */
-typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; } hx_space;
+ * k+1 (<= 32).  granularity 0: one flow node per replica; 1: one flow node per GPU.
+ * variant: cost-model variant bits, 0 for the model as written (see hx_cost_eval). */
+typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; uint32_t variant; } hx_space;
+
+/* Pipelined decode capacity: a decode replica's batches leave at the pace of its slowest
+ * stage (an alternative reading of Appendix A's decode capacity). */
+#define HX_VARIANT_PIPELINED 1u
 
 /* Candidate placements (Sec. 3.1).  assign[g][n] = group of GPU g in candidate n (HX_UNUSED
  * or >= max_groups: GPU unused); role[k][n] = HX_PREFILL, HX_DECODE, or anything else (no
@@ -149,7 +154,10 @@ int hx_validate(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_sp
  *         times s_out
  *   x = (1000*b)/latency milli-requests/s; cap = min(HX_CAP_MAX, floor(x)).
  * A prefill group keeps its lowest-latency strategy, a decode group its highest-x one (Sec.
- * 3.3 "Compute nodes"); ties keep the smaller tp. */
+ * 3.3 "Compute nodes"); ties keep the smaller tp.
+ * With space.variant & HX_VARIANT_PIPELINED, a decode strategy's x is (1000*b)/max_j T_j,
+ * T_j = (comp_j + tp_j) + pp_j (pp_j: the PP term of the link into stage j+1 as in the
+ * latency, none for the last stage); latencies and prefill are unchanged. */
 int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                  const hx_candidates *cand, const hx_cost_out *out, void *workspace,
                  size_t workspace_bytes, hipStream_t stream);

@@ -49,7 +49,10 @@ struct StrategyCost {
 // Returns false when the memory limit admits no batch of 1.  TPC > 0 fixes tp at compile
 // time: a stage's member ids are then held in registers and each device's peer loop is
 // unrolled, so its loads and divisions overlap; TPC == 0 is the same arithmetic for any tp.
-template <int TPC>
+// kPipe: the pipelined decode capacity variant (HX_VARIANT_PIPELINED): a decode replica's x is
+// 1000 b over its slowest stage, T_j = (comp_j + TP_j) + PP_j with the link into stage j+1
+// counted with stage j; the latency is the same sum either way.
+template <int TPC, bool kPipe>
 __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
                                               int tp_rt, int pp, int role, StrategyCost& out) {
     constexpr int kMax = TPC > 0 ? TPC : HX_MAX_TP;
@@ -89,6 +92,7 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
 
     int S[kMax], Sp[kMax];
     double s1 = 0.0, s2 = 0.0;
+    double tmax = 0.0, prev = 0.0;  // kPipe: slowest stage so far, previous stage's comp + TP
     for (int j = 0; j < pp; ++j) {
         const double l = (double)(lq + (j < lr ? 1 : 0));
         const uint8_t* Sl = mem + (j * tp) * stride;
@@ -123,7 +127,8 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
             if (r == 0 || sum > mx) mx = sum;
         }
         const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
-        s1 = s1 + (comp + tpc);
+        const double stage = comp + tpc;
+        s1 = s1 + stage;
         // PP row between stage j-1 and stage j: the fastest link.
         if (j > 0) {
             double mn = 0.0;
@@ -143,24 +148,31 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                     if ((r == 0 && q == 0) || v < mn) mn = v;
                 }
             }
-            s2 = s2 + (prefill ? mn : mn * p.s_out);
+            const double ppt = prefill ? mn : mn * p.s_out;
+            s2 = s2 + ppt;
+            if (kPipe) tmax = dmax(tmax, prev + ppt);
         }
+        if (kPipe) prev = stage;
 #pragma unroll
         for (int r = 0; r < kMax; ++r) Sp[r] = S[r];
     }
     out.lat = s1 + s2;
-    out.x = (1000.0 * b) / out.lat;
+    if (kPipe && !prefill)
+        out.x = (1000.0 * b) / dmax(tmax, prev);
+    else
+        out.x = (1000.0 * b) / out.lat;
     return true;
 }
 
+template <bool kPipe>
 __device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, const uint8_t* mem, int stride, int tp,
                                          int pp, int role, StrategyCost& out) {
     switch (tp) {
-        case 1: return cost_strategy<1>(p, tb, mem, stride, tp, pp, role, out);
-        case 2: return cost_strategy<2>(p, tb, mem, stride, tp, pp, role, out);
-        case 4: return cost_strategy<4>(p, tb, mem, stride, tp, pp, role, out);
-        case 8: return cost_strategy<8>(p, tb, mem, stride, tp, pp, role, out);
-        default: return cost_strategy<0>(p, tb, mem, stride, tp, pp, role, out);
+        case 1: return cost_strategy<1, kPipe>(p, tb, mem, stride, tp, pp, role, out);
+        case 2: return cost_strategy<2, kPipe>(p, tb, mem, stride, tp, pp, role, out);
+        case 4: return cost_strategy<4, kPipe>(p, tb, mem, stride, tp, pp, role, out);
+        case 8: return cost_strategy<8, kPipe>(p, tb, mem, stride, tp, pp, role, out);
+        default: return cost_strategy<0, kPipe>(p, tb, mem, stride, tp, pp, role, out);
     }
 }
 
@@ -437,6 +449,7 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
 
 // One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
 // is false for groups past the last large unit (they still join every wave-level sync).
+template <bool kPipe>
 __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, const uint8_t* adm_tab,
                           int gl, bool live, int n, int k, int role, uint64_t mask) {
     const int G = p.G;
@@ -517,7 +530,7 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
         }
         wave_sync();
         if (feas && gl == 0) {
-            double s1 = 0.0, s2 = 0.0;
+            double s1 = 0.0, s2 = 0.0, tmax = 0.0;
             for (int j = 0; j < pp; ++j) {
                 const double l = (double)(lq + (j < lr ? 1 : 0));
                 double mx = 0.0;
@@ -526,7 +539,20 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
                     if (r == 0 || v > mx) mx = v;
                 }
                 const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
-                s1 = s1 + (c.comp[j] + tpc);
+                const double stage = c.comp[j] + tpc;
+                s1 = s1 + stage;
+                if (kPipe && !prefill) {
+                    double T = stage;
+                    if (j + 1 < pp) {
+                        double mn = 0.0;
+                        for (int r = 0; r < tp; ++r) {
+                            const double v = c.pmin[j * tp + r];
+                            if (r == 0 || v < mn) mn = v;
+                        }
+                        T = T + mn * p.s_out;
+                    }
+                    tmax = dmax(tmax, T);
+                }
             }
             for (int j = 0; j + 1 < pp; ++j) {
                 double mn = 0.0;
@@ -537,7 +563,7 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
                 s2 = s2 + (prefill ? mn : mn * p.s_out);
             }
             const double lat = s1 + s2;
-            const double x = (1000.0 * b) / lat;
+            const double x = (1000.0 * b) / (kPipe && !prefill ? tmax : lat);
             const bool better = !have || (prefill ? lat < best_lat : x > best_x);
             if (better) {
                 have = true;
@@ -560,7 +586,7 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
     }
 }
 
-template <int W, bool kTables, int kEvalBlock>
+template <int W, bool kTables, int kEvalBlock, bool kPipe>
 __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
     const int G = p.G;
@@ -627,7 +653,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
                 role = (int)(w & 0xFF);
                 mask = rec[1];
             }
-            coop_unit(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
+            coop_unit<kPipe>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
@@ -651,7 +677,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
             const int tp = __ffs(am);
             const int pp = stage_count(cnt, tp);
             StrategyCost sc;
-            if (!cost_any(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            if (!cost_any<kPipe>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
             const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
             if (better) {
                 have = true;
@@ -668,6 +694,19 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
         o.bmax[o_] = (int32_t)best_b;
         o.cap[o_] = have ? quantize(best_x) : 0;
         o.lat[o_] = best_lat;
+    }
+}
+
+template <int W, bool kPipe>
+void launch_eval(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
+                 size_t lds, hipStream_t s) {
+    if (eb == 256) {
+        if (tables)
+            hipLaunchKernelGGL((eval_kernel<W, true, 256, kPipe>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
+        else
+            hipLaunchKernelGGL((eval_kernel<W, false, 256, kPipe>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
+    } else {
+        hipLaunchKernelGGL((eval_kernel<W, false, 128, kPipe>), dim3(blocks), dim3(128), lds, s, p, o, wk, nb);
     }
 }
 
@@ -728,14 +767,10 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     prof_mark(kKEval, false, s);
-    if (eb == 256) {
-        if (tables)
-            hipLaunchKernelGGL((eval_kernel<W, true, 256>), dim3(blocks), dim3(256), lds_eval, s, p, o, wk, nb);
-        else
-            hipLaunchKernelGGL((eval_kernel<W, false, 256>), dim3(blocks), dim3(256), lds_eval, s, p, o, wk, nb);
-    } else {
-        hipLaunchKernelGGL((eval_kernel<W, false, 128>), dim3(blocks), dim3(128), lds_eval, s, p, o, wk, nb);
-    }
+    if (p.variant & HX_VARIANT_PIPELINED)
+        launch_eval<W, true>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+    else
+        launch_eval<W, false>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
     prof_mark(kKEval, true, s);
     return hipGetLastError();
 }

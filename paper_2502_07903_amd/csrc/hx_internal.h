@@ -15,6 +15,7 @@ struct Problem {
     int32_t G, T, N, Kmax, L;
     uint32_t tp_mask, pp_mask;
     int32_t granularity;
+    uint32_t variant;  // HX_VARIANT_* bits
     double H, Hkv, B, s_in, s_out;
     int32_t coord_cap;
     const int32_t* gpu_type;

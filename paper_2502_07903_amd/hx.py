@@ -52,7 +52,8 @@ class hx_workload(C.Structure):
 
 
 class hx_space(C.Structure):
-    _fields_ = [("tp_mask", C.c_uint32), ("pp_mask", C.c_uint32), ("granularity", C.c_int32)]
+    _fields_ = [("tp_mask", C.c_uint32), ("pp_mask", C.c_uint32), ("granularity", C.c_int32),
+                ("variant", C.c_uint32)]
 
 
 class hx_candidates(C.Structure):
@@ -211,7 +212,8 @@ class DeviceProblem:
         n_cand = int(t["assign"].shape[1])
         k = hx_candidates(n_cand, int(prob.max_groups), _ptr(t["assign"]), _ptr(t["role"]))
         return cls(t, c, md, hx_workload(float(prob.s_in), float(prob.s_out)),
-                   hx_space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity)), k, cl.n_gpus,
+                   hx_space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity),
+                            int(getattr(prob, "variant", 0))), k, cl.n_gpus,
                    int(prob.max_groups))
 
     def with_candidates(self, assign, role) -> "DeviceProblem":

@@ -28,7 +28,7 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version_and_strings():
-    assert hx.lib().hx_abi_version() == 1
+    assert hx.lib().hx_abi_version() == 2
     for code in (0, -1, -2, -3, -4):
         assert hx.strerror(code)
     assert hx.lib().hx_last_error() is not None
@@ -58,6 +58,9 @@ def test_validate_accepts_workloads():
     for kw in (dict(G=8, T=2, N=256, Kmax=4), dict(G=32, N=65536, Kmax=16), dict(G=64, T=5, N=262144, Kmax=32),
                dict(G=128, T=6, N=131072, Kmax=32, gran=1)):
         assert _validate(*_args(**kw)) == hx.HX_OK
+    a = list(_args())
+    a[3].variant = 1                                    # HX_VARIANT_PIPELINED
+    assert _validate(*a) == hx.HX_OK
 
 
 @pytest.mark.parametrize("mutate", [
@@ -74,6 +77,7 @@ def test_validate_accepts_workloads():
     lambda a: setattr(a[3], "tp_mask", 1 << 8),      # TP degree 9 > 8
     lambda a: setattr(a[3], "pp_mask", 0),
     lambda a: setattr(a[3], "granularity", 2),
+    lambda a: setattr(a[3], "variant", 2),           # unknown cost-model variant bit
     lambda a: setattr(a[4], "n_cand", 0),
     lambda a: setattr(a[4], "max_groups", 256),
     lambda a: setattr(a[4], "role", None),

@@ -1,0 +1,87 @@
+"""GPU parity of the cost-model variants against the oracle, through the C-ABI: with the
+pipelined decode capacity (HX_VARIANT_PIPELINED) every strategy choice, batch limit,
+capacity and latency, the networks built on them, every flow value and the best candidate
+must equal the oracle's (integers bit-exact, latencies to 1e-5 relative and expected
+bit-identical)."""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import hxo
+from paper_2502_07903_amd import hx
+from paper_2502_07903_amd import inputs as I
+from tests import helpers as Hh
+
+pytestmark = pytest.mark.gpu
+N_THREADS = max(1, min(16, os.cpu_count() or 1))
+PIPE = 1
+
+
+def say(msg: str) -> None:
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm GPU (torch.cuda.is_available() is False)")
+    hx.lib()
+    return T
+
+
+def _gpu(torch, prob):
+    dp = hx.DeviceProblem.upload(prob)
+    assert dp.space.variant == prob.variant
+    ws = hx.Workspace.for_problem(dp)
+    hx.score(dp, ws)
+    torch.cuda.synchronize()
+    return ({k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")}, ws.net.host(),
+            ws.flow_value.cpu().numpy(), tuple(int(x) for x in ws.best.cpu().numpy()))
+
+
+@pytest.mark.parametrize("cfg,n", [(1, None), (2, None), (3, None), (3, 4097), (4, 4096), (2, 1)])
+def test_pipelined_parity(torch, cfg, n):
+    prob = dataclasses.replace(I.make_problem(cfg, n_cand=n), variant=PIPE)
+    say(f"pipelined decode capacity: workload {cfg}, N={prob.n_cand}")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    for k in ("tp", "pp", "bmax", "cap"):
+        bad = cost[k] != want["cost"][k]
+        assert not bad.any(), f"{k} differs at {np.argwhere(bad)[:5].tolist()}"
+    rel = np.abs(cost["lat"] - want["cost"]["lat"]) / np.maximum(np.abs(want["cost"]["lat"]), 1e-300)
+    assert (rel <= 1e-5).all()
+    assert np.array_equal(cost["lat"], want["cost"]["lat"])
+    Hh.compare_flownet(fn, want["flownet"])
+    assert np.array_equal(fv, want["flow_value"])
+    assert best == want["best"]
+    # the variant moves decode capacities only, and only up
+    base = hxo.cost_eval(dataclasses.replace(prob, variant=0))
+    dec = prob.role == I.DECODE
+    assert (cost["cap"][dec] >= base["cap"][dec]).all()
+    assert np.array_equal(cost["cap"][prob.role == I.PREFILL], base["cap"][prob.role == I.PREFILL])
+
+
+def test_pipelined_per_gpu_nodes(torch):
+    """Per-GPU flow nodes (128 GPUs) with the variant, on a seeded sample of round 0."""
+    prob = dataclasses.replace(I.make_problem(5, n_cand=1024), variant=PIPE)
+    say("pipelined decode capacity: per-GPU nodes, N=1024")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    for k in ("tp", "pp", "bmax", "cap", "lat"):
+        assert np.array_equal(cost[k], want["cost"][k]), k
+    assert np.array_equal(fv, want["flow_value"])
+    assert best == want["best"]
+
+
+def test_unknown_variant_rejected(torch):
+    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=2)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp)
+    with pytest.raises(hx.HxError) as e:
+        hx.cost_eval(dp, ws.cost)
+    assert e.value.code == hx.HX_EINVAL
