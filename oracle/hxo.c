@@ -73,9 +73,10 @@ typedef struct {
 
 typedef struct { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hxo_model;
 typedef struct { double s_in, s_out; } hxo_workload;
-/* variant bit 0: pipelined decode capacity (below) */
+/* variant bit 0: pipelined decode capacity; bit 1: KV stage-order search (both below) */
 typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; uint32_t variant; } hxo_space;
 #define HXO_VARIANT_PIPELINED 1u
+#define HXO_VARIANT_KV_ORDER 2u  /* bit 1: KV stage-order search (hxo_kv_time_best) */
 
 /* ------------------------------------------------------------------ helpers */
 
@@ -280,8 +281,12 @@ int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workloa
 /* KV-cache transfer time of one request from a prefill replica (members pm, ptp x ppp) to a
  * decode replica (dm, dtp x dpp): every GPU holding layer j's KV heads sends them to the
  * GPUs holding the same layer and heads on the decode side; the slowest link decides. */
-double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
-                   const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *dm, int32_t dtp, int32_t dpp)
+/* The same with an explicit stage order: the prefill replica's stage ord_p[a] (its members
+ * ranked ord_p[a]*ptp .. +ptp-1) serves pipeline position a, which holds the layers of position
+ * a; likewise ord_d on the decode side. */
+static double kv_time_ordered(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                              const int32_t *pm, int ptp, int ppp, const int *ord_p,
+                              const int32_t *dm, int dtp, int dpp, const int *ord_d)
 {
     const int L = m->n_layers;
     const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
@@ -298,7 +303,7 @@ double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload 
                     int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
                     int ov = hi - lo;
                     if (ov <= 0) continue;
-                    int g = pm[a * ptp + r], h = dm[bb * dtp + q];
+                    int g = pm[ord_p[a] * ptp + r], h = dm[ord_d[bb] * dtp + q];
                     double bytes = ((V1 * (double)nab) * (double)ov) / (double)(ptp * dtp);
                     double time = alpha_of(c, g, h) + bytes / beta_of(c, g, h);
                     if (time > worst) worst = time;
@@ -306,6 +311,59 @@ double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload 
         }
     }
     return worst;
+}
+
+double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                   const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *dm, int32_t dtp, int32_t dpp)
+{
+    int op[HXO_MAX_PP], od[HXO_MAX_PP];
+    for (int a = 0; a < ppp; a++) op[a] = a;
+    for (int b = 0; b < dpp; b++) od[b] = b;
+    return kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od);
+}
+
+/* next permutation of v[0..n) in lexicographic order; returns 0 after the last one */
+static int next_order(int *v, int n)
+{
+    int i = n - 2;
+    while (i >= 0 && v[i] >= v[i + 1]) i--;
+    if (i < 0) return 0;
+    int j = n - 1;
+    while (v[j] <= v[i]) j--;
+    int t = v[i]; v[i] = v[j]; v[j] = t;
+    for (int a = i + 1, b = n - 1; a < b; a++, b--) { t = v[a]; v[a] = v[b]; v[b] = t; }
+    return 1;
+}
+
+static long order_count(int pp)
+{
+    long f = 1;
+    for (int k = 2; k <= pp; k++) f *= k;
+    return f;
+}
+
+/* Stage-order search (Appendix A, "Edge capacity estimation": the pipeline stage order of both
+ * replicas is adjusted to minimise the KV cache communication cost, which sets the edge
+ * capacity).  The KV time is minimised over every pair of stage orders when there are at most
+ * HXO_ORDER_PAIRS of them (ppp! * dpp!); deeper pairs of pipelines keep the ascending orders.
+ * Node capacities are not affected (they keep the ascending order). */
+#define HXO_ORDER_PAIRS 720
+double hxo_kv_time_best(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                        const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *dm, int32_t dtp, int32_t dpp)
+{
+    if (order_count(ppp) * order_count(dpp) > HXO_ORDER_PAIRS)
+        return hxo_kv_time(c, m, w, pm, ptp, ppp, dm, dtp, dpp);
+    int op[HXO_MAX_PP], od[HXO_MAX_PP];
+    for (int a = 0; a < ppp; a++) op[a] = a;
+    double best = -1.0;
+    do {
+        for (int b = 0; b < dpp; b++) od[b] = b;
+        do {
+            double t = kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od);
+            if (best < 0.0 || t < best) best = t;
+        } while (next_order(od, dpp));
+    } while (next_order(op, ppp));
+    return best;
 }
 
 /* Per-GPU flow nodes: the link from prefill GPU g (one of n_p GPUs of its replica) to decode
@@ -431,7 +489,9 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
                     int32_t kv = 0;
                     (void)pn; (void)dn;
                     if (tp[gp] > 0 && tp[gd] > 0) {
-                        double t = hxo_kv_time(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                        double t = (bt->sp->variant & HXO_VARIANT_KV_ORDER)
+                                       ? hxo_kv_time_best(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd])
+                                       : hxo_kv_time(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
                         kv = hxo_quantize(1000.0 / t);
                     }
                     f->kv_cap[(int64_t)(i * nd + j) * N + n] = kv;

@@ -61,6 +61,7 @@ def lib():
         _lib = C.CDLL(LIB)
         _lib.hxo_maxflow_edges.restype = C.c_int64
         _lib.hxo_kv_time.restype = C.c_double
+        _lib.hxo_kv_time_best.restype = C.c_double
         _lib.hxo_kv_gpu_time.restype = C.c_double
         _lib.hxo_quantize.restype = C.c_int32
     return _lib
@@ -206,12 +207,16 @@ def group_select(prob, members: Sequence[int], role: int):
     return o[0].value, o[1].value, o[2].value, o[3].value, lat.value
 
 
-def kv_time(prob, pm: Sequence[int], ptp: int, ppp: int, dm: Sequence[int], dtp: int, dpp: int) -> float:
+def kv_time(prob, pm: Sequence[int], ptp: int, ppp: int, dm: Sequence[int], dtp: int, dpp: int,
+            best_order: bool = False) -> float:
+    """KV time of one request between two replicas (ascending stage orders, or the stage-order
+    search when best_order)."""
     a = _Args(prob)
     p = np.ascontiguousarray(np.asarray(pm, np.int32))
     d = np.ascontiguousarray(np.asarray(dm, np.int32))
-    return lib().hxo_kv_time(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(p), C.c_int32(ptp),
-                             C.c_int32(ppp), _p(d), C.c_int32(dtp), C.c_int32(dpp))
+    fn = lib().hxo_kv_time_best if best_order else lib().hxo_kv_time
+    return fn(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(p), C.c_int32(ptp),
+              C.c_int32(ppp), _p(d), C.c_int32(dtp), C.c_int32(dpp))
 
 
 def kv_gpu_time(prob, g: int, h: int, n_p: int) -> float:

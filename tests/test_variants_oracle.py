@@ -6,7 +6,13 @@ stage counted with stage j); the latency and prefill capacities are unchanged.  
 what that definition fixes: one stage changes nothing; the stage times bound the summed
 latency (lat / pp <= max T_j <= lat); identical GPUs on free links give the closed form
 max T_j = ceil(L/pp) * (per-layer time); and a batch's decode capacities can only rise while its
-prefill capacities and every latency stay as they were.
+prefill capacities stay as they were.
+
+KV stage-order search (variant bit 1): a KV edge's time is minimised over the stage orders of
+both replicas.  Checked on a hand-derived case whose ascending orders pair the slow links and
+whose best order pairs the fast ones, and by what a search over every order fixes: it never
+exceeds the ascending time, leaves single stages alone, and cannot tell in which order the
+stage blocks were handed to it.
 """
 import dataclasses
 
@@ -92,3 +98,73 @@ def test_pipelined_batch_raises_only_decode():
         assert np.array_equal(base["cap"][pre], pipe["cap"][pre])
         assert (pipe["cap"][dec] >= base["cap"][dec]).all()
         assert (pipe["cap"][dec] > base["cap"][dec]).any()
+
+
+# ------------------------------------------------------------------ KV stage-order search
+
+ORDER = 2
+
+
+def _crossed_cluster():
+    """Four GPUs of one type; links 0<->3 and 1<->2 at 300 GB/s, every other link 10 GB/s, alpha 0."""
+    G = 4
+    beta = np.full((G, G), 10e9)
+    for a, b in ((0, 3), (1, 2)):
+        beta[a, b] = beta[b, a] = 300e9
+    np.fill_diagonal(beta, 0.0)
+    t = np.array([I.GPU_TYPES["A"]], np.float64)
+    return I.Cluster(np.zeros(G, np.int32), t[:, 0].copy(), t[:, 1].copy(), t[:, 2].copy(),
+                     np.ascontiguousarray(beta.reshape(-1)), np.zeros(G * G))
+
+
+def test_kv_order_hand_case():
+    """Prefill {0, 1} and decode {2, 3}, one GPU per stage, two stages of 24 layers each.
+    Ascending orders pair 0->2 and 1->3 (10 GB/s); putting decode stage {3} first pairs 0->3 and
+    1->2 (300 GB/s).  Each link carries a stage's KV cache, 2 s_in H_kv B * 24 bytes."""
+    from tests import helpers as Hh
+    cl = _crossed_cluster()
+    a, r = I.placement_from_groups([[0, 1], [2, 3]], [I.PREFILL, I.DECODE], 4, 2)
+    prob = Hh.problem(cl, dict(I.OPT_30B), a, r, s_in=512.0, s_out=128.0, tp=(1,), pp=(2,))
+    V = 2.0 * 512.0 * 7168 * 2 * 24
+    assert hxo.kv_time(prob, [0, 1], 1, 2, [2, 3], 1, 2) == pytest.approx(V / 10e9, rel=1e-15)
+    assert hxo.kv_time(prob, [0, 1], 1, 2, [2, 3], 1, 2, best_order=True) == pytest.approx(V / 300e9, rel=1e-15)
+    # the whole network: the KV edge capacity follows the searched order only with the variant
+    plain = hxo.build_flownet(prob, hxo.cost_eval(prob))
+    p2 = dataclasses.replace(prob, variant=ORDER)
+    searched = hxo.build_flownet(p2, hxo.cost_eval(p2))
+    assert int(plain["kv_cap"][0, 0]) == int(np.floor(1000.0 / (V / 10e9)))
+    assert int(searched["kv_cap"][0, 0]) == int(np.floor(1000.0 / (V / 300e9)))
+
+
+def _stage_blocks(members, tp, perm):
+    return [g for s in perm for g in members[s * tp:(s + 1) * tp]]
+
+
+def test_kv_order_search_properties():
+    """On random replica pairs of the 32-GPU cluster: the searched time never exceeds the
+    ascending one, equals it for single stages and beyond the search limit, and does not change
+    when the stage blocks are handed over in another order (the search covers every order)."""
+    prob = I.make_problem(3, n_cand=4)
+    rng = np.random.default_rng(5)
+    fact = [1, 1, 2, 6, 24, 120, 720, 5040, 40320]
+    checked = strict = 0
+    for _ in range(300):
+        ptp, dtp = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 4]))
+        ppp, dpp = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        if ptp * ppp + dtp * dpp > prob.n_gpus:
+            continue
+        g = rng.permutation(prob.n_gpus)
+        pm = sorted(g[:ptp * ppp].tolist())
+        dm = sorted(g[ptp * ppp:ptp * ppp + dtp * dpp].tolist())
+        asc = hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp)
+        best = hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp, best_order=True)
+        assert best <= asc
+        if fact[ppp] * fact[dpp] > 720 or (ppp == 1 and dpp == 1):
+            assert best == asc
+            continue
+        checked += 1
+        strict += best < asc
+        pm2 = _stage_blocks(pm, ptp, rng.permutation(ppp))
+        dm2 = _stage_blocks(dm, dtp, rng.permutation(dpp))
+        assert hxo.kv_time(prob, pm2, ptp, ppp, dm2, dtp, dpp, best_order=True) == best
+    assert checked > 50 and strict > 10
