@@ -68,6 +68,10 @@ KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx
                  "best": "hx_best.hip"}
 
 
+# hx_space.variant bits: 1 pipelined decode capacity, 2 KV stage-order search
+VARIANTS = {"as-written": 0, "pipelined": 1, "kv-order": 2, "pipelined+kv-order": 3}
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -75,8 +79,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--variant", choices=["as-written", "pipelined"], default="as-written",
-                    help="cost-model variant: the model as written, or pipelined decode capacity")
+    ap.add_argument("--variant", choices=list(VARIANTS), default="as-written",
+                    help="cost-model variant: the model as written, pipelined decode capacity, KV stage-order "
+                         "search, or both")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
     ap.add_argument("--refine", action="store_true",
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
@@ -394,8 +399,8 @@ def main():
         return
     wl = I.WORKLOADS[args.workload]
     prob = I.make_problem(args.workload)
-    if args.variant == "pipelined":
-        prob = dataclasses.replace(prob, variant=1)
+    if VARIANTS[args.variant]:
+        prob = dataclasses.replace(prob, variant=VARIANTS[args.variant])
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp, flows=False)
     stream = torch.cuda.current_stream()

@@ -95,6 +95,9 @@ typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; uint32
 /* Pipelined decode capacity: a decode replica's batches leave at the pace of its slowest
  * stage (an alternative reading of Appendix A's decode capacity). */
 #define HX_VARIANT_PIPELINED 1u
+/* KV stage-order search (Appendix A, edge capacity estimation): each KV edge's time is
+ * minimised over the stage orders of both replicas (see hx_build_flownet). */
+#define HX_VARIANT_KV_ORDER 2u
 
 /* Candidate placements (Sec. 3.1).  assign[g][n] = group of GPU g in candidate n (HX_UNUSED
  * or >= max_groups: GPU unused); role[k][n] = HX_PREFILL, HX_DECODE, or anything else (no
@@ -180,7 +183,11 @@ int hx_member_words(int32_t n_gpus);
  * bytes = ((V1*n)*ov)/(tp_p*tp_d) with V1 = (2*s_in)*H_kv*B, in alpha_{gh} + bytes/beta_{gh};
  * the KV time is the largest of these, and the edge capacity floor(1000/time) clamped to
  * HX_CAP_MAX, or 0 when either replica is infeasible.  Granularity 1: the edge from prefill
- * GPU g (replica of n_g GPUs) to decode GPU h has time alpha_{gh} + ((V1*L)/n_g)/beta_{gh}. */
+ * GPU g (replica of n_g GPUs) to decode GPU h has time alpha_{gh} + ((V1*L)/n_g)/beta_{gh}.
+ * With space.variant & HX_VARIANT_KV_ORDER (granularity 0), pipeline position a of a replica
+ * may be served by any of its stages (stage s = the members ranked s*tp .. s*tp+tp-1): the
+ * KV time is the minimum over every pair of stage orders of the two replicas when there are
+ * at most 720 such pairs (pp_p! * pp_d! <= 720), else the ascending orders'. */
 int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                      const hx_candidates *cand, const hx_cost_out *cost, const hx_flownet *net,
                      hipStream_t stream);

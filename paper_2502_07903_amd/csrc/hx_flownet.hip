@@ -7,7 +7,9 @@
 //                 ascending group id, or GPUs in ascending id at per-GPU granularity) with
 //                 their source, node and sink capacities (Appendix A);
 //   kv_kernel     one lane per (KV edge, candidate): the edge capacity between prefill node
-//                 i and decode node j (connection type 3; Table 1 last row; Appendix A).
+//                 i and decode node j (connection type 3; Table 1 last row; Appendix A), with
+//                 the stage-order search of Appendix A (kv_order_kernel) when
+//                 HX_VARIANT_KV_ORDER is set.
 #include "hx_internal.h"
 
 namespace hx {
@@ -172,6 +174,145 @@ __device__ double kv_time(const Problem& p, const uint8_t* pm, int ptp, int ppp,
     return worst;
 }
 
+// KV stage-order search (HX_VARIANT_KV_ORDER; Appendix A, edge capacity estimation): the stage
+// order of both replicas is chosen to minimise the KV time.  Orders are packed 4 bits per
+// pipeline position (position a is served by stage (ord >> 4a) & 15); pairs of pipelines with
+// more than kOrderPairs order pairs keep the ascending orders.
+constexpr int kOrderPairs = 720;
+
+__device__ __forceinline__ int order_count(int pp) {
+    int f = 1;
+    for (int k = 2; k <= pp; ++k) f *= k;
+    return f;
+}
+
+__device__ __forceinline__ int nib(uint32_t v, int i) { return (int)((v >> (4 * i)) & 15u); }
+
+// kv_time with stage orders: position a of the prefill pipeline is served by its stage
+// nib(op, a), position b of the decode pipeline by stage nib(od, b).  The walk stops once a
+// link reaches `cutoff` (the time returned is then >= cutoff, which the search discards).
+__device__ double kv_time_ord(const Problem& p, const uint8_t* pm, int ptp, int ppp, uint32_t op, const uint8_t* dm,
+                              int dtp, int dpp, uint32_t od, int stride, double cutoff) {
+    const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
+    const int deni = ptp * dtp;
+    const double den = (double)deni;
+    const bool pow2 = (deni & (deni - 1)) == 0;
+    const double inv_den = 1.0 / den;
+    const int lqp = p.L / ppp, lrp = p.L % ppp, lqd = p.L / dpp, lrd = p.L % dpp;
+    double worst = 0.0;
+    int a = 0, bb = 0, a0 = 0, b0 = 0;
+    int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
+    while (a < ppp && bb < dpp) {
+        const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+        const double Vn = V1 * (double)nab;
+        const uint8_t* Sa = pm + (nib(op, a) * ptp) * stride;
+        const uint8_t* Sb = dm + (nib(od, bb) * dtp) * stride;
+        int r = 0, q = 0;
+        while (r < ptp && q < dtp) {
+            const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+            const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+            const int g = Sa[r * stride], h = Sb[q * stride];
+            const double bytes = pow2 ? (Vn * (double)ov) * inv_den : (Vn * (double)ov) / den;
+            const double time = p.alpha[g * p.G + h] + bytes / p.beta[g * p.G + h];
+            if (time > worst) {
+                worst = time;
+                if (worst >= cutoff) return worst;
+            }
+            if (re <= qe) ++r;
+            if (qe <= re) ++q;
+        }
+        const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
+        if (adv_a) {
+            ++a;
+            a0 = a1;
+            a1 = a0 + lqp + (a < lrp ? 1 : 0);
+        }
+        if (adv_b) {
+            ++bb;
+            b0 = b1;
+            b1 = b0 + lqd + (bb < lrd ? 1 : 0);
+        }
+    }
+    return worst;
+}
+
+// The order pair with index k in [0, ppp! dpp!): k = kp * dpp! + kd, each order the
+// Lehmer-code unranking of its index (the lexicographic rank among the orders of its side).
+__device__ uint32_t unrank_order(int k, int n) {
+    uint32_t out = 0, used = 0;
+    for (int i = 0; i < n; ++i) {
+        const int f = order_count(n - 1 - i);
+        int idx = k / f;
+        k -= idx * f;
+        int v = 0;
+        for (;; ++v)
+            if (!((used >> v) & 1u) && idx-- == 0) break;
+        used |= 1u << v;
+        out |= (uint32_t)v << (4 * i);
+    }
+    return out;
+}
+
+// One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: every lane
+// first takes its ascending-order time; then the wavefront searches the order pairs of each
+// lane that has more than one, together: lane l tries pairs l, l + 64, ... with branch and
+// bound (a walk stops once it reaches the best time the lane has seen, starting from the
+// ascending time), and a wavefront minimum gives the edge's time.  The minimum is the same
+// value an exhaustive enumeration finds.  Per-replica granularity only.
+template <int W>
+__global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o, FlowNet f) {
+    extern __shared__ uint8_t sm[];
+    const int tid = threadIdx.x;  // kKvBlock = 64: one wavefront per workgroup
+    const int stride = kKvBlock;
+    const int64_t gid = (int64_t)blockIdx.x * kKvBlock + tid;
+    const int64_t N = p.N;
+    bool live = gid < (int64_t)f.max_pd * N;
+    const int e = live ? (int)(gid / N) : 0;
+    const int n = live ? (int)(gid - (int64_t)e * N) : 0;
+    const int np = live ? f.n_p[n] : 0, nd = live ? f.n_d[n] : 0;
+    live = live && e < np * nd;
+    int ptp = 0, ppp = 0, dtp = 0, dpp = 0;
+    bool feas = false;
+    double t = 0.0;
+    uint8_t* pm = sm + tid;
+    uint8_t* dm = sm + p.G * stride + tid;
+    if (live) {
+        const int i = e / nd, j = e - i * nd;
+        const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
+        ptp = o.tp[(int64_t)kp * N + n];
+        ppp = o.pp[(int64_t)kp * N + n];
+        dtp = o.tp[(int64_t)kd * N + n];
+        dpp = o.pp[(int64_t)kd * N + n];
+        feas = ptp > 0 && dtp > 0 && expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
+               expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp;
+        if (feas) t = kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride);
+    }
+    const int pairs = feas ? order_count(ppp) * order_count(dpp) : 1;
+    uint64_t todo = __ballot(feas && pairs > 1 && pairs <= kOrderPairs);
+    while (todo) {
+        const int owner = __ffsll((unsigned long long)todo) - 1;
+        todo &= todo - 1;
+        const int optp = __shfl(ptp, owner), oppp = __shfl(ppp, owner);
+        const int odtp = __shfl(dtp, owner), odpp = __shfl(dpp, owner);
+        const int opairs = __shfl(pairs, owner);
+        double best = __shfl(t, owner);
+        const int dfact = order_count(odpp);
+        for (int k = tid; k < opairs; k += kKvBlock) {
+            const int kp = k / dfact, kd = k - kp * dfact;
+            const double v = kv_time_ord(p, sm + owner, optp, oppp, unrank_order(kp, oppp), sm + p.G * stride + owner,
+                                         odtp, odpp, unrank_order(kd, odpp), stride, best);
+            if (v < best) best = v;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+            const double u = __shfl_xor(best, off);
+            best = u < best ? u : best;
+        }
+        if (tid == owner) t = best;
+    }
+    if (!live) return;
+    f.kv_cap[(int64_t)e * N + n] = feas ? quantize(1000.0 / t) : 0;
+}
+
 template <int W>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ uint8_t sm[];
@@ -222,7 +363,10 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
     const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
     prof_mark(kKKv, false, s);
-    hipLaunchKernelGGL(kv_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    if (p.granularity == 0 && (p.variant & HX_VARIANT_KV_ORDER))
+        hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    else
+        hipLaunchKernelGGL(kv_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     prof_mark(kKKv, true, s);
     return hipGetLastError();
 }

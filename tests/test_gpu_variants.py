@@ -79,9 +79,51 @@ def test_pipelined_per_gpu_nodes(torch):
 
 
 def test_unknown_variant_rejected(torch):
-    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=2)
+    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=4)
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp)
     with pytest.raises(hx.HxError) as e:
         hx.cost_eval(dp, ws.cost)
     assert e.value.code == hx.HX_EINVAL
+
+
+ORDER = 2
+
+
+@pytest.mark.parametrize("cfg,n,variant", [(1, None, ORDER), (2, None, ORDER), (3, 16384, ORDER), (4, 2048, ORDER),
+                                           (2, 777, ORDER | PIPE), (3, 4096, ORDER | PIPE)])
+def test_kv_order_parity(torch, cfg, n, variant):
+    """KV stage-order search (alone and with the pipelined capacity): KV capacities, flows and
+    the best candidate equal the oracle's; every KV capacity is at least the ascending-order
+    one."""
+    prob = dataclasses.replace(I.make_problem(cfg, n_cand=n), variant=variant)
+    say(f"KV stage-order search: workload {cfg}, N={prob.n_cand}, variant {variant}")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    for k in ("tp", "pp", "bmax", "cap", "lat"):
+        assert np.array_equal(cost[k], want["cost"][k]), k
+    Hh.compare_flownet(fn, want["flownet"])
+    assert np.array_equal(fv, want["flow_value"])
+    assert best == want["best"]
+    asc = hxo.build_flownet(dataclasses.replace(prob, variant=variant & ~ORDER),
+                            hxo.cost_eval(dataclasses.replace(prob, variant=variant & ~ORDER)))
+    up, ud, upd = Hh.used_rows(fn)
+    assert (fn["kv_cap"][upd] >= asc["kv_cap"][upd]).all()
+
+
+def test_kv_order_crossed_links(torch):
+    """The hand-derived crossed-link case: the searched order pairs the 300 GB/s links."""
+    G = 4
+    beta = np.full((G, G), 10e9)
+    for a, b in ((0, 3), (1, 2)):
+        beta[a, b] = beta[b, a] = 300e9
+    np.fill_diagonal(beta, 0.0)
+    t = np.array([I.GPU_TYPES["A"]], np.float64)
+    cl = I.Cluster(np.zeros(G, np.int32), t[:, 0].copy(), t[:, 1].copy(), t[:, 2].copy(),
+                   np.ascontiguousarray(beta.reshape(-1)), np.zeros(G * G))
+    a, r = I.placement_from_groups([[0, 1], [2, 3]], [I.PREFILL, I.DECODE], 4, 2)
+    for variant, bw in ((0, 10e9), (ORDER, 300e9)):
+        prob = dataclasses.replace(Hh.problem(cl, dict(I.OPT_30B), a, r, tp=(1,), pp=(2,)), variant=variant)
+        _, fn, _, _ = _gpu(torch, prob)
+        V = 2.0 * 512.0 * 7168 * 2 * 24
+        assert int(fn["kv_cap"][0, 0]) == int(np.floor(1000.0 / (V / bw)))
