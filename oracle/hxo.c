@@ -1023,3 +1023,198 @@ int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------ graph partition (Sec. 3.2) */
+
+/*
+ * The first phase of the scheduler (Sec. 3.2) as a candidate generator.  The device graph has
+ * the GPUs as nodes, weighted by their memory limits, and the links as edges, weighted by
+ * bandwidth.  Readings (the paper names the methods, not their parameters):
+ *   - edge weight w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6): the symmetrised bandwidth in
+ *     whole MB/s, so that every cut and gain below is an exact integer sum; node weight = the
+ *     memory limit in whole bytes;
+ *   - Step (i), initial partition: spectral order by the Fiedler direction of the Laplacian
+ *     Deg - w (power iteration, hxo_spectral_order), cut into K contiguous groups of balanced
+ *     memory; K = floor(total memory / replica memory), a replica holding the weights and the
+ *     KV caches of 32 requests (Appendix A: 12 H^2 B L + 32 * 2 (s_in + s_out) H_kv B L);
+ *     then Kernighan-Lin: repeatedly the pair swap between two groups with the largest cut
+ *     reduction, among swaps that do not widen the memory gap between the two groups;
+ *   - Step (ii), coarsen and secondary partition: groups become super nodes joined by the
+ *     summed weights of their links; a local search for a maximum cut splits them into
+ *     prefill and decode replicas (single flips with the largest gain, both sides kept);
+ *   - Step (iii), projection: every GPU takes its group; groups are numbered by smallest member.
+ * Candidates of one batch differ by a 64-bit draw each: bits 0-2 shift K by (v mod 5) - 2,
+ * bits 3-10 rotate the spectral order by (v mod G), bits 11-42 set the initial side of super
+ * node k (bit 11 + k).
+ */
+
+static int64_t pg_weight(const hxo_cluster *c, int d, int e)
+{
+    if (d == e) return 0;
+    return (int64_t)floor(((beta_of(c, d, e) + beta_of(c, e, d)) * 0.5) / 1.0e6);
+}
+
+/* Spectral order: iters power iterations on (cap I - Lap), Lap = Deg - w, cap = 2 max_d Deg_d,
+ * from x_d = d - (G-1)/2, each iteration removing the mean (the constant eigenvector) and
+ * normalising; every sum runs in ascending index order.  order = GPUs sorted by (x_d, d);
+ * fiedler (nullable) receives x. */
+int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, double *fiedler)
+{
+    const int G = c->n_gpus;
+    double *x = (double *)malloc(sizeof(double) * G), *y = (double *)malloc(sizeof(double) * G);
+    double *deg = (double *)malloc(sizeof(double) * G);
+    double cap = 0.0;
+    for (int d = 0; d < G; d++) {
+        int64_t s = 0;
+        for (int e = 0; e < G; e++) s += pg_weight(c, d, e);
+        deg[d] = (double)s;
+        if (2.0 * deg[d] > cap) cap = 2.0 * deg[d];
+    }
+    for (int d = 0; d < G; d++) x[d] = (double)d - (double)(G - 1) * 0.5;
+    for (int it = 0; it < iters; it++) {
+        for (int d = 0; d < G; d++) {
+            double s = 0.0;
+            for (int e = 0; e < G; e++) s = s + (double)pg_weight(c, d, e) * x[e];
+            y[d] = (cap - deg[d]) * x[d] + s;
+        }
+        double mean = 0.0;
+        for (int d = 0; d < G; d++) mean = mean + y[d];
+        mean = mean / (double)G;
+        double nrm = 0.0;
+        for (int d = 0; d < G; d++) {
+            y[d] = y[d] - mean;
+            nrm = nrm + y[d] * y[d];
+        }
+        nrm = sqrt(nrm);
+        if (!(nrm > 0.0)) break;
+        for (int d = 0; d < G; d++) x[d] = y[d] / nrm;
+    }
+    for (int d = 0; d < G; d++) order[d] = d;
+    for (int i = 1; i < G; i++) {  /* insertion sort by (x, id) */
+        int v = order[i], j = i - 1;
+        while (j >= 0 && (x[order[j]] > x[v] || (x[order[j]] == x[v] && order[j] > v))) {
+            order[j + 1] = order[j];
+            j--;
+        }
+        order[j + 1] = v;
+    }
+    if (fiedler)
+        for (int d = 0; d < G; d++) fiedler[d] = x[d];
+    free(x); free(y); free(deg);
+    return 0;
+}
+
+/* K of the initial partition before the per-candidate shift. */
+int32_t hxo_partition_groups(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w)
+{
+    const double H = m->hidden, Hkv = kv_hidden(m), B = m->bytes_per_elem, L = m->n_layers;
+    double total = 0.0;
+    for (int d = 0; d < c->n_gpus; d++) total = total + (double)(int64_t)memlim_of(c, d);
+    const double rep = 12.0 * H * H * B * L + 32.0 * (2.0 * (w->s_in + w->s_out) * Hkv * B * L);
+    return (int32_t)floor(total / rep);
+}
+
+static int64_t iabs64(int64_t v) { return v < 0 ? -v : v; }
+
+int hxo_partition_candidates(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                             const int32_t *order, int32_t max_groups, int32_t n_cand, const uint64_t *rnd,
+                             uint8_t *assign, uint8_t *role)
+{
+    const int G = c->n_gpus;
+    int kmax = max_groups < G ? max_groups : G;
+    if (kmax > 32) kmax = 32;
+    const int32_t k_est = hxo_partition_groups(c, m, w);
+    int64_t *mem = (int64_t *)malloc(sizeof(int64_t) * G);
+    int64_t total = 0;
+    for (int d = 0; d < G; d++) {
+        mem[d] = (int64_t)memlim_of(c, d);
+        total += mem[d];
+    }
+    int *grp = (int *)malloc(sizeof(int) * G);
+    int64_t *gmem = (int64_t *)malloc(sizeof(int64_t) * 256);
+    int64_t *sw = (int64_t *)malloc(sizeof(int64_t) * 32 * 32);
+    for (int n = 0; n < n_cand; n++) {
+        const uint64_t r = rnd[n];
+        int K = k_est + (int)((r & 7) % 5) - 2;
+        if (K > kmax) K = kmax;
+        if (K < 2) K = 2;
+        const int rot = (int)(((r >> 3) & 0xFF) % (uint64_t)G);
+        /* step (i): balanced contiguous cut of the rotated spectral order, by memory midpoints */
+        int64_t cum = 0;
+        for (int i = 0; i < G; i++) {
+            const int d = order[(i + rot) % G];
+            int k = (int)(((int64_t)K * (2 * cum + mem[d])) / (2 * total));
+            grp[d] = k < K - 1 ? k : K - 1;
+            cum += mem[d];
+        }
+        for (int k = 0; k < K; k++) gmem[k] = 0;
+        for (int d = 0; d < G; d++) gmem[grp[d]] += mem[d];
+        /* Kernighan-Lin pair swaps */
+        for (int step = 0; step < 2 * G; step++) {
+            int64_t best = 0;
+            int bu = -1, bv = -1;
+            for (int u = 0; u < G; u++)
+                for (int v = u + 1; v < G; v++) {
+                    const int A = grp[u], Bk = grp[v];
+                    if (A == Bk) continue;
+                    const int64_t gap0 = iabs64(gmem[A] - gmem[Bk]);
+                    const int64_t gap1 = iabs64((gmem[A] - mem[u] + mem[v]) - (gmem[Bk] - mem[v] + mem[u]));
+                    if (gap1 > gap0) continue;
+                    int64_t gu = 0, gv = 0;  /* cut reduction of moving u to B and v to A */
+                    for (int x = 0; x < G; x++) {
+                        if (x == u || x == v) continue;
+                        if (grp[x] == Bk) gu += pg_weight(c, u, x);
+                        if (grp[x] == A) gu -= pg_weight(c, u, x);
+                        if (grp[x] == A) gv += pg_weight(c, v, x);
+                        if (grp[x] == Bk) gv -= pg_weight(c, v, x);
+                    }
+                    const int64_t gain = gu + gv;
+                    if (gain > best) { best = gain; bu = u; bv = v; }
+                }
+            if (bu < 0) break;
+            const int A = grp[bu], Bk = grp[bv];
+            gmem[A] += mem[bv] - mem[bu];
+            gmem[Bk] += mem[bu] - mem[bv];
+            grp[bu] = Bk;
+            grp[bv] = A;
+        }
+        /* step (iii) numbering: groups by smallest member */
+        int map[256], used = 0;
+        for (int k = 0; k < 256; k++) map[k] = -1;
+        for (int d = 0; d < G; d++)
+            if (map[grp[d]] < 0) map[grp[d]] = used++;
+        for (int d = 0; d < G; d++) grp[d] = map[grp[d]];
+        /* step (ii): coarsened weights and the max-cut split */
+        for (int k = 0; k < used * used; k++) sw[k] = 0;
+        for (int d = 0; d < G; d++)
+            for (int e = 0; e < G; e++)
+                if (grp[d] != grp[e]) sw[grp[d] * used + grp[e]] += pg_weight(c, d, e);
+        int side[32], n1 = 0;
+        for (int k = 0; k < used; k++) {
+            side[k] = (int)((r >> (11 + k)) & 1);
+            n1 += side[k];
+        }
+        if (n1 == 0 || n1 == used) { side[used - 1] ^= 1; n1 += side[used - 1] ? 1 : -1; }
+        for (int step = 0; step < used * used; step++) {
+            int64_t best = 0;
+            int bk = -1;
+            for (int k = 0; k < used; k++) {
+                if ((side[k] && n1 == 1) || (!side[k] && n1 == used - 1)) continue;  /* keep both sides */
+                int64_t gain = 0;
+                for (int l = 0; l < used; l++) {
+                    if (l == k) continue;
+                    gain += side[l] == side[k] ? sw[k * used + l] : -sw[k * used + l];
+                }
+                if (gain > best) { best = gain; bk = k; }
+            }
+            if (bk < 0) break;
+            n1 += side[bk] ? -1 : 1;
+            side[bk] ^= 1;
+        }
+        for (int d = 0; d < G; d++) assign[(int64_t)d * n_cand + n] = (uint8_t)grp[d];
+        for (int k = 0; k < max_groups; k++)
+            role[(int64_t)k * n_cand + n] = k < used ? (uint8_t)(side[k] ? HXO_DECODE : HXO_PREFILL) : (uint8_t)HXO_UNUSED;
+    }
+    free(mem); free(grp); free(gmem); free(sw);
+    return 0;
+}

@@ -277,3 +277,35 @@ def guided_moves(n_gpus: int, max_groups: int, granularity: int, p_assign: np.nd
                            _p(cls["node_cls"]), _p(cls["kv_cls"]), C.c_int32(Nc), _p(rnd),
                            _p(out["assign"]), _p(out["role"]), _p(out["move"]))
     return out
+
+
+# ------------------------------------------------------------------ graph partition (Sec. 3.2)
+
+def spectral_order(prob, iters: int = 1000) -> Tuple[np.ndarray, np.ndarray]:
+    """(order, fiedler): GPUs sorted by the power-iteration Fiedler direction, and that vector."""
+    a = _Args(prob)
+    G = prob.n_gpus
+    order = np.zeros(G, np.int32)
+    x = np.zeros(G, np.float64)
+    lib().hxo_spectral_order(C.byref(a.cluster), C.c_int32(iters), _p(order), _p(x))
+    return order, x
+
+
+def partition_groups(prob) -> int:
+    a = _Args(prob)
+    lib().hxo_partition_groups.restype = C.c_int32
+    return int(lib().hxo_partition_groups(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl)))
+
+
+def partition_candidates(prob, order: np.ndarray, rnd: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Candidates of the first phase (initial partition, Kernighan-Lin, coarsen and max-cut split,
+    projection), one per draw: assign [G][N], role [max_groups][N]."""
+    a = _Args(prob)
+    rnd = np.ascontiguousarray(rnd, np.uint64)
+    N = rnd.shape[0]
+    assign = np.zeros((prob.n_gpus, N), np.uint8)
+    role = np.zeros((prob.max_groups, N), np.uint8)
+    lib().hxo_partition_candidates(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl),
+                                   _p(np.ascontiguousarray(order, np.int32)), C.c_int32(prob.max_groups),
+                                   C.c_int32(N), _p(rnd), _p(assign), _p(role))
+    return assign, role

@@ -395,6 +395,14 @@ def make_problem(cfg: int, n_cand: Optional[int] = None, rnd: int = 0,
 GUIDED_STREAM = 1 << 20   # seed stream of guided refinement round r: GUIDED_STREAM + r
 
 
+PARTITION_STREAM = 1 << 21   # seed stream of the graph-partition candidate draws
+
+
+def partition_draws(cfg: int, n: int) -> np.ndarray:
+    """Uniform 64-bit draws, one per candidate of the graph-partition generator."""
+    return _rng(cfg, PARTITION_STREAM).integers(0, 2**64, size=n, dtype=np.uint64, endpoint=False)
+
+
 def move_draws(cfg: int, rnd: int, n: int) -> np.ndarray:
     """The uniform 64-bit draws of guided refinement round rnd of workload cfg, one per child
     (the move generator takes its random choices from them)."""
