@@ -1054,15 +1054,33 @@ static int64_t pg_weight(const hxo_cluster *c, int d, int e)
     return (int64_t)floor(((beta_of(c, d, e) + beta_of(c, e, d)) * 0.5) / 1.0e6);
 }
 
+/* Sum of v[0..G) (G <= 256) in a fixed association: 64 partial sums t_l = ((v_l + v_{l+64}) +
+ * v_{l+128}) + v_{l+192} (terms past G left out, t_l = 0 when l >= G), then six butterfly
+ * steps t_l <- t_l + t_{l xor s} for s = 32, 16, ..., 1; the result is t_0. */
+static double tree_sum(const double *v, int G)
+{
+    double t[64], u[64];
+    for (int l = 0; l < 64; l++) {
+        t[l] = l < G ? v[l] : 0.0;
+        for (int k = 1; k < 4; k++)
+            if (l + 64 * k < G) t[l] = t[l] + v[l + 64 * k];
+    }
+    for (int s = 32; s > 0; s >>= 1) {
+        for (int l = 0; l < 64; l++) u[l] = t[l] + t[l ^ s];
+        for (int l = 0; l < 64; l++) t[l] = u[l];
+    }
+    return t[0];
+}
+
 /* Spectral order: iters power iterations on (cap I - Lap), Lap = Deg - w, cap = 2 max_d Deg_d,
  * from x_d = d - (G-1)/2, each iteration removing the mean (the constant eigenvector) and
- * normalising; every sum runs in ascending index order.  order = GPUs sorted by (x_d, d);
- * fiedler (nullable) receives x. */
+ * normalising; a row's product runs in ascending index order, the mean and the norm use
+ * tree_sum.  order = GPUs sorted by (x_d, d); fiedler (nullable) receives x. */
 int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, double *fiedler)
 {
     const int G = c->n_gpus;
     double *x = (double *)malloc(sizeof(double) * G), *y = (double *)malloc(sizeof(double) * G);
-    double *deg = (double *)malloc(sizeof(double) * G);
+    double *deg = (double *)malloc(sizeof(double) * G), *sq = (double *)malloc(sizeof(double) * G);
     double cap = 0.0;
     for (int d = 0; d < G; d++) {
         int64_t s = 0;
@@ -1077,15 +1095,12 @@ int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, doub
             for (int e = 0; e < G; e++) s = s + (double)pg_weight(c, d, e) * x[e];
             y[d] = (cap - deg[d]) * x[d] + s;
         }
-        double mean = 0.0;
-        for (int d = 0; d < G; d++) mean = mean + y[d];
-        mean = mean / (double)G;
-        double nrm = 0.0;
+        const double mean = tree_sum(y, G) / (double)G;
         for (int d = 0; d < G; d++) {
             y[d] = y[d] - mean;
-            nrm = nrm + y[d] * y[d];
+            sq[d] = y[d] * y[d];
         }
-        nrm = sqrt(nrm);
+        const double nrm = sqrt(tree_sum(sq, G));
         if (!(nrm > 0.0)) break;
         for (int d = 0; d < G; d++) x[d] = y[d] / nrm;
     }
@@ -1100,7 +1115,7 @@ int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, doub
     }
     if (fiedler)
         for (int d = 0; d < G; d++) fiedler[d] = x[d];
-    free(x); free(y); free(deg);
+    free(x); free(y); free(deg); free(sq);
     return 0;
 }
 
