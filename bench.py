@@ -85,7 +85,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
     ap.add_argument("--refine", action="store_true",
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
+    ap.add_argument("--partition", action="store_true",
+                    help="time the graph-partition candidate generator (spectral order, partition, scoring) instead")
     ap.add_argument("--children", type=int, default=131072, help="children per refinement round (--refine)")
+    ap.add_argument("--partition-candidates", type=int, default=16384, help="candidates per step (--partition)")
+    ap.add_argument("--spectral-iters", type=int, default=1000, help="power iterations (--partition)")
     ap.add_argument("--quality-rounds", type=int, default=8,
                     help="--refine: also run this many guided and random-perturbation rounds and report the best")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -370,6 +374,76 @@ def refine_main(args, torch, hx, I):
     print(json.dumps(out))
 
 
+def partition_main(args, torch, hx, I):
+    """The first phase of Sec. 3.2 as a candidate generator on the headline workload: one
+    spectral order, then --partition-candidates candidates (one draw each), each scored by the
+    hot path.  value = candidates generated and scored per second."""
+    cfg = args.workload
+    wl = I.WORKLOADS[cfg]
+    n = args.partition_candidates
+    prob = I.make_problem(cfg, n_cand=1)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.partition_workspace(dp)
+    order = torch.empty(prob.n_gpus, dtype=torch.int32, device="cuda")
+    rnd = torch.as_tensor(I.partition_draws(cfg, n).view(np.int64)).to("cuda")
+    assign = torch.empty((prob.n_gpus, n), dtype=torch.uint8, device="cuda")
+    role = torch.empty((prob.max_groups, n), dtype=torch.uint8, device="cuda")
+    cand = dp.with_candidates(assign, role)
+    wsc = hx.Workspace.for_problem(cand)
+
+    def step():
+        hx.spectral_order(dp, ws, order, iters=args.spectral_iters)
+        hx.partition_candidates(dp, ws, order, rnd, assign, role)
+        hx.score(cand, wsc)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    hx.profile(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    prof = hx.profile_read()
+    hx.profile(False)
+    kernel_us = {k: 1000.0 * v / c for k, (v, c) in prof.items() if c > 0}
+    best = [int(x) for x in wsc.best.cpu().numpy()]
+    # the partition kernel against HBM: its algorithmic bytes are the candidates it writes (the
+    # weight table and order stay in cache); its time goes to Kernighan-Lin steps, each a
+    # workgroup-wide scan of the GPU pairs and two barriers, so the fraction is small
+    t_part = kernel_us["partition"] * 1e-6
+    out_bytes = n * (prob.n_gpus + prob.max_groups)
+    out = {
+        "metric": "graph-partition candidates generated and scored/sec (Sec. 3.2 first phase + hot path) at 1 GPU",
+        "value": n / (ms / 1000.0),
+        "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64+i64", "data": "synthetic",
+        "config": {"workload": f"workload{wl.cfg}: {wl.name}, graph-partition candidates", "candidates": n,
+                   "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "spectral_iters": args.spectral_iters},
+        "kernel_us": kernel_us,
+        "best": best,
+        "partition_roofline": {"kernel": "partition (hx_partition_candidates)", "bound": "hbm",
+                               "achieved": out_bytes / t_part / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": out_bytes / t_part / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                               "algorithmic_bytes_per_launch": out_bytes, "avg_launch_us": kernel_us["partition"]},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import hxo  # test infrastructure: only this baseline leg uses it
+        t = time.perf_counter()
+        o_order, _ = hxo.spectral_order(prob, args.spectral_iters)
+        m = 64
+        hxo.partition_candidates(prob, o_order, I.partition_draws(cfg, m))
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": m / dt, "unit": "candidates/s (generation only)", "cores": 1,
+                               "kind": "oracle", "sample": f"spectral order + {m} candidates, one thread"}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -396,6 +470,9 @@ def main():
         del src, dst
     if args.refine:
         refine_main(args, torch, hx, I)
+        return
+    if args.partition:
+        partition_main(args, torch, hx, I)
         return
     wl = I.WORKLOADS[args.workload]
     prob = I.make_problem(args.workload)

@@ -21,6 +21,11 @@
  *   hx_guided_moves       children of the best placements          (one lane per child)
  *   hx_gather_candidates  the chosen candidates into a new batch   (one lane per byte)
  *
+ * and the graph-partition phase of Sec. 3.2 that generates candidates in the first place:
+ *
+ *   hx_spectral_order        the Fiedler order of the device graph  (one workgroup)
+ *   hx_partition_candidates  partition, swaps, role split per draw  (one workgroup per candidate)
+ *
  * Conventions
  *   - Every array pointer is a DEVICE pointer unless marked [host].  The caller owns every
  *     buffer; libhx allocates no device memory and keeps no state between calls.
@@ -266,6 +271,47 @@ int hx_guided_moves(int32_t n_gpus, int32_t granularity, const hx_candidates *pa
 int hx_gather_candidates(int32_t n_gpus, const hx_candidates *src, const int32_t *index, int32_t count,
                          uint8_t *dst_assign, uint8_t *dst_role, hipStream_t stream);
 
+/* ---------------------------------------------------------------- graph partition (Sec. 3.2)
+ * The first phase of the scheduler as a candidate generator: the device graph (GPUs weighted by
+ * memory, links by bandwidth) is partitioned into K groups (spectral order, then Kernighan-Lin
+ * swaps), the groups are coarsened into super nodes and split into prefill and decode replicas
+ * by a cut of maximum weight, and the partition is projected back onto the GPUs.  Edge weights
+ * are w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6) clamped to [0, 2^23] (whole MB/s), node
+ * weights the memory limits in whole bytes, so cuts and gains are exact integer sums. */
+
+/* Device scratch both calls need (an [n_gpus][n_gpus] int32 weight table they fill first);
+ * 0 for n_gpus outside [2, 255]. */
+size_t hx_partition_workspace_bytes(int32_t n_gpus);
+
+/* Spectral order: the GPUs sorted by (x_d, d), x the Fiedler direction of the Laplacian
+ * Deg - w by `iters` power iterations on (c I - Lap), c = 2 max_d Deg_d, from x_d = d - (G-1)/2,
+ * each iteration taking out the mean and normalising.  A row's product sums in ascending index
+ * order; the mean and the norm sum by a fixed tree: 64 partial sums t_l = ((v_l + v_{l+64}) +
+ * v_{l+128}) + v_{l+192}, then t_l <- t_l + t_{l xor s} for s = 32, 16, ..., 1.  One workgroup.
+ *   order [n_gpus] device int32 out; fiedler [n_gpus] device double out, nullable. */
+int hx_spectral_order(const hx_cluster *cluster, int32_t iters, void *workspace, size_t workspace_bytes,
+                      int32_t *order, double *fiedler, hipStream_t stream);
+
+/* n_cand candidates of the first phase, one per 64-bit draw rnd[n]:
+ *   K = floor(total memory / (12 H^2 B L + 32 * (2 (s_in + s_out) H_kv B L))) (a replica holds the
+ *       weights and the KV caches of 32 requests, Appendix A), plus (bits 0-2 mod 5) - 2,
+ *       clamped to [2, min(n_gpus, max_groups, 32)];
+ *   step (i): the spectral order rotated by (bits 3-10 mod n_gpus); the i-th GPU d of it goes to
+ *       group min(K-1, floor(K (2 C_i + m_d) / (2 M))), C_i the memory before it, M the total;
+ *       then Kernighan-Lin: while some swap of two GPUs of different groups lowers the cut and
+ *       does not widen the memory gap between the two groups, the swap with the largest
+ *       reduction (lowest (u, v) on ties) is applied, at most 2 n_gpus times;
+ *   groups are numbered by smallest member;
+ *   step (ii): super node k starts on side bit (11 + k) of the draw (the last one flipped if all
+ *       agree); while flipping one super node raises the coarse cut with both sides occupied,
+ *       the flip with the largest gain (lowest k on ties) is applied; side 0 = prefill;
+ *   step (iii): assign[g][n] = the group of GPU g, role[k][n] = its side for k below the group
+ *       count, HX_UNUSED beyond.
+ *   order: the spectral order (hx_spectral_order).  One workgroup per candidate. */
+int hx_partition_candidates(const hx_cluster *cluster, hx_model model, hx_workload wl, int32_t max_groups,
+                            void *workspace, size_t workspace_bytes, const int32_t *order, int32_t n_cand,
+                            const uint64_t *rnd, uint8_t *assign, uint8_t *role, hipStream_t stream);
+
 /* Diagnostic per-kernel timing (not part of the scoring path; process-global, for one host
  * thread).  hx_profile(1) clears earlier records and makes every later launch by libhx record a
  * HIP event on the call's stream before and after each of its kernels; hx_profile(0) stops
@@ -274,8 +320,9 @@ int hx_gather_candidates(int32_t n_gpus, const hx_candidates *src, const int32_t
  * clears the records; n >= HX_KERNELS.  Returns HX_KERNELS or a negative error.  hx_kernel_name
  * gives kernel k's name: setup, decode, scatter, eval (hx_cost_eval), nodes, kv
  * (hx_build_flownet), maxflow, best, classes (hx_edge_classes), moves (hx_guided_moves),
- * gather (hx_gather_candidates). */
-#define HX_KERNELS 11
+ * gather (hx_gather_candidates), spectral (hx_spectral_order), partition
+ * (hx_partition_candidates). */
+#define HX_KERNELS 13
 int hx_profile(int32_t enable);
 int hx_profile_read(double *ms, int32_t *launches, int32_t n);
 const char *hx_kernel_name(int32_t k);

@@ -240,8 +240,9 @@ int hx_profile_read(double* ms, int32_t* launches, int32_t n) {
 }
 
 const char* hx_kernel_name(int32_t k) {
-    static const char* names[hx::kKCount] = {"setup",   "decode", "scatter", "eval",  "nodes", "kv",
-                                             "maxflow", "best",   "classes", "moves", "gather"};
+    static const char* names[hx::kKCount] = {"setup", "decode",  "scatter", "eval",     "nodes",
+                                             "kv",    "maxflow", "best",    "classes",  "moves",
+                                             "gather", "spectral", "partition"};
     return k >= 0 && k < hx::kKCount ? names[k] : "";
 }
 
@@ -339,6 +340,35 @@ int hx_guided_moves(int32_t n_gpus, int32_t granularity, const hx_candidates* pa
     hipError_t e = hx::launch_moves(n_gpus, parents->max_groups, granularity, parents->n_cand, parents->assign,
                                     parents->role, make_net(parent_net), node_cls, n_child, rnd, child_assign,
                                     child_role, move, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+size_t hx_partition_workspace_bytes(int32_t n_gpus) {
+    if (n_gpus < 2 || n_gpus > HX_MAX_GPUS) return 0;
+    return ((size_t)n_gpus * n_gpus * sizeof(int32_t) + 255) & ~(size_t)255;
+}
+
+int hx_spectral_order(const hx_cluster* cluster, int32_t iters, void* workspace, size_t workspace_bytes,
+                      int32_t* order, double* fiedler, hipStream_t stream) {
+    if (!cluster || cluster->n_gpus < 2 || cluster->n_gpus > HX_MAX_GPUS || !cluster->beta || !order) return HX_EINVAL;
+    if (iters < 0 || !workspace || workspace_bytes < hx_partition_workspace_bytes(cluster->n_gpus)) return HX_EINVAL;
+    hipError_t e = hx::launch_spectral(cluster->n_gpus, cluster->beta, static_cast<int32_t*>(workspace), iters, order,
+                                       fiedler, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_partition_candidates(const hx_cluster* cluster, hx_model model, hx_workload wl, int32_t max_groups,
+                            void* workspace, size_t workspace_bytes, const int32_t* order, int32_t n_cand,
+                            const uint64_t* rnd, uint8_t* assign, uint8_t* role, hipStream_t stream) {
+    const hx_space sp{1u, 1u, 0, 0u};
+    const hx_candidates cand{n_cand, max_groups, assign, role};
+    int rc = check_problem(cluster, model, wl, sp, &cand);
+    if (rc) return rc;
+    if (cluster->n_gpus < 2 || !order || !rnd || !workspace ||
+        workspace_bytes < hx_partition_workspace_bytes(cluster->n_gpus))
+        return HX_EINVAL;
+    hipError_t e = hx::launch_partition(make_problem(cluster, model, wl, sp, &cand), static_cast<int32_t*>(workspace),
+                                        order, rnd, assign, role, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

@@ -50,7 +50,8 @@ __device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / p
 
 // Kernels of libhx, for the diagnostic per-kernel timing behind hx_profile.
 enum KernelId {
-    kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKClasses, kKMoves, kKGather, kKCount
+    kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKClasses, kKMoves, kKGather,
+    kKSpectral, kKPartition, kKCount
 };
 // While profiling is enabled, records a HIP event on s before (end = false) or after
 // (end = true) a launch of kernel k; does nothing otherwise.
@@ -75,6 +76,11 @@ hipError_t launch_classes(const FlowNet& f, const int32_t* flow_value, const int
 hipError_t launch_moves(int32_t G, int32_t K, int32_t gran, int32_t M, const uint8_t* p_assign,
                         const uint8_t* p_role, const FlowNet& pn, const uint8_t* node_cls, int32_t n_child,
                         const uint64_t* rnd, uint8_t* c_assign, uint8_t* c_role, int32_t* move, hipStream_t s);
+// Graph partition (Sec. 3.2): w is an [G][G] int32 scratch both calls fill first.
+hipError_t launch_spectral(int32_t G, const double* beta, int32_t* w, int32_t iters, int32_t* order, double* fiedler,
+                           hipStream_t s);
+hipError_t launch_partition(const Problem& p, int32_t* w, const int32_t* order, const uint64_t* rnd, uint8_t* assign,
+                            uint8_t* role, hipStream_t s);
 hipError_t launch_gather(int32_t G, int32_t K, int32_t Ns, const uint8_t* sa, const uint8_t* sr, const int32_t* index,
                          int32_t count, uint8_t* da, uint8_t* dr, hipStream_t s);
 

@@ -74,8 +74,9 @@ class hx_flownet(C.Structure):
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
            "hx_maxflow_batch", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves", "hx_gather_candidates",
+           "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
            "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error", "hx_abi_version")
-HX_KERNELS = 11
+HX_KERNELS = 13
 
 _lib = None
 
@@ -105,6 +106,12 @@ def lib() -> C.CDLL:
                                       C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_gather_candidates.argtypes = [C.c_int32, P(hx_candidates), C.c_void_p, C.c_int32, C.c_void_p,
                                            C.c_void_p, C.c_void_p]
+        L.hx_partition_workspace_bytes.argtypes = [C.c_int32]
+        L.hx_partition_workspace_bytes.restype = C.c_size_t
+        L.hx_spectral_order.argtypes = [P(hx_cluster), C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p,
+                                        C.c_void_p]
+        L.hx_partition_candidates.argtypes = [P(hx_cluster), hx_model, hx_workload, C.c_int32, C.c_void_p, C.c_size_t,
+                                              C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_profile.argtypes = [C.c_int32]
         L.hx_profile.restype = C.c_int
         L.hx_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
@@ -438,3 +445,30 @@ class Refiner:
         guided_moves(p, pw.net, self.node_cls, rnd, ch.tensors["assign"], ch.tensors["role"], self.move, stream)
         score(ch, cw, stream)
         gather_candidates(ch, cw.best[:1], p.tensors["assign"], p.tensors["role"], stream)
+
+
+# ------------------------------------------------------------------ graph partition (Sec. 3.2)
+
+def partition_workspace(dp: DeviceProblem, device: str = "cuda"):
+    torch = _torch()
+    nb = int(lib().hx_partition_workspace_bytes(dp.n_gpus))
+    if nb <= 0:
+        raise ValueError("the partition needs 2..255 GPUs")
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def spectral_order(dp: DeviceProblem, workspace, order, fiedler=None, iters: int = 1000, stream=None):
+    """GPUs sorted along the Fiedler direction of the device graph (hx_spectral_order)."""
+    _check(lib().hx_spectral_order(C.byref(dp.cluster), C.c_int32(iters), _ptr(workspace),
+                                   C.c_size_t(int(workspace.numel())), _ptr(order), _ptr(fiedler), _stream(stream)),
+           "hx_spectral_order")
+    return order
+
+
+def partition_candidates(dp: DeviceProblem, workspace, order, rnd, assign, role, stream=None):
+    """One first-phase candidate per draw (hx_partition_candidates) into assign [G][N] / role [Kmax][N]."""
+    _check(lib().hx_partition_candidates(C.byref(dp.cluster), dp.model, dp.workload, C.c_int32(dp.max_groups),
+                                         _ptr(workspace), C.c_size_t(int(workspace.numel())), _ptr(order),
+                                         C.c_int32(int(rnd.shape[0])), _ptr(rnd), _ptr(assign), _ptr(role),
+                                         _stream(stream)), "hx_partition_candidates")
+    return assign, role

@@ -153,6 +153,24 @@ def test_refinement_calls_reject_before_any_device_work():
     assert L.hx_gather_candidates(32, C.byref(src), FAKE, 1, None, FAKE, None) == hx.HX_EINVAL
 
 
+def test_partition_calls_reject_before_any_device_work():
+    cl, md, wl, sp, cand, cost, net = _args()
+    L = hx.lib()
+    assert L.hx_partition_workspace_bytes(1) == 0 and L.hx_partition_workspace_bytes(256) == 0
+    need = L.hx_partition_workspace_bytes(32)
+    assert need >= 32 * 32 * 4
+    assert L.hx_spectral_order(C.byref(cl), 100, FAKE, need - 1, FAKE, None, None) == hx.HX_EINVAL
+    assert L.hx_spectral_order(C.byref(cl), 100, FAKE, need, None, None, None) == hx.HX_EINVAL
+    assert L.hx_spectral_order(C.byref(cl), -1, FAKE, need, FAKE, None, None) == hx.HX_EINVAL
+    args = [C.byref(cl), md, wl, 16, FAKE, need, FAKE, 100, FAKE, FAKE, FAKE, None]
+    for i, bad in ((3, 0), (4, None), (5, need - 1), (6, None), (7, 0), (8, None), (9, None), (10, None)):
+        a = list(args)
+        a[i] = bad
+        assert L.hx_partition_candidates(*a) == hx.HX_EINVAL, (i, bad)
+    cl.n_gpus = 1
+    assert L.hx_spectral_order(C.byref(cl), 100, FAKE, need, FAKE, None, None) == hx.HX_EINVAL
+
+
 def test_workspace_and_mask_sizes():
     L = hx.lib()
     assert [L.hx_member_words(g) for g in (1, 64, 65, 128, 129, 255)] == [1, 1, 2, 2, 4, 4]

@@ -1,0 +1,88 @@
+"""GPU parity of the graph-partition phase (Sec. 3.2) through the C-ABI: the spectral vector
+and order, and every candidate's assignment and roles, against the oracle on the same seeded
+inputs.  The spectral step is binary64 in the same order on both sides, so the vector must be
+bit-identical; everything after it is integer work and must be bit-exact."""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import hxo
+from paper_2502_07903_amd import hx
+from paper_2502_07903_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+N_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def say(msg: str) -> None:
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm GPU (torch.cuda.is_available() is False)")
+    hx.lib()
+    return T
+
+
+def _spectral(torch, prob, iters):
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.partition_workspace(dp)
+    order = torch.full((prob.n_gpus,), -1, dtype=torch.int32, device="cuda")
+    fied = torch.zeros(prob.n_gpus, dtype=torch.float64, device="cuda")
+    hx.spectral_order(dp, ws, order, fied, iters=iters)
+    torch.cuda.synchronize()
+    return dp, ws, order, fied
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_spectral_order_parity(torch, cfg):
+    prob = I.make_problem(cfg, n_cand=1)
+    for iters in (0, 7, 1000):
+        say(f"spectral order: workload {cfg}, {iters} iterations")
+        _, _, order, fied = _spectral(torch, prob, iters)
+        want_o, want_x = hxo.spectral_order(prob, iters)
+        assert np.array_equal(fied.cpu().numpy(), want_x), "Fiedler vectors not bit-identical"
+        assert np.array_equal(order.cpu().numpy(), want_o)
+
+
+@pytest.mark.parametrize("cfg,n", [(1, 256), (2, 512), (3, 300), (4, 40), (5, 8), (3, 1)])
+def test_partition_candidates_parity(torch, cfg, n):
+    prob = I.make_problem(cfg, n_cand=1)
+    dp, ws, order, _ = _spectral(torch, prob, 1000)
+    rnd_h = I.partition_draws(cfg, n)
+    rnd = torch.as_tensor(rnd_h.view(np.int64)).to("cuda")
+    assign = torch.full((prob.n_gpus, n), 0xEE, dtype=torch.uint8, device="cuda")
+    role = torch.full((prob.max_groups, n), 0xEE, dtype=torch.uint8, device="cuda")
+    say(f"partition candidates: workload {cfg}, N={n}")
+    hx.partition_candidates(dp, ws, order, rnd, assign, role)
+    torch.cuda.synchronize()
+    want_a, want_r = hxo.partition_candidates(prob, order.cpu().numpy(), rnd_h)
+    got_a, got_r = assign.cpu().numpy(), role.cpu().numpy()
+    bad = np.flatnonzero((got_a != want_a).any(0) | (got_r != want_r).any(0))
+    assert bad.size == 0, f"candidates differ: {bad[:8].tolist()}"
+
+
+def test_partition_then_score(torch):
+    """Generated candidates scored on the GPU: flows and the best equal the oracle's."""
+    cfg, n = 3, 2048
+    prob = I.make_problem(cfg, n_cand=1)
+    dp, ws, order, _ = _spectral(torch, prob, 1000)
+    rnd = torch.as_tensor(I.partition_draws(cfg, n).view(np.int64)).to("cuda")
+    assign = torch.empty((prob.n_gpus, n), dtype=torch.uint8, device="cuda")
+    role = torch.empty((prob.max_groups, n), dtype=torch.uint8, device="cuda")
+    hx.partition_candidates(dp, ws, order, rnd, assign, role)
+    cand = dp.with_candidates(assign, role)
+    wsc = hx.Workspace.for_problem(cand)
+    hx.score(cand, wsc)
+    torch.cuda.synchronize()
+    p2 = dataclasses.replace(prob, assign=assign.cpu().numpy(), role=role.cpu().numpy())
+    want = hxo.score_batch(p2, n_threads=N_THREADS)
+    assert np.array_equal(wsc.flow_value.cpu().numpy(), want["flow_value"])
+    assert tuple(int(x) for x in wsc.best.cpu().numpy()) == want["best"]

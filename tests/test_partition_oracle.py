@@ -22,7 +22,7 @@ from paper_2502_07903_amd import inputs as I
 def _weights(prob):
     G = prob.n_gpus
     b = np.asarray(prob.cluster.beta, np.float64).reshape(G, G)
-    w = np.floor(((b + b.T) * 0.5) / 1e6).astype(np.int64)
+    w = np.clip(np.floor(((b + b.T) * 0.5) / 1e6), 0, 2 ** 23).astype(np.int64)
     np.fill_diagonal(w, 0)
     return w
 
