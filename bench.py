@@ -63,6 +63,10 @@ KERNEL_TRAFFIC = {
 # 131,072 children, same scaling.
 MOVES_TRAFFIC = {"source_sha256_16": "2902f3b847ca3ebd", "children": 131072, "fetch_kib": 561.0,
                  "write_kib": 20990.0}
+# The partition kernel at workload 3 (profiles/partition_workload3.md), per launch of 16,384
+# candidates, same scaling.
+PARTITION_TRAFFIC = {"source_sha256_16": "4e14e097fd09e714", "candidates": 16384, "fetch_kib": 1180.0,
+                     "write_kib": 6192.0}
 KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
                  "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
                  "best": "hx_best.hip"}
@@ -417,6 +421,13 @@ def partition_main(args, torch, hx, I):
     # workgroup-wide scan of the GPU pairs and two barriers, so the fraction is small
     t_part = kernel_us["partition"] * 1e-6
     out_bytes = n * (prob.n_gpus + prob.max_groups)
+    import hashlib
+    src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", "hx_partition.hip")
+    ptraffic = None
+    if (hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] == PARTITION_TRAFFIC["source_sha256_16"]
+            and n == PARTITION_TRAFFIC["candidates"] and cfg == 3):
+        ptraffic = 1024.0 * (PARTITION_TRAFFIC["fetch_kib"] * COUNTER_SCALE["fetch"]
+                             + PARTITION_TRAFFIC["write_kib"] * COUNTER_SCALE["write"])
     out = {
         "metric": "graph-partition candidates generated and scored/sec (Sec. 3.2 first phase + hot path) at 1 GPU",
         "value": n / (ms / 1000.0),
@@ -429,7 +440,7 @@ def partition_main(args, torch, hx, I):
         "best": best,
         "partition_roofline": {"kernel": "partition (hx_partition_candidates)", "bound": "hbm",
                                "achieved": out_bytes / t_part / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                               "frac": out_bytes / t_part / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                               "frac": out_bytes / t_part / 1e9 / HBM_PEAK_GBS, "traffic": ptraffic,
                                "algorithmic_bytes_per_launch": out_bytes, "avg_launch_us": kernel_us["partition"]},
     }
     if not args.no_cpu_baseline:
