@@ -73,10 +73,12 @@ typedef struct {
 
 typedef struct { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hxo_model;
 typedef struct { double s_in, s_out; } hxo_workload;
-/* variant bit 0: pipelined decode capacity; bit 1: KV stage-order search (both below) */
+/* variant bit 0: pipelined decode capacity; bit 1: KV stage-order search; bit 2: asymmetric
+ * layer split (all below) */
 typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; uint32_t variant; } hxo_space;
 #define HXO_VARIANT_PIPELINED 1u
 #define HXO_VARIANT_KV_ORDER 2u  /* bit 1: KV stage-order search (hxo_kv_time_best) */
+#define HXO_VARIANT_ASYM 4u      /* bit 2: asymmetric layer split (layer_split) */
 
 /* ------------------------------------------------------------------ helpers */
 
@@ -93,12 +95,6 @@ static double kv_hidden(const hxo_model *m)
 
 /* layers held by stage j of pp stages: uniform split, remainder to earlier stages */
 static int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
-static int stage_first_layer(int L, int pp, int j)
-{
-    int s = 0;
-    for (int i = 0; i < j; i++) s += stage_layers(L, pp, i);
-    return s;
-}
 
 int32_t hxo_quantize(double x)
 {
@@ -111,6 +107,49 @@ int32_t hxo_coord_cap(const hxo_cluster *c)
 {
     if (c->coord_bw > 0.0 && c->req_bytes > 0.0) return hxo_quantize((1000.0 * c->coord_bw) / c->req_bytes);
     return HXO_CAP_MAX;
+}
+
+/* Layers of every stage of a (tp, pp) strategy of a group (members ascending).  As written: the
+ * uniform split.  Variant HXO_VARIANT_ASYM (the asymmetric split of HexGen, whose cost model the
+ * paper adopts; Table 1 leaves l_j open): every stage first takes one layer, the other L - pp
+ * are shared in proportion to the stage's compute c_j (its slowest device's FLOP/s), each share
+ * rounded down, f_j = floor(((L - pp) * c_j) / sum_k c_k) (the sum left to right), and the
+ * layers left over go one each to the first stages: l_j = 1 + f_j + [j < L - pp - sum_k f_k].
+ * Stages of one device type get the uniform split; no compute at all falls back to it. */
+static void layer_split(const hxo_cluster *c, int L, const int32_t *members, int tp, int pp, uint32_t variant,
+                        int *l)
+{
+    double cs[HXO_MAX_PP], C = 0.0;
+    if (variant & HXO_VARIANT_ASYM) {
+        for (int j = 0; j < pp; j++) {
+            double mn = flops_of(c, members[j * tp]);
+            for (int r = 1; r < tp; r++)
+                if (flops_of(c, members[j * tp + r]) < mn) mn = flops_of(c, members[j * tp + r]);
+            cs[j] = mn;
+            C = C + mn;
+        }
+    }
+    if (!(variant & HXO_VARIANT_ASYM) || !(C > 0.0)) {
+        for (int j = 0; j < pp; j++) l[j] = stage_layers(L, pp, j);
+        return;
+    }
+    const int base = L - pp;
+    int F = 0;
+    for (int j = 0; j < pp; j++) {
+        l[j] = (int)floor(((double)base * cs[j]) / C);
+        F += l[j];
+    }
+    for (int j = 0; j < pp; j++) l[j] = 1 + l[j] + (j < base - F ? 1 : 0);
+}
+
+int hxo_layer_split(const hxo_cluster *c, int32_t L, const int32_t *members, int32_t tp, int32_t pp,
+                    uint32_t variant, int32_t *l)
+{
+    int tmp[HXO_MAX_PP];
+    if (pp < 1 || pp > HXO_MAX_PP || pp > L) return -1;
+    layer_split(c, L, members, tp, pp, variant, tmp);
+    for (int j = 0; j < pp; j++) l[j] = tmp[j];
+    return 0;
 }
 
 /* ------------------------------------------------------------------ Table 1 */
@@ -212,9 +251,11 @@ int hxo_strategy_cost_v(const hxo_cluster *c, const hxo_model *m, const hxo_work
     const int L = m->n_layers;
     *bmax_out = 0; *lat_out = 0.0; *x_out = 0.0;
     if (tp < 1 || pp < 1 || tp * pp != n || pp > L) return 0;
+    int lay[HXO_MAX_PP];
+    layer_split(c, L, members, tp, pp, variant, lay);
     double bmax = HXO_BMAX_CLAMP;
     for (int j = 0; j < pp; j++) {
-        double bj = stage_batch_limit(c, m, w, members + j * tp, tp, stage_layers(L, pp, j));
+        double bj = stage_batch_limit(c, m, w, members + j * tp, tp, lay[j]);
         if (bj < bmax) bmax = bj;
     }
     *bmax_out = (int32_t)bmax;
@@ -223,7 +264,7 @@ int hxo_strategy_cost_v(const hxo_cluster *c, const hxo_model *m, const hxo_work
     double s1 = 0.0, s2 = 0.0;
     for (int j = 0; j < pp; j++) {
         const int32_t *S = members + j * tp;
-        const int l = stage_layers(L, pp, j);
+        const int l = lay[j];
         s1 = s1 + (stage_compute(c, m, w, S, tp, l, role, b) + stage_tp_comm(c, m, w, S, tp, l, role, b));
     }
     for (int j = 0; j + 1 < pp; j++)
@@ -235,7 +276,7 @@ int hxo_strategy_cost_v(const hxo_cluster *c, const hxo_model *m, const hxo_work
         double slowest = 0.0;
         for (int j = 0; j < pp; j++) {
             const int32_t *S = members + j * tp;
-            const int l = stage_layers(L, pp, j);
+            const int l = lay[j];
             double T = stage_compute(c, m, w, S, tp, l, role, b) + stage_tp_comm(c, m, w, S, tp, l, role, b);
             if (j + 1 < pp) T = T + stage_pp_comm(c, m, w, S, members + (j + 1) * tp, tp, role, b);
             if (T > slowest) slowest = T;
@@ -284,20 +325,22 @@ int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workloa
 /* The same with an explicit stage order: the prefill replica's stage ord_p[a] (its members
  * ranked ord_p[a]*ptp .. +ptp-1) serves pipeline position a, which holds the layers of position
  * a; likewise ord_d on the decode side. */
+/* lp / ld (nullable): the layers held by each pipeline position; the uniform split when null. */
 static double kv_time_ordered(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
                               const int32_t *pm, int ptp, int ppp, const int *ord_p,
-                              const int32_t *dm, int dtp, int dpp, const int *ord_d)
+                              const int32_t *dm, int dtp, int dpp, const int *ord_d, const int *lp, const int *ld)
 {
     const int L = m->n_layers;
     const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
     double worst = 0.0;
+    int a0 = 0;
     for (int a = 0; a < ppp; a++) {
-        int a0 = stage_first_layer(L, ppp, a), a1 = a0 + stage_layers(L, ppp, a);
+        const int a1 = a0 + (lp ? lp[a] : stage_layers(L, ppp, a));
+        int b0 = 0;
         for (int bb = 0; bb < dpp; bb++) {
-            int b0 = stage_first_layer(L, dpp, bb), b1 = b0 + stage_layers(L, dpp, bb);
-            int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
-            if (nab <= 0) continue;
-            for (int r = 0; r < ptp; r++)
+            const int b1 = b0 + (ld ? ld[bb] : stage_layers(L, dpp, bb));
+            const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+            for (int r = 0; r < ptp && nab > 0; r++)
                 for (int q = 0; q < dtp; q++) {
                     int hi = (r + 1) * dtp < (q + 1) * ptp ? (r + 1) * dtp : (q + 1) * ptp;
                     int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
@@ -308,7 +351,9 @@ static double kv_time_ordered(const hxo_cluster *c, const hxo_model *m, const hx
                     double time = alpha_of(c, g, h) + bytes / beta_of(c, g, h);
                     if (time > worst) worst = time;
                 }
+            b0 = b1;
         }
+        a0 = a1;
     }
     return worst;
 }
@@ -319,7 +364,7 @@ double hxo_kv_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload 
     int op[HXO_MAX_PP], od[HXO_MAX_PP];
     for (int a = 0; a < ppp; a++) op[a] = a;
     for (int b = 0; b < dpp; b++) od[b] = b;
-    return kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od);
+    return kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od, NULL, NULL);
 }
 
 /* next permutation of v[0..n) in lexicographic order; returns 0 after the last one */
@@ -359,7 +404,7 @@ double hxo_kv_time_best(const hxo_cluster *c, const hxo_model *m, const hxo_work
     do {
         for (int b = 0; b < dpp; b++) od[b] = b;
         do {
-            double t = kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od);
+            double t = kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od, NULL, NULL);
             if (best < 0.0 || t < best) best = t;
         } while (next_order(od, dpp));
     } while (next_order(op, ppp));
@@ -489,9 +534,20 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
                     int32_t kv = 0;
                     (void)pn; (void)dn;
                     if (tp[gp] > 0 && tp[gd] > 0) {
-                        double t = (bt->sp->variant & HXO_VARIANT_KV_ORDER)
-                                       ? hxo_kv_time_best(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd])
-                                       : hxo_kv_time(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                        double t;
+                        if (bt->sp->variant & HXO_VARIANT_ASYM) {
+                            /* each replica's layers follow its own (asymmetric) split */
+                            int lp[HXO_MAX_PP], ld[HXO_MAX_PP], op[HXO_MAX_PP], od[HXO_MAX_PP];
+                            layer_split(c, bt->m->n_layers, pm, tp[gp], pp[gp], bt->sp->variant, lp);
+                            layer_split(c, bt->m->n_layers, dm, tp[gd], pp[gd], bt->sp->variant, ld);
+                            for (int x = 0; x < pp[gp]; x++) op[x] = x;
+                            for (int x = 0; x < pp[gd]; x++) od[x] = x;
+                            t = kv_time_ordered(c, bt->m, bt->w, pm, tp[gp], pp[gp], op, dm, tp[gd], pp[gd], od, lp, ld);
+                        } else if (bt->sp->variant & HXO_VARIANT_KV_ORDER) {
+                            t = hxo_kv_time_best(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                        } else {
+                            t = hxo_kv_time(c, bt->m, bt->w, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                        }
                         kv = hxo_quantize(1000.0 / t);
                     }
                     f->kv_cap[(int64_t)(i * nd + j) * N + n] = kv;
@@ -1030,9 +1086,9 @@ int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
  * The first phase of the scheduler (Sec. 3.2) as a candidate generator.  The device graph has
  * the GPUs as nodes, weighted by their memory limits, and the links as edges, weighted by
  * bandwidth.  Readings (the paper names the methods, not their parameters):
- *   - edge weight w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6): the symmetrised bandwidth in
- *     whole MB/s, so that every cut and gain below is an exact integer sum; node weight = the
- *     memory limit in whole bytes;
+ *   - edge weight w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6), clamped to [0, 2^23]: the
+ *     symmetrised bandwidth in whole MB/s, so that every cut and gain below is an exact integer
+ *     sum; node weight = the memory limit in whole bytes;
  *   - Step (i), initial partition: spectral order by the Fiedler direction of the Laplacian
  *     Deg - w (power iteration, hxo_spectral_order), cut into K contiguous groups of balanced
  *     memory; K = floor(total memory / replica memory), a replica holding the weights and the
@@ -1048,10 +1104,14 @@ int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
  * node k (bit 11 + k).
  */
 
+/* clamped to [0, 2^23] MB/s (8.4 TB/s, beyond any link), so that a GPU's summed weights fit 31 bits */
 static int64_t pg_weight(const hxo_cluster *c, int d, int e)
 {
     if (d == e) return 0;
-    return (int64_t)floor(((beta_of(c, d, e) + beta_of(c, e, d)) * 0.5) / 1.0e6);
+    double v = floor(((beta_of(c, d, e) + beta_of(c, e, d)) * 0.5) / 1.0e6);
+    if (!(v >= 0.0)) v = 0.0;
+    if (v > 8388608.0) v = 8388608.0;
+    return (int64_t)v;
 }
 
 /* Sum of v[0..G) (G <= 256) in a fixed association: 64 partial sums t_l = ((v_l + v_{l+64}) +

@@ -309,3 +309,15 @@ def partition_candidates(prob, order: np.ndarray, rnd: np.ndarray) -> Tuple[np.n
                                    _p(np.ascontiguousarray(order, np.int32)), C.c_int32(prob.max_groups),
                                    C.c_int32(N), _p(rnd), _p(assign), _p(role))
     return assign, role
+
+
+def layer_split(prob, members: Sequence[int], tp: int, pp: int, variant: int) -> List[int]:
+    """Layers of each stage of a (tp, pp) strategy of a group (uniform, or asymmetric with bit 2)."""
+    a = _Args(prob)
+    mem = np.ascontiguousarray(np.asarray(members, np.int32))
+    out = np.zeros(max(pp, 1), np.int32)
+    rc = lib().hxo_layer_split(C.byref(a.cluster), C.c_int32(prob.model["n_layers"]), _p(mem), C.c_int32(tp),
+                               C.c_int32(pp), C.c_uint32(variant), _p(out))
+    if rc != 0:
+        raise ValueError("pp outside [1, min(32, L)]")
+    return out[:pp].tolist()

@@ -13,6 +13,11 @@ both replicas.  Checked on a hand-derived case whose ascending orders pair the s
 whose best order pairs the fast ones, and by what a search over every order fixes: it never
 exceeds the ascending time, leaves single stages alone, and cannot tell in which order the
 stage blocks were handed to it.
+
+Asymmetric layer split (variant bit 2): hand-derived splits, the invariants of the rule (sum L,
+at least one layer each, faster stages never fewer but the leftover, one type = uniform), whole
+batches unchanged on a one-type cluster, a free-link latency closed form, and a KV edge whose
+stages share the split's 40 layers.
 """
 import dataclasses
 
@@ -168,3 +173,84 @@ def test_kv_order_search_properties():
         dm2 = _stage_blocks(dm, dtp, rng.permutation(dpp))
         assert hxo.kv_time(prob, pm2, ptp, ppp, dm2, dtp, dpp, best_order=True) == best
     assert checked > 50 and strict > 10
+
+
+# ------------------------------------------------------------------ asymmetric layer split
+
+ASYM = 4
+
+
+def test_asym_split_hand_cases():
+    """16-GPU cluster: GPUs 0-3 type A (312 TFLOP/s), 4-7 B (125), 8-11 C (65); L = 48.
+    (A | C): shares of 46 are 46*312/377 = 38.07 and 46*65/377 = 7.93, floors 38 and 7, one
+    layer left over for stage 0: (1+38+1, 1+7) = (40, 8).  (A A | B B): 46*312/437 = 32.84 and
+    46*125/437 = 13.16: (34, 14).  One type: the uniform split."""
+    prob = I.make_problem(2, n_cand=1)
+    assert hxo.layer_split(prob, [0, 8], 1, 2, ASYM) == [40, 8]
+    assert hxo.layer_split(prob, [0, 1, 4, 5], 2, 2, ASYM) == [34, 14]
+    assert hxo.layer_split(prob, [0, 1, 2], 1, 3, ASYM) == [16, 16, 16]
+    assert hxo.layer_split(prob, [0, 8], 1, 2, 0) == [24, 24]
+
+
+def test_asym_split_invariants():
+    prob = I.make_problem(3, n_cand=1)
+    rng = np.random.default_rng(6)
+    flops = np.asarray(prob.cluster.type_flops)[np.asarray(prob.cluster.gpu_type)]
+    L = prob.model["n_layers"]
+    for _ in range(300):
+        tp = int(rng.choice([1, 2, 4]))
+        pp = int(rng.integers(1, 9))
+        members = sorted(rng.choice(prob.n_gpus, tp * pp, replace=False).tolist())
+        lay = hxo.layer_split(prob, members, tp, pp, ASYM)
+        assert sum(lay) == L and min(lay) >= 1
+        c = [flops[members[j * tp:(j + 1) * tp]].min() for j in range(pp)]
+        for i in range(pp):
+            for j in range(pp):
+                if c[i] > c[j]:
+                    assert lay[i] >= lay[j] - 1          # faster stages never get fewer layers (but the leftover)
+        if len(set(c)) == 1:
+            assert lay == hxo.layer_split(prob, members, tp, pp, 0)
+
+
+def test_asym_is_uniform_on_one_type():
+    """A cluster of one GPU type: the asymmetric split is the uniform one, so every capacity, KV
+    edge and flow is unchanged."""
+    prob = I.make_problem(3, n_cand=200)
+    cl = prob.cluster
+    one = I.Cluster(np.zeros_like(cl.gpu_type), cl.type_flops, cl.type_hbm_bw, cl.type_mem, cl.beta, cl.alpha)
+    p0 = dataclasses.replace(prob, cluster=one)
+    a = hxo.score_batch(p0)
+    b = hxo.score_batch(dataclasses.replace(p0, variant=ASYM))
+    for k in ("tp", "pp", "bmax", "cap", "lat"):
+        assert np.array_equal(a["cost"][k], b["cost"][k])
+    assert np.array_equal(a["flownet"]["kv_cap"], b["flownet"]["kv_cap"])
+    assert np.array_equal(a["flow_value"], b["flow_value"])
+
+
+def test_asym_free_links_closed_form_and_kv():
+    """Free links: a prefill group (A | C) has latency 24 s_in H^2 (40 / c_A + 8 / c_C).  Two (A | C)
+    replicas over links of one bandwidth: the uniform split puts 24 layers (29.6 GB of weights) on
+    the 16 GB C GPU, so neither replica is feasible; the asymmetric split gives it 8 and both
+    are, and their stage 0s share 40 layers, so the KV time is that of 40 layers."""
+    prob = I.make_problem(2, n_cand=1)
+    cl = prob.cluster
+    H = prob.model["hidden"]
+    free = I.Cluster(cl.gpu_type, cl.type_flops, cl.type_hbm_bw, cl.type_mem,
+                     np.full_like(cl.beta, 1e300), np.zeros_like(cl.alpha))
+    p2 = dataclasses.replace(prob, cluster=free, variant=ASYM)
+    ok, b, lat, x = hxo.strategy_cost(p2, [0, 8], 1, 2, 0)
+    assert ok
+    assert lat == pytest.approx(24.0 * p2.s_in * H * H * (40 / 312e12 + 8 / 65e12), rel=1e-12)
+    flat = I.Cluster(cl.gpu_type, cl.type_flops, cl.type_hbm_bw, cl.type_mem,
+                     np.full_like(cl.beta, 20e9), np.zeros_like(cl.alpha))
+    a, r = I.placement_from_groups([[0, 8], [1, 9]], [I.PREFILL, I.DECODE], 16, 2)
+    from tests import helpers as Hh
+    base = Hh.problem(flat, prob.model, a, r, s_in=prob.s_in, s_out=prob.s_out, tp=(1,), pp=(2,))
+    V1 = 2.0 * prob.s_in * (H * prob.model["n_kv_heads"] // prob.model["n_heads"]) * 2
+    uni = hxo.cost_eval(base)
+    assert (uni["cap"][:2, 0] == 0).all()
+    pv = dataclasses.replace(base, variant=ASYM)
+    cost = hxo.cost_eval(pv)
+    assert list(cost["pp"][:2, 0]) == [2, 2] and (cost["cap"][:2, 0] > 0).all()
+    fn = hxo.build_flownet(pv, cost)
+    assert int(fn["kv_cap"][0, 0]) == int(np.floor(1000.0 / ((V1 * 40) / 20e9)))
