@@ -72,8 +72,10 @@ KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx
                  "best": "hx_best.hip"}
 
 
-# hx_space.variant bits: 1 pipelined decode capacity, 2 KV stage-order search
-VARIANTS = {"as-written": 0, "pipelined": 1, "kv-order": 2, "pipelined+kv-order": 3}
+# hx_space.variant bits: 1 pipelined decode capacity, 2 KV stage-order search, 4 asymmetric
+# layer split
+VARIANTS = {"as-written": 0, "pipelined": 1, "kv-order": 2, "pipelined+kv-order": 3, "asym": 4,
+            "pipelined+asym": 5}
 
 
 def parse():
@@ -85,7 +87,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", choices=list(VARIANTS), default="as-written",
                     help="cost-model variant: the model as written, pipelined decode capacity, KV stage-order "
-                         "search, or both")
+                         "search, asymmetric layer split, or combinations")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
     ap.add_argument("--refine", action="store_true",
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")

@@ -103,6 +103,10 @@ typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; uint32
 /* KV stage-order search (Appendix A, edge capacity estimation): each KV edge's time is
  * minimised over the stage orders of both replicas (see hx_build_flownet). */
 #define HX_VARIANT_KV_ORDER 2u
+/* Asymmetric layer split (HexGen's asymmetric parallelism; Table 1 leaves l_j open): every
+ * stage holds one layer plus its compute's share of the other L - pp (see hx_cost_eval).  Not
+ * combinable with HX_VARIANT_KV_ORDER. */
+#define HX_VARIANT_ASYM 4u
 
 /* Candidate placements (Sec. 3.1).  assign[g][n] = group of GPU g in candidate n (HX_UNUSED
  * or >= max_groups: GPU unused); role[k][n] = HX_PREFILL, HX_DECODE, or anything else (no
@@ -165,7 +169,11 @@ int hx_validate(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_sp
  * 3.3 "Compute nodes"); ties keep the smaller tp.
  * With space.variant & HX_VARIANT_PIPELINED, a decode strategy's x is (1000*b)/max_j T_j,
  * T_j = (comp_j + tp_j) + pp_j (pp_j: the PP term of the link into stage j+1 as in the
- * latency, none for the last stage); latencies and prefill are unchanged. */
+ * latency, none for the last stage); latencies and prefill are unchanged.
+ * With space.variant & HX_VARIANT_ASYM, stage j holds l_j = 1 + f_j + [j < L - pp - sum_k f_k]
+ * layers instead, f_j = floor(((L - pp) * c_j) / sum_k c_k) with c_j the slowest FLOP/s of the
+ * stage's devices (the sum left to right; the uniform split when it is 0), in the memory row,
+ * the computation and the TP term alike, and each replica's KV layer ranges follow its split. */
 int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                  const hx_candidates *cand, const hx_cost_out *out, void *workspace,
                  size_t workspace_bytes, hipStream_t stream);

@@ -34,7 +34,8 @@ int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, 
     if (!finite_pos(w.s_in) || !finite_pos(w.s_out)) return HX_EINVAL;
     if (s.tp_mask == 0 || s.tp_mask >= (1u << HX_MAX_TP) || s.pp_mask == 0) return HX_EINVAL;
     if (s.granularity != 0 && s.granularity != 1) return HX_EINVAL;
-    if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER)) return HX_EINVAL;
+    if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM)) return HX_EINVAL;
+    if ((s.variant & HX_VARIANT_KV_ORDER) && (s.variant & HX_VARIANT_ASYM)) return HX_EINVAL;
     if (k->n_cand < 1 || k->max_groups < 1 || k->max_groups > HX_MAX_GROUPS || !k->assign || !k->role)
         return HX_EINVAL;
     return HX_OK;

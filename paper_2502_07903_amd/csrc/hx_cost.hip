@@ -49,12 +49,27 @@ struct StrategyCost {
 // Returns false when the memory limit admits no batch of 1.  TPC > 0 fixes tp at compile
 // time: a stage's member ids are then held in registers and each device's peer loop is
 // unrolled, so its loads and divisions overlap; TPC == 0 is the same arithmetic for any tp.
-// kPipe: the pipelined decode capacity variant (HX_VARIANT_PIPELINED): a decode replica's x is
-// 1000 b over its slowest stage, T_j = (comp_j + TP_j) + PP_j with the link into stage j+1
-// counted with stage j; the latency is the same sum either way.
-template <int TPC, bool kPipe>
+// Slowest FLOP/s among stage j's devices, member r at mem[(j*tp + r) * stride].
+__device__ __forceinline__ double stage_cmin(const Tables& tb, const uint8_t* mem, int stride, int j, int tp) {
+    double c = tb.gfl[mem[(j * tp) * stride]];
+    for (int r = 1; r < tp; ++r) c = dmin(c, tb.gfl[mem[(j * tp + r) * stride]]);
+    return c;
+}
+
+template <bool kAsym>
+__device__ __forceinline__ LayerSplit make_split(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
+                                                 int tp, int pp) {
+    return layer_split<kAsym>(p.L, pp, [&](int j) { return stage_cmin(tb, mem, stride, j, tp); });
+}
+
+// kVar: variant bits.  HX_VARIANT_PIPELINED: a decode replica's x is 1000 b over its slowest
+// stage, T_j = (comp_j + TP_j) + PP_j with the link into stage j+1 counted with stage j; the
+// latency is the same sum either way.  HX_VARIANT_ASYM: the asymmetric layer split above.
+template <int TPC, int kVar>
 __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
                                               int tp_rt, int pp, int role, StrategyCost& out) {
+    constexpr bool kPipe = (kVar & HX_VARIANT_PIPELINED) != 0;
+    constexpr bool kAsym = (kVar & HX_VARIANT_ASYM) != 0;
     constexpr int kMax = TPC > 0 ? TPC : HX_MAX_TP;
     const int tp = TPC > 0 ? TPC : tp_rt;
     const double t = (double)tp;
@@ -63,12 +78,12 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
     const double Kkv = 2.0 * (p.s_in + p.s_out) * p.Hkv * B;
     const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
     const int G = p.G;
-    const int lq = p.L / pp, lr = p.L % pp;
+    const LayerSplit split = make_split<kAsym>(p, tb, mem, stride, tp, pp);
 
     // Memory-limit row: b_j = floor((M_j - A_j)/K_j) on the stage's smallest memory.
     double bmin = kBmaxClamp;
     for (int j = 0; j < pp; ++j) {
-        const double l = (double)(lq + (j < lr ? 1 : 0));
+        const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, mem, stride, j, tp) : 0.0);
         const double A = (W12 / t) * l;
         const double K = (Kkv / t) * l + Kact;
         const uint8_t* S = mem + (j * tp) * stride;
@@ -94,7 +109,6 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
     double s1 = 0.0, s2 = 0.0;
     double tmax = 0.0, prev = 0.0;  // kPipe: slowest stage so far, previous stage's comp + TP
     for (int j = 0; j < pp; ++j) {
-        const double l = (double)(lq + (j < lr ? 1 : 0));
         const uint8_t* Sl = mem + (j * tp) * stride;
 #pragma unroll
         for (int r = 0; r < kMax; ++r) S[r] = (TPC > 0 || r < tp) ? Sl[r * stride] : 0;
@@ -105,6 +119,7 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                 cmin = dmin(cmin, tb.gfl[S[r]]);
                 hmin = dmin(hmin, tb.ghb[S[r]]);
             }
+        const double l = (double)split_layers<kAsym>(split, j, cmin);
         const double comp = prefill ? (Xcomp_p / (t * cmin)) * l
                                     : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
         // TP row: the device with the largest sum over its peers (ascending peer order).
@@ -164,15 +179,15 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
     return true;
 }
 
-template <bool kPipe>
+template <int kVar>
 __device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, const uint8_t* mem, int stride, int tp,
                                          int pp, int role, StrategyCost& out) {
     switch (tp) {
-        case 1: return cost_strategy<1, kPipe>(p, tb, mem, stride, tp, pp, role, out);
-        case 2: return cost_strategy<2, kPipe>(p, tb, mem, stride, tp, pp, role, out);
-        case 4: return cost_strategy<4, kPipe>(p, tb, mem, stride, tp, pp, role, out);
-        case 8: return cost_strategy<8, kPipe>(p, tb, mem, stride, tp, pp, role, out);
-        default: return cost_strategy<0, kPipe>(p, tb, mem, stride, tp, pp, role, out);
+        case 1: return cost_strategy<1, kVar>(p, tb, mem, stride, tp, pp, role, out);
+        case 2: return cost_strategy<2, kVar>(p, tb, mem, stride, tp, pp, role, out);
+        case 4: return cost_strategy<4, kVar>(p, tb, mem, stride, tp, pp, role, out);
+        case 8: return cost_strategy<8, kVar>(p, tb, mem, stride, tp, pp, role, out);
+        default: return cost_strategy<0, kVar>(p, tb, mem, stride, tp, pp, role, out);
     }
 }
 
@@ -449,9 +464,11 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
 
 // One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
 // is false for groups past the last large unit (they still join every wave-level sync).
-template <bool kPipe>
+template <int kVar>
 __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, const uint8_t* adm_tab,
                           int gl, bool live, int n, int k, int role, uint64_t mask) {
+    constexpr bool kPipe = (kVar & HX_VARIANT_PIPELINED) != 0;
+    constexpr bool kAsym = (kVar & HX_VARIANT_ASYM) != 0;
     const int G = p.G;
     const int cnt = live ? __popcll(mask) : 0;
     for (int g = gl; g < G && live; g += kCoopLanes)
@@ -470,11 +487,11 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
         const bool adm = (am >> (tp - 1)) & 1u;
         const int pp = adm ? stage_count(cnt, tp) : 0;
         const double t = (double)tp;
-        const int lq = adm ? p.L / pp : 0, lr = adm ? p.L % pp : 0;
+        const LayerSplit split = adm ? make_split<kAsym>(p, tb, c.mem, 1, tp, pp) : LayerSplit{0, 0, 0, 0, 0.0};
         // Memory-limit row, one lane per stage, then the group's minimum (exact).
         double bl = kBmaxClamp;
         for (int j = gl; j < pp; j += kCoopLanes) {
-            const double l = (double)(lq + (j < lr ? 1 : 0));
+            const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
             const double A = (W12 / t) * l;
             const double K = (Kkv / t) * l + Kact;
             const uint8_t* S = c.mem + j * tp;
@@ -518,13 +535,13 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
             }
         }
         for (int j = gl; feas && j < pp; j += kCoopLanes) {
-            const double l = (double)(lq + (j < lr ? 1 : 0));
             const uint8_t* S = c.mem + j * tp;
             double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
             for (int r = 1; r < tp; ++r) {
                 cmin = dmin(cmin, tb.gfl[S[r]]);
                 hmin = dmin(hmin, tb.ghb[S[r]]);
             }
+            const double l = (double)split_layers<kAsym>(split, j, cmin);
             c.comp[j] = prefill ? (Xcomp_p / (t * cmin)) * l
                                 : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
         }
@@ -532,7 +549,8 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
         if (feas && gl == 0) {
             double s1 = 0.0, s2 = 0.0, tmax = 0.0;
             for (int j = 0; j < pp; ++j) {
-                const double l = (double)(lq + (j < lr ? 1 : 0));
+                const double l =
+                    (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
                 double mx = 0.0;
                 for (int r = 0; r < tp; ++r) {
                     const double v = c.tsum[j * tp + r];
@@ -586,7 +604,7 @@ __device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, 
     }
 }
 
-template <int W, bool kTables, int kEvalBlock, bool kPipe>
+template <int W, bool kTables, int kEvalBlock, int kVar>
 __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
     const int G = p.G;
@@ -653,7 +671,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
                 role = (int)(w & 0xFF);
                 mask = rec[1];
             }
-            coop_unit<kPipe>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
+            coop_unit<kVar>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
@@ -677,7 +695,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
             const int tp = __ffs(am);
             const int pp = stage_count(cnt, tp);
             StrategyCost sc;
-            if (!cost_any<kPipe>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            if (!cost_any<kVar>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
             const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
             if (better) {
                 have = true;
@@ -697,16 +715,16 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     }
 }
 
-template <int W, bool kPipe>
+template <int W, int kVar>
 void launch_eval(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
                  size_t lds, hipStream_t s) {
     if (eb == 256) {
         if (tables)
-            hipLaunchKernelGGL((eval_kernel<W, true, 256, kPipe>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
+            hipLaunchKernelGGL((eval_kernel<W, true, 256, kVar>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
         else
-            hipLaunchKernelGGL((eval_kernel<W, false, 256, kPipe>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
+            hipLaunchKernelGGL((eval_kernel<W, false, 256, kVar>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
     } else {
-        hipLaunchKernelGGL((eval_kernel<W, false, 128, kPipe>), dim3(blocks), dim3(128), lds, s, p, o, wk, nb);
+        hipLaunchKernelGGL((eval_kernel<W, false, 128, kVar>), dim3(blocks), dim3(128), lds, s, p, o, wk, nb);
     }
 }
 
@@ -767,10 +785,14 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     prof_mark(kKEval, false, s);
-    if (p.variant & HX_VARIANT_PIPELINED)
-        launch_eval<W, true>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
-    else
-        launch_eval<W, false>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+    switch (p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) {
+        case 0: launch_eval<W, 0>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case HX_VARIANT_PIPELINED: launch_eval<W, HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case HX_VARIANT_ASYM: launch_eval<W, HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        default:
+            launch_eval<W, HX_VARIANT_PIPELINED | HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+            break;
+    }
     prof_mark(kKEval, true, s);
     return hipGetLastError();
 }

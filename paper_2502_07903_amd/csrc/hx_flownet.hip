@@ -313,7 +313,63 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
     f.kv_cap[(int64_t)e * N + n] = feas ? quantize(1000.0 / t) : 0;
 }
 
-template <int W>
+// FLOP/s of GPU g (0 for an unknown type, as the cost model reads it).
+__device__ __forceinline__ double gpu_flops(const Problem& p, int g) {
+    const int t = p.gpu_type[g];
+    return (t >= 0 && t < p.T) ? p.flops[t] : 0.0;
+}
+
+// Slowest FLOP/s among stage j's devices of a member list.
+__device__ double stage_flops(const Problem& p, const uint8_t* m, int stride, int j, int tp) {
+    double c = gpu_flops(p, m[(j * tp) * stride]);
+    for (int r = 1; r < tp; ++r) c = dmin(c, gpu_flops(p, m[(j * tp + r) * stride]));
+    return c;
+}
+
+// kv_time with each replica's layers following the asymmetric split (HX_VARIANT_ASYM).
+__device__ double kv_time_asym(const Problem& p, const uint8_t* pm, int ptp, int ppp, const uint8_t* dm, int dtp,
+                               int dpp, int stride) {
+    const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
+    const int deni = ptp * dtp;
+    const double den = (double)deni;
+    const bool pow2 = (deni & (deni - 1)) == 0;
+    const double inv_den = 1.0 / den;
+    const LayerSplit sp = layer_split<true>(p.L, ppp, [&](int j) { return stage_flops(p, pm, stride, j, ptp); });
+    const LayerSplit sd = layer_split<true>(p.L, dpp, [&](int j) { return stage_flops(p, dm, stride, j, dtp); });
+    double worst = 0.0;
+    int a = 0, bb = 0, a0 = 0, b0 = 0;
+    int a1 = split_layers<true>(sp, 0, stage_flops(p, pm, stride, 0, ptp));
+    int b1 = split_layers<true>(sd, 0, stage_flops(p, dm, stride, 0, dtp));
+    while (a < ppp && bb < dpp) {
+        const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+        const double Vn = V1 * (double)nab;
+        const uint8_t* Sa = pm + (a * ptp) * stride;
+        const uint8_t* Sb = dm + (bb * dtp) * stride;
+        int r = 0, q = 0;
+        while (r < ptp && q < dtp) {
+            const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+            const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+            const int g = Sa[r * stride], h = Sb[q * stride];
+            const double bytes = pow2 ? (Vn * (double)ov) * inv_den : (Vn * (double)ov) / den;
+            const double time = p.alpha[g * p.G + h] + bytes / p.beta[g * p.G + h];
+            if (time > worst) worst = time;
+            if (re <= qe) ++r;
+            if (qe <= re) ++q;
+        }
+        const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
+        if (adv_a && ++a < ppp) {
+            a0 = a1;
+            a1 = a0 + split_layers<true>(sp, a, stage_flops(p, pm, stride, a, ptp));
+        }
+        if (adv_b && ++bb < dpp) {
+            b0 = b1;
+            b1 = b0 + split_layers<true>(sd, bb, stage_flops(p, dm, stride, bb, dtp));
+        }
+    }
+    return worst;
+}
+
+template <int W, bool kAsym>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ uint8_t sm[];
     const int tid = threadIdx.x;
@@ -338,7 +394,8 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
             // is treated as infeasible rather than read past the member list.
             if (expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
                 expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp)
-                c = quantize(1000.0 / kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride));
+                c = quantize(1000.0 / (kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                             : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
         }
     } else {
         // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
@@ -365,8 +422,10 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     prof_mark(kKKv, false, s);
     if (p.granularity == 0 && (p.variant & HX_VARIANT_KV_ORDER))
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    else if (p.granularity == 0 && (p.variant & HX_VARIANT_ASYM))
+        hipLaunchKernelGGL((kv_kernel<W, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     else
-        hipLaunchKernelGGL(kv_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     prof_mark(kKKv, true, s);
     return hipGetLastError();
 }

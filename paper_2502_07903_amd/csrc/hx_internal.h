@@ -48,6 +48,39 @@ __device__ __forceinline__ double dmax(double a, double b) { return b > a ? b : 
 // Layers held by stage j of pp: floor(L/pp) + [j < L mod pp].
 __device__ __forceinline__ int stage_layers(int L, int pp, int j) { return L / pp + (j < L % pp ? 1 : 0); }
 
+// Layers per pipeline stage.  As written: the uniform split, floor(L/pp) + [j < L mod pp].
+// With HX_VARIANT_ASYM (the asymmetric split): every stage first takes one layer and the other
+// L - pp are shared in proportion to the stage's compute c_j (its slowest device's FLOP/s),
+// f_j = floor(((L - pp) c_j) / sum_k c_k) (summed left to right), the layers left over going one
+// each to the first stages: l_j = 1 + f_j + [j < L - pp - sum_k f_k].  Stages of one device
+// type get the uniform split; a zero compute sum falls back to it.
+struct LayerSplit {
+    int lq, lr, base, rem;
+    double csum;  // > 0: the asymmetric split applies
+};
+
+// stage_c(j): c_j of stage j.
+template <bool kAsym, class StageC>
+__device__ __forceinline__ LayerSplit layer_split(int L, int pp, StageC stage_c) {
+    LayerSplit s{L / pp, L % pp, L - pp, 0, 0.0};
+    if (kAsym) {
+        for (int j = 0; j < pp; ++j) s.csum = s.csum + stage_c(j);
+        if (s.csum > 0.0) {
+            int F = 0;
+            for (int j = 0; j < pp; ++j) F += (int)floor(((double)s.base * stage_c(j)) / s.csum);
+            s.rem = s.base - F;
+        }
+    }
+    return s;
+}
+
+// Layers of stage j whose slowest device has cj FLOP/s.
+template <bool kAsym>
+__device__ __forceinline__ int split_layers(const LayerSplit& s, int j, double cj) {
+    if (kAsym && s.csum > 0.0) return 1 + (int)floor(((double)s.base * cj) / s.csum) + (j < s.rem ? 1 : 0);
+    return s.lq + (j < s.lr ? 1 : 0);
+}
+
 // Kernels of libhx, for the diagnostic per-kernel timing behind hx_profile.
 enum KernelId {
     kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKClasses, kKMoves, kKGather,

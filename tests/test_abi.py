@@ -59,7 +59,7 @@ def test_validate_accepts_workloads():
                dict(G=128, T=6, N=131072, Kmax=32, gran=1)):
         assert _validate(*_args(**kw)) == hx.HX_OK
     a = list(_args())
-    for v in (1, 2, 3):                                 # HX_VARIANT_PIPELINED, HX_VARIANT_KV_ORDER
+    for v in (1, 2, 3, 4, 5):                           # HX_VARIANT_PIPELINED, _KV_ORDER, _ASYM
         a[3].variant = v
         assert _validate(*a) == hx.HX_OK
 
@@ -78,7 +78,8 @@ def test_validate_accepts_workloads():
     lambda a: setattr(a[3], "tp_mask", 1 << 8),      # TP degree 9 > 8
     lambda a: setattr(a[3], "pp_mask", 0),
     lambda a: setattr(a[3], "granularity", 2),
-    lambda a: setattr(a[3], "variant", 4),           # unknown cost-model variant bit
+    lambda a: setattr(a[3], "variant", 8),           # unknown cost-model variant bit
+    lambda a: setattr(a[3], "variant", 6),           # stage-order search with the asymmetric split
     lambda a: setattr(a[4], "n_cand", 0),
     lambda a: setattr(a[4], "max_groups", 256),
     lambda a: setattr(a[4], "role", None),

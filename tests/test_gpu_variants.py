@@ -79,7 +79,7 @@ def test_pipelined_per_gpu_nodes(torch):
 
 
 def test_unknown_variant_rejected(torch):
-    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=4)
+    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=8)
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp)
     with pytest.raises(hx.HxError) as e:
@@ -127,3 +127,43 @@ def test_kv_order_crossed_links(torch):
         _, fn, _, _ = _gpu(torch, prob)
         V = 2.0 * 512.0 * 7168 * 2 * 24
         assert int(fn["kv_cap"][0, 0]) == int(np.floor(1000.0 / (V / bw)))
+
+
+ASYM = 4
+
+
+@pytest.mark.parametrize("cfg,n,variant", [(1, None, ASYM), (2, None, ASYM), (3, None, ASYM), (4, 4096, ASYM),
+                                           (3, 8192, ASYM | PIPE), (2, 777, ASYM | PIPE)])
+def test_asym_parity(torch, cfg, n, variant):
+    """Asymmetric layer split (alone and with the pipelined capacity): every strategy, capacity,
+    latency, KV edge, flow and the best candidate equal the oracle's."""
+    prob = dataclasses.replace(I.make_problem(cfg, n_cand=n), variant=variant)
+    say(f"asymmetric layer split: workload {cfg}, N={prob.n_cand}, variant {variant}")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    for k in ("tp", "pp", "bmax", "cap"):
+        bad = cost[k] != want["cost"][k]
+        assert not bad.any(), f"{k} differs at {np.argwhere(bad)[:5].tolist()}"
+    assert np.array_equal(cost["lat"], want["cost"]["lat"])
+    Hh.compare_flownet(fn, want["flownet"])
+    assert np.array_equal(fv, want["flow_value"])
+    assert best == want["best"]
+
+
+def test_asym_per_gpu_nodes(torch):
+    prob = dataclasses.replace(I.make_problem(5, n_cand=1024), variant=ASYM)
+    say("asymmetric layer split: per-GPU nodes, N=1024")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    for k in ("tp", "pp", "bmax", "cap", "lat"):
+        assert np.array_equal(cost[k], want["cost"][k]), k
+    assert np.array_equal(fv, want["flow_value"])
+
+
+def test_asym_with_kv_order_rejected(torch):
+    prob = dataclasses.replace(I.make_problem(1, n_cand=4), variant=ASYM | ORDER)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp)
+    with pytest.raises(hx.HxError) as e:
+        hx.cost_eval(dp, ws.cost)
+    assert e.value.code == hx.HX_EINVAL
