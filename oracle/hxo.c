@@ -39,6 +39,11 @@
  *     per-GPU rule of kv_gpu_time().
  *   - Source and sink edges are unbounded (2^24 - 1) unless a coordinator
  *     bandwidth and request size are given.
+ *   - Request classes (length buckets, at most four, in place of the single mean
+ *     task): a strategy must fit every class; a replica's latency is the mix's
+ *     weighted mean, its capacity 1/(sum_k w_k/x_k) (the mix's time per request),
+ *     its b_max the smallest; a KV edge's time is the weighted mean of the class
+ *     times.  Not combined with the stage-order search or the asymmetric split.
  *
  * Floating point: IEEE-754 binary64, round to nearest, no contraction into FMA
  * (built with -ffp-contract=off, no fast-math), correctly rounded division, and
@@ -72,13 +77,40 @@ typedef struct {
 } hxo_cluster;
 
 typedef struct { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hxo_model;
-typedef struct { double s_in, s_out; } hxo_workload;
+/* The inference task t of Table 1: mean prompt and output lengths.  n_classes > 0: the requests
+ * form classes (length buckets), class k with lengths cls_in[k], cls_out[k] and weight cls_w[k]
+ * (its share of the requests); see hxo_group_select. */
+#define HXO_MAX_CLASSES 4
+typedef struct {
+    double s_in, s_out;
+    int32_t n_classes;
+    double cls_in[HXO_MAX_CLASSES], cls_out[HXO_MAX_CLASSES], cls_w[HXO_MAX_CLASSES];
+} hxo_workload;
+
+/* the single task of class k */
+static hxo_workload class_task(const hxo_workload *w, int k)
+{
+    hxo_workload t = *w;
+    t.s_in = w->cls_in[k];
+    t.s_out = w->cls_out[k];
+    t.n_classes = 0;
+    return t;
+}
 /* variant bit 0: pipelined decode capacity; bit 1: KV stage-order search; bit 2: asymmetric
  * layer split (all below) */
 typedef struct { uint32_t tp_mask, pp_mask; int32_t granularity; uint32_t variant; } hxo_space;
 #define HXO_VARIANT_PIPELINED 1u
 #define HXO_VARIANT_KV_ORDER 2u  /* bit 1: KV stage-order search (hxo_kv_time_best) */
 #define HXO_VARIANT_ASYM 4u      /* bit 2: asymmetric layer split (layer_split) */
+
+/* Request classes are read with the as-written stage layout only: with the stage-order search
+ * or the asymmetric split a class mix is refused (-1). */
+static int classes_ok(const hxo_workload *w, uint32_t variant)
+{
+    if (w->n_classes < 0 || w->n_classes > HXO_MAX_CLASSES) return 0;
+    if (w->n_classes > 0 && (variant & (HXO_VARIANT_KV_ORDER | HXO_VARIANT_ASYM))) return 0;
+    return 1;
+}
 
 /* ------------------------------------------------------------------ helpers */
 
@@ -294,7 +326,14 @@ int hxo_strategy_cost(const hxo_cluster *c, const hxo_model *m, const hxo_worklo
 }
 
 /* Try every admissible TP x PP of a group and keep prefill's latency-optimal and decode's
- * throughput-optimal strategy (ties keep the smaller tp).  No feasible strategy: all zero. */
+ * throughput-optimal strategy (ties keep the smaller tp).  No feasible strategy: all zero.
+ *
+ * Request classes (w->n_classes > 0; per-bucket workloads, an alternative to the single mean
+ * task): a strategy is feasible when it is for every class; a replica serving the mix spends
+ * tau = sum_k w_k / x_k per request (x_k its capacity on class k alone, the sum in class
+ * order), so its capacity is x = 1 / tau; its latency is the mix's mean sum_k w_k lat_k and its
+ * b_max the smallest over the classes.  Prefill keeps the lowest mix latency, decode the highest
+ * x. */
 int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, const hxo_space *sp,
                      const int32_t *members, int32_t n, int32_t role,
                      int32_t *tp_out, int32_t *pp_out, int32_t *bmax_out, int32_t *cap_out, double *lat_out)
@@ -309,7 +348,26 @@ int hxo_group_select(const hxo_cluster *c, const hxo_model *m, const hxo_workloa
         if (pp > HXO_MAX_PP || !((sp->pp_mask >> (pp - 1)) & 1u) || pp > m->n_layers) continue;
         int32_t bmax;
         double lat, x;
-        if (!hxo_strategy_cost_v(c, m, w, members, n, tp, pp, role, sp->variant, &bmax, &lat, &x)) continue;
+        if (w->n_classes > 0) {
+            int ok = 1;
+            double tau = 0.0;
+            lat = 0.0;
+            bmax = 0;
+            for (int k = 0; k < w->n_classes && ok; k++) {
+                const hxo_workload tk = class_task(w, k);
+                int32_t bk;
+                double lk, xk;
+                ok = hxo_strategy_cost_v(c, m, &tk, members, n, tp, pp, role, sp->variant, &bk, &lk, &xk);
+                if (!ok) break;
+                lat = lat + w->cls_w[k] * lk;
+                tau = tau + w->cls_w[k] / xk;
+                if (k == 0 || bk < bmax) bmax = bk;
+            }
+            if (!ok) continue;
+            x = 1.0 / tau;
+        } else if (!hxo_strategy_cost_v(c, m, w, members, n, tp, pp, role, sp->variant, &bmax, &lat, &x)) {
+            continue;
+        }
         int better = !have || (role == HXO_PREFILL ? lat < best_lat : x > best_x);
         if (better) {
             have = 1; best_lat = lat; best_x = x;
@@ -465,6 +523,7 @@ int hxo_cost_eval(const hxo_cluster *c, const hxo_model *m, const hxo_workload *
                   int32_t n_cand, int32_t max_groups, const uint8_t *assign, const uint8_t *role,
                   uint8_t *tp, uint8_t *pp, int32_t *bmax, int32_t *cap, double *lat)
 {
+    if (!classes_ok(w, sp->variant)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     cost_range(&bt, 0, n_cand, tp, pp, bmax, cap, lat);
     return 0;
@@ -535,7 +594,14 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
                     (void)pn; (void)dn;
                     if (tp[gp] > 0 && tp[gd] > 0) {
                         double t;
-                        if (bt->sp->variant & HXO_VARIANT_ASYM) {
+                        if (bt->w->n_classes > 0) {
+                            /* request classes: the mix's mean KV time (weights in class order) */
+                            t = 0.0;
+                            for (int k = 0; k < bt->w->n_classes; k++) {
+                                const hxo_workload tk = class_task(bt->w, k);
+                                t = t + bt->w->cls_w[k] * hxo_kv_time(c, bt->m, &tk, pm, tp[gp], pp[gp], dm, tp[gd], pp[gd]);
+                            }
+                        } else if (bt->sp->variant & HXO_VARIANT_ASYM) {
                             /* each replica's layers follow its own (asymmetric) split */
                             int lp[HXO_MAX_PP], ld[HXO_MAX_PP], op[HXO_MAX_PP], od[HXO_MAX_PP];
                             layer_split(c, bt->m->n_layers, pm, tp[gp], pp[gp], bt->sp->variant, lp);
@@ -580,8 +646,19 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
                     int h = dnode[j];
                     int kd = bt->assign[(int64_t)h * N + n];
                     int32_t kv = 0;
-                    if (tp[(int64_t)kp * N + n] > 0 && tp[(int64_t)kd * N + n] > 0)
-                        kv = hxo_quantize(1000.0 / hxo_kv_gpu_time(c, bt->m, bt->w, g, h, szp));
+                    if (tp[(int64_t)kp * N + n] > 0 && tp[(int64_t)kd * N + n] > 0) {
+                        double t;
+                        if (bt->w->n_classes > 0) {
+                            t = 0.0;
+                            for (int k = 0; k < bt->w->n_classes; k++) {
+                                const hxo_workload tk = class_task(bt->w, k);
+                                t = t + bt->w->cls_w[k] * hxo_kv_gpu_time(c, bt->m, &tk, g, h, szp);
+                            }
+                        } else {
+                            t = hxo_kv_gpu_time(c, bt->m, bt->w, g, h, szp);
+                        }
+                        kv = hxo_quantize(1000.0 / t);
+                    }
                     f->kv_cap[(int64_t)(i * nd + j) * N + n] = kv;
                 }
             }
@@ -597,6 +674,7 @@ int hxo_build_flownet(const hxo_cluster *c, const hxo_model *m, const hxo_worklo
                       int32_t *n_p, int32_t *n_d, int32_t *p_slot, int32_t *d_slot,
                       int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap)
 {
+    if (!classes_ok(w, sp->variant)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
     flownet_range(&bt, 0, n_cand, tp, pp, cap, &f);
@@ -805,6 +883,7 @@ int hxo_score_batch(const hxo_cluster *c, const hxo_model *m, const hxo_workload
                     int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap,
                     int32_t *flow_value, int32_t *best, int32_t n_threads)
 {
+    if (!classes_ok(w, sp->variant)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
     if (n_threads < 1) n_threads = 1;

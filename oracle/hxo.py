@@ -41,8 +41,25 @@ class _Model(C.Structure):
                 ("n_kv_heads", C.c_int32), ("bytes_per_elem", C.c_int32)]
 
 
+MAX_CLASSES = 4
+
+
 class _Workload(C.Structure):
-    _fields_ = [("s_in", C.c_double), ("s_out", C.c_double)]
+    _fields_ = [("s_in", C.c_double), ("s_out", C.c_double), ("n_classes", C.c_int32),
+                ("cls_in", C.c_double * MAX_CLASSES), ("cls_out", C.c_double * MAX_CLASSES),
+                ("cls_w", C.c_double * MAX_CLASSES)]
+
+
+def _workload(prob) -> _Workload:
+    """The task t, and the request classes (rows of (s_in, s_out, weight)) when prob has them."""
+    w = _Workload(float(prob.s_in), float(prob.s_out), 0)
+    cls = getattr(prob, "classes", None)
+    if cls is not None:
+        cls = np.asarray(cls, np.float64)
+        w.n_classes = len(cls)
+        for k, (i, o, wt) in enumerate(cls):
+            w.cls_in[k], w.cls_out[k], w.cls_w[k] = float(i), float(o), float(wt)
+    return w
 
 
 class _Space(C.Structure):
@@ -67,6 +84,11 @@ def lib():
     return _lib
 
 
+def _check(rc: int, what: str) -> None:
+    if rc != 0:
+        raise ValueError(f"{what}: the oracle refused the problem ({rc})")
+
+
 def _p(a: np.ndarray) -> C.c_void_p:
     assert a.flags["C_CONTIGUOUS"]
     return C.c_void_p(a.ctypes.data)
@@ -86,7 +108,7 @@ class _Args:
                                 _p(k[4]), _p(k[5]), float(cl.coord_bw), float(cl.req_bytes))
         m = prob.model
         self.model = _Model(m["n_layers"], m["hidden"], m["n_heads"], m["n_kv_heads"], m["bytes_per_elem"])
-        self.wl = _Workload(float(prob.s_in), float(prob.s_out))
+        self.wl = _workload(prob)
         self.space = _Space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity),
                             int(getattr(prob, "variant", 0)))
 
@@ -105,8 +127,9 @@ def cost_eval(prob) -> Dict[str, np.ndarray]:
     K, N = prob.max_groups, prob.n_cand
     out = dict(tp=np.zeros((K, N), np.uint8), pp=np.zeros((K, N), np.uint8), bmax=np.zeros((K, N), np.int32),
                cap=np.zeros((K, N), np.int32), lat=np.zeros((K, N), np.float64))
-    lib().hxo_cost_eval(*a.refs(), C.c_int32(N), C.c_int32(K), _p(prob.assign), _p(prob.role),
+    rc = lib().hxo_cost_eval(*a.refs(), C.c_int32(N), C.c_int32(K), _p(prob.assign), _p(prob.role),
                         _p(out["tp"]), _p(out["pp"]), _p(out["bmax"]), _p(out["cap"]), _p(out["lat"]))
+    _check(rc, "hxo_cost_eval")
     return out
 
 
@@ -124,11 +147,12 @@ def build_flownet(prob, cost: Dict[str, np.ndarray], dims: Optional[Tuple[int, i
     dims = dims or flownet_dims(prob)
     N = prob.n_cand
     f = _flownet_arrays(N, dims)
-    lib().hxo_build_flownet(*a.refs(), C.c_int32(N), C.c_int32(prob.max_groups), _p(prob.assign),
+    rc = lib().hxo_build_flownet(*a.refs(), C.c_int32(N), C.c_int32(prob.max_groups), _p(prob.assign),
                             _p(prob.role), _p(cost["tp"]), _p(cost["pp"]), _p(cost["cap"]),
                             *(C.c_int32(x) for x in dims),
                             *(_p(f[k]) for k in ("n_p", "n_d", "p_slot", "d_slot", "src_cap", "p_cap",
                                                  "kv_cap", "d_cap", "sink_cap")))
+    _check(rc, "hxo_build_flownet")
     f["dims"] = dims
     return f
 
@@ -169,12 +193,13 @@ def score_batch(prob, n_threads: int = 1, dims=None) -> Dict[str, object]:
     f = _flownet_arrays(N, dims)
     fv = np.zeros(N, np.int32)
     best = np.zeros(2, np.int32)
-    lib().hxo_score_batch(*a.refs(), C.c_int32(N), C.c_int32(K), _p(prob.assign), _p(prob.role),
+    rc = lib().hxo_score_batch(*a.refs(), C.c_int32(N), C.c_int32(K), _p(prob.assign), _p(prob.role),
                           *(_p(cost[k]) for k in ("tp", "pp", "bmax", "cap", "lat")),
                           *(C.c_int32(x) for x in dims),
                           *(_p(f[k]) for k in ("n_p", "n_d", "p_slot", "d_slot", "src_cap", "p_cap",
                                                "kv_cap", "d_cap", "sink_cap")),
                           _p(fv), _p(best), C.c_int32(n_threads))
+    _check(rc, "hxo_score_batch")
     f["dims"] = dims
     return dict(cost=cost, flownet=f, flow_value=fv, best=(int(best[0]), int(best[1])))
 

@@ -143,6 +143,7 @@ class Problem:
     assign: np.ndarray        # uint8 [G][N]
     role: np.ndarray          # uint8 [max_groups][N]
     variant: int = 0          # cost-model variant bits (bit 0: pipelined decode capacity)
+    classes: Optional[np.ndarray] = None   # float64 [n][3]: request classes (s_in, s_out, weight)
 
     @property
     def n_cand(self) -> int:
@@ -229,6 +230,28 @@ def mean_lengths(wl: Workload) -> Tuple[float, float]:
     """The task t's s_in and s_out: exact integer sums over the drawn requests / count."""
     a, b = request_lengths(wl)
     return float(int(a.sum())) / len(a), float(int(b.sum())) / len(b)
+
+
+MAX_CLASSES = 4
+
+
+def length_classes(wl: Workload, n: int = MAX_CLASSES) -> np.ndarray:
+    """Request classes: the drawn requests sorted by prompt length (ties by output length, then
+    draw index) and cut into n runs of equal count (the first N_REQUESTS mod n one longer); a
+    class's lengths are its run's exact means and its weight the run's share of the requests.
+    Rows (s_in, s_out, weight), float64 [n][3]."""
+    if not 1 <= n <= MAX_CLASSES:
+        raise ValueError(n)
+    a, b = request_lengths(wl)
+    order = np.lexsort((np.arange(len(a)), b, a))
+    out = np.zeros((n, 3), np.float64)
+    start = 0
+    for k in range(n):
+        cnt = len(a) // n + (1 if k < len(a) % n else 0)
+        idx = order[start:start + cnt]
+        start += cnt
+        out[k] = (float(int(a[idx].sum())) / cnt, float(int(b[idx].sum())) / cnt, cnt / len(a))
+    return out
 
 
 # --------------------------------------------------------------------------- candidates
