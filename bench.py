@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--variant", choices=list(VARIANTS), default="as-written",
                     help="cost-model variant: the model as written, pipelined decode capacity, KV stage-order "
                          "search, asymmetric layer split, or combinations")
+    ap.add_argument("--classes", type=int, default=0, choices=[0, 1, 2, 3, 4],
+                    help="request classes: cost the requests as this many prompt-length buckets (0: the mean task)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline wall time")
     ap.add_argument("--refine", action="store_true",
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
@@ -127,11 +129,14 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
     return dict(cost=cost, flownet=flownet, maxflow=maxflow, best=best)
 
 
-def kernel_traffic(kernel: str, workload: int):
-    """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply."""
+def kernel_traffic(kernel: str, workload: int, prob=None):
+    """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply (the
+    counters were taken on workload 3 with the cost model as written)."""
     import hashlib
     t = KERNEL_TRAFFIC.get(kernel)
     if t is None or workload != 3:
+        return None
+    if prob is not None and (getattr(prob, "variant", 0) or getattr(prob, "classes", None) is not None):
         return None
     src = os.path.join(ROOT, "paper_2502_07903_amd", "csrc", KERNEL_SOURCE[kernel])
     if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != t["source_sha256_16"]:
@@ -163,15 +168,18 @@ def eval_fp64_ops(prob) -> float:
     """Algorithmic FP64 operations of the strategy-evaluation kernel (Table 1 rows as written,
     each add, multiply, divide, min or max one operation; prefill link terms, which do not
     depend on the candidate, count one add each).  Every admissible strategy costs its memory
-    row; a strategy whose memory row admits a batch of 1 costs the full latency sum."""
+    row; a strategy whose memory row admits a batch of 1 costs the full latency sum.  With
+    request classes a strategy is costed class by class until a class does not fit, and each
+    costed class adds 4 operations to the mix."""
     m = prob.model
     L = m["n_layers"]
     H = float(m["hidden"])
     Hkv = float(m["hidden"] * m["n_kv_heads"] // m["n_heads"])
     B = float(m["bytes_per_elem"])
     W12 = 12.0 * H * H * B
-    Kkv = 2.0 * (prob.s_in + prob.s_out) * Hkv * B
-    Kact = 4.0 * (prob.s_in + prob.s_out) * H * B
+    classes = getattr(prob, "classes", None)
+    tasks = [(prob.s_in, prob.s_out)] if classes is None else [(float(i), float(o)) for i, o, _ in classes]
+    mix_ops = 0 if classes is None else 4
     cl = prob.cluster
     gmem = np.asarray(cl.type_mem, np.float64)[np.asarray(cl.gpu_type)]
     tps = [t for t in range(1, 9) if (prob.tp_mask >> (t - 1)) & 1]
@@ -184,21 +192,26 @@ def eval_fp64_ops(prob) -> float:
             pp = sz // tp
             if pp > 8 or not (prob.pp_mask >> (pp - 1)) & 1 or pp > L:
                 continue
-            bmin = np.full(len(mem), 2.0 ** 30)
-            for j in range(pp):
-                l = L // pp + (1 if j < L % pp else 0)
-                A = (W12 / tp) * l
-                Kj = (Kkv / tp) * l + Kact
-                mm = gmem[mem[:, j * tp:(j + 1) * tp]].min(axis=1)
-                bmin = np.minimum(bmin, np.floor((mm - A) / Kj))
-            feas = bmin >= 1.0
-            total += len(mem) * pp * (tp + 8)
-            nf_d = int((feas & dec).sum())
-            nf_p = int((feas & ~dec).sum())
-            common = 4 + 4 + pp * (2 + (tp - 1) + 2) + 3
-            pre = common + pp * (3 + tp * (tp - 1) + 2) + (pp - 1) * (tp * tp + 1)
-            dcd = common + pp * ((tp - 1) + 7 + 4 * tp * (tp - 1) + 3) + (pp - 1) * (3 * tp * tp + 2)
-            total += nf_p * pre + nf_d * dcd
+            alive = np.ones(len(mem), bool)
+            for s_in, s_out in tasks:
+                Kkv = 2.0 * (s_in + s_out) * Hkv * B
+                Kact = 4.0 * (s_in + s_out) * H * B
+                bmin = np.full(len(mem), 2.0 ** 30)
+                for j in range(pp):
+                    l = L // pp + (1 if j < L % pp else 0)
+                    A = (W12 / tp) * l
+                    Kj = (Kkv / tp) * l + Kact
+                    mm = gmem[mem[:, j * tp:(j + 1) * tp]].min(axis=1)
+                    bmin = np.minimum(bmin, np.floor((mm - A) / Kj))
+                feas = alive & (bmin >= 1.0)
+                total += int(alive.sum()) * pp * (tp + 8)
+                nf_d = int((feas & dec).sum())
+                nf_p = int((feas & ~dec).sum())
+                common = 4 + 4 + pp * (2 + (tp - 1) + 2) + 3
+                pre = common + pp * (3 + tp * (tp - 1) + 2) + (pp - 1) * (tp * tp + 1)
+                dcd = common + pp * ((tp - 1) + 7 + 4 * tp * (tp - 1) + 3) + (pp - 1) * (3 * tp * tp + 2)
+                total += nf_p * (pre + mix_ops) + nf_d * (dcd + mix_ops)
+                alive = feas
     return float(total)
 
 
@@ -210,21 +223,21 @@ def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
         ops = eval_fp64_ops(prob)
         achieved = ops / t_dom / 1e9
         roof = {"kernel": "eval (hx_cost_eval)", "bound": "alu", "achieved": achieved, "peak": FP64_VALU_PEAK_GOPS,
-                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", workload),
+                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", workload, prob),
                 "algorithmic_flops_per_launch": ops}
     elif dominant == "maxflow":
         alg = float(lds_floor_bytes(n_p, n_d).sum())
         achieved = alg / t_dom / 1e9
         roof = {"kernel": "maxflow (hx_maxflow_batch)", "bound": "lds", "achieved": achieved,
                 "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
-                "traffic": kernel_traffic("maxflow", workload), "algorithmic_bytes_per_launch": alg}
+                "traffic": kernel_traffic("maxflow", workload, prob), "algorithmic_bytes_per_launch": alg}
     else:
         call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(dominant,
                                                                                                           dominant)
         alg = float(hbm[call])
         achieved = alg / t_dom / 1e9
         roof = {"kernel": dominant, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, workload),
+                "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, workload, prob),
                 "algorithmic_bytes_per_launch": alg}
     roof["avg_launch_us"] = kernel_us[dominant]
     return roof
@@ -491,6 +504,8 @@ def main():
     prob = I.make_problem(args.workload)
     if VARIANTS[args.variant]:
         prob = dataclasses.replace(prob, variant=VARIANTS[args.variant])
+    if args.classes:
+        prob = dataclasses.replace(prob, classes=I.length_classes(wl, args.classes))
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp, flows=False)
     stream = torch.cuda.current_stream()
@@ -555,7 +570,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"workload{wl.cfg}: {wl.name}", "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
-                   "cost_model": args.variant},
+                   "cost_model": args.variant, "request_classes": args.classes},
         "kernel_ms": per_kernel,
         "kernel_us": kernel_us,
         "hbm_bytes_per_step": hbm,

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define HX_ABI_VERSION 2
+#define HX_ABI_VERSION 3
 #define HX_CAP_MAX 16777215      /* 2^24 - 1 */
 #define HX_MAX_GPUS 255
 #define HX_MAX_GROUPS 255
@@ -89,8 +89,25 @@ typedef struct hx_cluster {
  * divisible by n_heads. */
 typedef struct hx_model { int32_t n_layers, hidden, n_heads, n_kv_heads, bytes_per_elem; } hx_model;
 
-/* Inference task t of Table 1: prompt length s_in and output length s_out (> 0, may be means). */
-typedef struct hx_workload { double s_in, s_out; } hx_workload;
+/* Inference task t of Table 1: prompt length s_in and output length s_out (> 0, may be means).
+ *
+ * Request classes (per-bucket workloads): with n_classes in 1..HX_MAX_CLASSES the requests are
+ * costed as n_classes length classes instead of the single task (s_in, s_out), class k with
+ * prompt length cls_in[k], output length cls_out[k] (> 0) and weight cls_w[k] (> 0, its share of
+ * the requests; used as given, not normalised).  A strategy must then fit every class in
+ * memory: b_max is the smallest per-class b_max; the latency is the mix's mean sum_k w_k lat_k;
+ * a replica's capacity is x = 1 / tau with tau = sum_k w_k / x_k (x_k its capacity on class k
+ * alone; sums left to right in class order), so prefill keeps the strategy of lowest mix
+ * latency and decode the one of highest x; a KV edge's time is sum_k w_k t_k.  The graph
+ * partition still reads the single task (s_in, s_out).  Classes are refused (HX_EINVAL) with
+ * HX_VARIANT_KV_ORDER or HX_VARIANT_ASYM.  n_classes 0: the single task; entries past
+ * n_classes are ignored. */
+#define HX_MAX_CLASSES 4
+typedef struct hx_workload {
+    double s_in, s_out;
+    int32_t n_classes;
+    double cls_in[HX_MAX_CLASSES], cls_out[HX_MAX_CLASSES], cls_w[HX_MAX_CLASSES];
+} hx_workload;
 
 /* Strategy space: bit k of tp_mask admits TP degree k+1 (<= 8), bit k of pp_mask PP degree
  * k+1 (<= 32).  granularity 0: one flow node per replica; 1: one flow node per GPU.
@@ -173,7 +190,9 @@ int hx_validate(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_sp
  * With space.variant & HX_VARIANT_ASYM, stage j holds l_j = 1 + f_j + [j < L - pp - sum_k f_k]
  * layers instead, f_j = floor(((L - pp) * c_j) / sum_k c_k) with c_j the slowest FLOP/s of the
  * stage's devices (the sum left to right; the uniform split when it is 0), in the memory row,
- * the computation and the TP term alike, and each replica's KV layer ranges follow its split. */
+ * the computation and the TP term alike, and each replica's KV layer ranges follow its split.
+ * With request classes (wl.n_classes > 0) every strategy is costed per class and mixed as
+ * described at hx_workload; tp, pp, bmax, cap and lat are then the mix's. */
 int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                  const hx_candidates *cand, const hx_cost_out *out, void *workspace,
                  size_t workspace_bytes, hipStream_t stream);
@@ -200,7 +219,9 @@ int hx_member_words(int32_t n_gpus);
  * With space.variant & HX_VARIANT_KV_ORDER (granularity 0), pipeline position a of a replica
  * may be served by any of its stages (stage s = the members ranked s*tp .. s*tp+tp-1): the
  * KV time is the minimum over every pair of stage orders of the two replicas when there are
- * at most 720 such pairs (pp_p! * pp_d! <= 720), else the ascending orders'. */
+ * at most 720 such pairs (pp_p! * pp_d! <= 720), else the ascending orders'.  With request
+ * classes (wl.n_classes > 0) the KV time is sum_k w_k t_k, t_k the time above with s_in =
+ * cls_in[k] (left to right in class order), at either granularity. */
 int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                      const hx_candidates *cand, const hx_cost_out *cost, const hx_flownet *net,
                      hipStream_t stream);

@@ -32,6 +32,10 @@ int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, 
         return HX_EINVAL;
     if (((int64_t)m.hidden * m.n_kv_heads) % m.n_heads != 0) return HX_EINVAL;
     if (!finite_pos(w.s_in) || !finite_pos(w.s_out)) return HX_EINVAL;
+    if (w.n_classes < 0 || w.n_classes > HX_MAX_CLASSES) return HX_EINVAL;
+    for (int k = 0; k < w.n_classes; ++k)
+        if (!finite_pos(w.cls_in[k]) || !finite_pos(w.cls_out[k]) || !finite_pos(w.cls_w[k])) return HX_EINVAL;
+    if (w.n_classes > 0 && (s.variant & (HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM))) return HX_EINVAL;
     if (s.tp_mask == 0 || s.tp_mask >= (1u << HX_MAX_TP) || s.pp_mask == 0) return HX_EINVAL;
     if (s.granularity != 0 && s.granularity != 1) return HX_EINVAL;
     if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM)) return HX_EINVAL;
@@ -89,6 +93,13 @@ hx::Problem make_problem(const hx_cluster* c, const hx_model& m, const hx_worklo
     p.B = (double)m.bytes_per_elem;
     p.s_in = w.s_in;
     p.s_out = w.s_out;
+    p.n_cls = w.n_classes;
+    for (int k = 0; k < HX_MAX_CLASSES; ++k) {
+        const bool in = k < w.n_classes;
+        p.cls_in[k] = in ? w.cls_in[k] : 0.0;
+        p.cls_out[k] = in ? w.cls_out[k] : 0.0;
+        p.cls_w[k] = in ? w.cls_w[k] : 0.0;
+    }
     p.coord_cap = coord_cap(c);
     p.gpu_type = c->gpu_type;
     p.flops = c->type_flops;

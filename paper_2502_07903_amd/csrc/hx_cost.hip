@@ -191,6 +191,42 @@ __device__ __forceinline__ bool cost_any(const Problem& p, const Tables& tb, con
     }
 }
 
+// Template bit of the eval kernels (above the HX_VARIANT_* bits): request classes.
+constexpr int kVarClasses = 1 << 8;
+
+// The task of class k, and its prefill tables.
+__device__ __forceinline__ void class_task(const Problem& p, const Tables& tb, int k, Problem& pk, Tables& tk) {
+    const size_t blk = (size_t)(HX_MAX_TP + 1) * p.G * p.G;
+    pk = p;
+    pk.s_in = p.cls_in[k];
+    pk.s_out = p.cls_out[k];
+    tk = tb;
+    tk.tp_pre = tb.tp_pre + k * blk;
+    tk.pp_pre = tb.pp_pre + k * blk;
+}
+
+// Strategy (tp, pp) over the request classes: feasible when it is for every class; b_max the
+// smallest, latency sum_k w_k lat_k, capacity 1 / sum_k w_k / x_k (class order, left to right).
+template <int kVar>
+__device__ __forceinline__ bool cost_mix(const Problem& p, const Tables& tb, const uint8_t* mem, int stride, int tp,
+                                         int pp, int role, StrategyCost& out) {
+    double lat = 0.0, tau = 0.0, bmax = 0.0;
+    for (int k = 0; k < p.n_cls; ++k) {
+        Problem pk;
+        Tables tk;
+        class_task(p, tb, k, pk, tk);
+        StrategyCost sk;
+        if (!cost_any<kVar>(pk, tk, mem, stride, tp, pp, role, sk)) return false;
+        lat = lat + p.cls_w[k] * sk.lat;
+        tau = tau + p.cls_w[k] / sk.x;
+        if (k == 0 || sk.bmax < bmax) bmax = sk.bmax;
+    }
+    out.bmax = bmax;
+    out.lat = lat;
+    out.x = 1.0 / tau;
+    return true;
+}
+
 // ------------------------------------------------------------------ kernels
 
 struct CostWork {
@@ -198,30 +234,36 @@ struct CostWork {
     int32_t* cursor;  // [nb]: units placed so far per bucket
     uint64_t* units;  // [max units][1 + W]: (n << 16 | k << 8 | role), then the member mask words
     uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
-    double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables)
-    double* pp_pre;   // [G][G] prefill PP terms
+    double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables), class 0
+    double* pp_pre;   // [G][G] prefill PP terms, class 0; class k's tables sit k table blocks on
+                      // ((HX_MAX_TP + 1) G^2 doubles each)
 };
 
 // First kernel of a call: clears the histogram and cursors (n_clear words) and tabulates the
 // prefill link terms.  Prefill runs at batch 1, so its per-link TP and PP terms depend only on
 // the cluster and the task: alpha + X/(tp beta) for every TP degree of the mask and
 // alpha + X/beta, X = 1*s_in*H*B, evaluated exactly as the costing expressions do (the same
-// binary64 values).
+// binary64 values).  With request classes there is one table block per class (its s_in).
 __global__ void setup_kernel(Problem p, CostWork wk, int n_clear) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_clear; i += nth) wk.hist[i] = 0;
     const int G = p.G;
     const int64_t gg = (int64_t)G * G;
-    const double X = 1.0 * p.s_in * p.H * p.B;
-    for (int64_t i = tid; i < (HX_MAX_TP + 1) * gg; i += nth) {
-        const int slot = (int)(i / gg);
-        const int64_t de = i - slot * gg;
+    const int64_t blk = (HX_MAX_TP + 1) * gg;
+    const int nt = p.n_cls > 0 ? p.n_cls : 1;
+    for (int64_t i = tid; i < nt * blk; i += nth) {
+        const int cls = (int)(i / blk);
+        const int64_t ic = i - cls * blk;
+        const double X = 1.0 * (p.n_cls > 0 ? p.cls_in[cls] : p.s_in) * p.H * p.B;
+        const int slot = (int)(ic / gg);
+        const int64_t de = ic - slot * gg;
         if (slot == HX_MAX_TP) {
-            wk.pp_pre[de] = p.alpha[de] + X / p.beta[de];
+            wk.pp_pre[cls * blk + de] = p.alpha[de] + X / p.beta[de];
         } else {
             const int tp = slot + 1;
-            if (tp >= 2 && ((p.tp_mask >> (tp - 1)) & 1u)) wk.tp_pre[i] = p.alpha[de] + X / ((double)tp * p.beta[de]);
+            if (tp >= 2 && ((p.tp_mask >> (tp - 1)) & 1u))
+                wk.tp_pre[cls * blk + ic] = p.alpha[de] + X / ((double)tp * p.beta[de]);
         }
     }
 }
@@ -463,139 +505,169 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
 }
 
 // One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
-// is false for groups past the last large unit (they still join every wave-level sync).
+// is false for groups past the last large unit (they still join every wave-level sync).  With
+// request classes (kVarClasses) each strategy is costed once per class, and the mix kept as
+// cost_mix keeps it.
 template <int kVar>
-__device__ void coop_unit(const Problem& p, const Tables& tb, const CostOut& o, const CoopLds& c, const uint8_t* adm_tab,
-                          int gl, bool live, int n, int k, int role, uint64_t mask) {
+__device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o, const CoopLds& c,
+                          const uint8_t* adm_tab, int gl, bool live, int n, int k, int role, uint64_t mask) {
     constexpr bool kPipe = (kVar & HX_VARIANT_PIPELINED) != 0;
     constexpr bool kAsym = (kVar & HX_VARIANT_ASYM) != 0;
-    const int G = p.G;
+    constexpr bool kCls = (kVar & kVarClasses) != 0;
+    const int G = p0.G;
     const int cnt = live ? __popcll(mask) : 0;
     for (int g = gl; g < G && live; g += kCoopLanes)
         if ((mask >> g) & 1ull) c.mem[__popcll(mask & ((1ull << g) - 1))] = (uint8_t)g;
     wave_sync();
-    const double H = p.H, B = p.B;
+    const double H = p0.H, B = p0.B;
     const double W12 = 12.0 * H * H * B;
-    const double Kkv = 2.0 * (p.s_in + p.s_out) * p.Hkv * B;
-    const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
     const bool prefill = role == HX_PREFILL;
     bool have = false;
     int best_tp = 0, best_pp = 0;
     double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
     const uint32_t am = live ? adm_tab[cnt] : 0u;
+    const int n_task = kCls ? p0.n_cls : 1;
     for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
         const bool adm = (am >> (tp - 1)) & 1u;
         const int pp = adm ? stage_count(cnt, tp) : 0;
         const double t = (double)tp;
-        const LayerSplit split = adm ? make_split<kAsym>(p, tb, c.mem, 1, tp, pp) : LayerSplit{0, 0, 0, 0, 0.0};
-        // Memory-limit row, one lane per stage, then the group's minimum (exact).
-        double bl = kBmaxClamp;
-        for (int j = gl; j < pp; j += kCoopLanes) {
-            const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
-            const double A = (W12 / t) * l;
-            const double K = (Kkv / t) * l + Kact;
-            const uint8_t* S = c.mem + j * tp;
-            double Mmin = tb.gme[S[0]];
-            for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, tb.gme[S[r]]);
-            const double q = (Mmin - A) / K;
-            const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
-            bl = dmin(bl, b);
-        }
-        for (int off = kCoopLanes / 2; off > 0; off >>= 1) bl = dmin(bl, __shfl_xor(bl, off, kCoopLanes));
-        const bool feas = adm && bl >= 1.0;
-        const double b = prefill ? 1.0 : bl;
-        const double Xcomp_p = 24.0 * b * p.s_in * H * H;
-        const double Xscan_d = 12.0 * H * H * B * p.s_out;
-        const double Xcomp_d = 24.0 * b * p.s_out * H * H;
-        const double X = prefill ? b * p.s_in * H * B : b * H * B;
-        // Rows (stage j, device r): the device's TP sum over its peers (ascending) and its
-        // fastest link into stage j+1.
-        for (int it = gl; feas && it < cnt; it += kCoopLanes) {
-            const int j = it / tp, r = it - j * tp;
-            const uint8_t* S = c.mem + j * tp;
-            const int d = S[r];
-            const double* arow = tb.alpha + d * G;
-            const double* brow = tb.beta + d * G;
-            const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
-            const double* qrow = tb.pp_pre + (size_t)d * G;
-            double sum = 0.0;
-            for (int q = 0; q < tp; ++q) {
-                if (q == r) continue;
-                sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
+        const LayerSplit split = adm ? make_split<kAsym>(p0, tb0, c.mem, 1, tp, pp) : LayerSplit{0, 0, 0, 0, 0.0};
+        // ok: feasible in every task so far (uniform over the group); the mix at gl == 0.
+        bool ok = adm;
+        double mix_b = 0.0, mix_lat = 0.0, mix_x = 0.0, mix_tau = 0.0;
+        for (int task = 0; task < n_task; ++task) {
+            Problem p;
+            Tables tb;
+            if (kCls) {
+                class_task(p0, tb0, task, p, tb);
+            } else {
+                p = p0;
+                tb = tb0;
             }
-            c.tsum[it] = sum;
-            if (j + 1 < pp) {
-                const uint8_t* S2 = S + tp;
-                double mn = 0.0;
+            const double Kkv = 2.0 * (p.s_in + p.s_out) * p.Hkv * B;
+            const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
+            // Memory-limit row, one lane per stage, then the group's minimum (exact).
+            double bl = kBmaxClamp;
+            for (int j = gl; j < pp; j += kCoopLanes) {
+                const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
+                const double A = (W12 / t) * l;
+                const double K = (Kkv / t) * l + Kact;
+                const uint8_t* S = c.mem + j * tp;
+                double Mmin = tb.gme[S[0]];
+                for (int r = 1; r < tp; ++r) Mmin = dmin(Mmin, tb.gme[S[r]]);
+                const double q = (Mmin - A) / K;
+                const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
+                bl = dmin(bl, b);
+            }
+            for (int off = kCoopLanes / 2; off > 0; off >>= 1) bl = dmin(bl, __shfl_xor(bl, off, kCoopLanes));
+            const bool feas = ok && bl >= 1.0;
+            const double b = prefill ? 1.0 : bl;
+            const double Xcomp_p = 24.0 * b * p.s_in * H * H;
+            const double Xscan_d = 12.0 * H * H * B * p.s_out;
+            const double Xcomp_d = 24.0 * b * p.s_out * H * H;
+            const double X = prefill ? b * p.s_in * H * B : b * H * B;
+            // Rows (stage j, device r): the device's TP sum over its peers (ascending) and its
+            // fastest link into stage j+1.
+            for (int it = gl; feas && it < cnt; it += kCoopLanes) {
+                const int j = it / tp, r = it - j * tp;
+                const uint8_t* S = c.mem + j * tp;
+                const int d = S[r];
+                const double* arow = tb.alpha + d * G;
+                const double* brow = tb.beta + d * G;
+                const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
+                const double* qrow = tb.pp_pre + (size_t)d * G;
+                double sum = 0.0;
                 for (int q = 0; q < tp; ++q) {
-                    const double v = prefill ? qrow[S2[q]] : arow[S2[q]] + X / brow[S2[q]];
-                    if (q == 0 || v < mn) mn = v;
+                    if (q == r) continue;
+                    sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
                 }
-                c.pmin[it] = mn;
-            }
-        }
-        for (int j = gl; feas && j < pp; j += kCoopLanes) {
-            const uint8_t* S = c.mem + j * tp;
-            double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
-            for (int r = 1; r < tp; ++r) {
-                cmin = dmin(cmin, tb.gfl[S[r]]);
-                hmin = dmin(hmin, tb.ghb[S[r]]);
-            }
-            const double l = (double)split_layers<kAsym>(split, j, cmin);
-            c.comp[j] = prefill ? (Xcomp_p / (t * cmin)) * l
-                                : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
-        }
-        wave_sync();
-        if (feas && gl == 0) {
-            double s1 = 0.0, s2 = 0.0, tmax = 0.0;
-            for (int j = 0; j < pp; ++j) {
-                const double l =
-                    (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
-                double mx = 0.0;
-                for (int r = 0; r < tp; ++r) {
-                    const double v = c.tsum[j * tp + r];
-                    if (r == 0 || v > mx) mx = v;
-                }
-                const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
-                const double stage = c.comp[j] + tpc;
-                s1 = s1 + stage;
-                if (kPipe && !prefill) {
-                    double T = stage;
-                    if (j + 1 < pp) {
-                        double mn = 0.0;
-                        for (int r = 0; r < tp; ++r) {
-                            const double v = c.pmin[j * tp + r];
-                            if (r == 0 || v < mn) mn = v;
-                        }
-                        T = T + mn * p.s_out;
+                c.tsum[it] = sum;
+                if (j + 1 < pp) {
+                    const uint8_t* S2 = S + tp;
+                    double mn = 0.0;
+                    for (int q = 0; q < tp; ++q) {
+                        const double v = prefill ? qrow[S2[q]] : arow[S2[q]] + X / brow[S2[q]];
+                        if (q == 0 || v < mn) mn = v;
                     }
-                    tmax = dmax(tmax, T);
+                    c.pmin[it] = mn;
                 }
             }
-            for (int j = 0; j + 1 < pp; ++j) {
-                double mn = 0.0;
-                for (int r = 0; r < tp; ++r) {
-                    const double v = c.pmin[j * tp + r];
-                    if (r == 0 || v < mn) mn = v;
+            for (int j = gl; feas && j < pp; j += kCoopLanes) {
+                const uint8_t* S = c.mem + j * tp;
+                double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
+                for (int r = 1; r < tp; ++r) {
+                    cmin = dmin(cmin, tb.gfl[S[r]]);
+                    hmin = dmin(hmin, tb.ghb[S[r]]);
                 }
-                s2 = s2 + (prefill ? mn : mn * p.s_out);
+                const double l = (double)split_layers<kAsym>(split, j, cmin);
+                c.comp[j] = prefill ? (Xcomp_p / (t * cmin)) * l
+                                    : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
             }
-            const double lat = s1 + s2;
-            const double x = (1000.0 * b) / (kPipe && !prefill ? tmax : lat);
-            const bool better = !have || (prefill ? lat < best_lat : x > best_x);
+            wave_sync();
+            if (feas && gl == 0) {
+                double s1 = 0.0, s2 = 0.0, tmax = 0.0;
+                for (int j = 0; j < pp; ++j) {
+                    const double l =
+                        (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
+                    double mx = 0.0;
+                    for (int r = 0; r < tp; ++r) {
+                        const double v = c.tsum[j * tp + r];
+                        if (r == 0 || v > mx) mx = v;
+                    }
+                    const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
+                    const double stage = c.comp[j] + tpc;
+                    s1 = s1 + stage;
+                    if (kPipe && !prefill) {
+                        double T = stage;
+                        if (j + 1 < pp) {
+                            double mn = 0.0;
+                            for (int r = 0; r < tp; ++r) {
+                                const double v = c.pmin[j * tp + r];
+                                if (r == 0 || v < mn) mn = v;
+                            }
+                            T = T + mn * p.s_out;
+                        }
+                        tmax = dmax(tmax, T);
+                    }
+                }
+                for (int j = 0; j + 1 < pp; ++j) {
+                    double mn = 0.0;
+                    for (int r = 0; r < tp; ++r) {
+                        const double v = c.pmin[j * tp + r];
+                        if (r == 0 || v < mn) mn = v;
+                    }
+                    s2 = s2 + (prefill ? mn : mn * p.s_out);
+                }
+                const double lat = s1 + s2;
+                const double x = (1000.0 * b) / (kPipe && !prefill ? tmax : lat);
+                if (kCls) {
+                    mix_lat = mix_lat + p0.cls_w[task] * lat;
+                    mix_tau = mix_tau + p0.cls_w[task] / x;
+                    if (task == 0 || bl < mix_b) mix_b = bl;
+                } else {
+                    mix_lat = lat;
+                    mix_x = x;
+                    mix_b = bl;
+                }
+            }
+            ok = feas;
+            wave_sync();
+        }
+        if (ok && gl == 0) {
+            const double x = kCls ? 1.0 / mix_tau : mix_x;
+            const bool better = !have || (prefill ? mix_lat < best_lat : x > best_x);
             if (better) {
                 have = true;
                 best_tp = tp;
                 best_pp = pp;
-                best_b = bl;
-                best_lat = lat;
+                best_b = mix_b;
+                best_lat = mix_lat;
                 best_x = x;
             }
         }
-        wave_sync();
     }
     if (live && gl == 0) {
-        const int64_t o_ = (int64_t)k * p.N + n;
+        const int64_t o_ = (int64_t)k * p0.N + n;
         o.tp[o_] = (uint8_t)best_tp;
         o.pp[o_] = (uint8_t)best_pp;
         o.bmax[o_] = (int32_t)best_b;
@@ -695,7 +767,11 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
             const int tp = __ffs(am);
             const int pp = stage_count(cnt, tp);
             StrategyCost sc;
-            if (!cost_any<kVar>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            if constexpr ((kVar & kVarClasses) != 0) {
+                if (!cost_mix<kVar & ~kVarClasses>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
+            } else if (!cost_any<kVar>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) {
+                continue;
+            }
             const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
             if (better) {
                 have = true;
@@ -785,8 +861,12 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     prof_mark(kKEval, false, s);
-    switch (p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) {
+    switch ((p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) | (p.n_cls > 0 ? kVarClasses : 0)) {
         case 0: launch_eval<W, 0>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case kVarClasses: launch_eval<W, kVarClasses>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case kVarClasses | HX_VARIANT_PIPELINED:
+            launch_eval<W, kVarClasses | HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+            break;
         case HX_VARIANT_PIPELINED: launch_eval<W, HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
         case HX_VARIANT_ASYM: launch_eval<W, HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
         default:
@@ -809,7 +889,7 @@ static size_t units_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
-    const size_t tables = sizeof(double) * (HX_MAX_TP + 1) * (size_t)n_gpus * n_gpus;
+    const size_t tables = sizeof(double) * HX_MAX_CLASSES * (HX_MAX_TP + 1) * (size_t)n_gpus * n_gpus;
     return head + units_bytes(n_gpus, max_groups, n_cand) + tables;
 }
 

@@ -9,7 +9,7 @@
 //   kv_kernel     one lane per (KV edge, candidate): the edge capacity between prefill node
 //                 i and decode node j (connection type 3; Table 1 last row; Appendix A), with
 //                 the stage-order search of Appendix A (kv_order_kernel) when
-//                 HX_VARIANT_KV_ORDER is set.
+//                 HX_VARIANT_KV_ORDER is set, and the class mix with request classes.
 #include "hx_internal.h"
 
 namespace hx {
@@ -369,7 +369,22 @@ __device__ double kv_time_asym(const Problem& p, const uint8_t* pm, int ptp, int
     return worst;
 }
 
-template <int W, bool kAsym>
+// With request classes (kCls) an edge's time is sum_k w_k t_k over the classes (t_k the time
+// with s_in = cls_in[k], class order, left to right).
+template <bool kCls, class TimeOf>
+__device__ __forceinline__ double task_mix(const Problem& p, TimeOf time_of) {
+    if (!kCls) return time_of(p);
+    double t = 0.0;
+    for (int k = 0; k < p.n_cls; ++k) {
+        Problem pk = p;
+        pk.s_in = p.cls_in[k];
+        pk.s_out = p.cls_out[k];
+        t = t + p.cls_w[k] * time_of(pk);
+    }
+    return t;
+}
+
+template <int W, bool kAsym, bool kCls>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ uint8_t sm[];
     const int tid = threadIdx.x;
@@ -394,8 +409,10 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
             // is treated as infeasible rather than read past the member list.
             if (expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
                 expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp)
-                c = quantize(1000.0 / (kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                             : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
+                c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
+                                 return kAsym ? kv_time_asym(q, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                              : kv_time(q, pm, ptp, ppp, dm, dtp, dpp, stride);
+                             }));
         }
     } else {
         // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
@@ -403,9 +420,11 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
         const int kp = p.assign[(int64_t)g * N + n], kd = p.assign[(int64_t)h * N + n];
         if (o.tp[(int64_t)kp * N + n] > 0 && o.tp[(int64_t)kd * N + n] > 0) {
             const int szp = mask_size<W>(o.members, kp, N, n);
-            const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
-            const double share = (V1 * (double)p.L) / (double)szp;
-            c = quantize(1000.0 / (p.alpha[g * p.G + h] + share / p.beta[g * p.G + h]));
+            c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
+                             const double V1 = 2.0 * q.s_in * q.Hkv * q.B;
+                             const double share = (V1 * (double)q.L) / (double)szp;
+                             return q.alpha[g * q.G + h] + share / q.beta[g * q.G + h];
+                         }));
         }
     }
     f.kv_cap[(int64_t)e * N + n] = c;
@@ -423,9 +442,11 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     if (p.granularity == 0 && (p.variant & HX_VARIANT_KV_ORDER))
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     else if (p.granularity == 0 && (p.variant & HX_VARIANT_ASYM))
-        hipLaunchKernelGGL((kv_kernel<W, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    else if (p.n_cls > 0)
+        hipLaunchKernelGGL((kv_kernel<W, false, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     else
-        hipLaunchKernelGGL((kv_kernel<W, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, false, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     prof_mark(kKKv, true, s);
     return hipGetLastError();
 }

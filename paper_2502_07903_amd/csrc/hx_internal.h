@@ -17,6 +17,8 @@ struct Problem {
     int32_t granularity;
     uint32_t variant;  // HX_VARIANT_* bits
     double H, Hkv, B, s_in, s_out;
+    int32_t n_cls;  // request classes (0: the single task s_in, s_out)
+    double cls_in[HX_MAX_CLASSES], cls_out[HX_MAX_CLASSES], cls_w[HX_MAX_CLASSES];
     int32_t coord_cap;
     const int32_t* gpu_type;
     const double *flops, *hbm, *mem, *beta, *alpha;

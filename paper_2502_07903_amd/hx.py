@@ -47,8 +47,28 @@ class hx_model(C.Structure):
                 ("n_kv_heads", C.c_int32), ("bytes_per_elem", C.c_int32)]
 
 
+HX_MAX_CLASSES = 4
+
+
 class hx_workload(C.Structure):
-    _fields_ = [("s_in", C.c_double), ("s_out", C.c_double)]
+    _fields_ = [("s_in", C.c_double), ("s_out", C.c_double), ("n_classes", C.c_int32),
+                ("cls_in", C.c_double * HX_MAX_CLASSES), ("cls_out", C.c_double * HX_MAX_CLASSES),
+                ("cls_w", C.c_double * HX_MAX_CLASSES)]
+
+
+def make_workload(prob) -> hx_workload:
+    """The task (s_in, s_out) and, when prob has them, its request classes (rows of
+    (s_in, s_out, weight))."""
+    w = hx_workload(float(prob.s_in), float(prob.s_out), 0)
+    cls = getattr(prob, "classes", None)
+    if cls is not None:
+        cls = np.asarray(cls, np.float64)
+        if cls.ndim != 2 or cls.shape[1] != 3 or len(cls) > HX_MAX_CLASSES:
+            raise ValueError("classes: at most four rows of (s_in, s_out, weight)")
+        w.n_classes = len(cls)
+        for k, (i, o, wt) in enumerate(cls):
+            w.cls_in[k], w.cls_out[k], w.cls_w[k] = float(i), float(o), float(wt)
+    return w
 
 
 class hx_space(C.Structure):
@@ -218,7 +238,7 @@ class DeviceProblem:
         md = hx_model(m["n_layers"], m["hidden"], m["n_heads"], m["n_kv_heads"], m["bytes_per_elem"])
         n_cand = int(t["assign"].shape[1])
         k = hx_candidates(n_cand, int(prob.max_groups), _ptr(t["assign"]), _ptr(t["role"]))
-        return cls(t, c, md, hx_workload(float(prob.s_in), float(prob.s_out)),
+        return cls(t, c, md, make_workload(prob),
                    hx_space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity),
                             int(getattr(prob, "variant", 0))), k, cl.n_gpus,
                    int(prob.max_groups))

@@ -28,7 +28,7 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version_and_strings():
-    assert hx.lib().hx_abi_version() == 2
+    assert hx.lib().hx_abi_version() == 3
     for code in (0, -1, -2, -3, -4):
         assert hx.strerror(code)
     assert hx.lib().hx_last_error() is not None
@@ -62,6 +62,18 @@ def test_validate_accepts_workloads():
     for v in (1, 2, 3, 4, 5):                           # HX_VARIANT_PIPELINED, _KV_ORDER, _ASYM
         a[3].variant = v
         assert _validate(*a) == hx.HX_OK
+    a = list(_args())
+    for n in (1, 4):                                    # request classes, alone and pipelined
+        _classes(a[2], n)
+        for v in (0, 1):
+            a[3].variant = v
+            assert _validate(*a) == hx.HX_OK
+
+
+def _classes(wl, n):
+    wl.n_classes = n
+    for k in range(n):
+        wl.cls_in[k], wl.cls_out[k], wl.cls_w[k] = 300.0 * (k + 1), 400.0, 1.0 / n
 
 
 @pytest.mark.parametrize("mutate", [
@@ -74,6 +86,13 @@ def test_validate_accepts_workloads():
     lambda a: setattr(a[1], "n_heads", 48),          # H_kv = 8192 * 8 / 48 is not whole
     lambda a: setattr(a[2], "s_in", 0.0),
     lambda a: setattr(a[2], "s_out", float("nan")),
+    lambda a: setattr(a[2], "n_classes", 5),        # more than HX_MAX_CLASSES
+    lambda a: setattr(a[2], "n_classes", -1),
+    lambda a: (_classes(a[2], 2), a[2].cls_w.__setitem__(1, 0.0)),
+    lambda a: (_classes(a[2], 3), a[2].cls_in.__setitem__(2, float("inf"))),
+    lambda a: (_classes(a[2], 1), a[2].cls_out.__setitem__(0, -5.0)),
+    lambda a: (_classes(a[2], 4), setattr(a[3], "variant", 2)),   # classes with the stage-order search
+    lambda a: (_classes(a[2], 4), setattr(a[3], "variant", 4)),   # classes with the asymmetric split
     lambda a: setattr(a[3], "tp_mask", 0),
     lambda a: setattr(a[3], "tp_mask", 1 << 8),      # TP degree 9 > 8
     lambda a: setattr(a[3], "pp_mask", 0),
