@@ -174,6 +174,66 @@ __device__ double kv_time(const Problem& p, const uint8_t* pm, int ptp, int ppp,
     return worst;
 }
 
+// kv_time of every request class in one walk: the links, their member ids and alpha/beta are
+// the same for every class, only the bytes differ (V1 from the class's s_in), so the walk keeps
+// one running maximum per class and returns sum_k w_k worst_k (class order, left to right).
+// Each class's maximum is the binary64 value kv_time returns for that class.
+__device__ double kv_time_classes(const Problem& p, const uint8_t* pm, int ptp, int ppp, const uint8_t* dm, int dtp,
+                                  int dpp, int stride) {
+    const int nc = p.n_cls;
+    double V1[HX_MAX_CLASSES], worst[HX_MAX_CLASSES];
+#pragma unroll
+    for (int k = 0; k < HX_MAX_CLASSES; ++k) {
+        V1[k] = 2.0 * p.cls_in[k] * p.Hkv * p.B;
+        worst[k] = 0.0;
+    }
+    const int deni = ptp * dtp;
+    const double den = (double)deni;
+    const bool pow2 = (deni & (deni - 1)) == 0;
+    const double inv_den = 1.0 / den;
+    const int lqp = p.L / ppp, lrp = p.L % ppp, lqd = p.L / dpp, lrd = p.L % dpp;
+    int a = 0, bb = 0, a0 = 0, b0 = 0;
+    int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
+    while (a < ppp && bb < dpp) {
+        const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+        const uint8_t* Sa = pm + (a * ptp) * stride;
+        const uint8_t* Sb = dm + (bb * dtp) * stride;
+        int r = 0, q = 0;
+        while (r < ptp && q < dtp) {
+            const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+            const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+            const int g = Sa[r * stride], h = Sb[q * stride];
+            const double al = p.alpha[g * p.G + h], be = p.beta[g * p.G + h];
+#pragma unroll
+            for (int k = 0; k < HX_MAX_CLASSES; ++k) {
+                if (k >= nc) break;
+                const double Vn = V1[k] * (double)nab;
+                const double bytes = pow2 ? (Vn * (double)ov) * inv_den : (Vn * (double)ov) / den;
+                const double time = al + bytes / be;
+                if (time > worst[k]) worst[k] = time;
+            }
+            if (re <= qe) ++r;
+            if (qe <= re) ++q;
+        }
+        const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
+        if (adv_a) {
+            ++a;
+            a0 = a1;
+            a1 = a0 + lqp + (a < lrp ? 1 : 0);
+        }
+        if (adv_b) {
+            ++bb;
+            b0 = b1;
+            b1 = b0 + lqd + (bb < lrd ? 1 : 0);
+        }
+    }
+    double t = 0.0;
+#pragma unroll
+    for (int k = 0; k < HX_MAX_CLASSES; ++k)
+        if (k < nc) t = t + p.cls_w[k] * worst[k];
+    return t;
+}
+
 // KV stage-order search (HX_VARIANT_KV_ORDER; Appendix A, edge capacity estimation): the stage
 // order of both replicas is chosen to minimise the KV time.  Orders are packed 4 bits per
 // pipeline position (position a is served by stage (ord >> 4a) & 15); pairs of pipelines with
@@ -409,10 +469,9 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
             // is treated as infeasible rather than read past the member list.
             if (expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
                 expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp)
-                c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
-                                 return kAsym ? kv_time_asym(q, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                              : kv_time(q, pm, ptp, ppp, dm, dtp, dpp, stride);
-                             }));
+                c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                       : kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                               : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
         }
     } else {
         // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
