@@ -124,22 +124,52 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                                     : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
         // TP row: the device with the largest sum over its peers (ascending peer order).
         double mx = 0.0;
-#pragma unroll 1
-        for (int r = 0; r < tp; ++r) {
-            int d = S[0];
+        if (TPC > 0 && TPC <= 4 && !prefill) {
+            // Decode with tp fixed: the pairs (r, q), r < q, in ascending order.  Device r's sum
+            // takes its peers q > r here, after its peers q < r arrived from earlier r, so every
+            // device's sum is still formed in ascending peer order.  X / (t beta) of a link is
+            // computed once for both directions when beta_{dq} and beta_{qd} have the same bits
+            // (the same binary64 quotient), and separately otherwise.
+            double sum[kMax];
 #pragma unroll
-            for (int x = 1; x < kMax; ++x)
-                if (x == r) d = S[x];
-            const double* arow = tb.alpha + d * G;
-            const double* brow = tb.beta + d * G;
-            const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
-            double sum = 0.0;
+            for (int r = 0; r < kMax; ++r) sum[r] = 0.0;
 #pragma unroll
-            for (int q = 0; q < kMax; ++q) {
-                if ((TPC == 0 && q >= tp) || q == r) continue;
-                sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
+            for (int r = 0; r < kMax; ++r) {
+                const double* arow = tb.alpha + S[r] * G;
+                const double* brow = tb.beta + S[r] * G;
+#pragma unroll
+                for (int q = r + 1; q < kMax; ++q) {
+                    const double bf = brow[S[q]], bb = tb.beta[S[q] * G + S[r]];
+                    const double qf = X / (t * bf);
+                    double qb = qf;
+                    if (__double_as_longlong(bf) != __double_as_longlong(bb)) qb = X / (t * bb);
+                    sum[r] = sum[r] + (arow[S[q]] + qf);
+                    sum[q] = sum[q] + (tb.alpha[S[q] * G + S[r]] + qb);
+                    // keep each pair's loads and divisions together (bounded live ranges)
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
-            if (r == 0 || sum > mx) mx = sum;
+#pragma unroll
+            for (int r = 0; r < kMax; ++r)
+                if (r == 0 || sum[r] > mx) mx = sum[r];
+        } else {
+#pragma unroll 1
+            for (int r = 0; r < tp; ++r) {
+                int d = S[0];
+#pragma unroll
+                for (int x = 1; x < kMax; ++x)
+                    if (x == r) d = S[x];
+                const double* arow = tb.alpha + d * G;
+                const double* brow = tb.beta + d * G;
+                const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
+                double sum = 0.0;
+#pragma unroll
+                for (int q = 0; q < kMax; ++q) {
+                    if ((TPC == 0 && q >= tp) || q == r) continue;
+                    sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
+                }
+                if (r == 0 || sum > mx) mx = sum;
+            }
         }
         const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
         const double stage = comp + tpc;

@@ -3,6 +3,7 @@ on the same seeded inputs.  Integers (strategies, batch limits, capacities, flow
 minimum cut, the argmax) must be bit-exact; latencies must agree to 1e-5 relative (they are
 expected bit-identical: both sides evaluate the same binary64 expressions without FMA);
 KV flow assignments are not unique, so they are checked for validity instead."""
+import dataclasses
 import os
 import sys
 
@@ -119,6 +120,25 @@ def test_workload_parity(torch, cfg):
 @pytest.mark.parametrize("cfg,n", [(1, 1), (2, 7), (3, 1000), (4, 777), (3, 4097)])
 def test_ragged_batches(torch, cfg, n):
     full_parity(torch, I.make_problem(cfg, n_cand=n), f"workload {cfg} ragged")
+
+
+@pytest.mark.parametrize("cfg,frac", [(2, 1.0), (3, 0.5), (3, 0.02)])
+def test_asymmetric_links(torch, cfg, frac):
+    """Links whose two directions differ (beta_gh != beta_hg, alpha too) on a seeded fraction of
+    the GPU pairs: every direction-dependent term, and the decode TP row's reuse of a quotient
+    for both directions only where the two betas are the same, against the oracle."""
+    prob = I.make_problem(cfg, n_cand=4096)
+    G = prob.n_gpus
+    rng = np.random.default_rng(7000 + cfg)
+    beta = np.asarray(prob.cluster.beta, np.float64).reshape(G, G).copy()
+    alpha = np.asarray(prob.cluster.alpha, np.float64).reshape(G, G).copy()
+    pick = np.triu(rng.random((G, G)) < frac, 1)
+    beta[pick] *= rng.uniform(0.5, 1.5, int(pick.sum()))
+    alpha[pick] *= rng.uniform(0.5, 1.5, int(pick.sum()))
+    cl = dataclasses.replace(prob.cluster, beta=np.ascontiguousarray(beta.reshape(-1)),
+                             alpha=np.ascontiguousarray(alpha.reshape(-1)))
+    assert (beta != beta.T).any()
+    full_parity(torch, dataclasses.replace(prob, cluster=cl), f"workload {cfg} asymmetric links ({frac})")
 
 
 def test_refinement_round0_sample(torch):
