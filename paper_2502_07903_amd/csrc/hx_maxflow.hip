@@ -37,6 +37,8 @@
 //
 // Outputs: the flow value, the flow on every KV edge, and the canonical minimum cut (nodes of
 // the uncontracted network reachable from the source in the residual graph).
+#include <limits.h>
+
 #include "hx_internal.h"
 
 namespace hx {
@@ -133,13 +135,25 @@ __device__ __forceinline__ int32_t nw_overlap(int32_t ae, int32_t ai, int32_t be
 }
 
 // Value-only pre-pass of the workgroup plans.  Those plans give a workgroup one candidate,
-// whose KV rows then sit in as many cache lines as it has arcs; here one lane per candidate
-// (candidate-fastest, so every row load coalesces across the wavefront) tests the dominant-KV
-// condition on every arc and writes min(sum a, sum b) as the flow value when it holds, 0 when
-// no source-side or no sink-side node can carry flow, and -1 otherwise; maxflow_kernel then
-// solves only the candidates left at -1.  Networks with negative capacities or counts
-// outside the plan are left to maxflow_kernel.
+// whose KV rows then sit in as many cache lines as it has arcs; here lanes run over candidates
+// (candidate-fastest, so every row load coalesces across the wavefront) in two kernels:
+//   bound_kernel  one lane per candidate: writes min(sum a, sum b) as the candidate's flow
+//                 value, 0 when no source-side or no sink-side node can carry flow, and -1 for
+//                 networks with negative capacities or counts outside the plan;
+//   dom_kernel    the dominant-KV condition c_ij >= min(a_i, b_j) on every arc, the arcs of a
+//                 candidate split over kDomParts wavefronts (a long serial walk per candidate
+//                 would leave the kernel waiting on one memory round per few arcs): an arc
+//                 that fails it sets the flow value to -1.  It only ever writes -1, so the
+//                 order of its writes does not matter.  c_ij >= a_i already implies the
+//                 condition, so b_j is loaded only for arcs below a_i.
+// maxflow_kernel then solves only the candidates left at -1.
 constexpr int kBoundBlock = 256;
+constexpr int kDomParts = 32;
+constexpr int kDomUnroll = 8;
+
+__device__ __forceinline__ bool plan_ok(const FlowNet& f, int P, int D) {
+    return P >= 0 && D >= 0 && P <= f.max_p && D <= f.max_d && P * D <= f.max_pd;
+}
 
 __global__ void __launch_bounds__(kBoundBlock) bound_kernel(FlowNet f, int32_t* flow_value) {
     const int n = blockIdx.x * kBoundBlock + threadIdx.x;
@@ -147,50 +161,73 @@ __global__ void __launch_bounds__(kBoundBlock) bound_kernel(FlowNet f, int32_t* 
     const int64_t N = f.N;
     const int P = f.n_p[n], D = f.n_d[n];
     int32_t out = -1;
-    if (P >= 0 && D >= 0 && P <= f.max_p && D <= f.max_d && P * D <= f.max_pd) {
-        auto a_of = [&](int i) {
-            const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
-            return s < c ? s : c;
-        };
-        auto b_of = [&](int j) {
-            const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
-            return c < t ? c : t;
-        };
+    if (plan_ok(f, P, D)) {
         long long sa = 0, sb = 0;
         bool neg = false, any_a = false, any_b = false;
         for (int i = 0; i < P; ++i) {
-            const int32_t a = a_of(i);
+            const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+            const int32_t a = s < c ? s : c;
             sa += a;
             neg |= a < 0;
             any_a |= a > 0;
         }
         for (int j = 0; j < D; ++j) {
-            const int32_t b = b_of(j);
+            const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+            const int32_t b = c < t ? c : t;
             sb += b;
             neg |= b < 0;
             any_b |= b > 0;
         }
-        if (!neg) {
-            if (!any_a || !any_b) {
-                out = 0;
-            } else {
-                bool dom = true;
-                int i = 0, j = 0;
-                int32_t ai = a_of(0);
-                for (int e = 0; e < P * D && dom; ++e) {
-                    const int32_t c = f.kv_cap[(int64_t)e * N + n];
+        if (!neg) out = (!any_a || !any_b) ? 0 : (int32_t)(sa < sb ? sa : sb);
+    }
+    flow_value[n] = out;
+}
+
+// Wavefront (part k, candidate chunk): arcs e in [k R, (k + 1) R) of each lane's candidate,
+// R = ceil(max_pd / kDomParts), in ascending e (prefill node i = e / D, decode node j = e mod D).
+__global__ void __launch_bounds__(64) dom_kernel(FlowNet f, int32_t* flow_value) {
+    const int64_t N = f.N;
+    // part-major: consecutive wavefronts take neighbouring candidate chunks of the same rows
+    const int chunks = (int)((N + 63) / 64);
+    const int part = blockIdx.x / chunks;
+    const int64_t n = (int64_t)(blockIdx.x - part * chunks) * 64 + threadIdx.x;
+    if (n >= N) return;
+    if (flow_value[n] <= 0) return;  // -1: left to maxflow_kernel; 0: no flow either way
+    const int P = f.n_p[n], D = f.n_d[n];
+    const int R = (f.max_pd + kDomParts - 1) / kDomParts;
+    const int E = P * D;
+    const int lo = part * R, hi = lo + R < E ? lo + R : E;
+    if (lo >= hi) return;
+    auto a_of = [&](int i) {
+        const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+        return s < c ? s : c;
+    };
+    auto b_of = [&](int j) {
+        const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+        return c < t ? c : t;
+    };
+    int i = lo / D, j = lo - i * D;
+    int32_t ai = a_of(i);
+    bool dom = true;
+    for (int e0 = lo; e0 < hi && dom; e0 += kDomUnroll) {
+        int32_t c[kDomUnroll];
+#pragma unroll
+        for (int x = 0; x < kDomUnroll; ++x) c[x] = e0 + x < hi ? f.kv_cap[(int64_t)(e0 + x) * N + n] : INT_MAX;
+#pragma unroll
+        for (int x = 0; x < kDomUnroll; ++x) {
+            if (e0 + x < hi) {
+                if (c[x] < ai) {
                     const int32_t bj = b_of(j);
-                    dom = c >= (ai < bj ? ai : bj);
-                    if (++j == D) {
-                        j = 0;
-                        if (++i < P) ai = a_of(i);
-                    }
+                    dom = dom && c[x] >= (ai < bj ? ai : bj);
                 }
-                if (dom) out = (int32_t)(sa < sb ? sa : sb);
+                if (++j == D) {
+                    j = 0;
+                    if (++i < P && e0 + x + 1 < hi) ai = a_of(i);
+                }
             }
         }
     }
-    flow_value[n] = out;
+    if (!dom) flow_value[n] = -1;
 }
 
 // SEG lanes per candidate; the workgroup holds max(64, SEG) lanes, i.e. 64/SEG candidates
@@ -682,8 +719,11 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
     const int tiles = (f.N + kPer - 1) / kPer;
     const int blocks = 8 * ((tiles + 7) / 8);
     prof_mark(kKMaxflow, false, s);
-    if (SEG > 64 && kv == nullptr && cut == nullptr)
+    if (SEG > 64 && kv == nullptr && cut == nullptr) {
         hipLaunchKernelGGL(bound_kernel, dim3((f.N + kBoundBlock - 1) / kBoundBlock), dim3(kBoundBlock), 0, s, f, fv);
+        const int chunks = (f.N + 63) / 64;
+        hipLaunchKernelGGL(dom_kernel, dim3(chunks * kDomParts), dim3(64), 0, s, f, fv);
+    }
     hipLaunchKernelGGL(maxflow_kernel<SEG>, dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget);
     prof_mark(kKMaxflow, true, s);
     return hipGetLastError();
