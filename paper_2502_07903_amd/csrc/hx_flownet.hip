@@ -7,9 +7,10 @@
 //                 ascending group id, or GPUs in ascending id at per-GPU granularity) with
 //                 their source, node and sink capacities (Appendix A);
 //   kv_kernel     one lane per (KV edge, candidate): the edge capacity between prefill node
-//                 i and decode node j (connection type 3; Table 1 last row; Appendix A), with
-//                 the stage-order search of Appendix A (kv_order_kernel) when
-//                 HX_VARIANT_KV_ORDER is set, and the class mix with request classes.
+//                 i and decode node j (connection type 3; Table 1 last row; Appendix A) of
+//                 replica nodes, with the stage-order search of Appendix A (kv_order_kernel)
+//                 when HX_VARIANT_KV_ORDER is set, and the class mix with request classes;
+//   kv_gpu_kernel the same for per-GPU nodes, a workgroup per 64 candidates.
 #include "hx_internal.h"
 
 namespace hx {
@@ -117,6 +118,22 @@ __device__ __forceinline__ int expand(const uint64_t* gm, int k, int64_t N, int 
 #pragma unroll
     for (int i = 0; i < W; ++i) {
         uint64_t m = gm[((int64_t)k * W + i) * N + n];
+        while (m) {
+            out[(cnt++) * stride] = (uint8_t)(i * 64 + __builtin_ctzll(m));
+            m &= m - 1;
+        }
+    }
+    return cnt;
+}
+
+// Members of a group given its mask words, in ascending GPU id into out[r * stride]; returns the
+// count.
+template <int W>
+__device__ __forceinline__ int expand_words(const uint64_t* mw, uint8_t* out, int stride) {
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        uint64_t m = mw[i];
         while (m) {
             out[(cnt++) * stride] = (uint8_t)(i * 64 + __builtin_ctzll(m));
             m &= m - 1;
@@ -458,35 +475,105 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
     if (e >= np * nd) return;
     const int i = e / nd, j = e - i * nd;
     int32_t c = 0;
-    if (p.granularity == 0) {
-        const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
-        const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
-        const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
-        if (ptp > 0 && dtp > 0) {
-            uint8_t* pm = sm + tid;                   // [G][blockDim]
-            uint8_t* dm = sm + p.G * stride + tid;    // [G][blockDim]
-            // A strategy whose tp*pp is not the group's size (cost outputs of another batch)
-            // is treated as infeasible rather than read past the member list.
-            if (expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
-                expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp)
-                c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                       : kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                               : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
-        }
-    } else {
-        // Per-GPU edge g -> h: g's 1/n_g share of a request's KV cache for all L layers.
-        const int g = f.p_slot[(int64_t)i * N + n], h = f.d_slot[(int64_t)j * N + n];
-        const int kp = p.assign[(int64_t)g * N + n], kd = p.assign[(int64_t)h * N + n];
-        if (o.tp[(int64_t)kp * N + n] > 0 && o.tp[(int64_t)kd * N + n] > 0) {
-            const int szp = mask_size<W>(o.members, kp, N, n);
-            c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
-                             const double V1 = 2.0 * q.s_in * q.Hkv * q.B;
-                             const double share = (V1 * (double)q.L) / (double)szp;
-                             return q.alpha[g * q.G + h] + share / q.beta[g * q.G + h];
-                         }));
-        }
+    const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
+    // The member masks are loaded with the strategies (not after them), so the lane waits on
+    // one memory round for both.
+    uint64_t mp[W], md[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        mp[w] = o.members[((int64_t)kp * W + w) * N + n];
+        md[w] = o.members[((int64_t)kd * W + w) * N + n];
+    }
+    const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
+    const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
+    if (ptp > 0 && dtp > 0) {
+        uint8_t* pm = sm + tid;                 // [G][blockDim]
+        uint8_t* dm = sm + p.G * stride + tid;  // [G][blockDim]
+        // A strategy whose tp*pp is not the group's size (cost outputs of another batch) is
+        // treated as infeasible rather than read past the member list.
+        if (expand_words<W>(mp, pm, stride) == ptp * ppp && expand_words<W>(md, dm, stride) == dtp * dpp)
+            c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                   : kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                           : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
     }
     f.kv_cap[(int64_t)e * N + n] = c;
+}
+
+// Per-GPU nodes: one workgroup of kGpuKvWaves wavefronts per 64 candidates (a lane per
+// candidate in every wavefront).  The edge from prefill GPU g (replica of n_g GPUs) to decode
+// GPU h depends on g, h, n_g and whether both replicas are feasible, so the workgroup first
+// stages, per candidate, every GPU's replica size, 0 when the replica is infeasible ([G][64]
+// bytes in LDS), and the node lists' GPU ids; then each wavefront takes every kGpuKvWaves-th edge row (coalesced
+// stores across the 64 candidates) with no dependent global loads but alpha/beta.  One lane per
+// (edge, candidate) would repeat the lookups of both endpoints for every edge.
+constexpr int kGpuKvWaves = 4;
+
+// Node rows staged per side: a side has at most G per-GPU nodes.
+__host__ __device__ inline int kv_gpu_rows(int G, int max_rows) { return max_rows < G ? max_rows : G; }
+
+__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d) {
+    return ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
+}
+
+template <int W, bool kCls>
+__global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, CostOut o, FlowNet f) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char sm[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t N = p.N;
+    const int64_t n = (int64_t)blockIdx.x * 64 + lane;
+    const bool in = n < N;
+    const int G = p.G;
+    uint8_t* gd = sm;                         // [G][64]: replica size, 0 if infeasible or unused
+    uint8_t* ps = sm + (size_t)G * 64;        // [prow][64]: prefill node -> GPU
+    const int prow = kv_gpu_rows(G, f.max_p), drow = kv_gpu_rows(G, f.max_d);
+    uint8_t* ds = ps + (size_t)prow * 64;     // [drow][64]: decode node -> GPU
+    const int np = in ? f.n_p[n] : 0, nd = in ? f.n_d[n] : 0;
+    for (int g = wave; g < G; g += kGpuKvWaves) {
+        uint8_t d = 0;
+        if (in) {
+            const int k = p.assign[(int64_t)g * N + n];
+            if (k < p.Kmax && o.tp[(int64_t)k * N + n] > 0) d = (uint8_t)mask_size<W>(o.members, k, N, n);
+        }
+        gd[g * 64 + lane] = d;
+    }
+    for (int i = wave; i < prow; i += kGpuKvWaves)
+        ps[i * 64 + lane] = i < np ? (uint8_t)f.p_slot[(int64_t)i * N + n] : 0;
+    for (int j = wave; j < drow; j += kGpuKvWaves)
+        ds[j * 64 + lane] = j < nd ? (uint8_t)f.d_slot[(int64_t)j * N + n] : 0;
+    __syncthreads();
+    const int E = np * nd;
+    int emax = E;
+    for (int off = 32; off > 0; off >>= 1) {
+        const int v = __shfl_xor(emax, off, 64);
+        emax = v > emax ? v : emax;
+    }
+    // edge e = i * nd + j of this lane's candidate, rows wave, wave + kGpuKvWaves, ...
+    int i = 0, j = wave;
+    while (nd > 0 && j >= nd) {
+        j -= nd;
+        ++i;
+    }
+    for (int e = wave; e < emax; e += kGpuKvWaves) {
+        if (e < E) {
+            const int g = ps[i * 64 + lane], h = ds[j * 64 + lane];
+            const int szp = gd[g * 64 + lane], szd = gd[h * 64 + lane];
+            int32_t c = 0;
+            if (szp > 0 && szd > 0) {
+                // g's 1/n_g share of a request's KV cache for all L layers
+                c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
+                                 const double V1 = 2.0 * q.s_in * q.Hkv * q.B;
+                                 const double share = (V1 * (double)q.L) / (double)szp;
+                                 return q.alpha[g * q.G + h] + share / q.beta[g * q.G + h];
+                             }));
+            }
+            f.kv_cap[(int64_t)e * N + n] = c;
+            j += kGpuKvWaves;
+            while (j >= nd) {
+                j -= nd;
+                ++i;
+            }
+        }
+    }
 }
 
 template <int W>
@@ -496,16 +583,24 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     prof_mark(kKNodes, true, s);
     const int64_t lanes = (int64_t)f.max_pd * p.N;
     const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
-    const size_t lds = p.granularity == 0 ? 2 * (size_t)p.G * kKvBlock : 0;
+    const size_t lds = 2 * (size_t)p.G * kKvBlock;
     prof_mark(kKKv, false, s);
-    if (p.granularity == 0 && (p.variant & HX_VARIANT_KV_ORDER))
+    if (p.granularity != 0) {
+        const dim3 grid((p.N + 63) / 64), block(64 * kGpuKvWaves);
+        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d);
+        if (p.n_cls > 0)
+            hipLaunchKernelGGL((kv_gpu_kernel<W, true>), grid, block, glds, s, p, o, f);
+        else
+            hipLaunchKernelGGL((kv_gpu_kernel<W, false>), grid, block, glds, s, p, o, f);
+    } else if (p.variant & HX_VARIANT_KV_ORDER) {
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
-    else if (p.granularity == 0 && (p.variant & HX_VARIANT_ASYM))
+    } else if (p.variant & HX_VARIANT_ASYM) {
         hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
-    else if (p.n_cls > 0)
+    } else if (p.n_cls > 0) {
         hipLaunchKernelGGL((kv_kernel<W, false, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
-    else
+    } else {
         hipLaunchKernelGGL((kv_kernel<W, false, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+    }
     prof_mark(kKKv, true, s);
     return hipGetLastError();
 }
