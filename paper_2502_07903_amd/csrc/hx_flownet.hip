@@ -396,27 +396,27 @@ __device__ __forceinline__ double gpu_flops(const Problem& p, int g) {
     return (t >= 0 && t < p.T) ? p.flops[t] : 0.0;
 }
 
-// Slowest FLOP/s among stage j's devices of a member list.
-__device__ double stage_flops(const Problem& p, const uint8_t* m, int stride, int j, int tp) {
-    double c = gpu_flops(p, m[(j * tp) * stride]);
-    for (int r = 1; r < tp; ++r) c = dmin(c, gpu_flops(p, m[(j * tp + r) * stride]));
+// Slowest FLOP/s among stage j's devices of a member list (gfl: every GPU's FLOP/s, in LDS).
+__device__ double stage_flops(const double* gfl, const uint8_t* m, int stride, int j, int tp) {
+    double c = gfl[m[(j * tp) * stride]];
+    for (int r = 1; r < tp; ++r) c = dmin(c, gfl[m[(j * tp + r) * stride]]);
     return c;
 }
 
 // kv_time with each replica's layers following the asymmetric split (HX_VARIANT_ASYM).
-__device__ double kv_time_asym(const Problem& p, const uint8_t* pm, int ptp, int ppp, const uint8_t* dm, int dtp,
-                               int dpp, int stride) {
+__device__ double kv_time_asym(const Problem& p, const double* gfl, const uint8_t* pm, int ptp, int ppp,
+                               const uint8_t* dm, int dtp, int dpp, int stride) {
     const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
     const int deni = ptp * dtp;
     const double den = (double)deni;
     const bool pow2 = (deni & (deni - 1)) == 0;
     const double inv_den = 1.0 / den;
-    const LayerSplit sp = layer_split<true>(p.L, ppp, [&](int j) { return stage_flops(p, pm, stride, j, ptp); });
-    const LayerSplit sd = layer_split<true>(p.L, dpp, [&](int j) { return stage_flops(p, dm, stride, j, dtp); });
+    const LayerSplit sp = layer_split<true>(p.L, ppp, [&](int j) { return stage_flops(gfl, pm, stride, j, ptp); });
+    const LayerSplit sd = layer_split<true>(p.L, dpp, [&](int j) { return stage_flops(gfl, dm, stride, j, dtp); });
     double worst = 0.0;
     int a = 0, bb = 0, a0 = 0, b0 = 0;
-    int a1 = split_layers<true>(sp, 0, stage_flops(p, pm, stride, 0, ptp));
-    int b1 = split_layers<true>(sd, 0, stage_flops(p, dm, stride, 0, dtp));
+    int a1 = split_layers<true>(sp, 0, stage_flops(gfl, pm, stride, 0, ptp));
+    int b1 = split_layers<true>(sd, 0, stage_flops(gfl, dm, stride, 0, dtp));
     while (a < ppp && bb < dpp) {
         const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
         const double Vn = V1 * (double)nab;
@@ -436,11 +436,11 @@ __device__ double kv_time_asym(const Problem& p, const uint8_t* pm, int ptp, int
         const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
         if (adv_a && ++a < ppp) {
             a0 = a1;
-            a1 = a0 + split_layers<true>(sp, a, stage_flops(p, pm, stride, a, ptp));
+            a1 = a0 + split_layers<true>(sp, a, stage_flops(gfl, pm, stride, a, ptp));
         }
         if (adv_b && ++bb < dpp) {
             b0 = b1;
-            b1 = b0 + split_layers<true>(sd, bb, stage_flops(p, dm, stride, bb, dtp));
+            b1 = b0 + split_layers<true>(sd, bb, stage_flops(gfl, dm, stride, bb, dtp));
         }
     }
     return worst;
@@ -463,11 +463,18 @@ __device__ __forceinline__ double task_mix(const Problem& p, TimeOf time_of) {
 
 template <int W, bool kAsym, bool kCls>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
-    extern __shared__ uint8_t sm[];
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int tid = threadIdx.x;
     const int stride = blockDim.x;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
     const int64_t N = p.N;
+    // asymmetric split: every GPU's FLOP/s staged once per workgroup (the walk's layer ranges
+    // read them at every stage it enters)
+    double* gfl = reinterpret_cast<double*>(sm + 2 * (size_t)p.G * stride);
+    if (kAsym) {
+        for (int g = tid; g < p.G; g += blockDim.x) gfl[g] = gpu_flops(p, g);
+        __syncthreads();
+    }
     if (gid >= (int64_t)f.max_pd * N) return;
     const int e = (int)(gid / N);
     const int n = (int)(gid - (int64_t)e * N);
@@ -493,7 +500,7 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
         // treated as infeasible rather than read past the member list.
         if (expand_words<W>(mp, pm, stride) == ptp * ppp && expand_words<W>(md, dm, stride) == dtp * dpp)
             c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                   : kAsym ? kv_time_asym(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                   : kAsym ? kv_time_asym(p, gfl, pm, ptp, ppp, dm, dtp, dpp, stride)
                                            : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
     }
     f.kv_cap[(int64_t)e * N + n] = c;
@@ -595,7 +602,8 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
-        hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds + sizeof(double) * p.G, s,
+                           p, o, f);
     } else if (p.n_cls > 0) {
         hipLaunchKernelGGL((kv_kernel<W, false, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
     } else {
