@@ -129,6 +129,34 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
     return dict(cost=cost, flownet=flownet, maxflow=maxflow, best=best)
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (first processor in /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def measured_copy_gbs(torch, mib: int = 1024, reps: int = 10) -> float:
+    """Device-to-device copy bandwidth (bytes read + written per second) of a mib MiB buffer,
+    the measured counterpart of the HBM datasheet peak."""
+    src = torch.ones(mib * (1 << 18), dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t) / reps
+    del src, dst
+    return 2.0 * mib * (1 << 20) / dt / 1e9
+
+
 def kernel_traffic(kernel: str, workload: int, prob=None):
     """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply (the
     counters were taken on workload 3 with the cost model as written)."""
@@ -525,6 +553,20 @@ def main():
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     value = prob.n_cand / (ms_per_step / 1000.0)
 
+    # The same steps with the host-to-device copy of the candidate arrays (assign, role) from
+    # pinned host memory in each step: the rate a caller holding its candidates on the host sees.
+    h_assign = torch.from_numpy(prob.assign).pin_memory()
+    h_role = torch.from_numpy(prob.role).pin_memory()
+    d_assign, d_role = dp.tensors["assign"], dp.tensors["role"]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        d_assign.copy_(h_assign, non_blocking=True)
+        d_role.copy_(h_role, non_blocking=True)
+        hx.score(dp, ws)
+    torch.cuda.synchronize()
+    ms_h2d = (time.perf_counter() - t0) * 1000.0 / args.steps
+
     # Per-call durations: the same steps again with HIP events recorded between the calls on
     # the stream the kernels run on (kept out of the timed region).
     names = ("cost", "flownet", "maxflow", "best")
@@ -554,6 +596,12 @@ def main():
     hx.profile(False)
     kernel_us = {k: 1000.0 * ms / n for k, (ms, n) in prof.items() if n > 0}
 
+    # How the max-flow solved the batch (diagnostic counters, one extra untimed call).
+    mf = hx.maxflow_stats(ws.net, torch.empty_like(ws.flow_value))
+    pr = mf["push_relabel"]
+    mf["pushes_per_push_relabel_candidate"] = mf["pushes"] / pr if pr else 0.0
+    mf["relabels_per_push_relabel_candidate"] = mf["relabels"] / pr if pr else 0.0
+
     # Roofline of the kernel with the largest share of the step.
     n_p = ws.net.n_p.cpu().numpy()
     n_d = ws.net.n_d.cpu().numpy()
@@ -562,6 +610,7 @@ def main():
     dominant = max(kernel_us, key=kernel_us.get)
     hbm = hbm_bytes_per_step(prob, dims, n_p, n_d)
     roof = roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, args.workload)
+    roof["measured_hbm_copy_gbs"] = measured_copy_gbs(torch)
 
     out = {
         "metric": METRIC,
@@ -579,8 +628,12 @@ def main():
         "config": {"workload": f"workload{wl.cfg}: {wl.name}", "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
                    "cost_model": args.variant, "request_classes": args.classes},
+        "with_h2d_copy": {"value": prob.n_cand / (ms_h2d / 1000.0), "unit": "candidates/s",
+                          "ms_per_step": ms_h2d,
+                          "note": "assign and role copied from pinned host memory in every step"},
         "kernel_ms": per_kernel,
         "kernel_us": kernel_us,
+        "maxflow_paths": mf,
         "hbm_bytes_per_step": hbm,
         "best": best,
         "roofline": roof,
@@ -601,7 +654,7 @@ def main():
         med = float(np.median(times))
         out["cpu_baseline"] = {"value": prob.n_cand / med, "unit": "candidates/s", "cores": cores, "kind": "oracle",
                                "sample": f"the full {prob.n_cand}-candidate batch, {len(times)} runs, median",
-                               "agrees": list(r["best"]) == best}
+                               "agrees": list(r["best"]) == best, "cpu": cpu_model()}
     print(json.dumps(out))
 
 

@@ -244,6 +244,33 @@ int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, 
 int hx_maxflow_batch(const hx_flownet *net, int32_t *flow_value, int32_t *kv_flow, uint8_t *cut,
                      hipStream_t stream);
 
+/* Diagnostic (no counterpart in the paper): hx_maxflow_batch with the same arguments and
+ * results, which also counts how each candidate was solved and the push-relabel work.
+ * stats: device, 8-byte aligned, HX_MF_STATS uint64 words, cleared by the call then filled:
+ *   [HX_MF_NO_FLOW .. HX_MF_PUSH_RELABEL]  candidates by path: no source- or sink-side node can
+ *       carry flow; star closed form; dominant-KV closed form; direct minimum cut; push-relabel;
+ *   [HX_MF_PREPASS]  value-only calls on the per-workgroup plans: candidates the lane-per-
+ *       candidate pre-pass settled (they skip the kernel above);
+ *   [HX_MF_PUSHES], [HX_MF_RELABELS]  pushes (KV, sink and return-to-source) and node relabels
+ *       summed over all candidates;
+ *   [HX_MF_GLOBAL_RELABELS], [HX_MF_ROUNDS]  global-relabel passes and synchronous rounds,
+ *       counted once per workgroup (a packed plan's workgroup holds 64/SEG candidates).
+ * Networks rejected with HX_EINVAL in flow_value are not counted.  Slower than
+ * hx_maxflow_batch (global atomics); not for the search loop. */
+#define HX_MF_NO_FLOW 0
+#define HX_MF_STAR 1
+#define HX_MF_DOMINANT 2
+#define HX_MF_MIN_CUT 3
+#define HX_MF_PUSH_RELABEL 4
+#define HX_MF_PREPASS 5
+#define HX_MF_PUSHES 6
+#define HX_MF_RELABELS 7
+#define HX_MF_GLOBAL_RELABELS 8
+#define HX_MF_ROUNDS 9
+#define HX_MF_STATS 10
+int hx_maxflow_stats(const hx_flownet *net, int32_t *flow_value, int32_t *kv_flow, uint8_t *cut, uint64_t *stats,
+                     hipStream_t stream);
+
 /* The candidate with the highest flow_value (Sec. 3.1 objective), lowest index on ties.
  * best = device int32[2]: {index, value}.  n_cand >= 1. */
 int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, hipStream_t stream);

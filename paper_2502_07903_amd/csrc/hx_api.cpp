@@ -318,7 +318,18 @@ int hx_maxflow_batch(const hx_flownet* net, int32_t* flow_value, int32_t* kv_flo
     if (rc) return rc;
     if (!flow_value) return HX_EINVAL;
     if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
-    hipError_t e = hx::launch_maxflow(make_net(net), flow_value, kv_flow, cut, round_budget(), stream);
+    hipError_t e = hx::launch_maxflow(make_net(net), flow_value, kv_flow, cut, round_budget(), nullptr, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+int hx_maxflow_stats(const hx_flownet* net, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, uint64_t* stats,
+                     hipStream_t stream) {
+    int rc = check_net_shape(net);
+    if (rc) return rc;
+    if (!flow_value || !stats || ((uintptr_t)stats & 7)) return HX_EINVAL;
+    if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
+    hipError_t e = hx::launch_maxflow(make_net(net), flow_value, kv_flow, cut, round_budget(),
+                                      reinterpret_cast<unsigned long long*>(stats), stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

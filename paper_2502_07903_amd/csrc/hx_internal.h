@@ -99,8 +99,8 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
 hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s);
 // LDS bytes the max-flow kernel needs for a network plan; 0 if it does not fit.
 size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
-hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
-                          int32_t op_budget, hipStream_t s);
+hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
+                          unsigned long long* stats, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
 
 // Refinement (Sec. 3.4): edge classes of networks of at most kClsMaxV vertices, guided moves,

@@ -235,9 +235,13 @@ __global__ void __launch_bounds__(64) dom_kernel(FlowNet f, int32_t* flow_value)
 // workgroups to the 8 XCDs in turn, so workgroup w takes tile (w mod 8) * chunk + w / 8 and
 // each XCD walks a contiguous candidate range, sharing the L2 lines of the candidate-fastest
 // input arrays.
-template <int SEG>
+// kStats: the diagnostic instantiation behind hx_maxflow_stats, which also counts into stats
+// (HX_MF_STATS words, see hx.h) which path each candidate took and the push-relabel work; the
+// production instantiation compiles none of it.
+template <int SEG, bool kStats>
 __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 : 1)
-    maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget) {
+    maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
+                   unsigned long long* stats) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const int N = f.N;
@@ -252,7 +256,10 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
     bool valid = tile < tiles && n < N;
     // value-only workgroup plans: bound_kernel has already written the candidates it could
     // (one candidate per workgroup, so the exit is uniform)
-    if (SEG > 64 && kv_flow == nullptr && cut == nullptr && valid && flow_value[n] >= 0) return;
+    if (SEG > 64 && kv_flow == nullptr && cut == nullptr && valid && flow_value[n] >= 0) {
+        if (kStats && l == 0) atomicAdd(&stats[HX_MF_PREPASS], 1ull);
+        return;
+    }
 
     // Packed segments (SEG <= 64) own at most one node row per side and SEG/4 KV rows per
     // lane, so every global load is issued at once, before the counts that say which rows
@@ -318,6 +325,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
     }
     __syncthreads();
     const bool has_flow = P > 0 && D > 0 && L.misc[2] && L.misc[3];
+    int path = has_flow ? HX_MF_PUSH_RELABEL : HX_MF_NO_FLOW;  // kStats: the path this candidate takes
     for (int i = l; i < P; i += SEG) {
         const int32_t a = has_flow ? L.a[i] : 0;
         L.fs[i] = a;  // saturate every source edge
@@ -369,6 +377,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
         }
         const bool dominant = ((__ballot(thin) >> sh) & segmask) == 0;
         if (has_flow && (one_p || one_d)) {
+            path = HX_MF_STAR;
             const int is = __ffsll((unsigned long long)ba) - 1, js = __ffsll((unsigned long long)bb) - 1;
             int32_t v = 0;
             if (one_p) {
@@ -406,6 +415,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
             }
             if (l < P) L.ep[l] = 0;
         } else if (has_flow && dominant) {
+            path = HX_MF_DOMINANT;
             // lane l holds prefill node l and decode node l (packed plans: P, D <= SEG); the
             // sums stay below 64 * 2^24 < 2^31
             const int32_t av = l < P ? L.a[l] : 0, bv = l < D ? L.b[l] : 0;
@@ -477,6 +487,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
                     best = o2 < best ? o2 : best;
                 }
                 cut_value = best;
+                path = HX_MF_MIN_CUT;
                 if (l < P) L.ep[l] = 0;
             }
         }
@@ -491,6 +502,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
             thin |= L.cap[i * Ds + d] < m;
         }
         if (!__syncthreads_or(thin) && has_flow) {
+            path = HX_MF_DOMINANT;
             // block scan: lane l owns a contiguous run of nodes on each side; clamped inclusive
             // prefix sums go to ep (prefill) and ed (decode), then become the flows
             const int cp = (P + SEG - 1) / SEG, cd = (D + SEG - 1) / SEG;
@@ -547,7 +559,13 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
     const int INF = 2 * V + 2;
     bool active = false;
     for (int i = l; i < P; i += SEG) active |= L.ep[i] > 0;
+    unsigned long long pushes = 0, relabels = 0;  // kStats
+    if (kStats && valid && l == 0) atomicAdd(&stats[path], 1ull);
     for (int round = 0; __syncthreads_or(active) && round < round_budget; ++round) {
+        if (kStats && threadIdx.x == 0) {
+            atomicAdd(&stats[HX_MF_ROUNDS], 1ull);
+            if (round % kGlobalRelabelEvery == 0) atomicAdd(&stats[HX_MF_GLOBAL_RELABELS], 1ull);
+        }
         if (round % kGlobalRelabelEvery == 0) {
             global_relabel<SEG>(L, l, P, D, Ds, V, INF);
             __syncthreads();
@@ -571,6 +589,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
                     e -= amt;
                     r -= amt;
                     atomicAdd(&L.ed[d], amt);
+                    if (kStats) ++pushes;
                 }
                 if (r > 0 && hd < mh) mh = hd;
             }
@@ -578,10 +597,12 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
                 const int amt = L.fs[i] < e ? L.fs[i] : e;
                 L.fs[i] -= amt;
                 e -= amt;
+                if (kStats && amt > 0) ++pushes;
             }
             if (e > 0) {
                 if (L.fs[i] > 0 && V < mh) mh = V;
                 L.hp[i] = mh + 1 < INF ? mh + 1 : INF;
+                if (kStats) ++relabels;
             }
             L.ep[i] = e;
         }
@@ -598,6 +619,7 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
                 if (amt > 0) {
                     L.ft[j] += amt;
                     e -= amt;
+                    if (kStats) ++pushes;
                 }
             }
             int mh = INF;
@@ -611,12 +633,14 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
                     L.fl[q * Ds + j] = fq;
                     e -= amt;
                     atomicAdd(&L.ep[q], amt);
+                    if (kStats) ++pushes;
                 }
                 if (fq > 0 && hq < mh) mh = hq;
             }
             if (e > 0) {
                 if (L.b[j] - L.ft[j] > 0) mh = 0;
                 L.hd[j] = mh + 1 < INF ? mh + 1 : INF;
+                if (kStats) ++relabels;
             }
             L.ed[j] = e;
         }
@@ -624,6 +648,10 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
         active = false;
         for (int i = l; i < P; i += SEG) active |= L.ep[i] > 0;
         for (int j = l; j < D; j += SEG) active |= L.ed[j] > 0;
+    }
+    if (kStats) {
+        if (pushes) atomicAdd(&stats[HX_MF_PUSHES], pushes);
+        if (relabels) atomicAdd(&stats[HX_MF_RELABELS], relabels);
     }
     // Flow value = total flow into the sink; a candidate still holding excess ran out of rounds.
     for (int j = l; j < D; j += SEG)
@@ -711,8 +739,13 @@ int segment_lanes(int max_p, int max_d, int max_pd) {
     return s;
 }
 
+__global__ void clear_stats_kernel(unsigned long long* stats) {
+    if (threadIdx.x < HX_MF_STATS) stats[threadIdx.x] = 0;
+}
+
 template <int SEG>
-hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, int32_t budget, hipStream_t s) {
+hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, int32_t budget,
+                      unsigned long long* stats, hipStream_t s) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const size_t lds = kPer * mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
@@ -724,7 +757,14 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
         const int chunks = (f.N + 63) / 64;
         hipLaunchKernelGGL(dom_kernel, dim3(chunks * kDomParts), dim3(64), 0, s, f, fv);
     }
-    hipLaunchKernelGGL(maxflow_kernel<SEG>, dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget);
+    if (stats) {
+        hipLaunchKernelGGL(clear_stats_kernel, dim3(1), dim3(64), 0, s, stats);
+        hipLaunchKernelGGL((maxflow_kernel<SEG, true>), dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget,
+                           stats);
+    } else {
+        hipLaunchKernelGGL((maxflow_kernel<SEG, false>), dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget,
+                           nullptr);
+    }
     prof_mark(kKMaxflow, true, s);
     return hipGetLastError();
 }
@@ -739,14 +779,14 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd) {
 }
 
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
-                          hipStream_t s) {
+                          unsigned long long* stats, hipStream_t s) {
     switch (segment_lanes(f.max_p, f.max_d, f.max_pd)) {
-        case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, s);
-        case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, s);
-        case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, s);
-        case 64: return launch_seg<64>(f, flow_value, kv_flow, cut, round_budget, s);
-        case 128: return launch_seg<128>(f, flow_value, kv_flow, cut, round_budget, s);
-        default: return launch_seg<256>(f, flow_value, kv_flow, cut, round_budget, s);
+        case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        case 64: return launch_seg<64>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        case 128: return launch_seg<128>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        default: return launch_seg<256>(f, flow_value, kv_flow, cut, round_budget, stats, s);
     }
 }
 

@@ -93,7 +93,8 @@ class hx_flownet(C.Structure):
 
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
-           "hx_maxflow_batch", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves", "hx_gather_candidates",
+           "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves",
+           "hx_gather_candidates",
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
            "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error", "hx_abi_version")
 HX_KERNELS = 13
@@ -120,6 +121,7 @@ def lib() -> C.CDLL:
         L.hx_build_flownet.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
                                        P(hx_cost_out), P(hx_flownet), C.c_void_p]
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.hx_maxflow_stats.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_best_candidate.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
         L.hx_edge_classes.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_guided_moves.argtypes = [C.c_int32, C.c_int32, P(hx_candidates), P(hx_flownet), C.c_void_p,
@@ -353,6 +355,21 @@ def maxflow_batch(net: FlowNetBuffers, flow_value, kv_flow=None, cut=None, strea
     _check(lib().hx_maxflow_batch(C.byref(f), _ptr(flow_value), _ptr(kv_flow), _ptr(cut), _stream(stream)),
            "hx_maxflow_batch")
     return flow_value
+
+
+MF_STATS = ("no_flow", "star", "dominant", "min_cut", "push_relabel", "prepass", "pushes", "relabels",
+            "global_relabels", "rounds")
+
+
+def maxflow_stats(net: FlowNetBuffers, flow_value, kv_flow=None, cut=None, stream=None) -> Dict[str, int]:
+    """hx_maxflow_batch plus its diagnostic counters (synchronises the stream to read them)."""
+    torch = _torch()
+    f = net.struct()
+    st = torch.zeros(len(MF_STATS), dtype=torch.int64, device=flow_value.device)
+    _check(lib().hx_maxflow_stats(C.byref(f), _ptr(flow_value), _ptr(kv_flow), _ptr(cut), _ptr(st), _stream(stream)),
+           "hx_maxflow_stats")
+    (torch.cuda.current_stream() if stream is None else stream).synchronize()
+    return dict(zip(MF_STATS, (int(v) for v in st.cpu().tolist())))
 
 
 def best_candidate(flow_value, best, n_cand: Optional[int] = None, stream=None):

@@ -140,6 +140,11 @@ def test_calls_reject_before_any_device_work():
     assert L.hx_best_candidate(FAKE, 0, FAKE, None) == hx.HX_EINVAL
     big = _args(G=255, T=6, N=10, Kmax=32, gran=1)[6]
     assert L.hx_maxflow_batch(C.byref(big), FAKE, None, None, None) == hx.HX_ETOOBIG
+    # the diagnostic variant: same checks, plus an 8-byte aligned counter array
+    assert L.hx_maxflow_stats(C.byref(net), None, None, None, FAKE, None) == hx.HX_EINVAL
+    assert L.hx_maxflow_stats(C.byref(net), FAKE, None, None, None, None) == hx.HX_EINVAL
+    assert L.hx_maxflow_stats(C.byref(net), FAKE, None, None, FAKE + 4, None) == hx.HX_EINVAL
+    assert L.hx_maxflow_stats(C.byref(big), FAKE, None, None, FAKE, None) == hx.HX_ETOOBIG
 
 
 def test_refinement_calls_reject_before_any_device_work():
