@@ -518,8 +518,13 @@ constexpr int kGpuKvWaves = 4;
 // Node rows staged per side: a side has at most G per-GPU nodes.
 __host__ __device__ inline int kv_gpu_rows(int G, int max_rows) { return max_rows < G ? max_rows : G; }
 
-__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d) {
-    return ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
+// The share (V1 L) / n_g of a prefill GPU depends only on its replica's size n_g (1..255), so
+// it is tabulated once per workgroup for every size and task: [tasks][256] doubles.
+constexpr int kShareSizes = 256;
+
+__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d, int n_task) {
+    return sizeof(double) * n_task * kShareSizes +
+           ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
 }
 
 template <int W, bool kCls>
@@ -530,11 +535,19 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
     const int64_t n = (int64_t)blockIdx.x * 64 + lane;
     const bool in = n < N;
     const int G = p.G;
-    uint8_t* gd = sm;                         // [G][64]: replica size, 0 if infeasible or unused
-    uint8_t* ps = sm + (size_t)G * 64;        // [prow][64]: prefill node -> GPU
+    const int n_task = kCls ? p.n_cls : 1;
+    double* share = reinterpret_cast<double*>(sm);               // [task][size]: (V1 L) / size
+    uint8_t* gd = sm + sizeof(double) * n_task * kShareSizes;   // [G][64]: replica size, 0 if
+                                                                 // infeasible or unused
+    uint8_t* ps = gd + (size_t)G * 64;        // [prow][64]: prefill node -> GPU
     const int prow = kv_gpu_rows(G, f.max_p), drow = kv_gpu_rows(G, f.max_d);
     uint8_t* ds = ps + (size_t)prow * 64;     // [drow][64]: decode node -> GPU
     const int np = in ? f.n_p[n] : 0, nd = in ? f.n_d[n] : 0;
+    for (int x = threadIdx.x; x < n_task * kShareSizes; x += 64 * kGpuKvWaves) {
+        const int k = x / kShareSizes, sz = x - k * kShareSizes;
+        const double V1 = 2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B;
+        share[x] = sz > 0 ? (V1 * (double)p.L) / (double)sz : 0.0;
+    }
     for (int g = wave; g < G; g += kGpuKvWaves) {
         uint8_t d = 0;
         if (in) {
@@ -566,12 +579,17 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
             const int szp = gd[g * 64 + lane], szd = gd[h * 64 + lane];
             int32_t c = 0;
             if (szp > 0 && szd > 0) {
-                // g's 1/n_g share of a request's KV cache for all L layers
-                c = quantize(1000.0 / task_mix<kCls>(p, [&](const Problem& q) {
-                                 const double V1 = 2.0 * q.s_in * q.Hkv * q.B;
-                                 const double share = (V1 * (double)q.L) / (double)szp;
-                                 return q.alpha[g * q.G + h] + share / q.beta[g * q.G + h];
-                             }));
+                // g's 1/n_g share of a request's KV cache for all L layers, per task
+                const double al = p.alpha[g * G + h], be = p.beta[g * G + h];
+                double t;
+                if (kCls) {
+                    t = 0.0;
+                    for (int k = 0; k < p.n_cls; ++k)
+                        t = t + p.cls_w[k] * (al + share[k * kShareSizes + szp] / be);
+                } else {
+                    t = al + share[szp] / be;
+                }
+                c = quantize(1000.0 / t);
             }
             f.kv_cap[(int64_t)e * N + n] = c;
             j += kGpuKvWaves;
@@ -594,7 +612,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     prof_mark(kKKv, false, s);
     if (p.granularity != 0) {
         const dim3 grid((p.N + 63) / 64), block(64 * kGpuKvWaves);
-        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d);
+        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d, p.n_cls > 0 ? p.n_cls : 1);
         if (p.n_cls > 0)
             hipLaunchKernelGGL((kv_gpu_kernel<W, true>), grid, block, glds, s, p, o, f);
         else
