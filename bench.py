@@ -193,12 +193,17 @@ def group_members(prob):
 
 
 def eval_fp64_ops(prob) -> float:
+    return eval_fp64_counts(prob)[0]
+
+
+def eval_fp64_counts(prob):
     """Algorithmic FP64 operations of the strategy-evaluation kernel (Table 1 rows as written,
     each add, multiply, divide, min or max one operation; prefill link terms, which do not
     depend on the candidate, count one add each).  Every admissible strategy costs its memory
     row; a strategy whose memory row admits a batch of 1 costs the full latency sum.  With
     request classes a strategy is costed class by class until a class does not fit, and each
-    costed class adds 4 operations to the mix."""
+    costed class adds 4 operations to the mix.  Returns (operations, divisions among them): a
+    binary64 division is about ten VALU instructions on gfx9, so it is reported apart."""
     m = prob.model
     L = m["n_layers"]
     H = float(m["hidden"])
@@ -212,6 +217,7 @@ def eval_fp64_ops(prob) -> float:
     gmem = np.asarray(cl.type_mem, np.float64)[np.asarray(cl.gpu_type)]
     tps = [t for t in range(1, 9) if (prob.tp_mask >> (t - 1)) & 1]
     total = 0.0
+    divs = 0.0
     for sz, (mem, role) in group_members(prob).items():
         dec = role == 1
         for tp in tps:
@@ -233,14 +239,20 @@ def eval_fp64_ops(prob) -> float:
                     bmin = np.minimum(bmin, np.floor((mm - A) / Kj))
                 feas = alive & (bmin >= 1.0)
                 total += int(alive.sum()) * pp * (tp + 8)
+                divs += int(alive.sum()) * (2 + pp)  # W12 / t, K_kv / t, one per stage
                 nf_d = int((feas & dec).sum())
                 nf_p = int((feas & ~dec).sum())
                 common = 4 + 4 + pp * (2 + (tp - 1) + 2) + 3
                 pre = common + pp * (3 + tp * (tp - 1) + 2) + (pp - 1) * (tp * tp + 1)
                 dcd = common + pp * ((tp - 1) + 7 + 4 * tp * (tp - 1) + 3) + (pp - 1) * (3 * tp * tp + 2)
                 total += nf_p * (pre + mix_ops) + nf_d * (dcd + mix_ops)
+                # prefill: computation per stage and x (link terms from tables); decode: two
+                # computation terms per stage, X / (t beta) per ordered TP pair, X / beta per PP
+                # pair, and x; a class mix adds w / x
+                mix_div = 1 if mix_ops else 0
+                divs += nf_p * (pp + 1 + mix_div) + nf_d * (2 * pp + tp * (tp - 1) * pp + tp * tp * (pp - 1) + 1 + mix_div)
                 alive = feas
-    return float(total)
+    return float(total), float(divs)
 
 
 def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
@@ -248,11 +260,15 @@ def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
     max-flow, HBM for the streaming kernels."""
     t_dom = kernel_us[dominant] * 1e-6
     if dominant == "eval":
-        ops = eval_fp64_ops(prob)
+        ops, divs = eval_fp64_counts(prob)
         achieved = ops / t_dom / 1e9
+        # the same work weighted by issue cost: a division as ten operations
+        weighted = (ops + 9.0 * divs) / t_dom / 1e9
         roof = {"kernel": "eval (hx_cost_eval)", "bound": "alu", "achieved": achieved, "peak": FP64_VALU_PEAK_GOPS,
-                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS, "traffic": kernel_traffic("eval", workload, prob),
-                "algorithmic_flops_per_launch": ops}
+                "unit": "GFLOP/s", "frac": achieved / FP64_VALU_PEAK_GOPS,
+                "traffic": kernel_traffic("eval", workload, prob), "algorithmic_flops_per_launch": ops,
+                "fp64_divisions_per_launch": divs, "division_weighted_gops": weighted,
+                "division_weighted_frac": weighted / FP64_VALU_PEAK_GOPS}
     elif dominant == "maxflow":
         alg = float(lds_floor_bytes(n_p, n_d).sum())
         achieved = alg / t_dom / 1e9
