@@ -383,6 +383,14 @@ int hx_profile(int32_t enable);
 int hx_profile_read(double *ms, int32_t *launches, int32_t n);
 const char *hx_kernel_name(int32_t k);
 
+/* Measurement probe (not part of the scoring path): enqueues on `stream` a kernel of `blocks`
+ * workgroups (1..2^20) that fill 16 KB of LDS each and read it back, conflict-free, for `reps`
+ * rounds (1..2^20), and stores in *bytes the LDS bytes the launch reads; timing the launch gives
+ * the LDS read bandwidth the device sustains.  sink: device uint32[blocks * 256], caller-owned;
+ * the kernel writes nothing there (it exists so that the loads are kept).  HX_EINVAL on bad
+ * arguments, HX_EHIP on a launch error. */
+int hx_lds_probe(int32_t blocks, int32_t reps, uint32_t *sink, int64_t *bytes, hipStream_t stream);
+
 /* Human-readable text of a return code, and the last HIP error message kept by HX_EHIP. */
 const char *hx_strerror(int code);
 const char *hx_last_error(void);

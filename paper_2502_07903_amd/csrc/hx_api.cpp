@@ -339,6 +339,13 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 
+int hx_lds_probe(int32_t blocks, int32_t reps, uint32_t* sink, int64_t* bytes, hipStream_t stream) {
+    if (!sink || !bytes || blocks < 1 || blocks > (1 << 20) || reps < 1 || reps > (1 << 20)) return HX_EINVAL;
+    *bytes = hx::lds_probe_bytes(blocks, reps);
+    hipError_t e = hx::launch_lds_probe(blocks, reps, sink, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
 int hx_edge_classes(const hx_flownet* net, const int32_t* flow_value, const int32_t* kv_flow, uint8_t* node_cls,
                     uint8_t* kv_cls, hipStream_t stream) {
     int rc = check_net_shape(net);

@@ -102,6 +102,9 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           unsigned long long* stats, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
+// The LDS bandwidth probe: bytes a launch of `blocks` workgroups and `reps` rounds reads.
+hipError_t launch_lds_probe(int32_t blocks, int32_t reps, uint32_t* sink, hipStream_t s);
+int64_t lds_probe_bytes(int32_t blocks, int32_t reps);
 
 // Refinement (Sec. 3.4): edge classes of networks of at most kClsMaxV vertices, guided moves,
 // and the column gather.
