@@ -327,9 +327,11 @@ constexpr int kGpuChunk = 32;
 // bitmask of each group slot, built in the lane's LDS column from its assign column; absent
 // slots' zero outputs; a per-workgroup histogram of units per bucket, added to the global one
 // with one atomic per bucket.  Loads go in chunks (kGpuChunk assign rows, C role rows) that
-// issue together, so a lane waits on memory once per chunk.
+// issue together, so a lane waits on memory once per chunk.  The LDS columns hold Kc group
+// slots at a time; when Kmax exceeds Kc (very many slots of wide masks) the slots are built Kc
+// at a time, the assign column read once per block of slots.
 template <int W, int C>
-__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk) {
+__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk, int Kc) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int nb = 2 * (p.G + 1);
     int32_t* lhist = reinterpret_cast<int32_t*>(smem);
@@ -339,8 +341,11 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     const int n = blockIdx.x * bs + tid;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
-    if (n < N) {
-        for (int e = 0; e < Kmax * W; ++e) ms[e * bs + tid] = 0;
+    __syncthreads();  // lhist cleared
+    for (int kc = 0; kc < Kmax && n < N; kc += Kc) {
+        // slots [kc, ke) in the lane's column, slot k at row k - kc
+        const int ke = kc + Kc < Kmax ? kc + Kc : Kmax;
+        for (int e = 0; e < (ke - kc) * W; ++e) ms[e * bs + tid] = 0;
         for (int g0 = 0; g0 < p.G; g0 += kGpuChunk) {
             int a[kGpuChunk];
 #pragma unroll
@@ -348,25 +353,22 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
 #pragma unroll
             for (int x = 0; x < kGpuChunk; ++x) {
                 const int g = g0 + x, k = a[x];
-                if (k < Kmax) ms[(k * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
+                if (k >= kc && k < ke) ms[((k - kc) * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
             }
         }
-    }
-    __syncthreads();
-    if (n < N) {
-        for (int k0 = 0; k0 < Kmax; k0 += C) {
+        for (int k0 = kc; k0 < ke; k0 += C) {
             int rl[C];
 #pragma unroll
             for (int x = 0; x < C; ++x)
-                rl[x] = k0 + x < Kmax ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
+                rl[x] = k0 + x < ke ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
 #pragma unroll
             for (int x = 0; x < C; ++x) {
                 const int k = k0 + x;
-                if (k >= Kmax) break;
+                if (k >= ke) break;
                 int size = 0;
 #pragma unroll
                 for (int i = 0; i < W; ++i) {
-                    const uint64_t m = ms[(k * W + i) * bs + tid];
+                    const uint64_t m = ms[((k - kc) * W + i) * bs + tid];
                     wk.gmask[((int64_t)k * W + i) * N + n] = m;
                     size += __popcll(m);
                 }
@@ -849,15 +851,18 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
         hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1);
         prof_mark(kKSetup, true, s);
     }
-    // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS
+    // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS; beyond 64 lanes,
+    // slots are built in blocks of Kc that fit 48 KB
     int bs = 256;
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
-    const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)p.Kmax * W * bs * 8;
+    const size_t slot_bytes = (size_t)W * bs * 8;
+    const int Kc = (size_t)p.Kmax * slot_bytes <= 48 * 1024 ? p.Kmax : (int)(48 * 1024 / slot_bytes);
+    const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)Kc * slot_bytes;
     const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
     switch (slot_chunk(W, p.Kmax)) {
         case 8:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk);
@@ -865,7 +870,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
             break;
         case 16:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk);
@@ -873,7 +878,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
             break;
         default:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk);
+            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk);

@@ -122,6 +122,49 @@ def test_ragged_batches(torch, cfg, n):
     full_parity(torch, I.make_problem(cfg, n_cand=n), f"workload {cfg} ragged")
 
 
+def max_cluster_problem(max_groups: int, n_cand: int, k_hi: int):
+    """255 GPUs (the ABI's maximum: four mask words per group), 4 per node (the last node
+    holds 3), the five node types of the 64-GPU workload in turn, seeded inter-node links of
+    3-25 GB/s, Llama-2-70B shape and the 64-GPU workload's lengths and strategy space."""
+    G = 255
+    wl = dataclasses.replace(I.WORKLOADS[4], n_gpus=G, n_cand=n_cand, k_range=(2, k_hi), max_groups=max_groups)
+    node = np.arange(G) // I.GPUS_PER_NODE
+    n_nodes = int(node[-1]) + 1
+    gpu_type = (node % 5).astype(np.int32)
+    table = np.array([I.GPU_TYPES[c] for c in "ABCDE"], np.float64)
+    rng = np.random.default_rng([2502, 7903, 255])
+    inter = rng.uniform(3.0, 25.0, (n_nodes, n_nodes)) * 1e9
+    inter = np.triu(inter, 1) + np.triu(inter, 1).T
+    cl = I.cluster_from_nodes(gpu_type, table, inter)
+    a, r = I.random_candidates(wl)
+    s_in, s_out = I.mean_lengths(wl)
+    return I.Problem(cl, dict(wl.model), s_in, s_out, wl.tp_mask, wl.pp_mask, 0, max_groups, a, r)
+
+
+def test_maximum_cluster(torch):
+    """255 GPUs and up to 64 groups per candidate: the whole path against the oracle."""
+    full_parity(torch, max_cluster_problem(64, 96, 64), "255 GPUs")
+
+
+def test_maximum_group_slots(torch):
+    """255 GPUs and 255 group slots (both the ABI's maxima): cost model and network against the
+    oracle; the max-flow refuses networks beyond its LDS plan with HX_ETOOBIG."""
+    prob = max_cluster_problem(255, 24, 255)
+    say(f"255 GPUs, 255 slots: N={prob.n_cand}")
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    hx.cost_eval(dp, ws.cost)
+    hx.build_flownet(dp, ws.cost, ws.net)
+    torch.cuda.synchronize()
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    compare_cost({k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")}, want["cost"])
+    assert np.array_equal(ws.cost.members.cpu().numpy().view(np.uint64), expected_members(prob))
+    Hh.compare_flownet(ws.net.host(), want["flownet"])
+    with pytest.raises(hx.HxError) as err:
+        hx.maxflow_batch(ws.net, ws.flow_value)
+    assert err.value.code == hx.HX_ETOOBIG
+
+
 @pytest.mark.parametrize("cfg,frac", [(2, 1.0), (3, 0.5), (3, 0.02)])
 def test_asymmetric_links(torch, cfg, frac):
     """Links whose two directions differ (beta_gh != beta_hg, alpha too) on a seeded fraction of
