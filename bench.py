@@ -40,7 +40,8 @@ METRIC = "candidate placements scored/sec (cost model + max-flow) at 1 GPU; % HB
 # MI355X (gfx950) peaks: 256 CUs at 2.4 GHz.
 HBM_PEAK_GBS = 8000.0
 # LDS reads: 256 B/clk/CU on gfx950 (twice CDNA3's 128) -> 157,286 GB/s; libhx's probe kernel
-# sustains 158 TB/s (measured_lds_gbs in the bench line), which confirms the wider read path.
+# sustains about 128 TB/s (measured_lds_gbs in the bench line), more than 128 B/clk/CU could
+# give (78.6 TB/s), which confirms the wider read path.
 LDS_PEAK_GBS = 256 * 256 * 2.4
 # FP64 vector operations that are not fused multiply-adds: 256 CUs x 4 SIMDs x 16 lanes x
 # 2.4 GHz = 39,322 G op/s (the 78.6 TFLOP/s headline counts an FMA as two).
@@ -160,7 +161,7 @@ def measured_copy_gbs(torch, mib: int = 1024, reps: int = 10) -> float:
 
 
 
-def measured_lds_gbs(torch, hx, blocks: int = 4096, reps: int = 2048) -> float:
+def measured_lds_gbs(torch, hx, blocks: int = 8192, reps: int = 1024) -> float:
     """LDS read bandwidth of libhx's probe kernel (conflict-free 16-byte reads, eight in flight),
     the measured counterpart of the LDS datasheet peak."""
     sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")

@@ -3,8 +3,8 @@
 // (the max-flow residual graphs, the refinement closure).
 //
 // Each workgroup fills 16 KB of LDS, then every lane reads 16 bytes per load, the 64 lanes of a
-// wavefront on consecutive 16-byte words (no bank conflicts), eight loads in flight, for `reps`
-// rounds.  The XOR of everything read is stored only if it equals a value the data cannot give,
+// wavefront on consecutive 16-byte words (no bank conflicts), eight loads in flight at eight
+// distinct addresses (so that none can be merged with another), for `reps` rounds.  The XOR of everything read is stored only if it equals a value the data cannot give,
 // so the loads stay and nothing is written.
 #include "hx_internal.h"
 
@@ -25,7 +25,7 @@ __global__ void __launch_bounds__(kProbeBlock) lds_probe_kernel(int32_t reps, ui
     for (int r = 0; r < reps; ++r) {
         uint4 v[kProbeUnroll];
 #pragma unroll
-        for (int u = 0; u < kProbeUnroll; ++u) v[u] = buf[(idx + u * kProbeBlock) & (kProbeWords - 1)];
+        for (int u = 0; u < kProbeUnroll; ++u) v[u] = buf[(idx + u * (kProbeWords / kProbeUnroll)) & (kProbeWords - 1)];
 #pragma unroll
         for (int u = 0; u < kProbeUnroll; ++u) {
             acc.x ^= v[u].x;
