@@ -103,6 +103,9 @@ def parse():
     ap.add_argument("--spectral-iters", type=int, default=1000, help="power iterations (--partition)")
     ap.add_argument("--quality-rounds", type=int, default=8,
                     help="--refine: also run this many guided and random-perturbation rounds and report the best")
+    ap.add_argument("--candidates", type=int, default=0,
+                    help="score batches of this many candidates of the workload instead of its own count "
+                         "(a scaling study; the headline uses the workload's count)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -560,7 +563,7 @@ def main():
         partition_main(args, torch, hx, I)
         return
     wl = I.WORKLOADS[args.workload]
-    prob = I.make_problem(args.workload)
+    prob = I.make_problem(args.workload, n_cand=args.candidates or None)
     if VARIANTS[args.variant]:
         prob = dataclasses.replace(prob, variant=VARIANTS[args.variant])
     if args.classes:
@@ -656,7 +659,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f64+i32",
         "data": "synthetic",
-        "config": {"workload": f"workload{wl.cfg}: {wl.name}", "candidates": prob.n_cand,
+        "config": {"workload": f"workload{wl.cfg}: {wl.name}" +
+                               (f", scored in batches of {prob.n_cand:,}" if args.candidates else ""),
+                   "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
                    "cost_model": args.variant, "request_classes": args.classes},
         "with_h2d_copy": {"value": prob.n_cand / (ms_h2d / 1000.0), "unit": "candidates/s",
