@@ -122,7 +122,7 @@ def test_ragged_batches(torch, cfg, n):
     full_parity(torch, I.make_problem(cfg, n_cand=n), f"workload {cfg} ragged")
 
 
-def max_cluster_problem(max_groups: int, n_cand: int, k_hi: int):
+def max_cluster_problem(max_groups: int, n_cand: int, k_hi: int, granularity: int = 0):
     """255 GPUs (the ABI's maximum: four mask words per group), 4 per node (the last node
     holds 3), the five node types of the 64-GPU workload in turn, seeded inter-node links of
     3-25 GB/s, Llama-2-70B shape and the 64-GPU workload's lengths and strategy space."""
@@ -138,7 +138,7 @@ def max_cluster_problem(max_groups: int, n_cand: int, k_hi: int):
     cl = I.cluster_from_nodes(gpu_type, table, inter)
     a, r = I.random_candidates(wl)
     s_in, s_out = I.mean_lengths(wl)
-    return I.Problem(cl, dict(wl.model), s_in, s_out, wl.tp_mask, wl.pp_mask, 0, max_groups, a, r)
+    return I.Problem(cl, dict(wl.model), s_in, s_out, wl.tp_mask, wl.pp_mask, granularity, max_groups, a, r)
 
 
 def test_maximum_cluster(torch):
@@ -159,6 +159,24 @@ def test_maximum_group_slots(torch):
     want = hxo.score_batch(prob, n_threads=N_THREADS)
     compare_cost({k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")}, want["cost"])
     assert np.array_equal(ws.cost.members.cpu().numpy().view(np.uint64), expected_members(prob))
+    Hh.compare_flownet(ws.net.host(), want["flownet"])
+    with pytest.raises(hx.HxError) as err:
+        hx.maxflow_batch(ws.net, ws.flow_value)
+    assert err.value.code == hx.HX_ETOOBIG
+
+
+def test_maximum_cluster_per_gpu_nodes(torch):
+    """255 GPUs with a flow node per GPU: cost model and network (up to 255 nodes a side and
+    their per-GPU KV edges) against the oracle; the max-flow refuses such networks (HX_ETOOBIG)."""
+    prob = max_cluster_problem(32, 16, 32, granularity=1)
+    say(f"255 GPUs, per-GPU nodes: N={prob.n_cand}")
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    hx.cost_eval(dp, ws.cost)
+    hx.build_flownet(dp, ws.cost, ws.net)
+    torch.cuda.synchronize()
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    compare_cost({k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat")}, want["cost"])
     Hh.compare_flownet(ws.net.host(), want["flownet"])
     with pytest.raises(hx.HxError) as err:
         hx.maxflow_batch(ws.net, ws.flow_value)
