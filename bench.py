@@ -217,11 +217,14 @@ def eval_fp64_ops(prob) -> float:
 def eval_fp64_counts(prob):
     """Algorithmic FP64 operations of the strategy-evaluation kernel (Table 1 rows as written,
     each add, multiply, divide, min or max one operation; prefill link terms, which do not
-    depend on the candidate, count one add each).  Every admissible strategy costs its memory
-    row; a strategy whose memory row admits a batch of 1 costs the full latency sum.  With
-    request classes a strategy is costed class by class until a class does not fit, and each
-    costed class adds 4 operations to the mix.  Returns (operations, divisions among them): a
-    binary64 division is about ten VALU instructions on gfx9, so it is reported apart."""
+    depend on the candidate, count one add each).  The kernel costs the groups that the decode
+    pass's memory-row screen leaves (a group holding a GPU that fails the memory row of every
+    strategy of its size is settled there, its outputs all zero; no screen with the asymmetric
+    split).  For a costed group every admissible strategy costs its memory row, and a strategy
+    whose memory row admits a batch of 1 costs the full latency sum.  With request classes a
+    strategy is costed class by class until a class does not fit, and each costed class adds 4
+    operations to the mix.  Returns (operations, divisions among them): a binary64 division is
+    about ten VALU instructions on gfx9, so it is reported apart."""
     m = prob.model
     L = m["n_layers"]
     H = float(m["hidden"])
@@ -231,20 +234,32 @@ def eval_fp64_counts(prob):
     classes = getattr(prob, "classes", None)
     tasks = [(prob.s_in, prob.s_out)] if classes is None else [(float(i), float(o)) for i, o, _ in classes]
     mix_ops = 0 if classes is None else 4
+    screened_variant = not (getattr(prob, "variant", 0) & 4)
     cl = prob.cluster
-    gmem = np.asarray(cl.type_mem, np.float64)[np.asarray(cl.gpu_type)]
+    gt = np.asarray(cl.gpu_type)
+    ok_t = (gt >= 0) & (gt < len(cl.type_mem))
+    gmem = np.where(ok_t, np.asarray(cl.type_mem, np.float64)[np.clip(gt, 0, len(cl.type_mem) - 1)], 0.0)
+    wild = np.isnan(gmem)
     tps = [t for t in range(1, 9) if (prob.tp_mask >> (t - 1)) & 1]
-    total = 0.0
-    divs = 0.0
+    total = divs = 0.0
     for sz, (mem, role) in group_members(prob).items():
         dec = role == 1
-        for tp in tps:
-            if sz % tp:
-                continue
-            pp = sz // tp
-            if pp > 8 or not (prob.pp_mask >> (pp - 1)) & 1 or pp > L:
-                continue
-            alive = np.ones(len(mem), bool)
+        strats = [(tp, sz // tp) for tp in tps if sz % tp == 0 and sz // tp <= 8
+                  and (prob.pp_mask >> (sz // tp - 1)) & 1 and sz // tp <= L]
+        # the screen: GPUs failing every strategy's memory row at floor(L/pp) layers
+        fail_all = np.ones(len(gmem), bool)
+        for tp, pp in strats:
+            l = L // pp
+            fails = np.zeros(len(gmem), bool)
+            for s_in, s_out in tasks:
+                K = (2.0 * (s_in + s_out) * Hkv * B / tp) * l + 4.0 * (s_in + s_out) * H * B
+                fails |= np.floor((gmem - (W12 / tp) * l) / K) < 1.0
+            fail_all &= fails
+        costed = np.ones(len(mem), bool)
+        if screened_variant:
+            costed = ~(fail_all[mem].any(axis=1) & ~wild[mem].any(axis=1))
+        for tp, pp in strats:
+            alive = costed.copy()
             for s_in, s_out in tasks:
                 Kkv = 2.0 * (s_in + s_out) * Hkv * B
                 Kact = 4.0 * (s_in + s_out) * H * B

@@ -257,6 +257,24 @@ __device__ __forceinline__ bool cost_mix(const Problem& p, const Tables& tb, con
     return true;
 }
 
+// Admissible strategies of a group of c GPUs, bit tp-1 for each tp of the mask dividing c with
+// pp = c/tp in the PP mask and at most L (the strategy list of Sec. 3.2 for that size).
+__device__ __forceinline__ uint8_t admissible(const Problem& p, int c) {
+    uint8_t a = 0;
+    for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
+        if (!((p.tp_mask >> (tp - 1)) & 1u) || c % tp != 0) continue;
+        const int pp = c / tp;
+        if (pp >= 1 && pp <= HX_MAX_PP && ((p.pp_mask >> (pp - 1)) & 1u) && pp <= p.L) a |= (uint8_t)(1u << (tp - 1));
+    }
+    return a;
+}
+
+// c / tp for an admissible strategy (tp divides c <= 255): multiply by ceil(2^16 / tp).
+__device__ __forceinline__ int stage_count(int c, int tp) {
+    constexpr uint32_t kRecip[HX_MAX_TP + 1] = {0, 65536, 32768, 21846, 16384, 13108, 10923, 9363, 8192};
+    return (int)(((uint32_t)c * kRecip[tp]) >> 16);
+}
+
 // ------------------------------------------------------------------ kernels
 
 struct CostWork {
@@ -264,20 +282,86 @@ struct CostWork {
     int32_t* cursor;  // [nb]: units placed so far per bucket
     uint64_t* units;  // [max units][1 + W]: (n << 16 | k << 8 | role), then the member mask words
     uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
+    uint64_t* unfit;  // [G + 2][W] the memory-row screen: a row per group size, then wild
+    uint8_t* ukey;    // [Kmax][N] role of a group to cost, HX_UNUSED for a group decode settled
     double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables), class 0
     double* pp_pre;   // [G][G] prefill PP terms, class 0; class k's tables sit k table blocks on
                       // ((HX_MAX_TP + 1) G^2 doubles each)
 };
 
-// First kernel of a call: clears the histogram and cursors (n_clear words) and tabulates the
-// prefill link terms.  Prefill runs at batch 1, so its per-link TP and PP terms depend only on
+// The memory-row screen, a W-word GPU bitmask per group size c = 0..G, then wild (entry G + 1).
+// Row c holds the GPUs g that fail the memory row of every admissible strategy of size c on
+// their own memory, in some request class: for strategy (tp, pp) with the stage holding
+// floor(L/pp) layers, clamp(floor((M_g - A)/K)) < 1 with A, K and the clamp as the memory row
+// has them (row c is every GPU when size c has no strategy).  The row is monotone in the stage's
+// smallest memory and only gets stricter with one layer more, so a group of size c holding such
+// a GPU has no feasible strategy.  Wild: GPUs whose memory is NaN, where the stage minimum
+// depends on the member order, so a group holding one is not screened.  One wavefront per word
+// (a ballot over its 64 GPUs); the loop bound is wavefront-uniform.
+__device__ void unfit_table(const Problem& p, uint64_t* unfit, int W, int64_t tid, int64_t nth) {
+    const int lane = (int)(tid & 63);
+    const int nt = p.n_cls > 0 ? p.n_cls : 1;
+    for (int64_t e = tid >> 6; e < (int64_t)(p.G + 2) * W; e += nth >> 6) {
+        const int c = (int)(e / W), g = (int)(e - (int64_t)c * W) * 64 + lane;
+        double M = 0.0;
+        if (g < p.G) {
+            const int t = p.gpu_type[g];
+            M = t >= 0 && t < p.T ? p.mem[t] : 0.0;  // an unknown type holds nothing
+        }
+        bool bit = g < p.G;
+        if (c == p.G + 1) {
+            bit = bit && isnan(M);
+        } else {
+            const double H = p.H, B = p.B;
+            const double W12 = 12.0 * H * H * B;
+            for (uint32_t am = admissible(p, c); am && bit; am &= am - 1) {
+                const int tp = __ffs(am), pp = stage_count(c, tp);
+                const double t = (double)tp, l = (double)(p.L / pp);
+                bool fails = false;
+                for (int k = 0; k < nt; ++k) {
+                    const double s_in = p.n_cls > 0 ? p.cls_in[k] : p.s_in;
+                    const double s_out = p.n_cls > 0 ? p.cls_out[k] : p.s_out;
+                    const double Kkv = 2.0 * (s_in + s_out) * p.Hkv * B;
+                    const double Kact = 4.0 * (s_in + s_out) * H * B;
+                    const double A = (W12 / t) * l;
+                    const double K = (Kkv / t) * l + Kact;
+                    const double q = (M - A) / K;
+                    const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
+                    if (b < 1.0) fails = true;
+                }
+                bit = fails;
+            }
+        }
+        const uint64_t bits = __ballot(bit);
+        if (lane == 0) unfit[e] = bits;
+    }
+}
+
+// True when the screen settles a group of size c (member mask m): no member's memory is NaN
+// and a member fails every admissible strategy's memory row, so the costing would keep no
+// strategy and the group's outputs are all zero.  (Groups it does not settle are costed
+// exactly.)
+template <int W>
+__device__ __forceinline__ bool screened_out(const uint64_t* unfit, int G, const uint64_t (&m)[W], int c) {
+    uint64_t wild = 0, hit = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        wild |= m[i] & unfit[(G + 1) * W + i];
+        hit |= m[i] & unfit[c * W + i];
+    }
+    return hit != 0 && wild == 0;
+}
+
+// First kernel of a call: clears the histogram and cursors (n_clear words), tabulates the
+// memory-row screen and the prefill link terms.  Prefill runs at batch 1, so its per-link TP and PP terms depend only on
 // the cluster and the task: alpha + X/(tp beta) for every TP degree of the mask and
 // alpha + X/beta, X = 1*s_in*H*B, evaluated exactly as the costing expressions do (the same
 // binary64 values).  With request classes there is one table block per class (its s_in).
-__global__ void setup_kernel(Problem p, CostWork wk, int n_clear) {
+__global__ void setup_kernel(Problem p, CostWork wk, int n_clear, int W) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_clear; i += nth) wk.hist[i] = 0;
+    unfit_table(p, wk.unfit, W, tid, nth);
     const int G = p.G;
     const int64_t gg = (int64_t)G * G;
     const int64_t blk = (HX_MAX_TP + 1) * gg;
@@ -335,9 +419,12 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int nb = 2 * (p.G + 1);
     int32_t* lhist = reinterpret_cast<int32_t*>(smem);
-    uint64_t* ms = reinterpret_cast<uint64_t*>(smem + ((sizeof(int32_t) * nb + 15) & ~(size_t)15));
+    uint64_t* unfit = reinterpret_cast<uint64_t*>(smem + ((sizeof(int32_t) * nb + 15) & ~(size_t)15));
+    uint64_t* ms = unfit + (p.G + 2) * W;
     const int tid = threadIdx.x, bs = blockDim.x;
     for (int b = tid; b < nb; b += bs) lhist[b] = 0;
+    for (int e = tid; e < (p.G + 2) * W; e += bs) unfit[e] = wk.unfit[e];
+    const bool screen = (p.variant & HX_VARIANT_ASYM) == 0;  // the screen assumes the uniform split
     const int n = blockIdx.x * bs + tid;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
@@ -365,23 +452,27 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
             for (int x = 0; x < C; ++x) {
                 const int k = k0 + x;
                 if (k >= ke) break;
+                uint64_t m[W];
                 int size = 0;
 #pragma unroll
                 for (int i = 0; i < W; ++i) {
-                    const uint64_t m = ms[((k - kc) * W + i) * bs + tid];
-                    wk.gmask[((int64_t)k * W + i) * N + n] = m;
-                    size += __popcll(m);
+                    m[i] = ms[((k - kc) * W + i) * bs + tid];
+                    wk.gmask[((int64_t)k * W + i) * N + n] = m[i];
+                    size += __popcll(m[i]);
                 }
-                if (size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE)) {
+                const bool costed = size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE) &&
+                                    !(screen && screened_out<W>(unfit, p.G, m, size));
+                const int64_t o_ = (int64_t)k * N + n;
+                if (costed) {
                     atomicAdd(&lhist[bucket_of(p.G, size, rl[x])], 1);
                 } else {
-                    const int64_t o_ = (int64_t)k * N + n;
                     o.tp[o_] = 0;
                     o.pp[o_] = 0;
                     o.bmax[o_] = 0;
                     o.cap[o_] = 0;
                     o.lat[o_] = 0.0;
                 }
+                wk.ukey[o_] = costed ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
             }
         }
     }
@@ -438,7 +529,7 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
 #pragma unroll
     for (int x = 0; x < C; ++x) {
         const bool in = n < N && x < Kmax;
-        rl0[x] = in ? p.role[(int64_t)x * N + n] : HX_UNUSED;
+        rl0[x] = in ? wk.ukey[(int64_t)x * N + n] : HX_UNUSED;
 #pragma unroll
         for (int i = 0; i < W; ++i) m0[x][i] = in ? wk.gmask[((int64_t)x * W + i) * N + n] : 0;
     }
@@ -458,7 +549,7 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
 #pragma unroll
             for (int x = 0; x < C; ++x) {
                 const bool in = k0 + x < Kmax;
-                rl[x] = k0 == 0 ? rl0[x] : (in ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED);
+                rl[x] = k0 == 0 ? rl0[x] : (in ? wk.ukey[(int64_t)(k0 + x) * N + n] : HX_UNUSED);
 #pragma unroll
                 for (int i = 0; i < W; ++i)
                     m[x][i] = k0 == 0 ? m0[x][i] : (in ? wk.gmask[((int64_t)(k0 + x) * W + i) * N + n] : 0);
@@ -480,24 +571,6 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
             }
         }
     }
-}
-
-// Admissible strategies of a group of c GPUs, bit tp-1 for each tp of the mask dividing c with
-// pp = c/tp in the PP mask and at most L (the strategy list of Sec. 3.2 for that size).
-__device__ __forceinline__ uint8_t admissible(const Problem& p, int c) {
-    uint8_t a = 0;
-    for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
-        if (!((p.tp_mask >> (tp - 1)) & 1u) || c % tp != 0) continue;
-        const int pp = c / tp;
-        if (pp >= 1 && pp <= HX_MAX_PP && ((p.pp_mask >> (pp - 1)) & 1u) && pp <= p.L) a |= (uint8_t)(1u << (tp - 1));
-    }
-    return a;
-}
-
-// c / tp for an admissible strategy (tp divides c <= 255): multiply by ceil(2^16 / tp).
-__device__ __forceinline__ int stage_count(int c, int tp) {
-    constexpr uint32_t kRecip[HX_MAX_TP + 1] = {0, 65536, 32768, 21846, 16384, 13108, 10923, 9363, 8192};
-    return (int)(((uint32_t)c * kRecip[tp]) >> 16);
 }
 
 // ------------------------------------------------------------------ large groups
@@ -845,10 +918,12 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     {
         // hist and cursor are contiguous: 2 nb + 1 words to clear
         const int64_t cells = (int64_t)(HX_MAX_TP + 1) * p.G * p.G;
-        const int64_t want = (cells > 2 * nb + 1 ? cells : 2 * nb + 1) + 255;
+        const int64_t screen = (int64_t)(p.G + 2) * W * 64;  // a wavefront per screen word
+        const int64_t most = cells > screen ? cells : screen;
+        const int64_t want = (most > 2 * nb + 1 ? most : 2 * nb + 1) + 255;
         const int blocks = (int)(want / 256 < 1024 ? want / 256 : 1024);
         prof_mark(kKSetup, false, s);
-        hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1);
+        hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1, W);
         prof_mark(kKSetup, true, s);
     }
     // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS; beyond 64 lanes,
@@ -857,7 +932,8 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
     const size_t slot_bytes = (size_t)W * bs * 8;
     const int Kc = (size_t)p.Kmax * slot_bytes <= 48 * 1024 ? p.Kmax : (int)(48 * 1024 / slot_bytes);
-    const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + (size_t)Kc * slot_bytes;
+    const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + sizeof(uint64_t) * (p.G + 2) * W +
+                           (size_t)Kc * slot_bytes;
     const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
     switch (slot_chunk(W, p.Kmax)) {
         case 8:
@@ -921,11 +997,21 @@ static size_t units_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     return (b + 255) & ~(size_t)255;
 }
 
+static size_t tables_bytes(int32_t n_gpus) {
+    return sizeof(double) * HX_MAX_CLASSES * (HX_MAX_TP + 1) * (size_t)n_gpus * n_gpus;
+}
+
+static size_t unfit_bytes(int32_t n_gpus) {
+    return sizeof(uint64_t) * ((size_t)n_gpus + 2) * mask_words(n_gpus);
+}
+
+// Layout: histogram and cursors, unit records, prefill link tables, the memory-row screen, and a
+// key byte per group slot.
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
-    const size_t tables = sizeof(double) * HX_MAX_CLASSES * (HX_MAX_TP + 1) * (size_t)n_gpus * n_gpus;
-    return head + units_bytes(n_gpus, max_groups, n_cand) + tables;
+    return head + units_bytes(n_gpus, max_groups, n_cand) + tables_bytes(n_gpus) + unfit_bytes(n_gpus) +
+           (size_t)max_groups * n_cand;
 }
 
 hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
@@ -938,6 +1024,8 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
     wk.tp_pre = reinterpret_cast<double*>(reinterpret_cast<unsigned char*>(workspace) + head +
                                           units_bytes(p.G, p.Kmax, p.N));
     wk.pp_pre = wk.tp_pre + (size_t)HX_MAX_TP * p.G * p.G;
+    wk.unfit = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(wk.tp_pre) + tables_bytes(p.G));
+    wk.ukey = reinterpret_cast<uint8_t*>(wk.unfit) + unfit_bytes(p.G);
     wk.gmask = o.members;
     switch (mask_words(p.G)) {
         case 1: return launch_w<1>(p, o, wk, s);
