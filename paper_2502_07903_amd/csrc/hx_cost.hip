@@ -580,8 +580,14 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
 // lane-parallel over stages for the memory row and the computation term, over (stage,
 // device) rows for the TP sums and PP minima; one lane then combines the rows in the
 // documented order, so every value is the same binary64 the one-lane path produces.
+// Two settings: (12 GPUs, 16 lanes) where the batch keeps the chip busy, and (6 GPUs, 8 lanes)
+// for batches small enough that the longest lane chains set the kernel's time (N Kmax <=
+// kSmallBatch): more groups then get several lanes, each with a shorter chain.
 constexpr int kCoopMin = 12;
 constexpr int kCoopLanes = 16;
+constexpr int kCoopMinSmall = 6;
+constexpr int kCoopLanesSmall = 8;
+constexpr int64_t kSmallBatch = int64_t(1) << 21;
 
 __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -609,11 +615,11 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
     return c;
 }
 
-// One group of kCoopLanes lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
+// One group of kCL lanes (gl = lane within it) costs unit (n, k, role, mask); `live`
 // is false for groups past the last large unit (they still join every wave-level sync).  With
 // request classes (kVarClasses) each strategy is costed once per class, and the mix kept as
 // cost_mix keeps it.
-template <int kVar>
+template <int kVar, int kCL>
 __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o, const CoopLds& c,
                           const uint8_t* adm_tab, int gl, bool live, int n, int k, int role, uint64_t mask) {
     constexpr bool kPipe = (kVar & HX_VARIANT_PIPELINED) != 0;
@@ -621,7 +627,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
     constexpr bool kCls = (kVar & kVarClasses) != 0;
     const int G = p0.G;
     const int cnt = live ? __popcll(mask) : 0;
-    for (int g = gl; g < G && live; g += kCoopLanes)
+    for (int g = gl; g < G && live; g += kCL)
         if ((mask >> g) & 1ull) c.mem[__popcll(mask & ((1ull << g) - 1))] = (uint8_t)g;
     wave_sync();
     const double H = p0.H, B = p0.B;
@@ -653,7 +659,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
             const double Kact = 4.0 * (p.s_in + p.s_out) * H * B;
             // Memory-limit row, one lane per stage, then the group's minimum (exact).
             double bl = kBmaxClamp;
-            for (int j = gl; j < pp; j += kCoopLanes) {
+            for (int j = gl; j < pp; j += kCL) {
                 const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
                 const double A = (W12 / t) * l;
                 const double K = (Kkv / t) * l + Kact;
@@ -664,7 +670,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
                 const double b = q >= kBmaxClamp ? kBmaxClamp : (q <= -kBmaxClamp ? -kBmaxClamp : floor(q));
                 bl = dmin(bl, b);
             }
-            for (int off = kCoopLanes / 2; off > 0; off >>= 1) bl = dmin(bl, __shfl_xor(bl, off, kCoopLanes));
+            for (int off = kCL / 2; off > 0; off >>= 1) bl = dmin(bl, __shfl_xor(bl, off, kCL));
             const bool feas = ok && bl >= 1.0;
             const double b = prefill ? 1.0 : bl;
             const double Xcomp_p = 24.0 * b * p.s_in * H * H;
@@ -673,7 +679,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
             const double X = prefill ? b * p.s_in * H * B : b * H * B;
             // Rows (stage j, device r): the device's TP sum over its peers (ascending) and its
             // fastest link into stage j+1.
-            for (int it = gl; feas && it < cnt; it += kCoopLanes) {
+            for (int it = gl; feas && it < cnt; it += kCL) {
                 const int j = it / tp, r = it - j * tp;
                 const uint8_t* S = c.mem + j * tp;
                 const int d = S[r];
@@ -697,7 +703,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
                     c.pmin[it] = mn;
                 }
             }
-            for (int j = gl; feas && j < pp; j += kCoopLanes) {
+            for (int j = gl; feas && j < pp; j += kCL) {
                 const uint8_t* S = c.mem + j * tp;
                 double cmin = tb.gfl[S[0]], hmin = tb.ghb[S[0]];
                 for (int r = 1; r < tp; ++r) {
@@ -781,7 +787,7 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
     }
 }
 
-template <int W, bool kTables, int kEvalBlock, int kVar>
+template <int W, bool kTables, int kEvalBlock, int kVar, int kCMin, int kCL>
 __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
     const int G = p.G;
@@ -811,12 +817,12 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     // Admissible strategies by group size, for every size up to G.
     __shared__ uint8_t adm_tab[HX_MAX_GPUS + 1];
     for (int c = threadIdx.x; c <= G; c += kEvalBlock) adm_tab[c] = admissible(p, c);
-    // Units in all: the sum of the bucket counts.  Units before the (size kCoopMin - 1)
+    // Units in all: the sum of the bucket counts.  Units before the (size kCMin - 1)
     // buckets are the large groups (sizes descend).
     __shared__ int32_t counts[2];
     if (threadIdx.x < 64) {
         const int32_t t = wave_sum(wk.hist, nb, threadIdx.x);
-        const int32_t f = W == 1 && G >= kCoopMin ? wave_sum(wk.hist, bucket_of(G, kCoopMin - 1, 0), threadIdx.x) : 0;
+        const int32_t f = W == 1 && G >= kCMin ? wave_sum(wk.hist, bucket_of(G, kCMin - 1, 0), threadIdx.x) : 0;
         if (threadIdx.x == 0) {
             counts[0] = t;
             counts[1] = f;
@@ -827,11 +833,11 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     const int64_t N = p.N;
     uint8_t* mem = reinterpret_cast<uint8_t*>(tb_end) + threadIdx.x;  // [G][kEvalBlock] member list
     const int64_t first_small = counts[1];
-    if (W == 1 && G >= kCoopMin) {
+    if (W == 1 && G >= kCMin) {
         unsigned char* cbase = reinterpret_cast<unsigned char*>(tb_end) + (size_t)G * kEvalBlock;
-        const int lane = threadIdx.x & 63, grp = lane / kCoopLanes, gl = lane % kCoopLanes;
+        const int lane = threadIdx.x & 63, grp = lane / kCL, gl = lane % kCL;
         const int wave = threadIdx.x >> 6;
-        constexpr int kGroupsPerWave = 64 / kCoopLanes;
+        constexpr int kGroupsPerWave = 64 / kCL;
         const CoopLds c = carve_coop(cbase + (wave * kGroupsPerWave + grp) * coop_group_bytes(G), G);
         const int64_t waves = (int64_t)gridDim.x * (kEvalBlock / 64);
         for (int64_t base = ((int64_t)blockIdx.x * (kEvalBlock / 64) + wave) * kGroupsPerWave; base < first_small;
@@ -848,7 +854,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
                 role = (int)(w & 0xFF);
                 mask = rec[1];
             }
-            coop_unit<kVar>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
+            coop_unit<kVar, kCL>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
@@ -896,17 +902,32 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     }
 }
 
+template <int W, int kVar, int kCMin, int kCL>
+void launch_eval_coop(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
+                      size_t lds, hipStream_t s) {
+    if (eb == 256) {
+        if (tables)
+            hipLaunchKernelGGL((eval_kernel<W, true, 256, kVar, kCMin, kCL>), dim3(blocks), dim3(256), lds, s, p, o, wk,
+                               nb);
+        else
+            hipLaunchKernelGGL((eval_kernel<W, false, 256, kVar, kCMin, kCL>), dim3(blocks), dim3(256), lds, s, p, o,
+                               wk, nb);
+    } else {
+        hipLaunchKernelGGL((eval_kernel<W, false, 128, kVar, kCMin, kCL>), dim3(blocks), dim3(128), lds, s, p, o, wk,
+                           nb);
+    }
+}
+
+// Small batches (and only mask width 1 has the cooperative path) take the small-batch setting.
+__host__ inline bool small_batch(const Problem& p) { return (int64_t)p.N * p.Kmax <= kSmallBatch; }
+
 template <int W, int kVar>
 void launch_eval(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
                  size_t lds, hipStream_t s) {
-    if (eb == 256) {
-        if (tables)
-            hipLaunchKernelGGL((eval_kernel<W, true, 256, kVar>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
-        else
-            hipLaunchKernelGGL((eval_kernel<W, false, 256, kVar>), dim3(blocks), dim3(256), lds, s, p, o, wk, nb);
-    } else {
-        hipLaunchKernelGGL((eval_kernel<W, false, 128, kVar>), dim3(blocks), dim3(128), lds, s, p, o, wk, nb);
-    }
+    if (W == 1 && small_batch(p))
+        launch_eval_coop<W, kVar, kCoopMinSmall, kCoopLanesSmall>(p, o, wk, nb, tables, eb, blocks, lds, s);
+    else
+        launch_eval_coop<W, kVar, kCoopMin, kCoopLanes>(p, o, wk, nb, tables, eb, blocks, lds, s);
 }
 
 // Units a candidate can contribute: one per group, at most min(Kmax, G).
@@ -968,7 +989,9 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const int64_t units = max_units(p.G, p.Kmax, p.N);
     const int eb = p.G <= 128 ? 256 : 128;
     const size_t lds_eval = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) +
-                            (size_t)p.G * eb + (W == 1 ? (size_t)(eb / kCoopLanes) * coop_group_bytes(p.G) : 0);
+                            (size_t)p.G * eb +
+                            (W == 1 ? (size_t)(eb / (small_batch(p) ? kCoopLanesSmall : kCoopLanes)) * coop_group_bytes(p.G)
+                                    : 0);
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     prof_mark(kKEval, false, s);
