@@ -918,8 +918,12 @@ void launch_eval_coop(const Problem& p, const CostOut& o, const CostWork& wk, in
     }
 }
 
-// Small batches (and only mask width 1 has the cooperative path) take the small-batch setting.
-__host__ inline bool small_batch(const Problem& p) { return (int64_t)p.N * p.Kmax <= kSmallBatch; }
+// Small batches take the small-batch setting (only mask width 1 has the cooperative path),
+// unless every group is costed (the asymmetric split has no memory-row screen, and more lanes
+// per group then cost more than they save).
+__host__ inline bool small_batch(const Problem& p) {
+    return (int64_t)p.N * p.Kmax <= kSmallBatch && !(p.variant & HX_VARIANT_ASYM);
+}
 
 template <int W, int kVar>
 void launch_eval(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
