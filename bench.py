@@ -53,12 +53,12 @@ FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
-    "setup": {"source_sha256_16": "c2df7e53262b34db", "fetch_kib": 67.5, "write_kib": 32.81},
-    "decode": {"source_sha256_16": "c2df7e53262b34db", "fetch_kib": 1668.13, "write_kib": 27815.06},
-    "scatter": {"source_sha256_16": "c2df7e53262b34db", "fetch_kib": 4935.0, "write_kib": 1486.32},
-    "eval": {"source_sha256_16": "c2df7e53262b34db", "fetch_kib": 1146.8, "write_kib": 12111.59},
-    "nodes": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 6698.15, "write_kib": 17059.62},
-    "kv": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 5891.4, "write_kib": 13399.09},
+    "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 67.5, "write_kib": 32.81},
+    "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1668.06, "write_kib": 27815.06},
+    "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 4935.0, "write_kib": 1488.54},
+    "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1145.86, "write_kib": 12118.61},
+    "nodes": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 6698.15, "write_kib": 17042.95},
+    "kv": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 5891.39, "write_kib": 13399.09},
     "maxflow": {"source_sha256_16": "1b140d4d507b5f54", "fetch_kib": 16732.65, "write_kib": 256.0},
     "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.26, "write_kib": 0.03},
 }
