@@ -39,9 +39,7 @@ METRIC = "candidate placements scored/sec (cost model + max-flow) at 1 GPU; % HB
 
 # MI355X (gfx950) peaks: 256 CUs at 2.4 GHz.
 HBM_PEAK_GBS = 8000.0
-# LDS reads: 256 B/clk/CU on gfx950 (twice CDNA3's 128) -> 157,286 GB/s; libhx's probe kernel
-# sustains about 128 TB/s (measured_lds_gbs in the bench line), more than 128 B/clk/CU could
-# give (78.6 TB/s), which confirms the wider read path.
+# LDS reads: 256 B/clk/CU on gfx950 (twice CDNA3's 128) -> 157,286 GB/s (datasheet figure).
 LDS_PEAK_GBS = 256 * 256 * 2.4
 # FP64 vector operations that are not fused multiply-adds: 256 CUs x 4 SIMDs x 16 lanes x
 # 2.4 GHz = 39,322 G op/s (the 78.6 TFLOP/s headline counts an FMA as two).
@@ -163,17 +161,6 @@ def measured_copy_gbs(torch, mib: int = 1024, reps: int = 10) -> float:
     return 2.0 * mib * (1 << 20) / dt / 1e9
 
 
-
-def measured_lds_gbs(torch, hx, blocks: int = 8192, reps: int = 1024) -> float:
-    """LDS read bandwidth of libhx's probe kernel (conflict-free 16-byte reads, eight in flight),
-    the measured counterpart of the LDS datasheet peak."""
-    sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
-    hx.lds_probe(blocks, reps, sink)
-    torch.cuda.synchronize()
-    t = time.perf_counter()
-    nbytes = hx.lds_probe(blocks, reps, sink)
-    torch.cuda.synchronize()
-    return nbytes / (time.perf_counter() - t) / 1e9
 
 def kernel_traffic(kernel: str, workload: int, prob=None):
     """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply (the
@@ -692,7 +679,6 @@ def main():
     if dominant != "maxflow" and "maxflow" in kernel_us:
         # the LDS-resident max-flow beside the dominant kernel, against the LDS peak
         out["maxflow_roofline"] = roofline_for("maxflow", kernel_us, prob, hbm, n_p, n_d, args.workload)
-        out["maxflow_roofline"]["measured_lds_gbs"] = measured_lds_gbs(torch, hx)
 
     if not args.no_cpu_baseline:
         from oracle import hxo  # test infrastructure: only this baseline leg uses it

@@ -214,8 +214,10 @@ int hx_member_words(int32_t n_gpus);
  * ov = min((r+1)tp_d, (q+1)tp_p) - max(r tp_d, q tp_p) > 0, the link g -> h carries
  * bytes = ((V1*n)*ov)/(tp_p*tp_d) with V1 = (2*s_in)*H_kv*B, in alpha_{gh} + bytes/beta_{gh};
  * the KV time is the largest of these, and the edge capacity floor(1000/time) clamped to
- * HX_CAP_MAX, or 0 when either replica is infeasible.  Granularity 1: the edge from prefill
- * GPU g (replica of n_g GPUs) to decode GPU h has time alpha_{gh} + ((V1*L)/n_g)/beta_{gh}.
+ * HX_CAP_MAX, or 0 when either replica is infeasible.  Granularity 1: every edge counts
+ * requests, so the edge from prefill GPU g to decode GPU h carries one request's whole KV cache
+ * over the link g -> h: time alpha_{gh} + (V1*L)/beta_{gh} (the KV edge of two one-GPU
+ * replicas on that link), whatever the replicas' sizes; 0 when either replica is infeasible.
  * With space.variant & HX_VARIANT_KV_ORDER (granularity 0), pipeline position a of a replica
  * may be served by any of its stages (stage s = the members ranked s*tp .. s*tp+tp-1): the
  * KV time is the minimum over every pair of stage orders of the two replicas when there are
@@ -332,18 +334,18 @@ int hx_gather_candidates(int32_t n_gpus, const hx_candidates *src, const int32_t
  * memory, links by bandwidth) is partitioned into K groups (spectral order, then Kernighan-Lin
  * swaps), the groups are coarsened into super nodes and split into prefill and decode replicas
  * by a cut of maximum weight, and the partition is projected back onto the GPUs.  Edge weights
- * are w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6) clamped to [0, 2^23] (whole MB/s), node
- * weights the memory limits in whole bytes, so cuts and gains are exact integer sums. */
+ * are w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6) clamped to [0, 2^47] (whole MB/s; the
+ * bound keeps every cut of up to 255 GPUs below 2^62), node weights the memory limits in whole
+ * bytes, so cuts, gains and their sums are exact 64-bit integer sums. */
 
-/* Device scratch both calls need (an [n_gpus][n_gpus] int32 weight table they fill first);
+/* Device scratch both calls need (an [n_gpus][n_gpus] int64 weight table they fill first);
  * 0 for n_gpus outside [2, 255]. */
 size_t hx_partition_workspace_bytes(int32_t n_gpus);
 
 /* Spectral order: the GPUs sorted by (x_d, d), x the Fiedler direction of the Laplacian
  * Deg - w by `iters` power iterations on (c I - Lap), c = 2 max_d Deg_d, from x_d = d - (G-1)/2,
- * each iteration taking out the mean and normalising.  A row's product sums in ascending index
- * order; the mean and the norm sum by a fixed tree: 64 partial sums t_l = ((v_l + v_{l+64}) +
- * v_{l+128}) + v_{l+192}, then t_l <- t_l + t_{l xor s} for s = 32, 16, ..., 1.  One workgroup.
+ * each iteration taking out the mean and normalising.  Every sum (a row's product, the mean,
+ * the squared norm) runs in ascending index order.  One workgroup.
  *   order [n_gpus] device int32 out; fiedler [n_gpus] device double out, nullable. */
 int hx_spectral_order(const hx_cluster *cluster, int32_t iters, void *workspace, size_t workspace_bytes,
                       int32_t *order, double *fiedler, hipStream_t stream);
@@ -354,9 +356,12 @@ int hx_spectral_order(const hx_cluster *cluster, int32_t iters, void *workspace,
  *       clamped to [2, min(n_gpus, max_groups, 32)];
  *   step (i): the spectral order rotated by (bits 3-10 mod n_gpus); the i-th GPU d of it goes to
  *       group min(K-1, floor(K (2 C_i + m_d) / (2 M))), C_i the memory before it, M the total;
- *       then Kernighan-Lin: while some swap of two GPUs of different groups lowers the cut and
- *       does not widen the memory gap between the two groups, the swap with the largest
- *       reduction (lowest (u, v) on ties) is applied, at most 2 n_gpus times;
+ *       then Kernighan-Lin passes: with every GPU unlocked, repeatedly the swap of two unlocked
+ *       GPUs of different groups that does not widen the memory gap between the two groups and
+ *       has the largest cut reduction, negative or not (lowest (u, v) on ties), is made and both
+ *       GPUs locked, until no such pair is left; the pass keeps its first k swaps, k the
+ *       smallest with the largest summed reduction, when that sum is positive, and undoes the
+ *       rest; passes repeat while one lowers the cut, at most 64;
  *   groups are numbered by smallest member;
  *   step (ii): super node k starts on side bit (11 + k) of the draw (the last one flipped if all
  *       agree); while flipping one super node raises the coarse cut with both sides occupied,
@@ -382,14 +387,6 @@ int hx_partition_candidates(const hx_cluster *cluster, hx_model model, hx_worklo
 int hx_profile(int32_t enable);
 int hx_profile_read(double *ms, int32_t *launches, int32_t n);
 const char *hx_kernel_name(int32_t k);
-
-/* Measurement probe (not part of the scoring path): enqueues on `stream` a kernel of `blocks`
- * workgroups (1..2^20) that fill 16 KB of LDS each and read it back, conflict-free, for `reps`
- * rounds (1..2^20), and stores in *bytes the LDS bytes the launch reads; timing the launch gives
- * the LDS read bandwidth the device sustains.  sink: device uint32[blocks * 256], caller-owned;
- * the kernel writes nothing there (it exists so that the loads are kept).  HX_EINVAL on bad
- * arguments, HX_EHIP on a launch error. */
-int hx_lds_probe(int32_t blocks, int32_t reps, uint32_t *sink, int64_t *bytes, hipStream_t stream);
 
 /* Human-readable text of a return code, and the last HIP error message kept by HX_EHIP. */
 const char *hx_strerror(int code);

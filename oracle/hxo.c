@@ -36,7 +36,7 @@
  *     every pair of ranks whose KV-head slices overlap by a fraction f, a link
  *     carries 2*s_in*H_kv*B*n*f bytes in alpha + bytes/beta; links run in
  *     parallel, so the KV time is the slowest link.  Per-GPU flow nodes use the
- *     per-GPU rule of kv_gpu_time().
+ *     per-GPU rule of hxo_kv_gpu_time(): a whole request's KV cache per unit of flow.
  *   - Source and sink edges are unbounded (2^24 - 1) unless a coordinator
  *     bandwidth and request size are given.
  *   - Request classes (length buckets, at most four, in place of the single mean
@@ -469,14 +469,17 @@ double hxo_kv_time_best(const hxo_cluster *c, const hxo_model *m, const hxo_work
     return best;
 }
 
-/* Per-GPU flow nodes: the link from prefill GPU g (one of n_p GPUs of its replica) to decode
- * GPU h carries g's 1/n_p share of a request's KV cache for all L layers. */
-double hxo_kv_gpu_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
-                       int32_t g, int32_t h, int32_t n_p)
+/* Per-GPU flow nodes (a refinement of the Sec. 3.3 network that the paper does not draw): every
+ * edge of the network counts requests, and a GPU node carries its share of its replica's
+ * requests, so a unit of flow on the KV edge from prefill GPU g to decode GPU h is one request
+ * whose whole KV cache (2 s_in H_kv B bytes per layer, all L layers) crosses the link g -> h.
+ * The time is that of a KV edge between two one-GPU replicas on the same link (one stage pair
+ * sharing all L layers, one rank pair overlapping fully), whatever the replicas' sizes. */
+double hxo_kv_gpu_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w, int32_t g, int32_t h)
 {
     const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
-    const double share = (V1 * (double)m->n_layers) / (double)n_p;
-    return alpha_of(c, g, h) + share / beta_of(c, g, h);
+    const double bytes = V1 * (double)m->n_layers;
+    return alpha_of(c, g, h) + bytes / beta_of(c, g, h);
 }
 
 /* ------------------------------------------------------------------ batch cost model */
@@ -641,7 +644,6 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
             for (int i = 0; i < np; i++) {
                 int g = pnode[i];
                 int kp = bt->assign[(int64_t)g * N + n];
-                int szp = group_members(bt, n, kp, pm);
                 for (int j = 0; j < nd; j++) {
                     int h = dnode[j];
                     int kd = bt->assign[(int64_t)h * N + n];
@@ -652,10 +654,10 @@ static void flownet_range(const hxo_batch *bt, int n0, int n1, const uint8_t *tp
                             t = 0.0;
                             for (int k = 0; k < bt->w->n_classes; k++) {
                                 const hxo_workload tk = class_task(bt->w, k);
-                                t = t + bt->w->cls_w[k] * hxo_kv_gpu_time(c, bt->m, &tk, g, h, szp);
+                                t = t + bt->w->cls_w[k] * hxo_kv_gpu_time(c, bt->m, &tk, g, h);
                             }
                         } else {
-                            t = hxo_kv_gpu_time(c, bt->m, bt->w, g, h, szp);
+                            t = hxo_kv_gpu_time(c, bt->m, bt->w, g, h);
                         }
                         kv = hxo_quantize(1000.0 / t);
                     }
@@ -1165,15 +1167,18 @@ int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
  * The first phase of the scheduler (Sec. 3.2) as a candidate generator.  The device graph has
  * the GPUs as nodes, weighted by their memory limits, and the links as edges, weighted by
  * bandwidth.  Readings (the paper names the methods, not their parameters):
- *   - edge weight w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6), clamped to [0, 2^23]: the
+ *   - edge weight w_de = floor(((beta_de + beta_ed) * 0.5) / 1e6), clamped to [0, 2^47]: the
  *     symmetrised bandwidth in whole MB/s, so that every cut and gain below is an exact integer
- *     sum; node weight = the memory limit in whole bytes;
+ *     sum; the bound (1.4e20 bytes/s, far beyond any link) keeps every cut of a graph of up to
+ *     255 GPUs below 2^62, so cuts, gains and sums of gains are exact 64-bit integers; node
+ *     weight = the memory limit in whole bytes;
  *   - Step (i), initial partition: spectral order by the Fiedler direction of the Laplacian
  *     Deg - w (power iteration, hxo_spectral_order), cut into K contiguous groups of balanced
  *     memory; K = floor(total memory / replica memory), a replica holding the weights and the
  *     KV caches of 32 requests (Appendix A: 12 H^2 B L + 32 * 2 (s_in + s_out) H_kv B L);
- *     then Kernighan-Lin: repeatedly the pair swap between two groups with the largest cut
- *     reduction, among swaps that do not widen the memory gap between the two groups;
+ *     then Kernighan-Lin passes (hxo_kl_refine): tentative pair swaps on unlocked GPUs, each
+ *     the admissible swap of largest cut reduction even when it is negative, then the best
+ *     prefix of the pass kept; passes repeat while one lowers the cut;
  *   - Step (ii), coarsen and secondary partition: groups become super nodes joined by the
  *     summed weights of their links; a local search for a maximum cut splits them into
  *     prefill and decode replicas (single flips with the largest gain, both sides kept);
@@ -1183,38 +1188,21 @@ int hxo_guided_moves(int32_t n_gpus, int32_t max_groups, int32_t granularity,
  * node k (bit 11 + k).
  */
 
-/* clamped to [0, 2^23] MB/s (8.4 TB/s, beyond any link), so that a GPU's summed weights fit 31 bits */
+/* whole MB/s of the symmetrised bandwidth, clamped to [0, 2^47] */
+#define HXO_PG_WEIGHT_MAX 140737488355328.0  /* 2^47 */
 static int64_t pg_weight(const hxo_cluster *c, int d, int e)
 {
     if (d == e) return 0;
     double v = floor(((beta_of(c, d, e) + beta_of(c, e, d)) * 0.5) / 1.0e6);
     if (!(v >= 0.0)) v = 0.0;
-    if (v > 8388608.0) v = 8388608.0;
+    if (v > HXO_PG_WEIGHT_MAX) v = HXO_PG_WEIGHT_MAX;
     return (int64_t)v;
-}
-
-/* Sum of v[0..G) (G <= 256) in a fixed association: 64 partial sums t_l = ((v_l + v_{l+64}) +
- * v_{l+128}) + v_{l+192} (terms past G left out, t_l = 0 when l >= G), then six butterfly
- * steps t_l <- t_l + t_{l xor s} for s = 32, 16, ..., 1; the result is t_0. */
-static double tree_sum(const double *v, int G)
-{
-    double t[64], u[64];
-    for (int l = 0; l < 64; l++) {
-        t[l] = l < G ? v[l] : 0.0;
-        for (int k = 1; k < 4; k++)
-            if (l + 64 * k < G) t[l] = t[l] + v[l + 64 * k];
-    }
-    for (int s = 32; s > 0; s >>= 1) {
-        for (int l = 0; l < 64; l++) u[l] = t[l] + t[l ^ s];
-        for (int l = 0; l < 64; l++) t[l] = u[l];
-    }
-    return t[0];
 }
 
 /* Spectral order: iters power iterations on (cap I - Lap), Lap = Deg - w, cap = 2 max_d Deg_d,
  * from x_d = d - (G-1)/2, each iteration removing the mean (the constant eigenvector) and
- * normalising; a row's product runs in ascending index order, the mean and the norm use
- * tree_sum.  order = GPUs sorted by (x_d, d); fiedler (nullable) receives x. */
+ * normalising; every sum (a row's product, the mean, the squared norm) runs in ascending index
+ * order.  order = GPUs sorted by (x_d, d); fiedler (nullable) receives x. */
 int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, double *fiedler)
 {
     const int G = c->n_gpus;
@@ -1234,12 +1222,16 @@ int hxo_spectral_order(const hxo_cluster *c, int32_t iters, int32_t *order, doub
             for (int e = 0; e < G; e++) s = s + (double)pg_weight(c, d, e) * x[e];
             y[d] = (cap - deg[d]) * x[d] + s;
         }
-        const double mean = tree_sum(y, G) / (double)G;
+        double tot = 0.0;
+        for (int d = 0; d < G; d++) tot = tot + y[d];
+        const double mean = tot / (double)G;
         for (int d = 0; d < G; d++) {
             y[d] = y[d] - mean;
             sq[d] = y[d] * y[d];
         }
-        const double nrm = sqrt(tree_sum(sq, G));
+        double ss = 0.0;
+        for (int d = 0; d < G; d++) ss = ss + sq[d];
+        const double nrm = sqrt(ss);
         if (!(nrm > 0.0)) break;
         for (int d = 0; d < G; d++) x[d] = y[d] / nrm;
     }
@@ -1270,6 +1262,93 @@ int32_t hxo_partition_groups(const hxo_cluster *c, const hxo_model *m, const hxo
 
 static int64_t iabs64(int64_t v) { return v < 0 ? -v : v; }
 
+/* Cut reduction of exchanging GPUs u and v of different groups: u's links into v's group and
+ * v's links into u's group stop being cut, their links into their own groups start being cut,
+ * and the link u-v stays cut. */
+static int64_t kl_swap_gain(const hxo_cluster *c, const int *grp, int u, int v)
+{
+    const int A = grp[u], B = grp[v];
+    int64_t gain = 0;
+    for (int x = 0; x < c->n_gpus; x++) {
+        if (x == u || x == v) continue;
+        if (grp[x] == B) gain += pg_weight(c, u, x);
+        if (grp[x] == A) gain -= pg_weight(c, u, x);
+        if (grp[x] == A) gain += pg_weight(c, v, x);
+        if (grp[x] == B) gain -= pg_weight(c, v, x);
+    }
+    return gain;
+}
+
+/* A swap may not widen the memory gap between the two groups ("balances node weights"). */
+static int kl_balanced(const int64_t *gmem, const int64_t *mem, int A, int B, int u, int v)
+{
+    const int64_t gap0 = iabs64(gmem[A] - gmem[B]);
+    const int64_t gap1 = iabs64((gmem[A] - mem[u] + mem[v]) - (gmem[B] - mem[v] + mem[u]));
+    return gap1 <= gap0;
+}
+
+static void kl_exchange(int *grp, int64_t *gmem, const int64_t *mem, int u, int v)
+{
+    const int A = grp[u], B = grp[v];
+    gmem[A] += mem[v] - mem[u];
+    gmem[B] += mem[u] - mem[v];
+    grp[u] = B;
+    grp[v] = A;
+}
+
+/* Kernighan-Lin refinement of a partition of the GPUs into groups 0..K-1 (Sec. 3.2 step (i);
+ * Kernighan and Lin's pass structure, with the pair swaps taken between any two groups).
+ * A pass unlocks every GPU, then repeatedly takes, among the pairs of unlocked GPUs in
+ * different groups whose swap keeps the memory balance, the one with the largest cut reduction
+ * (possibly negative; lowest (u, v) on ties), exchanges them tentatively and locks both, until
+ * no pair is left.  With S_k the summed reduction of the first k swaps, the pass keeps the
+ * first k* swaps, k* the smallest k with the largest S_k, when S_k* > 0, and undoes the rest;
+ * otherwise it undoes every swap and the refinement stops.  At most HXO_KL_PASSES passes.
+ * Returns the number of passes that lowered the cut. */
+#define HXO_KL_PASSES 64
+int hxo_kl_refine(const hxo_cluster *c, int32_t *grp32)
+{
+    const int G = c->n_gpus;
+    int *grp = (int *)malloc(sizeof(int) * G), *locked = (int *)malloc(sizeof(int) * G);
+    int *su = (int *)malloc(sizeof(int) * G), *sv = (int *)malloc(sizeof(int) * G);
+    int64_t *mem = (int64_t *)malloc(sizeof(int64_t) * G), *gmem = (int64_t *)malloc(sizeof(int64_t) * 256);
+    int passes = 0;
+    for (int d = 0; d < G; d++) {
+        grp[d] = grp32[d];
+        mem[d] = (int64_t)memlim_of(c, d);
+    }
+    for (int k = 0; k < 256; k++) gmem[k] = 0;
+    for (int d = 0; d < G; d++) gmem[grp[d]] += mem[d];
+    for (; passes < HXO_KL_PASSES; passes++) {
+        for (int d = 0; d < G; d++) locked[d] = 0;
+        int n_swaps = 0, kbest = 0;
+        int64_t run = 0, best = 0;
+        for (;;) {
+            int bu = -1, bv = -1;
+            int64_t bg = 0;
+            for (int u = 0; u < G; u++)
+                for (int v = u + 1; v < G; v++) {
+                    if (locked[u] || locked[v] || grp[u] == grp[v]) continue;
+                    if (!kl_balanced(gmem, mem, grp[u], grp[v], u, v)) continue;
+                    const int64_t g = kl_swap_gain(c, grp, u, v);
+                    if (bu < 0 || g > bg) { bg = g; bu = u; bv = v; }
+                }
+            if (bu < 0) break;
+            kl_exchange(grp, gmem, mem, bu, bv);
+            locked[bu] = locked[bv] = 1;
+            su[n_swaps] = bu; sv[n_swaps] = bv; n_swaps++;
+            run += bg;
+            if (run > best) { best = run; kbest = n_swaps; }
+        }
+        /* undo the swaps past the best prefix, last first */
+        for (int i = n_swaps - 1; i >= kbest; i--) kl_exchange(grp, gmem, mem, su[i], sv[i]);
+        if (kbest == 0) break;
+    }
+    for (int d = 0; d < G; d++) grp32[d] = grp[d];
+    free(grp); free(locked); free(su); free(sv); free(mem); free(gmem);
+    return passes;
+}
+
 int hxo_partition_candidates(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
                              const int32_t *order, int32_t max_groups, int32_t n_cand, const uint64_t *rnd,
                              uint8_t *assign, uint8_t *role)
@@ -1284,8 +1363,8 @@ int hxo_partition_candidates(const hxo_cluster *c, const hxo_model *m, const hxo
         mem[d] = (int64_t)memlim_of(c, d);
         total += mem[d];
     }
-    int *grp = (int *)malloc(sizeof(int) * G);
-    int64_t *gmem = (int64_t *)malloc(sizeof(int64_t) * 256);
+    if (total <= 0) total = 1;  /* no memory anywhere: every GPU falls in group 0 */
+    int32_t *grp = (int32_t *)malloc(sizeof(int32_t) * G);
     int64_t *sw = (int64_t *)malloc(sizeof(int64_t) * 32 * 32);
     for (int n = 0; n < n_cand; n++) {
         const uint64_t r = rnd[n];
@@ -1301,37 +1380,7 @@ int hxo_partition_candidates(const hxo_cluster *c, const hxo_model *m, const hxo
             grp[d] = k < K - 1 ? k : K - 1;
             cum += mem[d];
         }
-        for (int k = 0; k < K; k++) gmem[k] = 0;
-        for (int d = 0; d < G; d++) gmem[grp[d]] += mem[d];
-        /* Kernighan-Lin pair swaps */
-        for (int step = 0; step < 2 * G; step++) {
-            int64_t best = 0;
-            int bu = -1, bv = -1;
-            for (int u = 0; u < G; u++)
-                for (int v = u + 1; v < G; v++) {
-                    const int A = grp[u], Bk = grp[v];
-                    if (A == Bk) continue;
-                    const int64_t gap0 = iabs64(gmem[A] - gmem[Bk]);
-                    const int64_t gap1 = iabs64((gmem[A] - mem[u] + mem[v]) - (gmem[Bk] - mem[v] + mem[u]));
-                    if (gap1 > gap0) continue;
-                    int64_t gu = 0, gv = 0;  /* cut reduction of moving u to B and v to A */
-                    for (int x = 0; x < G; x++) {
-                        if (x == u || x == v) continue;
-                        if (grp[x] == Bk) gu += pg_weight(c, u, x);
-                        if (grp[x] == A) gu -= pg_weight(c, u, x);
-                        if (grp[x] == A) gv += pg_weight(c, v, x);
-                        if (grp[x] == Bk) gv -= pg_weight(c, v, x);
-                    }
-                    const int64_t gain = gu + gv;
-                    if (gain > best) { best = gain; bu = u; bv = v; }
-                }
-            if (bu < 0) break;
-            const int A = grp[bu], Bk = grp[bv];
-            gmem[A] += mem[bv] - mem[bu];
-            gmem[Bk] += mem[bu] - mem[bv];
-            grp[bu] = Bk;
-            grp[bv] = A;
-        }
+        hxo_kl_refine(c, grp);
         /* step (iii) numbering: groups by smallest member */
         int map[256], used = 0;
         for (int k = 0; k < 256; k++) map[k] = -1;
@@ -1369,6 +1418,6 @@ int hxo_partition_candidates(const hxo_cluster *c, const hxo_model *m, const hxo
         for (int k = 0; k < max_groups; k++)
             role[(int64_t)k * n_cand + n] = k < used ? (uint8_t)(side[k] ? HXO_DECODE : HXO_PREFILL) : (uint8_t)HXO_UNUSED;
     }
-    free(mem); free(grp); free(gmem); free(sw);
+    free(mem); free(grp); free(sw);
     return 0;
 }

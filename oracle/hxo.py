@@ -244,10 +244,11 @@ def kv_time(prob, pm: Sequence[int], ptp: int, ppp: int, dm: Sequence[int], dtp:
               C.c_int32(ppp), _p(d), C.c_int32(dtp), C.c_int32(dpp))
 
 
-def kv_gpu_time(prob, g: int, h: int, n_p: int) -> float:
+def kv_gpu_time(prob, g: int, h: int) -> float:
+    """Per-GPU flow nodes: seconds for one request's whole KV cache over the link g -> h."""
     a = _Args(prob)
     return lib().hxo_kv_gpu_time(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), C.c_int32(g),
-                                 C.c_int32(h), C.c_int32(n_p))
+                                 C.c_int32(h))
 
 
 def quantize(x: float) -> int:
@@ -320,6 +321,15 @@ def partition_groups(prob) -> int:
     a = _Args(prob)
     lib().hxo_partition_groups.restype = C.c_int32
     return int(lib().hxo_partition_groups(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl)))
+
+
+def kl_refine(prob, grp: np.ndarray) -> Tuple[np.ndarray, int]:
+    """Kernighan-Lin refinement of one grouping of prob's GPUs (group ids < 256): (the refined
+    grouping, the number of passes that lowered the cut)."""
+    a = _Args(prob)
+    g = np.ascontiguousarray(np.asarray(grp, np.int32).copy())
+    passes = lib().hxo_kl_refine(C.byref(a.cluster), _p(g))
+    return g, int(passes)
 
 
 def partition_candidates(prob, order: np.ndarray, rnd: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhx.so")
 SOURCES = ["hx_api.cpp", "hx_cost.hip", "hx_flownet.hip", "hx_maxflow.hip", "hx_best.hip", "hx_refine.hip",
-           "hx_partition.hip", "hx_probe.hip"]
+           "hx_partition.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",

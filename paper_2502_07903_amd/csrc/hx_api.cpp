@@ -339,13 +339,6 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 
-int hx_lds_probe(int32_t blocks, int32_t reps, uint32_t* sink, int64_t* bytes, hipStream_t stream) {
-    if (!sink || !bytes || blocks < 1 || blocks > (1 << 20) || reps < 1 || reps > (1 << 20)) return HX_EINVAL;
-    *bytes = hx::lds_probe_bytes(blocks, reps);
-    hipError_t e = hx::launch_lds_probe(blocks, reps, sink, stream);
-    return e == hipSuccess ? HX_OK : hip_error(e);
-}
-
 int hx_edge_classes(const hx_flownet* net, const int32_t* flow_value, const int32_t* kv_flow, uint8_t* node_cls,
                     uint8_t* kv_cls, hipStream_t stream) {
     int rc = check_net_shape(net);
@@ -375,14 +368,14 @@ int hx_guided_moves(int32_t n_gpus, int32_t granularity, const hx_candidates* pa
 
 size_t hx_partition_workspace_bytes(int32_t n_gpus) {
     if (n_gpus < 2 || n_gpus > HX_MAX_GPUS) return 0;
-    return ((size_t)n_gpus * n_gpus * sizeof(int32_t) + 255) & ~(size_t)255;
+    return ((size_t)n_gpus * n_gpus * sizeof(int64_t) + 255) & ~(size_t)255;
 }
 
 int hx_spectral_order(const hx_cluster* cluster, int32_t iters, void* workspace, size_t workspace_bytes,
                       int32_t* order, double* fiedler, hipStream_t stream) {
     if (!cluster || cluster->n_gpus < 2 || cluster->n_gpus > HX_MAX_GPUS || !cluster->beta || !order) return HX_EINVAL;
     if (iters < 0 || !workspace || workspace_bytes < hx_partition_workspace_bytes(cluster->n_gpus)) return HX_EINVAL;
-    hipError_t e = hx::launch_spectral(cluster->n_gpus, cluster->beta, static_cast<int32_t*>(workspace), iters, order,
+    hipError_t e = hx::launch_spectral(cluster->n_gpus, cluster->beta, static_cast<int64_t*>(workspace), iters, order,
                                        fiedler, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
@@ -397,7 +390,7 @@ int hx_partition_candidates(const hx_cluster* cluster, hx_model model, hx_worklo
     if (cluster->n_gpus < 2 || !order || !rnd || !workspace ||
         workspace_bytes < hx_partition_workspace_bytes(cluster->n_gpus))
         return HX_EINVAL;
-    hipError_t e = hx::launch_partition(make_problem(cluster, model, wl, sp, &cand), static_cast<int32_t*>(workspace),
+    hipError_t e = hx::launch_partition(make_problem(cluster, model, wl, sp, &cand), static_cast<int64_t*>(workspace),
                                         order, rnd, assign, role, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }

@@ -507,24 +507,21 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
 }
 
 // Per-GPU nodes: one workgroup of kGpuKvWaves wavefronts per 64 candidates (a lane per
-// candidate in every wavefront).  The edge from prefill GPU g (replica of n_g GPUs) to decode
-// GPU h depends on g, h, n_g and whether both replicas are feasible, so the workgroup first
-// stages, per candidate, every GPU's replica size, 0 when the replica is infeasible ([G][64]
-// bytes in LDS), and the node lists' GPU ids; then each wavefront takes every kGpuKvWaves-th edge row (coalesced
-// stores across the 64 candidates) with no dependent global loads but alpha/beta.  One lane per
-// (edge, candidate) would repeat the lookups of both endpoints for every edge.
+// candidate in every wavefront).  Every edge of the per-GPU network counts requests (a GPU node
+// carries its share of its replica's requests), so the edge from prefill GPU g to decode GPU h
+// carries one request's whole KV cache, V1 L bytes, over the link g -> h: it depends on g, h and
+// whether both replicas are feasible.  The workgroup first stages, per candidate, every GPU's
+// feasibility ([G][64] bytes in LDS: 1 when its replica kept a strategy) and the node lists' GPU
+// ids; then each wavefront takes every kGpuKvWaves-th edge row (coalesced stores across the 64
+// candidates) with no dependent global loads but alpha/beta.  One lane per (edge, candidate)
+// would repeat the lookups of both endpoints for every edge.
 constexpr int kGpuKvWaves = 4;
 
 // Node rows staged per side: a side has at most G per-GPU nodes.
 __host__ __device__ inline int kv_gpu_rows(int G, int max_rows) { return max_rows < G ? max_rows : G; }
 
-// The share (V1 L) / n_g of a prefill GPU depends only on its replica's size n_g (1..255), so
-// it is tabulated once per workgroup for every size and task: [tasks][256] doubles.
-constexpr int kShareSizes = 256;
-
-__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d, int n_task) {
-    return sizeof(double) * n_task * kShareSizes +
-           ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
+__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d) {
+    return ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
 }
 
 template <int W, bool kCls>
@@ -535,26 +532,23 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
     const int64_t n = (int64_t)blockIdx.x * 64 + lane;
     const bool in = n < N;
     const int G = p.G;
-    const int n_task = kCls ? p.n_cls : 1;
-    double* share = reinterpret_cast<double*>(sm);               // [task][size]: (V1 L) / size
-    uint8_t* gd = sm + sizeof(double) * n_task * kShareSizes;   // [G][64]: replica size, 0 if
-                                                                 // infeasible or unused
-    uint8_t* ps = gd + (size_t)G * 64;        // [prow][64]: prefill node -> GPU
+    uint8_t* ok = sm;                          // [G][64]: 1 if the GPU's replica is feasible
+    uint8_t* ps = ok + (size_t)G * 64;         // [prow][64]: prefill node -> GPU
     const int prow = kv_gpu_rows(G, f.max_p), drow = kv_gpu_rows(G, f.max_d);
-    uint8_t* ds = ps + (size_t)prow * 64;     // [drow][64]: decode node -> GPU
+    uint8_t* ds = ps + (size_t)prow * 64;      // [drow][64]: decode node -> GPU
     const int np = in ? f.n_p[n] : 0, nd = in ? f.n_d[n] : 0;
-    for (int x = threadIdx.x; x < n_task * kShareSizes; x += 64 * kGpuKvWaves) {
-        const int k = x / kShareSizes, sz = x - k * kShareSizes;
-        const double V1 = 2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B;
-        share[x] = sz > 0 ? (V1 * (double)p.L) / (double)sz : 0.0;
-    }
+    // one request's KV cache for all L layers, per task
+    double vl[HX_MAX_CLASSES];
+#pragma unroll
+    for (int k = 0; k < HX_MAX_CLASSES; ++k)
+        vl[k] = (2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B) * (double)p.L;
     for (int g = wave; g < G; g += kGpuKvWaves) {
         uint8_t d = 0;
         if (in) {
             const int k = p.assign[(int64_t)g * N + n];
-            if (k < p.Kmax && o.tp[(int64_t)k * N + n] > 0) d = (uint8_t)mask_size<W>(o.members, k, N, n);
+            if (k < p.Kmax && o.tp[(int64_t)k * N + n] > 0) d = 1;
         }
-        gd[g * 64 + lane] = d;
+        ok[g * 64 + lane] = d;
     }
     for (int i = wave; i < prow; i += kGpuKvWaves)
         ps[i * 64 + lane] = i < np ? (uint8_t)f.p_slot[(int64_t)i * N + n] : 0;
@@ -576,18 +570,15 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
     for (int e = wave; e < emax; e += kGpuKvWaves) {
         if (e < E) {
             const int g = ps[i * 64 + lane], h = ds[j * 64 + lane];
-            const int szp = gd[g * 64 + lane], szd = gd[h * 64 + lane];
             int32_t c = 0;
-            if (szp > 0 && szd > 0) {
-                // g's 1/n_g share of a request's KV cache for all L layers, per task
+            if (ok[g * 64 + lane] && ok[h * 64 + lane]) {
                 const double al = p.alpha[g * G + h], be = p.beta[g * G + h];
                 double t;
                 if (kCls) {
                     t = 0.0;
-                    for (int k = 0; k < p.n_cls; ++k)
-                        t = t + p.cls_w[k] * (al + share[k * kShareSizes + szp] / be);
+                    for (int k = 0; k < p.n_cls; ++k) t = t + p.cls_w[k] * (al + vl[k] / be);
                 } else {
-                    t = al + share[szp] / be;
+                    t = al + vl[0] / be;
                 }
                 c = quantize(1000.0 / t);
             }
@@ -612,7 +603,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     prof_mark(kKKv, false, s);
     if (p.granularity != 0) {
         const dim3 grid((p.N + 63) / 64), block(64 * kGpuKvWaves);
-        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d, p.n_cls > 0 ? p.n_cls : 1);
+        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d);
         if (p.n_cls > 0)
             hipLaunchKernelGGL((kv_gpu_kernel<W, true>), grid, block, glds, s, p, o, f);
         else

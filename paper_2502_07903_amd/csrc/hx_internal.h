@@ -102,9 +102,6 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           unsigned long long* stats, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
-// The LDS bandwidth probe: bytes a launch of `blocks` workgroups and `reps` rounds reads.
-hipError_t launch_lds_probe(int32_t blocks, int32_t reps, uint32_t* sink, hipStream_t s);
-int64_t lds_probe_bytes(int32_t blocks, int32_t reps);
 
 // Refinement (Sec. 3.4): edge classes of networks of at most kClsMaxV vertices, guided moves,
 // and the column gather.
@@ -114,10 +111,10 @@ hipError_t launch_classes(const FlowNet& f, const int32_t* flow_value, const int
 hipError_t launch_moves(int32_t G, int32_t K, int32_t gran, int32_t M, const uint8_t* p_assign,
                         const uint8_t* p_role, const FlowNet& pn, const uint8_t* node_cls, int32_t n_child,
                         const uint64_t* rnd, uint8_t* c_assign, uint8_t* c_role, int32_t* move, hipStream_t s);
-// Graph partition (Sec. 3.2): w is an [G][G] int32 scratch both calls fill first.
-hipError_t launch_spectral(int32_t G, const double* beta, int32_t* w, int32_t iters, int32_t* order, double* fiedler,
+// Graph partition (Sec. 3.2): w is an [G][G] int64 scratch both calls fill first.
+hipError_t launch_spectral(int32_t G, const double* beta, int64_t* w, int32_t iters, int32_t* order, double* fiedler,
                            hipStream_t s);
-hipError_t launch_partition(const Problem& p, int32_t* w, const int32_t* order, const uint64_t* rnd, uint8_t* assign,
+hipError_t launch_partition(const Problem& p, int64_t* w, const int32_t* order, const uint64_t* rnd, uint8_t* assign,
                             uint8_t* role, hipStream_t s);
 hipError_t launch_gather(int32_t G, int32_t K, int32_t Ns, const uint8_t* sa, const uint8_t* sr, const int32_t* index,
                          int32_t count, uint8_t* da, uint8_t* dr, hipStream_t s);

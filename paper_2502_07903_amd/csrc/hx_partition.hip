@@ -1,22 +1,25 @@
 // hx_partition.hip -- the graph-partition phase of Sec. 3.2 as a candidate generator, on gfx950.
 //
 // The device graph has the GPUs as nodes, weighted by memory, and the links as edges, weighted by
-// bandwidth.  Edge weights are whole MB/s of the symmetrised bandwidth (clamped to 2^23), so
-// every cut, gain and coarsened weight is an exact integer sum and does not depend on the order
-// of the additions; only the spectral step is floating point, and it fixes its order.
+// bandwidth.  Edge weights are whole MB/s of the symmetrised bandwidth (clamped to 2^47, which
+// keeps every cut of a graph of up to 255 GPUs below 2^62), so every cut, gain and coarsened
+// weight is an exact 64-bit integer sum and does not depend on the order of the additions; only
+// the spectral step is floating point, and it sums in ascending index order.
 //
 //   graph_kernel      one lane per GPU pair: w = floor(((beta_de + beta_ed) * 0.5) / 1e6);
 //   spectral_kernel   one workgroup: power iteration on (cap I - Lap) for the Fiedler direction,
-//                     a lane per row (ascending products), the mean and the norm by a fixed
-//                     64-way summation tree (four strided terms per lane, then an xor
-//                     butterfly); the GPUs ranked by (x, id);
+//                     a lane per row (ascending products); the mean and the squared norm summed
+//                     in ascending order by one lane (255 dependent additions, twice per
+//                     iteration; the order depends only on the cluster, so a search computes it
+//                     once); the GPUs ranked by (x, id);
 //   partition_kernel  one workgroup per candidate: (i) the rotated spectral order cut into K
-//                     memory-balanced groups, then Kernighan-Lin pair swaps (a lane per pair
-//                     of GPUs scores the swap from per-GPU group sums kept in LDS; a workgroup
-//                     maximum picks the largest cut reduction, lowest pair on ties); (ii) groups
-//                     coarsened into super nodes (LDS atomics) and split into prefill and
-//                     decode by single flips that raise the cut; (iii) the projection written
-//                     as the candidate's assign and role columns.
+//                     memory-balanced groups, then Kernighan-Lin passes: a lane per pair of GPUs
+//                     scores the swap from per-GPU group sums kept in LDS, a workgroup maximum
+//                     picks the largest reduction (negative ones too; lowest pair on ties), the
+//                     swap is made tentatively and its two GPUs locked; the pass keeps its best
+//                     prefix and undoes the rest; (ii) groups coarsened into super nodes (LDS
+//                     atomics) and split into prefill and decode by single flips that raise the
+//                     cut; (iii) the projection written as the candidate's assign and role columns.
 // Graph and integer work: no MFMA.
 #include "hx_internal.h"
 
@@ -25,9 +28,10 @@ namespace {
 
 constexpr int kPgBlock = 256;   // >= HX_MAX_GPUS + 1: a lane per GPU
 constexpr int kPgMaxK = 32;     // groups of one candidate
-constexpr double kPgWeightMax = 8388608.0;  // 2^23 MB/s
+constexpr double kPgWeightMax = 140737488355328.0;  // 2^47 MB/s
+constexpr int kKlPasses = 64;   // Kernighan-Lin passes at most
 
-__global__ void graph_kernel(int G, const double* beta, int32_t* w) {
+__global__ void graph_kernel(int G, const double* beta, int64_t* w) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)G * G) return;
     const int d = (int)(i / G), e = (int)(i - (int64_t)d * G);
@@ -37,19 +41,10 @@ __global__ void graph_kernel(int G, const double* beta, int32_t* w) {
         if (!(v >= 0.0)) v = 0.0;
         if (v > kPgWeightMax) v = kPgWeightMax;
     }
-    w[i] = (int32_t)v;
+    w[i] = (int64_t)v;
 }
 
-// The fixed summation tree over v[0..G) (G <= 256); every lane of wavefront 0 returns the sum.
-__device__ double tree_sum(const double* v, int G, int lane) {
-    double t = lane < G ? v[lane] : 0.0;
-    for (int k = 1; k < 4; ++k)
-        if (lane + 64 * k < G) t = t + v[lane + 64 * k];
-    for (int s = 32; s > 0; s >>= 1) t = t + __shfl_xor(t, s, 64);
-    return t;
-}
-
-__global__ void __launch_bounds__(kPgBlock) spectral_kernel(int G, const int32_t* w, int iters, int32_t* order,
+__global__ void __launch_bounds__(kPgBlock) spectral_kernel(int G, const int64_t* w, int iters, int32_t* order,
                                                             double* fiedler) {
     __shared__ double x[kPgBlock], y[kPgBlock], sq[kPgBlock];
     __shared__ double deg[kPgBlock];
@@ -77,9 +72,10 @@ __global__ void __launch_bounds__(kPgBlock) spectral_kernel(int G, const int32_t
             y[d] = (cap - deg[d]) * x[d] + s;
         }
         __syncthreads();
-        if (d < 64) {
-            const double tot = tree_sum(y, G, d);
-            if (d == 0) scal[1] = tot / (double)G;
+        if (d == 0) {
+            double tot = 0.0;
+            for (int e = 0; e < G; ++e) tot = tot + y[e];
+            scal[1] = tot / (double)G;
         }
         __syncthreads();
         double yd = 0.0;
@@ -88,9 +84,10 @@ __global__ void __launch_bounds__(kPgBlock) spectral_kernel(int G, const int32_t
             sq[d] = yd * yd;
         }
         __syncthreads();
-        if (d < 64) {
-            const double tot = tree_sum(sq, G, d);
-            if (d == 0) scal[0] = sqrt(tot);
+        if (d == 0) {
+            double ss = 0.0;
+            for (int e = 0; e < G; ++e) ss = ss + sq[e];
+            scal[0] = sqrt(ss);
         }
         __syncthreads();
         const double nrm = scal[0];
@@ -113,24 +110,41 @@ __device__ __forceinline__ void drain_barrier() {
     __syncthreads();
 }
 
-// Workgroup maximum of a key (every lane receives it).
-__device__ long long block_max(long long v, long long* red) {
+// (gain, pair) ordered by larger gain, then lower pair index; pair kNoPair = none.
+constexpr int kNoPair = 0x7fffffff;
+__device__ __forceinline__ bool better(long long g, int p, long long g2, int p2) {
+    return p != kNoPair && (p2 == kNoPair || g > g2 || (g == g2 && p < p2));
+}
+
+// Workgroup best (gain, pair): every lane receives it.
+__device__ void block_best(long long& g, int& p, long long* redg, int* redp) {
     for (int s = 32; s > 0; s >>= 1) {
-        const long long o = __shfl_xor(v, s, 64);
-        v = o > v ? o : v;
+        const long long og = __shfl_xor(g, s, 64);
+        const int op = __shfl_xor(p, s, 64);
+        if (better(og, op, g, p)) {
+            g = og;
+            p = op;
+        }
     }
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    if ((threadIdx.x & 63) == 0) {
+        redg[threadIdx.x >> 6] = g;
+        redp[threadIdx.x >> 6] = p;
+    }
     __syncthreads();
-    long long m = red[0];
-    for (int k = 1; k < kPgBlock / 64; ++k) m = red[k] > m ? red[k] : m;
+    g = redg[0];
+    p = redp[0];
+    for (int k = 1; k < kPgBlock / 64; ++k)
+        if (better(redg[k], redp[k], g, p)) {
+            g = redg[k];
+            p = redp[k];
+        }
     __syncthreads();
-    return m;
 }
 
 struct PgArgs {
     int G, Kmax, N, L;
     double H, Hkv, B, s_in, s_out;
-    const int32_t* w;        // [G][G]
+    const int64_t* w;        // [G][G]
     const int32_t* order;    // [G] spectral order
     const int32_t* gpu_type;
     const double* mem;       // [T] memory limits
@@ -139,12 +153,40 @@ struct PgArgs {
     uint8_t *assign, *role;  // [G][N], [Kmax][N]
 };
 
+// Exchange GPUs u and v (different groups): the per-GPU group sums follow (a lane per GPU), then
+// lane 0 moves the two GPUs and the groups' memory.  The same call undoes it.
+__device__ void pg_exchange(const PgArgs& a, int u, int v, int* grp, long long* gval, long long* gmem,
+                            const long long* memv) {
+    const int G = a.G, tid = threadIdx.x;
+    const int A = grp[u], B = grp[v];
+    if (tid < G) {
+        const long long wxu = a.w[(int64_t)u * G + tid], wxv = a.w[(int64_t)v * G + tid];
+        gval[tid * kPgMaxK + A] += wxv - wxu;
+        gval[tid * kPgMaxK + B] += wxu - wxv;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        gmem[A] += memv[v] - memv[u];
+        gmem[B] += memv[u] - memv[v];
+        grp[u] = B;
+        grp[v] = A;
+    }
+    __syncthreads();
+}
+
+// Dynamic LDS of partition_kernel: gval[u][k], the sum of w(u, x) over the GPUs x of group k.
+__host__ __device__ inline size_t pg_lds_bytes(int G) { return (size_t)G * kPgMaxK * sizeof(long long); }
+
 __global__ void __launch_bounds__(kPgBlock) partition_kernel(PgArgs a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char pg_sm[];
+    long long* gval = reinterpret_cast<long long*>(pg_sm);  // [G][kPgMaxK]
     __shared__ long long memv[kPgBlock];
     __shared__ int grp[kPgBlock];
-    __shared__ int32_t gval[kPgBlock * kPgMaxK];  // gval[u][k]: sum of w(u, x) over x in group k
+    __shared__ int locked[kPgBlock];
+    __shared__ int su[kPgBlock / 2], sv[kPgBlock / 2];  // a pass's tentative swaps
     __shared__ long long gmem[kPgMaxK];
     __shared__ long long red[kPgBlock / 64];
+    __shared__ int redp[kPgBlock / 64];
     __shared__ int first[kPgMaxK], newid[kPgMaxK], side[kPgMaxK];
     __shared__ long long sw[kPgMaxK * kPgMaxK];
     __shared__ long long cum[kPgBlock];
@@ -197,49 +239,58 @@ __global__ void __launch_bounds__(kPgBlock) partition_kernel(PgArgs a) {
     __syncthreads();
     if (tid < G) atomicAdd((unsigned long long*)&gmem[grp[tid]], (unsigned long long)memv[tid]);
     if (tid < G) {
-        int32_t* row = gval + tid * kPgMaxK;
+        long long* row = gval + tid * kPgMaxK;
         for (int k = 0; k < kPgMaxK; ++k) row[k] = 0;
         for (int x = 0; x < G; ++x) row[grp[x]] += a.w[(int64_t)x * G + tid];
     }
     drain_barrier();
-    // Kernighan-Lin: the best pair swap while one lowers the cut
+    // Kernighan-Lin passes: tentative best swaps on unlocked GPUs (negative gains too), then the
+    // pass's best prefix is kept and the rest undone; passes repeat while one lowers the cut
     const int pairs = G * G;
-    for (int step = 0; step < 2 * G; ++step) {
-        long long key = 0;
-        for (int p = tid; p < pairs; p += kPgBlock) {
-            const int u = p / G, v = p - u * G;
-            if (v <= u) continue;
-            const int A = grp[u], B = grp[v];
-            if (A == B) continue;
-            const long long d0 = gmem[A] - gmem[B];
-            const long long d1 = (gmem[A] - memv[u] + memv[v]) - (gmem[B] - memv[v] + memv[u]);
-            if ((d1 < 0 ? -d1 : d1) > (d0 < 0 ? -d0 : d0)) continue;
-            const long long wuv = a.w[(int64_t)u * G + v];
-            const long long gain = ((long long)gval[u * kPgMaxK + B] - gval[u * kPgMaxK + A] - wuv) +
-                                   ((long long)gval[v * kPgMaxK + A] - gval[v * kPgMaxK + B] - wuv);
-            if (gain > 0) {
-                const long long k2 = gain * 65536 + (65535 - p);  // largest gain, then lowest pair
-                key = k2 > key ? k2 : key;
+    for (int pass = 0; pass < kKlPasses; ++pass) {
+        if (tid < G) locked[tid] = 0;
+        __syncthreads();
+        int n_swaps = 0, kbest = 0;
+        long long run = 0, bestsum = 0;
+        for (;;) {
+            long long bg = 0;
+            int bp = kNoPair;
+            for (int p = tid; p < pairs; p += kPgBlock) {
+                const int u = p / G, v = p - u * G;
+                if (v <= u || locked[u] || locked[v]) continue;
+                const int A = grp[u], B = grp[v];
+                if (A == B) continue;
+                const long long d0 = gmem[A] - gmem[B];
+                const long long d1 = (gmem[A] - memv[u] + memv[v]) - (gmem[B] - memv[v] + memv[u]);
+                if ((d1 < 0 ? -d1 : d1) > (d0 < 0 ? -d0 : d0)) continue;
+                const long long wuv = a.w[(int64_t)u * G + v];
+                const long long gain = (gval[u * kPgMaxK + B] - gval[u * kPgMaxK + A] - wuv) +
+                                       (gval[v * kPgMaxK + A] - gval[v * kPgMaxK + B] - wuv);
+                if (better(gain, p, bg, bp)) {
+                    bg = gain;
+                    bp = p;
+                }
+            }
+            block_best(bg, bp, red, redp);
+            if (bp == kNoPair) break;  // uniform: no admissible pair left
+            const int u = bp / G, v = bp - u * G;
+            pg_exchange(a, u, v, grp, gval, gmem, memv);
+            if (tid == 0) {
+                locked[u] = locked[v] = 1;
+                su[n_swaps] = u;
+                sv[n_swaps] = v;
+            }
+            __syncthreads();
+            ++n_swaps;
+            run += bg;
+            if (run > bestsum) {
+                bestsum = run;
+                kbest = n_swaps;
             }
         }
-        const long long best = block_max(key, red);
-        if (best <= 0) break;  // uniform
-        const int p = 65535 - (int)(best & 65535);
-        const int u = p / G, v = p - u * G;
-        const int A = grp[u], B = grp[v];
-        if (tid < G) {
-            const int32_t wxu = a.w[(int64_t)u * G + tid], wxv = a.w[(int64_t)v * G + tid];
-            gval[tid * kPgMaxK + A] += wxv - wxu;
-            gval[tid * kPgMaxK + B] += wxu - wxv;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            gmem[A] += memv[v] - memv[u];
-            gmem[B] += memv[u] - memv[v];
-            grp[u] = B;
-            grp[v] = A;
-        }
-        __syncthreads();
+        // undo the swaps past the best prefix, last first
+        for (int i = n_swaps - 1; i >= kbest; --i) pg_exchange(a, su[i], sv[i], grp, gval, gmem, memv);
+        if (kbest == 0) break;  // uniform
     }
     // groups numbered by smallest member
     if (tid < kPgMaxK) first[tid] = 1 << 30;
@@ -274,7 +325,8 @@ __global__ void __launch_bounds__(kPgBlock) partition_kernel(PgArgs a) {
     }
     __syncthreads();
     for (int step = 0; step < used * used; ++step) {
-        long long key = 0;
+        long long bg = 0;
+        int bk = kNoPair;
         if (tid < used) {
             const bool blocked = (side[tid] && n1 == 1) || (!side[tid] && n1 == used - 1);
             if (!blocked) {
@@ -284,12 +336,15 @@ __global__ void __launch_bounds__(kPgBlock) partition_kernel(PgArgs a) {
                     const long long s = sw[tid * kPgMaxK + l];
                     gain += side[l] == side[tid] ? s : -s;
                 }
-                if (gain > 0) key = gain * 64 + (63 - tid);  // largest gain, then lowest super node
+                if (gain > 0) {  // largest gain, then lowest super node
+                    bg = gain;
+                    bk = tid;
+                }
             }
         }
-        const long long best = block_max(key, red);
-        if (best <= 0) break;  // uniform
-        const int k = 63 - (int)(best & 63);
+        block_best(bg, bk, red, redp);
+        if (bk == kNoPair) break;  // uniform
+        const int k = bk;
         n1 += side[k] ? -1 : 1;
         __syncthreads();
         if (tid == 0) side[k] ^= 1;
@@ -303,7 +358,7 @@ __global__ void __launch_bounds__(kPgBlock) partition_kernel(PgArgs a) {
 
 }  // namespace
 
-hipError_t launch_spectral(int32_t G, const double* beta, int32_t* w, int32_t iters, int32_t* order, double* fiedler,
+hipError_t launch_spectral(int32_t G, const double* beta, int64_t* w, int32_t iters, int32_t* order, double* fiedler,
                            hipStream_t s) {
     const int64_t cells = (int64_t)G * G;
     hipLaunchKernelGGL(graph_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, s, G, beta, w);
@@ -313,14 +368,22 @@ hipError_t launch_spectral(int32_t G, const double* beta, int32_t* w, int32_t it
     return hipGetLastError();
 }
 
-hipError_t launch_partition(const Problem& p, int32_t* w, const int32_t* order, const uint64_t* rnd, uint8_t* assign,
+hipError_t launch_partition(const Problem& p, int64_t* w, const int32_t* order, const uint64_t* rnd, uint8_t* assign,
                             uint8_t* role, hipStream_t s) {
     const int64_t cells = (int64_t)p.G * p.G;
     hipLaunchKernelGGL(graph_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, s, p.G, p.beta, w);
     PgArgs a{p.G, p.Kmax, p.N, p.L, p.H, p.Hkv, p.B, p.s_in, p.s_out, w, order, p.gpu_type, p.mem, p.T, rnd,
              assign, role};
     prof_mark(kKPartition, false, s);
-    hipLaunchKernelGGL(partition_kernel, dim3((unsigned)p.N), dim3(kPgBlock), 0, s, a);
+    // gval of 255 GPUs (65,280 bytes) takes the workgroup past 64 KB of LDS, which gfx950 allows
+    // (160 KB per workgroup) once the kernel's dynamic limit is raised
+    const size_t lds = pg_lds_bytes(p.G);
+    if (lds > 32 * 1024) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(partition_kernel),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(partition_kernel, dim3((unsigned)p.N), dim3(kPgBlock), lds, s, a);
     prof_mark(kKPartition, true, s);
     return hipGetLastError();
 }

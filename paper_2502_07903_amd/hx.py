@@ -96,7 +96,7 @@ EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_
            "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves",
            "hx_gather_candidates",
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
-           "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_lds_probe", "hx_strerror", "hx_last_error",
+           "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error",
            "hx_abi_version")
 HX_KERNELS = 13
 
@@ -139,7 +139,6 @@ def lib() -> C.CDLL:
         L.hx_profile.restype = C.c_int
         L.hx_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
         L.hx_profile_read.restype = C.c_int
-        L.hx_lds_probe.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_kernel_name.argtypes = [C.c_int32]
         L.hx_kernel_name.restype = C.c_char_p
         L.hx_strerror.restype = C.c_char_p
@@ -153,17 +152,6 @@ def lib() -> C.CDLL:
 def profile(enable: bool) -> None:
     """Diagnostic per-kernel timing: HIP events around every later libhx kernel launch."""
     _check(lib().hx_profile(1 if enable else 0), "hx_profile")
-
-
-def lds_probe(blocks: int, reps: int, sink) -> int:
-    """Enqueues the LDS bandwidth probe on the current stream; returns the bytes it reads.  sink:
-    a device int32/uint32 tensor of blocks * 256 elements (never written)."""
-    if not sink.is_cuda or sink.element_size() != 4 or sink.numel() < blocks * 256:
-        raise ValueError("sink: a device tensor of blocks * 256 32-bit elements")
-    nbytes = C.c_int64(0)
-    _check(lib().hx_lds_probe(int(blocks), int(reps), C.c_void_p(sink.data_ptr()), C.byref(nbytes), _stream()),
-           "hx_lds_probe")
-    return int(nbytes.value)
 
 
 def profile_read() -> Dict[str, Tuple[float, int]]:

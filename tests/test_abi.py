@@ -206,19 +206,6 @@ def test_workspace_and_mask_sizes():
     assert L.hx_cost_workspace_bytes(8, 16, 1000) >= 8 * 8 * 1000
 
 
-def test_lds_probe_rejects_bad_arguments():
-    """The probe validates on the host before any HIP call."""
-    L = hx.lib()
-    n = C.c_int64(-1)
-    fake = C.c_void_p(0x1000)
-    assert L.hx_lds_probe(0, 1, fake, C.byref(n), None) == hx.HX_EINVAL
-    assert L.hx_lds_probe(1, 0, fake, C.byref(n), None) == hx.HX_EINVAL
-    assert L.hx_lds_probe((1 << 20) + 1, 1, fake, C.byref(n), None) == hx.HX_EINVAL
-    assert L.hx_lds_probe(1, 1, None, C.byref(n), None) == hx.HX_EINVAL
-    assert L.hx_lds_probe(1, 1, fake, None, None) == hx.HX_EINVAL
-    assert n.value == -1
-
-
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(hx, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(hx, "_lib", None)

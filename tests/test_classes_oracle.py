@@ -190,10 +190,9 @@ def test_kv_mix_per_gpu_nodes():
                 kp, kd = int(prob.assign[g, n]), int(prob.assign[h, n])
                 if cost["tp"][kp, n] == 0 or cost["tp"][kd, n] == 0:
                     continue
-                szp = int((prob.assign[:, n] == kp).sum())
                 t = 0.0
                 for s_in, s_out, w in cls:
-                    t = t + w * hxo.kv_gpu_time(_single(prob, s_in, s_out), g, h, szp)
+                    t = t + w * hxo.kv_gpu_time(_single(prob, s_in, s_out), g, h)
                 assert f["kv_cap"][i * nd + j, n] == hxo.quantize(1000.0 / t)
                 checked += 1
     assert checked > 10

@@ -516,16 +516,6 @@ def test_exhaustive_search_best():
     assert got["best"] == want["best"]
 
 
-def test_lds_probe(torch):
-    """The LDS probe reads what it reports (16-byte words, eight per round per lane) and writes
-    nothing to its sink."""
-    sink = torch.zeros(3 * 256, dtype=torch.int32, device="cuda")
-    nbytes = hx.lds_probe(3, 5, sink)
-    torch.cuda.synchronize()
-    assert nbytes == 3 * 256 * 16 * 8 * 5
-    assert int(sink.abs().sum()) == 0
-
-
 def test_profile_counts_each_kernel(torch):
     """The diagnostic per-kernel timing sees every kernel of one pass exactly once, with a
     positive duration, and records nothing once disabled."""

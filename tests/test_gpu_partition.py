@@ -1,7 +1,8 @@
 """GPU parity of the graph-partition phase (Sec. 3.2) through the C-ABI: the spectral vector
 and order, and every candidate's assignment and roles, against the oracle on the same seeded
 inputs.  The spectral step is binary64 in the same order on both sides, so the vector must be
-bit-identical; everything after it is integer work and must be bit-exact."""
+bit-identical; everything after it (memory-balanced cut, Kernighan-Lin passes, coarsening and
+the max-cut split) is integer work and must be bit-exact."""
 import dataclasses
 import os
 import sys
@@ -63,7 +64,10 @@ def test_partition_candidates_parity(torch, cfg, n):
     say(f"partition candidates: workload {cfg}, N={n}")
     hx.partition_candidates(dp, ws, order, rnd, assign, role)
     torch.cuda.synchronize()
-    want_a, want_r = hxo.partition_candidates(prob, order.cpu().numpy(), rnd_h)
+    # the oracle runs from its own spectral order (equal to the GPU's, checked here as well)
+    want_o, _ = hxo.spectral_order(prob, 1000)
+    assert np.array_equal(order.cpu().numpy(), want_o)
+    want_a, want_r = hxo.partition_candidates(prob, want_o, rnd_h)
     got_a, got_r = assign.cpu().numpy(), role.cpu().numpy()
     bad = np.flatnonzero((got_a != want_a).any(0) | (got_r != want_r).any(0))
     assert bad.size == 0, f"candidates differ: {bad[:8].tolist()}"
@@ -86,3 +90,31 @@ def test_partition_then_score(torch):
     want = hxo.score_batch(p2, n_threads=N_THREADS)
     assert np.array_equal(wsc.flow_value.cpu().numpy(), want["flow_value"])
     assert tuple(int(x) for x in wsc.best.cpu().numpy()) == want["best"]
+
+
+def test_partition_large_weights(torch):
+    """Links far faster than any real one (up to 1e21 bytes/s, past the 2^47 MB/s clamp): the
+    weights, cuts and gains are 64-bit integers on both sides, so the order and the candidates
+    still match bit for bit."""
+    prob = I.make_problem(2, n_cand=1)
+    G = prob.n_gpus
+    beta = np.asarray(prob.cluster.beta, np.float64).reshape(G, G) * 1e6
+    beta[0, 5] = beta[5, 0] = 1e21
+    beta[3, 9] = 3e20
+    cl = dataclasses.replace(prob.cluster, beta=np.ascontiguousarray(beta.reshape(-1)))
+    prob = dataclasses.replace(prob, cluster=cl)
+    n = 256
+    say(f"partition with large weights: N={n}")
+    dp, ws, order, fied = _spectral(torch, prob, 1000)
+    want_o, want_x = hxo.spectral_order(prob, 1000)
+    assert np.array_equal(fied.cpu().numpy(), want_x)
+    assert np.array_equal(order.cpu().numpy(), want_o)
+    rnd_h = I.partition_draws(2, n)
+    rnd = torch.as_tensor(rnd_h.view(np.int64)).to("cuda")
+    assign = torch.full((G, n), 0xEE, dtype=torch.uint8, device="cuda")
+    role = torch.full((prob.max_groups, n), 0xEE, dtype=torch.uint8, device="cuda")
+    hx.partition_candidates(dp, ws, order, rnd, assign, role)
+    torch.cuda.synchronize()
+    want_a, want_r = hxo.partition_candidates(prob, want_o, rnd_h)
+    assert np.array_equal(assign.cpu().numpy(), want_a)
+    assert np.array_equal(role.cpu().numpy(), want_r)

@@ -8,21 +8,26 @@ weights (not the oracle's gain bookkeeping): the number of groups follows K = fl
 memory / replica memory) shifted by the draw; no Kernighan-Lin swap that keeps the two groups'
 memory gap from widening lowers the cut (a local optimum); no single flip of a super node
 raises the coarse cut while both sides stay occupied; groups are numbered by smallest member;
-both roles are present.
+both roles are present.  Kernighan-Lin: a hand-derived case (tests/golden/kl_worked.txt) where
+no single swap lowers the cut but a pass that first takes a swap of negative gain does, reaching
+the smallest cut of all balanced splits (brute force); on random graphs the refinement never
+raises the cut and ends at a local optimum of single swaps.
 """
 import dataclasses
+import itertools
 
 import numpy as np
 import pytest
 
 from oracle import hxo
 from paper_2502_07903_amd import inputs as I
+from tests import helpers as Hh
 
 
 def _weights(prob):
     G = prob.n_gpus
     b = np.asarray(prob.cluster.beta, np.float64).reshape(G, G)
-    w = np.clip(np.floor(((b + b.T) * 0.5) / 1e6), 0, 2 ** 23).astype(np.int64)
+    w = np.clip(np.floor(((b + b.T) * 0.5) / 1e6), 0, 2 ** 47).astype(np.int64)
     np.fill_diagonal(w, 0)
     return w
 
@@ -120,3 +125,80 @@ def test_partition_candidates_are_local_optima(cfg, n):
             if len(set(s2.tolist())) < 2:
                 continue
             assert int((S * (s2[:, None] != s2[None, :])).sum()) <= cut0
+
+
+def _graph_problem(w, mem=None):
+    """A cluster whose device-graph weights are exactly w (whole MB/s): beta = (w + 1/2) MB/s."""
+    G = w.shape[0]
+    beta = (w.astype(np.float64) + 0.5) * 1e6
+    np.fill_diagonal(beta, 0.0)
+    mem = np.full(G, 80e9) if mem is None else np.asarray(mem, np.float64)
+    types, gpu_type = np.unique(mem, return_inverse=True)
+    T = len(types)
+    cl = I.Cluster(gpu_type.astype(np.int32), np.full(T, 312e12), np.full(T, 2e12), types.astype(np.float64),
+                   np.ascontiguousarray(beta.reshape(-1)), np.zeros(G * G))
+    a = np.zeros((G, 1), np.uint8)
+    r = np.zeros((1, 1), np.uint8)
+    return Hh.problem(cl, Hh.MODELS["opt30b"], a, r)
+
+
+def _swap_gains(w, grp, mem):
+    """Cut change of every balance-keeping single swap, from explicit cuts."""
+    base = _cut(w, grp)
+    gmem = {k: int(mem[grp == k].sum()) for k in set(grp.tolist())}
+    out = []
+    for u in range(len(grp)):
+        for v in range(u + 1, len(grp)):
+            A, B = grp[u], grp[v]
+            if A == B:
+                continue
+            if abs((gmem[A] - mem[u] + mem[v]) - (gmem[B] - mem[v] + mem[u])) > abs(gmem[A] - gmem[B]):
+                continue
+            g2 = grp.copy()
+            g2[u], g2[v] = B, A
+            out.append(base - _cut(w, g2))
+    return out
+
+
+def test_kl_worked_case():
+    case = Hh.parse_golden("kl_worked.txt")[0]
+    w = np.array([Hh.ints(row) for row in case["weights"].split(";")], np.int64)
+    assert (w == w.T).all()
+    prob = _graph_problem(w)
+    assert np.array_equal(_weights(prob), w)
+    start = np.array(Hh.ints(case["start"]), np.int64)
+    mem = np.full(len(start), 80_000_000_000, np.int64)
+    assert _cut(w, start) == int(case["start_cut"])
+    assert max(_swap_gains(w, start, mem)) == int(case["best_single_swap_gain"])  # greedy stops here
+    got, passes = hxo.kl_refine(prob, start)
+    assert got.tolist() == Hh.ints(case["result"])
+    assert _cut(w, got.astype(np.int64)) == int(case["result_cut"])
+    assert passes == int(case["improving_passes"])
+    best = min(_cut(w, np.array([0 if i in S else 1 for i in range(8)])) for S in itertools.combinations(range(8), 4))
+    assert best == int(case["result_cut"])
+
+
+def test_kl_random_graphs():
+    """Random weighted graphs, groups and memories: the refined grouping keeps the group sizes'
+    memory balance rule (no swap it made widened a gap, so no group is emptied), never has a
+    larger cut than the start, and no single balance-keeping swap lowers its cut."""
+    rng = np.random.default_rng(3502)
+    improved = 0
+    for trial in range(60):
+        G = int(rng.integers(4, 13))
+        K = int(rng.integers(2, min(G, 4) + 1))
+        w = rng.integers(0, 50, (G, G))
+        w = np.triu(w, 1)
+        w = w + w.T
+        mem = rng.choice([16e9, 24e9, 80e9], G)
+        prob = _graph_problem(w, mem)
+        start = np.arange(G) % K
+        rng.shuffle(start)
+        got, _ = hxo.kl_refine(prob, start)
+        got = got.astype(np.int64)
+        memi = mem.astype(np.int64)
+        assert sorted(set(got.tolist())) == sorted(set(start.tolist()))
+        assert _cut(w, got) <= _cut(w, start)
+        assert max(_swap_gains(w, got, memi), default=0) <= 0
+        improved += _cut(w, got) < _cut(w, start)
+    assert improved > 20
