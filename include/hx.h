@@ -202,6 +202,22 @@ int hx_cost_eval(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_s
  * aligned, contents ignored on entry.  Calls that share a workspace must not overlap. */
 size_t hx_cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc): hx_cost_eval without the workspace argument.  Its scratch is
+ * a static device array of HX_STATIC_SCRATCH_BYTES in libhx, one per GPU, resident from the
+ * first call on that GPU until the process ends; the call allocates nothing.  Same arguments
+ * (but the workspace), results and errors as hx_cost_eval, plus HX_ETOOBIG when the batch needs
+ * more scratch than that (hx_cost_workspace_bytes(n_gpus, max_groups, n_cand) >
+ * HX_STATIC_SCRATCH_BYTES; 17 bytes per group slot, n_cand * min(max_groups, n_gpus), at up to
+ * 64 GPUs, so about 1.9 million slots: 65,536 candidates of 32 GPUs and 16 groups take 17.3 MB,
+ * and 262,144 candidates of 64 GPUs and 32 groups are refused).  Every call on a GPU uses that GPU's one array: calls
+ * that overlap on one GPU (two streams, two host threads) race and must be serialised by the
+ * caller.  The scratch needs no clearing between calls.  The caller's device must be current. */
+#define HX_STATIC_SCRATCH_BYTES (32u << 20)
+int hx_cost_eval_static(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
+                        const hx_candidates *cand, const hx_cost_out *out, hipStream_t stream);
+size_t hx_static_scratch_bytes(void);
+
 /* 64-bit words per GPU bitmask: 1 for n_gpus <= 64, 2 for <= 128, 4 for <= 255. */
 int hx_member_words(int32_t n_gpus);
 

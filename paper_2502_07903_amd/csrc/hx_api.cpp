@@ -6,7 +6,14 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "hx_internal.h"
+
+// The scratch of hx_cost_eval_static: one copy per GPU, held until the process ends.  In host
+// code this name is only a stand-in for the symbol; its device address comes from
+// hipGetSymbolAddress (scratch_address below), and only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[HX_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -265,7 +272,7 @@ const char* hx_strerror(int code) {
     switch (code) {
         case HX_OK: return "ok";
         case HX_EINVAL: return "invalid argument";
-        case HX_ETOOBIG: return "flow network exceeds the max-flow kernel's LDS plan";
+        case HX_ETOOBIG: return "problem exceeds the max-flow kernel's LDS plan or the static scratch";
         case HX_EHIP: return "HIP launch error (see hx_last_error)";
         case HX_ENOCONV: return "max-flow did not converge within its round budget";
         default: return "unknown error";
@@ -301,6 +308,47 @@ int hx_cost_eval(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_s
         workspace_bytes < hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand))
         return HX_EINVAL;
     hipError_t e = hx::launch_cost(make_problem(cluster, model, wl, space, cand), make_cost(out), workspace, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
+namespace {
+
+// Device address of `scratch` on each device, looked up once per device (with that device
+// current) on the first hx_cost_eval_static call there.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_error(e);
+    if (dev < 0 || dev >= kMaxDevices) return HX_EINVAL;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_error(e);
+        if (!p) return HX_EINVAL;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return HX_OK;
+}
+
+}  // namespace
+
+size_t hx_static_scratch_bytes(void) { return HX_STATIC_SCRATCH_BYTES; }
+
+int hx_cost_eval_static(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
+                        const hx_candidates* cand, const hx_cost_out* out, hipStream_t stream) {
+    int rc = check_problem(cluster, model, wl, space, cand);
+    if (rc || (rc = check_cost(out))) return rc;
+    if (hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) > HX_STATIC_SCRATCH_BYTES)
+        return HX_ETOOBIG;
+    void* ws = nullptr;
+    if ((rc = scratch_address(&ws))) return rc;
+    hipError_t e = hx::launch_cost(make_problem(cluster, model, wl, space, cand), make_cost(out), ws, stream);
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

@@ -92,7 +92,7 @@ class hx_flownet(C.Structure):
                 ("sink_cap", C.c_void_p)]
 
 
-EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
+EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_eval_static", "hx_static_scratch_bytes", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
            "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves",
            "hx_gather_candidates",
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
@@ -115,6 +115,9 @@ def lib() -> C.CDLL:
                                   P(hx_cost_out), P(hx_flownet)]
         L.hx_cost_eval.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
                                    P(hx_cost_out), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.hx_cost_eval_static.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
+                                          P(hx_cost_out), C.c_void_p]
+        L.hx_static_scratch_bytes.restype = C.c_size_t
         L.hx_cost_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32]
         L.hx_cost_workspace_bytes.restype = C.c_size_t
         L.hx_member_words.argtypes = [C.c_int32]
@@ -340,6 +343,14 @@ def cost_eval(dp: DeviceProblem, out: CostBuffers, stream=None) -> CostBuffers:
     _check(lib().hx_cost_eval(C.byref(dp.cluster), dp.model, dp.workload, dp.space, C.byref(dp.cand), C.byref(o),
                               _ptr(out.workspace), C.c_size_t(int(out.workspace.numel())), _stream(stream)),
            "hx_cost_eval")
+    return out
+
+
+def cost_eval_static(dp: DeviceProblem, out: CostBuffers, stream=None) -> CostBuffers:
+    """hx_cost_eval_static: the cost model with libhx's static scratch (out.workspace unused)."""
+    o = out.struct()
+    _check(lib().hx_cost_eval_static(C.byref(dp.cluster), dp.model, dp.workload, dp.space, C.byref(dp.cand),
+                                     C.byref(o), _stream(stream)), "hx_cost_eval_static")
     return out
 
 

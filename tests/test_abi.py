@@ -121,6 +121,22 @@ def test_validate_too_big_for_lds():
     assert _validate(*a) == hx.HX_ETOOBIG
 
 
+def test_cost_eval_static_refuses_before_any_device_work():
+    """The entry point that allocates nothing refuses, on the host and before any HIP call, a
+    batch whose scratch exceeds its static array (262,144 candidates of 64 GPUs and 32 groups
+    need 137 MB), and invalid arguments as hx_cost_eval does."""
+    L = hx.lib()
+    assert L.hx_static_scratch_bytes() == 32 << 20
+    cl, md, wl, sp, cand, cost, net = _args(G=64, T=5, N=262144, Kmax=32)
+    assert L.hx_cost_workspace_bytes(64, 32, 262144) > L.hx_static_scratch_bytes()
+    assert L.hx_cost_eval_static(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None) == hx.HX_ETOOBIG
+    cand.n_cand = 0
+    assert L.hx_cost_eval_static(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None) == hx.HX_EINVAL
+    cand.n_cand = 1000
+    cost.lat = None
+    assert L.hx_cost_eval_static(C.byref(cl), md, wl, sp, C.byref(cand), C.byref(cost), None) == hx.HX_EINVAL
+
+
 def test_calls_reject_before_any_device_work():
     cl, md, wl, sp, cand, cost, net = _args()
     cand.n_cand = 0
