@@ -118,7 +118,8 @@ typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; uint32
  * stage (an alternative reading of Appendix A's decode capacity). */
 #define HX_VARIANT_PIPELINED 1u
 /* KV stage-order search (Appendix A, edge capacity estimation): each KV edge's time is
- * minimised over the stage orders of both replicas (see hx_build_flownet). */
+ * minimised over the stage orders of both replicas, pipelines of up to 8 stages (see
+ * hx_build_flownet). */
 #define HX_VARIANT_KV_ORDER 2u
 /* Asymmetric layer split (HexGen's asymmetric parallelism; Table 1 leaves l_j open): every
  * stage holds one layer plus its compute's share of the other L - pp (see hx_cost_eval).  Not
@@ -236,8 +237,8 @@ int hx_member_words(int32_t n_gpus);
  * replicas on that link), whatever the replicas' sizes; 0 when either replica is infeasible.
  * With space.variant & HX_VARIANT_KV_ORDER (granularity 0), pipeline position a of a replica
  * may be served by any of its stages (stage s = the members ranked s*tp .. s*tp+tp-1): the
- * KV time is the minimum over every pair of stage orders of the two replicas when there are
- * at most 720 such pairs (pp_p! * pp_d! <= 720), else the ascending orders'.  With request
+ * KV time is the minimum over every pair of stage orders of the two replicas (exact for
+ * pipelines of up to 8 stages; with this variant a pp_mask bit past 8 is HX_EINVAL).  With request
  * classes (wl.n_classes > 0) the KV time is sum_k w_k t_k, t_k the time above with s_in =
  * cls_in[k] (left to right in class order), at either granularity. */
 int hx_build_flownet(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,

@@ -112,6 +112,15 @@ static int classes_ok(const hxo_workload *w, uint32_t variant)
     return 1;
 }
 
+/* Variants the oracle reads: request classes as above, and the stage-order search on pipelines of
+ * up to 8 stages (the PP mask past 8 is refused with it). */
+static int space_ok(const hxo_workload *w, const hxo_space *sp)
+{
+    if (!classes_ok(w, sp->variant)) return 0;
+    if ((sp->variant & HXO_VARIANT_KV_ORDER) && (sp->pp_mask >> 8)) return 0;
+    return 1;
+}
+
 /* ------------------------------------------------------------------ helpers */
 
 static double flops_of(const hxo_cluster *c, int d) { return c->type_flops[c->gpu_type[d]]; }
@@ -438,34 +447,143 @@ static int next_order(int *v, int n)
     return 1;
 }
 
-static long order_count(int pp)
+/* KV time with explicit stage orders (ord_p[a]: the prefill stage serving pipeline position a;
+ * ord_d likewise), the uniform layer split. */
+double hxo_kv_time_orders(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                          const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *ord_p,
+                          const int32_t *dm, int32_t dtp, int32_t dpp, const int32_t *ord_d)
 {
-    long f = 1;
-    for (int k = 2; k <= pp; k++) f *= k;
-    return f;
+    int op[HXO_MAX_PP], od[HXO_MAX_PP];
+    for (int a = 0; a < ppp; a++) op[a] = ord_p[a];
+    for (int b = 0; b < dpp; b++) od[b] = ord_d[b];
+    return kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od, NULL, NULL);
+}
+
+/* Slowest link between prefill stage s and decode stage t when they serve pipeline positions
+ * sharing nab > 0 layers: the link times kv_time_ordered visits for that pair of positions. */
+static double kv_block_time(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
+                            const int32_t *pm, int ptp, int s, const int32_t *dm, int dtp, int t, int nab)
+{
+    const double V1 = 2.0 * w->s_in * kv_hidden(m) * (double)m->bytes_per_elem;
+    double worst = 0.0;
+    for (int r = 0; r < ptp; r++)
+        for (int q = 0; q < dtp; q++) {
+            int hi = (r + 1) * dtp < (q + 1) * ptp ? (r + 1) * dtp : (q + 1) * ptp;
+            int lo = r * dtp > q * ptp ? r * dtp : q * ptp;
+            int ov = hi - lo;
+            if (ov <= 0) continue;
+            int g = pm[s * ptp + r], h = dm[t * dtp + q];
+            double bytes = ((V1 * (double)nab) * (double)ov) / (double)(ptp * dtp);
+            double time = alpha_of(c, g, h) + bytes / beta_of(c, g, h);
+            if (time > worst) worst = time;
+        }
+    return worst;
+}
+
+/* Kuhn's augmenting path from row i over the entries of C (n x n) that are <= T. */
+static int kuhn_augment(const double *C, int n, double T, int i, int *row_of_col, int *seen)
+{
+    for (int j = 0; j < n; j++) {
+        if (C[i * n + j] > T || seen[j]) continue;
+        seen[j] = 1;
+        if (row_of_col[j] < 0 || kuhn_augment(C, n, T, row_of_col[j], row_of_col, seen)) {
+            row_of_col[j] = i;
+            return 1;
+        }
+    }
+    return 0;
+}
+
+static int perfect_matching_below(const double *C, int n, double T)
+{
+    int row_of_col[HXO_MAX_PP], seen[HXO_MAX_PP];
+    for (int j = 0; j < n; j++) row_of_col[j] = -1;
+    for (int i = 0; i < n; i++) {
+        for (int j = 0; j < n; j++) seen[j] = 0;
+        if (!kuhn_augment(C, n, T, i, row_of_col, seen)) return 0;
+    }
+    return 1;
+}
+
+/* Linear bottleneck assignment: the smallest over permutations pi of max_i C[i][pi(i)].  The
+ * value is one of C's entries, so the entries are tried in ascending order and the first one
+ * whose entries <= it admit a perfect matching is the answer. */
+static double bottleneck_assignment(const double *C, int n)
+{
+    double v[HXO_MAX_PP * HXO_MAX_PP];
+    const int k = n * n;
+    for (int i = 0; i < k; i++) v[i] = C[i];
+    for (int i = 1; i < k; i++) {  /* insertion sort */
+        double x = v[i];
+        int j = i - 1;
+        while (j >= 0 && v[j] > x) { v[j + 1] = v[j]; j--; }
+        v[j + 1] = x;
+    }
+    for (int i = 0; i < k; i++) {
+        if (i > 0 && v[i] == v[i - 1]) continue;
+        if (perfect_matching_below(C, n, v[i])) return v[i];
+    }
+    return v[k - 1];
 }
 
 /* Stage-order search (Appendix A, "Edge capacity estimation": the pipeline stage order of both
  * replicas is adjusted to minimise the KV cache communication cost, which sets the edge
- * capacity).  The KV time is minimised over every pair of stage orders when there are at most
- * HXO_ORDER_PAIRS of them (ppp! * dpp!); deeper pairs of pipelines keep the ascending orders.
- * Node capacities are not affected (they keep the ascending order). */
-#define HXO_ORDER_PAIRS 720
+ * capacity): the smallest KV time over every pair of stage orders.  Node capacities keep the
+ * ascending order.
+ *
+ * The KV time of an order pair is the largest block time over the pairs of pipeline positions
+ * that share layers (a block: the slowest link between the stages serving the two positions).
+ * Fix the order of one side X; each position y of the other side Y then contributes
+ * C[y][t] = max over the X positions sharing layers with y of the block time, when Y's stage t
+ * serves y, and the KV time is max_y C[y][ord_Y(y)].  So the best Y order for a fixed X order
+ * is a bottleneck assignment of C, and the minimum over both orders is the minimum over the X
+ * orders of that assignment's value: every order pair is covered, none is visited one by one.
+ * X is the pipeline with fewer stages (prefill on ties); its orders are enumerated in
+ * lexicographic order (at most 8! = 40,320). */
 double hxo_kv_time_best(const hxo_cluster *c, const hxo_model *m, const hxo_workload *w,
                         const int32_t *pm, int32_t ptp, int32_t ppp, const int32_t *dm, int32_t dtp, int32_t dpp)
 {
-    if (order_count(ppp) * order_count(dpp) > HXO_ORDER_PAIRS)
-        return hxo_kv_time(c, m, w, pm, ptp, ppp, dm, dtp, dpp);
-    int op[HXO_MAX_PP], od[HXO_MAX_PP];
-    for (int a = 0; a < ppp; a++) op[a] = a;
+    const int L = m->n_layers;
+    const int swap = dpp < ppp;  /* X = decode when it has fewer stages */
+    const int nx = swap ? dpp : ppp, ny = swap ? ppp : dpp;
+    int xb[HXO_MAX_PP + 1], yb[HXO_MAX_PP + 1];  /* layer boundaries of the positions */
+    xb[0] = yb[0] = 0;
+    for (int a = 0; a < nx; a++) xb[a + 1] = xb[a] + stage_layers(L, nx, a);
+    for (int b = 0; b < ny; b++) yb[b + 1] = yb[b] + stage_layers(L, ny, b);
+    /* blk[((xa * nx + xs) * ny + y) * ny + yt]: X position xa served by X stage xs, Y position y by
+     * Y stage yt; -1 where the two positions share no layer */
+    double *blk = (double *)malloc(sizeof(double) * nx * nx * ny * ny);
+    for (int xa = 0; xa < nx; xa++)
+        for (int y = 0; y < ny; y++) {
+            const int lo = xb[xa] > yb[y] ? xb[xa] : yb[y];
+            const int hi = xb[xa + 1] < yb[y + 1] ? xb[xa + 1] : yb[y + 1];
+            for (int xs = 0; xs < nx; xs++)
+                for (int yt = 0; yt < ny; yt++) {
+                    double v = -1.0;
+                    if (hi > lo)
+                        v = swap ? kv_block_time(c, m, w, pm, ptp, yt, dm, dtp, xs, hi - lo)
+                                 : kv_block_time(c, m, w, pm, ptp, xs, dm, dtp, yt, hi - lo);
+                    blk[((xa * nx + xs) * ny + y) * ny + yt] = v;
+                }
+        }
+    int ord[HXO_MAX_PP];
+    double C[HXO_MAX_PP * HXO_MAX_PP];
+    for (int a = 0; a < nx; a++) ord[a] = a;
     double best = -1.0;
     do {
-        for (int b = 0; b < dpp; b++) od[b] = b;
-        do {
-            double t = kv_time_ordered(c, m, w, pm, ptp, ppp, op, dm, dtp, dpp, od, NULL, NULL);
-            if (best < 0.0 || t < best) best = t;
-        } while (next_order(od, dpp));
-    } while (next_order(op, ppp));
+        for (int y = 0; y < ny; y++)
+            for (int yt = 0; yt < ny; yt++) {
+                double v = 0.0;
+                for (int xa = 0; xa < nx; xa++) {
+                    const double b = blk[((xa * nx + ord[xa]) * ny + y) * ny + yt];
+                    if (b > v) v = b;
+                }
+                C[y * ny + yt] = v;
+            }
+        const double t = bottleneck_assignment(C, ny);
+        if (best < 0.0 || t < best) best = t;
+    } while (next_order(ord, nx));
+    free(blk);
     return best;
 }
 
@@ -526,7 +644,7 @@ int hxo_cost_eval(const hxo_cluster *c, const hxo_model *m, const hxo_workload *
                   int32_t n_cand, int32_t max_groups, const uint8_t *assign, const uint8_t *role,
                   uint8_t *tp, uint8_t *pp, int32_t *bmax, int32_t *cap, double *lat)
 {
-    if (!classes_ok(w, sp->variant)) return -1;
+    if (!space_ok(w, sp)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     cost_range(&bt, 0, n_cand, tp, pp, bmax, cap, lat);
     return 0;
@@ -676,7 +794,7 @@ int hxo_build_flownet(const hxo_cluster *c, const hxo_model *m, const hxo_worklo
                       int32_t *n_p, int32_t *n_d, int32_t *p_slot, int32_t *d_slot,
                       int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap)
 {
-    if (!classes_ok(w, sp->variant)) return -1;
+    if (!space_ok(w, sp)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
     flownet_range(&bt, 0, n_cand, tp, pp, cap, &f);
@@ -885,7 +1003,7 @@ int hxo_score_batch(const hxo_cluster *c, const hxo_model *m, const hxo_workload
                     int32_t *src_cap, int32_t *p_cap, int32_t *kv_cap, int32_t *d_cap, int32_t *sink_cap,
                     int32_t *flow_value, int32_t *best, int32_t n_threads)
 {
-    if (!classes_ok(w, sp->variant)) return -1;
+    if (!space_ok(w, sp)) return -1;
     hxo_batch bt = {c, m, w, sp, n_cand, max_groups, assign, role};
     hxo_flownet f = {max_p, max_d, max_pd, n_p, n_d, p_slot, d_slot, src_cap, p_cap, kv_cap, d_cap, sink_cap};
     if (n_threads < 1) n_threads = 1;

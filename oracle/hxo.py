@@ -79,6 +79,7 @@ def lib():
         _lib.hxo_maxflow_edges.restype = C.c_int64
         _lib.hxo_kv_time.restype = C.c_double
         _lib.hxo_kv_time_best.restype = C.c_double
+        _lib.hxo_kv_time_orders.restype = C.c_double
         _lib.hxo_kv_gpu_time.restype = C.c_double
         _lib.hxo_quantize.restype = C.c_int32
     return _lib
@@ -242,6 +243,17 @@ def kv_time(prob, pm: Sequence[int], ptp: int, ppp: int, dm: Sequence[int], dtp:
     fn = lib().hxo_kv_time_best if best_order else lib().hxo_kv_time
     return fn(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(p), C.c_int32(ptp),
               C.c_int32(ppp), _p(d), C.c_int32(dtp), C.c_int32(dpp))
+
+
+def kv_time_orders(prob, pm: Sequence[int], ptp: int, ppp: int, ord_p: Sequence[int], dm: Sequence[int], dtp: int,
+                   dpp: int, ord_d: Sequence[int]) -> float:
+    """KV time of one request with explicit stage orders (ord_p[a]: the prefill stage serving
+    pipeline position a; ord_d likewise)."""
+    a = _Args(prob)
+    arr = lambda v: np.ascontiguousarray(np.asarray(v, np.int32))
+    p, d, op, od = arr(pm), arr(dm), arr(ord_p), arr(ord_d)
+    return lib().hxo_kv_time_orders(C.byref(a.cluster), C.byref(a.model), C.byref(a.wl), _p(p), C.c_int32(ptp),
+                                    C.c_int32(ppp), _p(op), _p(d), C.c_int32(dtp), C.c_int32(dpp), _p(od))
 
 
 def kv_gpu_time(prob, g: int, h: int) -> float:

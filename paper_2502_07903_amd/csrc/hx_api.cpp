@@ -47,6 +47,8 @@ int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, 
     if (s.granularity != 0 && s.granularity != 1) return HX_EINVAL;
     if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM)) return HX_EINVAL;
     if ((s.variant & HX_VARIANT_KV_ORDER) && (s.variant & HX_VARIANT_ASYM)) return HX_EINVAL;
+    // the stage-order search covers pipelines of up to 8 stages
+    if ((s.variant & HX_VARIANT_KV_ORDER) && (s.pp_mask >> 8)) return HX_EINVAL;
     if (k->n_cand < 1 || k->max_groups < 1 || k->max_groups > HX_MAX_GROUPS || !k->assign || !k->role)
         return HX_EINVAL;
     return HX_OK;

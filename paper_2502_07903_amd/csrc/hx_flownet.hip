@@ -252,10 +252,24 @@ __device__ double kv_time_classes(const Problem& p, const uint8_t* pm, int ptp, 
 }
 
 // KV stage-order search (HX_VARIANT_KV_ORDER; Appendix A, edge capacity estimation): the stage
-// order of both replicas is chosen to minimise the KV time.  Orders are packed 4 bits per
-// pipeline position (position a is served by stage (ord >> 4a) & 15); pairs of pipelines with
-// more than kOrderPairs order pairs keep the ascending orders.
-constexpr int kOrderPairs = 720;
+// orders of both replicas are chosen to minimise the KV time, over every pair of orders.
+//
+// The KV time of an order pair is the largest block time over the pairs of pipeline positions
+// that share layers (a block: the slowest link between the two stages serving the positions).
+// With the order of one side X fixed, each position y of the other side Y contributes
+// C[y][t] = max over the X positions sharing layers with y of the block time when Y's stage t
+// serves y, and the KV time is max_y C[y][ord_Y(y)]; the best Y order is a bottleneck
+// assignment of C.  So the search enumerates the orders of X, the side with fewer stages
+// (prefill on ties; at most 8! = 40,320), and solves one bottleneck assignment per order: the
+// smallest threshold T, among C's entries, under which a perfect matching of positions to
+// stages exists.  Orders are packed 4 bits per pipeline position (position a is served by stage
+// (ord >> 4a) & 15).  Pipelines of up to 8 stages (the PP mask is validated).
+constexpr int kOrderStages = 8;
+constexpr int kBlockPairs = 2 * kOrderStages - 1;  // position pairs sharing layers, at most
+// LDS of kv_order_kernel before the member lists: the block table [pair][xs][yt] (doubles), then
+// the pairs' X position, Y position and shared layers, and the first pair of each Y position.
+constexpr size_t kOrderLds = sizeof(double) * kBlockPairs * kOrderStages * kOrderStages +
+                             sizeof(int32_t) * (3 * kBlockPairs + kOrderStages + 1);
 
 __device__ __forceinline__ int order_count(int pp) {
     int f = 1;
@@ -265,56 +279,7 @@ __device__ __forceinline__ int order_count(int pp) {
 
 __device__ __forceinline__ int nib(uint32_t v, int i) { return (int)((v >> (4 * i)) & 15u); }
 
-// kv_time with stage orders: position a of the prefill pipeline is served by its stage
-// nib(op, a), position b of the decode pipeline by stage nib(od, b).  The walk stops once a
-// link reaches `cutoff` (the time returned is then >= cutoff, which the search discards).
-__device__ double kv_time_ord(const Problem& p, const uint8_t* pm, int ptp, int ppp, uint32_t op, const uint8_t* dm,
-                              int dtp, int dpp, uint32_t od, int stride, double cutoff) {
-    const double V1 = 2.0 * p.s_in * p.Hkv * p.B;
-    const int deni = ptp * dtp;
-    const double den = (double)deni;
-    const bool pow2 = (deni & (deni - 1)) == 0;
-    const double inv_den = 1.0 / den;
-    const int lqp = p.L / ppp, lrp = p.L % ppp, lqd = p.L / dpp, lrd = p.L % dpp;
-    double worst = 0.0;
-    int a = 0, bb = 0, a0 = 0, b0 = 0;
-    int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
-    while (a < ppp && bb < dpp) {
-        const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
-        const double Vn = V1 * (double)nab;
-        const uint8_t* Sa = pm + (nib(op, a) * ptp) * stride;
-        const uint8_t* Sb = dm + (nib(od, bb) * dtp) * stride;
-        int r = 0, q = 0;
-        while (r < ptp && q < dtp) {
-            const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
-            const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
-            const int g = Sa[r * stride], h = Sb[q * stride];
-            const double bytes = pow2 ? (Vn * (double)ov) * inv_den : (Vn * (double)ov) / den;
-            const double time = p.alpha[g * p.G + h] + bytes / p.beta[g * p.G + h];
-            if (time > worst) {
-                worst = time;
-                if (worst >= cutoff) return worst;
-            }
-            if (re <= qe) ++r;
-            if (qe <= re) ++q;
-        }
-        const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
-        if (adv_a) {
-            ++a;
-            a0 = a1;
-            a1 = a0 + lqp + (a < lrp ? 1 : 0);
-        }
-        if (adv_b) {
-            ++bb;
-            b0 = b1;
-            b1 = b0 + lqd + (bb < lrd ? 1 : 0);
-        }
-    }
-    return worst;
-}
-
-// The order pair with index k in [0, ppp! dpp!): k = kp * dpp! + kd, each order the
-// Lehmer-code unranking of its index (the lexicographic rank among the orders of its side).
+// The order with index k in [0, n!): the Lehmer-code unranking of k (its lexicographic rank).
 __device__ uint32_t unrank_order(int k, int n) {
     uint32_t out = 0, used = 0;
     for (int i = 0; i < n; ++i) {
@@ -330,15 +295,101 @@ __device__ uint32_t unrank_order(int k, int n) {
     return out;
 }
 
-// One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: every lane
-// first takes its ascending-order time; then the wavefront searches the order pairs of each
-// lane that has more than one, together: lane l tries pairs l, l + 64, ... with branch and
-// bound (a walk stops once it reaches the best time the lane has seen, starting from the
-// ascending time), and a wavefront minimum gives the edge's time.  The minimum is the same
-// value an exhaustive enumeration finds.  Per-replica granularity only.
+// First layer of pipeline position a of a pipeline of pp stages (uniform split, remainder to the
+// earlier positions).
+__device__ __forceinline__ int pos_first(int L, int pp, int a) { return a * (L / pp) + (a < L % pp ? a : L % pp); }
+
+// Slowest link between prefill stage s and decode stage t when they serve positions sharing nab
+// layers: the merge walk of kv_time over the rank pairs whose head slices overlap.
+__device__ double kv_block_time(const Problem& p, const uint8_t* pm, int ptp, int s, const uint8_t* dm, int dtp,
+                                int t, int nab, int stride) {
+    const double Vn = (2.0 * p.s_in * p.Hkv * p.B) * (double)nab;
+    const int deni = ptp * dtp;
+    const double den = (double)deni;
+    const bool pow2 = (deni & (deni - 1)) == 0;
+    const double inv_den = 1.0 / den;
+    const uint8_t* Sa = pm + (s * ptp) * stride;
+    const uint8_t* Sb = dm + (t * dtp) * stride;
+    double worst = 0.0;
+    int r = 0, q = 0;
+    while (r < ptp && q < dtp) {
+        const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+        const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+        const int g = Sa[r * stride], h = Sb[q * stride];
+        const double bytes = pow2 ? (Vn * (double)ov) * inv_den : (Vn * (double)ov) / den;
+        const double time = p.alpha[g * p.G + h] + bytes / p.beta[g * p.G + h];
+        if (time > worst) worst = time;
+        if (re <= qe) ++r;
+        if (qe <= re) ++q;
+    }
+    return worst;
+}
+
+// Whether the bipartite graph with rows 0..n-1 (n <= 8) and row y's columns the bits of byte y
+// of rm has a perfect matching: augmenting paths found by breadth-first search from each row,
+// with the matching and the search's parents packed 4 bits per column / row.
+__device__ bool perfect_matching(uint64_t rm, int n) {
+    uint32_t row_of_col = 0xFFFFFFFFu, col_of_row = 0xFFFFFFFFu;  // 15: none
+    for (int i = 0; i < n; ++i) {
+        uint32_t parent = 0, seen = 0, front = 1u << i;
+        int found = -1;
+        while (front && found < 0) {
+            const int u = __ffs(front) - 1;
+            front &= front - 1;
+            uint32_t av = (uint32_t)((rm >> (8 * u)) & 0xFFu) & ~seen;
+            while (av) {
+                const int j = __ffs(av) - 1;
+                av &= av - 1;
+                seen |= 1u << j;
+                parent = (parent & ~(15u << (4 * j))) | ((uint32_t)u << (4 * j));
+                const int r = (int)((row_of_col >> (4 * j)) & 15u);
+                if (r == 15) {
+                    found = j;
+                    break;
+                }
+                front |= 1u << r;
+            }
+        }
+        if (found < 0) return false;
+        for (int j = found;;) {  // flip the path: each row on it takes the column it reached
+            const int u = (int)((parent >> (4 * j)) & 15u);
+            const int prev = (int)((col_of_row >> (4 * u)) & 15u);
+            col_of_row = (col_of_row & ~(15u << (4 * u))) | ((uint32_t)j << (4 * u));
+            row_of_col = (row_of_col & ~(15u << (4 * j))) | ((uint32_t)u << (4 * j));
+            if (u == i) break;
+            j = prev;
+        }
+    }
+    return true;
+}
+
+// C[y][t] for X order sig: the largest block of the X positions sharing layers with y.
+__device__ __forceinline__ double order_cell(const double* blk, const int* px, const int* ystart, uint32_t sig, int y,
+                                             int t) {
+    double c = 0.0;
+    for (int k = ystart[y]; k < ystart[y + 1]; ++k) {
+        const double b = blk[(k * kOrderStages + nib(sig, px[k])) * kOrderStages + t];
+        c = b > c ? b : c;
+    }
+    return c;
+}
+
+// One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: every lane first
+// takes its ascending-order time; then the wavefront searches the edge of each lane whose
+// replicas are not both single-stage, together: the block table of that edge goes to LDS, lane l
+// takes the X orders l, l + 64, ..., and for each order whose lower bound max_y min_t C[y][t]
+// is below the best time found so far (shared across the wavefront after every 64 orders, and
+// starting from the ascending time), solves the bottleneck assignment from that bound upwards.
+// The minimum is the one the enumeration of every order pair finds.  Per-replica granularity.
 template <int W>
 __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o, FlowNet f) {
-    extern __shared__ uint8_t sm[];
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
+    double* blk = reinterpret_cast<double*>(sm);
+    int32_t* px = reinterpret_cast<int32_t*>(blk + kBlockPairs * kOrderStages * kOrderStages);
+    int32_t* py = px + kBlockPairs;
+    int32_t* pn = py + kBlockPairs;
+    int32_t* ystart = pn + kBlockPairs;
+    uint8_t* mem = sm + kOrderLds;
     const int tid = threadIdx.x;  // kKvBlock = 64: one wavefront per workgroup
     const int stride = kKvBlock;
     const int64_t gid = (int64_t)blockIdx.x * kKvBlock + tid;
@@ -351,8 +402,8 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
     int ptp = 0, ppp = 0, dtp = 0, dpp = 0;
     bool feas = false;
     double t = 0.0;
-    uint8_t* pm = sm + tid;
-    uint8_t* dm = sm + p.G * stride + tid;
+    uint8_t* pm = mem + tid;
+    uint8_t* dm = mem + p.G * stride + tid;
     if (live) {
         const int i = e / nd, j = e - i * nd;
         const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
@@ -360,31 +411,84 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
         ppp = o.pp[(int64_t)kp * N + n];
         dtp = o.tp[(int64_t)kd * N + n];
         dpp = o.pp[(int64_t)kd * N + n];
-        feas = ptp > 0 && dtp > 0 && expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
+        feas = ptp > 0 && dtp > 0 && ppp <= kOrderStages && dpp <= kOrderStages &&
+               expand<W>(o.members, kp, N, n, pm, stride) == ptp * ppp &&
                expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp;
         if (feas) t = kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride);
     }
-    const int pairs = feas ? order_count(ppp) * order_count(dpp) : 1;
-    uint64_t todo = __ballot(feas && pairs > 1 && pairs <= kOrderPairs);
+    uint64_t todo = __ballot(feas && (ppp > 1 || dpp > 1));
     while (todo) {
         const int owner = __ffsll((unsigned long long)todo) - 1;
         todo &= todo - 1;
         const int optp = __shfl(ptp, owner), oppp = __shfl(ppp, owner);
         const int odtp = __shfl(dtp, owner), odpp = __shfl(dpp, owner);
-        const int opairs = __shfl(pairs, owner);
         double best = __shfl(t, owner);
-        const int dfact = order_count(odpp);
-        for (int k = tid; k < opairs; k += kKvBlock) {
-            const int kp = k / dfact, kd = k - kp * dfact;
-            const double v = kv_time_ord(p, sm + owner, optp, oppp, unrank_order(kp, oppp), sm + p.G * stride + owner,
-                                         odtp, odpp, unrank_order(kd, odpp), stride, best);
-            if (v < best) best = v;
+        const bool swap = odpp < oppp;  // X = the side with fewer stages, prefill on ties
+        const int nx = swap ? odpp : oppp, ny = swap ? oppp : odpp;
+        const uint8_t* opm = mem + owner;
+        const uint8_t* odm = mem + p.G * stride + owner;
+        if (tid == 0) {  // position pairs sharing layers, a merge walk: Y positions nondecreasing
+            int a = 0, b = 0, k = 0;
+            ystart[0] = 0;
+            while (a < nx && b < ny) {
+                const int xl = pos_first(p.L, nx, a), xh = pos_first(p.L, nx, a + 1);
+                const int yl = pos_first(p.L, ny, b), yh = pos_first(p.L, ny, b + 1);
+                px[k] = a;
+                py[k] = b;
+                pn[k] = (xh < yh ? xh : yh) - (xl > yl ? xl : yl);
+                ++k;
+                if (xh <= yh) ++a;
+                if (yh <= xh) ystart[++b] = k;
+            }
         }
-        for (int off = 32; off > 0; off >>= 1) {
-            const double u = __shfl_xor(best, off);
-            best = u < best ? u : best;
+        __syncthreads();
+        const int npairs = ystart[ny];
+        for (int it = tid; it < npairs * nx * ny; it += kKvBlock) {
+            const int k = it / (nx * ny), rest = it - k * nx * ny;
+            const int xs = rest / ny, yt = rest - xs * ny;
+            blk[(k * kOrderStages + xs) * kOrderStages + yt] =
+                swap ? kv_block_time(p, opm, optp, yt, odm, odtp, xs, pn[k], stride)
+                     : kv_block_time(p, opm, optp, xs, odm, odtp, yt, pn[k], stride);
+        }
+        __syncthreads();
+        const int nfact = order_count(nx);
+        for (int base = 0; base < nfact; base += kKvBlock) {
+            const int k = base + tid;
+            if (k < nfact) {
+                const uint32_t sig = unrank_order(k, nx);
+                double lb = 0.0;
+                for (int y = 0; y < ny; ++y) {
+                    double m = order_cell(blk, px, ystart, sig, y, 0);
+                    for (int c = 1; c < ny; ++c) {
+                        const double v = order_cell(blk, px, ystart, sig, y, c);
+                        m = v < m ? v : m;
+                    }
+                    lb = m > lb ? m : lb;
+                }
+                double T = lb;
+                while (T < best) {
+                    uint64_t rm = 0;
+                    double next = best;
+                    for (int y = 0; y < ny; ++y)
+                        for (int c = 0; c < ny; ++c) {
+                            const double v = order_cell(blk, px, ystart, sig, y, c);
+                            if (v <= T) rm |= 1ull << (8 * y + c);
+                            else if (v < next) next = v;
+                        }
+                    if (perfect_matching(rm, ny)) {
+                        best = T;
+                        break;
+                    }
+                    T = next;  // the next entry above T, or best when none is below it
+                }
+            }
+            for (int off = 32; off > 0; off >>= 1) {
+                const double u = __shfl_xor(best, off);
+                best = u < best ? u : best;
+            }
         }
         if (tid == owner) t = best;
+        __syncthreads();  // the next edge overwrites the block table
     }
     if (!live) return;
     f.kv_cap[(int64_t)e * N + n] = feas ? quantize(1000.0 / t) : 0;
@@ -609,7 +713,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
         else
             hipLaunchKernelGGL((kv_gpu_kernel<W, false>), grid, block, glds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
-        hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), kOrderLds + lds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
         hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds + sizeof(double) * p.G, s,
                            p, o, f);

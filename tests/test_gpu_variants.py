@@ -91,11 +91,11 @@ ORDER = 2
 
 
 @pytest.mark.parametrize("cfg,n,variant", [(1, None, ORDER), (2, None, ORDER), (3, 16384, ORDER), (4, 2048, ORDER),
-                                           (2, 777, ORDER | PIPE), (3, 4096, ORDER | PIPE)])
+                                           (4, 8191, ORDER), (2, 777, ORDER | PIPE), (3, 4096, ORDER | PIPE)])
 def test_kv_order_parity(torch, cfg, n, variant):
-    """KV stage-order search (alone and with the pipelined capacity): KV capacities, flows and
-    the best candidate equal the oracle's; every KV capacity is at least the ascending-order
-    one."""
+    """KV stage-order search (alone and with the pipelined capacity), exact at every pipeline depth
+    up to 8 stages: KV capacities, flows and the best candidate equal the oracle's; every KV
+    capacity is at least the ascending-order one."""
     prob = dataclasses.replace(I.make_problem(cfg, n_cand=n), variant=variant)
     say(f"KV stage-order search: workload {cfg}, N={prob.n_cand}, variant {variant}")
     cost, fn, fv, best = _gpu(torch, prob)
@@ -109,6 +109,35 @@ def test_kv_order_parity(torch, cfg, n, variant):
                             hxo.cost_eval(dataclasses.replace(prob, variant=variant & ~ORDER)))
     up, ud, upd = Hh.used_rows(fn)
     assert (fn["kv_cap"][upd] >= asc["kv_cap"][upd]).all()
+
+
+@pytest.mark.parametrize("dpp", [8, 4])
+def test_kv_order_deep_hidden_pairing(torch, dpp):
+    """Eight one-GPU prefill stages against eight or four one-GPU decode stages whose fast links
+    follow a hidden pairing (the oracle's hand-derived case): the searched KV edge carries every
+    overlapping block on a 300 GB/s link, 6 layers each."""
+    pi = [3, 6, 0, 7, 2, 5, 1, 4]
+    G = 16
+    beta = np.full((G, G), 10e9)
+    for i in range(8):
+        for t in range(8):
+            if (pi[i] == t) if dpp == 8 else (pi[i] // 2 == t):
+                beta[i, 8 + t] = beta[8 + t, i] = 300e9
+    np.fill_diagonal(beta, 0.0)
+    tt = np.array([I.GPU_TYPES["A"]], np.float64)
+    cl = I.Cluster(np.zeros(G, np.int32), tt[:, 0].copy(), tt[:, 1].copy(), tt[:, 2].copy(),
+                   np.ascontiguousarray(beta.reshape(-1)), np.zeros(G * G))
+    a, r = I.placement_from_groups([list(range(8)), list(range(8, 8 + dpp))], [I.PREFILL, I.DECODE], G, 2)
+    prob = Hh.problem(cl, dict(I.OPT_30B), a, r, s_in=512.0, s_out=128.0, tp=(1,), pp=(4, 8))
+    prob = dataclasses.replace(prob, variant=ORDER)
+    say(f"KV stage-order search: 8 x {dpp} hidden pairing")
+    cost, fn, fv, best = _gpu(torch, prob)
+    want = hxo.score_batch(prob)
+    assert cost["pp"][0, 0] == 8 and cost["pp"][1, 0] == dpp
+    V6 = 2.0 * 512.0 * 7168 * 2 * 6
+    assert int(fn["kv_cap"][0, 0]) == int(np.floor(1000.0 / (V6 / 300e9)))
+    Hh.compare_flownet(fn, want["flownet"])
+    assert np.array_equal(fv, want["flow_value"])
 
 
 def test_kv_order_crossed_links(torch):

@@ -9,9 +9,10 @@ max T_j = ceil(L/pp) * (per-layer time); and a batch's decode capacities can onl
 prefill capacities stay as they were.
 
 KV stage-order search (variant bit 1): a KV edge's time is minimised over the stage orders of
-both replicas.  Checked on a hand-derived case whose ascending orders pair the slow links and
-whose best order pairs the fast ones, and by what a search over every order fixes: it never
-exceeds the ascending time, leaves single stages alone, and cannot tell in which order the
+both replicas.  Checked on hand-derived cases whose ascending orders pair the slow links and
+whose best orders pair the fast ones (two and eight stages a side), against brute force over
+every order pair (up to five stages a side), and by what a search over every order fixes: it
+never exceeds the ascending time, leaves single stages alone, and cannot tell in which order the
 stage blocks were handed to it.
 
 Asymmetric layer split (variant bit 2): hand-derived splits, the invariants of the rule (sum L,
@@ -20,6 +21,7 @@ batches unchanged on a one-type cluster, a free-link latency closed form, and a 
 stages share the split's 40 layers.
 """
 import dataclasses
+import itertools
 
 import numpy as np
 import pytest
@@ -146,12 +148,11 @@ def _stage_blocks(members, tp, perm):
 
 
 def test_kv_order_search_properties():
-    """On random replica pairs of the 32-GPU cluster: the searched time never exceeds the
-    ascending one, equals it for single stages and beyond the search limit, and does not change
-    when the stage blocks are handed over in another order (the search covers every order)."""
+    """On random replica pairs of the 32-GPU cluster, up to five stages a side: the searched time
+    never exceeds the ascending one, equals it for single stages, and does not change when the
+    stage blocks are handed over in another order (the search covers every order)."""
     prob = I.make_problem(3, n_cand=4)
     rng = np.random.default_rng(5)
-    fact = [1, 1, 2, 6, 24, 120, 720, 5040, 40320]
     checked = strict = 0
     for _ in range(300):
         ptp, dtp = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 4]))
@@ -164,7 +165,7 @@ def test_kv_order_search_properties():
         asc = hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp)
         best = hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp, best_order=True)
         assert best <= asc
-        if fact[ppp] * fact[dpp] > 720 or (ppp == 1 and dpp == 1):
+        if ppp == 1 and dpp == 1:
             assert best == asc
             continue
         checked += 1
@@ -173,6 +174,80 @@ def test_kv_order_search_properties():
         dm2 = _stage_blocks(dm, dtp, rng.permutation(dpp))
         assert hxo.kv_time(prob, pm2, ptp, ppp, dm2, dtp, dpp, best_order=True) == best
     assert checked > 50 and strict > 10
+
+
+@pytest.mark.parametrize("ppp,dpp,ptp,dtp,seed", [(2, 3, 2, 1, 1), (3, 3, 1, 2, 2), (4, 3, 1, 1, 3), (3, 5, 2, 1, 4),
+                                                  (4, 4, 1, 2, 5), (5, 4, 1, 1, 6), (2, 6, 2, 1, 7), (6, 2, 1, 4, 8),
+                                                  (5, 5, 1, 1, 9)])
+def test_kv_order_search_brute_force(ppp, dpp, ptp, dtp, seed):
+    """The search's minimum equals the smallest KV time over every pair of stage orders, each
+    order pair's time taken by the oracle's plain walk with explicit orders."""
+    prob = I.make_problem(4, n_cand=1)
+    rng = np.random.default_rng(seed)
+    g = rng.permutation(prob.n_gpus)
+    pm = sorted(g[:ptp * ppp].tolist())
+    dm = sorted(g[ptp * ppp:ptp * ppp + dtp * dpp].tolist())
+    brute = min(hxo.kv_time_orders(prob, pm, ptp, ppp, op, dm, dtp, dpp, od)
+                for op in itertools.permutations(range(ppp)) for od in itertools.permutations(range(dpp)))
+    assert hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp, best_order=True) == brute
+    assert hxo.kv_time_orders(prob, pm, ptp, ppp, range(ppp), dm, dtp, dpp, range(dpp)) == \
+        hxo.kv_time(prob, pm, ptp, ppp, dm, dtp, dpp)
+
+
+def _hidden_pairing_cluster(fast):
+    """16 GPUs of one type: prefill GPUs 0-7, decode GPUs 8-15; the link i -> 8 + t is 300 GB/s
+    when fast(i, t), 10 GB/s otherwise; alpha 0."""
+    G = 16
+    beta = np.full((G, G), 10e9)
+    for i in range(8):
+        for t in range(8):
+            if fast(i, t):
+                beta[i, 8 + t] = beta[8 + t, i] = 300e9
+    np.fill_diagonal(beta, 0.0)
+    tt = np.array([I.GPU_TYPES["A"]], np.float64)
+    return I.Cluster(np.zeros(G, np.int32), tt[:, 0].copy(), tt[:, 1].copy(), tt[:, 2].copy(),
+                     np.ascontiguousarray(beta.reshape(-1)), np.zeros(G * G))
+
+
+@pytest.mark.parametrize("dpp", [8, 4])
+def test_kv_order_deep_hand_case(dpp):
+    """Eight one-GPU prefill stages against eight or four one-GPU decode stages, 48 layers.  A hidden pairing makes some links 300 GB/s and the rest 10 GB/s; an order that puts
+    every overlapping pair of positions on a fast link exists, so the minimum is the fast time of
+    the largest overlap.
+      dpp = 8: positions a and b share 6 layers iff a = b; link i -> t is fast iff t = pi(i) for
+               a permutation pi, so ordering decode stages as pi of the prefill order makes all
+               eight links fast: 2 s_in H_kv B * 6 / 300e9.
+      dpp = 4: decode position b (12 layers) shares 6 layers with prefill positions 2b and 2b+1;
+               link i -> t is fast iff pi(i) // 2 = t, so each decode stage has two fast prefill
+               stages; placing them at 2b, 2b+1 makes every link fast: again 6 layers at 300 GB/s.
+    The ascending orders hit a slow link (pi is not the identity pairing)."""
+    pi = [3, 6, 0, 7, 2, 5, 1, 4]
+    fast = (lambda i, t: pi[i] == t) if dpp == 8 else (lambda i, t: pi[i] // 2 == t)
+    from tests import helpers as Hh
+    cl = _hidden_pairing_cluster(fast)
+    groups = [list(range(8)), list(range(8, 8 + dpp))]
+    a, r = I.placement_from_groups(groups, [I.PREFILL, I.DECODE], 16, 2)
+    prob = Hh.problem(cl, dict(I.OPT_30B), a, r, s_in=512.0, s_out=128.0, tp=(1,), pp=(4, 8))
+    V6 = 2.0 * 512.0 * 7168 * 2 * 6
+    best = hxo.kv_time(prob, groups[0], 1, 8, groups[1], 1, dpp, best_order=True)
+    assert best == V6 / 300e9
+    assert hxo.kv_time(prob, groups[0], 1, 8, groups[1], 1, dpp) == V6 / 10e9
+    # an optimal order pair, checked with the plain walk
+    if dpp == 8:
+        od = pi
+    else:
+        od = [0, 1, 2, 3]
+        op = sorted(range(8), key=lambda i: (pi[i] // 2, i))
+    op = list(range(8)) if dpp == 8 else op
+    assert hxo.kv_time_orders(prob, groups[0], 1, 8, op, groups[1], 1, dpp, od) == best
+
+
+def test_kv_order_rejects_deep_pp_mask():
+    """The search covers pipelines of up to 8 stages: with it, a PP mask past 8 is refused."""
+    prob = I.make_problem(2, n_cand=4)
+    p2 = dataclasses.replace(prob, variant=ORDER, pp_mask=prob.pp_mask | (1 << 8))
+    with pytest.raises(ValueError):
+        hxo.build_flownet(p2, hxo.cost_eval(dataclasses.replace(p2, variant=0)))
 
 
 # ------------------------------------------------------------------ asymmetric layer split
