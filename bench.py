@@ -84,7 +84,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4])
+    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5],
+                    help="5: the refinement chain (--rounds rounds of 131,072 perturbations of the previous "
+                         "round's best, per-GPU flow nodes)")
+    ap.add_argument("--rounds", type=int, default=0, help="--workload 5: rounds of the chain (default: 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", choices=list(VARIANTS), default="as-written",
                     help="cost-model variant: the model as written, pipelined decode capacity, KV stage-order "
@@ -96,6 +99,9 @@ def parse():
                     help="time max-flow guided refinement rounds on the 128-GPU per-GPU-network workload instead")
     ap.add_argument("--partition", action="store_true",
                     help="time the graph-partition candidate generator (spectral order, partition, scoring) instead")
+    ap.add_argument("--pushrelabel", choices=["workload3", "workload5"], default=None,
+                    help="time the max-flow alone on networks that need push-relabel, at the network shapes of "
+                         "that workload (both sides of at least two nodes, KV arcs below min(a_i, b_j))")
     ap.add_argument("--children", type=int, default=131072, help="children per refinement round (--refine)")
     ap.add_argument("--partition-candidates", type=int, default=16384, help="candidates per step (--partition)")
     ap.add_argument("--spectral-iters", type=int, default=1000, help="power iterations (--partition)")
@@ -134,15 +140,20 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
 
 
 def cpu_model() -> str:
-    """The host CPU's model name (first processor in /proc/cpuinfo), or "unknown"."""
+    """The host CPU: model name, vendor, family / model / stepping (first processor in
+    /proc/cpuinfo) and the logical CPU count, or "unknown"."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if not line.strip():
+                    break
+                k, _, v = line.partition(":")
+                info[k.strip()] = v.strip()
     except OSError:
-        pass
-    return "unknown"
+        return "unknown"
+    return (f"{info.get('model name', 'unknown')} ({info.get('vendor_id', '?')}, family {info.get('cpu family', '?')} "
+            f"model {info.get('model', '?')} stepping {info.get('stepping', '?')}; {os.cpu_count()} logical CPUs)")
 
 
 def measured_copy_gbs(torch, mib: int = 1024, reps: int = 10) -> float:
@@ -436,24 +447,28 @@ def refine_main(args, torch, hx, I):
     if not args.no_cpu_baseline:
         from oracle import hxo  # test infrastructure: only this baseline leg uses it
         cores = max(1, min(len(os.sched_getaffinity(0)), 64))
-        par = prob0
-
-        def oracle_round(n):
-            fn = hxo.build_flownet(par, hxo.cost_eval(par))
-            cls = hxo.edge_classes(fn)
-            rnd_h = I.move_draws(cfg, 0, n)
-            ch = hxo.guided_moves(par.n_gpus, par.max_groups, par.granularity, par.assign, par.role, fn, cls, rnd_h)
-            hxo.score_batch(dataclasses.replace(par, assign=ch["assign"], role=ch["role"]), n_threads=cores)
-        n = 1024
         t = time.perf_counter()
-        oracle_round(n)
+        r = hxo.score_batch(prob, n_threads=cores)
         first = time.perf_counter() - t
-        n = int(min(n_child, max(1024, n * args.cpu_seconds / max(first, 1e-3))))
+        reps = max(1, min(50, int(args.cpu_seconds / max(first, 1e-3))))
+        times = [first]
+        for _ in range(reps - 1):
+            t = time.perf_counter()
+            hxo.score_batch(prob, n_threads=cores)
+            times.append(time.perf_counter() - t)
+        med = float(np.median(times))
+        # one thread on a bounded sample (about a tenth of the all-core time budget)
+        m1 = int(min(prob.n_cand, max(256, prob.n_cand * (args.cpu_seconds / 10.0) / (med * cores))))
         t = time.perf_counter()
-        oracle_round(n)
-        dt = time.perf_counter() - t
-        out["cpu_baseline"] = {"value": n / dt, "unit": "children/s", "cores": cores, "kind": "oracle",
-                               "sample": f"round 0 from the base placement with {n} children (of {n_child})"}
+        hxo.score_batch(prob.subset(np.arange(m1)), n_threads=1)
+        one = m1 / (time.perf_counter() - t)
+        gpu_fv = ws.flow_value.cpu().numpy()
+        out["cpu_baseline"] = {"value": prob.n_cand / med, "unit": "candidates/s", "cores": cores, "kind": "oracle",
+                               "sample": f"the full {prob.n_cand}-candidate batch, {len(times)} runs, median; "
+                                         f"1 thread: the first {m1} candidates",
+                               "single_thread": {"value": one, "unit": "candidates/s", "cores": 1},
+                               "agrees": bool(np.array_equal(r["flow_value"], gpu_fv)) and list(r["best"]) == best,
+                               "cpu": cpu_model()}
     print(json.dumps(out))
 
 
@@ -534,6 +549,214 @@ def partition_main(args, torch, hx, I):
     print(json.dumps(out))
 
 
+def chain_main(args, torch, hx, I):
+    """Workload 5 as defined: rounds of 131,072 single-step perturbations (45% move one GPU, 45%
+    swap two GPUs, 10% merge two groups) of the previous round's best placement, the GPU argmax,
+    from the one-group-per-node base; per-GPU flow nodes (up to 258 nodes, ~4,000 KV edges).
+    Each round's batch is generated on the host (timed apart), copied to the GPU (timed apart),
+    then scored; value = all rounds' candidates / their summed scoring time, inputs resident."""
+    cfg = 5
+    wl = I.WORKLOADS[cfg]
+    n = args.candidates or wl.n_cand
+    rounds = args.rounds or wl.rounds
+    G = wl.n_gpus
+    cur = I.base_placement(wl)
+    prob = I.make_problem(cfg, n_cand=n, rnd=0, base=cur)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    h_assign = torch.empty((G, n), dtype=torch.uint8).pin_memory()
+    h_role = torch.empty((prob.max_groups, n), dtype=torch.uint8).pin_memory()
+    d_assign, d_role = dp.tensors["assign"], dp.tensors["role"]
+    for _ in range(args.warmup):
+        hx.score(dp, ws)
+    torch.cuda.synchronize()
+    per_round, probs = [], []
+    for r in range(rounds):
+        t = time.perf_counter()
+        pr = prob if r == 0 else I.make_problem(cfg, n_cand=n, rnd=r, base=cur)
+        gen_s = time.perf_counter() - t
+        h_assign.copy_(torch.from_numpy(pr.assign))
+        h_role.copy_(torch.from_numpy(pr.role))
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        d_assign.copy_(h_assign, non_blocking=True)
+        d_role.copy_(h_role, non_blocking=True)
+        torch.cuda.synchronize()
+        h2d_ms = (time.perf_counter() - t) * 1000.0
+        t = time.perf_counter()
+        hx.score(dp, ws)
+        torch.cuda.synchronize()
+        score_ms = (time.perf_counter() - t) * 1000.0
+        bi, bv = (int(x) for x in ws.best.cpu().numpy())
+        per_round.append({"round": r, "score_ms": score_ms, "h2d_ms": h2d_ms, "host_generation_s": gen_s,
+                          "best_index": bi, "best_flow": bv})
+        probs.append((pr, bi, bv))
+        cur = (pr.assign[:, bi].copy(), pr.role[:, bi].copy())
+        print(f"[chain] round {r}: {score_ms:.3f} ms, best {bv} at {bi}", file=sys.stderr, flush=True)
+    total_ms = sum(x["score_ms"] for x in per_round)
+    value = rounds * n / (total_ms / 1000.0)
+
+    # per-kernel durations: the last round's batch scored again with libhx's kernel events
+    hx.profile(True)
+    for _ in range(args.steps):
+        hx.score(dp, ws)
+    torch.cuda.synchronize()
+    prof = hx.profile_read()
+    hx.profile(False)
+    kernel_us = {k: 1000.0 * ms / c for k, (ms, c) in prof.items() if c > 0}
+    mf = hx.maxflow_stats(ws.net, torch.empty_like(ws.flow_value))
+    last = probs[-1][0]
+    n_p = ws.net.n_p.cpu().numpy()
+    n_d = ws.net.n_d.cpu().numpy()
+    hbm = hbm_bytes_per_step(last, ws.net.dims, n_p, n_d)
+    dominant = max(kernel_us, key=kernel_us.get)
+    roof = roofline_for(dominant, kernel_us, last, hbm, n_p, n_d, cfg)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": rounds,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / rounds,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64+i32",
+        "data": "synthetic",
+        "config": {"workload": f"workload5: {wl.name}; {rounds} chained rounds of {n:,}, each perturbing "
+                               "the previous round's GPU best",
+                   "candidates": rounds * n, "cluster_gpus": G, "max_groups": prob.max_groups,
+                   "granularity": prob.granularity},
+        "rounds": per_round,
+        "host_generation_s": sum(x["host_generation_s"] for x in per_round),
+        "with_h2d_copy": {"value": rounds * n / ((total_ms + sum(x["h2d_ms"] for x in per_round)) / 1000.0),
+                          "unit": "candidates/s", "note": "each round's assign and role copied from pinned host memory"},
+        "kernel_us": kernel_us,
+        "maxflow_paths": mf,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import hxo  # test infrastructure: only this baseline leg uses it
+        # the oracle on a bounded sample of the last round (plus every round's GPU best, which
+        # it must score the same)
+        m = min(n, 2048)
+        sub = last.subset(np.arange(m))
+        cores = max(1, min(len(os.sched_getaffinity(0)), 64))
+        t = time.perf_counter()
+        ra = hxo.score_batch(sub, n_threads=cores)
+        all_cores = m / (time.perf_counter() - t)
+        m1 = min(m, 256)
+        t = time.perf_counter()
+        hxo.score_batch(last.subset(np.arange(m1)), n_threads=1)
+        one = m1 / (time.perf_counter() - t)
+        gpu_fv = ws.flow_value.cpu().numpy()
+        agrees = bool(np.array_equal(ra["flow_value"], gpu_fv[:m]))
+        for pr, bi, bv in probs:
+            agrees = agrees and int(hxo.score_batch(pr.subset(np.array([bi])))["flow_value"][0]) == bv
+        out["cpu_baseline"] = {"value": all_cores, "unit": "candidates/s", "cores": cores, "kind": "oracle",
+                               "sample": f"the first {m} candidates of the last round on {cores} threads; "
+                                         f"1 thread: the first {m1}",
+                               "single_thread": {"value": one, "unit": "candidates/s", "cores": 1},
+                               "agrees": agrees, "cpu": cpu_model()}
+    print(json.dumps(out))
+
+
+# Network shapes of the push-relabel leg: (max_p, max_d, max_pd, nodes per side (lo, hi), N).
+PR_SHAPES = {"workload3": (16, 16, 64, (2, 8), 65536), "workload5": (128, 128, 4096, (16, 64), 4096)}
+
+
+def pushrelabel_networks(shape: str, seed: int = 7903):
+    """Seeded networks of a workload's shape that need push-relabel: P, D nodes per side drawn in
+    the shape's range (P * D within its KV rows), node capacities a_i, b_j uniform in [1, 10^4]
+    (the per-GPU and replica capacities of the workloads are of that order), source and sink edges
+    unbounded, and every KV arc a uniform draw in [0, min(a_i, b_j) - 1]: below what it would
+    need to carry for the closed form, so the flow must be found by pushes and relabels."""
+    mp, md, mpd, (lo, hi), N = PR_SHAPES[shape]
+    rng = np.random.default_rng(seed)
+    n_p = rng.integers(lo, hi + 1, N)
+    n_d = np.minimum(rng.integers(lo, hi + 1, N), mpd // n_p)
+    fn = {"n_p": n_p.astype(np.int32), "n_d": n_d.astype(np.int32), "dims": (mp, md, mpd)}
+    for k, rows in (("src_cap", mp), ("p_cap", mp), ("d_cap", md), ("sink_cap", md), ("kv_cap", mpd),
+                    ("p_slot", mp), ("d_slot", md)):
+        fn[k] = np.zeros((rows, N), np.int32)
+    a = rng.integers(1, 10001, (mp, N)) * (np.arange(mp)[:, None] < n_p[None, :])
+    b = rng.integers(1, 10001, (md, N)) * (np.arange(md)[:, None] < n_d[None, :])
+    fn["p_cap"][:] = a
+    fn["d_cap"][:] = b
+    fn["src_cap"][:] = np.where(a > 0, 16777215, 0)
+    fn["sink_cap"][:] = np.where(b > 0, 16777215, 0)
+    fn["p_slot"][:] = np.arange(mp)[:, None]
+    fn["d_slot"][:] = np.arange(md)[:, None]
+    e = np.arange(mpd)[:, None]
+    row_i, row_j = e // n_d[None, :], e % n_d[None, :]
+    live = e < (n_p * n_d)[None, :]
+    amin = np.minimum(np.take_along_axis(a, np.minimum(row_i, mp - 1), 0),
+                      np.take_along_axis(b, np.minimum(row_j, md - 1), 0))
+    fn["kv_cap"][:] = np.where(live, np.floor(rng.random((mpd, N)) * amin), 0).astype(np.int32)
+    return fn
+
+
+def pushrelabel_main(args, torch, hx):
+    """The max-flow kernel alone on networks that need push-relabel (with flows and the canonical
+    cut requested, as the refinement step asks), at a workload's network shapes."""
+    fn = pushrelabel_networks(args.pushrelabel)
+    net = hx.FlowNetBuffers.from_host(fn)
+    N = int(fn["n_p"].shape[0])
+    mp, md, mpd = fn["dims"]
+    fv = torch.empty(N, dtype=torch.int32, device="cuda")
+    kv = torch.empty((mpd, N), dtype=torch.int32, device="cuda")
+    cut = torch.empty((mp + md, N), dtype=torch.uint8, device="cuda")
+    for _ in range(args.warmup):
+        hx.maxflow_batch(net, fv, kv, cut)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        hx.maxflow_batch(net, fv, kv, cut)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    hx.profile(True)
+    for _ in range(args.steps):
+        hx.maxflow_batch(net, fv, kv, cut)
+    torch.cuda.synchronize()
+    prof = hx.profile_read()
+    hx.profile(False)
+    kernel_us = {k: 1000.0 * t / c for k, (t, c) in prof.items() if c > 0}
+    st = hx.maxflow_stats(net, torch.empty_like(fv), torch.empty_like(kv), torch.empty_like(cut))
+    pr = max(1, st["push_relabel"])
+    alg = float(lds_floor_bytes(fn["n_p"], fn["n_d"]).sum())
+    t_mf = kernel_us["maxflow"] * 1e-6
+    out = {
+        "metric": "push-relabel networks solved/sec (max-flow with flows and cut) at 1 GPU",
+        "value": N / (ms / 1000.0), "unit": "networks/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i32",
+        "data": "synthetic",
+        "config": {"workload": f"push-relabel networks at {args.pushrelabel} shapes", "networks": N,
+                   "max_p": mp, "max_d": md, "max_pd": mpd},
+        "kernel_us": kernel_us,
+        "maxflow_paths": st,
+        "per_push_relabel_network": {"pushes": st["pushes"] / pr, "relabels": st["relabels"] / pr},
+        "per_workgroup": {"global_relabels": st["global_relabels"], "rounds": st["rounds"]},
+        "roofline": {"kernel": "maxflow (hx_maxflow_batch)", "bound": "lds", "achieved": alg / t_mf / 1e9,
+                     "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": alg / t_mf / 1e9 / LDS_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": alg, "avg_launch_us": kernel_us["maxflow"],
+                     "note": "algorithmic bytes = the residual graph written once and every arc read once; "
+                             "push-relabel reads arcs many times per network (pushes, relabels above)"},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import hxo  # test infrastructure: only this baseline leg uses it
+        m = N if args.pushrelabel == "workload3" else min(N, 2048)
+        sub = {k: (np.ascontiguousarray(v[..., :m]) if isinstance(v, np.ndarray) else v) for k, v in fn.items()}
+        t = time.perf_counter()
+        want = hxo.maxflow_batch(sub, want_flows=True)
+        rate = m / (time.perf_counter() - t)
+        out["cpu_baseline"] = {"value": rate, "unit": "networks/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the first {m} networks, Edmonds-Karp on one thread",
+                               "agrees": bool(np.array_equal(want["flow_value"], fv.cpu().numpy()[:m])),
+                               "cpu": cpu_model()}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -563,6 +786,12 @@ def main():
         return
     if args.partition:
         partition_main(args, torch, hx, I)
+        return
+    if args.workload == 5:
+        chain_main(args, torch, hx, I)
+        return
+    if args.pushrelabel:
+        pushrelabel_main(args, torch, hx)
         return
     wl = I.WORKLOADS[args.workload]
     prob = I.make_problem(args.workload, n_cand=args.candidates or None)
@@ -676,8 +905,10 @@ def main():
         "best": best,
         "roofline": roof,
     }
-    if dominant != "maxflow" and "maxflow" in kernel_us:
-        # the LDS-resident max-flow beside the dominant kernel, against the LDS peak
+    if dominant != "maxflow" and "maxflow" in kernel_us and mf["push_relabel"] > 0:
+        # the LDS-resident max-flow beside the dominant kernel, against the LDS peak, when some
+        # candidate needed push-relabel (closed forms touch their arcs once, so an LDS fraction
+        # of those would credit work the kernel never did)
         out["maxflow_roofline"] = roofline_for("maxflow", kernel_us, prob, hbm, n_p, n_d, args.workload)
 
     if not args.no_cpu_baseline:
