@@ -613,30 +613,54 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
 // Per-GPU nodes: one workgroup of kGpuKvWaves wavefronts per 64 candidates (a lane per
 // candidate in every wavefront).  Every edge of the per-GPU network counts requests (a GPU node
 // carries its share of its replica's requests), so the edge from prefill GPU g to decode GPU h
-// carries one request's whole KV cache, V1 L bytes, over the link g -> h: it depends on g, h and
-// whether both replicas are feasible.  The workgroup first stages, per candidate, every GPU's
-// feasibility ([G][64] bytes in LDS: 1 when its replica kept a strategy) and the node lists' GPU
-// ids; then each wavefront takes every kGpuKvWaves-th edge row (coalesced stores across the 64
-// candidates) with no dependent global loads but alpha/beta.  One lane per (edge, candidate)
-// would repeat the lookups of both endpoints for every edge.
+// carries one request's whole KV cache, V1 L bytes, over the link g -> h: its capacity depends
+// only on g and h, and is 0 unless both replicas are feasible.  With kTable (G <= 128) the
+// workgroup first tabulates the capacity of every link in LDS ([G][G] int32, at most 64 KB: two
+// divisions per link, a few per lane, instead of two per edge); then it stages, per candidate,
+// every GPU's feasibility ([G][64] bytes: 1 when its replica kept a strategy) and the node lists'
+// GPU ids; then each wavefront takes every kGpuKvWaves-th edge row (coalesced stores across the
+// 64 candidates), each edge a table lookup (or, without the table, its two divisions).  One
+// lane per (edge, candidate) would repeat the lookups of both endpoints for every edge.
 constexpr int kGpuKvWaves = 4;
+constexpr int kGpuKvWavesTable = 16;  // the table leaves one workgroup per CU: more wavefronts
+constexpr int kGpuTableMaxG = 128;
 
 // Node rows staged per side: a side has at most G per-GPU nodes.
 __host__ __device__ inline int kv_gpu_rows(int G, int max_rows) { return max_rows < G ? max_rows : G; }
 
-__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d) {
-    return ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
+__host__ __device__ inline size_t kv_gpu_lds(int G, int max_p, int max_d, bool table) {
+    return (table ? sizeof(int32_t) * (size_t)G * G : 0) +
+           ((size_t)G + (size_t)kv_gpu_rows(G, max_p) + (size_t)kv_gpu_rows(G, max_d)) * 64;
 }
 
-template <int W, bool kCls>
-__global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, CostOut o, FlowNet f) {
+// Capacity of the per-GPU KV edge over the link g -> h: one request's whole KV cache (V1 L
+// bytes; with request classes the mix's mean time).
+template <bool kCls>
+__device__ __forceinline__ int32_t kv_gpu_cap(const Problem& p, const double* vl, int g, int h) {
+    const double al = p.alpha[g * p.G + h], be = p.beta[g * p.G + h];
+    double t;
+    if (kCls) {
+        t = 0.0;
+        for (int k = 0; k < p.n_cls; ++k) t = t + p.cls_w[k] * (al + vl[k] / be);
+    } else {
+        t = al + vl[0] / be;
+    }
+    return quantize(1000.0 / t);
+}
+
+template <int W, bool kCls, bool kTable>
+__global__ void __launch_bounds__(64 * (kTable ? kGpuKvWavesTable : kGpuKvWaves))
+    kv_gpu_kernel(Problem p, CostOut o, FlowNet f) {
+    constexpr int kWaves = kTable ? kGpuKvWavesTable : kGpuKvWaves;
     extern __shared__ __attribute__((aligned(16))) unsigned char sm[];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t N = p.N;
     const int64_t n = (int64_t)blockIdx.x * 64 + lane;
     const bool in = n < N;
     const int G = p.G;
-    uint8_t* ok = sm;                          // [G][64]: 1 if the GPU's replica is feasible
+    int32_t* tab = reinterpret_cast<int32_t*>(sm);                    // [G][G] (kTable)
+    uint8_t* ok = sm + (kTable ? sizeof(int32_t) * (size_t)G * G : 0);  // [G][64]: 1 if the GPU's
+                                                                      // replica is feasible
     uint8_t* ps = ok + (size_t)G * 64;         // [prow][64]: prefill node -> GPU
     const int prow = kv_gpu_rows(G, f.max_p), drow = kv_gpu_rows(G, f.max_d);
     uint8_t* ds = ps + (size_t)prow * 64;      // [drow][64]: decode node -> GPU
@@ -646,7 +670,12 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
 #pragma unroll
     for (int k = 0; k < HX_MAX_CLASSES; ++k)
         vl[k] = (2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B) * (double)p.L;
-    for (int g = wave; g < G; g += kGpuKvWaves) {
+    if (kTable)
+        for (int x = threadIdx.x; x < G * G; x += 64 * kWaves) {
+            const int g = x / G, h = x - g * G;
+            tab[x] = g == h ? 0 : kv_gpu_cap<kCls>(p, vl, g, h);
+        }
+    for (int g = wave; g < G; g += kWaves) {
         uint8_t d = 0;
         if (in) {
             const int k = p.assign[(int64_t)g * N + n];
@@ -654,9 +683,9 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
         }
         ok[g * 64 + lane] = d;
     }
-    for (int i = wave; i < prow; i += kGpuKvWaves)
+    for (int i = wave; i < prow; i += kWaves)
         ps[i * 64 + lane] = i < np ? (uint8_t)f.p_slot[(int64_t)i * N + n] : 0;
-    for (int j = wave; j < drow; j += kGpuKvWaves)
+    for (int j = wave; j < drow; j += kWaves)
         ds[j * 64 + lane] = j < nd ? (uint8_t)f.d_slot[(int64_t)j * N + n] : 0;
     __syncthreads();
     const int E = np * nd;
@@ -665,35 +694,38 @@ __global__ void __launch_bounds__(64 * kGpuKvWaves) kv_gpu_kernel(Problem p, Cos
         const int v = __shfl_xor(emax, off, 64);
         emax = v > emax ? v : emax;
     }
-    // edge e = i * nd + j of this lane's candidate, rows wave, wave + kGpuKvWaves, ...
+    // edge e = i * nd + j of this lane's candidate, rows wave, wave + kWaves, ...
     int i = 0, j = wave;
     while (nd > 0 && j >= nd) {
         j -= nd;
         ++i;
     }
-    for (int e = wave; e < emax; e += kGpuKvWaves) {
+    for (int e = wave; e < emax; e += kWaves) {
         if (e < E) {
             const int g = ps[i * 64 + lane], h = ds[j * 64 + lane];
             int32_t c = 0;
-            if (ok[g * 64 + lane] && ok[h * 64 + lane]) {
-                const double al = p.alpha[g * G + h], be = p.beta[g * G + h];
-                double t;
-                if (kCls) {
-                    t = 0.0;
-                    for (int k = 0; k < p.n_cls; ++k) t = t + p.cls_w[k] * (al + vl[k] / be);
-                } else {
-                    t = al + vl[0] / be;
-                }
-                c = quantize(1000.0 / t);
-            }
+            if (ok[g * 64 + lane] && ok[h * 64 + lane]) c = kTable ? tab[g * G + h] : kv_gpu_cap<kCls>(p, vl, g, h);
             f.kv_cap[(int64_t)e * N + n] = c;
-            j += kGpuKvWaves;
+            j += kWaves;
             while (j >= nd) {
                 j -= nd;
                 ++i;
             }
         }
     }
+}
+
+template <int W, bool kCls, bool kTable>
+hipError_t launch_kv_gpu(const Problem& p, const FlowNet& f, const CostOut& o, hipStream_t s) {
+    constexpr int waves = kTable ? kGpuKvWavesTable : kGpuKvWaves;
+    const size_t lds = kv_gpu_lds(p.G, f.max_p, f.max_d, kTable);
+    if (lds > 64 * 1024) {  // gfx950 gives a workgroup up to 160 KB once the limit is raised
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kv_gpu_kernel<W, kCls, kTable>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((kv_gpu_kernel<W, kCls, kTable>), dim3((p.N + 63) / 64), dim3(64 * waves), lds, s, p, o, f);
+    return hipSuccess;
 }
 
 template <int W>
@@ -706,12 +738,13 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     const size_t lds = 2 * (size_t)p.G * kKvBlock;
     prof_mark(kKKv, false, s);
     if (p.granularity != 0) {
-        const dim3 grid((p.N + 63) / 64), block(64 * kGpuKvWaves);
-        const size_t glds = kv_gpu_lds(p.G, f.max_p, f.max_d);
+        const bool table = p.G <= kGpuTableMaxG;
+        hipError_t e;
         if (p.n_cls > 0)
-            hipLaunchKernelGGL((kv_gpu_kernel<W, true>), grid, block, glds, s, p, o, f);
+            e = table ? launch_kv_gpu<W, true, true>(p, f, o, s) : launch_kv_gpu<W, true, false>(p, f, o, s);
         else
-            hipLaunchKernelGGL((kv_gpu_kernel<W, false>), grid, block, glds, s, p, o, f);
+            e = table ? launch_kv_gpu<W, false, true>(p, f, o, s) : launch_kv_gpu<W, false, false>(p, f, o, s);
+        if (e != hipSuccess) return e;
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), kOrderLds + lds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
