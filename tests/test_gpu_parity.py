@@ -112,9 +112,30 @@ def test_golden_candidates(torch):
 
 # ------------------------------------------------------------------ workloads
 
+_WORKLOAD_ORACLE = {}
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 def test_workload_parity(torch, cfg):
-    full_parity(torch, I.make_problem(cfg), f"workload {cfg}")
+    _, want = full_parity(torch, I.make_problem(cfg), f"workload {cfg}")
+    _WORKLOAD_ORACLE[cfg] = (want["flow_value"], want["best"])
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_workload_parity_value_only(torch, cfg):
+    """The path the benchmark times: no flow assignment or cut requested, so the max-flow may
+    take its value-only shortcuts (the pre-passes of the workgroup plans, the direct minimum
+    cut); every flow value of the full batch and the best equal the oracle's."""
+    prob = I.make_problem(cfg)
+    say(f"workload {cfg} value only: N={prob.n_cand}")
+    got = run_gpu(torch, prob, flows=False)
+    if cfg not in _WORKLOAD_ORACLE:
+        res = hxo.score_batch(prob, n_threads=N_THREADS)
+        _WORKLOAD_ORACLE[cfg] = (res["flow_value"], res["best"])
+    want_fv, want_best = _WORKLOAD_ORACLE[cfg]
+    assert np.array_equal(got["flow_value"], want_fv), \
+        f"flow values differ at {np.flatnonzero(got['flow_value'] != want_fv)[:8].tolist()}"
+    assert got["best"] == want_best
 
 
 @pytest.mark.parametrize("cfg,n", [(1, 1), (2, 7), (3, 1000), (4, 777), (3, 4097)])
