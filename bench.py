@@ -568,7 +568,7 @@ def chain_main(args, torch, hx, I):
     h_role = torch.empty((prob.max_groups, n), dtype=torch.uint8).pin_memory()
     d_assign, d_role = dp.tensors["assign"], dp.tensors["role"]
     for _ in range(args.warmup):
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
     per_round, probs = [], []
     for r in range(rounds):
@@ -584,7 +584,7 @@ def chain_main(args, torch, hx, I):
         torch.cuda.synchronize()
         h2d_ms = (time.perf_counter() - t) * 1000.0
         t = time.perf_counter()
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
         torch.cuda.synchronize()
         score_ms = (time.perf_counter() - t) * 1000.0
         bi, bv = (int(x) for x in ws.best.cpu().numpy())
@@ -599,7 +599,7 @@ def chain_main(args, torch, hx, I):
     # per-kernel durations: the last round's batch scored again with libhx's kernel events
     hx.profile(True)
     for _ in range(args.steps):
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
     prof = hx.profile_read()
     hx.profile(False)
@@ -804,7 +804,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     for _ in range(args.warmup):
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
 
     # Timed region: K steps and nothing else (event markers between the calls cost the GPU a
@@ -812,7 +812,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
@@ -828,7 +828,7 @@ def main():
     for _ in range(args.steps):
         d_assign.copy_(h_assign, non_blocking=True)
         d_role.copy_(h_role, non_blocking=True)
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
     ms_h2d = (time.perf_counter() - t0) * 1000.0 / args.steps
 
@@ -855,7 +855,7 @@ def main():
     # its kernels on this stream (kept out of the timed region above).
     hx.profile(True)
     for _ in range(args.steps):
-        hx.score(dp, ws)
+        hx.score_batch(dp, ws)
     torch.cuda.synchronize()
     prof = hx.profile_read()
     hx.profile(False)

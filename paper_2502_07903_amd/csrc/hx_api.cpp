@@ -389,6 +389,32 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 
+int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
+                   const hx_candidates* cand, const hx_cost_out* cost, const hx_flownet* net, int32_t* flow_value,
+                   int32_t* best, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    int rc = check_problem(cluster, model, wl, space, cand);
+    if (rc || (rc = check_cost(cost)) || (rc = check_net_for(cluster, space, cand, net))) return rc;
+    if (!flow_value || !best) return HX_EINVAL;
+    if (!workspace || ((uintptr_t)workspace & 255) ||
+        workspace_bytes < hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand))
+        return HX_EINVAL;
+    if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
+    const hx::Problem p = make_problem(cluster, model, wl, space, cand);
+    const hx::FlowNet f = make_net(net);
+    hipError_t e = hx::launch_cost(p, make_cost(cost), workspace, stream);
+    if (e == hipSuccess) {
+        if (hx::flownet_values_direct(p) && hx::maxflow_workgroup_plan(net->max_p, net->max_d, net->max_pd)) {
+            e = hx::launch_flownet_values(p, make_cost(cost), f, flow_value, stream);
+            if (e == hipSuccess) e = hx::launch_maxflow_unsettled(f, flow_value, round_budget(), stream);
+        } else {
+            e = hx::launch_flownet(p, make_cost(cost), f, stream);
+            if (e == hipSuccess) e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream);
+        }
+    }
+    if (e == hipSuccess) e = hx::launch_best(flow_value, cand->n_cand, best, stream);
+    return e == hipSuccess ? HX_OK : hip_error(e);
+}
+
 int hx_edge_classes(const hx_flownet* net, const int32_t* flow_value, const int32_t* kv_flow, uint8_t* node_cls,
                     uint8_t* kv_cls, hipStream_t stream) {
     int rc = check_net_shape(net);

@@ -728,6 +728,109 @@ hipError_t launch_kv_gpu(const Problem& p, const FlowNet& f, const CostOut& o, h
     return hipSuccess;
 }
 
+// Value-only scoring of per-GPU networks (hx_score_batch): a KV edge's capacity depends only on
+// its link, so whether a network's every KV edge can carry min(a_i, b_j) (a_i the prefill
+// node's source-or-node capacity, b_j the decode node's node-or-sink capacity) can be read off a
+// table of link capacities without writing the edges.  Such a network's maximum flow is
+// U = min(sum a, sum b) (the dominant-KV closed form of the max-flow kernel); only the others
+// get their KV rows written and flow_value -1, for the max-flow kernel to solve.  A lane per
+// candidate; the workgroup tabulates every link's capacity ([G][G] int32 in LDS, G <= 128) and
+// each GPU's smallest outgoing one, rmin[g]: every arc of prefill GPU g is dominant when
+// rmin[g] >= min(a_i, max_j b_j), which settles most networks without visiting their arcs; the
+// rest are checked arc by arc (stopping at the first thin arc).  Edges with an end of capacity 0
+// never bind (min(a_i, b_j) = 0), and an infeasible replica's GPUs carry 0.
+constexpr int kValueBlock = 256;
+
+__host__ __device__ inline size_t value_lds_bytes(int G) { return sizeof(int32_t) * ((size_t)G * G + G); }
+
+template <bool kCls>
+__global__ void __launch_bounds__(kValueBlock) pergpu_value_kernel(Problem p, CostOut o, FlowNet f, int32_t* flow_value) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char sm[];
+    const int G = p.G;
+    int32_t* tab = reinterpret_cast<int32_t*>(sm);  // [G][G]
+    int32_t* rmin = tab + G * G;                    // [G]
+    double vl[HX_MAX_CLASSES];
+#pragma unroll
+    for (int k = 0; k < HX_MAX_CLASSES; ++k)
+        vl[k] = (2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B) * (double)p.L;
+    for (int x = threadIdx.x; x < G * G; x += kValueBlock) {
+        const int g = x / G, h = x - g * G;
+        tab[x] = g == h ? 0 : kv_gpu_cap<kCls>(p, vl, g, h);
+    }
+    __syncthreads();
+    for (int g = threadIdx.x; g < G; g += kValueBlock) {
+        int32_t m = HX_CAP_MAX;
+        for (int h = 0; h < G; ++h)
+            if (h != g && tab[g * G + h] < m) m = tab[g * G + h];
+        rmin[g] = m;
+    }
+    __syncthreads();
+    const int64_t N = p.N;
+    const int64_t n = (int64_t)blockIdx.x * kValueBlock + threadIdx.x;
+    if (n >= N) return;
+    const int P = f.n_p[n], D = f.n_d[n];
+    if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || (int64_t)P * D > f.max_pd) {
+        flow_value[n] = -1;  // outside the plan: the max-flow kernel reports it
+        return;
+    }
+    long long sb = 0;
+    int32_t bmax = 0;
+    for (int j = 0; j < D; ++j) {
+        const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+        const int32_t b = c < t ? c : t;
+        sb += b;
+        bmax = b > bmax ? b : bmax;
+    }
+    long long sa = 0;
+    bool any_a = false, quick = true;
+    for (int i = 0; i < P; ++i) {
+        const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+        const int32_t a = s < c ? s : c;
+        sa += a;
+        if (a > 0) {
+            any_a = true;
+            const int g = f.p_slot[(int64_t)i * N + n];
+            quick = quick && rmin[g] >= (a < bmax ? a : bmax);
+        }
+    }
+    bool dominant = quick;
+    if (!quick)
+        for (int i = 0; i < P && dominant; ++i) {
+            const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
+            const int32_t a = s < c ? s : c;
+            if (a <= 0) continue;
+            const int g = f.p_slot[(int64_t)i * N + n];
+            for (int j = 0; j < D; ++j) {
+                const int32_t cd = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
+                const int32_t b = cd < t ? cd : t;
+                if (b <= 0) continue;
+                const int h = f.d_slot[(int64_t)j * N + n];
+                if (tab[g * G + h] < (a < b ? a : b)) {
+                    dominant = false;
+                    break;
+                }
+            }
+        }
+    if (dominant) {
+        // < 2^31: the smaller side has at most 127 nodes of at most 2^24 - 1
+        flow_value[n] = (!any_a || bmax <= 0) ? 0 : (int32_t)(sa < sb ? sa : sb);
+        return;
+    }
+    // a thin arc: the max-flow kernel solves this network from its KV rows
+    for (int i = 0; i < P; ++i) {
+        const int g = f.p_slot[(int64_t)i * N + n];
+        const int kg = p.assign[(int64_t)g * N + n];
+        const bool okg = kg < p.Kmax && o.tp[(int64_t)kg * N + n] > 0;
+        for (int j = 0; j < D; ++j) {
+            const int h = f.d_slot[(int64_t)j * N + n];
+            const int kh = p.assign[(int64_t)h * N + n];
+            const bool okh = kh < p.Kmax && o.tp[(int64_t)kh * N + n] > 0;
+            f.kv_cap[(int64_t)(i * D + j) * N + n] = okg && okh ? tab[g * G + h] : 0;
+        }
+    }
+    flow_value[n] = -1;
+}
+
 template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
     prof_mark(kKNodes, false, s);
@@ -767,6 +870,44 @@ hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, 
         case 2: return launch_w<2>(p, o, f, s);
         default: return launch_w<4>(p, o, f, s);
     }
+}
+
+}  // namespace hx
+
+namespace hx {
+
+bool flownet_values_direct(const Problem& p) { return p.granularity == 1 && p.G <= kGpuTableMaxG; }
+
+hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
+                                 hipStream_t s) {
+    prof_mark(kKNodes, false, s);
+    switch (mask_words(p.G)) {
+        case 1: hipLaunchKernelGGL(nodes_kernel<1>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s,
+                                   p, o, f); break;
+        default: hipLaunchKernelGGL(nodes_kernel<2>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s,
+                                    p, o, f); break;
+    }
+    prof_mark(kKNodes, true, s);
+    const size_t lds = value_lds_bytes(p.G);
+    prof_mark(kKKv, false, s);
+    const dim3 grid((p.N + kValueBlock - 1) / kValueBlock);
+    if (p.n_cls > 0) {
+        if (lds > 64 * 1024) {
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(pergpu_value_kernel<true>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(pergpu_value_kernel<true>, grid, dim3(kValueBlock), lds, s, p, o, f, flow_value);
+    } else {
+        if (lds > 64 * 1024) {
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(pergpu_value_kernel<false>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(pergpu_value_kernel<false>, grid, dim3(kValueBlock), lds, s, p, o, f, flow_value);
+    }
+    prof_mark(kKKv, true, s);
+    return hipGetLastError();
 }
 
 }  // namespace hx

@@ -778,6 +778,25 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd) {
     return bytes <= kMaxLds ? bytes : 0;
 }
 
+bool maxflow_workgroup_plan(int32_t max_p, int32_t max_d, int32_t max_pd) {
+    return segment_lanes(max_p, max_d, max_pd) > 64;
+}
+
+hipError_t launch_maxflow_unsettled(const FlowNet& f, int32_t* flow_value, int32_t round_budget, hipStream_t s) {
+    const int seg = segment_lanes(f.max_p, f.max_d, f.max_pd);
+    const size_t lds = mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
+    const int blocks = 8 * ((f.N + 7) / 8);
+    prof_mark(kKMaxflow, false, s);
+    if (seg == 128)
+        hipLaunchKernelGGL((maxflow_kernel<128, false>), dim3(blocks), dim3(128), lds, s, f, flow_value, nullptr,
+                           nullptr, round_budget, nullptr);
+    else
+        hipLaunchKernelGGL((maxflow_kernel<256, false>), dim3(blocks), dim3(256), lds, s, f, flow_value, nullptr,
+                           nullptr, round_budget, nullptr);
+    prof_mark(kKMaxflow, true, s);
+    return hipGetLastError();
+}
+
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           unsigned long long* stats, hipStream_t s) {
     switch (segment_lanes(f.max_p, f.max_d, f.max_pd)) {

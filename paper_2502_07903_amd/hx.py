@@ -93,7 +93,7 @@ class hx_flownet(C.Structure):
 
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_eval_static", "hx_static_scratch_bytes", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
-           "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_edge_classes", "hx_guided_moves",
+           "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_score_batch", "hx_edge_classes", "hx_guided_moves",
            "hx_gather_candidates",
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
            "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error",
@@ -127,6 +127,9 @@ def lib() -> C.CDLL:
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_maxflow_stats.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_best_candidate.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+        L.hx_score_batch.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
+                                     P(hx_cost_out), P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                     C.c_void_p]
         L.hx_edge_classes.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_guided_moves.argtypes = [C.c_int32, C.c_int32, P(hx_candidates), P(hx_flownet), C.c_void_p,
                                       C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
@@ -423,6 +426,16 @@ def score(dp: DeviceProblem, ws: Workspace, stream=None) -> None:
     best_candidate(ws.flow_value, ws.best, dp.n_cand, stream)
 
 
+def score_batch(dp: DeviceProblem, ws: Workspace, stream=None) -> None:
+    """Enqueues the whole hot path in one call, value only (hx_score_batch): cost outputs, node
+    rows, flow values and the best; kv_cap rows only where a network needs them."""
+    o = ws.cost.struct()
+    f = ws.net.struct()
+    _check(lib().hx_score_batch(C.byref(dp.cluster), dp.model, dp.workload, dp.space, C.byref(dp.cand), C.byref(o),
+                                C.byref(f), _ptr(ws.flow_value), _ptr(ws.best), _ptr(ws.cost.workspace),
+                                C.c_size_t(int(ws.cost.workspace.numel())), _stream(stream)), "hx_score_batch")
+
+
 # ------------------------------------------------------------------ refinement (Sec. 3.4)
 
 def edge_classes(net: FlowNetBuffers, flow_value, kv_flow, node_cls, kv_cls, stream=None):
@@ -492,7 +505,7 @@ class Refiner:
         score(p, pw, stream)
         edge_classes(pw.net, pw.flow_value, pw.kv_flow, self.node_cls, self.kv_cls, stream)
         guided_moves(p, pw.net, self.node_cls, rnd, ch.tensors["assign"], ch.tensors["role"], self.move, stream)
-        score(ch, cw, stream)
+        score_batch(ch, cw, stream)
         gather_candidates(ch, cw.best[:1], p.tensors["assign"], p.tensors["role"], stream)
 
 

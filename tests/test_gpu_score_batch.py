@@ -1,0 +1,119 @@
+"""hx_score_batch, the whole scoring path in one value-only call, through the C-ABI: on every
+workload its cost outputs, node rows, flow values and best equal the four calls' bit for bit (and
+the KV rows too at replica granularity); on per-GPU networks whose KV edges bind (slow links) the
+networks it hands to push-relabel are solved to the oracle's values; ragged batch sizes and
+request classes."""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import hxo
+from paper_2502_07903_amd import hx
+from paper_2502_07903_amd import inputs as I
+from tests import helpers as Hh
+
+pytestmark = pytest.mark.gpu
+N_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def say(msg: str) -> None:
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm GPU (torch.cuda.is_available() is False)")
+    hx.lib()
+    return T
+
+
+def _both(torch, prob):
+    """(four calls, one call): host copies of every output."""
+    dp = hx.DeviceProblem.upload(prob)
+    out = []
+    for fused in (False, True):
+        ws = hx.Workspace.for_problem(dp, flows=False)
+        for t in (ws.flow_value, ws.best, ws.net.kv_cap):
+            t.fill_(-7)
+        if fused:
+            hx.score_batch(dp, ws)
+        else:
+            hx.score(dp, ws)
+        torch.cuda.synchronize()
+        out.append(dict(cost={k: getattr(ws.cost, k).cpu().numpy() for k in ("tp", "pp", "bmax", "cap", "lat", "members")},
+                        net=ws.net.host(), flow_value=ws.flow_value.cpu().numpy(),
+                        best=tuple(int(x) for x in ws.best.cpu().numpy())))
+    return out
+
+
+def _same(a, b, granularity):
+    for k in a["cost"]:
+        assert np.array_equal(a["cost"][k].view(np.uint8), b["cost"][k].view(np.uint8)), f"cost {k} differs"
+    assert np.array_equal(a["net"]["n_p"], b["net"]["n_p"]) and np.array_equal(a["net"]["n_d"], b["net"]["n_d"])
+    up, ud, upd = Hh.used_rows(a["net"])
+    for k in ("p_slot", "src_cap", "p_cap"):
+        assert np.array_equal(a["net"][k][up], b["net"][k][up]), k
+    for k in ("d_slot", "d_cap", "sink_cap"):
+        assert np.array_equal(a["net"][k][ud], b["net"][k][ud]), k
+    if granularity == 0:
+        assert np.array_equal(a["net"]["kv_cap"][upd], b["net"]["kv_cap"][upd])
+    bad = np.flatnonzero(a["flow_value"] != b["flow_value"])
+    assert bad.size == 0, f"flow values differ at {bad[:8].tolist()}"
+    assert a["best"] == b["best"]
+
+
+@pytest.mark.parametrize("cfg,n", [(1, None), (2, None), (3, None), (4, None), (5, None), (3, 1), (5, 7), (5, 777),
+                                   (2, 4097)])
+def test_score_batch_matches_four_calls(torch, cfg, n):
+    prob = I.make_problem(cfg, n_cand=n)
+    say(f"hx_score_batch vs four calls: workload {cfg}, N={prob.n_cand}")
+    four, one = _both(torch, prob)
+    _same(four, one, prob.granularity)
+    # and the oracle, on the whole batch (workloads 1-3) or a sample
+    idx = np.arange(prob.n_cand) if cfg <= 3 else np.unique(np.concatenate(
+        [np.random.default_rng(cfg).choice(prob.n_cand, min(prob.n_cand, 1024), replace=False), [one["best"][0]]]))
+    want = hxo.score_batch(prob.subset(idx), n_threads=N_THREADS)
+    assert np.array_equal(one["flow_value"][idx], want["flow_value"])
+    if cfg <= 3:
+        assert one["best"] == want["best"]
+
+
+def test_score_batch_request_classes_per_gpu(torch):
+    prob = I.make_problem(5, n_cand=2048)
+    prob = dataclasses.replace(prob, classes=I.length_classes(I.WORKLOADS[5], 4))
+    say("hx_score_batch vs four calls: per-GPU networks, four request classes")
+    four, one = _both(torch, prob)
+    _same(four, one, 1)
+
+
+def test_score_batch_per_gpu_binding_kv(torch):
+    """The 128-GPU cluster with every link 100 times slower: KV edges fall below the node shares,
+    so networks are handed to push-relabel with their KV rows; their values equal the oracle's
+    (a sample) and the four calls' (all)."""
+    prob = I.make_problem(5, n_cand=2048)
+    cl = dataclasses.replace(prob.cluster, beta=np.ascontiguousarray(np.asarray(prob.cluster.beta) * 0.01))
+    prob = dataclasses.replace(prob, cluster=cl)
+    say("hx_score_batch: per-GPU networks with binding KV edges")
+    four, one = _both(torch, prob)
+    _same(four, one, 1)
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    st = hx.maxflow_stats(_net_of(torch, dp, ws), torch.empty_like(ws.flow_value))
+    assert st["push_relabel"] > 100, st
+    idx = np.random.default_rng(51).choice(prob.n_cand, 96, replace=False)
+    want = hxo.score_batch(prob.subset(idx), n_threads=N_THREADS)
+    assert np.array_equal(one["flow_value"][idx], want["flow_value"])
+
+
+def _net_of(torch, dp, ws):
+    """The full network of the batch (the four calls' cost model and builder), for the counters."""
+    hx.cost_eval(dp, ws.cost)
+    hx.build_flownet(dp, ws.cost, ws.net)
+    torch.cuda.synchronize()
+    return ws.net
