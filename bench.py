@@ -139,6 +139,38 @@ def hbm_bytes_per_step(prob, dims, n_p, n_d) -> dict:
     return dict(cost=cost, flownet=flownet, maxflow=maxflow, best=best)
 
 
+def kernel_bytes(prob, n_p, n_d, settled_per_gpu: bool = False) -> dict:
+    """Algorithmic HBM bytes of one launch of each streaming kernel (every input read once,
+    every output written once):
+      decode   assign and role of each candidate in, the group member masks out;
+      scatter  the member masks in, one unit record (8 B + the mask) per present group out;
+      nodes    each slot's mask, role and capacity (and per GPU its assign entry at granularity
+               1) in, the counts and 12 B per node out;
+      kv       replica networks: per used KV row the two slots, the two strategies and masks in,
+               4 B out; per-GPU networks settled from the link table: the node rows in (12 B per
+               node and the counts), the flow value out;
+      maxflow  the network in (node rows, KV rows), the flow value out;
+      best     4 B per candidate."""
+    G, K, N = prob.n_gpus, prob.max_groups, prob.n_cand
+    W = 1 if G <= 64 else (2 if G <= 128 else 4)
+    groups = 0
+    for n0 in range(0, N, 65536):
+        a = prob.assign[:, n0:n0 + 65536]
+        groups += int(sum(((a == k).any(axis=0)).sum() for k in range(K)))
+    nodes = int(n_p.astype(np.int64).sum() + n_d.astype(np.int64).sum())
+    pd = int((n_p.astype(np.int64) * n_d).sum())
+    gran1 = prob.granularity == 1
+    out = {
+        "decode": N * (G + K) + N * K * 8 * W,
+        "scatter": N * K * 8 * W + groups * 8 * (1 + W),
+        "nodes": N * K * (8 * W + 1 + 4) + (N * G if gran1 else 0) + N * 8 + nodes * 12,
+        "kv": (N * 8 + nodes * 12 + N * 4) if settled_per_gpu else (N * 8 + pd * (8 + 4 + 16 * W + 4)),
+        "maxflow": N * 8 + nodes * 16 + pd * 4 + N * 4,
+        "best": N * 4 + 8,
+    }
+    return out
+
+
 def cpu_model() -> str:
     """The host CPU: model name, vendor, family / model / stepping (first processor in
     /proc/cpuinfo) and the logical CPU count, or "unknown"."""
@@ -286,7 +318,7 @@ def eval_fp64_counts(prob):
     return float(total), float(divs)
 
 
-def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
+def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload, kbytes=None):
     """Roofline object of one kernel: FP64 ALU for the strategy evaluation, LDS for the
     max-flow, HBM for the streaming kernels."""
     t_dom = kernel_us[dominant] * 1e-6
@@ -307,9 +339,12 @@ def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload):
                 "peak": LDS_PEAK_GBS, "unit": "GB/s", "frac": achieved / LDS_PEAK_GBS,
                 "traffic": kernel_traffic("maxflow", workload, prob), "algorithmic_bytes_per_launch": alg}
     else:
-        call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(dominant,
-                                                                                                          dominant)
-        alg = float(hbm[call])
+        if kbytes is not None and dominant in kbytes:
+            alg = float(kbytes[dominant])
+        else:
+            call = {"setup": "cost", "decode": "cost", "scatter": "cost", "nodes": "flownet", "kv": "flownet"}.get(
+                dominant, dominant)
+            alg = float(hbm[call])
         achieved = alg / t_dom / 1e9
         roof = {"kernel": dominant, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS, "traffic": kernel_traffic(dominant, workload, prob),
@@ -376,7 +411,8 @@ def refine_main(args, torch, hx, I):
     if dominant in scoring:
         # a round launches each scoring kernel twice, on the parent (one candidate) and on the
         # children; the roofline charges the children's work with both launches' time
-        roof = roofline_for(dominant, {dominant: 1000.0 * kernel_ms_per_round[dominant]}, cp, hbm, n_p, n_d, cfg)
+        kb = kernel_bytes(cp, n_p, n_d, settled_per_gpu=cp.n_gpus <= 128)
+        roof = roofline_for(dominant, {dominant: 1000.0 * kernel_ms_per_round[dominant]}, cp, hbm, n_p, n_d, cfg, kb)
     else:
         alg = float(hbm.get(dominant, 0))
         t = kernel_ms_per_round[dominant] * 1e-3
@@ -604,13 +640,18 @@ def chain_main(args, torch, hx, I):
     prof = hx.profile_read()
     hx.profile(False)
     kernel_us = {k: 1000.0 * ms / c for k, (ms, c) in prof.items() if c > 0}
+    # the counters need every network in full: hx_score_batch leaves the KV rows of the networks
+    # it settled from the link table unwritten, so the network is built again by the two calls
+    hx.cost_eval(dp, ws.cost)
+    hx.build_flownet(dp, ws.cost, ws.net)
     mf = hx.maxflow_stats(ws.net, torch.empty_like(ws.flow_value))
     last = probs[-1][0]
     n_p = ws.net.n_p.cpu().numpy()
     n_d = ws.net.n_d.cpu().numpy()
     hbm = hbm_bytes_per_step(last, ws.net.dims, n_p, n_d)
+    kb = kernel_bytes(last, n_p, n_d, settled_per_gpu=last.granularity == 1 and last.n_gpus <= 128)
     dominant = max(kernel_us, key=kernel_us.get)
-    roof = roofline_for(dominant, kernel_us, last, hbm, n_p, n_d, cfg)
+    roof = roofline_for(dominant, kernel_us, last, hbm, n_p, n_d, cfg, kb)
     out = {
         "metric": METRIC,
         "value": value,
@@ -874,7 +915,8 @@ def main():
     best = [int(x) for x in ws.best.cpu().numpy()]
     dominant = max(kernel_us, key=kernel_us.get)
     hbm = hbm_bytes_per_step(prob, dims, n_p, n_d)
-    roof = roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, args.workload)
+    kb = kernel_bytes(prob, n_p, n_d, settled_per_gpu=prob.granularity == 1 and prob.n_gpus <= 128)
+    roof = roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, args.workload, kb)
     roof["measured_hbm_copy_gbs"] = measured_copy_gbs(torch)
 
     out = {

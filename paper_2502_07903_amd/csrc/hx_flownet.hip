@@ -111,6 +111,93 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
     f.n_d[n] = nd;
 }
 
+// Per-GPU nodes with every group's role, capacity, size and a running member count staged in
+// LDS ([Kmax][64] per field, loads of eight slots issued together), then the GPUs taken in
+// ascending id with their group ids loaded eight at a time: the k-th member of a group met so far
+// is its rank.  The same rows as nodes_kernel's per-GPU branch with ~(Kmax + G)/8 memory round
+// trips per lane instead of two per GPU.  Kmax <= kNodesGpuMaxK (the staging fits 64 KB).
+constexpr int kNodesGpuMaxK = 128;
+__host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax * 64 * 7; }
+
+template <int W>
+__global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, FlowNet f) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
+    const int lane = threadIdx.x;
+    const int Kmax = p.Kmax;
+    int32_t* gcap = reinterpret_cast<int32_t*>(sm);        // [Kmax][64]
+    uint8_t* grole = sm + sizeof(int32_t) * (size_t)Kmax * 64;  // [Kmax][64]
+    uint8_t* gsize = grole + (size_t)Kmax * 64;              // [Kmax][64]
+    uint8_t* gseen = gsize + (size_t)Kmax * 64;              // [Kmax][64]: members met so far
+    const int64_t N = p.N;
+    const int64_t n = (int64_t)blockIdx.x * 64 + lane;
+    if (n >= N) return;  // no barrier below: every lane stages and reads its own column
+    constexpr int kC = 8;
+    for (int k0 = 0; k0 < Kmax; k0 += kC) {
+        int32_t cp[kC];
+        int rl[kC], sz[kC];
+#pragma unroll
+        for (int x = 0; x < kC; ++x) {
+            const int k = k0 + x;
+            const bool ok = k < Kmax;
+            sz[x] = ok ? mask_size<W>(o.members, k, N, (int)n) : 0;
+            rl[x] = ok ? p.role[(int64_t)k * N + n] : HX_UNUSED;
+            cp[x] = ok ? o.cap[(int64_t)k * N + n] : 0;
+        }
+#pragma unroll
+        for (int x = 0; x < kC; ++x) {
+            const int k = k0 + x;
+            if (k >= Kmax) break;
+            gcap[k * 64 + lane] = cp[x];
+            grole[k * 64 + lane] = (uint8_t)rl[x];
+            gsize[k * 64 + lane] = (uint8_t)sz[x];
+            gseen[k * 64 + lane] = 0;
+        }
+    }
+    int np = 0, nd = 0;
+    for (int g0 = 0; g0 < p.G; g0 += kC) {
+        int kk[kC];
+#pragma unroll
+        for (int x = 0; x < kC; ++x) kk[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
+#pragma unroll
+        for (int x = 0; x < kC; ++x) {
+            const int g = g0 + x, k = kk[x];
+            if (g >= p.G || k >= Kmax) continue;
+            const int r = grole[k * 64 + lane];
+            if (r != HX_PREFILL && r != HX_DECODE) continue;
+            const int rk = gseen[k * 64 + lane];
+            gseen[k * 64 + lane] = (uint8_t)(rk + 1);
+            const int sz = gsize[k * 64 + lane];
+            const int32_t C = gcap[k * 64 + lane];
+            const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
+            if (r == HX_PREFILL) {
+                const int64_t e = (int64_t)np * N + n;
+                f.p_slot[e] = g;
+                f.src_cap[e] = p.coord_cap;
+                f.p_cap[e] = share;
+                ++np;
+            } else {
+                const int64_t e = (int64_t)nd * N + n;
+                f.d_slot[e] = g;
+                f.d_cap[e] = share;
+                f.sink_cap[e] = p.coord_cap;
+                ++nd;
+            }
+        }
+    }
+    f.n_p[n] = np;
+    f.n_d[n] = nd;
+}
+
+// Launches the node rows: nodes_gpu_kernel for per-GPU networks of up to kNodesGpuMaxK slots,
+// nodes_kernel otherwise.
+template <int W>
+void launch_nodes(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
+    if (p.granularity == 1 && p.Kmax <= kNodesGpuMaxK)
+        hipLaunchKernelGGL(nodes_gpu_kernel<W>, dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p, o, f);
+    else
+        hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
+}
+
 // Members of group k in ascending GPU id into out[r * stride]; returns the count.
 template <int W>
 __device__ __forceinline__ int expand(const uint64_t* gm, int k, int64_t N, int n, uint8_t* out, int stride) {
@@ -834,7 +921,7 @@ __global__ void __launch_bounds__(kValueBlock) pergpu_value_kernel(Problem p, Co
 template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
     prof_mark(kKNodes, false, s);
-    hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
+    launch_nodes<W>(p, o, f, s);
     prof_mark(kKNodes, true, s);
     const int64_t lanes = (int64_t)f.max_pd * p.N;
     const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
@@ -881,12 +968,8 @@ bool flownet_values_direct(const Problem& p) { return p.granularity == 1 && p.G 
 hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
                                  hipStream_t s) {
     prof_mark(kKNodes, false, s);
-    switch (mask_words(p.G)) {
-        case 1: hipLaunchKernelGGL(nodes_kernel<1>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s,
-                                   p, o, f); break;
-        default: hipLaunchKernelGGL(nodes_kernel<2>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s,
-                                    p, o, f); break;
-    }
+    if (mask_words(p.G) == 1) launch_nodes<1>(p, o, f, s);
+    else launch_nodes<2>(p, o, f, s);
     prof_mark(kKNodes, true, s);
     const size_t lds = value_lds_bytes(p.G);
     prof_mark(kKKv, false, s);
