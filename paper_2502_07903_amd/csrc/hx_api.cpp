@@ -389,6 +389,12 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 
+size_t hx_score_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    const size_t c = hx_cost_workspace_bytes(n_gpus, max_groups, n_cand);
+    if (c == 0) return 0;
+    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus) + 255) & ~(size_t)255);
+}
+
 int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
                    const hx_candidates* cand, const hx_cost_out* cost, const hx_flownet* net, int32_t* flow_value,
                    int32_t* best, void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -396,7 +402,7 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
     if (rc || (rc = check_cost(cost)) || (rc = check_net_for(cluster, space, cand, net))) return rc;
     if (!flow_value || !best) return HX_EINVAL;
     if (!workspace || ((uintptr_t)workspace & 255) ||
-        workspace_bytes < hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand))
+        workspace_bytes < hx_score_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand))
         return HX_EINVAL;
     if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
     const hx::Problem p = make_problem(cluster, model, wl, space, cand);
@@ -404,7 +410,11 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
     hipError_t e = hx::launch_cost(p, make_cost(cost), workspace, stream);
     if (e == hipSuccess) {
         if (hx::flownet_values_direct(p) && hx::maxflow_workgroup_plan(net->max_p, net->max_d, net->max_pd)) {
-            e = hx::launch_flownet_values(p, make_cost(cost), f, flow_value, stream);
+            // the link table follows the cost model's scratch, 256-byte aligned
+            const size_t off = (hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
+                               ~(size_t)255;
+            void* table = static_cast<unsigned char*>(workspace) + off;
+            e = hx::launch_flownet_values(p, make_cost(cost), f, flow_value, table, stream);
             if (e == hipSuccess) e = hx::launch_maxflow_unsettled(f, flow_value, round_budget(), stream);
         } else {
             e = hx::launch_flownet(p, make_cost(cost), f, stream);

@@ -119,8 +119,18 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
 constexpr int kNodesGpuMaxK = 128;
 __host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax * 64 * 7; }
 
-template <int W>
-__global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, FlowNet f) {
+// kValue (hx_score_batch): the kernel also settles the network's value.  Every KV edge of a per-GPU
+// network has its link's capacity (tab: [G][G], computed once per call), so when every edge can
+// carry min(a_i, b_j) (a_i the prefill node's source-or-node capacity, b_j the decode node's
+// node-or-sink capacity) the maximum flow is min(sum a, sum b), the max-flow kernel's
+// dominant-KV closed form, and the KV rows are never needed.  rmin[g], the smallest capacity of
+// GPU g's links, decides most networks on the fly: an edge out of prefill node i can be thin
+// only if rmin[g_i] < min(a_i, b_max).  The others are checked edge by edge; a network with a
+// thin edge gets its KV rows and flow_value -1, for the max-flow kernel.  Edges with an end of
+// capacity 0 never bind (min(a_i, b_j) = 0); an infeasible replica's GPUs carry 0.
+template <int W, bool kValue>
+__global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, FlowNet f, const int32_t* tab,
+                                                       const int32_t* rmin, int32_t* flow_value) {
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int lane = threadIdx.x;
     const int Kmax = p.Kmax;
@@ -154,6 +164,9 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
         }
     }
     int np = 0, nd = 0;
+    long long sa = 0, sb = 0;  // kValue
+    int32_t bmax = 0, t1 = 0x7fffffff;
+    bool any_a = false;
     for (int g0 = 0; g0 < p.G; g0 += kC) {
         int kk[kC];
 #pragma unroll
@@ -175,25 +188,77 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
                 f.src_cap[e] = p.coord_cap;
                 f.p_cap[e] = share;
                 ++np;
+                if (kValue) {
+                    const int32_t a = p.coord_cap < share ? p.coord_cap : share;
+                    sa += a;
+                    if (a > 0) {
+                        any_a = true;
+                        const int32_t m = rmin[g];
+                        if (m < a && m < t1) t1 = m;
+                    }
+                }
             } else {
                 const int64_t e = (int64_t)nd * N + n;
                 f.d_slot[e] = g;
                 f.d_cap[e] = share;
                 f.sink_cap[e] = p.coord_cap;
                 ++nd;
+                if (kValue) {
+                    const int32_t b = share < p.coord_cap ? share : p.coord_cap;
+                    sb += b;
+                    bmax = b > bmax ? b : bmax;
+                }
             }
         }
     }
     f.n_p[n] = np;
     f.n_d[n] = nd;
+    if (!kValue) return;
+    const int G = p.G;
+    bool dominant = t1 >= bmax;
+    if (!dominant) {  // edge by edge (this lane's own rows, just written)
+        bool thin = false;
+        for (int i = 0; i < np && !thin; ++i) {
+            const int32_t ps = f.src_cap[(int64_t)i * N + n], pc = f.p_cap[(int64_t)i * N + n];
+            const int32_t a = ps < pc ? ps : pc;
+            if (a <= 0) continue;
+            const int g = f.p_slot[(int64_t)i * N + n];
+            for (int j = 0; j < nd && !thin; ++j) {
+                const int32_t dc = f.d_cap[(int64_t)j * N + n], dt = f.sink_cap[(int64_t)j * N + n];
+                const int32_t b = dc < dt ? dc : dt;
+                thin = b > 0 && tab[g * G + f.d_slot[(int64_t)j * N + n]] < (a < b ? a : b);
+            }
+        }
+        dominant = !thin;
+    }
+    if (dominant) {
+        // < 2^31: the smaller side has at most 127 nodes of at most 2^24 - 1
+        flow_value[n] = (!any_a || bmax <= 0) ? 0 : (int32_t)(sa < sb ? sa : sb);
+        return;
+    }
+    // a thin edge: the max-flow kernel solves this network from its KV rows
+    for (int i = 0; i < np; ++i) {
+        const int g = f.p_slot[(int64_t)i * N + n];
+        const int kg = p.assign[(int64_t)g * N + n];
+        const bool okg = o.tp[(int64_t)kg * N + n] > 0;
+        for (int j = 0; j < nd; ++j) {
+            const int h = f.d_slot[(int64_t)j * N + n];
+            const int kh = p.assign[(int64_t)h * N + n];
+            const bool okh = o.tp[(int64_t)kh * N + n] > 0;
+            f.kv_cap[(int64_t)(i * nd + j) * N + n] = okg && okh ? tab[g * G + h] : 0;
+        }
+    }
+    flow_value[n] = -1;
 }
+
 
 // Launches the node rows: nodes_gpu_kernel for per-GPU networks of up to kNodesGpuMaxK slots,
 // nodes_kernel otherwise.
 template <int W>
 void launch_nodes(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
     if (p.granularity == 1 && p.Kmax <= kNodesGpuMaxK)
-        hipLaunchKernelGGL(nodes_gpu_kernel<W>, dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p, o, f);
+        hipLaunchKernelGGL((nodes_gpu_kernel<W, false>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
+                           o, f, nullptr, nullptr, nullptr);
     else
         hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
 }
@@ -815,107 +880,34 @@ hipError_t launch_kv_gpu(const Problem& p, const FlowNet& f, const CostOut& o, h
     return hipSuccess;
 }
 
-// Value-only scoring of per-GPU networks (hx_score_batch): a KV edge's capacity depends only on
-// its link, so whether a network's every KV edge can carry min(a_i, b_j) (a_i the prefill
-// node's source-or-node capacity, b_j the decode node's node-or-sink capacity) can be read off a
-// table of link capacities without writing the edges.  Such a network's maximum flow is
-// U = min(sum a, sum b) (the dominant-KV closed form of the max-flow kernel); only the others
-// get their KV rows written and flow_value -1, for the max-flow kernel to solve.  A lane per
-// candidate; the workgroup tabulates every link's capacity ([G][G] int32 in LDS, G <= 128) and
-// each GPU's smallest outgoing one, rmin[g]: every arc of prefill GPU g is dominant when
-// rmin[g] >= min(a_i, max_j b_j), which settles most networks without visiting their arcs; the
-// rest are checked arc by arc (stopping at the first thin arc).  Edges with an end of capacity 0
-// never bind (min(a_i, b_j) = 0), and an infeasible replica's GPUs carry 0.
-constexpr int kValueBlock = 256;
-
-__host__ __device__ inline size_t value_lds_bytes(int G) { return sizeof(int32_t) * ((size_t)G * G + G); }
+// The capacity of every per-GPU KV link (kv_gpu_cap) and each GPU's smallest one, for
+// hx_score_batch: a workgroup per GPU row, its minimum by a workgroup reduction.
+constexpr int kLinkBlock = 256;
 
 template <bool kCls>
-__global__ void __launch_bounds__(kValueBlock) pergpu_value_kernel(Problem p, CostOut o, FlowNet f, int32_t* flow_value) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char sm[];
-    const int G = p.G;
-    int32_t* tab = reinterpret_cast<int32_t*>(sm);  // [G][G]
-    int32_t* rmin = tab + G * G;                    // [G]
+__global__ void __launch_bounds__(kLinkBlock) link_table_kernel(Problem p, int32_t* tab, int32_t* rmin) {
+    __shared__ int32_t red[kLinkBlock / 64];
+    const int g = blockIdx.x, G = p.G;
     double vl[HX_MAX_CLASSES];
 #pragma unroll
     for (int k = 0; k < HX_MAX_CLASSES; ++k)
         vl[k] = (2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B) * (double)p.L;
-    for (int x = threadIdx.x; x < G * G; x += kValueBlock) {
-        const int g = x / G, h = x - g * G;
-        tab[x] = g == h ? 0 : kv_gpu_cap<kCls>(p, vl, g, h);
+    int32_t m = HX_CAP_MAX;
+    for (int h = threadIdx.x; h < G; h += kLinkBlock) {
+        const int32_t c = g == h ? 0 : kv_gpu_cap<kCls>(p, vl, g, h);
+        tab[(int64_t)g * G + h] = c;
+        if (h != g && c < m) m = c;
     }
+    for (int off = 32; off > 0; off >>= 1) {
+        const int32_t o2 = __shfl_xor(m, off, 64);
+        m = o2 < m ? o2 : m;
+    }
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
     __syncthreads();
-    for (int g = threadIdx.x; g < G; g += kValueBlock) {
-        int32_t m = HX_CAP_MAX;
-        for (int h = 0; h < G; ++h)
-            if (h != g && tab[g * G + h] < m) m = tab[g * G + h];
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kLinkBlock / 64; ++w) m = red[w] < m ? red[w] : m;
         rmin[g] = m;
     }
-    __syncthreads();
-    const int64_t N = p.N;
-    const int64_t n = (int64_t)blockIdx.x * kValueBlock + threadIdx.x;
-    if (n >= N) return;
-    const int P = f.n_p[n], D = f.n_d[n];
-    if (P < 0 || D < 0 || P > f.max_p || D > f.max_d || (int64_t)P * D > f.max_pd) {
-        flow_value[n] = -1;  // outside the plan: the max-flow kernel reports it
-        return;
-    }
-    long long sb = 0;
-    int32_t bmax = 0;
-    for (int j = 0; j < D; ++j) {
-        const int32_t c = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
-        const int32_t b = c < t ? c : t;
-        sb += b;
-        bmax = b > bmax ? b : bmax;
-    }
-    long long sa = 0;
-    bool any_a = false, quick = true;
-    for (int i = 0; i < P; ++i) {
-        const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
-        const int32_t a = s < c ? s : c;
-        sa += a;
-        if (a > 0) {
-            any_a = true;
-            const int g = f.p_slot[(int64_t)i * N + n];
-            quick = quick && rmin[g] >= (a < bmax ? a : bmax);
-        }
-    }
-    bool dominant = quick;
-    if (!quick)
-        for (int i = 0; i < P && dominant; ++i) {
-            const int32_t s = f.src_cap[(int64_t)i * N + n], c = f.p_cap[(int64_t)i * N + n];
-            const int32_t a = s < c ? s : c;
-            if (a <= 0) continue;
-            const int g = f.p_slot[(int64_t)i * N + n];
-            for (int j = 0; j < D; ++j) {
-                const int32_t cd = f.d_cap[(int64_t)j * N + n], t = f.sink_cap[(int64_t)j * N + n];
-                const int32_t b = cd < t ? cd : t;
-                if (b <= 0) continue;
-                const int h = f.d_slot[(int64_t)j * N + n];
-                if (tab[g * G + h] < (a < b ? a : b)) {
-                    dominant = false;
-                    break;
-                }
-            }
-        }
-    if (dominant) {
-        // < 2^31: the smaller side has at most 127 nodes of at most 2^24 - 1
-        flow_value[n] = (!any_a || bmax <= 0) ? 0 : (int32_t)(sa < sb ? sa : sb);
-        return;
-    }
-    // a thin arc: the max-flow kernel solves this network from its KV rows
-    for (int i = 0; i < P; ++i) {
-        const int g = f.p_slot[(int64_t)i * N + n];
-        const int kg = p.assign[(int64_t)g * N + n];
-        const bool okg = kg < p.Kmax && o.tp[(int64_t)kg * N + n] > 0;
-        for (int j = 0; j < D; ++j) {
-            const int h = f.d_slot[(int64_t)j * N + n];
-            const int kh = p.assign[(int64_t)h * N + n];
-            const bool okh = kh < p.Kmax && o.tp[(int64_t)kh * N + n] > 0;
-            f.kv_cap[(int64_t)(i * D + j) * N + n] = okg && okh ? tab[g * G + h] : 0;
-        }
-    }
-    flow_value[n] = -1;
 }
 
 template <int W>
@@ -963,33 +955,30 @@ hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, 
 
 namespace hx {
 
-bool flownet_values_direct(const Problem& p) { return p.granularity == 1 && p.G <= kGpuTableMaxG; }
+bool flownet_values_direct(const Problem& p) {
+    return p.granularity == 1 && p.G <= kGpuTableMaxG && p.Kmax <= kNodesGpuMaxK;
+}
+
+size_t link_table_bytes(int32_t n_gpus) { return sizeof(int32_t) * ((size_t)n_gpus * n_gpus + n_gpus); }
 
 hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
-                                 hipStream_t s) {
-    prof_mark(kKNodes, false, s);
-    if (mask_words(p.G) == 1) launch_nodes<1>(p, o, f, s);
-    else launch_nodes<2>(p, o, f, s);
-    prof_mark(kKNodes, true, s);
-    const size_t lds = value_lds_bytes(p.G);
+                                 void* table, hipStream_t s) {
+    int32_t* tab = static_cast<int32_t*>(table);
+    int32_t* rmin = tab + (size_t)p.G * p.G;
     prof_mark(kKKv, false, s);
-    const dim3 grid((p.N + kValueBlock - 1) / kValueBlock);
-    if (p.n_cls > 0) {
-        if (lds > 64 * 1024) {
-            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(pergpu_value_kernel<true>),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-        }
-        hipLaunchKernelGGL(pergpu_value_kernel<true>, grid, dim3(kValueBlock), lds, s, p, o, f, flow_value);
-    } else {
-        if (lds > 64 * 1024) {
-            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(pergpu_value_kernel<false>),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-        }
-        hipLaunchKernelGGL(pergpu_value_kernel<false>, grid, dim3(kValueBlock), lds, s, p, o, f, flow_value);
-    }
+    if (p.n_cls > 0)
+        hipLaunchKernelGGL(link_table_kernel<true>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin);
+    else
+        hipLaunchKernelGGL(link_table_kernel<false>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin);
     prof_mark(kKKv, true, s);
+    prof_mark(kKNodes, false, s);
+    if (mask_words(p.G) == 1)
+        hipLaunchKernelGGL((nodes_gpu_kernel<1, true>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
+                           o, f, tab, rmin, flow_value);
+    else
+        hipLaunchKernelGGL((nodes_gpu_kernel<2, true>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
+                           o, f, tab, rmin, flow_value);
+    prof_mark(kKNodes, true, s);
     return hipGetLastError();
 }
 

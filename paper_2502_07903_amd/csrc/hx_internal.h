@@ -102,13 +102,15 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           unsigned long long* stats, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
-// hx_score_batch: per-GPU networks of up to 128 GPUs are settled from a table of link capacities
-// (flownet_values_direct): node rows written, flow_value the closed form where every KV edge is
-// dominant, else -1 with the KV rows written; launch_maxflow_unsettled then solves the -1
-// networks (workgroup plans only: maxflow_workgroup_plan).
+// hx_score_batch: per-GPU networks of up to 128 GPUs and 128 slots are settled from a table of
+// link capacities (flownet_values_direct): node rows written, flow_value the closed form where
+// every KV edge is dominant, else -1 with the KV rows written; launch_maxflow_unsettled then
+// solves the -1 networks (workgroup plans only: maxflow_workgroup_plan).
 bool flownet_values_direct(const Problem& p);
+// Bytes of the link table (int32 [G][G] capacities, then [G] row minima) it needs.
+size_t link_table_bytes(int32_t n_gpus);
 hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
-                                 hipStream_t s);
+                                 void* table, hipStream_t s);
 bool maxflow_workgroup_plan(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow_unsettled(const FlowNet& f, int32_t* flow_value, int32_t round_budget, hipStream_t s);
 

@@ -93,7 +93,7 @@ class hx_flownet(C.Structure):
 
 
 EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_eval_static", "hx_static_scratch_bytes", "hx_cost_workspace_bytes", "hx_member_words", "hx_build_flownet",
-           "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_score_batch", "hx_edge_classes", "hx_guided_moves",
+           "hx_maxflow_batch", "hx_maxflow_stats", "hx_best_candidate", "hx_score_batch", "hx_score_workspace_bytes", "hx_edge_classes", "hx_guided_moves",
            "hx_gather_candidates",
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
            "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error",
@@ -127,6 +127,8 @@ def lib() -> C.CDLL:
         L.hx_maxflow_batch.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_maxflow_stats.argtypes = [P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.hx_best_candidate.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+        L.hx_score_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32]
+        L.hx_score_workspace_bytes.restype = C.c_size_t
         L.hx_score_batch.argtypes = [P(hx_cluster), hx_model, hx_workload, hx_space, P(hx_candidates),
                                      P(hx_cost_out), P(hx_flownet), C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                                      C.c_void_p]
@@ -267,14 +269,14 @@ class CostBuffers:
     cap: object
     lat: object
     members: object     # int64 [Kmax * W, N]: the group member bitmasks (uint64 bit patterns)
-    workspace: object   # uint8 scratch of hx_cost_workspace_bytes
+    workspace: object   # uint8 scratch of hx_score_workspace_bytes (>= hx_cost_workspace_bytes)
 
     @classmethod
     def empty(cls, max_groups: int, n_cand: int, n_gpus: int, device: str = "cuda") -> "CostBuffers":
         torch = _torch()
         z = lambda dt: torch.empty((max_groups, n_cand), dtype=dt, device=device)
         words = lib().hx_member_words(n_gpus)
-        wsb = int(lib().hx_cost_workspace_bytes(n_gpus, max_groups, n_cand))
+        wsb = int(lib().hx_score_workspace_bytes(n_gpus, max_groups, n_cand))
         if words <= 0 or wsb <= 0:
             raise ValueError("invalid sizes for the cost-model buffers")
         return cls(z(torch.uint8), z(torch.uint8), z(torch.int32), z(torch.int32), z(torch.float64),
