@@ -392,7 +392,7 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
 size_t hx_score_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t c = hx_cost_workspace_bytes(n_gpus, max_groups, n_cand);
     if (c == 0) return 0;
-    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus) + 255) & ~(size_t)255);
+    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus, n_cand) + 255) & ~(size_t)255);
 }
 
 int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
@@ -415,7 +415,8 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
                                ~(size_t)255;
             void* table = static_cast<unsigned char*>(workspace) + off;
             e = hx::launch_flownet_values(p, make_cost(cost), f, flow_value, table, stream);
-            if (e == hipSuccess) e = hx::launch_maxflow_unsettled(f, flow_value, round_budget(), stream);
+            int32_t* count = hx::flownet_values_list_count(table, cluster->n_gpus);
+            if (e == hipSuccess) e = hx::launch_maxflow_listed(f, flow_value, round_budget(), count + 16, count, stream);
         } else {
             e = hx::launch_flownet(p, make_cost(cost), f, stream);
             if (e == hipSuccess) e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream);

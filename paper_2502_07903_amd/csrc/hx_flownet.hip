@@ -126,11 +126,13 @@ __host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax 
 // dominant-KV closed form, and the KV rows are never needed.  rmin[g], the smallest capacity of
 // GPU g's links, decides most networks on the fly: an edge out of prefill node i can be thin
 // only if rmin[g_i] < min(a_i, b_max).  The others are checked edge by edge; a network with a
-// thin edge gets its KV rows and flow_value -1, for the max-flow kernel.  Edges with an end of
+// thin edge gets its KV rows and flow_value -1, and its candidate goes to the list the max-flow
+// kernel works through (list_count, cleared by link_table_kernel).  Edges with an end of
 // capacity 0 never bind (min(a_i, b_j) = 0); an infeasible replica's GPUs carry 0.
 template <int W, bool kValue>
 __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, FlowNet f, const int32_t* tab,
-                                                       const int32_t* rmin, int32_t* flow_value) {
+                                                       const int32_t* rmin, int32_t* flow_value, int32_t* list,
+                                                       int32_t* list_count) {
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int lane = threadIdx.x;
     const int Kmax = p.Kmax;
@@ -249,6 +251,7 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
         }
     }
     flow_value[n] = -1;
+    list[atomicAdd(list_count, 1)] = (int32_t)n;
 }
 
 
@@ -258,7 +261,7 @@ template <int W>
 void launch_nodes(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s) {
     if (p.granularity == 1 && p.Kmax <= kNodesGpuMaxK)
         hipLaunchKernelGGL((nodes_gpu_kernel<W, false>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
-                           o, f, nullptr, nullptr, nullptr);
+                           o, f, nullptr, nullptr, nullptr, nullptr, nullptr);
     else
         hipLaunchKernelGGL(nodes_kernel<W>, dim3((p.N + kNodeBlock - 1) / kNodeBlock), dim3(kNodeBlock), 0, s, p, o, f);
 }
@@ -881,13 +884,16 @@ hipError_t launch_kv_gpu(const Problem& p, const FlowNet& f, const CostOut& o, h
 }
 
 // The capacity of every per-GPU KV link (kv_gpu_cap) and each GPU's smallest one, for
-// hx_score_batch: a workgroup per GPU row, its minimum by a workgroup reduction.
+// hx_score_batch: a workgroup per GPU row, its minimum by a workgroup reduction; also clears the
+// count of the candidates left to the max-flow.
 constexpr int kLinkBlock = 256;
 
 template <bool kCls>
-__global__ void __launch_bounds__(kLinkBlock) link_table_kernel(Problem p, int32_t* tab, int32_t* rmin) {
+__global__ void __launch_bounds__(kLinkBlock) link_table_kernel(Problem p, int32_t* tab, int32_t* rmin,
+                                                                int32_t* list_count) {
     __shared__ int32_t red[kLinkBlock / 64];
     const int g = blockIdx.x, G = p.G;
+    if (g == 0 && threadIdx.x == 0) *list_count = 0;
     double vl[HX_MAX_CLASSES];
 #pragma unroll
     for (int k = 0; k < HX_MAX_CLASSES; ++k)
@@ -959,25 +965,38 @@ bool flownet_values_direct(const Problem& p) {
     return p.granularity == 1 && p.G <= kGpuTableMaxG && p.Kmax <= kNodesGpuMaxK;
 }
 
-size_t link_table_bytes(int32_t n_gpus) { return sizeof(int32_t) * ((size_t)n_gpus * n_gpus + n_gpus); }
+// Layout: int32 tab [G][G], rmin [G]; then, 256-byte aligned, the list count and the list [N].
+static size_t list_offset(int32_t n_gpus) {
+    return (sizeof(int32_t) * ((size_t)n_gpus * n_gpus + n_gpus) + 255) & ~(size_t)255;
+}
+
+size_t link_table_bytes(int32_t n_gpus, int32_t n_cand) {
+    return list_offset(n_gpus) + sizeof(int32_t) * (16 + (size_t)n_cand);
+}
+
+int32_t* flownet_values_list_count(void* table, int32_t n_gpus) {
+    return reinterpret_cast<int32_t*>(static_cast<unsigned char*>(table) + list_offset(n_gpus));
+}
 
 hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
                                  void* table, hipStream_t s) {
     int32_t* tab = static_cast<int32_t*>(table);
     int32_t* rmin = tab + (size_t)p.G * p.G;
+    int32_t* list_count = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(table) + list_offset(p.G));
+    int32_t* list = list_count + 16;
     prof_mark(kKKv, false, s);
     if (p.n_cls > 0)
-        hipLaunchKernelGGL(link_table_kernel<true>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin);
+        hipLaunchKernelGGL(link_table_kernel<true>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin, list_count);
     else
-        hipLaunchKernelGGL(link_table_kernel<false>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin);
+        hipLaunchKernelGGL(link_table_kernel<false>, dim3(p.G), dim3(kLinkBlock), 0, s, p, tab, rmin, list_count);
     prof_mark(kKKv, true, s);
     prof_mark(kKNodes, false, s);
     if (mask_words(p.G) == 1)
         hipLaunchKernelGGL((nodes_gpu_kernel<1, true>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
-                           o, f, tab, rmin, flow_value);
+                           o, f, tab, rmin, flow_value, list, list_count);
     else
         hipLaunchKernelGGL((nodes_gpu_kernel<2, true>), dim3((p.N + 63) / 64), dim3(64), nodes_gpu_lds(p.Kmax), s, p,
-                           o, f, tab, rmin, flow_value);
+                           o, f, tab, rmin, flow_value, list, list_count);
     prof_mark(kKNodes, true, s);
     return hipGetLastError();
 }

@@ -104,15 +104,20 @@ hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flo
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
 // hx_score_batch: per-GPU networks of up to 128 GPUs and 128 slots are settled from a table of
 // link capacities (flownet_values_direct): node rows written, flow_value the closed form where
-// every KV edge is dominant, else -1 with the KV rows written; launch_maxflow_unsettled then
-// solves the -1 networks (workgroup plans only: maxflow_workgroup_plan).
+// every KV edge is dominant, else -1 with the KV rows written and the candidate appended to a
+// list; launch_maxflow_listed then solves the listed networks (workgroup plans only:
+// maxflow_workgroup_plan).
 bool flownet_values_direct(const Problem& p);
-// Bytes of the link table (int32 [G][G] capacities, then [G] row minima) it needs.
-size_t link_table_bytes(int32_t n_gpus);
+// Bytes of its scratch: the link table (int32 [G][G] capacities, [G] row minima), then the count
+// and list of the candidates left to the max-flow (int32 [1 + N]).
+size_t link_table_bytes(int32_t n_gpus, int32_t n_cand);
+// The list count inside that scratch (the list follows it at +16 words).
+int32_t* flownet_values_list_count(void* table, int32_t n_gpus);
 hipError_t launch_flownet_values(const Problem& p, const CostOut& o, const FlowNet& f, int32_t* flow_value,
                                  void* table, hipStream_t s);
 bool maxflow_workgroup_plan(int32_t max_p, int32_t max_d, int32_t max_pd);
-hipError_t launch_maxflow_unsettled(const FlowNet& f, int32_t* flow_value, int32_t round_budget, hipStream_t s);
+hipError_t launch_maxflow_listed(const FlowNet& f, int32_t* flow_value, int32_t round_budget, const int32_t* list,
+                                 const int32_t* count, hipStream_t s);
 
 // Refinement (Sec. 3.4): edge classes of networks of at most kClsMaxV vertices, guided moves,
 // and the column gather.

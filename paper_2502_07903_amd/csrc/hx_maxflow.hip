@@ -238,16 +238,15 @@ __global__ void __launch_bounds__(64) dom_kernel(FlowNet f, int32_t* flow_value)
 // kStats: the diagnostic instantiation behind hx_maxflow_stats, which also counts into stats
 // (HX_MF_STATS words, see hx.h) which path each candidate took and the push-relabel work; the
 // production instantiation compiles none of it.
+// The work of one tile (64/SEG candidates of a packed plan, or one candidate of a workgroup
+// plan); every lane of the workgroup calls it with the same tile.
 template <int SEG, bool kStats>
-__global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 : 1)
-    maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
-                   unsigned long long* stats) {
+__device__ __forceinline__ void maxflow_tile(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
+                                             int32_t round_budget, unsigned long long* stats, int tile) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const int N = f.N;
     const int tiles = (N + kPer - 1) / kPer;
-    const int chunk = (tiles + 7) / 8;
-    const int tile = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
     const int seg = threadIdx.x / SEG, l = threadIdx.x % SEG;
     const int n = tile * kPer + seg;
 
@@ -727,6 +726,29 @@ __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 :
     for (int j = l; j < D; j += SEG) cut[(int64_t)(f.max_p + j) * N + n] = (uint8_t)(din[j] | (dout[j] << 1));
 }
 
+template <int SEG, bool kStats>
+__global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 : 1)
+    maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
+                   unsigned long long* stats) {
+    constexpr int kPer = (SEG < 64 ? kPackedLanes : SEG) / SEG;
+    const int tiles = (f.N + kPer - 1) / kPer;
+    const int chunk = (tiles + 7) / 8;
+    maxflow_tile<SEG, kStats>(f, flow_value, kv_flow, cut, round_budget, stats,
+                              (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3));
+}
+
+// Value only, workgroup plans: the candidates listed (list[0 .. *count), written by the kernel that
+// settled the others), a workgroup taking every gridDim.x-th entry.
+template <int SEG>
+__global__ void __launch_bounds__(SEG) maxflow_list_kernel(FlowNet f, int32_t* flow_value, int32_t round_budget,
+                                                           const int32_t* list, const int32_t* count) {
+    const int c = *count;
+    for (int idx = blockIdx.x; idx < c; idx += gridDim.x) {
+        maxflow_tile<SEG, false>(f, flow_value, nullptr, nullptr, round_budget, nullptr, list[idx]);
+        __syncthreads();  // the next candidate reuses the LDS
+    }
+}
+
 constexpr size_t kMaxLds = 64 * 1024;
 
 // Lanes per candidate: the smallest power of two (at least 8) with one lane per node of the
@@ -782,17 +804,18 @@ bool maxflow_workgroup_plan(int32_t max_p, int32_t max_d, int32_t max_pd) {
     return segment_lanes(max_p, max_d, max_pd) > 64;
 }
 
-hipError_t launch_maxflow_unsettled(const FlowNet& f, int32_t* flow_value, int32_t round_budget, hipStream_t s) {
+hipError_t launch_maxflow_listed(const FlowNet& f, int32_t* flow_value, int32_t round_budget, const int32_t* list,
+                                 const int32_t* count, hipStream_t s) {
     const int seg = segment_lanes(f.max_p, f.max_d, f.max_pd);
     const size_t lds = mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
-    const int blocks = 8 * ((f.N + 7) / 8);
+    const int blocks = f.N < 2048 ? f.N : 2048;  // eight workgroups per CU at most
     prof_mark(kKMaxflow, false, s);
     if (seg == 128)
-        hipLaunchKernelGGL((maxflow_kernel<128, false>), dim3(blocks), dim3(128), lds, s, f, flow_value, nullptr,
-                           nullptr, round_budget, nullptr);
+        hipLaunchKernelGGL(maxflow_list_kernel<128>, dim3(blocks), dim3(128), lds, s, f, flow_value, round_budget, list,
+                           count);
     else
-        hipLaunchKernelGGL((maxflow_kernel<256, false>), dim3(blocks), dim3(256), lds, s, f, flow_value, nullptr,
-                           nullptr, round_budget, nullptr);
+        hipLaunchKernelGGL(maxflow_list_kernel<256>, dim3(blocks), dim3(256), lds, s, f, flow_value, round_budget, list,
+                           count);
     prof_mark(kKMaxflow, true, s);
     return hipGetLastError();
 }
