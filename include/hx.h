@@ -300,16 +300,16 @@ int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, 
  * candidate but not a flow assignment (Sec. 3.1 objective, Sec. 3.3 network, Appendix A
  * capacities): hx_cost_eval, hx_build_flownet, hx_maxflow_batch with kv_flow and cut null, and
  * hx_best_candidate, enqueued by one call with the same arguments and errors, a workspace of
- * hx_score_workspace_bytes (the cost model's scratch and a table of link capacities, 256-byte
- * aligned, contents ignored on entry), and the same results: every cost output, the network's
- * node rows (n_p, n_d, slots, source, node and sink capacities), flow_value and best, bit for
- * bit.  At granularity 1 on clusters of up to 128 GPUs a KV edge's capacity depends only on its
- * link, so a network whose every KV edge can carry min(a_i, b_j) (the dominant-KV closed form:
- * maximum flow min(sum a, sum b)) is settled from a table of link capacities while its node
- * rows are built, and only the other networks get their KV rows written and solved by
- * push-relabel; the kv_cap rows of the settled networks are then left as they were.  At
- * granularity 0, and beyond 128 GPUs or 128 group slots, every row is written as by
- * hx_build_flownet. */
+ * hx_score_workspace_bytes (the cost model's scratch, then a table of link capacities and a list
+ * of candidates, 256-byte aligned, contents ignored on entry), and the same results: every cost
+ * output, the network's node counts (n_p, n_d), flow_value and best, bit for bit.  At
+ * granularity 0, and beyond 128 GPUs or 128 group slots, every row of the network is written as
+ * by hx_build_flownet.  At granularity 1 on clusters of up to 128 GPUs a KV edge's capacity
+ * depends only on its link, so a network whose every KV edge can carry min(a_i, b_j) (the
+ * dominant-KV closed form: maximum flow min(sum a, sum b)) is settled from a table of link
+ * capacities while its nodes are counted, and only the other networks get their node and KV rows
+ * written and are solved by push-relabel; the rows of the settled networks are left as they
+ * were. */
 size_t hx_score_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
 int hx_score_batch(const hx_cluster *cluster, hx_model model, hx_workload wl, hx_space space,
                    const hx_candidates *cand, const hx_cost_out *cost, const hx_flownet *net, int32_t *flow_value,

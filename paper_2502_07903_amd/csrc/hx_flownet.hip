@@ -119,7 +119,8 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
 constexpr int kNodesGpuMaxK = 128;
 __host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax * 64 * 7; }
 
-// kValue (hx_score_batch): the kernel also settles the network's value.  Every KV edge of a per-GPU
+// kValue (hx_score_batch): the kernel also settles the network's value, and writes the node rows
+// only of the networks it does not settle (the counts always).  Every KV edge of a per-GPU
 // network has its link's capacity (tab: [G][G], computed once per call), so when every edge can
 // carry min(a_i, b_j) (a_i the prefill node's source-or-node capacity, b_j the decode node's
 // node-or-sink capacity) the maximum flow is min(sum a, sum b), the max-flow kernel's
@@ -169,56 +170,78 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
     long long sa = 0, sb = 0;  // kValue
     int32_t bmax = 0, t1 = 0x7fffffff;
     bool any_a = false;
-    for (int g0 = 0; g0 < p.G; g0 += kC) {
-        int kk[kC];
+    // One pass over the GPUs in ascending id: node counts, sums for kValue, and the node rows
+    // when `rows` (a replayed pass starts from zeroed member counts).
+    auto pass = [&](bool rows, bool replay) {
+        np = nd = 0;
+        sa = sb = 0;
+        bmax = 0;
+        t1 = 0x7fffffff;
+        any_a = false;
+        if (replay)
+            for (int k = 0; k < Kmax; ++k) gseen[k * 64 + lane] = 0;
+        for (int g0 = 0; g0 < p.G; g0 += kC) {
+            int kk[kC];
 #pragma unroll
-        for (int x = 0; x < kC; ++x) kk[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
+            for (int x = 0; x < kC; ++x) kk[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
 #pragma unroll
-        for (int x = 0; x < kC; ++x) {
-            const int g = g0 + x, k = kk[x];
-            if (g >= p.G || k >= Kmax) continue;
-            const int r = grole[k * 64 + lane];
-            if (r != HX_PREFILL && r != HX_DECODE) continue;
-            const int rk = gseen[k * 64 + lane];
-            gseen[k * 64 + lane] = (uint8_t)(rk + 1);
-            const int sz = gsize[k * 64 + lane];
-            const int32_t C = gcap[k * 64 + lane];
-            const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
-            if (r == HX_PREFILL) {
-                const int64_t e = (int64_t)np * N + n;
-                f.p_slot[e] = g;
-                f.src_cap[e] = p.coord_cap;
-                f.p_cap[e] = share;
-                ++np;
-                if (kValue) {
-                    const int32_t a = p.coord_cap < share ? p.coord_cap : share;
-                    sa += a;
-                    if (a > 0) {
-                        any_a = true;
-                        const int32_t m = rmin[g];
-                        if (m < a && m < t1) t1 = m;
+            for (int x = 0; x < kC; ++x) {
+                const int g = g0 + x, k = kk[x];
+                if (g >= p.G || k >= Kmax) continue;
+                const int r = grole[k * 64 + lane];
+                if (r != HX_PREFILL && r != HX_DECODE) continue;
+                const int rk = gseen[k * 64 + lane];
+                gseen[k * 64 + lane] = (uint8_t)(rk + 1);
+                const int sz = gsize[k * 64 + lane];
+                const int32_t C = gcap[k * 64 + lane];
+                const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
+                if (r == HX_PREFILL) {
+                    if (rows) {
+                        const int64_t e = (int64_t)np * N + n;
+                        f.p_slot[e] = g;
+                        f.src_cap[e] = p.coord_cap;
+                        f.p_cap[e] = share;
                     }
-                }
-            } else {
-                const int64_t e = (int64_t)nd * N + n;
-                f.d_slot[e] = g;
-                f.d_cap[e] = share;
-                f.sink_cap[e] = p.coord_cap;
-                ++nd;
-                if (kValue) {
-                    const int32_t b = share < p.coord_cap ? share : p.coord_cap;
-                    sb += b;
-                    bmax = b > bmax ? b : bmax;
+                    ++np;
+                    if (kValue) {
+                        const int32_t a = p.coord_cap < share ? p.coord_cap : share;
+                        sa += a;
+                        if (a > 0) {
+                            any_a = true;
+                            const int32_t m = rmin[g];
+                            if (m < a && m < t1) t1 = m;
+                        }
+                    }
+                } else {
+                    if (rows) {
+                        const int64_t e = (int64_t)nd * N + n;
+                        f.d_slot[e] = g;
+                        f.d_cap[e] = share;
+                        f.sink_cap[e] = p.coord_cap;
+                    }
+                    ++nd;
+                    if (kValue) {
+                        const int32_t b = share < p.coord_cap ? share : p.coord_cap;
+                        sb += b;
+                        bmax = b > bmax ? b : bmax;
+                    }
                 }
             }
         }
-    }
+    };
+    pass(!kValue, false);
     f.n_p[n] = np;
     f.n_d[n] = nd;
     if (!kValue) return;
+    if (t1 >= bmax) {  // every KV edge dominant: no row is needed
+        // < 2^31: the smaller side has at most 127 nodes of at most 2^24 - 1
+        flow_value[n] = (!any_a || bmax <= 0) ? 0 : (int32_t)(sa < sb ? sa : sb);
+        return;
+    }
+    pass(true, true);  // the rows, for the edge-by-edge check and the max-flow
     const int G = p.G;
-    bool dominant = t1 >= bmax;
-    if (!dominant) {  // edge by edge (this lane's own rows, just written)
+    bool dominant;
+    {  // edge by edge (this lane's own rows, just written)
         bool thin = false;
         for (int i = 0; i < np && !thin; ++i) {
             const int32_t ps = f.src_cap[(int64_t)i * N + n], pc = f.p_cap[(int64_t)i * N + n];

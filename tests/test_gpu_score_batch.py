@@ -1,8 +1,8 @@
 """hx_score_batch, the whole scoring path in one value-only call, through the C-ABI: on every
-workload its cost outputs, node rows, flow values and best equal the four calls' bit for bit (and
-the KV rows too at replica granularity); on per-GPU networks whose KV edges bind (slow links) the
-networks it hands to push-relabel are solved to the oracle's values; ragged batch sizes and
-request classes."""
+workload its cost outputs, node counts, flow values and best equal the four calls' bit for bit
+(and every node and KV row too at replica granularity); on per-GPU networks whose KV edges bind
+(slow links) the networks it hands to push-relabel are solved to the oracle's values; ragged
+batch sizes and request classes."""
 import dataclasses
 import os
 import sys
@@ -56,12 +56,12 @@ def _same(a, b, granularity):
     for k in a["cost"]:
         assert np.array_equal(a["cost"][k].view(np.uint8), b["cost"][k].view(np.uint8)), f"cost {k} differs"
     assert np.array_equal(a["net"]["n_p"], b["net"]["n_p"]) and np.array_equal(a["net"]["n_d"], b["net"]["n_d"])
-    up, ud, upd = Hh.used_rows(a["net"])
-    for k in ("p_slot", "src_cap", "p_cap"):
-        assert np.array_equal(a["net"][k][up], b["net"][k][up]), k
-    for k in ("d_slot", "d_cap", "sink_cap"):
-        assert np.array_equal(a["net"][k][ud], b["net"][k][ud]), k
-    if granularity == 0:
+    if granularity == 0:  # per-GPU networks settled from the link table keep their rows unwritten
+        up, ud, upd = Hh.used_rows(a["net"])
+        for k in ("p_slot", "src_cap", "p_cap"):
+            assert np.array_equal(a["net"][k][up], b["net"][k][up]), k
+        for k in ("d_slot", "d_cap", "sink_cap"):
+            assert np.array_equal(a["net"][k][ud], b["net"][k][ud]), k
         assert np.array_equal(a["net"]["kv_cap"][upd], b["net"]["kv_cap"][upd])
     bad = np.flatnonzero(a["flow_value"] != b["flow_value"])
     assert bad.size == 0, f"flow values differ at {bad[:8].tolist()}"
