@@ -45,20 +45,35 @@ LDS_PEAK_GBS = 256 * 256 * 2.4
 # 2.4 GHz = 39,322 G op/s (the 78.6 TFLOP/s headline counts an FMA as two).
 FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 
-# HBM bytes per launch at workload 3 from rocprofv3 FETCH_SIZE and WRITE_SIZE passes
-# (profiles/all_kernels_workload3.md), each scaled by what the counter reads for a 256 MiB
+# HBM bytes per launch from rocprofv3 FETCH_SIZE and WRITE_SIZE passes (workload 3:
+# profiles/all_kernels_workload3.md; workload 5: profiles/chain_workload5.md), each scaled by what the counter reads for a 256 MiB
 # device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for the kernel source they were
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
-    "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 67.5, "write_kib": 32.81},
-    "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1668.06, "write_kib": 27815.06},
-    "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 4935.0, "write_kib": 1488.54},
-    "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1145.86, "write_kib": 12118.61},
-    "nodes": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 6698.15, "write_kib": 17042.95},
-    "kv": {"source_sha256_16": "dafb5344b2d4ce0c", "fetch_kib": 5891.39, "write_kib": 13399.09},
-    "maxflow": {"source_sha256_16": "1b140d4d507b5f54", "fetch_kib": 16732.65, "write_kib": 256.0},
-    "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.26, "write_kib": 0.03},
+    # workload 3 (profiles/all_kernels_workload3.md)
+    3: {
+        "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 67.5, "write_kib": 32.81},
+        "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1668.0, "write_kib": 27820.0},
+        "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 4935.0, "write_kib": 1487.0},
+        "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1148.0, "write_kib": 12130.0},
+        "nodes": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 6698.0, "write_kib": 20280.0},
+        "kv": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 5891.0, "write_kib": 13400.0},
+        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 16740.0, "write_kib": 256.0},
+        "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.3, "write_kib": 0.03125},
+    },
+    # workload 5, one chain round through hx_score_batch (profiles/chain_workload5.md): nodes is the
+    # settling nodes kernel, kv the link table, maxflow the list-driven kernel
+    5: {
+        "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 181.9, "write_kib": 516.1},
+        "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 20670.0, "write_kib": 112600.0},
+        "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 53820.0, "write_kib": 61410.0},
+        "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 41590.0, "write_kib": 120200.0},
+        "nodes": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 61550.0, "write_kib": 1536.0},
+        "kv": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 146.2, "write_kib": 68.03},
+        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 13.17, "write_kib": 0.0},
+        "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 262.5, "write_kib": 0.03125},
+    },
 }
 # The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
 # 131,072 children, same scaling.
@@ -66,8 +81,8 @@ MOVES_TRAFFIC = {"source_sha256_16": "2902f3b847ca3ebd", "children": 131072, "fe
                  "write_kib": 20990.0}
 # The partition kernel at workload 3 (profiles/partition_workload3.md), per launch of 16,384
 # candidates, same scaling.
-PARTITION_TRAFFIC = {"source_sha256_16": "4e14e097fd09e714", "candidates": 16384, "fetch_kib": 1180.0,
-                     "write_kib": 6192.0}
+PARTITION_TRAFFIC = {"source_sha256_16": "72b4245b3df4f290", "candidates": 16384, "fetch_kib": 1158.0,
+                     "write_kib": 6144.0}
 KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
                  "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
                  "best": "hx_best.hip"}
@@ -207,10 +222,11 @@ def measured_copy_gbs(torch, mib: int = 1024, reps: int = 10) -> float:
 
 def kernel_traffic(kernel: str, workload: int, prob=None):
     """Counter-measured HBM bytes per launch of a kernel, or None when they do not apply (the
-    counters were taken on workload 3 with the cost model as written)."""
+    counters were taken on workloads 3 and 5 with the cost model as written, on the sources whose
+    hashes they carry)."""
     import hashlib
-    t = KERNEL_TRAFFIC.get(kernel)
-    if t is None or workload != 3:
+    t = KERNEL_TRAFFIC.get(workload, {}).get(kernel)
+    if t is None:
         return None
     if prob is not None and (getattr(prob, "variant", 0) or getattr(prob, "classes", None) is not None):
         return None
