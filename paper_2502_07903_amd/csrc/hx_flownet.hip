@@ -437,41 +437,22 @@ __device__ double kv_time_classes(const Problem& p, const uint8_t* pm, int ptp, 
 // With the order of one side X fixed, each position y of the other side Y contributes
 // C[y][t] = max over the X positions sharing layers with y of the block time when Y's stage t
 // serves y, and the KV time is max_y C[y][ord_Y(y)]; the best Y order is a bottleneck
-// assignment of C.  So the search enumerates the orders of X, the side with fewer stages
-// (prefill on ties; at most 8! = 40,320), and solves one bottleneck assignment per order: the
-// smallest threshold T, among C's entries, under which a perfect matching of positions to
-// stages exists.  Orders are packed 4 bits per pipeline position (position a is served by stage
-// (ord >> 4a) & 15).  Pipelines of up to 8 stages (the PP mask is validated).
+// assignment of C.  So the search runs over the orders of X, the side with fewer stages
+// (prefill on ties; at most 8! = 40,320), cutting those that bounds rule out, and solves one
+// bottleneck assignment per order left: the smallest threshold T, among C's entries, under which
+// a perfect matching of positions to stages exists.  Orders are packed 4 bits per pipeline
+// position (position a is served by stage (ord >> 4a) & 15).  Pipelines of up to 8 stages (the
+// PP mask is validated).
 constexpr int kOrderStages = 8;
 constexpr int kBlockPairs = 2 * kOrderStages - 1;  // position pairs sharing layers, at most
-// LDS of kv_order_kernel before the member lists: the block table [pair][xs][yt] (doubles), then
-// the pairs' X position, Y position and shared layers, and the first pair of each Y position.
-constexpr size_t kOrderLds = sizeof(double) * kBlockPairs * kOrderStages * kOrderStages +
-                             sizeof(int32_t) * (3 * kBlockPairs + kOrderStages + 1);
-
-__device__ __forceinline__ int order_count(int pp) {
-    int f = 1;
-    for (int k = 2; k <= pp; ++k) f *= k;
-    return f;
-}
+// LDS of kv_order_kernel before the member lists: the block table [pair][xs][yt] (doubles), each
+// lane's saved bounds per search depth and the best time, then the pairs' X position, Y position
+// and shared layers, the first pair of each Y position and the rows final at each depth.
+constexpr size_t kOrderLds = sizeof(double) * kBlockPairs * kOrderStages * kOrderStages +  // blk
+                             sizeof(double) * (kOrderStages * 64 + 2) +  // saved bounds per lane, best, bound
+                             sizeof(int32_t) * (3 * kBlockPairs + 3 * kOrderStages + 4);
 
 __device__ __forceinline__ int nib(uint32_t v, int i) { return (int)((v >> (4 * i)) & 15u); }
-
-// The order with index k in [0, n!): the Lehmer-code unranking of k (its lexicographic rank).
-__device__ uint32_t unrank_order(int k, int n) {
-    uint32_t out = 0, used = 0;
-    for (int i = 0; i < n; ++i) {
-        const int f = order_count(n - 1 - i);
-        int idx = k / f;
-        k -= idx * f;
-        int v = 0;
-        for (;; ++v)
-            if (!((used >> v) & 1u) && idx-- == 0) break;
-        used |= 1u << v;
-        out |= (uint32_t)v << (4 * i);
-    }
-    return out;
-}
 
 // First layer of pipeline position a of a pipeline of pp stages (uniform split, remainder to the
 // earlier positions).
@@ -504,9 +485,11 @@ __device__ double kv_block_time(const Problem& p, const uint8_t* pm, int ptp, in
 }
 
 // Whether the bipartite graph with rows 0..n-1 (n <= 8) and row y's columns the bits of byte y
-// of rm has a perfect matching: augmenting paths found by breadth-first search from each row,
-// with the matching and the search's parents packed 4 bits per column / row.
-__device__ bool perfect_matching(uint64_t rm, int n) {
+// of rm has a matching covering at least need rows: augmenting paths found by breadth-first
+// search from each row in turn (a row with none now never gains one later), with the matching
+// and the search's parents packed 4 bits per column / row.
+__device__ bool has_matching(uint64_t rm, int n, int need) {
+    int missed = 0;
     uint32_t row_of_col = 0xFFFFFFFFu, col_of_row = 0xFFFFFFFFu;  // 15: none
     for (int i = 0; i < n; ++i) {
         uint32_t parent = 0, seen = 0, front = 1u << i;
@@ -528,7 +511,10 @@ __device__ bool perfect_matching(uint64_t rm, int n) {
                 front |= 1u << r;
             }
         }
-        if (found < 0) return false;
+        if (found < 0) {
+            if (++missed > n - need) return false;
+            continue;
+        }
         for (int j = found;;) {  // flip the path: each row on it takes the column it reached
             const int u = (int)((parent >> (4 * j)) & 15u);
             const int prev = (int)((col_of_row >> (4 * u)) & 15u);
@@ -552,21 +538,133 @@ __device__ __forceinline__ double order_cell(const double* blk, const int* px, c
     return c;
 }
 
+// The largest, over the rows y in [y0, y1), of row y's smallest entry min_t C[y][t] (C of the X
+// order sig): every Y order takes one entry of each row, so this bounds its KV time from below.
+__device__ __forceinline__ double rows_bound(const double* blk, const int* px, const int* ystart, uint32_t sig, int y0,
+                                             int y1, int ny) {
+    double lb = 0.0;
+    for (int y = y0; y < y1; ++y) {
+        double m = order_cell(blk, px, ystart, sig, y, 0);
+        for (int c = 1; c < ny; ++c) {
+            const double v = order_cell(blk, px, ystart, sig, y, c);
+            m = v < m ? v : m;
+        }
+        lb = m > lb ? m : lb;
+    }
+    return lb;
+}
+
+// A complete X order sig whose row bound lb is below the best: the column bound, a test that a
+// perfect matching below the best exists at all, then the bottleneck assignment from the bound
+// upwards; returns the KV time if below best.
+__device__ double order_leaf(const double* blk, const int* px, const int* ystart, uint32_t sig, int ny, double lb,
+                             double best) {
+    for (int c = 0; c < ny && lb < best; ++c) {
+        double m = order_cell(blk, px, ystart, sig, 0, c);
+        for (int y = 1; y < ny; ++y) {
+            const double v = order_cell(blk, px, ystart, sig, y, c);
+            m = v < m ? v : m;
+        }
+        lb = m > lb ? m : lb;
+    }
+    if (lb >= best) return best;
+    {  // no perfect matching strictly below best: this order cannot improve on it
+        uint64_t rm = 0;
+        for (int y = 0; y < ny; ++y)
+            for (int c = 0; c < ny; ++c)
+                if (order_cell(blk, px, ystart, sig, y, c) < best) rm |= 1ull << (8 * y + c);
+        if (!has_matching(rm, ny, ny)) return best;
+    }
+    double T = lb;
+    while (T < best) {
+        uint64_t rm = 0;
+        double next = best;
+        for (int y = 0; y < ny; ++y)
+            for (int c = 0; c < ny; ++c) {
+                const double v = order_cell(blk, px, ystart, sig, y, c);
+                if (v <= T) rm |= 1ull << (8 * y + c);
+                else if (v < next) next = v;
+            }
+        if (has_matching(rm, ny, ny)) return T;
+        T = next;  // the next entry above T, or best when none is below it
+    }
+    return best;
+}
+
+// A bound below the KV time of every order pair, from the position pairs sharing layers: take
+// pairs with no position in common (S: a greedy matching along the merge walk, here among the
+// pairs sharing at least pn[k0] layers).  Any order pair serves S by |S| distinct X stages and
+// |S| distinct Y stages, and a block time never decreases with the layers shared, so the KV
+// time is at least the smallest threshold under which the block times of S's fewest shared
+// layers admit a matching of |S| X stages to Y stages.  Found by bisection over the entries.
+__device__ double pairs_bound(const double* blk, const int* px, const int* py, const int* pn, int npairs, int k0,
+                              int nx, int ny) {
+    const int q = pn[k0];
+    uint32_t ux = 0, uy = 0;
+    int size = 0, kmin = -1;
+    for (int k = 0; k < npairs; ++k) {
+        if (pn[k] < q || ((ux >> px[k]) & 1u) || ((uy >> py[k]) & 1u)) continue;
+        ux |= 1u << px[k];
+        uy |= 1u << py[k];
+        ++size;
+        if (kmin < 0 || pn[k] < pn[kmin]) kmin = k;
+    }
+    const double* w = blk + kmin * kOrderStages * kOrderStages;  // [xs][yt]
+    double lo = 0.0, hi = 0.0;  // lo: no matching of size entries (times are positive); hi: one
+    for (int xs = 0; xs < nx; ++xs)
+        for (int yt = 0; yt < ny; ++yt) hi = w[xs * kOrderStages + yt] > hi ? w[xs * kOrderStages + yt] : hi;
+    for (;;) {
+        const double mid = 0.5 * (lo + hi);
+        double piv = hi, gap = 0.0;
+        bool any = false;
+        for (int xs = 0; xs < nx; ++xs)
+            for (int yt = 0; yt < ny; ++yt) {
+                const double v = w[xs * kOrderStages + yt];
+                const double g = v > mid ? v - mid : mid - v;
+                if (v > lo && v < hi && (!any || g < gap)) {
+                    piv = v;
+                    gap = g;
+                    any = true;
+                }
+            }
+        if (!any) return hi;
+        uint64_t rm = 0;
+        for (int xs = 0; xs < nx; ++xs)
+            for (int yt = 0; yt < ny; ++yt)
+                if (w[xs * kOrderStages + yt] <= piv) rm |= 1ull << (8 * xs + yt);
+        if (has_matching(rm, nx, size)) hi = piv;
+        else lo = piv;
+    }
+}
+
+__device__ __forceinline__ uint32_t set_nib(uint32_t v, int i, int x) {
+    return (v & ~(15u << (4 * i))) | ((uint32_t)x << (4 * i));
+}
+
 // One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: every lane first
 // takes its ascending-order time; then the wavefront searches the edge of each lane whose
-// replicas are not both single-stage, together: the block table of that edge goes to LDS, lane l
-// takes the X orders l, l + 64, ..., and for each order whose lower bound max_y min_t C[y][t]
-// is below the best time found so far (shared across the wavefront after every 64 orders, and
-// starting from the ascending time), solves the bottleneck assignment from that bound upwards.
-// The minimum is the one the enumeration of every order pair finds.  Per-replica granularity.
+// replicas are not both single-stage, together.  The block table of that edge goes to LDS, and
+// the orders of the side with fewer stages (X) are searched depth first, position by position:
+// row y of C is final once every X position sharing layers with y is assigned, and the largest
+// row minimum so far bounds every completion, so a branch whose bound reaches the best time
+// found (shared in LDS, starting from the ascending time) is cut, and the whole search ends once
+// the best reaches a bound below every order pair (pairs_bound, the largest over the lanes).
+// Lane l takes the orders whose first two positions are its prefix l (at most 8 x 7 = 56); a
+// complete order adds the column bound and solves the bottleneck assignment.  The minimum is the
+// one the enumeration of every order pair finds.  Per-replica granularity.
 template <int W>
 __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     double* blk = reinterpret_cast<double*>(sm);
-    int32_t* px = reinterpret_cast<int32_t*>(blk + kBlockPairs * kOrderStages * kOrderStages);
+    double* lbsave = blk + kBlockPairs * kOrderStages * kOrderStages;  // [kOrderStages][64]
+    double* sbest = lbsave + kOrderStages * 64;
+    double* sglb = sbest + 1;
+    volatile double* vbest = sbest;
+    int32_t* px = reinterpret_cast<int32_t*>(sbest + 2);
     int32_t* py = px + kBlockPairs;
     int32_t* pn = py + kBlockPairs;
-    int32_t* ystart = pn + kBlockPairs;
+    int32_t* ystart = pn + kBlockPairs;     // [kOrderStages + 1]
+    int32_t* yfin = ystart + kOrderStages + 1;  // [kOrderStages + 1]: rows made final by X position d
     uint8_t* mem = sm + kOrderLds;
     const int tid = threadIdx.x;  // kKvBlock = 64: one wavefront per workgroup
     const int stride = kKvBlock;
@@ -600,7 +698,7 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
         todo &= todo - 1;
         const int optp = __shfl(ptp, owner), oppp = __shfl(ppp, owner);
         const int odtp = __shfl(dtp, owner), odpp = __shfl(dpp, owner);
-        double best = __shfl(t, owner);
+        const double t_asc = __shfl(t, owner);
         const bool swap = odpp < oppp;  // X = the side with fewer stages, prefill on ties
         const int nx = swap ? odpp : oppp, ny = swap ? oppp : odpp;
         const uint8_t* opm = mem + owner;
@@ -608,6 +706,7 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
         if (tid == 0) {  // position pairs sharing layers, a merge walk: Y positions nondecreasing
             int a = 0, b = 0, k = 0;
             ystart[0] = 0;
+            for (int d = 0; d <= nx; ++d) yfin[d] = 0;
             while (a < nx && b < ny) {
                 const int xl = pos_first(p.L, nx, a), xh = pos_first(p.L, nx, a + 1);
                 const int yl = pos_first(p.L, ny, b), yh = pos_first(p.L, ny, b + 1);
@@ -616,8 +715,17 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
                 pn[k] = (xh < yh ? xh : yh) - (xl > yl ? xl : yl);
                 ++k;
                 if (xh <= yh) ++a;
-                if (yh <= xh) ystart[++b] = k;
+                if (yh <= xh) {
+                    // Y position b's last overlapping X position is px[k - 1]: its row is final
+                    // once that X position is assigned
+                    yfin[px[k - 1] + 1] = b + 1;
+                    ystart[++b] = k;
+                }
             }
+            // yfin[d + 1]: rows below it are final after X positions 0..d (nondecreasing)
+            for (int d = 1; d <= nx; ++d) yfin[d] = yfin[d] > yfin[d - 1] ? yfin[d] : yfin[d - 1];
+            *sbest = t_asc;
+            *sglb = 0.0;
         }
         __syncthreads();
         const int npairs = ystart[ny];
@@ -629,43 +737,68 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
                      : kv_block_time(p, opm, optp, xs, odm, odtp, yt, pn[k], stride);
         }
         __syncthreads();
-        const int nfact = order_count(nx);
-        for (int base = 0; base < nfact; base += kKvBlock) {
-            const int k = base + tid;
-            if (k < nfact) {
-                const uint32_t sig = unrank_order(k, nx);
-                double lb = 0.0;
-                for (int y = 0; y < ny; ++y) {
-                    double m = order_cell(blk, px, ystart, sig, y, 0);
-                    for (int c = 1; c < ny; ++c) {
-                        const double v = order_cell(blk, px, ystart, sig, y, c);
-                        m = v < m ? v : m;
-                    }
-                    lb = m > lb ? m : lb;
-                }
-                double T = lb;
-                while (T < best) {
-                    uint64_t rm = 0;
-                    double next = best;
-                    for (int y = 0; y < ny; ++y)
-                        for (int c = 0; c < ny; ++c) {
-                            const double v = order_cell(blk, px, ystart, sig, y, c);
-                            if (v <= T) rm |= 1ull << (8 * y + c);
-                            else if (v < next) next = v;
-                        }
-                    if (perfect_matching(rm, ny)) {
-                        best = T;
-                        break;
-                    }
-                    T = next;  // the next entry above T, or best when none is below it
-                }
+        if (tid < npairs) {
+            const double b = pairs_bound(blk, px, py, pn, npairs, tid, nx, ny);
+            atomicMax(reinterpret_cast<unsigned long long*>(sglb), (unsigned long long)__double_as_longlong(b));
+        }
+        __syncthreads();
+        // the search ends once the best reaches the bound: no order pair is below it
+        const double glb = *sglb;
+        // lane tid: the orders whose first two positions (one if nx == 1) are its prefix
+        const int nprefix = nx == 1 ? 1 : nx * (nx - 1);
+        if (tid < nprefix && *vbest > glb) {
+            uint32_t sig = 0, used = 0;
+            int start;
+            double lb;
+            if (nx == 1) {
+                start = 1;
+                lb = rows_bound(blk, px, ystart, sig, yfin[0], yfin[1], ny);
+            } else {
+                const int s0 = tid / (nx - 1), r1 = tid - s0 * (nx - 1);
+                const int s1 = r1 + (r1 >= s0 ? 1 : 0);
+                sig = (uint32_t)s0 | ((uint32_t)s1 << 4);
+                used = (1u << s0) | (1u << s1);
+                start = 2;
+                lb = rows_bound(blk, px, ystart, sig, yfin[0], yfin[2], ny);
             }
-            for (int off = 32; off > 0; off >>= 1) {
-                const double u = __shfl_xor(best, off);
-                best = u < best ? u : best;
+            uint32_t next = 0;  // nibble d: the next stage to try at position d
+            int d = start;
+            if (lb < *vbest) {
+                for (;;) {
+                    if (*vbest <= glb) break;  // another lane reached the bound
+                    if (d == nx) {  // a complete order
+                        const double v = order_leaf(blk, px, ystart, sig, ny, lb, *vbest);
+                        if (v < *vbest)
+                            atomicMin(reinterpret_cast<unsigned long long*>(sbest),
+                                      (unsigned long long)__double_as_longlong(v));
+                        if (--d < start) break;
+                        used &= ~(1u << nib(sig, d));
+                        lb = lbsave[d * 64 + tid];
+                        continue;
+                    }
+                    int st = nib(next, d);
+                    while (st < nx && ((used >> st) & 1u)) ++st;
+                    if (st >= nx) {  // position d exhausted: back to d - 1
+                        next = set_nib(next, d, 0);
+                        if (--d < start) break;
+                        used &= ~(1u << nib(sig, d));
+                        lb = lbsave[d * 64 + tid];
+                        continue;
+                    }
+                    next = set_nib(next, d, st + 1);
+                    sig = set_nib(sig, d, st);
+                    const double b2 = rows_bound(blk, px, ystart, sig, yfin[d], yfin[d + 1], ny);
+                    const double lb2 = b2 > lb ? b2 : lb;
+                    if (lb2 >= *vbest) continue;  // cut: the next stage at position d
+                    lbsave[d * 64 + tid] = lb;
+                    used |= 1u << st;
+                    lb = lb2;
+                    ++d;
+                }
             }
         }
-        if (tid == owner) t = best;
+        __syncthreads();
+        if (tid == owner) t = *sbest;
         __syncthreads();  // the next edge overwrites the block table
     }
     if (!live) return;
