@@ -445,13 +445,6 @@ __device__ double kv_time_classes(const Problem& p, const uint8_t* pm, int ptp, 
 // PP mask is validated).
 constexpr int kOrderStages = 8;
 constexpr int kBlockPairs = 2 * kOrderStages - 1;  // position pairs sharing layers, at most
-// LDS of kv_order_kernel before the member lists: the block table [pair][xs][yt] (doubles), each
-// lane's saved bounds per search depth and the best time, then the pairs' X position, Y position
-// and shared layers, the first pair of each Y position and the rows final at each depth.
-constexpr size_t kOrderLds = sizeof(double) * kBlockPairs * kOrderStages * kOrderStages +  // blk
-                             sizeof(double) * (kOrderStages * 64 + 2) +  // saved bounds per lane, best, bound
-                             sizeof(int32_t) * (3 * kBlockPairs + 3 * kOrderStages + 4);
-
 __device__ __forceinline__ int nib(uint32_t v, int i) { return (int)((v >> (4 * i)) & 15u); }
 
 // First layer of pipeline position a of a pipeline of pp stages (uniform split, remainder to the
@@ -538,20 +531,22 @@ __device__ __forceinline__ double order_cell(const double* blk, const int* px, c
     return c;
 }
 
-// The largest, over the rows y in [y0, y1), of row y's smallest entry min_t C[y][t] (C of the X
-// order sig): every Y order takes one entry of each row, so this bounds its KV time from below.
-__device__ __forceinline__ double rows_bound(const double* blk, const int* px, const int* ystart, uint32_t sig, int y0,
-                                             int y1, int ny) {
-    double lb = 0.0;
+// Rows y in [y0, y1) of C (X order sig): the largest row minimum min_t C[y][t] (every Y order
+// takes one entry of each row, so this bounds its KV time from below) into lb, and the entries
+// below best into mask bits 8y + t.
+__device__ __forceinline__ void rows_scan(const double* blk, const int* px, const int* ystart, uint32_t sig, int y0,
+                                          int y1, int ny, double best, double& lb, uint64_t& mask) {
+    lb = 0.0;
+    mask = 0;
     for (int y = y0; y < y1; ++y) {
-        double m = order_cell(blk, px, ystart, sig, y, 0);
-        for (int c = 1; c < ny; ++c) {
+        double m = 0.0;
+        for (int c = 0; c < ny; ++c) {
             const double v = order_cell(blk, px, ystart, sig, y, c);
-            m = v < m ? v : m;
+            m = (c == 0 || v < m) ? v : m;
+            if (v < best) mask |= 1ull << (8 * y + c);
         }
         lb = m > lb ? m : lb;
     }
-    return lb;
 }
 
 // A complete X order sig whose row bound lb is below the best: the column bound, a test that a
@@ -641,36 +636,154 @@ __device__ __forceinline__ uint32_t set_nib(uint32_t v, int i, int x) {
     return (v & ~(15u << (4 * i))) | ((uint32_t)x << (4 * i));
 }
 
-// One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: every lane first
-// takes its ascending-order time; then the wavefront searches the edge of each lane whose
-// replicas are not both single-stage, together.  The block table of that edge goes to LDS, and
-// the orders of the side with fewer stages (X) are searched depth first, position by position:
-// row y of C is final once every X position sharing layers with y is assigned, and the largest
-// row minimum so far bounds every completion, so a branch whose bound reaches the best time
-// found (shared in LDS, starting from the ascending time) is cut, and the whole search ends once
-// the best reaches a bound below every order pair (pairs_bound, the largest over the lanes).
-// Lane l takes the orders whose first two positions are its prefix l (at most 8 x 7 = 56); a
-// complete order adds the column bound and solves the bottleneck assignment.  The minimum is the
+constexpr int kOrderThreads = 256;  // kv_order_kernel: wave 0 holds the lanes, all four waves search
+constexpr int kOrderLevels = 4;     // search levels below a queued prefix, at most
+constexpr int kOrderQueue = 2 * kOrderThreads;  // prefixes handed out per edge, at least (when nx allows)
+
+// LDS of kv_order_kernel before the member lists.
+struct OrderShared {
+    double blk[kBlockPairs * kOrderStages * kOrderStages];  // [pair][X stage][Y stage]
+    double lbsave[kOrderLevels * kOrderThreads];             // [level][thread]: row bound before the level
+    uint64_t mksave[kOrderLevels * kOrderThreads];           // [level][thread]: final-row mask before it
+    double t[kKvBlock];                                      // lanes' ascending-order times
+    double best, glb;
+    uint32_t colord[kBlockPairs * kOrderStages];  // [pair][Y stage]: X stages by ascending block time
+    int32_t shape[kKvBlock];                      // lanes' ptp | ppp << 8 | dtp << 16 | dpp << 24
+    int32_t list[kKvBlock];                       // lanes whose edge is searched
+    int32_t px[kBlockPairs], py[kBlockPairs], pn[kBlockPairs];
+    int32_t ystart[kOrderStages + 1];  // first pair of each Y position
+    int32_t yfin[kOrderStages + 1];    // rows below yfin[d] are final once X positions 0..d-1 are assigned
+    int32_t count, queue;
+};
+constexpr size_t kOrderLds = (sizeof(OrderShared) + 15) & ~(size_t)15;
+
+// Whether an order pair below best can still complete the partial X order sig (positions
+// 0..nass-1 assigned, stages used taken): every entry of C is bounded below by taking, at each
+// unassigned position sharing layers with its row, the cheapest block over the stages still
+// unused (colord lists them by block time), and a perfect matching of the rows to the Y stages
+// over entries whose bound is below best must exist.
+__device__ bool order_bound_ok(const OrderShared& S, uint32_t sig, int nass, uint32_t used, int ny, double best) {
+    uint64_t m = 0;
+    for (int y = 0; y < ny; ++y)
+        for (int c = 0; c < ny; ++c) {
+            double v = 0.0;
+            for (int k = S.ystart[y]; k < S.ystart[y + 1]; ++k) {
+                int st;
+                if (S.px[k] < nass) {
+                    st = nib(sig, S.px[k]);
+                } else {  // some stage is unused while a position is unassigned
+                    const uint32_t ord = S.colord[k * kOrderStages + c];
+                    int j = 0;
+                    do st = nib(ord, j++);
+                    while ((used >> st) & 1u);
+                }
+                const double b = S.blk[(k * kOrderStages + st) * kOrderStages + c];
+                v = b > v ? b : v;
+            }
+            if (v < best) m |= 1ull << (8 * y + c);
+        }
+    return has_matching(m, ny, ny);
+}
+
+// One thread's part of an edge's search: prefixes of the X order (the first pd positions) are
+// taken from a queue in LDS, then searched depth first below the prefix.  A branch is cut when
+// the largest final-row minimum reaches the best time found, when the final rows cannot be
+// matched to distinct Y stages by entries below it, or (three or more positions left) when
+// order_bound_ok fails; a complete order solves its bottleneck assignment.  Returns when the
+// queue is empty or the best has reached the edge's global bound.
+__device__ __forceinline__ void order_search(OrderShared& S, int nx, int ny, int tid) {
+    volatile double* vbest = &S.best;
+    const double glb = S.glb;
+    int pd = 0, P = 1;  // prefix depth: at least kOrderQueue prefixes, at most kOrderLevels levels below
+    while (pd < nx && (P < kOrderQueue || nx - pd > kOrderLevels)) P *= nx - pd++;
+    for (;;) {
+        if (*vbest <= glb) return;
+        int r = atomicAdd(&S.queue, 1);
+        if (r >= P) return;
+        uint32_t sig = 0, used = 0;
+        double lb = 0.0;
+        bool cut = false;
+        for (int l = 0, f = P; l < pd && !cut; ++l) {  // prefix r: mixed radix nx, nx - 1, ...
+            f /= nx - l;
+            int k = r / f, st = 0;
+            r -= k * f;
+            for (;; ++st)
+                if (!((used >> st) & 1u) && k-- == 0) break;
+            sig = set_nib(sig, l, st);
+            used |= 1u << st;
+            double b;
+            uint64_t unused_mask;
+            rows_scan(S.blk, S.px, S.ystart, sig, S.yfin[l], S.yfin[l + 1], ny, 0.0, b, unused_mask);
+            lb = b > lb ? b : lb;
+            cut = lb >= *vbest;
+        }
+        if (cut) continue;
+        double best = *vbest, b0;
+        uint64_t mk;
+        rows_scan(S.blk, S.px, S.ystart, sig, 0, S.yfin[pd], ny, best, b0, mk);
+        if (!has_matching(mk, S.yfin[pd], S.yfin[pd])) continue;
+        if (pd <= nx - 3 && !order_bound_ok(S, sig, pd, used, ny, best)) continue;
+        uint32_t next = 0;  // nibble d: the next stage to try at position d
+        int d = pd;
+        for (;;) {
+            best = *vbest;
+            if (best <= glb) return;
+            if (d == nx) {  // a complete order
+                const double v = order_leaf(S.blk, S.px, S.ystart, sig, ny, lb, best);
+                if (v < best)
+                    atomicMin(reinterpret_cast<unsigned long long*>(&S.best),
+                              (unsigned long long)__double_as_longlong(v));
+            } else {
+                int st = nib(next, d);
+                while (st < nx && ((used >> st) & 1u)) ++st;
+                if (st < nx) {
+                    next = set_nib(next, d, st + 1);
+                    sig = set_nib(sig, d, st);
+                    double b;
+                    uint64_t add;
+                    rows_scan(S.blk, S.px, S.ystart, sig, S.yfin[d], S.yfin[d + 1], ny, best, b, add);
+                    const double lb2 = b > lb ? b : lb;
+                    const uint64_t mk2 = mk | add;
+                    if (lb2 >= best) continue;  // cut: the next stage at position d
+                    if (S.yfin[d + 1] > S.yfin[d] && !has_matching(mk2, S.yfin[d + 1], S.yfin[d + 1])) continue;
+                    if (d + 1 <= nx - 3 && !order_bound_ok(S, sig, d + 1, used | (1u << st), ny, best)) continue;
+                    S.lbsave[(d - pd) * kOrderThreads + tid] = lb;
+                    S.mksave[(d - pd) * kOrderThreads + tid] = mk;
+                    used |= 1u << st;
+                    lb = lb2;
+                    mk = mk2;
+                    ++d;
+                    continue;
+                }
+                next = set_nib(next, d, 0);  // position d exhausted
+            }
+            if (--d < pd) break;  // back to position d
+            used &= ~(1u << nib(sig, d));
+            lb = S.lbsave[(d - pd) * kOrderThreads + tid];
+            mk = S.mksave[(d - pd) * kOrderThreads + tid];
+        }
+    }
+}
+
+// One lane per (KV edge, candidate), as kv_kernel, with the stage-order search: the lanes (wave 0
+// of a 256-thread workgroup) first take their ascending-order times; then all four waves search
+// the edge of each lane whose replicas are not both single-stage, one edge at a time.  The block
+// table of that edge goes to LDS, and the orders of the side with fewer stages (X) are searched
+// position by position: row y of C is final once every X position sharing layers with y is
+// assigned, and the bounds of order_search cut branches that cannot beat the best time found
+// (shared in LDS, starting from the ascending time).  The search ends once the best reaches a
+// bound below every order pair (pairs_bound, the largest over the threads).  The minimum is the
 // one the enumeration of every order pair finds.  Per-replica granularity.
 template <int W>
-__global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o, FlowNet f) {
+__global__ void __launch_bounds__(kOrderThreads) kv_order_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
-    double* blk = reinterpret_cast<double*>(sm);
-    double* lbsave = blk + kBlockPairs * kOrderStages * kOrderStages;  // [kOrderStages][64]
-    double* sbest = lbsave + kOrderStages * 64;
-    double* sglb = sbest + 1;
-    volatile double* vbest = sbest;
-    int32_t* px = reinterpret_cast<int32_t*>(sbest + 2);
-    int32_t* py = px + kBlockPairs;
-    int32_t* pn = py + kBlockPairs;
-    int32_t* ystart = pn + kBlockPairs;     // [kOrderStages + 1]
-    int32_t* yfin = ystart + kOrderStages + 1;  // [kOrderStages + 1]: rows made final by X position d
+    OrderShared& S = *reinterpret_cast<OrderShared*>(sm);
     uint8_t* mem = sm + kOrderLds;
-    const int tid = threadIdx.x;  // kKvBlock = 64: one wavefront per workgroup
+    const int tid = threadIdx.x;
     const int stride = kKvBlock;
     const int64_t gid = (int64_t)blockIdx.x * kKvBlock + tid;
     const int64_t N = p.N;
-    bool live = gid < (int64_t)f.max_pd * N;
+    bool live = tid < kKvBlock && gid < (int64_t)f.max_pd * N;
     const int e = live ? (int)(gid / N) : 0;
     const int n = live ? (int)(gid - (int64_t)e * N) : 0;
     const int np = live ? f.n_p[n] : 0, nd = live ? f.n_d[n] : 0;
@@ -678,9 +791,9 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
     int ptp = 0, ppp = 0, dtp = 0, dpp = 0;
     bool feas = false;
     double t = 0.0;
-    uint8_t* pm = mem + tid;
-    uint8_t* dm = mem + p.G * stride + tid;
     if (live) {
+        uint8_t* pm = mem + tid;
+        uint8_t* dm = mem + p.G * stride + tid;
         const int i = e / nd, j = e - i * nd;
         const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
         ptp = o.tp[(int64_t)kp * N + n];
@@ -692,114 +805,79 @@ __global__ void __launch_bounds__(kKvBlock) kv_order_kernel(Problem p, CostOut o
                expand<W>(o.members, kd, N, n, dm, stride) == dtp * dpp;
         if (feas) t = kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride);
     }
-    uint64_t todo = __ballot(feas && (ppp > 1 || dpp > 1));
-    while (todo) {
-        const int owner = __ffsll((unsigned long long)todo) - 1;
-        todo &= todo - 1;
-        const int optp = __shfl(ptp, owner), oppp = __shfl(ppp, owner);
-        const int odtp = __shfl(dtp, owner), odpp = __shfl(dpp, owner);
-        const double t_asc = __shfl(t, owner);
+    if (tid == 0) S.count = 0;
+    __syncthreads();
+    if (tid < kKvBlock) {
+        S.t[tid] = t;
+        S.shape[tid] = ptp | ppp << 8 | dtp << 16 | dpp << 24;
+        if (feas && (ppp > 1 || dpp > 1)) S.list[atomicAdd(&S.count, 1)] = tid;
+    }
+    __syncthreads();
+    const int count = S.count;
+    for (int li = 0; li < count; ++li) {
+        const int owner = S.list[li];
+        const int sh = S.shape[owner];
+        const int optp = sh & 255, oppp = (sh >> 8) & 255, odtp = (sh >> 16) & 255, odpp = (sh >> 24) & 255;
         const bool swap = odpp < oppp;  // X = the side with fewer stages, prefill on ties
         const int nx = swap ? odpp : oppp, ny = swap ? oppp : odpp;
         const uint8_t* opm = mem + owner;
         const uint8_t* odm = mem + p.G * stride + owner;
         if (tid == 0) {  // position pairs sharing layers, a merge walk: Y positions nondecreasing
             int a = 0, b = 0, k = 0;
-            ystart[0] = 0;
-            for (int d = 0; d <= nx; ++d) yfin[d] = 0;
+            S.ystart[0] = 0;
+            for (int d = 0; d <= nx; ++d) S.yfin[d] = 0;
             while (a < nx && b < ny) {
                 const int xl = pos_first(p.L, nx, a), xh = pos_first(p.L, nx, a + 1);
                 const int yl = pos_first(p.L, ny, b), yh = pos_first(p.L, ny, b + 1);
-                px[k] = a;
-                py[k] = b;
-                pn[k] = (xh < yh ? xh : yh) - (xl > yl ? xl : yl);
+                S.px[k] = a;
+                S.py[k] = b;
+                S.pn[k] = (xh < yh ? xh : yh) - (xl > yl ? xl : yl);
                 ++k;
                 if (xh <= yh) ++a;
                 if (yh <= xh) {
                     // Y position b's last overlapping X position is px[k - 1]: its row is final
                     // once that X position is assigned
-                    yfin[px[k - 1] + 1] = b + 1;
-                    ystart[++b] = k;
+                    S.yfin[S.px[k - 1] + 1] = b + 1;
+                    S.ystart[++b] = k;
                 }
             }
-            // yfin[d + 1]: rows below it are final after X positions 0..d (nondecreasing)
-            for (int d = 1; d <= nx; ++d) yfin[d] = yfin[d] > yfin[d - 1] ? yfin[d] : yfin[d - 1];
-            *sbest = t_asc;
-            *sglb = 0.0;
+            for (int d = 1; d <= nx; ++d) S.yfin[d] = S.yfin[d] > S.yfin[d - 1] ? S.yfin[d] : S.yfin[d - 1];
+            S.best = S.t[owner];
+            S.glb = 0.0;
+            S.queue = 0;
         }
         __syncthreads();
-        const int npairs = ystart[ny];
-        for (int it = tid; it < npairs * nx * ny; it += kKvBlock) {
+        const int npairs = S.ystart[ny];
+        for (int it = tid; it < npairs * nx * ny; it += kOrderThreads) {
             const int k = it / (nx * ny), rest = it - k * nx * ny;
             const int xs = rest / ny, yt = rest - xs * ny;
-            blk[(k * kOrderStages + xs) * kOrderStages + yt] =
-                swap ? kv_block_time(p, opm, optp, yt, odm, odtp, xs, pn[k], stride)
-                     : kv_block_time(p, opm, optp, xs, odm, odtp, yt, pn[k], stride);
+            S.blk[(k * kOrderStages + xs) * kOrderStages + yt] =
+                swap ? kv_block_time(p, opm, optp, yt, odm, odtp, xs, S.pn[k], stride)
+                     : kv_block_time(p, opm, optp, xs, odm, odtp, yt, S.pn[k], stride);
         }
         __syncthreads();
+        if (tid < npairs * ny) {  // X stages by ascending block time (ties by index), per pair and Y stage
+            const int k = tid / ny, c = tid - k * ny;
+            const double* col = S.blk + k * kOrderStages * kOrderStages + c;
+            uint32_t ord = 0, taken = 0;
+            for (int r = 0; r < nx; ++r) {
+                int bs = -1;
+                for (int st = 0; st < nx; ++st)
+                    if (!((taken >> st) & 1u) && (bs < 0 || col[st * kOrderStages] < col[bs * kOrderStages])) bs = st;
+                taken |= 1u << bs;
+                ord = set_nib(ord, r, bs);
+            }
+            S.colord[k * kOrderStages + c] = ord;
+        }
         if (tid < npairs) {
-            const double b = pairs_bound(blk, px, py, pn, npairs, tid, nx, ny);
-            atomicMax(reinterpret_cast<unsigned long long*>(sglb), (unsigned long long)__double_as_longlong(b));
+            const double b = pairs_bound(S.blk, S.px, S.py, S.pn, npairs, tid, nx, ny);
+            atomicMax(reinterpret_cast<unsigned long long*>(&S.glb), (unsigned long long)__double_as_longlong(b));
         }
         __syncthreads();
-        // the search ends once the best reaches the bound: no order pair is below it
-        const double glb = *sglb;
-        // lane tid: the orders whose first two positions (one if nx == 1) are its prefix
-        const int nprefix = nx == 1 ? 1 : nx * (nx - 1);
-        if (tid < nprefix && *vbest > glb) {
-            uint32_t sig = 0, used = 0;
-            int start;
-            double lb;
-            if (nx == 1) {
-                start = 1;
-                lb = rows_bound(blk, px, ystart, sig, yfin[0], yfin[1], ny);
-            } else {
-                const int s0 = tid / (nx - 1), r1 = tid - s0 * (nx - 1);
-                const int s1 = r1 + (r1 >= s0 ? 1 : 0);
-                sig = (uint32_t)s0 | ((uint32_t)s1 << 4);
-                used = (1u << s0) | (1u << s1);
-                start = 2;
-                lb = rows_bound(blk, px, ystart, sig, yfin[0], yfin[2], ny);
-            }
-            uint32_t next = 0;  // nibble d: the next stage to try at position d
-            int d = start;
-            if (lb < *vbest) {
-                for (;;) {
-                    if (*vbest <= glb) break;  // another lane reached the bound
-                    if (d == nx) {  // a complete order
-                        const double v = order_leaf(blk, px, ystart, sig, ny, lb, *vbest);
-                        if (v < *vbest)
-                            atomicMin(reinterpret_cast<unsigned long long*>(sbest),
-                                      (unsigned long long)__double_as_longlong(v));
-                        if (--d < start) break;
-                        used &= ~(1u << nib(sig, d));
-                        lb = lbsave[d * 64 + tid];
-                        continue;
-                    }
-                    int st = nib(next, d);
-                    while (st < nx && ((used >> st) & 1u)) ++st;
-                    if (st >= nx) {  // position d exhausted: back to d - 1
-                        next = set_nib(next, d, 0);
-                        if (--d < start) break;
-                        used &= ~(1u << nib(sig, d));
-                        lb = lbsave[d * 64 + tid];
-                        continue;
-                    }
-                    next = set_nib(next, d, st + 1);
-                    sig = set_nib(sig, d, st);
-                    const double b2 = rows_bound(blk, px, ystart, sig, yfin[d], yfin[d + 1], ny);
-                    const double lb2 = b2 > lb ? b2 : lb;
-                    if (lb2 >= *vbest) continue;  // cut: the next stage at position d
-                    lbsave[d * 64 + tid] = lb;
-                    used |= 1u << st;
-                    lb = lb2;
-                    ++d;
-                }
-            }
-        }
+        order_search(S, nx, ny, tid);
         __syncthreads();
-        if (tid == owner) t = *sbest;
-        __syncthreads();  // the next edge overwrites the block table
+        if (tid == owner) t = S.best;
+        __syncthreads();  // the next edge overwrites the shared state
     }
     if (!live) return;
     f.kv_cap[(int64_t)e * N + n] = feas ? quantize(1000.0 / t) : 0;
@@ -1090,7 +1168,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
             e = table ? launch_kv_gpu<W, false, true>(p, f, o, s) : launch_kv_gpu<W, false, false>(p, f, o, s);
         if (e != hipSuccess) return e;
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
-        hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kKvBlock), kOrderLds + lds, s, p, o, f);
+        hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kOrderThreads), kOrderLds + lds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
         hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds + sizeof(double) * p.G, s,
                            p, o, f);
