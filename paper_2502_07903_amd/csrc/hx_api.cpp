@@ -392,7 +392,8 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
 size_t hx_score_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t c = hx_cost_workspace_bytes(n_gpus, max_groups, n_cand);
     if (c == 0) return 0;
-    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus, n_cand) + 255) & ~(size_t)255);
+    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus, n_cand) + 255) & ~(size_t)255) +
+           ((hx::best_parts_bytes() + 255) & ~(size_t)255);
 }
 
 int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
@@ -422,7 +423,16 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
             if (e == hipSuccess) e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream);
         }
     }
-    if (e == hipSuccess) e = hx::launch_best(flow_value, cand->n_cand, best, stream);
+    if (e == hipSuccess) {
+        // the argmax's workgroup winners follow the link table; its counter is the cost
+        // workspace's word that the cost model's first kernel cleared
+        const size_t off = ((hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
+                            ~(size_t)255) +
+                           ((hx::link_table_bytes(cluster->n_gpus, cand->n_cand) + 255) & ~(size_t)255);
+        uint64_t* part = reinterpret_cast<uint64_t*>(static_cast<unsigned char*>(workspace) + off);
+        e = hx::launch_best_parts(flow_value, cand->n_cand, best, hx::cost_workspace_counter(workspace, cluster->n_gpus),
+                                  part, stream);
+    }
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 

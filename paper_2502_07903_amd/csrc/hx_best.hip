@@ -4,6 +4,8 @@
 // One workgroup of 1024 lanes: each lane scans a strided slice with coalesced loads, keeping
 // its first maximum; the wavefront reduces with cross-lane shuffles and the 16 wavefront
 // winners meet in LDS.  Order of comparison makes the result independent of the launch shape.
+// With a scratch area (hx_score_batch), up to 256 workgroups of 256 lanes each take a
+// contiguous slice, and the last workgroup to finish reduces their winners.
 #include <limits.h>
 #include <stdint.h>
 
@@ -75,11 +77,99 @@ __global__ void __launch_bounds__(kBestBlock) best_kernel(const int32_t* __restr
     }
 }
 
+constexpr int kPartBlock = 256;
+constexpr int kPartMax = 256;        // workgroups of best_parts_kernel, at most
+constexpr int kPartPerLane = 4;      // candidates per lane before another workgroup is added
+
+__device__ __forceinline__ void wave_take(int32_t& bv, int32_t& bi) {
+    for (int off = 32; off > 0; off >>= 1) {
+        const int32_t ov = __shfl_down(bv, off, 64);
+        const int32_t oi = __shfl_down(bi, off, 64);
+        take(bv, bi, ov, oi);
+    }
+}
+
+// Workgroup b takes candidates [b chunk, (b + 1) chunk); its winner goes to part[b] as
+// value << 32 | index.  The workgroup whose ticket is the last reads every part (after the
+// others' release fences) and writes best.
+__global__ void __launch_bounds__(kPartBlock) best_parts_kernel(const int32_t* __restrict__ v, int32_t n, int32_t chunk,
+                                                                int32_t* best, int32_t* counter, uint64_t* part) {
+    __shared__ int32_t wv[kPartBlock / 64], wi[kPartBlock / 64];
+    __shared__ int32_t last;
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    const int64_t lo = (int64_t)blockIdx.x * chunk;
+    const int64_t hi = lo + chunk < n ? lo + chunk : n;
+    int32_t bv = INT_MIN, bi = INT_MAX;
+    // eight loads in flight per lane, the ones past the slice predicated off
+    constexpr int kUnroll = 8;
+    for (int64_t i = lo + tid; i < hi; i += kUnroll * kPartBlock) {
+        int32_t x[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) x[k] = i + k * kPartBlock < hi ? v[i + k * kPartBlock] : INT_MIN;
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k)
+            if (i + k * kPartBlock < hi) take(bv, bi, x[k], (int32_t)(i + k * kPartBlock));
+    }
+    wave_take(bv, bi);
+    if (lane == 0) {
+        wv[w] = bv;
+        wi[w] = bi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t gv = wv[0], gi = wi[0];
+        for (int k = 1; k < kPartBlock / 64; ++k) take(gv, gi, wv[k], wi[k]);
+        __hip_atomic_store(&part[blockIdx.x], ((uint64_t)(uint32_t)gv << 32) | (uint32_t)gi, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __threadfence();
+        last = atomicAdd(counter, 1) == (int32_t)gridDim.x - 1;
+        __threadfence();
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    bv = INT_MIN;
+    bi = INT_MAX;
+    for (int b = tid; b < (int)gridDim.x; b += kPartBlock) {
+        const uint64_t k = __hip_atomic_load(&part[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        take(bv, bi, (int32_t)(uint32_t)(k >> 32), (int32_t)(uint32_t)k);
+    }
+    wave_take(bv, bi);
+    if (lane == 0) {
+        wv[w] = bv;
+        wi[w] = bi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t gv = wv[0], gi = wi[0];
+        for (int k = 1; k < kPartBlock / 64; ++k) take(gv, gi, wv[k], wi[k]);
+        best[0] = gi;
+        best[1] = gv;
+        *counter = 0;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s) {
     prof_mark(kKBest, false, s);
     hipLaunchKernelGGL(best_kernel, dim3(1), dim3(kBestBlock), 0, s, flow_value, n, best);
+    prof_mark(kKBest, true, s);
+    return hipGetLastError();
+}
+
+size_t best_parts_bytes() { return sizeof(uint64_t) * kPartMax; }
+
+hipError_t launch_best_parts(const int32_t* flow_value, int32_t n, int32_t* best, int32_t* counter, uint64_t* part,
+                             hipStream_t s) {
+    const int64_t per = (int64_t)kPartBlock * kPartPerLane;
+    int64_t blocks = (n + per - 1) / per;
+    blocks = blocks < 1 ? 1 : blocks > kPartMax ? kPartMax : blocks;
+    const int32_t chunk = (int32_t)((n + blocks - 1) / blocks);
+    blocks = (n + chunk - 1) / chunk;  // every workgroup has a candidate
+    prof_mark(kKBest, false, s);
+    hipLaunchKernelGGL(best_parts_kernel, dim3((unsigned)blocks), dim3(kPartBlock), 0, s, flow_value, n, chunk, best,
+                       counter, part);
     prof_mark(kKBest, true, s);
     return hipGetLastError();
 }

@@ -352,7 +352,7 @@ __device__ __forceinline__ bool screened_out(const uint64_t* unfit, int G, const
     return hit != 0 && wild == 0;
 }
 
-// First kernel of a call: clears the histogram and cursors (n_clear words), tabulates the
+// First kernel of a call: clears the histogram, cursors and argmax counter (n_clear words), tabulates the
 // memory-row screen and the prefill link terms.  Prefill runs at batch 1, so its per-link TP and PP terms depend only on
 // the cluster and the task: alpha + X/(tp beta) for every TP degree of the mask and
 // alpha + X/beta, X = 1*s_in*H*B, evaluated exactly as the costing expressions do (the same
@@ -941,14 +941,14 @@ template <int W>
 hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipStream_t s) {
     const int nb = 2 * (p.G + 1);
     {
-        // hist and cursor are contiguous: 2 nb + 1 words to clear
+        // hist, cursor and the argmax counter are contiguous: 2 nb + 2 words to clear
         const int64_t cells = (int64_t)(HX_MAX_TP + 1) * p.G * p.G;
         const int64_t screen = (int64_t)(p.G + 2) * W * 64;  // a wavefront per screen word
         const int64_t most = cells > screen ? cells : screen;
-        const int64_t want = (most > 2 * nb + 1 ? most : 2 * nb + 1) + 255;
+        const int64_t want = (most > 2 * nb + 2 ? most : 2 * nb + 2) + 255;
         const int blocks = (int)(want / 256 < 1024 ? want / 256 : 1024);
         prof_mark(kKSetup, false, s);
-        hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 1, W);
+        hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 2, W);
         prof_mark(kKSetup, true, s);
     }
     // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS; beyond 64 lanes,
@@ -1032,18 +1032,23 @@ static size_t unfit_bytes(int32_t n_gpus) {
     return sizeof(uint64_t) * ((size_t)n_gpus + 2) * mask_words(n_gpus);
 }
 
-// Layout: histogram and cursors, unit records, prefill link tables, the memory-row screen, and a
-// key byte per group slot.
+// Layout: histogram and cursors, one more word (cleared with them; hx_score_batch's argmax
+// counts its finished workgroups there), unit records, prefill link tables, the memory-row
+// screen, and a key byte per group slot.
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
-    const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
+    const size_t head = ((2 * nb + 2) * sizeof(int32_t) + 255) & ~(size_t)255;
     return head + units_bytes(n_gpus, max_groups, n_cand) + tables_bytes(n_gpus) + unfit_bytes(n_gpus) +
            (size_t)max_groups * n_cand;
 }
 
+int32_t* cost_workspace_counter(void* workspace, int32_t n_gpus) {
+    return reinterpret_cast<int32_t*>(workspace) + 4 * ((size_t)n_gpus + 1) + 1;
+}
+
 hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
     const size_t nb = 2 * ((size_t)p.G + 1);
-    const size_t head = ((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
+    const size_t head = ((2 * nb + 2) * sizeof(int32_t) + 255) & ~(size_t)255;
     CostWork wk;
     wk.hist = reinterpret_cast<int32_t*>(workspace);
     wk.cursor = wk.hist + nb + 1;

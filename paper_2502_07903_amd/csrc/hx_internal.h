@@ -95,6 +95,9 @@ void prof_mark(int k, bool end, hipStream_t s);
 // 64-bit words of a GPU bitmask: 1 up to 64 GPUs, 2 up to 128, 4 up to 255.
 int mask_words(int32_t n_gpus);
 size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
+// The word after the histogram and cursors of a cost workspace: zero once launch_cost's first
+// kernel has run, untouched by the cost kernels.
+int32_t* cost_workspace_counter(void* workspace, int32_t n_gpus);
 hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s);
 hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s);
 // LDS bytes the max-flow kernel needs for a network plan; 0 if it does not fit.
@@ -102,6 +105,12 @@ size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
                           unsigned long long* stats, hipStream_t s);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
+// The same argmax over several workgroups: each writes its winner to part, and the last to
+// finish (counted in *counter, which must be zero at launch and is zero again after it) reduces
+// them.  part holds best_parts_bytes().
+size_t best_parts_bytes();
+hipError_t launch_best_parts(const int32_t* flow_value, int32_t n, int32_t* best, int32_t* counter, uint64_t* part,
+                             hipStream_t s);
 // hx_score_batch: per-GPU networks of up to 128 GPUs and 128 slots are settled from a table of
 // link capacities (flownet_values_direct): node rows written, flow_value the closed form where
 // every KV edge is dominant, else -1 with the KV rows written and the candidate appended to a

@@ -117,3 +117,31 @@ def _net_of(torch, dp, ws):
     hx.build_flownet(dp, ws.cost, ws.net)
     torch.cuda.synchronize()
     return ws.net
+
+
+@pytest.mark.parametrize("cfg,sizes", [(3, (65536, 1, 1023, 1025, 4097)), (5, (131072, 777))])
+def test_score_batch_argmax_over_workgroups(torch, cfg, sizes):
+    """The value-only call's argmax splits the batch over up to 256 workgroups and lets the last
+    one to finish reduce their winners (its counter lives in the workspace): with the workspace
+    filled with garbage before every call, and batch sizes that give one to 256 workgroups, the
+    best equals the single-workgroup argmax of hx_best_candidate over the same flow values, and
+    the first maximum of the host copy."""
+    full = I.make_problem(cfg)
+    for n in sizes:
+        prob = full if n == full.n_cand else full.subset(np.arange(n))
+        say(f"hx_score_batch argmax: workload {cfg}, N={n}")
+        dp = hx.DeviceProblem.upload(prob)
+        ws = hx.Workspace.for_problem(dp, flows=False)
+        for rep in range(3):
+            ws.cost.workspace.fill_(0xA5 if rep % 2 == 0 else 0xFF)
+            ws.best.fill_(-7)
+            hx.score_batch(dp, ws)
+            torch.cuda.synchronize()
+            fv = ws.flow_value.cpu().numpy()
+            got = tuple(int(x) for x in ws.best.cpu().numpy())
+            first = int(np.flatnonzero(fv == fv.max())[0])
+            assert got == (first, int(fv.max())), (n, rep, got)
+            one = torch.full_like(ws.best, -7)
+            hx.best_candidate(ws.flow_value, one, dp.n_cand)
+            torch.cuda.synchronize()
+            assert tuple(int(x) for x in one.cpu().numpy()) == got
