@@ -500,26 +500,26 @@ def refine_main(args, torch, hx, I):
         from oracle import hxo  # test infrastructure: only this baseline leg uses it
         cores = max(1, min(len(os.sched_getaffinity(0)), 64))
         t = time.perf_counter()
-        r = hxo.score_batch(prob, n_threads=cores)
+        r = hxo.score_batch(cp, n_threads=cores)
         first = time.perf_counter() - t
         reps = max(1, min(50, int(args.cpu_seconds / max(first, 1e-3))))
         times = [first]
         for _ in range(reps - 1):
             t = time.perf_counter()
-            hxo.score_batch(prob, n_threads=cores)
+            hxo.score_batch(cp, n_threads=cores)
             times.append(time.perf_counter() - t)
         med = float(np.median(times))
         # one thread on a bounded sample (about a tenth of the all-core time budget)
-        m1 = int(min(prob.n_cand, max(256, prob.n_cand * (args.cpu_seconds / 10.0) / (med * cores))))
+        m1 = int(min(cp.n_cand, max(256, cp.n_cand * (args.cpu_seconds / 10.0) / (med * cores))))
         t = time.perf_counter()
-        hxo.score_batch(prob.subset(np.arange(m1)), n_threads=1)
+        hxo.score_batch(cp.subset(np.arange(m1)), n_threads=1)
         one = m1 / (time.perf_counter() - t)
-        gpu_fv = ws.flow_value.cpu().numpy()
-        out["cpu_baseline"] = {"value": prob.n_cand / med, "unit": "candidates/s", "cores": cores, "kind": "oracle",
-                               "sample": f"the full {prob.n_cand}-candidate batch, {len(times)} runs, median; "
-                                         f"1 thread: the first {m1} candidates",
-                               "single_thread": {"value": one, "unit": "candidates/s", "cores": 1},
-                               "agrees": bool(np.array_equal(r["flow_value"], gpu_fv)) and list(r["best"]) == best,
+        gpu_fv = ref.child_ws.flow_value.cpu().numpy()
+        out["cpu_baseline"] = {"value": cp.n_cand / med, "unit": "children/s", "cores": cores, "kind": "oracle",
+                               "sample": f"the last round's {cp.n_cand} children scored, {len(times)} runs, median; "
+                                         f"1 thread: the first {m1} children",
+                               "single_thread": {"value": one, "unit": "children/s", "cores": 1},
+                               "agrees": bool(np.array_equal(r["flow_value"], gpu_fv)) and list(r["best"]) == final,
                                "cpu": cpu_model()}
     print(json.dumps(out))
 
@@ -982,9 +982,18 @@ def main():
             hxo.score_batch(prob, n_threads=cores)
             times.append(time.perf_counter() - t)
         med = float(np.median(times))
+        # one thread on a bounded sample (about a tenth of the all-core time budget)
+        m1 = int(min(prob.n_cand, max(256, prob.n_cand * (args.cpu_seconds / 10.0) / (med * cores))))
+        t = time.perf_counter()
+        hxo.score_batch(prob.subset(np.arange(m1)), n_threads=1)
+        one = m1 / (time.perf_counter() - t)
+        gpu_fv = ws.flow_value.cpu().numpy()
         out["cpu_baseline"] = {"value": prob.n_cand / med, "unit": "candidates/s", "cores": cores, "kind": "oracle",
-                               "sample": f"the full {prob.n_cand}-candidate batch, {len(times)} runs, median",
-                               "agrees": list(r["best"]) == best, "cpu": cpu_model()}
+                               "sample": f"the full {prob.n_cand}-candidate batch, {len(times)} runs, median; "
+                                         f"1 thread: the first {m1} candidates",
+                               "single_thread": {"value": one, "unit": "candidates/s", "cores": 1},
+                               "agrees": bool(np.array_equal(r["flow_value"], gpu_fv)) and list(r["best"]) == best,
+                               "cpu": cpu_model()}
     print(json.dumps(out))
 
 
