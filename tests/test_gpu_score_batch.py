@@ -145,3 +145,24 @@ def test_score_batch_argmax_over_workgroups(torch, cfg, sizes):
             hx.best_candidate(ws.flow_value, one, dp.n_cand)
             torch.cuda.synchronize()
             assert tuple(int(x) for x in one.cpu().numpy()) == got
+
+
+@pytest.mark.parametrize("cfg,n,variant,classes", [(3, 4096, 0, 4), (2, None, 4, 0), (3, 8192, 1, 0), (2, 1000, 2, 0),
+                                                   (4, 2048, 5, 0)])
+def test_score_batch_replica_variants(torch, cfg, n, variant, classes):
+    """Replica networks under the cost-model variants (request classes, the asymmetric split,
+    the pipelined capacity, the stage-order search, asymmetric + pipelined): the fused call's
+    outputs equal the four calls', and the oracle's
+    flow values on a sample."""
+    prob = I.make_problem(cfg, n_cand=n)
+    if variant:
+        prob = dataclasses.replace(prob, variant=variant)
+    if classes:
+        prob = dataclasses.replace(prob, classes=I.length_classes(I.WORKLOADS[cfg], classes))
+    say(f"hx_score_batch vs four calls: workload {cfg}, N={prob.n_cand}, variant {variant}, classes {classes}")
+    four, one = _both(torch, prob)
+    _same(four, one, prob.granularity)
+    idx = np.unique(np.concatenate([np.random.default_rng(cfg + variant).choice(prob.n_cand, min(prob.n_cand, 512),
+                                                                              replace=False), [one["best"][0]]]))
+    want = hxo.score_batch(prob.subset(idx), n_threads=N_THREADS)
+    assert np.array_equal(one["flow_value"][idx], want["flow_value"])
