@@ -591,9 +591,12 @@ __device__ double order_leaf(const double* blk, const int* px, const int* ystart
 // pairs sharing at least pn[k0] layers).  Any order pair serves S by |S| distinct X stages and
 // |S| distinct Y stages, and a block time never decreases with the layers shared, so the KV
 // time is at least the smallest threshold under which the block times of S's fewest shared
-// layers admit a matching of |S| X stages to Y stages.  Found by bisection over the entries.
+// layers admit a matching of |S| X stages to Y stages.  One wavefront finds it by bisection over
+// the entries: lane l holds entry (X stage l / 8, Y stage l % 8), a wavefront minimum picks the
+// entry inside (lo, hi) nearest the middle, and the ballot of the entries at most that pivot is
+// the matching's bit mask (byte x, bit y).  Every lane returns the bound.
 __device__ double pairs_bound(const double* blk, const int* px, const int* py, const int* pn, int npairs, int k0,
-                              int nx, int ny) {
+                              int nx, int ny, int lane) {
     const int q = pn[k0];
     uint32_t ux = 0, uy = 0;
     int size = 0, kmin = -1;
@@ -604,29 +607,32 @@ __device__ double pairs_bound(const double* blk, const int* px, const int* py, c
         ++size;
         if (kmin < 0 || pn[k] < pn[kmin]) kmin = k;
     }
-    const double* w = blk + kmin * kOrderStages * kOrderStages;  // [xs][yt]
-    double lo = 0.0, hi = 0.0;  // lo: no matching of size entries (times are positive); hi: one
-    for (int xs = 0; xs < nx; ++xs)
-        for (int yt = 0; yt < ny; ++yt) hi = w[xs * kOrderStages + yt] > hi ? w[xs * kOrderStages + yt] : hi;
+    const int xs = lane >> 3, yt = lane & 7;
+    const bool ok = xs < nx && yt < ny;
+    const double v = ok ? blk[kmin * kOrderStages * kOrderStages + lane] : 0.0;
+    double hi = v;  // the largest entry admits a matching of size |S| (times are positive)
+    for (int off = 32; off > 0; off >>= 1) {
+        const double o = __shfl_xor(hi, off, 64);
+        hi = o > hi ? o : hi;
+    }
+    double lo = 0.0;  // no entry is at most 0: no matching
     for (;;) {
         const double mid = 0.5 * (lo + hi);
-        double piv = hi, gap = 0.0;
-        bool any = false;
-        for (int xs = 0; xs < nx; ++xs)
-            for (int yt = 0; yt < ny; ++yt) {
-                const double v = w[xs * kOrderStages + yt];
-                const double g = v > mid ? v - mid : mid - v;
-                if (v > lo && v < hi && (!any || g < gap)) {
-                    piv = v;
-                    gap = g;
-                    any = true;
-                }
+        const bool inside = ok && v > lo && v < hi;
+        double g = inside ? (v > mid ? v - mid : mid - v) : hi;  // hi - lo bounds every gap inside
+        double piv = inside ? v : hi;
+        bool any = inside;
+        for (int off = 32; off > 0; off >>= 1) {
+            const double og = __shfl_xor(g, off, 64), op = __shfl_xor(piv, off, 64);
+            const bool oa = __shfl_xor((int)any, off, 64) != 0;
+            if (oa && (!any || og < g || (og == g && op < piv))) {
+                g = og;
+                piv = op;
+                any = true;
             }
+        }
         if (!any) return hi;
-        uint64_t rm = 0;
-        for (int xs = 0; xs < nx; ++xs)
-            for (int yt = 0; yt < ny; ++yt)
-                if (w[xs * kOrderStages + yt] <= piv) rm |= 1ull << (8 * xs + yt);
+        const uint64_t rm = __ballot(ok && v <= piv);
         if (has_matching(rm, nx, size)) hi = piv;
         else lo = piv;
     }
@@ -859,19 +865,31 @@ __global__ void __launch_bounds__(kOrderThreads) kv_order_kernel(Problem p, Cost
         if (tid < npairs * ny) {  // X stages by ascending block time (ties by index), per pair and Y stage
             const int k = tid / ny, c = tid - k * ny;
             const double* col = S.blk + k * kOrderStages * kOrderStages + c;
-            uint32_t ord = 0, taken = 0;
-            for (int r = 0; r < nx; ++r) {
-                int bs = -1;
-                for (int st = 0; st < nx; ++st)
-                    if (!((taken >> st) & 1u) && (bs < 0 || col[st * kOrderStages] < col[bs * kOrderStages])) bs = st;
-                taken |= 1u << bs;
-                ord = set_nib(ord, r, bs);
+            double v[kOrderStages];
+#pragma unroll
+            for (int st = 0; st < kOrderStages; ++st) v[st] = st < nx ? col[st * kOrderStages] : 0.0;
+            uint32_t ord = 0;
+#pragma unroll
+            for (int st = 0; st < kOrderStages; ++st) {
+                int r = 0;  // the stage's rank: smaller times first, then smaller index
+#pragma unroll
+                for (int s2 = 0; s2 < kOrderStages; ++s2)
+                    r += (s2 < nx && (v[s2] < v[st] || (v[s2] == v[st] && s2 < st))) ? 1 : 0;
+                if (st < nx) ord |= (uint32_t)st << (4 * r);
             }
             S.colord[k * kOrderStages + c] = ord;
         }
-        if (tid < npairs) {
-            const double b = pairs_bound(S.blk, S.px, S.py, S.pn, npairs, tid, nx, ny);
-            atomicMax(reinterpret_cast<unsigned long long*>(&S.glb), (unsigned long long)__double_as_longlong(b));
+        {  // the global bound: a wavefront per distinct shared-layer count
+            const int w = tid >> 6, lane = tid & 63;
+            for (int k0 = w; k0 < npairs; k0 += kOrderThreads / 64) {
+                bool seen = false;
+                for (int k = 0; k < k0; ++k) seen = seen || S.pn[k] == S.pn[k0];
+                if (seen) continue;
+                const double b = pairs_bound(S.blk, S.px, S.py, S.pn, npairs, k0, nx, ny, lane);
+                if (lane == 0)
+                    atomicMax(reinterpret_cast<unsigned long long*>(&S.glb),
+                              (unsigned long long)__double_as_longlong(b));
+            }
         }
         __syncthreads();
         order_search(S, nx, ny, tid);
