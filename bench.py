@@ -51,28 +51,28 @@ FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
-    # workload 3 (profiles/all_kernels_workload3.md)
+    # workload 3 (profiles/all_kernels_workload3.md); best is hx_score_batch's split argmax
     3: {
-        "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 67.5, "write_kib": 32.81},
-        "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1668.0, "write_kib": 27820.0},
-        "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 4935.0, "write_kib": 1487.0},
-        "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 1148.0, "write_kib": 12130.0},
-        "nodes": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 6698.0, "write_kib": 20280.0},
-        "kv": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 5891.0, "write_kib": 13400.0},
+        "setup": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 67.5, "write_kib": 32.81},
+        "decode": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 1668.0, "write_kib": 27820.0},
+        "scatter": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 4935.0, "write_kib": 1488.0},
+        "eval": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 1147.0, "write_kib": 12140.0},
+        "nodes": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 6698.0, "write_kib": 20400.0},
+        "kv": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 5885.0, "write_kib": 13400.0},
         "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 16740.0, "write_kib": 256.0},
-        "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 134.3, "write_kib": 0.03125},
+        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 165.8, "write_kib": 4.062},
     },
     # workload 5, one chain round through hx_score_batch (profiles/chain_workload5.md): nodes is the
     # settling nodes kernel, kv the link table, maxflow the list-driven kernel
     5: {
-        "setup": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 181.9, "write_kib": 516.1},
-        "decode": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 20670.0, "write_kib": 112600.0},
-        "scatter": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 53820.0, "write_kib": 61410.0},
-        "eval": {"source_sha256_16": "dd5d9a64e5cc7db7", "fetch_kib": 41590.0, "write_kib": 120200.0},
-        "nodes": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 61550.0, "write_kib": 1536.0},
-        "kv": {"source_sha256_16": "93a15688704c79e7", "fetch_kib": 146.2, "write_kib": 68.03},
+        "setup": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 181.9, "write_kib": 516.1},
+        "decode": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 20670.0, "write_kib": 112600.0},
+        "scatter": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 53820.0, "write_kib": 61410.0},
+        "eval": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 41490.0, "write_kib": 120100.0},
+        "nodes": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 61540.0, "write_kib": 1536.0},
+        "kv": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 146.2, "write_kib": 68.03},
         "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 13.17, "write_kib": 0.0},
-        "best": {"source_sha256_16": "c5dd3bcb6e1178fe", "fetch_kib": 262.5, "write_kib": 0.03125},
+        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 294.3, "write_kib": 8.062},
     },
 }
 # The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
