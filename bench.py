@@ -125,6 +125,10 @@ def parse():
     ap.add_argument("--candidates", type=int, default=0,
                     help="score batches of this many candidates of the workload instead of its own count "
                          "(a scaling study; the headline uses the workload's count)")
+    ap.add_argument("--streams", type=int, default=3,
+                    help="independent steps in flight, each on its own HIP stream with its own workspace and "
+                         "outputs (a search loop scoring independently drawn batches); 1 runs the steps one "
+                         "after another")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -859,21 +863,37 @@ def main():
     dp = hx.DeviceProblem.upload(prob)
     ws = hx.Workspace.for_problem(dp, flows=False)
     stream = torch.cuda.current_stream()
+    # Independent steps in flight: step s runs on stream s mod S with workspace s mod S (every
+    # kernel of a step is bound by the latency of its longest chains, so steps on other streams
+    # fill the chip meanwhile).  Inputs are shared and only read; all streams at default priority.
+    n_str = max(1, args.streams)
+    streams = [stream] + [torch.cuda.Stream() for _ in range(n_str - 1)]
+    wss = [ws] + [hx.Workspace.for_problem(dp, flows=False) for _ in range(n_str - 1)]
 
     for _ in range(args.warmup):
-        hx.score_batch(dp, ws)
+        for i in range(n_str):
+            hx.score_batch(dp, wss[i], stream=streams[i])
     torch.cuda.synchronize()
 
     # Timed region: K steps and nothing else (event markers between the calls cost the GPU a
     # few microseconds each, so the per-call durations come from a separate pass below).
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        hx.score_batch(dp, ws)
+    for st in range(args.steps):
+        hx.score_batch(dp, wss[st % n_str], stream=streams[st % n_str])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     value = prob.n_cand / (ms_per_step / 1000.0)
+    stream_bests = [[int(x) for x in w.best.cpu().numpy()] for w in wss]
+
+    # The same K steps one after another on one stream: the latency of one step.
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        hx.score_batch(dp, ws)
+    torch.cuda.synchronize()
+    ms_single = (time.perf_counter() - t0) * 1000.0 / args.steps
 
     # The same steps with the host-to-device copy of the candidate arrays (assign, role) from
     # pinned host memory in each step: the rate a caller holding its candidates on the host sees.
@@ -952,7 +972,11 @@ def main():
                                (f", scored in batches of {prob.n_cand:,}" if args.candidates else ""),
                    "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
-                   "cost_model": args.variant, "request_classes": args.classes},
+                   "cost_model": args.variant, "request_classes": args.classes, "streams": n_str},
+        "single_stream": {"value": prob.n_cand / (ms_single / 1000.0), "unit": "candidates/s",
+                          "ms_per_step": ms_single,
+                          "note": "the same steps one after another on one stream (one step's latency)"},
+        "streams_agree": all(b == stream_bests[0] for b in stream_bests),
         "with_h2d_copy": {"value": prob.n_cand / (ms_h2d / 1000.0), "unit": "candidates/s",
                           "ms_per_step": ms_h2d,
                           "note": "assign and role copied from pinned host memory in every step"},

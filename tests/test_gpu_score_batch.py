@@ -166,3 +166,24 @@ def test_score_batch_replica_variants(torch, cfg, n, variant, classes):
                                                                               replace=False), [one["best"][0]]]))
     want = hxo.score_batch(prob.subset(idx), n_threads=N_THREADS)
     assert np.array_equal(one["flow_value"][idx], want["flow_value"])
+
+
+def test_score_batch_concurrent_streams(torch):
+    """Independent calls in flight on three streams (each with its own workspace and outputs, the
+    inputs shared): every stream's flow values and best equal a single-stream call's, call after
+    call (the library keeps no state between calls)."""
+    prob = I.make_problem(3)
+    dp = hx.DeviceProblem.upload(prob)
+    ref = hx.Workspace.for_problem(dp, flows=False)
+    hx.score_batch(dp, ref)
+    torch.cuda.synchronize()
+    want_fv, want_best = ref.flow_value.cpu().numpy(), tuple(int(x) for x in ref.best.cpu().numpy())
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    wss = [hx.Workspace.for_problem(dp, flows=False) for _ in range(3)]
+    say("hx_score_batch on three streams at once, 12 calls")
+    for s in range(12):
+        hx.score_batch(dp, wss[s % 3], stream=streams[s % 3])
+    torch.cuda.synchronize()
+    for w in wss:
+        assert np.array_equal(w.flow_value.cpu().numpy(), want_fv)
+        assert tuple(int(x) for x in w.best.cpu().numpy()) == want_best
