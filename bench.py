@@ -125,10 +125,13 @@ def parse():
     ap.add_argument("--candidates", type=int, default=0,
                     help="score batches of this many candidates of the workload instead of its own count "
                          "(a scaling study; the headline uses the workload's count)")
-    ap.add_argument("--streams", type=int, default=3,
-                    help="independent steps in flight, each on its own HIP stream with its own workspace and "
-                         "outputs (a search loop scoring independently drawn batches); 1 runs the steps one "
-                         "after another")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="independent steps in flight in the timed region, each on its own HIP stream with its "
+                         "own workspace and outputs (a search loop scoring independently drawn batches); 1 runs "
+                         "the steps one after another")
+    ap.add_argument("--concurrent-streams", type=int, default=3,
+                    help="also report the rate with this many independent steps in flight (a short extra pass; "
+                         "0 or 1: none)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -887,52 +890,84 @@ def main():
     value = prob.n_cand / (ms_per_step / 1000.0)
     stream_bests = [[int(x) for x in w.best.cpu().numpy()] for w in wss]
 
-    # The same K steps one after another on one stream: the latency of one step.
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        hx.score_batch(dp, ws)
-    torch.cuda.synchronize()
-    ms_single = (time.perf_counter() - t0) * 1000.0 / args.steps
+    # With several streams in the timed region: up to 10 steps one after another on one stream,
+    # the latency of one step.  Without: a short pass with --concurrent-streams steps in flight.
+    # (Short, so that a kernel trace of the run averages over dispatches made like the passes
+    # below, which keep the timed region's streams.)
+    extra = None
+    if n_str > 1:
+        k1 = min(args.steps, 10)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(k1):
+            hx.score_batch(dp, ws)
+        torch.cuda.synchronize()
+        ms1 = (time.perf_counter() - t0) * 1000.0 / k1
+        extra = ("single_stream", {"value": prob.n_cand / (ms1 / 1000.0), "unit": "candidates/s", "ms_per_step": ms1,
+                                   "note": "steps one after another on one stream (one step's latency)"})
+    elif args.concurrent_streams > 1:
+        nc = args.concurrent_streams
+        cst = [stream] + [torch.cuda.Stream() for _ in range(nc - 1)]
+        cws = [ws] + [hx.Workspace.for_problem(dp, flows=False) for _ in range(nc - 1)]
+        for i in range(nc):
+            hx.score_batch(dp, cws[i], stream=cst[i])
+        kc = min(args.steps, 20)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for st in range(kc):
+            hx.score_batch(dp, cws[st % nc], stream=cst[st % nc])
+        torch.cuda.synchronize()
+        msc = (time.perf_counter() - t0) * 1000.0 / kc
+        cb = [[int(x) for x in w.best.cpu().numpy()] for w in cws]
+        extra = ("concurrent_streams", {"streams": nc, "steps": kc, "value": prob.n_cand / (msc / 1000.0),
+                                        "unit": "candidates/s", "ms_per_step": msc,
+                                        "agree": all(b == stream_bests[0] for b in cb),
+                                        "note": "independent steps in flight, each on its own stream with its own "
+                                                "workspace and outputs (inputs shared, read only)"})
 
     # The same steps with the host-to-device copy of the candidate arrays (assign, role) from
     # pinned host memory in each step: the rate a caller holding its candidates on the host sees.
+    # Each stream copies into its own input buffers, then scores them.
     h_assign = torch.from_numpy(prob.assign).pin_memory()
     h_role = torch.from_numpy(prob.role).pin_memory()
-    d_assign, d_role = dp.tensors["assign"], dp.tensors["role"]
+    dps = [dp] + [hx.DeviceProblem.upload(prob) for _ in range(n_str - 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        d_assign.copy_(h_assign, non_blocking=True)
-        d_role.copy_(h_role, non_blocking=True)
-        hx.score_batch(dp, ws)
+    for st in range(args.steps):
+        i = st % n_str
+        with torch.cuda.stream(streams[i]):
+            dps[i].tensors["assign"].copy_(h_assign, non_blocking=True)
+            dps[i].tensors["role"].copy_(h_role, non_blocking=True)
+        hx.score_batch(dps[i], wss[i], stream=streams[i])
     torch.cuda.synchronize()
     ms_h2d = (time.perf_counter() - t0) * 1000.0 / args.steps
 
-    # Per-call durations: the same steps again with HIP events recorded between the calls on
-    # the stream the kernels run on (kept out of the timed region).
+    # Per-call durations: the same steps again through the four calls, HIP events recorded
+    # between the calls on the stream each step runs on (kept out of the timed region).
     names = ("cost", "flownet", "maxflow", "best")
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for s in range(args.steps):
-        e = ev[s]
-        e[0].record(stream)
-        hx.cost_eval(dp, ws.cost)
-        e[1].record(stream)
-        hx.build_flownet(dp, ws.cost, ws.net)
-        e[2].record(stream)
-        hx.maxflow_batch(ws.net, ws.flow_value)
-        e[3].record(stream)
-        hx.best_candidate(ws.flow_value, ws.best, dp.n_cand)
-        e[4].record(stream)
+    for st in range(args.steps):
+        e, i = ev[st], st % n_str
+        sx, w = streams[i], wss[i]
+        e[0].record(sx)
+        hx.cost_eval(dp, w.cost, stream=sx)
+        e[1].record(sx)
+        hx.build_flownet(dp, w.cost, w.net, stream=sx)
+        e[2].record(sx)
+        hx.maxflow_batch(w.net, w.flow_value, stream=sx)
+        e[3].record(sx)
+        hx.best_candidate(w.flow_value, w.best, dp.n_cand, stream=sx)
+        e[4].record(sx)
     torch.cuda.synchronize()
     per_kernel = {k: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)]))
                   for i, k in enumerate(names)}
 
-    # Per-kernel durations: the same steps again with libhx recording HIP events around each of
-    # its kernels on this stream (kept out of the timed region above).
+    # Per-kernel durations: the same steps again, with the timed region's streams in flight, with
+    # libhx recording HIP events around each of its kernels on the stream it runs on (kept out
+    # of the timed region above).
     hx.profile(True)
-    for _ in range(args.steps):
-        hx.score_batch(dp, ws)
+    for st in range(args.steps):
+        hx.score_batch(dp, wss[st % n_str], stream=streams[st % n_str])
     torch.cuda.synchronize()
     prof = hx.profile_read()
     hx.profile(False)
@@ -973,9 +1008,6 @@ def main():
                    "candidates": prob.n_cand,
                    "cluster_gpus": prob.n_gpus, "max_groups": prob.max_groups, "granularity": prob.granularity,
                    "cost_model": args.variant, "request_classes": args.classes, "streams": n_str},
-        "single_stream": {"value": prob.n_cand / (ms_single / 1000.0), "unit": "candidates/s",
-                          "ms_per_step": ms_single,
-                          "note": "the same steps one after another on one stream (one step's latency)"},
         "streams_agree": all(b == stream_bests[0] for b in stream_bests),
         "with_h2d_copy": {"value": prob.n_cand / (ms_h2d / 1000.0), "unit": "candidates/s",
                           "ms_per_step": ms_h2d,
@@ -987,6 +1019,8 @@ def main():
         "best": best,
         "roofline": roof,
     }
+    if extra is not None:
+        out[extra[0]] = extra[1]
     if dominant != "maxflow" and "maxflow" in kernel_us and mf["push_relabel"] > 0:
         # the LDS-resident max-flow beside the dominant kernel, against the LDS peak, when some
         # candidate needed push-relabel (closed forms touch their arcs once, so an LDS fraction
