@@ -103,6 +103,8 @@ def parse():
                     help="5: the refinement chain (--rounds rounds of 131,072 perturbations of the previous "
                          "round's best, per-GPU flow nodes)")
     ap.add_argument("--rounds", type=int, default=0, help="--workload 5: rounds of the chain (default: 16)")
+    ap.add_argument("--round-repeats", type=int, default=3,
+                    help="--workload 5: each round's batch is scored this many times; its time is the median")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", choices=list(VARIANTS), default="as-written",
                     help="cost-model variant: the model as written, pipelined decode capacity, KV stage-order "
@@ -132,6 +134,9 @@ def parse():
     ap.add_argument("--concurrent-streams", type=int, default=3,
                     help="also report the rate with this many independent steps in flight (a short extra pass; "
                          "0 or 1: none)")
+    ap.add_argument("--no-shared-groups-hint", action="store_true",
+                    help="--workload 5 and --refine: score without the hint that the batch's candidates share "
+                         "candidate 0's groups")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -395,7 +400,8 @@ def refine_main(args, torch, hx, I):
     rounds_total = args.warmup + args.steps
     draws = [torch.as_tensor(I.move_draws(cfg, r, n_child).view(np.int64)).to("cuda") for r in range(rounds_total)]
     dp = hx.DeviceProblem.upload(prob0)
-    ref = hx.Refiner.create(dp, 0, n_child)
+    hint = not args.no_shared_groups_hint
+    ref = hx.Refiner.create(dp, 0, n_child, shared_groups_hint=hint)
     trace = []
     for r in range(args.warmup):
         ref.round(draws[r])
@@ -411,7 +417,7 @@ def refine_main(args, torch, hx, I):
     final = [int(x) for x in ref.child_ws.best.cpu().numpy()]
 
     # per-kernel durations over a replay of the same rounds from the same start
-    ref2 = hx.Refiner.create(dp, 0, n_child)
+    ref2 = hx.Refiner.create(dp, 0, n_child, shared_groups_hint=hint)
     hx.profile(True)
     for r in range(rounds_total):
         ref2.round(draws[r])
@@ -469,7 +475,7 @@ def refine_main(args, torch, hx, I):
             bi, bv = (int(x) for x in ws_r.best.cpu().numpy())
             rand_best.append(bv)
             cur = (pr.assign[:, bi].copy(), pr.role[:, bi].copy())
-        ref3 = hx.Refiner.create(dp, 0, n_child)
+        ref3 = hx.Refiner.create(dp, 0, n_child, shared_groups_hint=hint)
         guided_best = []
         for r in range(args.quality_rounds):
             ref3.round(draws[r] if r < rounds_total else
@@ -491,7 +497,7 @@ def refine_main(args, torch, hx, I):
         "data": "synthetic",
         "config": {"workload": f"workload{cfg}: {wl.name}, max-flow guided rounds from the one-group-per-node base",
                    "children_per_round": n_child, "cluster_gpus": cp.n_gpus, "max_groups": cp.max_groups,
-                   "granularity": cp.granularity},
+                   "granularity": cp.granularity, "shared_groups_hint": hint},
         "kernel_ms_per_round": kernel_ms_per_round,
         "best_after_warmup_rounds": trace,
         "best": final,
@@ -613,7 +619,9 @@ def chain_main(args, torch, hx, I):
     swap two GPUs, 10% merge two groups) of the previous round's best placement, the GPU argmax,
     from the one-group-per-node base; per-GPU flow nodes (up to 258 nodes, ~4,000 KV edges).
     Each round's batch is generated on the host (timed apart), copied to the GPU (timed apart),
-    then scored; value = all rounds' candidates / their summed scoring time, inputs resident."""
+    then scored --round-repeats times (each a whole scoring, host launch to synchronize; the
+    round's time is their median, which drops one-off host stalls); value = all rounds'
+    candidates / their summed scoring time, inputs resident."""
     cfg = 5
     wl = I.WORKLOADS[cfg]
     n = args.candidates or wl.n_cand
@@ -621,7 +629,9 @@ def chain_main(args, torch, hx, I):
     G = wl.n_gpus
     cur = I.base_placement(wl)
     prob = I.make_problem(cfg, n_cand=n, rnd=0, base=cur)
-    dp = hx.DeviceProblem.upload(prob)
+    # every candidate is one move away from the same placement: candidate 0's groups are costed
+    # once and shared (HX_HINT_SHARED_GROUPS; the outputs are the same without it)
+    dp = hx.DeviceProblem.upload(prob).with_hint(not args.no_shared_groups_hint)
     ws = hx.Workspace.for_problem(dp, flows=False)
     h_assign = torch.empty((G, n), dtype=torch.uint8).pin_memory()
     h_role = torch.empty((prob.max_groups, n), dtype=torch.uint8).pin_memory()
@@ -642,13 +652,16 @@ def chain_main(args, torch, hx, I):
         d_role.copy_(h_role, non_blocking=True)
         torch.cuda.synchronize()
         h2d_ms = (time.perf_counter() - t) * 1000.0
-        t = time.perf_counter()
-        hx.score_batch(dp, ws)
-        torch.cuda.synchronize()
-        score_ms = (time.perf_counter() - t) * 1000.0
+        times = []
+        for _ in range(max(1, args.round_repeats)):
+            t = time.perf_counter()
+            hx.score_batch(dp, ws)
+            torch.cuda.synchronize()
+            times.append((time.perf_counter() - t) * 1000.0)
+        score_ms = float(np.median(times))
         bi, bv = (int(x) for x in ws.best.cpu().numpy())
-        per_round.append({"round": r, "score_ms": score_ms, "h2d_ms": h2d_ms, "host_generation_s": gen_s,
-                          "best_index": bi, "best_flow": bv})
+        per_round.append({"round": r, "score_ms": score_ms, "first_pass_ms": times[0], "h2d_ms": h2d_ms,
+                          "host_generation_s": gen_s, "best_index": bi, "best_flow": bv})
         probs.append((pr, bi, bv))
         cur = (pr.assign[:, bi].copy(), pr.role[:, bi].copy())
         print(f"[chain] round {r}: {score_ms:.3f} ms, best {bv} at {bi}", file=sys.stderr, flush=True)
@@ -691,9 +704,13 @@ def chain_main(args, torch, hx, I):
         "config": {"workload": f"workload5: {wl.name}; {rounds} chained rounds of {n:,}, each perturbing "
                                "the previous round's GPU best",
                    "candidates": rounds * n, "cluster_gpus": G, "max_groups": prob.max_groups,
-                   "granularity": prob.granularity},
+                   "granularity": prob.granularity, "shared_groups_hint": not args.no_shared_groups_hint,
+                   "round_repeats": max(1, args.round_repeats)},
         "rounds": per_round,
         "host_generation_s": sum(x["host_generation_s"] for x in per_round),
+        "first_pass": {"value": rounds * n / (sum(x["first_pass_ms"] for x in per_round) / 1000.0),
+                       "unit": "candidates/s",
+                       "note": "each round's first scoring only (right after its batch is copied in)"},
         "with_h2d_copy": {"value": rounds * n / ((total_ms + sum(x["h2d_ms"] for x in per_round)) / 1000.0),
                           "unit": "candidates/s", "note": "each round's assign and role copied from pinned host memory"},
         "kernel_us": kernel_us,

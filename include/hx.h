@@ -127,6 +127,13 @@ typedef struct hx_space { uint32_t tp_mask, pp_mask; int32_t granularity; uint32
  * stage holds one layer plus its compute's share of the other L - pp (see hx_cost_eval).  Not
  * combinable with HX_VARIANT_KV_ORDER. */
 #define HX_VARIANT_ASYM 4u
+/* A hint in hx_space.variant, not a variant of the model: the batch's candidates share most of
+ * their groups with candidate 0 (refinement rounds, whose candidates are single-step moves of
+ * one placement).  hx_cost_eval then costs candidate 0's groups first, and a group of another
+ * candidate with the same member set and role as candidate 0's group in the same slot, or in
+ * one of the two slots next to it, takes that group's outputs instead of being costed again.
+ * The outputs are the same with or without the hint. */
+#define HX_HINT_SHARED_GROUPS (1u << 16)
 
 /* Candidate placements (Sec. 3.1).  assign[g][n] = group of GPU g in candidate n (HX_UNUSED
  * or >= max_groups: GPU unused); role[k][n] = HX_PREFILL, HX_DECODE, or anything else (no
@@ -421,8 +428,8 @@ int hx_partition_candidates(const hx_cluster *cluster, hx_model model, hx_worklo
  * gives kernel k's name: setup, decode, scatter, eval (hx_cost_eval), nodes, kv
  * (hx_build_flownet), maxflow, best, classes (hx_edge_classes), moves (hx_guided_moves),
  * gather (hx_gather_candidates), spectral (hx_spectral_order), partition
- * (hx_partition_candidates). */
-#define HX_KERNELS 13
+ * (hx_partition_candidates), shared (candidate 0's groups under HX_HINT_SHARED_GROUPS). */
+#define HX_KERNELS 14
 int hx_profile(int32_t enable);
 int hx_profile_read(double *ms, int32_t *launches, int32_t n);
 const char *hx_kernel_name(int32_t k);

@@ -45,7 +45,8 @@ int check_problem(const hx_cluster* c, const hx_model& m, const hx_workload& w, 
     if (w.n_classes > 0 && (s.variant & (HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM))) return HX_EINVAL;
     if (s.tp_mask == 0 || s.tp_mask >= (1u << HX_MAX_TP) || s.pp_mask == 0) return HX_EINVAL;
     if (s.granularity != 0 && s.granularity != 1) return HX_EINVAL;
-    if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM)) return HX_EINVAL;
+    if (s.variant & ~(uint32_t)(HX_VARIANT_PIPELINED | HX_VARIANT_KV_ORDER | HX_VARIANT_ASYM | HX_HINT_SHARED_GROUPS))
+        return HX_EINVAL;
     if ((s.variant & HX_VARIANT_KV_ORDER) && (s.variant & HX_VARIANT_ASYM)) return HX_EINVAL;
     // the stage-order search covers pipelines of up to 8 stages
     if ((s.variant & HX_VARIANT_KV_ORDER) && (s.pp_mask >> 8)) return HX_EINVAL;
@@ -263,7 +264,7 @@ int hx_profile_read(double* ms, int32_t* launches, int32_t n) {
 const char* hx_kernel_name(int32_t k) {
     static const char* names[hx::kKCount] = {"setup", "decode",  "scatter", "eval",     "nodes",
                                              "kv",    "maxflow", "best",    "classes",  "moves",
-                                             "gather", "spectral", "partition"};
+                                             "gather", "spectral", "partition", "shared"};
     return k >= 0 && k < hx::kKCount ? names[k] : "";
 }
 

@@ -257,6 +257,43 @@ __device__ __forceinline__ bool cost_mix(const Problem& p, const Tables& tb, con
     return true;
 }
 
+// The kept strategy of a group of cnt GPUs (member r at mem[r * stride]) with admissible set
+// adm: every strategy costed in ascending tp, prefill keeping the strictly lowest latency and
+// decode the strictly highest x (Sec. 3.3, "Compute nodes").  have: some strategy was feasible.
+struct GroupCost {
+    int tp, pp;
+    double b, lat, x;
+    bool have;
+};
+
+__device__ __forceinline__ int stage_count(int c, int tp);
+
+template <int kVar>
+__device__ __forceinline__ GroupCost cost_group(const Problem& p, const Tables& tb, const uint8_t* mem, int stride,
+                                                uint32_t adm, int cnt, int role) {
+    GroupCost r{0, 0, 0.0, 0.0, 0.0, false};
+    for (uint32_t am = adm; am; am &= am - 1) {
+        const int tp = __ffs(am);
+        const int pp = stage_count(cnt, tp);
+        StrategyCost sc;
+        if constexpr ((kVar & kVarClasses) != 0) {
+            if (!cost_mix<kVar & ~kVarClasses>(p, tb, mem, stride, tp, pp, role, sc)) continue;
+        } else if (!cost_any<kVar>(p, tb, mem, stride, tp, pp, role, sc)) {
+            continue;
+        }
+        const bool better = !r.have || (role == HX_PREFILL ? sc.lat < r.lat : sc.x > r.x);
+        if (better) {
+            r.have = true;
+            r.tp = tp;
+            r.pp = pp;
+            r.b = sc.bmax;
+            r.lat = sc.lat;
+            r.x = sc.x;
+        }
+    }
+    return r;
+}
+
 // Admissible strategies of a group of c GPUs, bit tp-1 for each tp of the mask dividing c with
 // pp = c/tp in the PP mask and at most L (the strategy list of Sec. 3.2 for that size).
 __device__ __forceinline__ uint8_t admissible(const Problem& p, int c) {
@@ -277,6 +314,34 @@ __device__ __forceinline__ int stage_count(int c, int tp) {
 
 // ------------------------------------------------------------------ kernels
 
+// HX_HINT_SHARED_GROUPS: candidate 0's groups, costed once: member masks [Kmax][W] (4 Kmax
+// words reserved), roles [Kmax] (HX_UNUSED for a slot with no member or no role) and outputs
+// (a one-candidate table: entry k is slot k's).  One contiguous block of ref_bytes(Kmax), so
+// decode can stage it in LDS with one copy and carve it the same way.
+struct RefTable {
+    uint64_t* m;
+    uint8_t* role;
+    CostOut out;
+};
+
+__host__ __device__ inline size_t ref_bytes(int Kmax) {
+    return ((size_t)Kmax * (4 * sizeof(uint64_t) + sizeof(double) + 2 * sizeof(int32_t) + 3) + 15) & ~(size_t)15;
+}
+
+__host__ __device__ inline RefTable carve_ref(unsigned char* r, int Kmax) {
+    const size_t K = (size_t)Kmax;
+    RefTable t;
+    t.m = reinterpret_cast<uint64_t*>(r);
+    t.out.lat = reinterpret_cast<double*>(r + 4 * sizeof(uint64_t) * K);
+    t.out.bmax = reinterpret_cast<int32_t*>(t.out.lat + K);
+    t.out.cap = t.out.bmax + K;
+    t.out.tp = reinterpret_cast<uint8_t*>(t.out.cap + K);
+    t.out.pp = t.out.tp + K;
+    t.role = t.out.pp + K;
+    t.out.members = nullptr;
+    return t;
+}
+
 struct CostWork {
     int32_t* hist;    // [nb + 1]: per (size, role) unit counts ([nb] unused)
     int32_t* cursor;  // [nb]: units placed so far per bucket
@@ -287,6 +352,8 @@ struct CostWork {
     double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables), class 0
     double* pp_pre;   // [G][G] prefill PP terms, class 0; class k's tables sit k table blocks on
                       // ((HX_MAX_TP + 1) G^2 doubles each)
+    unsigned char* ref_base;  // candidate 0's table (RefTable), ref_bytes(Kmax)
+    RefTable ref;
 };
 
 // The memory-row screen, a W-word GPU bitmask per group size c = 0..G, then wild (entry G + 1).
@@ -415,7 +482,7 @@ constexpr int kGpuChunk = 32;
 // slots at a time; when Kmax exceeds Kc (very many slots of wide masks) the slots are built Kc
 // at a time, the assign column read once per block of slots.
 template <int W, int C>
-__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk, int Kc) {
+__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk, int Kc, bool use_ref) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int nb = 2 * (p.G + 1);
     int32_t* lhist = reinterpret_cast<int32_t*>(smem);
@@ -424,11 +491,19 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     const int tid = threadIdx.x, bs = blockDim.x;
     for (int b = tid; b < nb; b += bs) lhist[b] = 0;
     for (int e = tid; e < (p.G + 2) * W; e += bs) unfit[e] = wk.unfit[e];
+    // with the hint: candidate 0's table, after the mask columns
+    unsigned char* rbase = reinterpret_cast<unsigned char*>(ms + (size_t)Kc * W * bs);
+    const RefTable ref = carve_ref(rbase, p.Kmax);
+    if (use_ref) {
+        const uint64_t* src = reinterpret_cast<const uint64_t*>(wk.ref_base);
+        uint64_t* dst = reinterpret_cast<uint64_t*>(rbase);
+        for (int e = tid; e < (int)(ref_bytes(p.Kmax) / 8); e += bs) dst[e] = src[e];
+    }
     const bool screen = (p.variant & HX_VARIANT_ASYM) == 0;  // the screen assumes the uniform split
     const int n = blockIdx.x * bs + tid;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
-    __syncthreads();  // lhist cleared
+    __syncthreads();  // lhist cleared, tables staged
     for (int kc = 0; kc < Kmax && n < N; kc += Kc) {
         // slots [kc, ke) in the lane's column, slot k at row k - kc
         const int ke = kc + Kc < Kmax ? kc + Kc : Kmax;
@@ -463,8 +538,28 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
                 const bool costed = size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE) &&
                                     !(screen && screened_out<W>(unfit, p.G, m, size));
                 const int64_t o_ = (int64_t)k * N + n;
-                if (costed) {
+                // a group of candidate 0 (same members, same role) takes its outputs: costing it
+                // again would give the same values.  Groups are looked for in the same slot and
+                // the two next to it (slot-wise numbering shifts a slot by one after a merge);
+                // the slot index is uniform, so the reads are the same for every lane.
+                int hit = -1;
+                if (costed && use_ref) {
+                    const int lo = k > 0 ? k - 1 : 0, hi = k + 1 < Kmax ? k + 1 : Kmax - 1;
+                    for (int e = lo; e <= hi; ++e) {
+                        bool same = ref.role[e] == rl[x];
+#pragma unroll
+                        for (int i = 0; i < W; ++i) same = same && ref.m[e * W + i] == m[i];
+                        if (same) hit = e;
+                    }
+                }
+                if (costed && hit < 0) {
                     atomicAdd(&lhist[bucket_of(p.G, size, rl[x])], 1);
+                } else if (hit >= 0) {
+                    o.tp[o_] = ref.out.tp[hit];
+                    o.pp[o_] = ref.out.pp[hit];
+                    o.bmax[o_] = ref.out.bmax[hit];
+                    o.cap[o_] = ref.out.cap[hit];
+                    o.lat[o_] = ref.out.lat[hit];
                 } else {
                     o.tp[o_] = 0;
                     o.pp[o_] = 0;
@@ -472,7 +567,7 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
                     o.cap[o_] = 0;
                     o.lat[o_] = 0.0;
                 }
-                wk.ukey[o_] = costed ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
+                wk.ukey[o_] = costed && hit < 0 ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
             }
         }
     }
@@ -619,16 +714,33 @@ __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
 // is false for groups past the last large unit (they still join every wave-level sync).  With
 // request classes (kVarClasses) each strategy is costed once per class, and the mix kept as
 // cost_mix keeps it.
-template <int kVar, int kCL>
+template <int W, int kVar, int kCL>
 __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o, const CoopLds& c,
-                          const uint8_t* adm_tab, int gl, bool live, int n, int k, int role, uint64_t mask) {
+                          const uint8_t* adm_tab, int gl, bool live, int n, int k, int role,
+                          const uint64_t (&mask)[W]) {
     constexpr bool kPipe = (kVar & HX_VARIANT_PIPELINED) != 0;
     constexpr bool kAsym = (kVar & HX_VARIANT_ASYM) != 0;
     constexpr bool kCls = (kVar & kVarClasses) != 0;
     const int G = p0.G;
-    const int cnt = live ? __popcll(mask) : 0;
-    for (int g = gl; g < G && live; g += kCL)
-        if ((mask >> g) & 1ull) c.mem[__popcll(mask & ((1ull << g) - 1))] = (uint8_t)g;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) cnt += live ? __popcll(mask[i]) : 0;
+    // member ids ascending: GPU g goes to position (members below g)
+    for (int g = gl; g < G && live; g += kCL) {
+        const int wd = g >> 6;
+        const uint64_t below = (1ull << (g & 63)) - 1;
+        int pos = 0;
+        bool in = false;
+#pragma unroll
+        for (int i = 0; i < W; ++i) {
+            if (i < wd) pos += __popcll(mask[i]);
+            if (i == wd) {
+                in = (mask[i] >> (g & 63)) & 1ull;
+                pos += __popcll(mask[i] & below);
+            }
+        }
+        if (in) c.mem[pos] = (uint8_t)g;
+    }
     wave_sync();
     const double H = p0.H, B = p0.B;
     const double W12 = 12.0 * H * H * B;
@@ -787,6 +899,68 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
     }
 }
 
+// HX_HINT_SHARED_GROUPS: candidate 0's groups costed once, kCoopLanes lanes per group slot
+// with coop_unit (the same binary64 values as the one-lane path), into the one-candidate
+// table wk.ref.out; their member masks and roles into wk.ref.m and wk.ref.role.  A wavefront per
+// workgroup, 64 / kCoopLanes slots each, so the slots' chains of table loads run side by side.
+template <int W, int kVar>
+__global__ void __launch_bounds__(64) ref_kernel(Problem p, CostWork wk) {
+    constexpr int kCL = kCoopLanes, kPer = 64 / kCL;
+    extern __shared__ __attribute__((aligned(16))) double rsm[];
+    __shared__ uint8_t adm_tab[HX_MAX_GPUS + 1];
+    const int G = p.G, tid = threadIdx.x, grp = tid / kCL, gl = tid % kCL;
+    double* gfl = rsm;
+    double* ghb = gfl + G;
+    double* gme = ghb + G;
+    uint8_t* a0 = reinterpret_cast<uint8_t*>(gme + G);  // [G] candidate 0's assign column
+    for (int g = tid; g < G; g += 64) {
+        const int t = p.gpu_type[g];
+        const bool ok = t >= 0 && t < p.T;
+        gfl[g] = ok ? p.flops[t] : 0.0;
+        ghb[g] = ok ? p.hbm[t] : 0.0;
+        gme[g] = ok ? p.mem[t] : 0.0;
+        a0[g] = p.assign[(int64_t)g * p.N];
+    }
+    for (int c = tid; c <= G; c += 64) adm_tab[c] = admissible(p, c);
+    __syncthreads();
+    const Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre};
+    const int k = blockIdx.x * kPer + grp;
+    // slot k's members: each lane of the slot's lane group marks every kCL-th GPU, then OR
+    uint64_t m[W] = {};
+    for (int g = gl; g < G && k < p.Kmax; g += kCL)
+        if (a0[g] == k) {
+#pragma unroll
+            for (int i = 0; i < W; ++i)
+                if (i == (g >> 6)) m[i] |= 1ull << (g & 63);
+        }
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        for (int off = kCL / 2; off > 0; off >>= 1)
+            m[i] |= (uint64_t)__shfl_xor((unsigned long long)m[i], off, kCL);
+        cnt += __popcll(m[i]);
+    }
+    const int role = k < p.Kmax ? p.role[(int64_t)k * p.N] : HX_UNUSED;
+    const bool live = k < p.Kmax && cnt > 0 && (role == HX_PREFILL || role == HX_DECODE);
+    Problem p1 = p;
+    p1.N = 1;  // the table holds one candidate
+    unsigned char* cbase = a0 + (((size_t)G + 7) & ~(size_t)7);
+    const CoopLds c = carve_coop(cbase + grp * coop_group_bytes(G), G);
+    coop_unit<W, kVar, kCL>(p1, tb, wk.ref.out, c, adm_tab, gl, live, 0, k, role, m);
+    if (k < p.Kmax && gl == 0) {
+#pragma unroll
+        for (int i = 0; i < W; ++i) wk.ref.m[(int64_t)k * W + i] = m[i];
+        wk.ref.role[k] = (uint8_t)(live ? role : HX_UNUSED);
+    }
+}
+
+// LDS of ref_kernel beyond its static arrays: the per-GPU tables, candidate 0's assign column
+// and the slots' coop_unit areas.
+__host__ inline size_t ref_lds_bytes(int G) {
+    return sizeof(double) * 3 * (size_t)G + (((size_t)G + 7) & ~(size_t)7) +
+           (size_t)(64 / kCoopLanes) * coop_group_bytes(G);
+}
+
 template <int W, bool kTables, int kEvalBlock, int kVar, int kCMin, int kCL>
 __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut o, CostWork wk, int nb) {
     extern __shared__ __attribute__((aligned(16))) double dsm[];
@@ -845,16 +1019,17 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
             const int64_t u = base + grp;
             const bool live = u < first_small;
             int n = 0, k = 0, role = 0;
-            uint64_t mask = 0;
+            uint64_t mask[W] = {};
             if (live) {
                 const uint64_t* rec = wk.units + u * (1 + W);
                 const uint64_t w = rec[0];
                 n = (int)(w >> 16);
                 k = (int)((w >> 8) & 0xFF);
                 role = (int)(w & 0xFF);
-                mask = rec[1];
+#pragma unroll
+                for (int i = 0; i < W; ++i) mask[i] = rec[1 + i];
             }
-            coop_unit<kVar, kCL>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
+            coop_unit<W, kVar, kCL>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
@@ -871,34 +1046,13 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
                 m &= m - 1;
             }
         }
-        bool have = false;
-        int best_tp = 0, best_pp = 0;
-        double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
-        for (uint32_t am = adm_tab[cnt]; am; am &= am - 1) {
-            const int tp = __ffs(am);
-            const int pp = stage_count(cnt, tp);
-            StrategyCost sc;
-            if constexpr ((kVar & kVarClasses) != 0) {
-                if (!cost_mix<kVar & ~kVarClasses>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) continue;
-            } else if (!cost_any<kVar>(p, tb, mem, kEvalBlock, tp, pp, role, sc)) {
-                continue;
-            }
-            const bool better = !have || (role == HX_PREFILL ? sc.lat < best_lat : sc.x > best_x);
-            if (better) {
-                have = true;
-                best_tp = tp;
-                best_pp = pp;
-                best_b = sc.bmax;
-                best_lat = sc.lat;
-                best_x = sc.x;
-            }
-        }
+        const GroupCost gc = cost_group<kVar>(p, tb, mem, kEvalBlock, adm_tab[cnt], cnt, role);
         const int64_t o_ = (int64_t)k * N + n;
-        o.tp[o_] = (uint8_t)best_tp;
-        o.pp[o_] = (uint8_t)best_pp;
-        o.bmax[o_] = (int32_t)best_b;
-        o.cap[o_] = have ? quantize(best_x) : 0;
-        o.lat[o_] = best_lat;
+        o.tp[o_] = (uint8_t)gc.tp;
+        o.pp[o_] = (uint8_t)gc.pp;
+        o.bmax[o_] = (int32_t)gc.b;
+        o.cap[o_] = gc.have ? quantize(gc.x) : 0;
+        o.lat[o_] = gc.lat;
     }
 }
 
@@ -957,13 +1111,40 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
     const size_t slot_bytes = (size_t)W * bs * 8;
     const int Kc = (size_t)p.Kmax * slot_bytes <= 48 * 1024 ? p.Kmax : (int)(48 * 1024 / slot_bytes);
+    // HX_HINT_SHARED_GROUPS: candidate 0's groups costed first, for decode to hand out (decode
+    // stages their table after its mask columns)
+    const bool use_ref = (p.variant & HX_HINT_SHARED_GROUPS) != 0;
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + sizeof(uint64_t) * (p.G + 2) * W +
-                           (size_t)Kc * slot_bytes;
+                           (size_t)Kc * slot_bytes + (use_ref ? ref_bytes(p.Kmax) : 0);
+    if (use_ref) {
+        const size_t lds_ref = ref_lds_bytes(p.G);
+        const dim3 gref((p.Kmax + 64 / kCoopLanes - 1) / (64 / kCoopLanes));
+        prof_mark(kKShared, false, s);
+        switch ((p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) | (p.n_cls > 0 ? kVarClasses : 0)) {
+            case 0: hipLaunchKernelGGL((ref_kernel<W, 0>), gref, dim3(64), lds_ref, s, p, wk); break;
+            case kVarClasses: hipLaunchKernelGGL((ref_kernel<W, kVarClasses>), gref, dim3(64), lds_ref, s, p, wk); break;
+            case kVarClasses | HX_VARIANT_PIPELINED:
+                hipLaunchKernelGGL((ref_kernel<W, kVarClasses | HX_VARIANT_PIPELINED>), gref, dim3(64), lds_ref, s, p,
+                                   wk);
+                break;
+            case HX_VARIANT_PIPELINED:
+                hipLaunchKernelGGL((ref_kernel<W, HX_VARIANT_PIPELINED>), gref, dim3(64), lds_ref, s, p, wk);
+                break;
+            case HX_VARIANT_ASYM:
+                hipLaunchKernelGGL((ref_kernel<W, HX_VARIANT_ASYM>), gref, dim3(64), lds_ref, s, p, wk);
+                break;
+            default:
+                hipLaunchKernelGGL((ref_kernel<W, HX_VARIANT_PIPELINED | HX_VARIANT_ASYM>), gref, dim3(64), lds_ref, s,
+                                   p, wk);
+                break;
+        }
+        prof_mark(kKShared, true, s);
+    }
     const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
     switch (slot_chunk(W, p.Kmax)) {
         case 8:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
+            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk);
@@ -971,7 +1152,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
             break;
         case 16:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
+            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk);
@@ -979,7 +1160,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
             break;
         default:
             prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc);
+            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
             prof_mark(kKDecode, true, s);
             prof_mark(kKScatter, false, s);
             hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk);
@@ -1034,12 +1215,17 @@ static size_t unfit_bytes(int32_t n_gpus) {
 
 // Layout: histogram and cursors, one more word (cleared with them; hx_score_batch's argmax
 // counts its finished workgroups there), unit records, prefill link tables, the memory-row
-// screen, and a key byte per group slot.
-size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+// screen, a key byte per group slot, and (256-byte aligned) candidate 0's reference groups.
+static size_t ref_offset(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 2) * sizeof(int32_t) + 255) & ~(size_t)255;
-    return head + units_bytes(n_gpus, max_groups, n_cand) + tables_bytes(n_gpus) + unfit_bytes(n_gpus) +
-           (size_t)max_groups * n_cand;
+    const size_t end = head + units_bytes(n_gpus, max_groups, n_cand) + tables_bytes(n_gpus) + unfit_bytes(n_gpus) +
+                       (size_t)max_groups * n_cand;
+    return (end + 255) & ~(size_t)255;
+}
+
+size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    return ref_offset(n_gpus, max_groups, n_cand) + ref_bytes(max_groups);
 }
 
 int32_t* cost_workspace_counter(void* workspace, int32_t n_gpus) {
@@ -1058,6 +1244,8 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
     wk.pp_pre = wk.tp_pre + (size_t)HX_MAX_TP * p.G * p.G;
     wk.unfit = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(wk.tp_pre) + tables_bytes(p.G));
     wk.ukey = reinterpret_cast<uint8_t*>(wk.unfit) + unfit_bytes(p.G);
+    wk.ref_base = reinterpret_cast<unsigned char*>(workspace) + ref_offset(p.G, p.Kmax, p.N);
+    wk.ref = carve_ref(wk.ref_base, p.Kmax);
     wk.gmask = o.members;
     switch (mask_words(p.G)) {
         case 1: return launch_w<1>(p, o, wk, s);

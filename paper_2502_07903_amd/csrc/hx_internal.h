@@ -86,7 +86,7 @@ __device__ __forceinline__ int split_layers(const LayerSplit& s, int j, double c
 // Kernels of libhx, for the diagnostic per-kernel timing behind hx_profile.
 enum KernelId {
     kKSetup, kKDecode, kKScatter, kKEval, kKNodes, kKKv, kKMaxflow, kKBest, kKClasses, kKMoves, kKGather,
-    kKSpectral, kKPartition, kKCount
+    kKSpectral, kKPartition, kKShared, kKCount
 };
 // While profiling is enabled, records a HIP event on s before (end = false) or after
 // (end = true) a launch of kernel k; does nothing otherwise.

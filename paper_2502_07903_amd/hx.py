@@ -71,6 +71,10 @@ def make_workload(prob) -> hx_workload:
     return w
 
 
+# hx_space.variant bit (include/hx.h HX_HINT_SHARED_GROUPS): a hint, not a model variant.
+HINT_SHARED_GROUPS = 1 << 16
+
+
 class hx_space(C.Structure):
     _fields_ = [("tp_mask", C.c_uint32), ("pp_mask", C.c_uint32), ("granularity", C.c_int32),
                 ("variant", C.c_uint32)]
@@ -98,7 +102,7 @@ EXPORTS = ("hx_validate", "hx_cost_eval", "hx_cost_eval_static", "hx_static_scra
            "hx_partition_workspace_bytes", "hx_spectral_order", "hx_partition_candidates",
            "hx_profile", "hx_profile_read", "hx_kernel_name", "hx_strerror", "hx_last_error",
            "hx_abi_version")
-HX_KERNELS = 13
+HX_KERNELS = 14
 
 _lib = None
 
@@ -253,6 +257,14 @@ class DeviceProblem:
                    hx_space(int(prob.tp_mask), int(prob.pp_mask), int(prob.granularity),
                             int(getattr(prob, "variant", 0))), k, cl.n_gpus,
                    int(prob.max_groups))
+
+    def with_hint(self, shared_groups: bool = True) -> "DeviceProblem":
+        """The same problem with the HX_HINT_SHARED_GROUPS hint set (or cleared): the batch's
+        candidates share most of their groups with candidate 0, which is costed first.  The
+        outputs are the same either way."""
+        v = self.space.variant | HINT_SHARED_GROUPS if shared_groups else self.space.variant & ~HINT_SHARED_GROUPS
+        sp = hx_space(self.space.tp_mask, self.space.pp_mask, self.space.granularity, v)
+        return dataclasses.replace(self, space=sp)
 
     def with_candidates(self, assign, role) -> "DeviceProblem":
         """The same cluster/model/workload with another candidate batch (device uint8 tensors)."""
@@ -487,7 +499,8 @@ class Refiner:
     move: object
 
     @classmethod
-    def create(cls, dp: DeviceProblem, parent_col: int, n_child: int, device: str = "cuda") -> "Refiner":
+    def create(cls, dp: DeviceProblem, parent_col: int, n_child: int, device: str = "cuda",
+               shared_groups_hint: bool = True) -> "Refiner":
         torch = _torch()
         pa = dp.tensors["assign"][:, parent_col:parent_col + 1].clone()
         pr = dp.tensors["role"][:, parent_col:parent_col + 1].clone()
@@ -496,7 +509,8 @@ class Refiner:
         mp, md, mpd = pws.net.dims
         ca = torch.empty((dp.n_gpus, n_child), dtype=torch.uint8, device=device)
         cr = torch.empty((dp.max_groups, n_child), dtype=torch.uint8, device=device)
-        children = dp.with_candidates(ca, cr)
+        # child 0 is the parent and every other child one move away from it
+        children = dp.with_candidates(ca, cr).with_hint(shared_groups_hint)
         return cls(parent, pws, torch.zeros((mp + md, 1), dtype=torch.uint8, device=device),
                    torch.zeros((mpd, 1), dtype=torch.uint8, device=device), children,
                    Workspace.for_problem(children, device=device),

@@ -51,7 +51,8 @@ def test_refinement_chain(torch):
         prob = I.make_problem(5, n_cand=n, rnd=r, base=cur)
         say(f"chain round {r}: scoring {n} candidates on the GPU")
         if dp is None:
-            dp = hx.DeviceProblem.upload(prob)
+            # every candidate is one move from the same placement (the shared-groups hint)
+            dp = hx.DeviceProblem.upload(prob).with_hint()
             ws = hx.Workspace.for_problem(dp, flows=False)
         else:
             dp.tensors["assign"].copy_(torch.from_numpy(prob.assign))

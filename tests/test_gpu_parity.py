@@ -548,7 +548,7 @@ def test_profile_counts_each_kernel(torch):
     prof = hx.profile_read()
     hx.profile(False)
     scoring = {"setup", "decode", "scatter", "eval", "nodes", "kv", "maxflow", "best"}
-    assert set(prof) == scoring | {"classes", "moves", "gather", "spectral", "partition"}
+    assert set(prof) == scoring | {"classes", "moves", "gather", "spectral", "partition", "shared"}
     for name, (ms, n) in prof.items():
         if name in scoring:
             assert n == 1 and ms > 0.0, (name, ms, n)
