@@ -474,15 +474,24 @@ __host__ inline int slot_chunk(int W, int Kmax) {
 // GPUs per chunk of assign rows a lane loads together.
 constexpr int kGpuChunk = 32;
 
+// Group slots whose masks decode builds at a time: 128 bytes of LDS columns per lane, so that a
+// 256-lane workgroup takes 32 KB and four of them share a CU (16, 8, 4 slots for 1, 2, 4 mask
+// words).
+template <int W>
+__host__ __device__ constexpr int decode_slots() {
+    return 128 / (8 * W);
+}
+
 // One lane per candidate (candidate-fastest, so every [row][n] access coalesces): the member
 // bitmask of each group slot, built in the lane's LDS column from its assign column; absent
 // slots' zero outputs; a per-workgroup histogram of units per bucket, added to the global one
-// with one atomic per bucket.  Loads go in chunks (kGpuChunk assign rows, C role rows) that
-// issue together, so a lane waits on memory once per chunk.  The LDS columns hold Kc group
-// slots at a time; when Kmax exceeds Kc (very many slots of wide masks) the slots are built Kc
-// at a time, the assign column read once per block of slots.
-template <int W, int C>
-__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk, int Kc, bool use_ref) {
+// with one atomic per bucket.  The assign column is loaded once, in chunks of kGpuChunk rows
+// that issue together, and kept in registers (four GPUs' group ids per word); the slots are
+// then built decode_slots<W>() at a time from it, their role rows loaded together per block.
+template <int W>
+__global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostWork wk, bool use_ref) {
+    constexpr int Kc = decode_slots<W>();
+    constexpr int kWords = 16 * W;  // packed assign words: 64 W GPUs
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int nb = 2 * (p.G + 1);
     int32_t* lhist = reinterpret_cast<int32_t*>(smem);
@@ -504,72 +513,102 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
     __syncthreads();  // lhist cleared, tables staged
-    for (int kc = 0; kc < Kmax && n < N; kc += Kc) {
+    if (n < N) {
+    // the lane's assign column: GPU g's group id in byte g % 4 of word g / 4 (HX_UNUSED past G,
+    // which no slot block holds: slots are < Kmax <= 255)
+    uint32_t pk[kWords];
+#pragma unroll
+    for (int c = 0; c < kWords / 8; ++c) {
+        if (c * kGpuChunk >= p.G) {
+#pragma unroll
+            for (int w = 0; w < 8; ++w) pk[c * 8 + w] = 0xFFFFFFFFu;
+            continue;
+        }
+        // every load issued (rows past G read row G - 1 and are replaced), so that the chunk's
+        // loads are in flight together
+        uint32_t a[kGpuChunk];
+#pragma unroll
+        for (int x = 0; x < kGpuChunk; ++x) {
+            const int g = c * kGpuChunk + x;
+            a[x] = p.assign[(int64_t)(g < p.G ? g : p.G - 1) * N + n];
+        }
+#pragma unroll
+        for (int x = 0; x < kGpuChunk; ++x)
+            if (c * kGpuChunk + x >= p.G) a[x] = HX_UNUSED;
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+            pk[c * 8 + w] = a[4 * w] | (a[4 * w + 1] << 8) | (a[4 * w + 2] << 16) | (a[4 * w + 3] << 24);
+    }
+    for (int kc = 0; kc < Kmax; kc += Kc) {
         // slots [kc, ke) in the lane's column, slot k at row k - kc
         const int ke = kc + Kc < Kmax ? kc + Kc : Kmax;
-        for (int e = 0; e < (ke - kc) * W; ++e) ms[e * bs + tid] = 0;
-        for (int g0 = 0; g0 < p.G; g0 += kGpuChunk) {
-            int a[kGpuChunk];
 #pragma unroll
-            for (int x = 0; x < kGpuChunk; ++x) a[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
+        for (int e = 0; e < Kc * W; ++e) ms[e * bs + tid] = 0;
 #pragma unroll
-            for (int x = 0; x < kGpuChunk; ++x) {
-                const int g = g0 + x, k = a[x];
-                if (k >= kc && k < ke) ms[((k - kc) * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
+        for (int w = 0; w < kWords; ++w) {
+            if (4 * w >= p.G) break;
+#pragma unroll
+            for (int y = 0; y < 4; ++y) {
+                const int g = 4 * w + y;
+                const uint32_t r = ((pk[w] >> (8 * y)) & 0xFFu) - (uint32_t)kc;
+                if (r < (uint32_t)(ke - kc)) ms[(r * W + (g >> 6)) * bs + tid] |= 1ull << (g & 63);
             }
         }
-        for (int k0 = kc; k0 < ke; k0 += C) {
-            int rl[C];
+        int rl[Kc];
 #pragma unroll
-            for (int x = 0; x < C; ++x)
-                rl[x] = k0 + x < ke ? p.role[(int64_t)(k0 + x) * N + n] : HX_UNUSED;
+        for (int x = 0; x < Kc; ++x) rl[x] = p.role[(int64_t)(kc + x < ke ? kc + x : ke - 1) * N + n];
 #pragma unroll
-            for (int x = 0; x < C; ++x) {
-                const int k = k0 + x;
-                if (k >= ke) break;
-                uint64_t m[W];
-                int size = 0;
+        for (int x = 0; x < Kc; ++x)
+            if (kc + x >= ke) rl[x] = HX_UNUSED;
 #pragma unroll
-                for (int i = 0; i < W; ++i) {
-                    m[i] = ms[((k - kc) * W + i) * bs + tid];
-                    wk.gmask[((int64_t)k * W + i) * N + n] = m[i];
-                    size += __popcll(m[i]);
-                }
-                const bool costed = size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE) &&
-                                    !(screen && screened_out<W>(unfit, p.G, m, size));
-                const int64_t o_ = (int64_t)k * N + n;
-                // a group of candidate 0 (same members, same role) takes its outputs: costing it
-                // again would give the same values.  Groups are looked for in the same slot and
-                // the two next to it (slot-wise numbering shifts a slot by one after a merge);
-                // the slot index is uniform, so the reads are the same for every lane.
-                int hit = -1;
-                if (costed && use_ref) {
-                    const int lo = k > 0 ? k - 1 : 0, hi = k + 1 < Kmax ? k + 1 : Kmax - 1;
-                    for (int e = lo; e <= hi; ++e) {
-                        bool same = ref.role[e] == rl[x];
+        for (int x = 0; x < Kc; ++x) {
+            const int k = kc + x;
+            if (k >= ke) break;
+            uint64_t m[W];
+            int size = 0;
 #pragma unroll
-                        for (int i = 0; i < W; ++i) same = same && ref.m[e * W + i] == m[i];
-                        if (same) hit = e;
-                    }
-                }
-                if (costed && hit < 0) {
-                    atomicAdd(&lhist[bucket_of(p.G, size, rl[x])], 1);
-                } else if (hit >= 0) {
-                    o.tp[o_] = ref.out.tp[hit];
-                    o.pp[o_] = ref.out.pp[hit];
-                    o.bmax[o_] = ref.out.bmax[hit];
-                    o.cap[o_] = ref.out.cap[hit];
-                    o.lat[o_] = ref.out.lat[hit];
-                } else {
-                    o.tp[o_] = 0;
-                    o.pp[o_] = 0;
-                    o.bmax[o_] = 0;
-                    o.cap[o_] = 0;
-                    o.lat[o_] = 0.0;
-                }
-                wk.ukey[o_] = costed && hit < 0 ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
+            for (int i = 0; i < W; ++i) {
+                m[i] = ms[(x * W + i) * bs + tid];
+                wk.gmask[((int64_t)k * W + i) * N + n] = m[i];
+                size += __popcll(m[i]);
             }
+            const bool costed = size > 0 && (rl[x] == HX_PREFILL || rl[x] == HX_DECODE) &&
+                                !(screen && screened_out<W>(unfit, p.G, m, size));
+            const int64_t o_ = (int64_t)k * N + n;
+            // a group of candidate 0 (same members, same role) takes its outputs: costing it
+            // again would give the same values.  Groups are looked for in the same slot and
+            // the two next to it (slot-wise numbering shifts a slot by one after a merge);
+            // the slot index is uniform, so the reads are the same for every lane.
+            int hit = -1;
+            if (costed && use_ref) {
+#pragma unroll
+                for (int d = -1; d <= 1; ++d) {
+                    const int e = k + d;
+                    if (e < 0 || e >= Kmax) continue;
+                    bool same = ref.role[e] == rl[x];
+#pragma unroll
+                    for (int i = 0; i < W; ++i) same = same && ref.m[e * W + i] == m[i];
+                    if (same) hit = e;
+                }
+            }
+            if (costed && hit < 0) {
+                atomicAdd(&lhist[bucket_of(p.G, size, rl[x])], 1);
+            } else if (hit >= 0) {
+                o.tp[o_] = ref.out.tp[hit];
+                o.pp[o_] = ref.out.pp[hit];
+                o.bmax[o_] = ref.out.bmax[hit];
+                o.cap[o_] = ref.out.cap[hit];
+                o.lat[o_] = ref.out.lat[hit];
+            } else {
+                o.tp[o_] = 0;
+                o.pp[o_] = 0;
+                o.bmax[o_] = 0;
+                o.cap[o_] = 0;
+                o.lat[o_] = 0.0;
+            }
+            wk.ukey[o_] = costed && hit < 0 ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
         }
+    }
     }
     lds_drain_barrier();
     for (int b = tid; b < nb; b += bs)
@@ -1105,17 +1144,13 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
         hipLaunchKernelGGL(setup_kernel, dim3(blocks), dim3(256), 0, s, p, wk, 2 * nb + 2, W);
         prof_mark(kKSetup, true, s);
     }
-    // decode: the widest workgroup whose per-lane masks fit in 32 KB of LDS; beyond 64 lanes,
-    // slots are built in blocks of Kc that fit 48 KB
-    int bs = 256;
-    while (bs > 64 && (size_t)p.Kmax * W * bs * 8 > 32 * 1024) bs /= 2;
-    const size_t slot_bytes = (size_t)W * bs * 8;
-    const int Kc = (size_t)p.Kmax * slot_bytes <= 48 * 1024 ? p.Kmax : (int)(48 * 1024 / slot_bytes);
+    // decode: 256 lanes, 32 KB of mask columns (decode_slots<W>() slots of W words per lane)
+    constexpr int bs = 256;
     // HX_HINT_SHARED_GROUPS: candidate 0's groups costed first, for decode to hand out (decode
     // stages their table after its mask columns)
     const bool use_ref = (p.variant & HX_HINT_SHARED_GROUPS) != 0;
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + sizeof(uint64_t) * (p.G + 2) * W +
-                           (size_t)Kc * slot_bytes + (use_ref ? ref_bytes(p.Kmax) : 0);
+                           sizeof(uint64_t) * decode_slots<W>() * W * bs + (use_ref ? ref_bytes(p.Kmax) : 0);
     if (use_ref) {
         const size_t lds_ref = ref_lds_bytes(p.G);
         const dim3 gref((p.Kmax + 64 / kCoopLanes - 1) / (64 / kCoopLanes));
@@ -1141,32 +1176,16 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
         prof_mark(kKShared, true, s);
     }
     const dim3 gdec((p.N + bs - 1) / bs), gsc((p.N + 255) / 256);
+    prof_mark(kKDecode, false, s);
+    hipLaunchKernelGGL((decode_kernel<W>), gdec, dim3(bs), lds_dec, s, p, o, wk, use_ref);
+    prof_mark(kKDecode, true, s);
+    prof_mark(kKScatter, false, s);
     switch (slot_chunk(W, p.Kmax)) {
-        case 8:
-            prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, 8>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
-            prof_mark(kKDecode, true, s);
-            prof_mark(kKScatter, false, s);
-            hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk);
-            prof_mark(kKScatter, true, s);
-            break;
-        case 16:
-            prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W <= 2 ? 16 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
-            prof_mark(kKDecode, true, s);
-            prof_mark(kKScatter, false, s);
-            hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk);
-            prof_mark(kKScatter, true, s);
-            break;
-        default:
-            prof_mark(kKDecode, false, s);
-            hipLaunchKernelGGL((decode_kernel<W, (W == 1 ? 32 : 8)>), gdec, dim3(bs), lds_dec, s, p, o, wk, Kc, use_ref);
-            prof_mark(kKDecode, true, s);
-            prof_mark(kKScatter, false, s);
-            hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk);
-            prof_mark(kKScatter, true, s);
-            break;
+        case 8: hipLaunchKernelGGL((scatter_kernel<W, 8>), gsc, dim3(256), 0, s, p, wk); break;
+        case 16: hipLaunchKernelGGL((scatter_kernel<W, (W <= 2 ? 16 : 8)>), gsc, dim3(256), 0, s, p, wk); break;
+        default: hipLaunchKernelGGL((scatter_kernel<W, (W == 1 ? 32 : 8)>), gsc, dim3(256), 0, s, p, wk); break;
     }
+    prof_mark(kKScatter, true, s);
     const bool tables = p.G <= kTableMaxG;
     // A grid-stride loop over the units: enough workgroups to fill the chip several times.
     // 256 lanes per workgroup amortise the staged tables; the per-lane member columns take

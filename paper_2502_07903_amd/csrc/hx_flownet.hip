@@ -53,14 +53,22 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
         for (int k0 = 0; k0 < p.Kmax; k0 += kC) {
             int sz[kC], rl[kC];
             int32_t cp[kC];
+            // every load issued (slots past Kmax read slot Kmax - 1 and are replaced), so that
+            // the chunk's loads are in flight together
 #pragma unroll
             for (int x = 0; x < kC; ++x) {
-                const int k = k0 + x;
-                const bool in = k < p.Kmax;
-                sz[x] = in ? mask_size<W>(o.members, k, N, n) : 0;
-                rl[x] = in ? p.role[(int64_t)k * N + n] : HX_UNUSED;
-                cp[x] = in ? o.cap[(int64_t)k * N + n] : 0;
+                const int k = k0 + x < p.Kmax ? k0 + x : p.Kmax - 1;
+                sz[x] = mask_size<W>(o.members, k, N, n);
+                rl[x] = p.role[(int64_t)k * N + n];
+                cp[x] = o.cap[(int64_t)k * N + n];
             }
+#pragma unroll
+            for (int x = 0; x < kC; ++x)
+                if (k0 + x >= p.Kmax) {
+                    sz[x] = 0;
+                    rl[x] = HX_UNUSED;
+                    cp[x] = 0;
+                }
 #pragma unroll
             for (int x = 0; x < kC; ++x) {
                 if (sz[x] == 0) continue;
@@ -148,14 +156,22 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
     for (int k0 = 0; k0 < Kmax; k0 += kC) {
         int32_t cp[kC];
         int rl[kC], sz[kC];
+        // every load issued (slots past Kmax read slot Kmax - 1 and are replaced), so that the
+        // chunk's loads are in flight together
 #pragma unroll
         for (int x = 0; x < kC; ++x) {
-            const int k = k0 + x;
-            const bool ok = k < Kmax;
-            sz[x] = ok ? mask_size<W>(o.members, k, N, (int)n) : 0;
-            rl[x] = ok ? p.role[(int64_t)k * N + n] : HX_UNUSED;
-            cp[x] = ok ? o.cap[(int64_t)k * N + n] : 0;
+            const int k = k0 + x < Kmax ? k0 + x : Kmax - 1;
+            sz[x] = mask_size<W>(o.members, k, N, (int)n);
+            rl[x] = p.role[(int64_t)k * N + n];
+            cp[x] = o.cap[(int64_t)k * N + n];
         }
+#pragma unroll
+        for (int x = 0; x < kC; ++x)
+            if (k0 + x >= Kmax) {
+                sz[x] = 0;
+                rl[x] = HX_UNUSED;
+                cp[x] = 0;
+            }
 #pragma unroll
         for (int x = 0; x < kC; ++x) {
             const int k = k0 + x;
@@ -181,9 +197,19 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
         if (replay)
             for (int k = 0; k < Kmax; ++k) gseen[k * 64 + lane] = 0;
         for (int g0 = 0; g0 < p.G; g0 += kC) {
+            // the chunk's loads issued together (rows past G read row G - 1 and are replaced);
+            // kValue: the GPUs' smallest link capacities with them
             int kk[kC];
+            int32_t rm[kC];
 #pragma unroll
-            for (int x = 0; x < kC; ++x) kk[x] = g0 + x < p.G ? p.assign[(int64_t)(g0 + x) * N + n] : HX_UNUSED;
+            for (int x = 0; x < kC; ++x) {
+                const int g = g0 + x < p.G ? g0 + x : p.G - 1;
+                kk[x] = p.assign[(int64_t)g * N + n];
+                rm[x] = kValue ? rmin[g] : 0;
+            }
+#pragma unroll
+            for (int x = 0; x < kC; ++x)
+                if (g0 + x >= p.G) kk[x] = HX_UNUSED;
 #pragma unroll
             for (int x = 0; x < kC; ++x) {
                 const int g = g0 + x, k = kk[x];
@@ -208,7 +234,7 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
                         sa += a;
                         if (a > 0) {
                             any_a = true;
-                            const int32_t m = rmin[g];
+                            const int32_t m = rm[x];
                             if (m < a && m < t1) t1 = m;
                         }
                     }
