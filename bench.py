@@ -85,7 +85,7 @@ PARTITION_TRAFFIC = {"source_sha256_16": "72b4245b3df4f290", "candidates": 16384
                      "write_kib": 6144.0}
 KERNEL_SOURCE = {"setup": "hx_cost.hip", "decode": "hx_cost.hip", "scatter": "hx_cost.hip", "eval": "hx_cost.hip",
                  "nodes": "hx_flownet.hip", "kv": "hx_flownet.hip", "maxflow": "hx_maxflow.hip",
-                 "best": "hx_best.hip"}
+                 "best": "hx_best.hip", "shared": "hx_cost.hip"}
 
 
 # hx_space.variant bits: 1 pipelined decode capacity, 2 KV stage-order search, 4 asymmetric

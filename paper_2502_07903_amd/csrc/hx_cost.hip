@@ -163,10 +163,21 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                 const double* brow = tb.beta + d * G;
                 const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
                 double sum = 0.0;
+                if (prefill) {
+                    // table lookups: the row's loads issued together (S[q] is 0 past tp), then
+                    // summed in ascending peer order
+                    double v[kMax];
 #pragma unroll
-                for (int q = 0; q < kMax; ++q) {
-                    if ((TPC == 0 && q >= tp) || q == r) continue;
-                    sum = sum + (prefill ? prow[S[q]] : (arow[S[q]] + X / (t * brow[S[q]])));
+                    for (int q = 0; q < kMax; ++q) v[q] = prow[S[q]];
+#pragma unroll
+                    for (int q = 0; q < kMax; ++q)
+                        if (!((TPC == 0 && q >= tp) || q == r)) sum = sum + v[q];
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kMax; ++q) {
+                        if ((TPC == 0 && q >= tp) || q == r) continue;
+                        sum = sum + (arow[S[q]] + X / (t * brow[S[q]]));
+                    }
                 }
                 if (r == 0 || sum > mx) mx = sum;
             }
@@ -186,11 +197,20 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
                 const double* arow = tb.alpha + d * G;
                 const double* brow = tb.beta + d * G;
                 const double* prow = tb.pp_pre + (size_t)d * G;
+                if (prefill) {
+                    double v[kMax];
 #pragma unroll
-                for (int q = 0; q < kMax; ++q) {
-                    if (TPC == 0 && q >= tp) continue;
-                    const double v = prefill ? prow[S[q]] : arow[S[q]] + X / brow[S[q]];
-                    if ((r == 0 && q == 0) || v < mn) mn = v;
+                    for (int q = 0; q < kMax; ++q) v[q] = prow[S[q]];
+#pragma unroll
+                    for (int q = 0; q < kMax; ++q)
+                        if (!(TPC == 0 && q >= tp) && ((r == 0 && q == 0) || v[q] < mn)) mn = v[q];
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kMax; ++q) {
+                        if (TPC == 0 && q >= tp) continue;
+                        const double v = arow[S[q]] + X / brow[S[q]];
+                        if ((r == 0 && q == 0) || v < mn) mn = v;
+                    }
                 }
             }
             const double ppt = prefill ? mn : mn * p.s_out;
