@@ -53,26 +53,28 @@ COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
     # workload 3 (profiles/all_kernels_workload3.md); best is hx_score_batch's split argmax
     3: {
-        "setup": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 67.5, "write_kib": 32.81},
-        "decode": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 1668.0, "write_kib": 27820.0},
-        "scatter": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 4935.0, "write_kib": 1488.0},
-        "eval": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 1147.0, "write_kib": 12140.0},
-        "nodes": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 6698.0, "write_kib": 20400.0},
-        "kv": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 5885.0, "write_kib": 13400.0},
+        "setup": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 69.5, "write_kib": 32.81},
+        "decode": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 1718.0, "write_kib": 27820.0},
+        "scatter": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 4935.0, "write_kib": 1487.0},
+        "eval": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 1154.0, "write_kib": 12140.0},
+        "nodes": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 6697.0, "write_kib": 18230.0},
+        "kv": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 5883.0, "write_kib": 13400.0},
         "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 16740.0, "write_kib": 256.0},
         "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 165.8, "write_kib": 4.062},
     },
-    # workload 5, one chain round through hx_score_batch (profiles/chain_workload5.md): nodes is the
-    # settling nodes kernel, kv the link table, maxflow the list-driven kernel
+    # workload 5, one chain round through hx_score_batch with the shared-groups hint
+    # (profiles/chain_workload5.md): nodes is the settling nodes kernel, kv the link table,
+    # maxflow the list-driven kernel, shared candidate 0's groups
     5: {
-        "setup": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 181.9, "write_kib": 516.1},
-        "decode": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 20670.0, "write_kib": 112600.0},
-        "scatter": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 53820.0, "write_kib": 61410.0},
-        "eval": {"source_sha256_16": "94731d0e02a7dea0", "fetch_kib": 41490.0, "write_kib": 120100.0},
-        "nodes": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 61540.0, "write_kib": 1536.0},
-        "kv": {"source_sha256_16": "0b9a85d3a63b8eb9", "fetch_kib": 146.2, "write_kib": 68.03},
-        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 13.17, "write_kib": 0.0},
-        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 294.3, "write_kib": 8.062},
+        "setup": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 183.2, "write_kib": 516.1},
+        "shared": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 173.4, "write_kib": 2.0},
+        "decode": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 10470.0, "write_kib": 143000.0},
+        "scatter": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 48350.0, "write_kib": 7560.0},
+        "eval": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 9220.0, "write_kib": 32660.0},
+        "nodes": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 61510.0, "write_kib": 1536.0},
+        "kv": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 140.3, "write_kib": 68.03},
+        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 12.79, "write_kib": 0.0},
+        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 294.1, "write_kib": 8.062},
     },
 }
 # The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
@@ -248,8 +250,37 @@ def kernel_traffic(kernel: str, workload: int, prob=None):
     return 1024.0 * (t["fetch_kib"] * COUNTER_SCALE["fetch"] + t["write_kib"] * COUNTER_SCALE["write"])
 
 
-def group_members(prob):
-    """(members [U][size] ascending GPU ids, role [U]) of every present group, listed by size."""
+def shared_with_first(prob) -> np.ndarray:
+    """[max_groups][N] bool: group slot k of candidate n is handed candidate 0's outputs under the
+    shared-groups hint, i.e. it has a role (prefill or decode) and candidate 0's slot k - 1, k or
+    k + 1 holds the same member set with the same role (candidate 0's own groups included: the
+    hint costs them in their own kernel)."""
+    G, K, N = prob.n_gpus, prob.max_groups, prob.n_cand
+    words = (G + 63) // 64
+    m = np.zeros((words, K + 1, N), np.uint64)  # row K collects unused GPUs
+    cols = np.arange(N)
+    for g in range(G):
+        k = np.minimum(prob.assign[g].astype(np.int64), K)
+        m[g // 64, k, cols] |= np.uint64(1) << np.uint64(g % 64)
+    m = m[:, :K]
+    role = prob.role.astype(np.int64)
+    present = (m != 0).any(axis=0) & ((role == 0) | (role == 1))
+    out = np.zeros((K, N), bool)
+    for d in (-1, 0, 1):
+        for k in range(K):
+            e = k + d
+            if e < 0 or e >= K or not present[e, 0]:
+                continue
+            same = present[k] & (role[k] == role[e, 0])
+            for w in range(words):
+                same &= m[w, k] == m[w, e, 0]
+            out[k] |= same
+    return out
+
+
+def group_members(prob, exclude=None):
+    """(members [U][size] ascending GPU ids, role [U]) of every present group, listed by size;
+    exclude ([max_groups][N] bool): slots to leave out."""
     G, K, N = prob.n_gpus, prob.max_groups, prob.n_cand
     g, n = np.nonzero(prob.assign < K)
     k = prob.assign[g, n].astype(np.int64)
@@ -260,6 +291,8 @@ def group_members(prob):
     sizes = np.diff(np.concatenate([starts, [len(key)]]))
     role = prob.role[k[starts], n[starts]]
     keep = (role == 0) | (role == 1)
+    if exclude is not None:
+        keep &= ~exclude[k[starts], n[starts]]
     out = {}
     for sz in np.unique(sizes[keep]):
         sel = starts[keep & (sizes == sz)]
@@ -272,7 +305,7 @@ def eval_fp64_ops(prob) -> float:
     return eval_fp64_counts(prob)[0]
 
 
-def eval_fp64_counts(prob):
+def eval_fp64_counts(prob, exclude=None):
     """Algorithmic FP64 operations of the strategy-evaluation kernel (Table 1 rows as written,
     each add, multiply, divide, min or max one operation; prefill link terms, which do not
     depend on the candidate, count one add each).  The kernel costs the groups that the decode
@@ -281,8 +314,9 @@ def eval_fp64_counts(prob):
     split).  For a costed group every admissible strategy costs its memory row, and a strategy
     whose memory row admits a batch of 1 costs the full latency sum.  With request classes a
     strategy is costed class by class until a class does not fit, and each costed class adds 4
-    operations to the mix.  Returns (operations, divisions among them): a binary64 division is
-    about ten VALU instructions on gfx9, so it is reported apart."""
+    operations to the mix.  Under the shared-groups hint the groups handed candidate 0's outputs
+    are not the kernel's (exclude, from shared_with_first).  Returns (operations, divisions among
+    them): a binary64 division is about ten VALU instructions on gfx9, so it is reported apart."""
     m = prob.model
     L = m["n_layers"]
     H = float(m["hidden"])
@@ -300,7 +334,7 @@ def eval_fp64_counts(prob):
     wild = np.isnan(gmem)
     tps = [t for t in range(1, 9) if (prob.tp_mask >> (t - 1)) & 1]
     total = divs = 0.0
-    for sz, (mem, role) in group_members(prob).items():
+    for sz, (mem, role) in group_members(prob, exclude).items():
         dec = role == 1
         strats = [(tp, sz // tp) for tp in tps if sz % tp == 0 and sz // tp <= 8
                   and (prob.pp_mask >> (sz // tp - 1)) & 1 and sz // tp <= L]
@@ -346,12 +380,13 @@ def eval_fp64_counts(prob):
     return float(total), float(divs)
 
 
-def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload, kbytes=None):
+def roofline_for(dominant, kernel_us, prob, hbm, n_p, n_d, workload, kbytes=None, exclude=None):
     """Roofline object of one kernel: FP64 ALU for the strategy evaluation, LDS for the
-    max-flow, HBM for the streaming kernels."""
+    max-flow, HBM for the streaming kernels.  exclude: the slots the shared-groups hint takes
+    out of the evaluation kernel."""
     t_dom = kernel_us[dominant] * 1e-6
     if dominant == "eval":
-        ops, divs = eval_fp64_counts(prob)
+        ops, divs = eval_fp64_counts(prob, exclude)
         achieved = ops / t_dom / 1e9
         # the same work weighted by issue cost: a division as ten operations
         weighted = (ops + 9.0 * divs) / t_dom / 1e9
@@ -441,7 +476,8 @@ def refine_main(args, torch, hx, I):
         # a round launches each scoring kernel twice, on the parent (one candidate) and on the
         # children; the roofline charges the children's work with both launches' time
         kb = kernel_bytes(cp, n_p, n_d, settled_per_gpu=cp.n_gpus <= 128)
-        roof = roofline_for(dominant, {dominant: 1000.0 * kernel_ms_per_round[dominant]}, cp, hbm, n_p, n_d, cfg, kb)
+        roof = roofline_for(dominant, {dominant: 1000.0 * kernel_ms_per_round[dominant]}, cp, hbm, n_p, n_d, cfg, kb,
+                            exclude=shared_with_first(cp) if hint else None)
     else:
         alg = float(hbm.get(dominant, 0))
         t = kernel_ms_per_round[dominant] * 1e-3
@@ -687,7 +723,8 @@ def chain_main(args, torch, hx, I):
     hbm = hbm_bytes_per_step(last, ws.net.dims, n_p, n_d)
     kb = kernel_bytes(last, n_p, n_d, settled_per_gpu=last.granularity == 1 and last.n_gpus <= 128)
     dominant = max(kernel_us, key=kernel_us.get)
-    roof = roofline_for(dominant, kernel_us, last, hbm, n_p, n_d, cfg, kb)
+    roof = roofline_for(dominant, kernel_us, last, hbm, n_p, n_d, cfg, kb,
+                        exclude=None if args.no_shared_groups_hint else shared_with_first(last))
     out = {
         "metric": METRIC,
         "value": value,
