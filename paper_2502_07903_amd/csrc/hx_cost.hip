@@ -750,14 +750,22 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // Per-group LDS: member ids [G], row values tsum/pmin [G] (one per (stage, device)), stage
-// computation terms comp [HX_MAX_PP].
+// computation terms comp [max_stages(pp_mask)].
 struct CoopLds {
     uint8_t* mem;
     double *tsum, *pmin, *comp;
 };
 
-__host__ __device__ inline size_t coop_group_bytes(int G) {
-    return ((size_t)G + 7) / 8 * 8 + sizeof(double) * (2 * (size_t)G + HX_MAX_PP);
+// The most pipeline stages a strategy can have: the highest PP of the mask.
+__host__ __device__ inline int max_stages(uint32_t pp_mask) {
+    int m = 0;
+    for (int b = 0; b < 32; ++b)
+        if ((pp_mask >> b) & 1u) m = b + 1;
+    return m;
+}
+
+__host__ __device__ inline size_t coop_group_bytes(int G, int stages) {
+    return ((size_t)G + 7) / 8 * 8 + sizeof(double) * (2 * (size_t)G + stages);
 }
 
 __device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
@@ -1004,7 +1012,7 @@ __global__ void __launch_bounds__(64) ref_kernel(Problem p, CostWork wk) {
     Problem p1 = p;
     p1.N = 1;  // the table holds one candidate
     unsigned char* cbase = a0 + (((size_t)G + 7) & ~(size_t)7);
-    const CoopLds c = carve_coop(cbase + grp * coop_group_bytes(G), G);
+    const CoopLds c = carve_coop(cbase + grp * coop_group_bytes(G, max_stages(p.pp_mask)), G);
     coop_unit<W, kVar, kCL>(p1, tb, wk.ref.out, c, adm_tab, gl, live, 0, k, role, m);
     if (k < p.Kmax && gl == 0) {
 #pragma unroll
@@ -1015,9 +1023,15 @@ __global__ void __launch_bounds__(64) ref_kernel(Problem p, CostWork wk) {
 
 // LDS of ref_kernel beyond its static arrays: the per-GPU tables, candidate 0's assign column
 // and the slots' coop_unit areas.
-__host__ inline size_t ref_lds_bytes(int G) {
+__host__ inline size_t ref_lds_bytes(int G, int stages) {
     return sizeof(double) * 3 * (size_t)G + (((size_t)G + 7) & ~(size_t)7) +
-           (size_t)(64 / kCoopLanes) * coop_group_bytes(G);
+           (size_t)(64 / kCoopLanes) * coop_group_bytes(G, stages);
+}
+
+// LDS of one eval wavefront: its cooperative groups' rows (kCL lanes a group), or, without the
+// cooperative path, its lanes' member columns; the columns (64 G bytes) fit in the rows.
+__host__ __device__ inline size_t eval_wave_bytes(int G, bool coop, int kCL, int stages) {
+    return coop ? (size_t)(64 / kCL) * coop_group_bytes(G, stages) : (size_t)G * 64;
 }
 
 template <int W, bool kTables, int kEvalBlock, int kVar, int kCMin, int kCL>
@@ -1064,14 +1078,18 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     __syncthreads();
     const int64_t total = counts[0];
     const int64_t N = p.N;
-    uint8_t* mem = reinterpret_cast<uint8_t*>(tb_end) + threadIdx.x;  // [G][kEvalBlock] member list
     const int64_t first_small = counts[1];
-    if (W == 1 && G >= kCMin) {
-        unsigned char* cbase = reinterpret_cast<unsigned char*>(tb_end) + (size_t)G * kEvalBlock;
-        const int lane = threadIdx.x & 63, grp = lane / kCL, gl = lane % kCL;
-        const int wave = threadIdx.x >> 6;
+    // Each wavefront's LDS area: its cooperative groups' rows, which its lanes' member columns
+    // ([G][64], one-lane path) reuse once its cooperative items are done.
+    const bool coop = W == 1 && G >= kCMin;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int stages = max_stages(p.pp_mask);
+    unsigned char* warea = reinterpret_cast<unsigned char*>(tb_end) + wave * eval_wave_bytes(G, coop, kCL, stages);
+    uint8_t* mem = warea + lane;
+    if (coop) {
+        const int grp = lane / kCL, gl = lane % kCL;
         constexpr int kGroupsPerWave = 64 / kCL;
-        const CoopLds c = carve_coop(cbase + (wave * kGroupsPerWave + grp) * coop_group_bytes(G), G);
+        const CoopLds c = carve_coop(warea + grp * coop_group_bytes(G, stages), G);
         const int64_t waves = (int64_t)gridDim.x * (kEvalBlock / 64);
         for (int64_t base = ((int64_t)blockIdx.x * (kEvalBlock / 64) + wave) * kGroupsPerWave; base < first_small;
              base += waves * kGroupsPerWave) {
@@ -1090,6 +1108,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
             }
             coop_unit<W, kVar, kCL>(p, tb, o, c, adm_tab, gl, live, n, k, role, mask);
         }
+        wave_sync();  // the wavefront's member columns overwrite its cooperative rows
     }
     for (int64_t u = first_small + (int64_t)blockIdx.x * kEvalBlock + threadIdx.x; u < total;
          u += (int64_t)gridDim.x * kEvalBlock) {
@@ -1101,11 +1120,11 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
         for (int i = 0; i < W; ++i) {
             uint64_t m = rec[1 + i];
             while (m) {
-                mem[(cnt++) * kEvalBlock] = (uint8_t)(i * 64 + __builtin_ctzll(m));
+                mem[(cnt++) * 64] = (uint8_t)(i * 64 + __builtin_ctzll(m));
                 m &= m - 1;
             }
         }
-        const GroupCost gc = cost_group<kVar>(p, tb, mem, kEvalBlock, adm_tab[cnt], cnt, role);
+        const GroupCost gc = cost_group<kVar>(p, tb, mem, 64, adm_tab[cnt], cnt, role);
         const int64_t o_ = (int64_t)k * N + n;
         o.tp[o_] = (uint8_t)gc.tp;
         o.pp[o_] = (uint8_t)gc.pp;
@@ -1117,7 +1136,9 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
 
 template <int W, int kVar, int kCMin, int kCL>
 void launch_eval_coop(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
-                      size_t lds, hipStream_t s) {
+                      hipStream_t s) {
+    const size_t lds = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) +
+                       (size_t)(eb / 64) * eval_wave_bytes(p.G, W == 1 && p.G >= kCMin, kCL, max_stages(p.pp_mask));
     if (eb == 256) {
         if (tables)
             hipLaunchKernelGGL((eval_kernel<W, true, 256, kVar, kCMin, kCL>), dim3(blocks), dim3(256), lds, s, p, o, wk,
@@ -1140,11 +1161,11 @@ __host__ inline bool small_batch(const Problem& p) {
 
 template <int W, int kVar>
 void launch_eval(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
-                 size_t lds, hipStream_t s) {
+                 hipStream_t s) {
     if (W == 1 && small_batch(p))
-        launch_eval_coop<W, kVar, kCoopMinSmall, kCoopLanesSmall>(p, o, wk, nb, tables, eb, blocks, lds, s);
+        launch_eval_coop<W, kVar, kCoopMinSmall, kCoopLanesSmall>(p, o, wk, nb, tables, eb, blocks, s);
     else
-        launch_eval_coop<W, kVar, kCoopMin, kCoopLanes>(p, o, wk, nb, tables, eb, blocks, lds, s);
+        launch_eval_coop<W, kVar, kCoopMin, kCoopLanes>(p, o, wk, nb, tables, eb, blocks, s);
 }
 
 // Units a candidate can contribute: one per group, at most min(Kmax, G).
@@ -1172,7 +1193,7 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     const size_t lds_dec = ((sizeof(int32_t) * nb + 15) & ~(size_t)15) + sizeof(uint64_t) * (p.G + 2) * W +
                            sizeof(uint64_t) * decode_slots<W>() * W * bs + (use_ref ? ref_bytes(p.Kmax) : 0);
     if (use_ref) {
-        const size_t lds_ref = ref_lds_bytes(p.G);
+        const size_t lds_ref = ref_lds_bytes(p.G, max_stages(p.pp_mask));
         const dim3 gref((p.Kmax + 64 / kCoopLanes - 1) / (64 / kCoopLanes));
         prof_mark(kKShared, false, s);
         switch ((p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) | (p.n_cls > 0 ? kVarClasses : 0)) {
@@ -1212,23 +1233,19 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const CostWork& wk, hipS
     // G bytes per lane, so beyond 128 GPUs the workgroup halves to stay within 64 KB of LDS.
     const int64_t units = max_units(p.G, p.Kmax, p.N);
     const int eb = p.G <= 128 ? 256 : 128;
-    const size_t lds_eval = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) +
-                            (size_t)p.G * eb +
-                            (W == 1 ? (size_t)(eb / (small_batch(p) ? kCoopLanesSmall : kCoopLanes)) * coop_group_bytes(p.G)
-                                    : 0);
     const int64_t want = (units + eb - 1) / eb;
     const int blocks = (int)(want < 2048 ? want : 2048);
     prof_mark(kKEval, false, s);
     switch ((p.variant & (HX_VARIANT_PIPELINED | HX_VARIANT_ASYM)) | (p.n_cls > 0 ? kVarClasses : 0)) {
-        case 0: launch_eval<W, 0>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
-        case kVarClasses: launch_eval<W, kVarClasses>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case 0: launch_eval<W, 0>(p, o, wk, nb, tables, eb, blocks, s); break;
+        case kVarClasses: launch_eval<W, kVarClasses>(p, o, wk, nb, tables, eb, blocks, s); break;
         case kVarClasses | HX_VARIANT_PIPELINED:
-            launch_eval<W, kVarClasses | HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+            launch_eval<W, kVarClasses | HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, s);
             break;
-        case HX_VARIANT_PIPELINED: launch_eval<W, HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
-        case HX_VARIANT_ASYM: launch_eval<W, HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, lds_eval, s); break;
+        case HX_VARIANT_PIPELINED: launch_eval<W, HX_VARIANT_PIPELINED>(p, o, wk, nb, tables, eb, blocks, s); break;
+        case HX_VARIANT_ASYM: launch_eval<W, HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, s); break;
         default:
-            launch_eval<W, HX_VARIANT_PIPELINED | HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, lds_eval, s);
+            launch_eval<W, HX_VARIANT_PIPELINED | HX_VARIANT_ASYM>(p, o, wk, nb, tables, eb, blocks, s);
             break;
     }
     prof_mark(kKEval, true, s);
