@@ -119,10 +119,10 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
     f.n_d[n] = nd;
 }
 
-// Per-GPU nodes with every group's role, capacity, size and a running member count staged in
-// LDS ([Kmax][64] per field, loads of eight slots issued together), then the GPUs taken in
-// ascending id with their group ids loaded eight at a time: the k-th member of a group met so far
-// is its rank.  The same rows as nodes_kernel's per-GPU branch with ~(Kmax + G)/8 memory round
+// Per-GPU nodes with every group's role, capacity share floor(C/sz) and remainder C mod sz, and
+// a running member count staged in LDS ([Kmax][64] per field, loads of eight slots issued
+// together; one division per group, not per GPU), then the GPUs taken in ascending id with their
+// group ids loaded eight at a time: the k-th member of a group met so far is its rank.  The same rows as nodes_kernel's per-GPU branch with ~(Kmax + G)/8 memory round
 // trips per lane instead of two per GPU.  Kmax <= kNodesGpuMaxK (the staging fits 64 KB).
 constexpr int kNodesGpuMaxK = 128;
 __host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax * 64 * 7; }
@@ -145,10 +145,10 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int lane = threadIdx.x;
     const int Kmax = p.Kmax;
-    int32_t* gcap = reinterpret_cast<int32_t*>(sm);        // [Kmax][64]
+    int32_t* gquo = reinterpret_cast<int32_t*>(sm);        // [Kmax][64] floor(C / sz)
     uint8_t* grole = sm + sizeof(int32_t) * (size_t)Kmax * 64;  // [Kmax][64]
-    uint8_t* gsize = grole + (size_t)Kmax * 64;              // [Kmax][64]
-    uint8_t* gseen = gsize + (size_t)Kmax * 64;              // [Kmax][64]: members met so far
+    uint8_t* grem = grole + (size_t)Kmax * 64;               // [Kmax][64] C mod sz (< sz <= 255)
+    uint8_t* gseen = grem + (size_t)Kmax * 64;               // [Kmax][64]: members met so far
     const int64_t N = p.N;
     const int64_t n = (int64_t)blockIdx.x * 64 + lane;
     if (n >= N) return;  // no barrier below: every lane stages and reads its own column
@@ -176,9 +176,11 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
         for (int x = 0; x < kC; ++x) {
             const int k = k0 + x;
             if (k >= Kmax) break;
-            gcap[k * 64 + lane] = cp[x];
+            // a slot with no member is never looked up (no GPU names it)
+            const int d = sz[x] > 0 ? sz[x] : 1;
+            gquo[k * 64 + lane] = cp[x] / d;
+            grem[k * 64 + lane] = (uint8_t)(cp[x] % d);
             grole[k * 64 + lane] = (uint8_t)rl[x];
-            gsize[k * 64 + lane] = (uint8_t)sz[x];
             gseen[k * 64 + lane] = 0;
         }
     }
@@ -218,9 +220,7 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
                 if (r != HX_PREFILL && r != HX_DECODE) continue;
                 const int rk = gseen[k * 64 + lane];
                 gseen[k * 64 + lane] = (uint8_t)(rk + 1);
-                const int sz = gsize[k * 64 + lane];
-                const int32_t C = gcap[k * 64 + lane];
-                const int32_t share = C / sz + (rk < C % sz ? 1 : 0);
+                const int32_t share = gquo[k * 64 + lane] + (rk < grem[k * 64 + lane] ? 1 : 0);
                 if (r == HX_PREFILL) {
                     if (rows) {
                         const int64_t e = (int64_t)np * N + n;
