@@ -1003,7 +1003,6 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int tid = threadIdx.x;
     const int stride = blockDim.x;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tid;
     const int64_t N = p.N;
     // asymmetric split: every GPU's FLOP/s staged once per workgroup (the walk's layer ranges
     // read them at every stage it enters)
@@ -1012,9 +1011,10 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
         for (int g = tid; g < p.G; g += blockDim.x) gfl[g] = gpu_flops(p, g);
         __syncthreads();
     }
-    if (gid >= (int64_t)f.max_pd * N) return;
-    const int e = (int)(gid / N);
-    const int n = (int)(gid - (int64_t)e * N);
+    // KV row e = blockIdx.y (a grid row per row, so no lane divides by N), candidates along x
+    const int e = (int)blockIdx.y;
+    const int n = (int)blockIdx.x * kKvBlock + tid;
+    if (n >= N) return;
     const int np = f.n_p[n], nd = f.n_d[n];
     if (e >= np * nd) return;
     const int i = e / nd, j = e - i * nd;
@@ -1201,6 +1201,11 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     prof_mark(kKNodes, true, s);
     const int64_t lanes = (int64_t)f.max_pd * p.N;
     const int blocks = (int)((lanes + kKvBlock - 1) / kKvBlock);
+    // kv_kernel: a grid row per KV row a replica network can have (its n_p + n_d <= Kmax nodes
+    // give at most floor(Kmax/2) ceil(Kmax/2) <= 16,256 rows, within the grid's y limit)
+    const int64_t rows_pd = (int64_t)(p.Kmax / 2) * ((p.Kmax + 1) / 2);
+    const dim3 grid_kv((unsigned)((p.N + kKvBlock - 1) / kKvBlock),
+                       (unsigned)(f.max_pd < rows_pd ? f.max_pd : rows_pd));
     const size_t lds = 2 * (size_t)p.G * kKvBlock;
     prof_mark(kKKv, false, s);
     if (p.granularity != 0) {
@@ -1214,12 +1219,12 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kOrderThreads), kOrderLds + lds, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
-        hipLaunchKernelGGL((kv_kernel<W, true, false>), dim3(blocks), dim3(kKvBlock), lds + sizeof(double) * p.G, s,
-                           p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, true, false>), grid_kv, dim3(kKvBlock), lds + sizeof(double) * p.G, s, p,
+                           o, f);
     } else if (p.n_cls > 0) {
-        hipLaunchKernelGGL((kv_kernel<W, false, true>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, false, true>), grid_kv, dim3(kKvBlock), lds, s, p, o, f);
     } else {
-        hipLaunchKernelGGL((kv_kernel<W, false, false>), dim3(blocks), dim3(kKvBlock), lds, s, p, o, f);
+        hipLaunchKernelGGL((kv_kernel<W, false, false>), grid_kv, dim3(kKvBlock), lds, s, p, o, f);
     }
     prof_mark(kKKv, true, s);
     return hipGetLastError();
