@@ -308,8 +308,8 @@ int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, 
  * capacities): hx_cost_eval, hx_build_flownet, hx_maxflow_batch with kv_flow and cut null, and
  * hx_best_candidate, enqueued by one call with the same arguments and errors, a workspace of
  * hx_score_workspace_bytes (the cost model's scratch, then a table of link capacities and a list
- * of candidates, then the argmax's per-workgroup winners, 256-byte aligned, contents ignored on
- * entry), and the same results: every cost
+ * of candidates, then the argmax's partial winners (one per workgroup, or one per slot that the max-flow
+ * kernel's workgroups fold into), 256-byte aligned, contents ignored on entry), and the same results: every cost
  * output, the network's node counts (n_p, n_d), flow_value and best, bit for bit.  At
  * granularity 0, and beyond 128 GPUs or 128 group slots, every row of the network is written as
  * by hx_build_flownet.  At granularity 1 on clusters of up to 128 GPUs a KV edge's capacity

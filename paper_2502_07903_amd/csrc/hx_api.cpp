@@ -409,9 +409,17 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
     if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
     const hx::Problem p = make_problem(cluster, model, wl, space, cand);
     const hx::FlowNet f = make_net(net);
-    hipError_t e = hx::launch_cost(p, make_cost(cost), workspace, stream);
+    // the argmax's area follows the link table: per-workgroup winners for the per-GPU path, the
+    // fused argmax's slots (zeroed by the cost model's first kernel) otherwise
+    const size_t off_part = ((hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
+                             ~(size_t)255) +
+                            ((hx::link_table_bytes(cluster->n_gpus, cand->n_cand) + 255) & ~(size_t)255);
+    unsigned char* part = static_cast<unsigned char*>(workspace) + off_part;
+    const bool direct = hx::flownet_values_direct(p) && hx::maxflow_workgroup_plan(net->max_p, net->max_d, net->max_pd);
+    unsigned long long* slots = direct ? nullptr : reinterpret_cast<unsigned long long*>(part);
+    hipError_t e = hx::launch_cost(p, make_cost(cost), workspace, stream, slots, direct ? 0 : hx::kArgSlots);
     if (e == hipSuccess) {
-        if (hx::flownet_values_direct(p) && hx::maxflow_workgroup_plan(net->max_p, net->max_d, net->max_pd)) {
+        if (direct) {
             // the link table follows the cost model's scratch, 256-byte aligned
             const size_t off = (hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
                                ~(size_t)255;
@@ -421,18 +429,19 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
             if (e == hipSuccess) e = hx::launch_maxflow_listed(f, flow_value, round_budget(), count + 16, count, stream);
         } else {
             e = hx::launch_flownet(p, make_cost(cost), f, stream);
-            if (e == hipSuccess) e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream);
+            if (e == hipSuccess)
+                e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream, slots);
         }
     }
     if (e == hipSuccess) {
-        // the argmax's workgroup winners follow the link table; its counter is the cost
-        // workspace's word that the cost model's first kernel cleared
-        const size_t off = ((hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
-                            ~(size_t)255) +
-                           ((hx::link_table_bytes(cluster->n_gpus, cand->n_cand) + 255) & ~(size_t)255);
-        uint64_t* part = reinterpret_cast<uint64_t*>(static_cast<unsigned char*>(workspace) + off);
-        e = hx::launch_best_parts(flow_value, cand->n_cand, best, hx::cost_workspace_counter(workspace, cluster->n_gpus),
-                                  part, stream);
+        // per-GPU path: the argmax's counter is the cost workspace's word that the cost model's
+        // first kernel cleared
+        if (direct)
+            e = hx::launch_best_parts(flow_value, cand->n_cand, best,
+                                      hx::cost_workspace_counter(workspace, cluster->n_gpus),
+                                      reinterpret_cast<uint64_t*>(part), stream);
+        else
+            e = hx::launch_best_final(slots, best, stream);
     }
     return e == hipSuccess ? HX_OK : hip_error(e);
 }

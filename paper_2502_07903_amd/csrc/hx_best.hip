@@ -149,7 +149,40 @@ __global__ void __launch_bounds__(kPartBlock) best_parts_kernel(const int32_t* _
     }
 }
 
+// The fused argmax's last step: kFinalLanes lanes, each over every kFinalLanes-th slot, the
+// largest key (argmax_key order) decoded to {index, value}.
+constexpr int kFinalLanes = 1024;
+static_assert(kArgSlots % kFinalLanes == 0, "whole slot rows per lane");
+__global__ void __launch_bounds__(kFinalLanes) best_final_kernel(const unsigned long long* __restrict__ slots,
+                                                                 int32_t* best) {
+    __shared__ unsigned long long wk[kFinalLanes / 64];
+    unsigned long long key = 0;
+#pragma unroll
+    for (int i = 0; i < kArgSlots / kFinalLanes; ++i) {
+        const unsigned long long v = slots[i * kFinalLanes + threadIdx.x];
+        key = v > key ? v : key;
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        const unsigned long long o = __shfl_xor(key, off, 64);
+        key = o > key ? o : key;
+    }
+    if ((threadIdx.x & 63) == 0) wk[threadIdx.x >> 6] = key;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kFinalLanes / 64; ++w) key = wk[w] > key ? wk[w] : key;
+        best[0] = (int32_t)(0xFFFFFFFFu - (uint32_t)key);
+        best[1] = (int32_t)((uint32_t)(key >> 32) ^ 0x80000000u);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_best_final(const unsigned long long* slots, int32_t* best, hipStream_t s) {
+    prof_mark(kKBest, false, s);
+    hipLaunchKernelGGL(best_final_kernel, dim3(1), dim3(kFinalLanes), 0, s, slots, best);
+    prof_mark(kKBest, true, s);
+    return hipGetLastError();
+}
 
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s) {
     prof_mark(kKBest, false, s);
@@ -158,7 +191,7 @@ hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipS
     return hipGetLastError();
 }
 
-size_t best_parts_bytes() { return sizeof(uint64_t) * kPartMax; }
+size_t best_parts_bytes() { return sizeof(uint64_t) * (kPartMax > kArgSlots ? kPartMax : kArgSlots); }
 
 hipError_t launch_best_parts(const int32_t* flow_value, int32_t n, int32_t* best, int32_t* counter, uint64_t* part,
                              hipStream_t s) {

@@ -374,6 +374,8 @@ struct CostWork {
                       // ((HX_MAX_TP + 1) G^2 doubles each)
     unsigned char* ref_base;  // candidate 0's table (RefTable), ref_bytes(Kmax)
     RefTable ref;
+    unsigned long long* clear2;  // [n_clear2] more words the first kernel zeroes (or null)
+    int n_clear2;
 };
 
 // The memory-row screen, a W-word GPU bitmask per group size c = 0..G, then wild (entry G + 1).
@@ -448,6 +450,7 @@ __global__ void setup_kernel(Problem p, CostWork wk, int n_clear, int W) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_clear; i += nth) wk.hist[i] = 0;
+    for (int64_t i = tid; i < wk.n_clear2; i += nth) wk.clear2[i] = 0;
     unfit_table(p, wk.unfit, W, tid, nth);
     const int G = p.G;
     const int64_t gg = (int64_t)G * G;
@@ -1288,7 +1291,8 @@ int32_t* cost_workspace_counter(void* workspace, int32_t n_gpus) {
     return reinterpret_cast<int32_t*>(workspace) + 4 * ((size_t)n_gpus + 1) + 1;
 }
 
-hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s) {
+hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s, unsigned long long* clear,
+                       int n_clear) {
     const size_t nb = 2 * ((size_t)p.G + 1);
     const size_t head = ((2 * nb + 2) * sizeof(int32_t) + 255) & ~(size_t)255;
     CostWork wk;
@@ -1301,6 +1305,8 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
     wk.unfit = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(wk.tp_pre) + tables_bytes(p.G));
     wk.ukey = reinterpret_cast<uint8_t*>(wk.unfit) + unfit_bytes(p.G);
     wk.ref_base = reinterpret_cast<unsigned char*>(workspace) + ref_offset(p.G, p.Kmax, p.N);
+    wk.clear2 = clear;
+    wk.n_clear2 = clear ? n_clear : 0;
     wk.ref = carve_ref(wk.ref_base, p.Kmax);
     wk.gmask = o.members;
     switch (mask_words(p.G)) {

@@ -98,17 +98,29 @@ size_t cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand);
 // The word after the histogram and cursors of a cost workspace: zero once launch_cost's first
 // kernel has run, untouched by the cost kernels.
 int32_t* cost_workspace_counter(void* workspace, int32_t n_gpus);
-hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s);
+// clear / n_clear: more 64-bit words for the cost model's first kernel to zero (the fused
+// argmax's slots in hx_score_batch).
+hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipStream_t s,
+                       unsigned long long* clear = nullptr, int n_clear = 0);
 hipError_t launch_flownet(const Problem& p, const CostOut& o, const FlowNet& f, hipStream_t s);
 // LDS bytes the max-flow kernel needs for a network plan; 0 if it does not fit.
 size_t maxflow_lds_bytes(int32_t max_p, int32_t max_d, int32_t max_pd);
+// arg (hx_score_batch, replica networks): kArgSlots zeroed slots that the max-flow kernel folds
+// each wavefront's best candidate into (argmax_key); launch_best_final then reduces them.
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
-                          unsigned long long* stats, hipStream_t s);
+                          unsigned long long* stats, hipStream_t s, unsigned long long* arg = nullptr);
 hipError_t launch_best(const int32_t* flow_value, int32_t n, int32_t* best, hipStream_t s);
 // The same argmax over several workgroups: each writes its winner to part, and the last to
 // finish (counted in *counter, which must be zero at launch and is zero again after it) reduces
 // them.  part holds best_parts_bytes().
 size_t best_parts_bytes();
+// The fused argmax: slots of 64-bit keys, ordered as (value, then lower index) so that a larger key
+// is a better candidate; 0 is no candidate (below every value a flow or an error code takes).
+constexpr int kArgSlots = 4096;
+__host__ __device__ inline unsigned long long argmax_key(int32_t value, int32_t n) {
+    return ((unsigned long long)((uint32_t)value ^ 0x80000000u) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)n);
+}
+hipError_t launch_best_final(const unsigned long long* slots, int32_t* best, hipStream_t s);
 hipError_t launch_best_parts(const int32_t* flow_value, int32_t n, int32_t* best, int32_t* counter, uint64_t* part,
                              hipStream_t s);
 // hx_score_batch: per-GPU networks of up to 128 GPUs and 128 slots are settled from a table of

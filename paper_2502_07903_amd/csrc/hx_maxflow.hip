@@ -240,9 +240,21 @@ __global__ void __launch_bounds__(64) dom_kernel(FlowNet f, int32_t* flow_value)
 // production instantiation compiles none of it.
 // The work of one tile (64/SEG candidates of a packed plan, or one candidate of a workgroup
 // plan); every lane of the workgroup calls it with the same tile.
-template <int SEG, bool kStats>
+// kArg: fold the best of each wavefront's candidates (lane 0 of a segment holds its candidate's
+// key, argmax_key) into slot blockIdx mod kArgSlots of arg with a 64-bit atomic max; every lane of
+// the wavefront calls it.
+__device__ __forceinline__ void fold_argmax(unsigned long long key, unsigned long long* arg) {
+    for (int off = 32; off > 0; off >>= 1) {
+        const unsigned long long o = __shfl_xor(key, off, 64);
+        key = o > key ? o : key;
+    }
+    if ((threadIdx.x & 63) == 0 && key != 0) atomicMax(&arg[blockIdx.x % kArgSlots], key);
+}
+
+template <int SEG, bool kStats, bool kArg = false>
 __device__ __forceinline__ void maxflow_tile(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut,
-                                             int32_t round_budget, unsigned long long* stats, int tile) {
+                                             int32_t round_budget, unsigned long long* stats, int tile,
+                                             unsigned long long* arg = nullptr) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const int N = f.N;
@@ -255,10 +267,16 @@ __device__ __forceinline__ void maxflow_tile(const FlowNet& f, int32_t* flow_val
     bool valid = tile < tiles && n < N;
     // value-only workgroup plans: bound_kernel has already written the candidates it could
     // (one candidate per workgroup, so the exit is uniform)
-    if (SEG > 64 && kv_flow == nullptr && cut == nullptr && valid && flow_value[n] >= 0) {
-        if (kStats && l == 0) atomicAdd(&stats[HX_MF_PREPASS], 1ull);
-        return;
+    if (SEG > 64 && kv_flow == nullptr && cut == nullptr && valid) {
+        const int32_t pre = flow_value[n];
+        if (pre >= 0) {
+            if (kStats && l == 0) atomicAdd(&stats[HX_MF_PREPASS], 1ull);
+            if (kArg) fold_argmax(l == 0 ? argmax_key(pre, n) : 0ull, arg);
+            return;
+        }
     }
+    // kArg: a candidate in range that the checks below reject (HX_EINVAL) ends with valid false
+    const bool in_range = valid;
 
     // Packed segments (SEG <= 64) own at most one node row per side and SEG/4 KV rows per
     // lane, so every global load is issued at once, before the counts that say which rows
@@ -657,7 +675,9 @@ __device__ __forceinline__ void maxflow_tile(const FlowNet& f, int32_t* flow_val
         if (L.ft[j] > 0) atomicAdd(&L.misc[0], L.ft[j]);
     if (active) L.misc[1] = 1;
     __syncthreads();
-    if (valid && l == 0) flow_value[n] = cut_value >= 0 ? cut_value : (L.misc[1] ? HX_ENOCONV : L.misc[0]);
+    const int32_t value = cut_value >= 0 ? cut_value : (L.misc[1] ? HX_ENOCONV : L.misc[0]);
+    if (valid && l == 0) flow_value[n] = value;
+    if (kArg) fold_argmax(l == 0 && in_range ? argmax_key(valid ? value : HX_EINVAL, n) : 0ull, arg);
     if (valid && kv_flow)
         for (int e = l; e < P * D; e += SEG) {
             const int i = e / D, d = e - i * D;
@@ -726,15 +746,19 @@ __device__ __forceinline__ void maxflow_tile(const FlowNet& f, int32_t* flow_val
     for (int j = l; j < D; j += SEG) cut[(int64_t)(f.max_p + j) * N + n] = (uint8_t)(din[j] | (dout[j] << 1));
 }
 
-template <int SEG, bool kStats>
+// kArg (hx_score_batch): each wavefront also takes the best of its candidates' flow values
+// (highest value, lowest index) and folds it into slot blockIdx mod kArgSlots of arg, as the key
+// argmax_key, with a 64-bit atomic max; the slots must be zero at launch, and best_final_kernel
+// reduces them.
+template <int SEG, bool kStats, bool kArg = false>
 __global__ void __launch_bounds__(SEG < 64 ? kPackedLanes : SEG, SEG <= 64 ? 8 : 1)
     maxflow_kernel(FlowNet f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
-                   unsigned long long* stats) {
+                   unsigned long long* stats, unsigned long long* arg) {
     constexpr int kPer = (SEG < 64 ? kPackedLanes : SEG) / SEG;
     const int tiles = (f.N + kPer - 1) / kPer;
     const int chunk = (tiles + 7) / 8;
-    maxflow_tile<SEG, kStats>(f, flow_value, kv_flow, cut, round_budget, stats,
-                              (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3));
+    const int tile = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
+    maxflow_tile<SEG, kStats, kArg>(f, flow_value, kv_flow, cut, round_budget, stats, tile, arg);
 }
 
 // Value only, workgroup plans: the candidates listed (list[0 .. *count), written by the kernel that
@@ -767,7 +791,7 @@ __global__ void clear_stats_kernel(unsigned long long* stats) {
 
 template <int SEG>
 hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, int32_t budget,
-                      unsigned long long* stats, hipStream_t s) {
+                      unsigned long long* stats, unsigned long long* arg, hipStream_t s) {
     constexpr int kLanes = SEG < 64 ? kPackedLanes : SEG;
     constexpr int kPer = kLanes / SEG;
     const size_t lds = kPer * mf_words(f.max_p, f.max_d, f.max_pd) * sizeof(int32_t);
@@ -782,10 +806,13 @@ hipError_t launch_seg(const FlowNet& f, int32_t* fv, int32_t* kv, uint8_t* cut, 
     if (stats) {
         hipLaunchKernelGGL(clear_stats_kernel, dim3(1), dim3(64), 0, s, stats);
         hipLaunchKernelGGL((maxflow_kernel<SEG, true>), dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget,
-                           stats);
+                           stats, nullptr);
+    } else if (arg) {
+        hipLaunchKernelGGL((maxflow_kernel<SEG, false, true>), dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut,
+                           budget, nullptr, arg);
     } else {
         hipLaunchKernelGGL((maxflow_kernel<SEG, false>), dim3(blocks), dim3(kLanes), lds, s, f, fv, kv, cut, budget,
-                           nullptr);
+                           nullptr, nullptr);
     }
     prof_mark(kKMaxflow, true, s);
     return hipGetLastError();
@@ -821,14 +848,14 @@ hipError_t launch_maxflow_listed(const FlowNet& f, int32_t* flow_value, int32_t 
 }
 
 hipError_t launch_maxflow(const FlowNet& f, int32_t* flow_value, int32_t* kv_flow, uint8_t* cut, int32_t round_budget,
-                          unsigned long long* stats, hipStream_t s) {
+                          unsigned long long* stats, hipStream_t s, unsigned long long* arg) {
     switch (segment_lanes(f.max_p, f.max_d, f.max_pd)) {
-        case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, stats, s);
-        case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, stats, s);
-        case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, stats, s);
-        case 64: return launch_seg<64>(f, flow_value, kv_flow, cut, round_budget, stats, s);
-        case 128: return launch_seg<128>(f, flow_value, kv_flow, cut, round_budget, stats, s);
-        default: return launch_seg<256>(f, flow_value, kv_flow, cut, round_budget, stats, s);
+        case 8: return launch_seg<8>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
+        case 16: return launch_seg<16>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
+        case 32: return launch_seg<32>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
+        case 64: return launch_seg<64>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
+        case 128: return launch_seg<128>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
+        default: return launch_seg<256>(f, flow_value, kv_flow, cut, round_budget, stats, arg, s);
     }
 }
 
