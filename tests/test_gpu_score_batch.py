@@ -121,9 +121,11 @@ def _net_of(torch, dp, ws):
 
 @pytest.mark.parametrize("cfg,sizes", [(3, (65536, 1, 1023, 1025, 4097)), (5, (131072, 777))])
 def test_score_batch_argmax_over_workgroups(torch, cfg, sizes):
-    """The value-only call's argmax splits the batch over up to 256 workgroups and lets the last
-    one to finish reduce their winners (its counter lives in the workspace): with the workspace
-    filled with garbage before every call, and batch sizes that give one to 256 workgroups, the
+    """The value-only call's argmax: for replica networks each max-flow wavefront folds its best
+    candidate into one of the workspace's slots (zeroed by the call's first kernel) and one
+    workgroup reduces them; for per-GPU networks the batch is split over up to 256 workgroups and
+    the last one to finish reduces their winners (its counter lives in the workspace). With the
+    workspace filled with garbage before every call, and batch sizes from one candidate up, the
     best equals the single-workgroup argmax of hx_best_candidate over the same flow values, and
     the first maximum of the host copy."""
     full = I.make_problem(cfg)
@@ -145,6 +147,45 @@ def test_score_batch_argmax_over_workgroups(torch, cfg, sizes):
             hx.best_candidate(ws.flow_value, one, dp.n_cand)
             torch.cuda.synchronize()
             assert tuple(int(x) for x in one.cpu().numpy()) == got
+
+
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_score_batch_argmax_ties(torch, cfg):
+    """Ties for the best flow across slots and workgroups: the best candidate's placement copied
+    to indices spread over the batch (both ends included) must give the lowest of those indices;
+    a batch whose every flow is 0 (every group's role cleared) must give index 0."""
+    full = I.make_problem(cfg, n_cand=16384)
+    dp0 = hx.DeviceProblem.upload(full)
+    ws0 = hx.Workspace.for_problem(dp0, flows=False)
+    hx.score_batch(dp0, ws0)
+    torch.cuda.synchronize()
+    b, bv = (int(x) for x in ws0.best.cpu().numpy())
+    N = full.n_cand
+    for spots in ((N - 1, 9000, 4097, 1025), (0, N - 1), (b + 1, N - 1)):
+        spots = [x for x in spots if 0 <= x < N]
+        assign, role = full.assign.copy(), full.role.copy()
+        for x in spots:
+            assign[:, x] = full.assign[:, b]
+            role[:, x] = full.role[:, b]
+        prob = dataclasses.replace(full, assign=assign, role=role)
+        say(f"hx_score_batch argmax ties: workload {cfg}, best {b} copied to {spots}")
+        dp = hx.DeviceProblem.upload(prob)
+        ws = hx.Workspace.for_problem(dp, flows=False)
+        ws.cost.workspace.fill_(0xFF)
+        hx.score_batch(dp, ws)
+        torch.cuda.synchronize()
+        got = tuple(int(x) for x in ws.best.cpu().numpy())
+        assert got == (min(spots + [b]), bv), (spots, got)
+    role = np.full_like(full.role, 0xFF)
+    prob = dataclasses.replace(full, role=role)
+    say(f"hx_score_batch argmax: workload {cfg}, every flow 0")
+    dp = hx.DeviceProblem.upload(prob)
+    ws = hx.Workspace.for_problem(dp, flows=False)
+    ws.cost.workspace.fill_(0xA5)
+    hx.score_batch(dp, ws)
+    torch.cuda.synchronize()
+    assert not ws.flow_value.cpu().numpy().any()
+    assert tuple(int(x) for x in ws.best.cpu().numpy()) == (0, 0)
 
 
 @pytest.mark.parametrize("cfg,n,variant,classes", [(3, 4096, 0, 4), (2, None, 4, 0), (3, 8192, 1, 0), (2, 1000, 2, 0),
