@@ -218,8 +218,8 @@ size_t hx_cost_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_can
  * first call on that GPU until the process ends; the call allocates nothing.  Same arguments
  * (but the workspace), results and errors as hx_cost_eval, plus HX_ETOOBIG when the batch needs
  * more scratch than that (hx_cost_workspace_bytes(n_gpus, max_groups, n_cand) >
- * HX_STATIC_SCRATCH_BYTES; 17 bytes per group slot, n_cand * min(max_groups, n_gpus), at up to
- * 64 GPUs, so about 1.9 million slots: 65,536 candidates of 32 GPUs and 16 groups take 17.3 MB,
+ * HX_STATIC_SCRATCH_BYTES; 18 bytes per group slot, n_cand * min(max_groups, n_gpus), at up to
+ * 64 GPUs, so about 1.8 million slots: 65,536 candidates of 32 GPUs and 16 groups take 19.2 MB,
  * and 262,144 candidates of 64 GPUs and 32 groups are refused).  Every call on a GPU uses that GPU's one array: calls
  * that overlap on one GPU (two streams, two host threads) race and must be serialised by the
  * caller.  The scratch needs no clearing between calls.  The caller's device must be current. */

@@ -368,7 +368,7 @@ struct CostWork {
     uint64_t* units;  // [max units][1 + W]: (n << 16 | k << 8 | role), then the member mask words
     uint64_t* gmask;  // [Kmax][W][N] group member bitmasks (the hx_cost_out output)
     uint64_t* unfit;  // [G + 2][W] the memory-row screen: a row per group size, then wild
-    uint8_t* ukey;    // [Kmax][N] role of a group to cost, HX_UNUSED for a group decode settled
+    uint16_t* ukey;   // [Kmax][N] bucket of a group to cost (bucket_of), kNoUnit for a group decode settled
     double* tp_pre;   // [HX_MAX_TP][G][G] prefill TP terms (see Tables), class 0
     double* pp_pre;   // [G][G] prefill PP terms, class 0; class k's tables sit k table blocks on
                       // ((HX_MAX_TP + 1) G^2 doubles each)
@@ -473,8 +473,10 @@ __global__ void setup_kernel(Problem p, CostWork wk, int n_clear, int W) {
 }
 
 
-// Bucket of a present group: largest sizes first, roles interleaved.
+// Bucket of a present group: largest sizes first, roles interleaved (< 2 (G + 1) <= 512); the
+// role is the bucket's low bit.
 __device__ __forceinline__ int bucket_of(int G, int size, int role) { return (G - size) * 2 + role; }
+constexpr uint16_t kNoUnit = 0xFFFF;  // a slot with no unit to cost
 
 // Workgroup barrier that first drains the calling wave's outstanding LDS operations
 // (lgkmcnt(0); the vector-memory and export counters are left at their maxima).  The counting
@@ -629,7 +631,7 @@ __global__ void __launch_bounds__(256) decode_kernel(Problem p, CostOut o, CostW
                 o.cap[o_] = 0;
                 o.lat[o_] = 0.0;
             }
-            wk.ukey[o_] = costed && hit < 0 ? (uint8_t)rl[x] : (uint8_t)HX_UNUSED;
+            wk.ukey[o_] = costed && hit < 0 ? (uint16_t)bucket_of(p.G, size, rl[x]) : kNoUnit;
         }
     }
     }
@@ -646,10 +648,11 @@ __device__ __forceinline__ int32_t wave_sum(const int32_t* h, int hi, int lane) 
     return s;
 }
 
-// One lane per candidate: every present group becomes a unit record (candidate, slot, role,
-// member mask) in its bucket.  Each workgroup scans the bucket counts into bucket offsets
-// itself (a few hundred words from L2).  Two passes over the slots: count per bucket, reserve
-// the workgroup's range of each bucket with one atomic on the bucket's cursor, then write.
+// One lane per candidate: every group decode left to cost becomes a unit record (candidate,
+// slot, role, member mask) in its bucket.  Each workgroup scans the bucket counts into bucket
+// offsets itself (a few hundred words from L2).  Two passes over the slots: count per bucket
+// (from the slots' bucket codes alone), reserve the workgroup's range of each bucket with one
+// atomic on the bucket's cursor, then write, loading the member masks of C slots together.
 template <int W, int C>
 __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     __shared__ int32_t lcount[2 * (HX_MAX_GPUS + 1)];
@@ -679,17 +682,6 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
     const int n = blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t N = p.N;
     const int Kmax = p.Kmax;
-    // The first chunk of slots is loaded once and serves both passes (every slot, when
-    // Kmax <= C); later chunks are loaded in each pass.
-    int rl0[C];
-    uint64_t m0[C][W];
-#pragma unroll
-    for (int x = 0; x < C; ++x) {
-        const bool in = n < N && x < Kmax;
-        rl0[x] = in ? wk.ukey[(int64_t)x * N + n] : HX_UNUSED;
-#pragma unroll
-        for (int i = 0; i < W; ++i) m0[x][i] = in ? wk.gmask[((int64_t)x * W + i) * N + n] : 0;
-    }
     for (int pass = 0; pass < 2; ++pass) {
         if (pass == 1) {
             lds_drain_barrier();
@@ -701,30 +693,34 @@ __global__ void __launch_bounds__(256) scatter_kernel(Problem p, CostWork wk) {
         }
         if (n >= N) continue;
         for (int k0 = 0; k0 < Kmax; k0 += C) {
-            int rl[C];
+            // every load issued (slots past Kmax read slot Kmax - 1 and are dropped)
+            int bk[C];
+#pragma unroll
+            for (int x = 0; x < C; ++x) bk[x] = wk.ukey[(int64_t)(k0 + x < Kmax ? k0 + x : Kmax - 1) * N + n];
+#pragma unroll
+            for (int x = 0; x < C; ++x)
+                if (k0 + x >= Kmax) bk[x] = kNoUnit;
+            if (pass == 0) {
+#pragma unroll
+                for (int x = 0; x < C; ++x)
+                    if (bk[x] != kNoUnit) atomicAdd(&lcount[bk[x]], 1);
+                continue;
+            }
             uint64_t m[C][W];
 #pragma unroll
-            for (int x = 0; x < C; ++x) {
-                const bool in = k0 + x < Kmax;
-                rl[x] = k0 == 0 ? rl0[x] : (in ? wk.ukey[(int64_t)(k0 + x) * N + n] : HX_UNUSED);
+            for (int x = 0; x < C; ++x)
 #pragma unroll
                 for (int i = 0; i < W; ++i)
-                    m[x][i] = k0 == 0 ? m0[x][i] : (in ? wk.gmask[((int64_t)(k0 + x) * W + i) * N + n] : 0);
-            }
+                    m[x][i] = wk.gmask[((int64_t)(k0 + x < Kmax ? k0 + x : Kmax - 1) * W + i) * N + n];
 #pragma unroll
             for (int x = 0; x < C; ++x) {
-                int size = 0;
-#pragma unroll
-                for (int i = 0; i < W; ++i) size += __popcll(m[x][i]);
-                if (size == 0 || (rl[x] != HX_PREFILL && rl[x] != HX_DECODE)) continue;
-                const int b = bucket_of(p.G, size, rl[x]);
+                if (bk[x] == kNoUnit) continue;
+                const int b = bk[x];
                 const int rank = atomicAdd(&lcount[b], 1);
-                if (pass == 1) {
-                    uint64_t* rec = wk.units + (int64_t)(lbase[b] + rank) * (1 + W);
-                    rec[0] = ((uint64_t)n << 16) | ((uint64_t)(k0 + x) << 8) | (uint64_t)rl[x];
+                uint64_t* rec = wk.units + (int64_t)(lbase[b] + rank) * (1 + W);
+                rec[0] = ((uint64_t)n << 16) | ((uint64_t)(k0 + x) << 8) | (uint64_t)(b & 1);
 #pragma unroll
-                    for (int i = 0; i < W; ++i) rec[1 + i] = m[x][i];
-                }
+                for (int i = 0; i < W; ++i) rec[1 + i] = m[x][i];
             }
         }
     }
@@ -1279,7 +1275,7 @@ static size_t ref_offset(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t nb = 2 * ((size_t)n_gpus + 1);
     const size_t head = ((2 * nb + 2) * sizeof(int32_t) + 255) & ~(size_t)255;
     const size_t end = head + units_bytes(n_gpus, max_groups, n_cand) + tables_bytes(n_gpus) + unfit_bytes(n_gpus) +
-                       (size_t)max_groups * n_cand;
+                       sizeof(uint16_t) * (size_t)max_groups * n_cand;
     return (end + 255) & ~(size_t)255;
 }
 
@@ -1303,7 +1299,7 @@ hipError_t launch_cost(const Problem& p, const CostOut& o, void* workspace, hipS
                                           units_bytes(p.G, p.Kmax, p.N));
     wk.pp_pre = wk.tp_pre + (size_t)HX_MAX_TP * p.G * p.G;
     wk.unfit = reinterpret_cast<uint64_t*>(reinterpret_cast<unsigned char*>(wk.tp_pre) + tables_bytes(p.G));
-    wk.ukey = reinterpret_cast<uint8_t*>(wk.unfit) + unfit_bytes(p.G);
+    wk.ukey = reinterpret_cast<uint16_t*>(reinterpret_cast<unsigned char*>(wk.unfit) + unfit_bytes(p.G));
     wk.ref_base = reinterpret_cast<unsigned char*>(workspace) + ref_offset(p.G, p.Kmax, p.N);
     wk.clear2 = clear;
     wk.n_clear2 = clear ? n_clear : 0;
