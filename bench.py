@@ -51,30 +51,31 @@ FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
-    # workload 3 (profiles/all_kernels_workload3.md); best is hx_score_batch's split argmax
+    # workload 3 (profiles/all_kernels_workload3.md); maxflow is the instantiation with the folded
+    # argmax, best the final reduction of its slots
     3: {
-        "setup": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 69.5, "write_kib": 32.81},
-        "decode": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 1718.0, "write_kib": 27820.0},
-        "scatter": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 4935.0, "write_kib": 1487.0},
-        "eval": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 1154.0, "write_kib": 12140.0},
-        "nodes": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 6697.0, "write_kib": 18230.0},
-        "kv": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 5883.0, "write_kib": 13400.0},
-        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 16740.0, "write_kib": 256.0},
-        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 165.8, "write_kib": 4.062},
+        "setup": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 70.54, "write_kib": 57.43},
+        "decode": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 1702.0, "write_kib": 28840.0},
+        "scatter": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 5419.0, "write_kib": 1478.0},
+        "eval": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 1224.0, "write_kib": 14620.0},
+        "nodes": {"source_sha256_16": "b2723c48341ccf52", "fetch_kib": 6691.0, "write_kib": 15750.0},
+        "kv": {"source_sha256_16": "b2723c48341ccf52", "fetch_kib": 5878.0, "write_kib": 13400.0},
+        "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 16740.0, "write_kib": 768.0},
+        "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 18.1, "write_kib": 0.03125},
     },
     # workload 5, one chain round through hx_score_batch with the shared-groups hint
     # (profiles/chain_workload5.md): nodes is the settling nodes kernel, kv the link table,
-    # maxflow the list-driven kernel, shared candidate 0's groups
+    # maxflow the list-driven kernel, shared candidate 0's groups, best the split argmax
     5: {
-        "setup": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 183.2, "write_kib": 516.1},
-        "shared": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 173.4, "write_kib": 2.0},
-        "decode": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 10470.0, "write_kib": 143000.0},
-        "scatter": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 48350.0, "write_kib": 7560.0},
-        "eval": {"source_sha256_16": "6d3af7f8a2740805", "fetch_kib": 9220.0, "write_kib": 32660.0},
-        "nodes": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 61510.0, "write_kib": 1536.0},
-        "kv": {"source_sha256_16": "644ae5019406f538", "fetch_kib": 140.3, "write_kib": 68.03},
-        "maxflow": {"source_sha256_16": "aa02138c6b5505da", "fetch_kib": 12.79, "write_kib": 0.0},
-        "best": {"source_sha256_16": "1fa0dd0b24f74de3", "fetch_kib": 294.1, "write_kib": 8.062},
+        "setup": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 184.2, "write_kib": 516.1},
+        "shared": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 175.4, "write_kib": 2.0},
+        "decode": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 10470.0, "write_kib": 147100.0},
+        "scatter": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 39670.0, "write_kib": 7566.0},
+        "eval": {"source_sha256_16": "7d06bb1c1ceaa1ed", "fetch_kib": 9335.0, "write_kib": 32670.0},
+        "nodes": {"source_sha256_16": "b2723c48341ccf52", "fetch_kib": 61510.0, "write_kib": 1536.0},
+        "kv": {"source_sha256_16": "b2723c48341ccf52", "fetch_kib": 145.8, "write_kib": 68.03},
+        "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 10.64, "write_kib": 0.0},
+        "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 297.2, "write_kib": 8.062},
     },
 }
 # The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
