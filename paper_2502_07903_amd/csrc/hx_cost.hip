@@ -748,11 +748,12 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Per-group LDS: member ids [G], row values tsum/pmin [G] (one per (stage, device)), stage
-// computation terms comp [max_stages(pp_mask)].
+// Per-group LDS: member ids [G], row values tsum/pmin [G] (one per (stage, device)), per stage
+// [max_stages(pp_mask)] the computation term (then the stage's whole time) and the PP link time
+// into the next stage.
 struct CoopLds {
     uint8_t* mem;
-    double *tsum, *pmin, *comp;
+    double *tsum, *pmin, *comp, *ppt;
 };
 
 // The most pipeline stages a strategy can have: the highest PP of the mask.
@@ -764,15 +765,16 @@ __host__ __device__ inline int max_stages(uint32_t pp_mask) {
 }
 
 __host__ __device__ inline size_t coop_group_bytes(int G, int stages) {
-    return ((size_t)G + 7) / 8 * 8 + sizeof(double) * (2 * (size_t)G + stages);
+    return ((size_t)G + 7) / 8 * 8 + sizeof(double) * (2 * (size_t)G + 2 * (size_t)stages);
 }
 
-__device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G) {
+__device__ __forceinline__ CoopLds carve_coop(unsigned char* base, int G, int stages) {
     CoopLds c;
     c.mem = base;
     c.tsum = reinterpret_cast<double*>(base + ((size_t)G + 7) / 8 * 8);
     c.pmin = c.tsum + G;
     c.comp = c.pmin + G;
+    c.ppt = c.comp + stages;
     return c;
 }
 
@@ -893,40 +895,38 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
                                     : (Xscan_d / (t * hmin)) * l + (Xcomp_d / (t * cmin)) * l;
             }
             wave_sync();
-            if (feas && gl == 0) {
-                double s1 = 0.0, s2 = 0.0, tmax = 0.0;
-                for (int j = 0; j < pp; ++j) {
-                    const double l =
-                        (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
-                    double mx = 0.0;
-                    for (int r = 0; r < tp; ++r) {
-                        const double v = c.tsum[j * tp + r];
-                        if (r == 0 || v > mx) mx = v;
-                    }
-                    const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
-                    const double stage = c.comp[j] + tpc;
-                    s1 = s1 + stage;
-                    if (kPipe && !prefill) {
-                        double T = stage;
-                        if (j + 1 < pp) {
-                            double mn = 0.0;
-                            for (int r = 0; r < tp; ++r) {
-                                const double v = c.pmin[j * tp + r];
-                                if (r == 0 || v < mn) mn = v;
-                            }
-                            T = T + mn * p.s_out;
-                        }
-                        tmax = dmax(tmax, T);
-                    }
+            // Per stage, a lane each: the stage's time (computation + TP row maximum, rows in
+            // ascending device order) over its comp entry, and the PP link into the next stage.
+            for (int j = gl; feas && j < pp; j += kCL) {
+                const double l = (double)split_layers<kAsym>(split, j, kAsym ? stage_cmin(tb, c.mem, 1, j, tp) : 0.0);
+                double mx = 0.0;
+                for (int r = 0; r < tp; ++r) {
+                    const double v = c.tsum[j * tp + r];
+                    if (r == 0 || v > mx) mx = v;
                 }
-                for (int j = 0; j + 1 < pp; ++j) {
+                const double tpc = prefill ? (mx * 4.0) * l : ((mx * 4.0) * p.s_out) * l;
+                double pt = 0.0;
+                if (j + 1 < pp) {
                     double mn = 0.0;
                     for (int r = 0; r < tp; ++r) {
                         const double v = c.pmin[j * tp + r];
                         if (r == 0 || v < mn) mn = v;
                     }
-                    s2 = s2 + (prefill ? mn : mn * p.s_out);
+                    pt = prefill ? mn : mn * p.s_out;
                 }
+                c.comp[j] = c.comp[j] + tpc;
+                c.ppt[j] = pt;
+            }
+            wave_sync();
+            // one lane sums them in stage order
+            if (feas && gl == 0) {
+                double s1 = 0.0, s2 = 0.0, tmax = 0.0;
+                for (int j = 0; j < pp; ++j) {
+                    const double stage = c.comp[j];
+                    s1 = s1 + stage;
+                    if (kPipe && !prefill) tmax = dmax(tmax, j + 1 < pp ? stage + c.ppt[j] : stage);
+                }
+                for (int j = 0; j + 1 < pp; ++j) s2 = s2 + c.ppt[j];
                 const double lat = s1 + s2;
                 const double x = (1000.0 * b) / (kPipe && !prefill ? tmax : lat);
                 if (kCls) {
@@ -1011,7 +1011,7 @@ __global__ void __launch_bounds__(64) ref_kernel(Problem p, CostWork wk) {
     Problem p1 = p;
     p1.N = 1;  // the table holds one candidate
     unsigned char* cbase = a0 + (((size_t)G + 7) & ~(size_t)7);
-    const CoopLds c = carve_coop(cbase + grp * coop_group_bytes(G, max_stages(p.pp_mask)), G);
+    const CoopLds c = carve_coop(cbase + grp * coop_group_bytes(G, max_stages(p.pp_mask)), G, max_stages(p.pp_mask));
     coop_unit<W, kVar, kCL>(p1, tb, wk.ref.out, c, adm_tab, gl, live, 0, k, role, m);
     if (k < p.Kmax && gl == 0) {
 #pragma unroll
@@ -1088,7 +1088,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
     if (coop) {
         const int grp = lane / kCL, gl = lane % kCL;
         constexpr int kGroupsPerWave = 64 / kCL;
-        const CoopLds c = carve_coop(warea + grp * coop_group_bytes(G, stages), G);
+        const CoopLds c = carve_coop(warea + grp * coop_group_bytes(G, stages), G, stages);
         const int64_t waves = (int64_t)gridDim.x * (kEvalBlock / 64);
         for (int64_t base = ((int64_t)blockIdx.x * (kEvalBlock / 64) + wave) * kGroupsPerWave; base < first_small;
              base += waves * kGroupsPerWave) {
