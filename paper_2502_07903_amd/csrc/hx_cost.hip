@@ -818,7 +818,12 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
     double best_b = 0.0, best_lat = 0.0, best_x = 0.0;
     const uint32_t am = live ? adm_tab[cnt] : 0u;
     const int n_task = kCls ? p0.n_cls : 1;
-    for (int tp = 1; tp <= HX_MAX_TP; ++tp) {
+    // the TP degrees some group of the wavefront can take, ascending (the loop holds wavefront
+    // operations, so every lane runs it the same number of times)
+    uint32_t wave_am = am;
+    for (int off = 32; off > 0; off >>= 1) wave_am |= (uint32_t)__shfl_xor((int)wave_am, off, 64);
+    for (uint32_t rest = wave_am; rest; rest &= rest - 1) {
+        const int tp = __ffs(rest);
         const bool adm = (am >> (tp - 1)) & 1u;
         const int pp = adm ? stage_count(cnt, tp) : 0;
         const double t = (double)tp;
