@@ -122,8 +122,9 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
 // Per-GPU nodes with every group's role, capacity share floor(C/sz) and remainder C mod sz, and
 // a running member count staged in LDS ([Kmax][64] per field, loads of eight slots issued
 // together; one division per group, not per GPU), then the GPUs taken in ascending id with their
-// group ids loaded eight at a time: the k-th member of a group met so far is its rank.  The same rows as nodes_kernel's per-GPU branch with ~(Kmax + G)/8 memory round
-// trips per lane instead of two per GPU.  Kmax <= kNodesGpuMaxK (the staging fits 64 KB).
+// group ids loaded sixteen at a time: the k-th member of a group met so far is its rank.  The
+// same rows as nodes_kernel's per-GPU branch with ~Kmax/8 + G/16 memory round trips per lane
+// instead of two per GPU.  Kmax <= kNodesGpuMaxK (the staging fits 64 KB).
 constexpr int kNodesGpuMaxK = 128;
 __host__ __device__ inline size_t nodes_gpu_lds(int Kmax) { return (size_t)Kmax * 64 * 7; }
 
@@ -198,22 +199,23 @@ __global__ void __launch_bounds__(64) nodes_gpu_kernel(Problem p, CostOut o, Flo
         any_a = false;
         if (replay)
             for (int k = 0; k < Kmax; ++k) gseen[k * 64 + lane] = 0;
-        for (int g0 = 0; g0 < p.G; g0 += kC) {
+        constexpr int kCG = 16;  // GPUs per batch of loads (eight slots per batch above)
+        for (int g0 = 0; g0 < p.G; g0 += kCG) {
             // the chunk's loads issued together (rows past G read row G - 1 and are replaced);
             // kValue: the GPUs' smallest link capacities with them
-            int kk[kC];
-            int32_t rm[kC];
+            int kk[kCG];
+            int32_t rm[kCG];
 #pragma unroll
-            for (int x = 0; x < kC; ++x) {
+            for (int x = 0; x < kCG; ++x) {
                 const int g = g0 + x < p.G ? g0 + x : p.G - 1;
                 kk[x] = p.assign[(int64_t)g * N + n];
                 rm[x] = kValue ? rmin[g] : 0;
             }
 #pragma unroll
-            for (int x = 0; x < kC; ++x)
+            for (int x = 0; x < kCG; ++x)
                 if (g0 + x >= p.G) kk[x] = HX_UNUSED;
 #pragma unroll
-            for (int x = 0; x < kC; ++x) {
+            for (int x = 0; x < kCG; ++x) {
                 const int g = g0 + x, k = kk[x];
                 if (g >= p.G || k >= Kmax) continue;
                 const int r = grole[k * 64 + lane];
