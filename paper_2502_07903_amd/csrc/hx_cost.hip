@@ -4,21 +4,26 @@
 // stages, how many TP peers); mixing sizes in one wavefront serialises every size's loop
 // nest.  So the batch is first sorted, globally, into work units bucketed by (size, role),
 // largest groups first so that the longest lanes start at once, and the costing kernel then
-// runs one unit per lane with a wavefront-uniform control path:
+// runs the units with a wavefront-uniform control path:
 //
+//   setup_kernel    clears the bucket histogram, tabulates the prefill link terms (batch 1
+//                   makes them candidate independent) and the memory-row screen;
+//   ref_kernel      with HX_HINT_SHARED_GROUPS only: candidate 0's groups, costed once;
 //   decode_kernel   one lane per candidate: each group's member set as a GPU bitmask (an
-//                   output: the flow-network build reuses it), absent slots zeroed, and a
-//                   per-workgroup histogram of units per bucket added to the global one;
-//   scan_kernel     one wavefront: exclusive scan of the histogram into bucket offsets;
-//   scatter_kernel  one lane per candidate: each present group's unit record
-//                   (candidate, slot, role, member mask) written into its bucket, a workgroup
-//                   reserving its range of each bucket with one atomic;
-//   eval_kernel     one lane per unit: every admissible TP x PP strategy, prefill keeping its
+//                   output: the flow-network build reuses it), absent and screened slots
+//                   zeroed, groups equal to one of candidate 0's given its outputs, and each
+//                   remaining group's bucket code with a per-workgroup histogram of units per
+//                   bucket added to the global one;
+//   scatter_kernel  one lane per candidate: each workgroup scans the histogram into bucket
+//                   offsets, then writes each unit record (candidate, slot, role, member mask)
+//                   into its bucket, reserving its range of each bucket with one atomic;
+//   eval_kernel     every admissible TP x PP strategy of a unit, prefill keeping its
 //                   latency-optimal and decode its throughput-optimal one (Sec. 3.3,
-//                   "Compute nodes").  The unit's mask is expanded into the lane's own LDS
-//                   column of member ids (ascending), from which stage j of (tp, pp) is the
-//                   slice [j*tp, (j+1)*tp); for tp in {1, 2, 4, 8} the stage's ids sit in
-//                   registers and each device's peer loop is unrolled.
+//                   "Compute nodes").  Large groups take several lanes (coop_unit); the others
+//                   one lane each, whose mask is expanded into the lane's own LDS column of
+//                   member ids (ascending), from which stage j of (tp, pp) is the slice
+//                   [j*tp, (j+1)*tp); for tp in {1, 2, 4, 8} the stage's ids sit in registers
+//                   and each device's peer loop is unrolled.
 // Per-GPU parameters, and the alpha/beta tables when they fit, are staged in LDS.  The
 // arithmetic is FP64 scalar work, not a dense contraction, so there is no MFMA here.
 //

@@ -11,6 +11,10 @@
 //                 replica nodes, with the stage-order search of Appendix A (kv_order_kernel)
 //                 when HX_VARIANT_KV_ORDER is set, and the class mix with request classes;
 //   kv_gpu_kernel the same for per-GPU nodes, a workgroup per 64 candidates.
+// hx_score_batch's per-GPU path (up to 128 GPUs and 128 slots) replaces the last two: a table of
+// every link's capacity (link_table_kernel), and nodes_gpu_kernel<W, true>, which settles each
+// network whose KV edges all dominate while it counts its nodes and lists the others for the
+// max-flow.
 #include "hx_internal.h"
 
 namespace hx {
