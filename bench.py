@@ -54,12 +54,12 @@ KERNEL_TRAFFIC = {
     # workload 3 (profiles/all_kernels_workload3.md); maxflow is the instantiation with the folded
     # argmax, best the final reduction of its slots
     3: {
-        "setup": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 70.54, "write_kib": 57.43},
-        "decode": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 1714, "write_kib": 2.884e+04},
-        "scatter": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 5425, "write_kib": 1485},
-        "eval": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 1104, "write_kib": 1.205e+04},
-        "nodes": {"source_sha256_16": "177e8f7865aa07d0", "fetch_kib": 6694, "write_kib": 1.578e+04},
-        "kv": {"source_sha256_16": "177e8f7865aa07d0", "fetch_kib": 5882, "write_kib": 1.34e+04},
+        "setup": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 70.55, "write_kib": 57.43},
+        "decode": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1714, "write_kib": 2.884e+04},
+        "scatter": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 5425, "write_kib": 1485},
+        "eval": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1103, "write_kib": 1.206e+04},
+        "nodes": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 6694, "write_kib": 1.577e+04},
+        "kv": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 5882, "write_kib": 1.34e+04},
         "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 1.674e+04, "write_kib": 768},
         "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 18.1, "write_kib": 0.03125},
     },
@@ -67,13 +67,13 @@ KERNEL_TRAFFIC = {
     # (profiles/chain_workload5.md): nodes is the settling nodes kernel, kv the link table,
     # maxflow the list-driven kernel, shared candidate 0's groups, best the split argmax
     5: {
-        "setup": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 184.2, "write_kib": 516.1},
-        "shared": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 179.9, "write_kib": 2},
-        "decode": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 1.047e+04, "write_kib": 1.471e+05},
-        "scatter": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 3.969e+04, "write_kib": 7569},
-        "eval": {"source_sha256_16": "58198b79e2fb1fed", "fetch_kib": 9315, "write_kib": 3.267e+04},
-        "nodes": {"source_sha256_16": "177e8f7865aa07d0", "fetch_kib": 6.153e+04, "write_kib": 1536},
-        "kv": {"source_sha256_16": "177e8f7865aa07d0", "fetch_kib": 145.8, "write_kib": 68.03},
+        "setup": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 184.2, "write_kib": 516.1},
+        "shared": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 179.9, "write_kib": 2},
+        "decode": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1.047e+04, "write_kib": 1.471e+05},
+        "scatter": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 3.97e+04, "write_kib": 7566},
+        "eval": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 9310, "write_kib": 3.267e+04},
+        "nodes": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 6.153e+04, "write_kib": 1536},
+        "kv": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 145.8, "write_kib": 68.03},
         "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 10.64, "write_kib": 0},
         "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 297.2, "write_kib": 8.062},
     },
