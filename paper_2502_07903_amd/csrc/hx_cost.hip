@@ -35,15 +35,16 @@
 namespace hx {
 namespace {
 
-constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40^2 doubles (25.6 KB)
+constexpr int kTableMaxG = 40;  // alpha and beta staged in LDS up to 2 * 40 * 41 doubles (26.2 KB)
 
 
 // ------------------------------------------------------------------ one strategy
 
 struct Tables {
-    const double *gfl, *ghb, *gme, *alpha, *beta;
+    const double *gfl, *ghb, *gme, *alpha, *beta;  // alpha, beta: row d at d * ld
     const double* tp_pre;  // [tp - 1][G][G] alpha + X/(tp beta) at batch 1 (prefill), per call
     const double* pp_pre;  // [G][G] alpha + X/beta at batch 1
+    int ld;                // row stride of alpha and beta: G in memory, G + 1 staged in LDS
 };
 
 struct StrategyCost {
@@ -140,16 +141,16 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
             for (int r = 0; r < kMax; ++r) sum[r] = 0.0;
 #pragma unroll
             for (int r = 0; r < kMax; ++r) {
-                const double* arow = tb.alpha + S[r] * G;
-                const double* brow = tb.beta + S[r] * G;
+                const double* arow = tb.alpha + S[r] * tb.ld;
+                const double* brow = tb.beta + S[r] * tb.ld;
 #pragma unroll
                 for (int q = r + 1; q < kMax; ++q) {
-                    const double bf = brow[S[q]], bb = tb.beta[S[q] * G + S[r]];
+                    const double bf = brow[S[q]], bb = tb.beta[S[q] * tb.ld + S[r]];
                     const double qf = X / (t * bf);
                     double qb = qf;
                     if (__double_as_longlong(bf) != __double_as_longlong(bb)) qb = X / (t * bb);
                     sum[r] = sum[r] + (arow[S[q]] + qf);
-                    sum[q] = sum[q] + (tb.alpha[S[q] * G + S[r]] + qb);
+                    sum[q] = sum[q] + (tb.alpha[S[q] * tb.ld + S[r]] + qb);
                     // keep each pair's loads and divisions together (bounded live ranges)
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -164,8 +165,8 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
 #pragma unroll
                 for (int x = 1; x < kMax; ++x)
                     if (x == r) d = S[x];
-                const double* arow = tb.alpha + d * G;
-                const double* brow = tb.beta + d * G;
+                const double* arow = tb.alpha + d * tb.ld;
+                const double* brow = tb.beta + d * tb.ld;
                 const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
                 double sum = 0.0;
                 if (prefill) {
@@ -199,8 +200,8 @@ __device__ __forceinline__ bool cost_strategy(const Problem& p, const Tables& tb
 #pragma unroll
                 for (int x = 1; x < kMax; ++x)
                     if (x == r) d = Sp[x];
-                const double* arow = tb.alpha + d * G;
-                const double* brow = tb.beta + d * G;
+                const double* arow = tb.alpha + d * tb.ld;
+                const double* brow = tb.beta + d * tb.ld;
                 const double* prow = tb.pp_pre + (size_t)d * G;
                 if (prefill) {
                     double v[kMax];
@@ -873,8 +874,8 @@ __device__ void coop_unit(const Problem& p0, const Tables& tb0, const CostOut& o
                 const int j = it / tp, r = it - j * tp;
                 const uint8_t* S = c.mem + j * tp;
                 const int d = S[r];
-                const double* arow = tb.alpha + d * G;
-                const double* brow = tb.beta + d * G;
+                const double* arow = tb.alpha + d * tb.ld;
+                const double* brow = tb.beta + d * tb.ld;
                 const double* prow = tb.tp_pre + ((size_t)(tp - 1) * G + d) * G;
                 const double* qrow = tb.pp_pre + (size_t)d * G;
                 double sum = 0.0;
@@ -999,7 +1000,7 @@ __global__ void __launch_bounds__(64) ref_kernel(Problem p, CostWork wk) {
     }
     for (int c = tid; c <= G; c += 64) adm_tab[c] = admissible(p, c);
     __syncthreads();
-    const Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre};
+    const Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre, G};
     const int k = blockIdx.x * kPer + grp;
     // slot k's members: each lane of the slot's lane group marks every kCL-th GPU, then OR
     uint64_t m[W] = {};
@@ -1057,18 +1058,24 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
         ghb[g] = ok ? p.hbm[t] : 0.0;
         gme[g] = ok ? p.mem[t] : 0.0;
     }
-    Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre};
+    Tables tb{gfl, ghb, gme, p.alpha, p.beta, wk.tp_pre, wk.pp_pre, G};
     double* tb_end = gme + G;
     if (kTables) {
+        // rows padded to G + 1 doubles: the lanes of a cooperative group read one column of
+        // several rows at once, which an unpadded stride of G doubles maps onto one bank
+        // whenever G is a multiple of 32
+        const int ld = G + 1;
         double* a = gme + G;
-        double* b = a + G * G;
+        double* b = a + G * ld;
         for (int e = threadIdx.x; e < G * G; e += kEvalBlock) {
-            a[e] = p.alpha[e];
-            b[e] = p.beta[e];
+            const int d = e / G, c = e - d * G;
+            a[d * ld + c] = p.alpha[e];
+            b[d * ld + c] = p.beta[e];
         }
         tb.alpha = a;
         tb.beta = b;
-        tb_end = b + G * G;
+        tb.ld = ld;
+        tb_end = b + G * ld;
     }
     // Admissible strategies by group size, for every size up to G.
     __shared__ uint8_t adm_tab[HX_MAX_GPUS + 1];
@@ -1146,7 +1153,7 @@ __global__ void __launch_bounds__(kEvalBlock, 4) eval_kernel(Problem p, CostOut 
 template <int W, int kVar, int kCMin, int kCL>
 void launch_eval_coop(const Problem& p, const CostOut& o, const CostWork& wk, int nb, bool tables, int eb, int blocks,
                       hipStream_t s) {
-    const size_t lds = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * p.G : 0)) +
+    const size_t lds = sizeof(double) * (3 * (size_t)p.G + (tables ? 2 * (size_t)p.G * (p.G + 1) : 0)) +
                        (size_t)(eb / 64) * eval_wave_bytes(p.G, W == 1 && p.G >= kCMin, kCL, max_stages(p.pp_mask));
     if (eb == 256) {
         if (tables)
