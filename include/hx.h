@@ -307,14 +307,17 @@ int hx_best_candidate(const int32_t *flow_value, int32_t n_cand, int32_t *best, 
  * candidate but not a flow assignment (Sec. 3.1 objective, Sec. 3.3 network, Appendix A
  * capacities): hx_cost_eval, hx_build_flownet, hx_maxflow_batch with kv_flow and cut null, and
  * hx_best_candidate, enqueued by one call with the same arguments and errors, a workspace of
- * hx_score_workspace_bytes (the cost model's scratch, then a table of link capacities and a list
- * of candidates, then the argmax's partial winners (one per workgroup, or one per slot that the max-flow
- * kernel's workgroups fold into), 256-byte aligned, contents ignored on entry), and the same results: every cost
+ * hx_score_workspace_bytes (the cost model's scratch; then a table of link capacities and a list
+ * of candidates, or, for up to 32 group slots, the KV edge lists: a word per candidate marking
+ * its nodes with a strategy and, twice, 4 bytes for each of its possible KV edges; then the
+ * argmax's partial winners (one per workgroup, or one per slot that the max-flow kernel's
+ * workgroups fold into); 256-byte aligned, contents ignored on entry), and the same results: every cost
  * output, the network's node counts (n_p, n_d), flow_value and best, bit for bit.  At
  * granularity 0, and beyond 128 GPUs or 128 group slots, every row of the network is written as
- * by hx_build_flownet.  At granularity 1 on clusters of up to 128 GPUs a KV edge's capacity
- * depends only on its link, so a network whose every KV edge can carry min(a_i, b_j) (the
- * dominant-KV closed form: maximum flow min(sum a, sum b)) is settled from a table of link
+ * by hx_build_flownet (with up to 32 group slots the KV edges whose two replicas both have a
+ * strategy are listed and walked apart from the others, which are written 0).  At
+ * granularity 1 on clusters of up to 128 GPUs a KV edge's capacity depends only on its link,
+ * so a network whose every KV edge can carry min(a_i, b_j) (the dominant-KV closed form: maximum flow min(sum a, sum b)) is settled from a table of link
  * capacities while its nodes are counted, and only the other networks get their node and KV rows
  * written and are solved by push-relabel; the rows of the settled networks are left as they
  * were. */

@@ -390,11 +390,19 @@ int hx_best_candidate(const int32_t* flow_value, int32_t n_cand, int32_t* best, 
     return e == hipSuccess ? HX_OK : hip_error(e);
 }
 
+// hx_score_batch's scratch after the cost model's: the link table and list (per-GPU path) or the
+// listed KV path's feasibility words and edge list (replica path), whichever is larger, then the
+// argmax's area.
+static size_t score_mid_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
+    const size_t t = hx::link_table_bytes(n_gpus, n_cand);
+    const size_t f = max_groups <= 32 && n_cand <= (1 << 22) ? hx::kv_list_bytes(max_groups, n_cand) : 0;
+    return ((t > f ? t : f) + 255) & ~(size_t)255;
+}
+
 size_t hx_score_workspace_bytes(int32_t n_gpus, int32_t max_groups, int32_t n_cand) {
     const size_t c = hx_cost_workspace_bytes(n_gpus, max_groups, n_cand);
     if (c == 0) return 0;
-    return ((c + 255) & ~(size_t)255) + ((hx::link_table_bytes(n_gpus, n_cand) + 255) & ~(size_t)255) +
-           ((hx::best_parts_bytes() + 255) & ~(size_t)255);
+    return ((c + 255) & ~(size_t)255) + score_mid_bytes(n_gpus, max_groups, n_cand) + ((hx::best_parts_bytes() + 255) & ~(size_t)255);
 }
 
 int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx_space space,
@@ -408,26 +416,26 @@ int hx_score_batch(const hx_cluster* cluster, hx_model model, hx_workload wl, hx
         return HX_EINVAL;
     if (hx::maxflow_lds_bytes(net->max_p, net->max_d, net->max_pd) == 0) return HX_ETOOBIG;
     const hx::Problem p = make_problem(cluster, model, wl, space, cand);
-    const hx::FlowNet f = make_net(net);
-    // the argmax's area follows the link table: per-workgroup winners for the per-GPU path, the
-    // fused argmax's slots (zeroed by the cost model's first kernel) otherwise
-    const size_t off_part = ((hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
-                             ~(size_t)255) +
-                            ((hx::link_table_bytes(cluster->n_gpus, cand->n_cand) + 255) & ~(size_t)255);
+    hx::FlowNet f = make_net(net);
+    // the link table (or the feasibility words) follows the cost model's scratch, the argmax's
+    // area follows them: per-workgroup winners for the per-GPU path, the fused argmax's slots
+    // (zeroed by the cost model's first kernel) otherwise
+    const size_t off_mid =
+        (hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) & ~(size_t)255;
+    const size_t off_part = off_mid + score_mid_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand);
     unsigned char* part = static_cast<unsigned char*>(workspace) + off_part;
     const bool direct = hx::flownet_values_direct(p) && hx::maxflow_workgroup_plan(net->max_p, net->max_d, net->max_pd);
     unsigned long long* slots = direct ? nullptr : reinterpret_cast<unsigned long long*>(part);
     hipError_t e = hx::launch_cost(p, make_cost(cost), workspace, stream, slots, direct ? 0 : hx::kArgSlots);
     if (e == hipSuccess) {
         if (direct) {
-            // the link table follows the cost model's scratch, 256-byte aligned
-            const size_t off = (hx::cost_workspace_bytes(cluster->n_gpus, cand->max_groups, cand->n_cand) + 255) &
-                               ~(size_t)255;
-            void* table = static_cast<unsigned char*>(workspace) + off;
+            void* table = static_cast<unsigned char*>(workspace) + off_mid;
             e = hx::launch_flownet_values(p, make_cost(cost), f, flow_value, table, stream);
             int32_t* count = hx::flownet_values_list_count(table, cluster->n_gpus);
             if (e == hipSuccess) e = hx::launch_maxflow_listed(f, flow_value, round_budget(), count + 16, count, stream);
         } else {
+            if (hx::kv_list_fits(p.granularity, cand->max_groups, cand->n_cand))
+                hx::kv_list_carve(f, static_cast<unsigned char*>(workspace) + off_mid, cand->max_groups, cand->n_cand);
             e = hx::launch_flownet(p, make_cost(cost), f, stream);
             if (e == hipSuccess)
                 e = hx::launch_maxflow(f, flow_value, nullptr, nullptr, round_budget(), nullptr, stream, slots);

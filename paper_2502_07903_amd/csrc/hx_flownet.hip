@@ -5,11 +5,16 @@
 // of the [row][n] arrays coalesce across the wavefront:
 //   nodes_kernel  one lane per candidate: lists the prefill and decode nodes (replicas in
 //                 ascending group id, or GPUs in ascending id at per-GPU granularity) with
-//                 their source, node and sink capacities (Appendix A);
+//                 their source, node and sink capacities (Appendix A), and, for the listed KV
+//                 path, which replica nodes have a strategy (FlowNet::feas);
 //   kv_kernel     one lane per (KV edge, candidate): the edge capacity between prefill node
 //                 i and decode node j (connection type 3; Table 1 last row; Appendix A) of
 //                 replica nodes, with the stage-order search of Appendix A (kv_order_kernel)
 //                 when HX_VARIANT_KV_ORDER is set, and the class mix with request classes;
+//   kv_rows_kernel, kv_scan_kernel, kv_compact_kernel, kv_walk_group_kernel  the same edges as
+//                 kv_kernel when hx_score_batch hands over scratch for an edge list: one lane per
+//                 candidate writes every edge with an infeasible end (0, row by row) and lists
+//                 the others, the lists are packed, then 16 lanes per listed edge walk it;
 //   kv_gpu_kernel the same for per-GPU nodes, a workgroup per 64 candidates.
 // hx_score_batch's per-GPU path (up to 128 GPUs and 128 slots) replaces the last two: a table of
 // every link's capacity (link_table_kernel), and nodes_gpu_kernel<W, true>, which settles each
@@ -54,8 +59,9 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
         // Group slots in chunks of 8: the chunk's loads are issued together, then its slots
         // are appended to the node lists in ascending order.
         constexpr int kC = 8;
+        uint32_t pf = 0, df = 0;  // nodes whose replica has a strategy (tp > 0), by node index
         for (int k0 = 0; k0 < p.Kmax; k0 += kC) {
-            int sz[kC], rl[kC];
+            int sz[kC], rl[kC], tq[kC];
             int32_t cp[kC];
             // every load issued (slots past Kmax read slot Kmax - 1 and are replaced), so that
             // the chunk's loads are in flight together
@@ -65,6 +71,7 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
                 sz[x] = mask_size<W>(o.members, k, N, n);
                 rl[x] = p.role[(int64_t)k * N + n];
                 cp[x] = o.cap[(int64_t)k * N + n];
+                tq[x] = o.tp[(int64_t)k * N + n];
             }
 #pragma unroll
             for (int x = 0; x < kC; ++x)
@@ -82,16 +89,19 @@ __global__ void __launch_bounds__(kNodeBlock) nodes_kernel(Problem p, CostOut o,
                     f.p_slot[e] = k;
                     f.src_cap[e] = p.coord_cap;
                     f.p_cap[e] = cp[x];
+                    if (tq[x] > 0 && np < 32) pf |= 1u << np;
                     ++np;
                 } else if (rl[x] == HX_DECODE) {
                     const int64_t e = (int64_t)nd * N + n;
                     f.d_slot[e] = k;
                     f.d_cap[e] = cp[x];
                     f.sink_cap[e] = p.coord_cap;
+                    if (tq[x] > 0 && nd < 32) df |= 1u << nd;
                     ++nd;
                 }
             }
         }
+        if (f.feas) f.feas[n] = (uint64_t)pf | ((uint64_t)df << 32);
     } else {
         // Per-GPU nodes: the k-th member (by GPU id) of a replica of sz GPUs and capacity C
         // carries floor(C/sz) + [k < C mod sz].
@@ -1004,6 +1014,35 @@ __device__ __forceinline__ double task_mix(const Problem& p, TimeOf time_of) {
     return t;
 }
 
+// Capacity of the KV edge from prefill node i to decode node j of candidate n (0 unless both
+// replicas have a strategy).  pm, dm: the lane's two member columns in LDS, stride bytes apart.
+template <int W, bool kAsym, bool kCls>
+__device__ __forceinline__ int32_t kv_edge(const Problem& p, const CostOut& o, const FlowNet& f, const double* gfl,
+                                           int i, int j, int64_t n, uint8_t* pm, uint8_t* dm, int stride) {
+    const int64_t N = p.N;
+    int32_t c = 0;
+    const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
+    // The member masks are loaded with the strategies (not after them), so the lane waits on
+    // one memory round for both.
+    uint64_t mp[W], md[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        mp[w] = o.members[((int64_t)kp * W + w) * N + n];
+        md[w] = o.members[((int64_t)kd * W + w) * N + n];
+    }
+    const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
+    const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
+    if (ptp > 0 && dtp > 0) {
+        // A strategy whose tp*pp is not the group's size (cost outputs of another batch) is
+        // treated as infeasible rather than read past the member list.
+        if (expand_words<W>(mp, pm, stride) == ptp * ppp && expand_words<W>(md, dm, stride) == dtp * dpp)
+            c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                   : kAsym ? kv_time_asym(p, gfl, pm, ptp, ppp, dm, dtp, dpp, stride)
+                                           : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
+    }
+    return c;
+}
+
 template <int W, bool kAsym, bool kCls>
 __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, FlowNet f) {
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
@@ -1024,29 +1063,286 @@ __global__ void __launch_bounds__(kKvBlock) kv_kernel(Problem p, CostOut o, Flow
     const int np = f.n_p[n], nd = f.n_d[n];
     if (e >= np * nd) return;
     const int i = e / nd, j = e - i * nd;
-    int32_t c = 0;
-    const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
-    // The member masks are loaded with the strategies (not after them), so the lane waits on
-    // one memory round for both.
-    uint64_t mp[W], md[W];
+    // member columns [G][blockDim] each
+    f.kv_cap[(int64_t)e * N + n] = kv_edge<W, kAsym, kCls>(p, o, f, gfl, i, j, n, sm + tid, sm + p.G * stride + tid,
+                                                           stride);
+}
+
+// The listed KV path, first kernel: a wavefront per piece (64 candidates, blockIdx.y the slice
+// of their KV rows), a lane per candidate walking its rows of the slice below n_p n_d in order
+// (row e of every lane at once, so the stores coalesce): 0 for an edge with an infeasible end
+// (FlowNet::feas), the others listed in the piece's own part of the list (no atomics: a counter
+// that every wavefront bumps serialises them).
+constexpr int kRowsBlock = 256;
+
+__global__ void __launch_bounds__(kRowsBlock) kv_rows_kernel(FlowNet f) {
+    const int64_t N = f.N;
+    const int64_t n0 = (int64_t)blockIdx.x * kRowsBlock + threadIdx.x;
+    const int64_t seg = n0 >> 6;
+    if (seg * 64 >= N) return;  // a wavefront wholly past N owns no piece
+    const bool in = n0 < N;
+    const int64_t n = in ? n0 : N - 1;  // every lane loads, lanes past N own no row
+    const int np = f.n_p[n], nd = f.n_d[n];
+    const uint64_t fz = f.feas[n];
+    const int lane = threadIdx.x & 63;
+    const int r0 = (int)blockIdx.y * f.kv_rows;
+    const int pd = in ? np * nd : 0;
+    const int hi = pd < r0 + f.kv_rows ? pd : r0 + f.kv_rows;  // this lane's rows: [r0, hi)
+    int rows = hi;
+    for (int off = 32; off > 0; off >>= 1) {
+        const int o2 = __shfl_xor(rows, off, 64);
+        rows = o2 > rows ? o2 : rows;
+    }
+    const int64_t piece = seg * kKvSlices + blockIdx.y;
+    uint32_t* list = f.kv_list + piece * (int64_t)(64 * f.kv_rows);
+    int i = 0, j = 0;
+    if (r0 < hi) {
+        i = r0 / nd;
+        j = r0 - i * nd;
+    }
+    const uint32_t dm = (uint32_t)(fz >> 32);
+    bool pi = (fz >> i) & 1;  // prefill node i has a strategy
+    int cnt = 0;
+    for (int e = r0; e < rows; ++e) {
+        const bool live = e < hi;
+        const bool walk = live && pi && ((dm >> j) & 1);
+        if (live && !walk) f.kv_cap[(int64_t)e * N + n] = 0;
+        const uint64_t bal = __ballot(walk);
+        if (walk) list[cnt + __popcll(bal & ((1ull << lane) - 1))] = ((uint32_t)n << 10) | ((uint32_t)i << 5) | (uint32_t)j;
+        cnt += __popcll(bal);
+        if (live && ++j == nd) {
+            j = 0;
+            ++i;
+            pi = (fz >> i) & 1;
+        }
+    }
+    if (lane == 0) f.kv_count[piece] = cnt;
+}
+
+// LDS written by some lanes of a wavefront and then read by others of the same wavefront.
+__device__ __forceinline__ void lane_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The listed KV path's packing: one workgroup forms the exclusive prefix sums of the pieces'
+// counts (kv_offs, the total last); each thread takes a contiguous run of pieces (a multiple of
+// four: the piece count is one), sums it, the workgroup scans the 1024 sums, and the thread
+// writes its run's offsets.  A run is read and written in 16-byte words, kScanChunk counts at a
+// time with their loads issued together (the run's last word repeated past its end): one CU
+// does all of it, so the number of memory requests, not bytes, sets the time.
+constexpr int kScanBlock = 1024;
+constexpr int kScanChunk = 16;
+
+__global__ void __launch_bounds__(kScanBlock) kv_scan_kernel(FlowNet f) {
+    __shared__ int32_t part[kScanBlock / 64];
+    constexpr int kWords = kScanChunk / 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t P = (f.N + 63) / 64 * kKvSlices;  // a multiple of 4
+    const int64_t run = (P + 4 * kScanBlock - 1) / (4 * kScanBlock) * 4;
+    const int64_t lo = tid * run < P ? tid * run : P, hi = lo + run < P ? lo + run : P;
+    const int4* cw = reinterpret_cast<const int4*>(f.kv_count);
+    int4* ow = reinterpret_cast<int4*>(f.kv_offs);
+    const int64_t wlo = lo / 4, whi = hi / 4;
+    int32_t sum = 0;
+    for (int64_t c0 = wlo; c0 < whi; c0 += kWords) {
+        int4 v[kWords];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) v[k] = cw[c0 + k < whi ? c0 + k : whi - 1];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k)
+            if (c0 + k < whi) sum += v[k].x + v[k].y + v[k].z + v[k].w;
+    }
+    int32_t x = sum;  // inclusive scan over the wavefront
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) part[wave] = x;
+    __syncthreads();
+    int32_t before = 0, total = 0;
+    for (int w = 0; w < kScanBlock / 64; ++w) {
+        const int32_t v = part[w];
+        if (w < wave) before += v;
+        total += v;
+    }
+    int32_t off = before + x - sum;
+    for (int64_t c0 = wlo; c0 < whi; c0 += kWords) {
+        int4 v[kWords];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) v[k] = cw[c0 + k < whi ? c0 + k : whi - 1];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k)
+            if (c0 + k < whi) {
+                int4 o;
+                o.x = off;
+                o.y = o.x + v[k].x;
+                o.z = o.y + v[k].y;
+                o.w = o.z + v[k].z;
+                off = o.w + v[k].w;
+                ow[c0 + k] = o;
+            }
+    }
+    if (tid == 0) f.kv_offs[P] = total;
+}
+
+// Then a wavefront per piece copies its listed edges to kv_flat from its offset on.
+__global__ void __launch_bounds__(256) kv_compact_kernel(FlowNet f) {
+    const int64_t P = (f.N + 63) / 64 * kKvSlices;
+    const int64_t s = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (s >= P) return;
+    const int cnt = f.kv_count[s];
+    const int32_t off = f.kv_offs[s];
+    const uint32_t* list = f.kv_list + s * (int64_t)(64 * f.kv_rows);
+    for (int x = threadIdx.x & 63; x < cnt; x += 64) f.kv_flat[off + x] = list[x];
+}
+
+// The listed KV path's walk: kWalkLanes lanes per listed edge.  An edge's links are every
+// overlapping (stage, stage) pair crossed with every overlapping (rank, rank) pair, and the rank
+// pairs (head slices of ptp x dtp) are the same for every stage pair, so lane l of the group
+// takes the l-th rank pair of the merge walk (there are at most ptp + dtp - 1 <= 15) and walks
+// the stage pairs (at most ppp + dpp - 1) with it; the group's maximum is the edge's KV time
+// (with kCls one maximum per request class, then sum_k w_k max_k in class order).  Each link's
+// time is the binary64 value kv_time or kv_time_classes forms, and a maximum does not depend on
+// the order.  (The asymmetric split stays with kv_kernel: every lane of a group would recompute
+// the stages' layer counts, which measured twice as slow.)  The
+// group's lanes expand the two member masks together (4W bits a lane) into the group's two
+// member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
+// over a grid of kGroupGrid workgroups (about what the chip holds at once): the walks run side
+// by side, each starting with a chain of dependent loads (its list entry, slots, then masks and
+// strategies).  Alpha and beta are read from memory: staging them in LDS per workgroup measured
+// slower.
+constexpr int kWalkLanes = 16;
+constexpr int kGroupBlock = 256;
+constexpr int kGroupGrid = 2048;
+
+__host__ __device__ inline size_t kv_group_lds(int G) { return (size_t)kGroupBlock / kWalkLanes * 2 * G; }
+
+template <int W>
+__device__ __forceinline__ int expand_group(const uint64_t* m, uint8_t* col, int sub) {
+    int below = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) total += __popcll(m[w]);
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-        mp[w] = o.members[((int64_t)kp * W + w) * N + n];
-        md[w] = o.members[((int64_t)kd * W + w) * N + n];
+        const int b0 = sub * 4;
+        const uint64_t mine = (m[w] >> b0) & 0xF;
+        int idx = below + __popcll(m[w] & ((1ull << b0) - 1));
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if ((mine >> t) & 1) col[idx++] = (uint8_t)(w * 64 + b0 + t);
+        below += __popcll(m[w]);
     }
-    const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
-    const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
-    if (ptp > 0 && dtp > 0) {
-        uint8_t* pm = sm + tid;                 // [G][blockDim]
-        uint8_t* dm = sm + p.G * stride + tid;  // [G][blockDim]
+    return total;
+}
+
+template <int W, bool kCls>
+__global__ void __launch_bounds__(kGroupBlock) kv_walk_group_kernel(Problem p, CostOut o, FlowNet f) {
+    constexpr int kGroups = 64 / kWalkLanes, kWaves = kGroupBlock / 64;
+    constexpr int kC = kCls ? HX_MAX_CLASSES : 1;
+    static_assert(64 % kWalkLanes == 0 && kWalkLanes * 4 == 64, "a lane expands 4 bits of each mask word");
+    static_assert(2 * HX_MAX_TP - 1 <= kWalkLanes, "a lane per rank pair");
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = lane / kWalkLanes, sub = lane % kWalkLanes;
+    const int G = p.G;
+    const int64_t N = p.N;
+    uint8_t* colp = sm + (size_t)(wave * kGroups + grp) * 2 * G;  // [G] prefill member ids
+    uint8_t* cold = colp + G;                                     // [G] decode member ids
+    const int nc = kCls ? p.n_cls : 1;
+    double V1[kC];
+#pragma unroll
+    for (int k = 0; k < kC; ++k) V1[k] = 2.0 * (kCls ? p.cls_in[k] : p.s_in) * p.Hkv * p.B;
+    const int64_t total = f.kv_offs[(N + 63) / 64 * kKvSlices];
+    for (int64_t w = (int64_t)blockIdx.x * kWaves + wave; w * kGroups < total; w += (int64_t)gridDim.x * kWaves) {
+        const int64_t x = w * kGroups + grp;
+        const bool live = x < total;
+        const uint32_t v = f.kv_flat[live ? x : w * kGroups];
+        const int64_t n = v >> 10;
+        const int i = (v >> 5) & 31, j = v & 31;
+        const int nd = f.n_d[n];
+        const int kp = f.p_slot[(int64_t)i * N + n], kd = f.d_slot[(int64_t)j * N + n];
+        uint64_t mp[W], md[W];
+#pragma unroll
+        for (int ww = 0; ww < W; ++ww) {
+            mp[ww] = o.members[((int64_t)kp * W + ww) * N + n];
+            md[ww] = o.members[((int64_t)kd * W + ww) * N + n];
+        }
+        const int ptp = o.tp[(int64_t)kp * N + n], ppp = o.pp[(int64_t)kp * N + n];
+        const int dtp = o.tp[(int64_t)kd * N + n], dpp = o.pp[(int64_t)kd * N + n];
+        const int cp = expand_group<W>(mp, colp, sub), cd = expand_group<W>(md, cold, sub);
+        lane_sync();
         // A strategy whose tp*pp is not the group's size (cost outputs of another batch) is
         // treated as infeasible rather than read past the member list.
-        if (expand_words<W>(mp, pm, stride) == ptp * ppp && expand_words<W>(md, dm, stride) == dtp * dpp)
-            c = quantize(1000.0 / (kCls    ? kv_time_classes(p, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                   : kAsym ? kv_time_asym(p, gfl, pm, ptp, ppp, dm, dtp, dpp, stride)
-                                           : kv_time(p, pm, ptp, ppp, dm, dtp, dpp, stride)));
+        const bool ok = live && ptp > 0 && dtp > 0 && cp == ptp * ppp && cd == dtp * dpp;
+        double worst[kC];
+#pragma unroll
+        for (int k = 0; k < kC; ++k) worst[k] = 0.0;
+        if (ok) {
+            // this lane's rank pair: step sub of the merge of the two head partitions
+            int r = 0, q = 0, rl = -1, ql = 0, ovl = 0;
+            for (int t = 0; t <= sub && r < ptp && q < dtp; ++t) {
+                const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+                if (t == sub) {
+                    rl = r;
+                    ql = q;
+                    ovl = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+                }
+                if (re <= qe) ++r;
+                if (qe <= re) ++q;
+            }
+            const int deni = ptp * dtp;
+            const double den = (double)deni;
+            const bool pow2 = (deni & (deni - 1)) == 0;
+            const double inv_den = 1.0 / den;
+            const int lqp = p.L / ppp, lrp = p.L % ppp, lqd = p.L / dpp, lrd = p.L % dpp;
+            int a = 0, bb = 0, a0 = 0, b0 = 0;
+            int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
+            while (a < ppp && bb < dpp) {
+                if (rl >= 0) {
+                    const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+                    const int e = colp[a * ptp + rl] * G + cold[bb * dtp + ql];
+                    const double al = p.alpha[e], be = p.beta[e];
+#pragma unroll
+                    for (int k = 0; k < kC; ++k) {
+                        if (k >= nc) break;
+                        const double Vn = V1[k] * (double)nab;
+                        const double bytes = pow2 ? (Vn * (double)ovl) * inv_den : (Vn * (double)ovl) / den;
+                        const double time = al + bytes / be;
+                        if (time > worst[k]) worst[k] = time;
+                    }
+                }
+                const bool adv_a = a1 <= b1, adv_b = b1 <= a1;
+                if (adv_a) {
+                    ++a;
+                    a0 = a1;
+                    a1 = a0 + lqp + (a < lrp ? 1 : 0);
+                }
+                if (adv_b) {
+                    ++bb;
+                    b0 = b1;
+                    b1 = b0 + lqd + (bb < lrd ? 1 : 0);
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kC; ++k)
+#pragma unroll
+            for (int off = kWalkLanes / 2; off > 0; off >>= 1) {
+                const double w2 = __shfl_xor(worst[k], off, 64);
+                worst[k] = w2 > worst[k] ? w2 : worst[k];
+            }
+        double t = worst[0];
+        if (kCls) {
+            t = 0.0;
+#pragma unroll
+            for (int k = 0; k < kC; ++k)
+                if (k < nc) t = t + p.cls_w[k] * worst[k];
+        }
+        if (live && sub == 0) f.kv_cap[(int64_t)(i * nd + j) * N + n] = ok ? quantize(1000.0 / t) : 0;
+        lane_sync();  // the next edge's expansion overwrites the columns
     }
-    f.kv_cap[(int64_t)e * N + n] = c;
 }
 
 // Per-GPU nodes: one workgroup of kGpuKvWaves wavefronts per 64 candidates (a lane per
@@ -1224,6 +1520,18 @@ hipError_t launch_w(const Problem& p, const CostOut& o, const FlowNet& f, hipStr
         if (e != hipSuccess) return e;
     } else if (p.variant & HX_VARIANT_KV_ORDER) {
         hipLaunchKernelGGL(kv_order_kernel<W>, dim3(blocks), dim3(kOrderThreads), kOrderLds + lds, s, p, o, f);
+    } else if (f.kv_list && !(p.variant & HX_VARIANT_ASYM)) {
+        // the listed path: zero rows and the edge list, its packing, then the walks
+        const int64_t pieces = (p.N + 63) / 64 * kKvSlices;
+        hipLaunchKernelGGL(kv_rows_kernel, dim3((unsigned)((p.N + kRowsBlock - 1) / kRowsBlock), kKvSlices),
+                           dim3(kRowsBlock), 0, s, f);
+        hipLaunchKernelGGL(kv_scan_kernel, dim3(1), dim3(kScanBlock), 0, s, f);
+        hipLaunchKernelGGL(kv_compact_kernel, dim3((unsigned)((pieces + 3) / 4)), dim3(256), 0, s, f);
+        const size_t gl = kv_group_lds(p.G);
+        if (p.n_cls > 0)
+            hipLaunchKernelGGL((kv_walk_group_kernel<W, true>), dim3(kGroupGrid), dim3(kGroupBlock), gl, s, p, o, f);
+        else
+            hipLaunchKernelGGL((kv_walk_group_kernel<W, false>), dim3(kGroupGrid), dim3(kGroupBlock), gl, s, p, o, f);
     } else if (p.variant & HX_VARIANT_ASYM) {
         hipLaunchKernelGGL((kv_kernel<W, true, false>), grid_kv, dim3(kKvBlock), lds + sizeof(double) * p.G, s, p,
                            o, f);

@@ -35,7 +35,60 @@ struct CostOut {
 struct FlowNet {
     int32_t N, max_p, max_d, max_pd;
     int32_t *n_p, *n_d, *p_slot, *d_slot, *src_cap, *p_cap, *kv_cap, *d_cap, *sink_cap;
+    // Optional scratch of the listed KV path (replica nodes, kv_list_fits), per piece: 64
+    // candidates (s = n / 64) and a slice r of kKvSlices of their KV rows (rows r kv_rows to
+    // (r + 1) kv_rows - 1):
+    //   feas     [N]: bit i of the low word set when prefill node i's replica has a strategy,
+    //            bit j of the high word the same for decode node j (nodes_kernel writes it);
+    //   kv_count [ceil(N / 64)][kKvSlices]: how many of the piece's KV edges are listed;
+    //   kv_list  [ceil(N / 64)][kKvSlices][64 kv_rows]: the piece's KV edges whose two replicas
+    //            have a strategy, (n << 10) | (i << 5) | j, in row order (kv_rows_kernel writes
+    //            both, kv_walk_kernel walks them).
+    //   kv_offs  [pieces + 1]: exclusive prefix sums of kv_count, the total last;
+    //   kv_flat  the listed edges of all pieces, packed in piece order (kv_offs[s] onwards).
+    uint64_t* feas = nullptr;
+    int32_t* kv_count = nullptr;
+    uint32_t* kv_list = nullptr;
+    int32_t* kv_offs = nullptr;
+    uint32_t* kv_flat = nullptr;
+    int32_t kv_rows = 0;  // ceil(floor(Kmax/2) ceil(Kmax/2) / kKvSlices)
 };
+
+constexpr int kKvSlices = 4;
+
+// The listed KV path takes networks of up to 32 replica slots (node indices in 5 bits, bits of
+// feas) and up to 2^22 candidates (n in the list entry's other 22 bits).
+inline bool kv_list_fits(int32_t granularity, int32_t max_groups, int32_t n_cand) {
+    return granularity == 0 && max_groups <= 32 && n_cand <= (1 << 22);
+}
+// Its scratch: the pieces' counts and offsets, feas, then twice room for every KV row of every
+// piece (the per-piece lists and the packed list).
+inline int32_t kv_slice_rows(int32_t max_groups) {
+    return ((max_groups / 2) * ((max_groups + 1) / 2) + kKvSlices - 1) / kKvSlices;
+}
+inline size_t kv_pieces(int32_t n_cand) { return (size_t)kKvSlices * (((size_t)n_cand + 63) / 64); }
+inline size_t kv_round256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline size_t kv_list_entries(int32_t max_groups, int32_t n_cand) {
+    return kv_pieces(n_cand) * 64 * (size_t)kv_slice_rows(max_groups);
+}
+inline size_t kv_list_bytes(int32_t max_groups, int32_t n_cand) {
+    return kv_round256(sizeof(int32_t) * kv_pieces(n_cand)) + kv_round256(sizeof(int32_t) * (kv_pieces(n_cand) + 1)) +
+           kv_round256(sizeof(uint64_t) * (size_t)n_cand) +
+           2 * kv_round256(sizeof(uint32_t) * kv_list_entries(max_groups, n_cand));
+}
+inline void kv_list_carve(FlowNet& f, void* base, int32_t max_groups, int32_t n_cand) {
+    unsigned char* b = static_cast<unsigned char*>(base);
+    f.kv_count = reinterpret_cast<int32_t*>(b);
+    b += kv_round256(sizeof(int32_t) * kv_pieces(n_cand));
+    f.kv_offs = reinterpret_cast<int32_t*>(b);
+    b += kv_round256(sizeof(int32_t) * (kv_pieces(n_cand) + 1));
+    f.feas = reinterpret_cast<uint64_t*>(b);
+    b += kv_round256(sizeof(uint64_t) * (size_t)n_cand);
+    f.kv_list = reinterpret_cast<uint32_t*>(b);
+    b += kv_round256(sizeof(uint32_t) * kv_list_entries(max_groups, n_cand));
+    f.kv_flat = reinterpret_cast<uint32_t*>(b);
+    f.kv_rows = kv_slice_rows(max_groups);
+}
 
 // Capacity in milli-requests/s: floor(x), clamped to [0, HX_CAP_MAX].
 __device__ __forceinline__ int32_t quantize(double x) {

@@ -209,6 +209,25 @@ def test_score_batch_replica_variants(torch, cfg, n, variant, classes):
     assert np.array_equal(one["flow_value"][idx], want["flow_value"])
 
 
+@pytest.mark.parametrize("variant", [0, 4])
+def test_score_batch_listed_kv_maximum_cluster(torch, variant):
+    """255 GPUs (four mask words per group) and 32 group slots: the largest networks whose KV
+    edges the fused call lists for one lane per edge, here with alpha and beta read from memory
+    (too many GPUs to stage them); with the asymmetric split (variant 4) the walk's extra LDS
+    sends them back to one lane per (edge, candidate).  Rows and values equal the four calls',
+    and the oracle's."""
+    from tests.test_gpu_parity import max_cluster_problem
+    prob = max_cluster_problem(32, 96, 32)
+    if variant:
+        prob = dataclasses.replace(prob, variant=variant)
+    say(f"hx_score_batch vs four calls: 255 GPUs, 32 slots, N={prob.n_cand}, variant {variant}")
+    four, one = _both(torch, prob)
+    _same(four, one, prob.granularity)
+    want = hxo.score_batch(prob, n_threads=N_THREADS)
+    assert np.array_equal(one["flow_value"], want["flow_value"])
+    assert one["best"] == want["best"]
+
+
 def test_score_batch_concurrent_streams(torch):
     """Independent calls in flight on three streams (each with its own workspace and outputs, the
     inputs shared): every stream's flow values and best equal a single-stream call's, call after
