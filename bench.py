@@ -51,15 +51,16 @@ FP64_VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 # taken on (first 16 hex digits of the source file's SHA-256); otherwise traffic is null.
 COUNTER_SCALE = {"fetch": 2.0, "write": 1.0}
 KERNEL_TRAFFIC = {
-    # workload 3 (profiles/all_kernels_workload3.md); maxflow is the instantiation with the folded
-    # argmax, best the final reduction of its slots
+    # workload 3 (profiles/all_kernels_workload3.md); kv the listed path's four kernels (rows,
+    # scan, packing, walks), maxflow the instantiation with the folded argmax, best the final
+    # reduction of its slots
     3: {
-        "setup": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 70.55, "write_kib": 57.43},
-        "decode": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1714, "write_kib": 2.884e+04},
-        "scatter": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 5425, "write_kib": 1485},
-        "eval": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1103, "write_kib": 1.206e+04},
-        "nodes": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 6694, "write_kib": 1.577e+04},
-        "kv": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 5882, "write_kib": 1.34e+04},
+        "setup": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 70.54, "write_kib": 57.43},
+        "decode": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1714, "write_kib": 2.884e+04},
+        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 5425, "write_kib": 1487},
+        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1108, "write_kib": 1.207e+04},
+        "nodes": {"source_sha256_16": "18b89df167ec18cf", "fetch_kib": 7206, "write_kib": 1.649e+04},
+        "kv": {"source_sha256_16": "18b89df167ec18cf", "fetch_kib": 5710, "write_kib": 1.424e+04},
         "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 1.674e+04, "write_kib": 768},
         "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 18.1, "write_kib": 0.03125},
     },
@@ -67,15 +68,15 @@ KERNEL_TRAFFIC = {
     # (profiles/chain_workload5.md): nodes is the settling nodes kernel, kv the link table,
     # maxflow the list-driven kernel, shared candidate 0's groups, best the split argmax
     5: {
-        "setup": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 184.2, "write_kib": 516.1},
-        "shared": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 179.9, "write_kib": 2},
-        "decode": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 1.047e+04, "write_kib": 1.471e+05},
-        "scatter": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 3.97e+04, "write_kib": 7566},
-        "eval": {"source_sha256_16": "1f259718a22258d2", "fetch_kib": 9310, "write_kib": 3.267e+04},
-        "nodes": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 6.153e+04, "write_kib": 1536},
-        "kv": {"source_sha256_16": "080edb9f490bb0a1", "fetch_kib": 145.8, "write_kib": 68.03},
-        "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 10.64, "write_kib": 0},
-        "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 297.2, "write_kib": 8.062},
+        "setup": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 184.2, "write_kib": 516.1},
+        "shared": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 179.9, "write_kib": 2},
+        "decode": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1.047e+04, "write_kib": 1.471e+05},
+        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 3.968e+04, "write_kib": 7566},
+        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 9326, "write_kib": 3.268e+04},
+        "nodes": {"source_sha256_16": "18b89df167ec18cf", "fetch_kib": 6.153e+04, "write_kib": 1536},
+        "kv": {"source_sha256_16": "18b89df167ec18cf", "fetch_kib": 145.8, "write_kib": 68.03},
+        "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 18.21, "write_kib": 0},
+        "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 297.3, "write_kib": 8.062},
     },
 }
 # The guided-moves kernel at the refinement workload (profiles/refine_workload5.md), per launch of
