@@ -14,7 +14,7 @@
 //   kv_rows_kernel, kv_scan_kernel, kv_compact_kernel, kv_walk_group_kernel  the same edges as
 //                 kv_kernel when hx_score_batch hands over scratch for an edge list: one lane per
 //                 candidate writes every edge with an infeasible end (0, row by row) and lists
-//                 the others, the lists are packed, then 16 lanes per listed edge walk it;
+//                 the others, the lists are packed, then 4 lanes per listed edge walk it;
 //   kv_gpu_kernel the same for per-GPU nodes, a workgroup per 64 candidates.
 // hx_score_batch's per-GPU path (up to 128 GPUs and 128 slots) replaces the last two: a table of
 // every link's capacity (link_table_kernel), and nodes_gpu_kernel<W, true>, which settles each
@@ -1201,19 +1201,20 @@ __global__ void __launch_bounds__(256) kv_compact_kernel(FlowNet f) {
 // The listed KV path's walk: kWalkLanes lanes per listed edge.  An edge's links are every
 // overlapping (stage, stage) pair crossed with every overlapping (rank, rank) pair, and the rank
 // pairs (head slices of ptp x dtp) are the same for every stage pair, so lane l of the group
-// takes the l-th rank pair of the merge walk (there are at most ptp + dtp - 1 <= 15) and walks
-// the stage pairs (at most ppp + dpp - 1) with it; the group's maximum is the edge's KV time
+// takes the rank pairs l, l + kWalkLanes, ... of the merge walk (there are
+// ptp + dtp - gcd(ptp, dtp) <= 15 of them, at most 8 when both degrees are powers of two) and
+// walks the stage pairs (at most ppp + dpp - 1) with them; the group's maximum is the edge's KV time
 // (with kCls one maximum per request class, then sum_k w_k max_k in class order).  Each link's
 // time is the binary64 value kv_time or kv_time_classes forms, and a maximum does not depend on
 // the order.  (The asymmetric split stays with kv_kernel: every lane of a group would recompute
 // the stages' layer counts, which measured twice as slow.)  The
-// group's lanes expand the two member masks together (4W bits a lane) into the group's two
-// member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
+// group's lanes expand the two member masks together (64 / kWalkLanes bits of each word a
+// lane) into the group's two member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
 // over a grid of kGroupGrid workgroups (about what the chip holds at once): the walks run side
 // by side, each starting with a chain of dependent loads (its list entry, slots, then masks and
 // strategies).  Alpha and beta are read from memory: staging them in LDS per workgroup measured
 // slower.
-constexpr int kWalkLanes = 16;
+constexpr int kWalkLanes = 4;
 constexpr int kGroupBlock = 256;
 constexpr int kGroupGrid = 2048;
 
@@ -1221,16 +1222,17 @@ __host__ __device__ inline size_t kv_group_lds(int G) { return (size_t)kGroupBlo
 
 template <int W>
 __device__ __forceinline__ int expand_group(const uint64_t* m, uint8_t* col, int sub) {
+    constexpr int kBits = 64 / kWalkLanes;
     int below = 0, total = 0;
 #pragma unroll
     for (int w = 0; w < W; ++w) total += __popcll(m[w]);
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-        const int b0 = sub * 4;
-        const uint64_t mine = (m[w] >> b0) & 0xF;
+        const int b0 = sub * kBits;
+        const uint64_t mine = (m[w] >> b0) & ((1ull << kBits) - 1);
         int idx = below + __popcll(m[w] & ((1ull << b0) - 1));
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < kBits; ++t)
             if ((mine >> t) & 1) col[idx++] = (uint8_t)(w * 64 + b0 + t);
         below += __popcll(m[w]);
     }
@@ -1241,8 +1243,8 @@ template <int W, bool kCls>
 __global__ void __launch_bounds__(kGroupBlock) kv_walk_group_kernel(Problem p, CostOut o, FlowNet f) {
     constexpr int kGroups = 64 / kWalkLanes, kWaves = kGroupBlock / 64;
     constexpr int kC = kCls ? HX_MAX_CLASSES : 1;
-    static_assert(64 % kWalkLanes == 0 && kWalkLanes * 4 == 64, "a lane expands 4 bits of each mask word");
-    static_assert(2 * HX_MAX_TP - 1 <= kWalkLanes, "a lane per rank pair");
+    static_assert(64 % kWalkLanes == 0 && kWalkLanes <= 64, "lanes of a group split each mask word");
+    constexpr int kPairs = (2 * HX_MAX_TP - 1 + kWalkLanes - 1) / kWalkLanes;  // rank pairs a lane
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = lane / kWalkLanes, sub = lane % kWalkLanes;
@@ -1280,17 +1282,30 @@ __global__ void __launch_bounds__(kGroupBlock) kv_walk_group_kernel(Problem p, C
 #pragma unroll
         for (int k = 0; k < kC; ++k) worst[k] = 0.0;
         if (ok) {
-            // this lane's rank pair: step sub of the merge of the two head partitions
-            int r = 0, q = 0, rl = -1, ql = 0, ovl = 0;
-            for (int t = 0; t <= sub && r < ptp && q < dtp; ++t) {
-                const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
-                if (t == sub) {
-                    rl = r;
-                    ql = q;
-                    ovl = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+            // this lane's rank pairs: steps sub, sub + kWalkLanes, ... of the merge of the two
+            // head partitions (rl < 0: none)
+            int rl[kPairs], ql[kPairs], ovl[kPairs];
+#pragma unroll
+            for (int h = 0; h < kPairs; ++h) {
+                rl[h] = -1;
+                ql[h] = 0;
+                ovl[h] = 0;
+            }
+            {
+                int r = 0, q = 0;
+                for (int t = 0; t < kPairs * kWalkLanes && r < ptp && q < dtp; ++t) {
+                    const int re = (r + 1) * dtp, qe = (q + 1) * ptp;
+                    const int ov = (re < qe ? re : qe) - (r * dtp > q * ptp ? r * dtp : q * ptp);
+#pragma unroll
+                    for (int h = 0; h < kPairs; ++h)
+                        if (t == sub + h * kWalkLanes) {
+                            rl[h] = r;
+                            ql[h] = q;
+                            ovl[h] = ov;
+                        }
+                    if (re <= qe) ++r;
+                    if (qe <= re) ++q;
                 }
-                if (re <= qe) ++r;
-                if (qe <= re) ++q;
             }
             const int deni = ptp * dtp;
             const double den = (double)deni;
@@ -1300,15 +1315,18 @@ __global__ void __launch_bounds__(kGroupBlock) kv_walk_group_kernel(Problem p, C
             int a = 0, bb = 0, a0 = 0, b0 = 0;
             int a1 = lqp + (0 < lrp ? 1 : 0), b1 = lqd + (0 < lrd ? 1 : 0);
             while (a < ppp && bb < dpp) {
-                if (rl >= 0) {
-                    const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
-                    const int e = colp[a * ptp + rl] * G + cold[bb * dtp + ql];
+                const int nab = (a1 < b1 ? a1 : b1) - (a0 > b0 ? a0 : b0);
+#pragma unroll
+                for (int h = 0; h < kPairs; ++h) {
+                    const int rr = rl[h], qq = ql[h], oo = ovl[h];
+                    if (rr < 0) continue;
+                    const int e = colp[a * ptp + rr] * G + cold[bb * dtp + qq];
                     const double al = p.alpha[e], be = p.beta[e];
 #pragma unroll
                     for (int k = 0; k < kC; ++k) {
                         if (k >= nc) break;
                         const double Vn = V1[k] * (double)nab;
-                        const double bytes = pow2 ? (Vn * (double)ovl) * inv_den : (Vn * (double)ovl) / den;
+                        const double bytes = pow2 ? (Vn * (double)oo) * inv_den : (Vn * (double)oo) / den;
                         const double time = al + bytes / be;
                         if (time > worst[k]) worst[k] = time;
                     }
