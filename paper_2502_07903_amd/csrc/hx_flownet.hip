@@ -1101,20 +1101,23 @@ __global__ void __launch_bounds__(kRowsBlock) kv_rows_kernel(FlowNet f) {
         j = r0 - i * nd;
     }
     const uint32_t dm = (uint32_t)(fz >> 32);
-    bool pi = (fz >> i) & 1;  // prefill node i has a strategy
+    // The row advance is formed with selects (i <= n_p <= 32, so the shift stays below 64), so
+    // that only the two stores are predicated.
     int cnt = 0;
-    for (int e = r0; e < rows; ++e) {
+    int32_t* row = f.kv_cap + (int64_t)r0 * N + n;
+    for (int e = r0; e < rows; ++e, row += N) {
         const bool live = e < hi;
-        const bool walk = live && pi && ((dm >> j) & 1);
-        if (live && !walk) f.kv_cap[(int64_t)e * N + n] = 0;
+        const bool walk = live && ((((uint32_t)(fz >> i) & (dm >> j)) & 1) != 0);
+        if (live && !walk) *row = 0;
         const uint64_t bal = __ballot(walk);
-        if (walk) list[cnt + __popcll(bal & ((1ull << lane) - 1))] = ((uint32_t)n << 10) | ((uint32_t)i << 5) | (uint32_t)j;
-        cnt += __popcll(bal);
-        if (live && ++j == nd) {
-            j = 0;
-            ++i;
-            pi = (fz >> i) & 1;
+        if (bal) {
+            if (walk)
+                list[cnt + __popcll(bal & ((1ull << lane) - 1))] = ((uint32_t)n << 10) | ((uint32_t)i << 5) | (uint32_t)j;
+            cnt += __popcll(bal);
         }
+        const bool wrap = live && j + 1 == nd;
+        i += wrap ? 1 : 0;
+        j = wrap ? 0 : (live ? j + 1 : j);
     }
     if (lane == 0) f.kv_count[piece] = cnt;
 }

@@ -189,12 +189,13 @@ def test_score_batch_argmax_ties(torch, cfg):
 
 
 @pytest.mark.parametrize("cfg,n,variant,classes", [(3, 4096, 0, 4), (2, None, 4, 0), (3, 8192, 1, 0), (2, 1000, 2, 0),
-                                                   (4, 2048, 5, 0)])
+                                                   (4, 2048, 5, 0), (4, 1000, 0, 4), (2, 777, 1, 3)])
 def test_score_batch_replica_variants(torch, cfg, n, variant, classes):
     """Replica networks under the cost-model variants (request classes, the asymmetric split,
-    the pipelined capacity, the stage-order search, asymmetric + pipelined): the fused call's
-    outputs equal the four calls', and the oracle's
-    flow values on a sample."""
+    the pipelined capacity, the stage-order search, asymmetric + pipelined; request classes on
+    32 group slots, whose KV edges go through the packed list, and three classes with the
+    pipelined capacity on 16 GPUs, many feasible edges per candidate): the fused call's outputs
+    equal the four calls', and the oracle's flow values on a sample."""
     prob = I.make_problem(cfg, n_cand=n)
     if variant:
         prob = dataclasses.replace(prob, variant=variant)
