@@ -1206,13 +1206,13 @@ __global__ void __launch_bounds__(256) kv_compact_kernel(FlowNet f) {
 // pairs (head slices of ptp x dtp) are the same for every stage pair, so lane l of the group
 // takes the rank pairs l, l + kWalkLanes, ... of the merge walk (there are
 // ptp + dtp - gcd(ptp, dtp) <= 15 of them, at most 8 when both degrees are powers of two) and
-// walks the stage pairs (at most ppp + dpp - 1) with them; the group's maximum is the edge's KV time
-// (with kCls one maximum per request class, then sum_k w_k max_k in class order).  Each link's
-// time is the binary64 value kv_time or kv_time_classes forms, and a maximum does not depend on
-// the order.  (The asymmetric split stays with kv_kernel: every lane of a group would recompute
-// the stages' layer counts, which measured twice as slow.)  The
-// group's lanes expand the two member masks together (64 / kWalkLanes bits of each word a
-// lane) into the group's two member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
+// walks the stage pairs (at most ppp + dpp - 1) with them; the group's maximum is the edge's KV
+// time (with kCls one maximum per request class, then sum_k w_k max_k in class order).  Each
+// link's time is the binary64 value kv_time or kv_time_classes forms, and a maximum does not
+// depend on the order.  (The asymmetric split stays with kv_kernel: every lane of a group would
+// recompute the stages' layer counts, which measured twice as slow.)  The group's lanes expand
+// the two member masks together (64 / kWalkLanes bits of each word a lane) into the group's two
+// member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
 // over a grid of kGroupGrid workgroups (about what the chip holds at once): the walks run side
 // by side, each starting with a chain of dependent loads (its list entry, slots, then masks and
 // strategies).  Alpha and beta are read from memory: staging them in LDS per workgroup measured
