@@ -1195,10 +1195,15 @@ __global__ void __launch_bounds__(256) kv_compact_kernel(FlowNet f) {
     const int64_t P = (f.N + 63) / 64 * kKvSlices;
     const int64_t s = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (s >= P) return;
+    const int lane = threadIdx.x & 63;
+    const uint32_t* list = f.kv_list + s * (int64_t)(64 * f.kv_rows);
+    // the part's first 64 entries are loaded with its count and offset (a part has room for
+    // 64 kv_rows >= 64 entries, so the load stays inside it; entries past the count are unused)
+    const uint32_t first = list[lane];
     const int cnt = f.kv_count[s];
     const int32_t off = f.kv_offs[s];
-    const uint32_t* list = f.kv_list + s * (int64_t)(64 * f.kv_rows);
-    for (int x = threadIdx.x & 63; x < cnt; x += 64) f.kv_flat[off + x] = list[x];
+    if (lane < cnt) f.kv_flat[off + lane] = first;
+    for (int x = lane + 64; x < cnt; x += 64) f.kv_flat[off + x] = list[x];
 }
 
 // The listed KV path's walk: kWalkLanes lanes per listed edge.  An edge's links are every
