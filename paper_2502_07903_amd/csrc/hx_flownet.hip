@@ -1149,13 +1149,13 @@ __global__ void __launch_bounds__(kScanBlock) kv_scan_kernel(FlowNet f) {
     int4* ow = reinterpret_cast<int4*>(f.kv_offs);
     const int64_t wlo = lo / 4, whi = hi / 4;
     int32_t sum = 0;
+    int4 v0[kWords];  // the last chunk read: the whole run when it fits in one
     for (int64_t c0 = wlo; c0 < whi; c0 += kWords) {
-        int4 v[kWords];
 #pragma unroll
-        for (int k = 0; k < kWords; ++k) v[k] = cw[c0 + k < whi ? c0 + k : whi - 1];
+        for (int k = 0; k < kWords; ++k) v0[k] = cw[c0 + k < whi ? c0 + k : whi - 1];
 #pragma unroll
         for (int k = 0; k < kWords; ++k)
-            if (c0 + k < whi) sum += v[k].x + v[k].y + v[k].z + v[k].w;
+            if (c0 + k < whi) sum += v0[k].x + v0[k].y + v0[k].z + v0[k].w;
     }
     int32_t x = sum;  // inclusive scan over the wavefront
     for (int off = 1; off < 64; off <<= 1) {
@@ -1171,6 +1171,19 @@ __global__ void __launch_bounds__(kScanBlock) kv_scan_kernel(FlowNet f) {
         total += v;
     }
     int32_t off = before + x - sum;
+    if (whi - wlo <= kWords) {  // a run of one chunk: its counts are still in v0
+#pragma unroll
+        for (int k = 0; k < kWords; ++k)
+            if (wlo + k < whi) {
+                int4 o;
+                o.x = off;
+                o.y = o.x + v0[k].x;
+                o.z = o.y + v0[k].y;
+                o.w = o.z + v0[k].z;
+                off = o.w + v0[k].w;
+                ow[wlo + k] = o;
+            }
+    } else
     for (int64_t c0 = wlo; c0 < whi; c0 += kWords) {
         int4 v[kWords];
 #pragma unroll
