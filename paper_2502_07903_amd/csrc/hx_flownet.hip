@@ -1231,13 +1231,13 @@ __global__ void __launch_bounds__(256) kv_compact_kernel(FlowNet f) {
 // recompute the stages' layer counts, which measured twice as slow.)  The group's lanes expand
 // the two member masks together (64 / kWalkLanes bits of each word a lane) into the group's two
 // member columns in LDS.  The edges come from the packed list, kGroups per wavefront at a time,
-// over a grid of kGroupGrid workgroups (about what the chip holds at once): the walks run side
-// by side, each starting with a chain of dependent loads (its list entry, slots, then masks and
-// strategies).  Alpha and beta are read from memory: staging them in LDS per workgroup measured
+// over a grid of kGroupGrid workgroups (about twice what the chip holds at once, so that
+// workgroups that finish early are replaced): the walks run side by side, each starting with a
+// chain of dependent loads (its list entry, slots, then masks and strategies).  Alpha and beta are read from memory: staging them in LDS per workgroup measured
 // slower.
 constexpr int kWalkLanes = 4;
 constexpr int kGroupBlock = 256;
-constexpr int kGroupGrid = 2048;
+constexpr int kGroupGrid = 4096;
 
 __host__ __device__ inline size_t kv_group_lds(int G) { return (size_t)kGroupBlock / kWalkLanes * 2 * G; }
 
