@@ -55,12 +55,12 @@ KERNEL_TRAFFIC = {
     # scan, packing, walks), maxflow the instantiation with the folded argmax, best the final
     # reduction of its slots
     3: {
-        "setup": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 70.54, "write_kib": 57.43},
+        "setup": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 70.55, "write_kib": 57.43},
         "decode": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1714, "write_kib": 2.884e+04},
-        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 5425, "write_kib": 1486},
-        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1110, "write_kib": 1.203e+04},
-        "nodes": {"source_sha256_16": "104e67fa37bbc180", "fetch_kib": 7215, "write_kib": 1.644e+04},
-        "kv": {"source_sha256_16": "104e67fa37bbc180", "fetch_kib": 4536, "write_kib": 1.423e+04},
+        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 5425, "write_kib": 1482},
+        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1110, "write_kib": 1.204e+04},
+        "nodes": {"source_sha256_16": "5fbb928bf73c535c", "fetch_kib": 7215, "write_kib": 1.654e+04},
+        "kv": {"source_sha256_16": "5fbb928bf73c535c", "fetch_kib": 4536, "write_kib": 1.423e+04},
         "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 1.674e+04, "write_kib": 768},
         "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 18.1, "write_kib": 0.03125},
     },
@@ -71,10 +71,10 @@ KERNEL_TRAFFIC = {
         "setup": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 184.2, "write_kib": 516.1},
         "shared": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 179.9, "write_kib": 2},
         "decode": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 1.047e+04, "write_kib": 1.471e+05},
-        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 3.966e+04, "write_kib": 7570},
-        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 9322, "write_kib": 3.268e+04},
-        "nodes": {"source_sha256_16": "104e67fa37bbc180", "fetch_kib": 6.153e+04, "write_kib": 1536},
-        "kv": {"source_sha256_16": "104e67fa37bbc180", "fetch_kib": 138.3, "write_kib": 68.03},
+        "scatter": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 3.967e+04, "write_kib": 7565},
+        "eval": {"source_sha256_16": "cfe308a8f566cbcf", "fetch_kib": 9326, "write_kib": 3.268e+04},
+        "nodes": {"source_sha256_16": "5fbb928bf73c535c", "fetch_kib": 6.153e+04, "write_kib": 1536},
+        "kv": {"source_sha256_16": "5fbb928bf73c535c", "fetch_kib": 138.3, "write_kib": 68.03},
         "maxflow": {"source_sha256_16": "b931fad73ca81326", "fetch_kib": 18.21, "write_kib": 0},
         "best": {"source_sha256_16": "89724c3a7f9a387f", "fetch_kib": 297.3, "write_kib": 8.062},
     },
